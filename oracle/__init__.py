@@ -1,0 +1,87 @@
+"""CPU oracle for NDVM -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the package smoke check and the benchmark's CPU-baseline leg
+may import this package.  The GPU path never calls it.
+
+``run`` evaluates a stack-bytecode program for L parameter vectors with the
+plain C interpreter in ``ndvm_oracle.c`` (per-lane realized trace, Wengert
+list, reverse sweep; paper Section 3.4 and Appendix C table tab:adjoints).
+``run_ld`` is the same source evaluated in x87 extended precision, used to
+estimate how strongly rounding disturbs a lane's fp64 result.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "ndvm_oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+LIB_LD = os.path.join(HERE, "liboracle_ld.so")
+_lock = threading.Lock()
+_libs = {}
+
+
+def build(force: bool = True) -> None:
+    """Compile the oracle (fp64 and extended-precision copies) in-tree."""
+    base = ["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math",
+            "-fPIC", "-shared", "-pthread", SRC, "-lm"]
+    for out, extra in ((LIB, []), (LIB_LD, ["-DORACLE_LONG_DOUBLE"])):
+        if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(SRC):
+            tmp = out + ".tmp"
+            subprocess.check_call(base[:-2] + extra + [SRC, "-o", tmp, "-lm"])
+            os.replace(tmp, out)
+
+
+def _lib(ld: bool):
+    with _lock:
+        key = "ld" if ld else "d"
+        if key not in _libs:
+            path = LIB_LD if ld else LIB
+            if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(SRC):
+                build(force=True)
+            lib = ctypes.CDLL(path)
+            fn = getattr(lib, "ndvm_oracle_run_ld" if ld else "ndvm_oracle_run")
+            fn.restype = ctypes.c_int
+            fn.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64,
+                           ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                           ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int]
+            err = getattr(lib, "ndvm_oracle_error_ld" if ld else "ndvm_oracle_error")
+            err.restype = ctypes.c_char_p
+            _libs[key] = (lib, fn, err)
+        return _libs[key]
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"oracle error {code}: {msg}")
+        self.code = code
+
+
+def _ptr(a):
+    return a.ctypes.data if a is not None else None
+
+
+def run(bytecode: bytes, params, obs, grad: bool = True, threads: int = 0,
+        margin: bool = False, extended: bool = False):
+    """Return (loss[L], grad[L, P] or None, margin[L] or None)."""
+    _, fn, err = _lib(extended)
+    params = np.ascontiguousarray(params, dtype=np.float64)
+    if params.ndim == 1:
+        params = params[None, :]
+    obs = np.ascontiguousarray(obs, dtype=np.float64)
+    L, P = params.shape
+    loss = np.empty(L)
+    g = np.empty((L, P)) if grad else None
+    m = np.empty(L) if margin else None
+    if threads <= 0:
+        threads = max(1, min(os.cpu_count() or 1, 16))
+    rc = fn(bytecode, len(bytecode), _ptr(params), L, P, _ptr(obs), obs.size,
+            _ptr(loss), _ptr(g), P, _ptr(m), threads)
+    if rc != 0:
+        raise OracleError(rc, err().decode(errors="replace"))
+    return loss, g, m
