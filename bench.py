@@ -1,0 +1,182 @@
+"""Benchmark: lane-gradient evaluations per second (forward replay + reverse
+sweep) on one MI355X, for one of the five synthetic workloads.
+
+A step is one ndvm_grad call (ndvm_grad_many for the program population) that
+produces loss[L] and grad[L, P] for a batch of L parameter vectors whose
+inputs are already resident in HBM.  Tape production and upload happen before
+the timed region.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+Prints one JSON line with the metric, a roofline object for the replay
+kernel (its average duration measured with HIP events on the launch stream)
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from workloads import configs  # noqa: E402
+
+PEAK_FP64 = 78.6e12        # MI355X fp64 vector FLOP/s
+PEAK_HBM = 8.0e12          # MI355X HBM3E bytes/s
+DEFAULT_WORKLOAD = configs.ORDER[1]
+
+
+def tape_flops(tape_bytes: bytes) -> float:
+    """Algorithmic fp64 operations per lane of one forward + reverse pass over
+    the realized trace: forward = one per output element of an elementwise
+    op (transcendentals count 1), 2mkn for an m x k by k x n product, 2n for a
+    dot; reverse = the flops of the adjoint rules (table tab:adjoints) for
+    every op that depends on a parameter."""
+    import struct
+    (_, n_params, n_obs, n_ops, n_consts, n_aux, loss) = struct.unpack_from("<7I", tape_bytes, 4)
+    off = 32 + 8 * n_consts + 4 * n_aux
+    ops = [struct.unpack_from("<HBB5I", tape_bytes, off + 24 * k) for k in range(n_ops)]
+    active = [False] * n_ops
+    fwd = rev = 0.0
+    for k, (code, r, c, a, b, cc, d, imm) in enumerate(ops):
+        n = r * c
+        if code == 0x02:
+            active[k] = True
+            continue
+        if code in (0x01, 0x03):
+            continue
+        if code == 0x28:   # PACK: data movement only
+            continue
+        srcs = [a, b] if code in (0x10, 0x11, 0x12, 0x13, 0x1D, 0x20, 0x21, 0x27) else \
+            [cc, d] if code == 0x40 else [a]
+        active[k] = any(active[s] for s in srcs if s < k)
+        ra, ca = ops[a][1], ops[a][2]
+        if code == 0x21:
+            f = 2.0 * ra * ca * c
+            fr = 2 * f
+        elif code == 0x20:
+            f = 2.0 * ra * ca
+            fr = 2 * f
+        elif code in (0x23, 0x24, 0x25):
+            f, fr = 10.0, 40.0
+        elif code in (0x22, 0x29, 0x40):
+            f, fr = 0.0, 0.0
+        else:
+            f, fr = float(n), 2.0 * n
+        fwd += f
+        if active[k]:
+            rev += fr
+    return fwd + rev
+
+
+def build_inputs(name, torch, device):
+    import paper_2607_03574_amd as nd
+    w = configs.build(name)
+    o = torch.tensor(w.obs, device=device)
+    p = torch.tensor(w.params, device=device)
+    if name == "random_programs":
+        tapes_b = [nd.tape_build(bc) for bc in w.programs]
+        tapes = [nd.tape_upload(t) for t in tapes_b]
+        n_prog, L, P = p.shape
+        loss = torch.empty((n_prog, L), dtype=torch.float64, device=device)
+        grad = torch.zeros((n_prog, L, P), dtype=torch.float64, device=device)
+        ws = torch.empty(max(nd.workspace_bytes_many(tapes, L), 8), dtype=torch.uint8, device=device)
+        flops = sum(tape_flops(t) for t in tapes_b) * L
+
+        def step(stream):
+            nd.grad_many(tapes, p, o, loss, grad, ws, stream)
+        lanes = n_prog * L
+        meta = dict(programs=n_prog, lanes_per_program=L)
+        return w, step, lanes, flops, meta, (w.programs, w.params, w.n_params_each)
+    tape_b = nd.tape_build(w.bytecode)
+    tape = nd.tape_upload(tape_b)
+    L, P = p.shape
+    loss = torch.empty(L, dtype=torch.float64, device=device)
+    grad = torch.empty((L, P), dtype=torch.float64, device=device)
+    ws = torch.empty(max(nd.workspace_bytes(tape, L, True), 8), dtype=torch.uint8, device=device)
+    flops = tape_flops(tape_b) * L
+
+    def step(stream):
+        nd.grad(tape, p, o, loss, grad, ws, stream)
+    meta = dict(lanes=L, params=P, tape_ops=nd.tape_info(tape)["n_ops"])
+    return w, step, L, flops, meta, ([w.bytecode], w.params[None], [P])
+
+
+def cpu_baseline(w, progs, budget_s=10.0):
+    """The oracle, as it stands, on a bounded sample of the same workload."""
+    import oracle
+    bcs, params, nps = progs
+    threads = max(1, min(os.cpu_count() or 1, 16))
+    lanes = 16
+    while True:
+        t0 = time.perf_counter()
+        done = 0
+        for q in range(len(bcs)):
+            sub = params[q][:lanes, :nps[q]]
+            oracle.run(bcs[q], sub, w.obs, threads=threads)
+            done += sub.shape[0]
+            if time.perf_counter() - t0 > budget_s:
+                break
+        dt = time.perf_counter() - t0
+        if dt > budget_s / 4 or lanes >= params.shape[1]:
+            break
+        lanes = min(params.shape[1], lanes * 4)
+    return dict(value=done / dt, unit="lane-gradient evals/s", cores=threads, kind="oracle",
+                sample=f"{done} lanes of {len(bcs)} program(s) ({w.name}), {dt:.1f} s wall")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=configs.ORDER)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
+                          "(the path shards by lanes or programs, see the design notes)"}))
+        sys.exit(2)
+    import torch
+    device = torch.device("cuda:0")
+    stream = torch.cuda.Stream(device=device)
+    with torch.cuda.stream(stream):
+        w, step, lanes, flops, meta, progs = build_inputs(args.workload, torch, device)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        step(stream)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step(stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_s = ev0.elapsed_time(ev1) / 1e3 / args.steps
+    ms_per_step = wall / args.steps * 1e3
+    value = lanes / (wall / args.steps)
+    achieved = flops / kern_s
+    out = {
+        "metric": "lane-gradient evals/sec (fwd+rev) on 1 MI355X",
+        "value": value, "unit": "lane-gradient evals/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": dict(workload=w.name, **meta),
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_FP64 / 1e12,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP64, "traffic": None,
+                     "kernel": "ndvm_replay", "kernel_ms": kern_s * 1e3,
+                     "alg_flops_per_launch": flops},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, progs)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

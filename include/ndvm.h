@@ -1,0 +1,178 @@
+/*
+ * ndvm.h -- C ABI of the MI355X NDVM hot path.
+ *
+ * The method (arXiv 2607.03574, "Differentiate the Evaluator, Not the
+ * Program"): a fixed evaluator walks a program held as runtime data together
+ * with numeric parameters theta and returns y = E(P, theta); the goal is
+ * dy/dtheta (Section 2).  Structure (control, locals, loop counters) stays
+ * on the host; numeric payloads live in dense batched buffers whose leading
+ * axis is the lane (parameter-vector) axis (Section 3.1, Definition "Payload
+ * table"); reverse mode is a define-by-run tape over numeric primitives only,
+ * replayed in reverse with vectorised loops over the batch axis (Section
+ * 3.4); one structural walk serves B parameter vectors (Section 3.5); the
+ * result is each lane's loss and its exact gradient on the realized trace
+ * (Section 4, Property 1).
+ *
+ * Here the structural walk happens once per program on the host
+ * (ndvm_tape_build) and yields a lane-invariant tape in which numeric
+ * branches are per-lane selects.  ndvm_tape_upload schedules the tape for the
+ * GPU; ndvm_forward / ndvm_grad replay it on the device for L lanes, one lane
+ * per GPU thread, and ndvm_grad_many does so for many programs in a single
+ * launch.
+ *
+ * Conventions for every entry point:
+ *  - All functions return ndvm_status; on a non-OK status a message is
+ *    available from ndvm_last_error() (per calling thread).  No C++
+ *    exception crosses this boundary.
+ *  - Argument and size errors are reported synchronously, before any GPU
+ *    work is enqueued (NDVM_E_ARG).
+ *  - Device pointers are plain HIP device addresses (for example a torch
+ *    tensor's data_ptr()).  `stream` is a hipStream_t passed as void*; NULL
+ *    means the default stream.  Compute calls only enqueue work; faults inside
+ *    a kernel surface at the caller's next synchronisation, launch failures
+ *    as NDVM_E_DEVICE.
+ *  - The caller owns every buffer it passes and must keep it alive until the
+ *    enqueued work has completed.  The library keeps no caller pointer after
+ *    a call returns.  Tape handles are owned by the library until
+ *    ndvm_tape_free().
+ *  - Numerics are fp64.  Non-finite lane results are values, not errors; a
+ *    lane never influences another lane.
+ *  - A tape handle may be used from several streams at once; a workspace must
+ *    not be shared by calls that can run concurrently.
+ */
+#ifndef NDVM_H
+#define NDVM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ndvm_tape ndvm_tape;
+
+typedef enum {
+    NDVM_OK = 0,
+    NDVM_E_ARG = 1,             /* bad pointer, size, stride or count */
+    NDVM_E_BYTECODE = 2,        /* malformed bytecode or a program that cannot be traced */
+    NDVM_E_STRUCT_DIVERGE = 3,  /* numeric branch arms leave different structure */
+    NDVM_E_TAPE = 4,            /* malformed tape bytes */
+    NDVM_E_NOMEM = 5,           /* host or device allocation failed / workspace too small */
+    NDVM_E_DEVICE = 6,          /* HIP runtime error */
+    NDVM_E_UNSUPPORTED = 7      /* valid input outside what this build handles */
+} ndvm_status;
+
+/* Save policies for the reverse sweep (argument `policy` of ndvm_tape_upload). */
+#define NDVM_POLICY_RECOMPUTE 2  /* checkpoint segment inputs, recompute inside segments */
+
+typedef struct {
+    uint32_t n_params;    /* P: parameters per lane */
+    uint32_t n_obs;       /* observations the program reads */
+    uint32_t n_ops;       /* tape ops (leaves included) */
+    uint32_t n_consts;    /* tape constant pool entries */
+    uint32_t loss_slot;   /* tape slot holding the loss */
+    uint32_t n_selects;   /* per-lane select ops (numeric branches) */
+    uint64_t tape_bytes;  /* size of the serialized tape */
+} ndvm_tape_info;
+
+/*
+ * Trace producer (host only; Section 3.3 control as realized trace, Section
+ * 3.4 payload-only tape, Section 6 lane-masked divergent control).
+ * Walks the stack bytecode once with symbolic values and returns the
+ * serialized lane-invariant tape in *tape (malloc'd by the library; release
+ * with ndvm_free).  Counted loops are unrolled; a numeric IFLT traces both
+ * arms and merges differing stack positions and locals with SELECT ops; an
+ * IFLT on two constants resolves here.  No folding or CSE is performed.
+ * Errors: NDVM_E_ARG (null pointers), NDVM_E_BYTECODE, NDVM_E_STRUCT_DIVERGE.
+ */
+ndvm_status ndvm_tape_build(const uint8_t *bytecode, size_t bytecode_len,
+                            uint8_t **tape, size_t *tape_len);
+
+/*
+ * Validate a serialized tape (host bytes), schedule it for the device and
+ * copy the device program to GPU memory on `stream` (Section 3.4 replay;
+ * the schedule decides register placement, checkpoint segments and what is
+ * recomputed in the reverse sweep).  `policy` is NDVM_POLICY_RECOMPUTE.
+ * On success *out receives a handle owned by the library.
+ * Errors: NDVM_E_ARG, NDVM_E_TAPE (malformed tape), NDVM_E_NOMEM,
+ * NDVM_E_DEVICE, NDVM_E_UNSUPPORTED (unknown policy).
+ */
+ndvm_status ndvm_tape_upload(const uint8_t *tape, size_t tape_len, int policy,
+                             void *stream, ndvm_tape **out);
+
+/* Sizes of an uploaded tape.  Errors: NDVM_E_ARG. */
+ndvm_status ndvm_tape_info_get(const ndvm_tape *tape, ndvm_tape_info *out);
+
+/*
+ * Bytes of device workspace ndvm_forward (with_grad = 0) or ndvm_grad
+ * (with_grad = 1) needs for L lanes.  The workspace holds segment
+ * checkpoints and any lane registers that do not fit in LDS.
+ * Errors: NDVM_E_ARG (null handle/pointer, L < 0).
+ */
+ndvm_status ndvm_workspace_bytes(const ndvm_tape *tape, int64_t L, int with_grad,
+                                 size_t *bytes);
+
+/*
+ * Batched forward replay (Section 3.5): loss[l] = E(P, theta_l) for
+ * l = 0..L-1.
+ *   params : device fp64, element (l, p) at params[l*ld_p + p], ld_p >= P
+ *   obs    : device fp64 [n_obs]; n_obs must equal the tape's n_obs
+ *   loss   : device fp64 [L]
+ *   workspace : device buffer of at least ndvm_workspace_bytes(tape, L, 0)
+ *               bytes (may be NULL when that size is 0), 256-byte aligned
+ * L = 0 is a no-op.  Errors: NDVM_E_ARG, NDVM_E_NOMEM (workspace too small),
+ * NDVM_E_DEVICE.
+ */
+ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
+                         int64_t ld_p, const double *obs, int64_t n_obs, double *loss,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Batched forward replay plus the exact reverse-mode sweep (Section 3.4,
+ * Appendix C table tab:adjoints; Property 1 for branches): loss[l] as above
+ * and grad[l*ld_g + p] = d loss_l / d theta_{l,p}.  Branch predicates carry
+ * no gradient; a node whose incoming adjoint is exactly zero contributes
+ * nothing, so untaken select arms cannot poison gradients.
+ * Same argument rules as ndvm_forward plus ld_g >= P; the workspace must
+ * hold ndvm_workspace_bytes(tape, L, 1) bytes.
+ */
+ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L,
+                      int64_t ld_p, const double *obs, int64_t n_obs, double *loss,
+                      double *grad, int64_t ld_g, void *workspace, size_t workspace_bytes,
+                      void *stream);
+
+/*
+ * Many programs in one launch (candidate-level parallelism of Section 6,
+ * "Across cores", mapped onto the GPU grid): program q uses
+ *   params : params + q*prog_stride_p, element (l, p) at [l*ld_p + p]
+ *   loss   : loss + q*L
+ *   grad   : grad + q*prog_stride_g, element (l, p) at [l*ld_g + p]
+ * All programs read the same obs[n_obs] and must declare that n_obs; ld_p and
+ * ld_g must cover the largest P.  Workspace: ndvm_workspace_bytes_many.
+ */
+ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const double *params,
+                           int64_t L, int64_t ld_p, int64_t prog_stride_p, const double *obs,
+                           int64_t n_obs, double *loss, double *grad, int64_t ld_g,
+                           int64_t prog_stride_g, void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/* Workspace bytes for ndvm_grad_many.  Errors: NDVM_E_ARG. */
+ndvm_status ndvm_workspace_bytes_many(const ndvm_tape *const *tapes, int n_prog, int64_t L,
+                                      size_t *bytes);
+
+/* Release a tape handle (NULL is ignored).  Waits for nothing: the caller
+ * must not free a tape while work that uses it is still pending. */
+void ndvm_tape_free(ndvm_tape *tape);
+
+/* Release memory returned by ndvm_tape_build (NULL is ignored). */
+void ndvm_free(void *p);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char *ndvm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NDVM_H */

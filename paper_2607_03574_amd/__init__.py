@@ -1,0 +1,209 @@
+"""Python binding of libndvm (the C ABI declared in include/ndvm.h).
+
+Argument marshalling only: every step of the hot path (trace production,
+scheduling, forward replay, reverse sweep) runs inside libndvm.so.  Torch is
+used for device memory and streams.  If the library has not been built the
+import fails: there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libndvm.so")
+
+OK, E_ARG, E_BYTECODE, E_STRUCT_DIVERGE, E_TAPE, E_NOMEM, E_DEVICE, E_UNSUPPORTED = range(8)
+STATUS_NAMES = {0: "NDVM_OK", 1: "NDVM_E_ARG", 2: "NDVM_E_BYTECODE", 3: "NDVM_E_STRUCT_DIVERGE",
+                4: "NDVM_E_TAPE", 5: "NDVM_E_NOMEM", 6: "NDVM_E_DEVICE", 7: "NDVM_E_UNSUPPORTED"}
+POLICY_RECOMPUTE = 2
+
+# exported symbols of include/ndvm.h
+EXPORTS = ["ndvm_tape_build", "ndvm_tape_upload", "ndvm_tape_info_get", "ndvm_workspace_bytes",
+           "ndvm_forward", "ndvm_grad", "ndvm_grad_many", "ndvm_workspace_bytes_many",
+           "ndvm_tape_free", "ndvm_free", "ndvm_last_error"]
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_03574_amd/build.py "
+                      "(or __graft_entry__.build()); there is no fallback path")
+
+_lib = ctypes.CDLL(LIB_PATH)
+_vp, _i64, _sz, _int = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t, ctypes.c_int
+
+
+class _Info(ctypes.Structure):
+    _fields_ = [("n_params", ctypes.c_uint32), ("n_obs", ctypes.c_uint32), ("n_ops", ctypes.c_uint32),
+                ("n_consts", ctypes.c_uint32), ("loss_slot", ctypes.c_uint32),
+                ("n_selects", ctypes.c_uint32), ("tape_bytes", ctypes.c_uint64)]
+
+
+def _sig(name, res, args):
+    f = getattr(_lib, name)
+    f.restype = res
+    f.argtypes = args
+    return f
+
+
+_tape_build = _sig("ndvm_tape_build", _int, [ctypes.c_char_p, _sz, ctypes.POINTER(_vp), ctypes.POINTER(_sz)])
+_tape_upload = _sig("ndvm_tape_upload", _int, [ctypes.c_char_p, _sz, _int, _vp, ctypes.POINTER(_vp)])
+_tape_info = _sig("ndvm_tape_info_get", _int, [_vp, ctypes.POINTER(_Info)])
+_ws_bytes = _sig("ndvm_workspace_bytes", _int, [_vp, _i64, _int, ctypes.POINTER(_sz)])
+_ws_bytes_many = _sig("ndvm_workspace_bytes_many", _int, [ctypes.POINTER(_vp), _int, _i64, ctypes.POINTER(_sz)])
+_forward = _sig("ndvm_forward", _int, [_vp, _vp, _i64, _i64, _vp, _i64, _vp, _vp, _sz, _vp])
+_grad = _sig("ndvm_grad", _int, [_vp, _vp, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp, _sz, _vp])
+_grad_many = _sig("ndvm_grad_many", _int, [ctypes.POINTER(_vp), _int, _vp, _i64, _i64, _i64, _vp, _i64, _vp,
+                                            _vp, _i64, _i64, _vp, _sz, _vp])
+_tape_free = _sig("ndvm_tape_free", None, [_vp])
+_free = _sig("ndvm_free", None, [_vp])
+_last_error = _sig("ndvm_last_error", ctypes.c_char_p, [])
+
+
+class NdvmError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        msg = (_last_error() or b"").decode(errors="replace")
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def _check(st: int, where: str):
+    if st != OK:
+        raise NdvmError(st, where)
+
+
+def last_error() -> str:
+    return (_last_error() or b"").decode(errors="replace")
+
+
+def tape_build(bytecode: bytes) -> bytes:
+    """Trace producer: stack bytecode -> serialized lane-invariant tape."""
+    out, n = _vp(), _sz()
+    _check(_tape_build(bytecode, len(bytecode), ctypes.byref(out), ctypes.byref(n)), "ndvm_tape_build")
+    try:
+        return ctypes.string_at(out, n.value)
+    finally:
+        _free(out)
+
+
+class Tape:
+    """Owner of an uploaded tape handle."""
+
+    def __init__(self, handle: int):
+        self.handle = handle
+
+    def __del__(self):
+        h, self.handle = getattr(self, "handle", None), None
+        if h:
+            _tape_free(h)
+
+    @property
+    def info(self) -> dict:
+        return tape_info(self)
+
+
+def _stream_ptr(stream):
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def tape_upload(tape_bytes: bytes, policy: int = POLICY_RECOMPUTE, stream=None) -> Tape:
+    h = _vp()
+    _check(_tape_upload(tape_bytes, len(tape_bytes), policy, _stream_ptr(stream), ctypes.byref(h)),
+           "ndvm_tape_upload")
+    return Tape(h.value)
+
+
+def tape_info(tape: Tape) -> dict:
+    info = _Info()
+    _check(_tape_info(tape.handle, ctypes.byref(info)), "ndvm_tape_info_get")
+    return {k: getattr(info, k) for k, _ in _Info._fields_}
+
+
+def workspace_bytes(tape: Tape, L: int, with_grad: bool = True) -> int:
+    n = _sz()
+    _check(_ws_bytes(tape.handle, L, int(with_grad), ctypes.byref(n)), "ndvm_workspace_bytes")
+    return n.value
+
+
+def workspace_bytes_many(tapes: Sequence[Tape], L: int) -> int:
+    arr = (_vp * len(tapes))(*[t.handle for t in tapes])
+    n = _sz()
+    _check(_ws_bytes_many(arr, len(tapes), L, ctypes.byref(n)), "ndvm_workspace_bytes_many")
+    return n.value
+
+
+def _dev_f64(t, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.float64 or not t.is_cuda:
+        raise TypeError(f"{name} must be a float64 CUDA/ROCm tensor")
+    return t
+
+
+def _workspace(tape_or_bytes, device, workspace):
+    import torch
+    need = tape_or_bytes
+    if workspace is None:
+        return torch.empty(max(need, 8), dtype=torch.uint8, device=device), need
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError("workspace too small")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def forward(tape: Tape, params, obs, loss=None, workspace=None, stream=None):
+    """loss[L] for params[L, P] (rows may be padded: params.stride(0) >= P)."""
+    import torch
+    _dev_f64(params, "params")
+    _dev_f64(obs, "obs")
+    if params.dim() != 2 or params.stride(1) != 1 or not obs.is_contiguous():
+        raise ValueError("params must be [L, P] with unit inner stride; obs contiguous")
+    L = params.shape[0]
+    if loss is None:
+        loss = torch.empty(L, dtype=torch.float64, device=params.device)
+    ws, nbytes = _workspace(workspace_bytes(tape, L, False), params.device, workspace)
+    _check(_forward(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
+                    loss.data_ptr(), ws.data_ptr(), nbytes, _stream_ptr(stream)), "ndvm_forward")
+    return loss
+
+
+def grad(tape: Tape, params, obs, loss=None, grad_out=None, workspace=None, stream=None):
+    """(loss[L], grad[L, P]) for params[L, P]."""
+    import torch
+    _dev_f64(params, "params")
+    _dev_f64(obs, "obs")
+    if params.dim() != 2 or params.stride(1) != 1 or not obs.is_contiguous():
+        raise ValueError("params must be [L, P] with unit inner stride; obs contiguous")
+    L, P = params.shape
+    if loss is None:
+        loss = torch.empty(L, dtype=torch.float64, device=params.device)
+    if grad_out is None:
+        grad_out = torch.empty((L, P), dtype=torch.float64, device=params.device)
+    ws, nbytes = _workspace(workspace_bytes(tape, L, True), params.device, workspace)
+    _check(_grad(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
+                 loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(0), ws.data_ptr(), nbytes,
+                 _stream_ptr(stream)), "ndvm_grad")
+    return loss, grad_out
+
+
+def grad_many(tapes: Sequence[Tape], params, obs, loss=None, grad_out=None, workspace=None, stream=None):
+    """Many programs in one launch: params[n_prog, L, Pmax] -> loss[n_prog, L],
+    grad[n_prog, L, Pmax] (entries beyond a program's own P are left as is)."""
+    import torch
+    _dev_f64(params, "params")
+    _dev_f64(obs, "obs")
+    if params.dim() != 3 or params.stride(2) != 1 or not obs.is_contiguous():
+        raise ValueError("params must be [n_prog, L, Pmax] with unit inner stride")
+    n_prog, L, P = params.shape
+    if n_prog != len(tapes):
+        raise ValueError("one tape per program row")
+    if loss is None:
+        loss = torch.empty((n_prog, L), dtype=torch.float64, device=params.device)
+    if grad_out is None:
+        grad_out = torch.zeros((n_prog, L, P), dtype=torch.float64, device=params.device)
+    ws, nbytes = _workspace(workspace_bytes_many(tapes, L), params.device, workspace)
+    arr = (_vp * n_prog)(*[t.handle for t in tapes])
+    _check(_grad_many(arr, n_prog, params.data_ptr(), L, params.stride(1), params.stride(0), obs.data_ptr(),
+                      obs.numel(), loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(1),
+                      grad_out.stride(0), ws.data_ptr(), nbytes, _stream_ptr(stream)), "ndvm_grad_many")
+    return loss, grad_out

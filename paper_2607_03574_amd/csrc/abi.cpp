@@ -1,0 +1,469 @@
+// C ABI of libndvm: tape handles, device programs, workspace sizing and the
+// launch of the replay kernel.  Every entry point validates its arguments
+// before enqueuing anything and converts exceptions into status codes.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstdio>
+#include <cstdlib>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <new>
+
+#include "common.h"
+#include "isa.h"
+#include "sched.h"
+
+namespace ndvm {
+hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
+                         uint32_t r_lds, hipStream_t stream);
+}
+
+using namespace ndvm;
+
+namespace {
+
+struct DeviceProps {
+    int cus = 256;
+    size_t lds_per_cu = 160 * 1024;
+    size_t lds_per_block = 64 * 1024;
+};
+
+std::mutex g_props_mu;
+std::map<int, DeviceProps> g_props;
+
+ndvm_status device_props(DeviceProps *out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        set_error("hipGetDevice failed");
+        return NDVM_E_DEVICE;
+    }
+    std::lock_guard<std::mutex> lk(g_props_mu);
+    auto it = g_props.find(dev);
+    if (it == g_props.end()) {
+        DeviceProps p;
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) p.cus = v;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && v > 0)
+            p.lds_per_block = size_t(v);
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess && v > 0)
+            p.lds_per_cu = size_t(v);
+        it = g_props.emplace(dev, p).first;
+    }
+    *out = it->second;
+    return NDVM_OK;
+}
+
+constexpr size_t kRegBytes = 64 * sizeof(double);   // one register of one wave
+constexpr uint32_t kMaxWavesPerCuTarget = 8;
+
+// Registers per lane that may live in LDS for a launch of `waves` waves:
+// enough waves resident per CU to cover the launch (at most 8), LDS split
+// evenly between them.
+uint32_t reg_budget(const DeviceProps &p, int64_t waves) {
+    int64_t per_cu = (waves + p.cus - 1) / p.cus;
+    per_cu = std::max<int64_t>(1, std::min<int64_t>(per_cu, kMaxWavesPerCuTarget));
+    size_t bytes = std::min(p.lds_per_cu / size_t(per_cu), p.lds_per_block);
+    return uint32_t(bytes / kRegBytes);
+}
+
+struct DevProg {
+    Schedule meta;          // host copy of counts (code/aux vectors released)
+    void *buf = nullptr;    // device: code | aux | consts
+    const uint32_t *code = nullptr;
+    const uint32_t *aux = nullptr;
+    const double *consts = nullptr;
+    ~DevProg() {
+        if (buf) (void)hipFree(buf);
+    }
+};
+
+std::atomic<uint64_t> g_next_id{1};
+
+}  // namespace
+
+struct ndvm_tape {
+    uint64_t id = 0;
+    Tape tape;
+    uint64_t tape_bytes = 0;
+    uint32_t n_selects = 0;
+    int policy = NDVM_POLICY_RECOMPUTE;
+    std::mutex mu;
+    std::unique_ptr<DevProg> fwd;
+    std::map<uint32_t, std::unique_ptr<DevProg>> grad;   // keyed by register budget
+};
+
+namespace {
+
+ndvm_status upload_program(Schedule &&S, const Tape &t, hipStream_t stream, std::unique_ptr<DevProg> *out) {
+    auto dp = std::make_unique<DevProg>();
+    size_t code_b = S.code.size() * 4, aux_b = S.aux.size() * 4, con_b = t.consts.size() * 8;
+    size_t aux_off = (code_b + 255) / 256 * 256, con_off = aux_off + (aux_b + 255) / 256 * 256;
+    size_t total = con_off + std::max<size_t>(con_b, 8);
+    if (hipMalloc(&dp->buf, total) != hipSuccess) {
+        (void)hipGetLastError();
+        dp->buf = nullptr;
+        set_error("hipMalloc of the device program failed");
+        return NDVM_E_NOMEM;
+    }
+    std::vector<uint8_t> host(total, 0);
+    std::memcpy(host.data(), S.code.data(), code_b);
+    if (aux_b) std::memcpy(host.data() + aux_off, S.aux.data(), aux_b);
+    if (con_b) std::memcpy(host.data() + con_off, t.consts.data(), con_b);
+    if (hipMemcpyAsync(dp->buf, host.data(), total, hipMemcpyHostToDevice, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess) {
+        set_error("copy of the device program failed");
+        return NDVM_E_DEVICE;
+    }
+    dp->code = reinterpret_cast<const uint32_t *>(dp->buf);
+    dp->aux = reinterpret_cast<const uint32_t *>(static_cast<uint8_t *>(dp->buf) + aux_off);
+    dp->consts = reinterpret_cast<const double *>(static_cast<uint8_t *>(dp->buf) + con_off);
+    S.code.clear();
+    S.code.shrink_to_fit();
+    S.aux.clear();
+    S.aux.shrink_to_fit();
+    dp->meta = std::move(S);
+    *out = std::move(dp);
+    return NDVM_OK;
+}
+
+// Device program of `tape` for gradient launches with register budget b.
+ndvm_status grad_program(ndvm_tape *tape, uint32_t b, hipStream_t stream, DevProg **out) {
+    std::lock_guard<std::mutex> lk(tape->mu);
+    auto it = tape->grad.find(b);
+    if (it == tape->grad.end()) {
+        std::unique_ptr<DevProg> dp;
+        ndvm_status st = upload_program(schedule_grad(tape->tape, b), tape->tape, stream, &dp);
+        if (st != NDVM_OK) return st;
+        it = tape->grad.emplace(b, std::move(dp)).first;
+    }
+    *out = it->second.get();
+    return NDVM_OK;
+}
+
+int64_t lpad_of(int64_t L) { return (L + 63) / 64 * 64; }
+
+// Workspace rows (fp64 per lane) of one program launched with LDS budget b.
+uint64_t ws_rows(const DevProg &dp, uint32_t b) {
+    uint32_t r_lds = std::min(dp.meta.n_regs, b);
+    return uint64_t(dp.meta.n_ckpt_rows) + (dp.meta.n_regs - r_lds);
+}
+
+ndvm_status check_stream_and_launch(const LaunchArgs &A, const ProgStatic *table, const ProgStatic &single,
+                                    uint32_t n_prog, uint32_t r_lds, hipStream_t stream) {
+    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, stream);
+    if (e != hipSuccess) {
+        set_error(std::string("kernel launch failed: ") + hipGetErrorString(e));
+        return NDVM_E_DEVICE;
+    }
+    return NDVM_OK;
+}
+
+// Device tables of ProgStatic for ndvm_grad_many, cached per program set.
+std::mutex g_table_mu;
+std::map<std::vector<uint64_t>, void *> g_tables;
+
+template <class F>
+ndvm_status guarded(F f) {
+    try {
+        return f();
+    } catch (const std::bad_alloc &) {
+        set_error("out of host memory");
+        return NDVM_E_NOMEM;
+    } catch (const std::exception &e) {
+        set_error(std::string("internal error: ") + e.what());
+        return NDVM_E_ARG;
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ndvm_last_error(void) { return get_error(); }
+
+void ndvm_free(void *p) { std::free(p); }
+
+ndvm_status ndvm_tape_build(const uint8_t *bytecode, size_t len, uint8_t **tape, size_t *tape_len) {
+    return guarded([&]() -> ndvm_status {
+        if (!bytecode || !tape || !tape_len) {
+            set_error("ndvm_tape_build: null argument");
+            return NDVM_E_ARG;
+        }
+        std::vector<uint8_t> out;
+        ndvm_status st = build_tape(bytecode, len, &out);
+        if (st != NDVM_OK) return st;
+        void *p = std::malloc(out.size());
+        if (!p) {
+            set_error("out of host memory");
+            return NDVM_E_NOMEM;
+        }
+        std::memcpy(p, out.data(), out.size());
+        *tape = static_cast<uint8_t *>(p);
+        *tape_len = out.size();
+        return NDVM_OK;
+    });
+}
+
+ndvm_status ndvm_tape_upload(const uint8_t *bytes, size_t len, int policy, void *stream, ndvm_tape **out) {
+    return guarded([&]() -> ndvm_status {
+        if (!bytes || !out) {
+            set_error("ndvm_tape_upload: null argument");
+            return NDVM_E_ARG;
+        }
+        if (policy != NDVM_POLICY_RECOMPUTE) {
+            set_error("ndvm_tape_upload: unsupported save policy");
+            return NDVM_E_UNSUPPORTED;
+        }
+        auto h = std::make_unique<ndvm_tape>();
+        ndvm_status st = parse_tape(bytes, len, &h->tape);
+        if (st != NDVM_OK) return st;
+        h->id = g_next_id++;
+        h->tape_bytes = len;
+        h->policy = policy;
+        for (const TapeOp &o : h->tape.ops) h->n_selects += o.code == tp::SELECT;
+        st = upload_program(schedule_forward(h->tape), h->tape, static_cast<hipStream_t>(stream), &h->fwd);
+        if (st != NDVM_OK) return st;
+        *out = h.release();
+        return NDVM_OK;
+    });
+}
+
+ndvm_status ndvm_tape_info_get(const ndvm_tape *t, ndvm_tape_info *out) {
+    if (!t || !out) {
+        set_error("ndvm_tape_info_get: null argument");
+        return NDVM_E_ARG;
+    }
+    out->n_params = t->tape.n_params;
+    out->n_obs = t->tape.n_obs;
+    out->n_ops = uint32_t(t->tape.ops.size());
+    out->n_consts = uint32_t(t->tape.consts.size());
+    out->loss_slot = t->tape.loss;
+    out->n_selects = t->n_selects;
+    out->tape_bytes = t->tape_bytes;
+    return NDVM_OK;
+}
+
+void ndvm_tape_free(ndvm_tape *t) {
+    if (!t) return;
+    {
+        std::lock_guard<std::mutex> lk(g_table_mu);
+        for (auto it = g_tables.begin(); it != g_tables.end();) {
+            bool uses = false;
+            for (size_t i = 0; i + 1 < it->first.size(); i += 2) uses = uses || it->first[i] == t->id;
+            if (uses) {
+                (void)hipFree(it->second);
+                it = g_tables.erase(it);
+            } else {
+                ++it;
+            }
+        }
+    }
+    delete t;
+}
+
+ndvm_status ndvm_workspace_bytes(const ndvm_tape *tape, int64_t L, int with_grad, size_t *bytes) {
+    return guarded([&]() -> ndvm_status {
+        if (!tape || !bytes || L < 0) {
+            set_error("ndvm_workspace_bytes: bad argument");
+            return NDVM_E_ARG;
+        }
+        DeviceProps p;
+        ndvm_status st = device_props(&p);
+        if (st != NDVM_OK) return st;
+        int64_t Lp = lpad_of(L);
+        uint32_t b = reg_budget(p, Lp / 64);
+        uint64_t rows;
+        if (with_grad) {
+            DevProg *dp;
+            st = grad_program(const_cast<ndvm_tape *>(tape), b, nullptr, &dp);
+            if (st != NDVM_OK) return st;
+            rows = ws_rows(*dp, b);
+        } else {
+            uint32_t bf = uint32_t(p.lds_per_block / kRegBytes);
+            rows = ws_rows(*tape->fwd, bf);
+        }
+        *bytes = size_t(rows * uint64_t(Lp) * sizeof(double));
+        return NDVM_OK;
+    });
+}
+
+ndvm_status ndvm_workspace_bytes_many(const ndvm_tape *const *tapes, int n_prog, int64_t L, size_t *bytes) {
+    return guarded([&]() -> ndvm_status {
+        if (!tapes || n_prog < 0 || !bytes || L < 0) {
+            set_error("ndvm_workspace_bytes_many: bad argument");
+            return NDVM_E_ARG;
+        }
+        DeviceProps p;
+        ndvm_status st = device_props(&p);
+        if (st != NDVM_OK) return st;
+        int64_t Lp = lpad_of(L);
+        uint32_t b = reg_budget(p, Lp / 64 * n_prog);
+        uint64_t rows = 0;
+        for (int q = 0; q < n_prog; ++q) {
+            if (!tapes[q]) {
+                set_error("ndvm_workspace_bytes_many: null tape");
+                return NDVM_E_ARG;
+            }
+            DevProg *dp;
+            st = grad_program(const_cast<ndvm_tape *>(tapes[q]), b, nullptr, &dp);
+            if (st != NDVM_OK) return st;
+            rows += ws_rows(*dp, b);
+        }
+        *bytes = size_t(rows * uint64_t(Lp) * sizeof(double));
+        return NDVM_OK;
+    });
+}
+
+static ndvm_status check_common(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p,
+                                const double *obs, int64_t n_obs, const double *loss, const char *who) {
+    if (!tape) {
+        set_error(std::string(who) + ": null tape");
+        return NDVM_E_ARG;
+    }
+    if (L < 0 || (L > 0 && (!loss || (tape->tape.n_params > 0 && !params)))) {
+        set_error(std::string(who) + ": bad lane count or null buffer");
+        return NDVM_E_ARG;
+    }
+    if (ld_p < int64_t(tape->tape.n_params) || ld_p < 0) {
+        set_error(std::string(who) + ": ld_p smaller than the parameter count");
+        return NDVM_E_ARG;
+    }
+    if (n_obs != int64_t(tape->tape.n_obs) || (n_obs > 0 && !obs)) {
+        set_error(std::string(who) + ": n_obs does not match the tape");
+        return NDVM_E_ARG;
+    }
+    return NDVM_OK;
+}
+
+ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p, const double *obs,
+                         int64_t n_obs, double *loss, void *ws, size_t ws_bytes, void *stream) {
+    return guarded([&]() -> ndvm_status {
+        ndvm_status st = check_common(tape, params, L, ld_p, obs, n_obs, loss, "ndvm_forward");
+        if (st != NDVM_OK) return st;
+        if (L == 0) return NDVM_OK;
+        DeviceProps p;
+        if ((st = device_props(&p)) != NDVM_OK) return st;
+        const DevProg &dp = *tape->fwd;
+        uint32_t r_lds = std::min<uint32_t>(dp.meta.n_regs, uint32_t(p.lds_per_block / kRegBytes));
+        int64_t Lp = lpad_of(L);
+        size_t need = size_t(ws_rows(dp, r_lds) * uint64_t(Lp) * sizeof(double));
+        if (need && (!ws || ws_bytes < need)) {
+            set_error("ndvm_forward: workspace too small");
+            return NDVM_E_NOMEM;
+        }
+        LaunchArgs A{obs, params, loss, loss, static_cast<double *>(ws), ld_p, 0, L, Lp, 0, 0};
+        ProgStatic S{dp.code, dp.aux, dp.consts, 0, 0, r_lds, 0};
+        return check_stream_and_launch(A, nullptr, S, 1, r_lds, static_cast<hipStream_t>(stream));
+    });
+}
+
+ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p, const double *obs,
+                      int64_t n_obs, double *loss, double *grad, int64_t ld_g, void *ws, size_t ws_bytes,
+                      void *stream) {
+    return guarded([&]() -> ndvm_status {
+        ndvm_status st = check_common(tape, params, L, ld_p, obs, n_obs, loss, "ndvm_grad");
+        if (st != NDVM_OK) return st;
+        if (ld_g < int64_t(tape->tape.n_params) || ld_g < 0 || (L > 0 && tape->tape.n_params > 0 && !grad)) {
+            set_error("ndvm_grad: bad grad buffer or ld_g");
+            return NDVM_E_ARG;
+        }
+        if (L == 0) return NDVM_OK;
+        DeviceProps p;
+        if ((st = device_props(&p)) != NDVM_OK) return st;
+        int64_t Lp = lpad_of(L);
+        uint32_t b = reg_budget(p, Lp / 64);
+        DevProg *dp;
+        if ((st = grad_program(const_cast<ndvm_tape *>(tape), b, static_cast<hipStream_t>(stream), &dp)) != NDVM_OK)
+            return st;
+        uint32_t r_lds = std::min(dp->meta.n_regs, b);
+        size_t need = size_t(ws_rows(*dp, b) * uint64_t(Lp) * sizeof(double));
+        if (need && (!ws || ws_bytes < need)) {
+            set_error("ndvm_grad: workspace too small");
+            return NDVM_E_NOMEM;
+        }
+        double *wsd = static_cast<double *>(ws);
+        LaunchArgs A{obs, params, loss, grad, wsd, ld_p, ld_g, L, Lp, 0, 0};
+        ProgStatic S{dp->code, dp->aux, dp->consts, 0, dp->meta.n_ckpt_rows, r_lds, 0};
+        return check_stream_and_launch(A, nullptr, S, 1, r_lds, static_cast<hipStream_t>(stream));
+    });
+}
+
+ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const double *params, int64_t L, int64_t ld_p,
+                           int64_t prog_stride_p, const double *obs, int64_t n_obs, double *loss, double *grad,
+                           int64_t ld_g, int64_t prog_stride_g, void *ws, size_t ws_bytes, void *stream) {
+    return guarded([&]() -> ndvm_status {
+        if (!tapes || n_prog < 0) {
+            set_error("ndvm_grad_many: bad program list");
+            return NDVM_E_ARG;
+        }
+        if (n_prog == 0 || L == 0) return NDVM_OK;
+        uint32_t pmax = 0;
+        for (int q = 0; q < n_prog; ++q) {
+            ndvm_status st = check_common(tapes[q], params, L, ld_p, obs, n_obs, loss, "ndvm_grad_many");
+            if (st != NDVM_OK) return st;
+            pmax = std::max(pmax, tapes[q]->tape.n_params);
+        }
+        if (ld_g < int64_t(pmax) || (pmax > 0 && !grad) || prog_stride_p < L * ld_p ||
+            prog_stride_g < L * ld_g || L < 0) {
+            set_error("ndvm_grad_many: bad strides");
+            return NDVM_E_ARG;
+        }
+        DeviceProps p;
+        ndvm_status st = device_props(&p);
+        if (st != NDVM_OK) return st;
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        int64_t Lp = lpad_of(L);
+        uint32_t b = reg_budget(p, Lp / 64 * n_prog);
+        std::vector<ProgStatic> table(static_cast<size_t>(n_prog), ProgStatic{});
+        std::vector<uint64_t> key;
+        uint64_t row = 0;
+        uint32_t r_launch = 0;
+        for (int q = 0; q < n_prog; ++q) {
+            DevProg *dp;
+            if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), b, s, &dp)) != NDVM_OK) return st;
+            uint32_t r_lds = std::min(dp->meta.n_regs, b);
+            r_launch = std::max(r_launch, r_lds);
+            table[q] = ProgStatic{dp->code, dp->aux, dp->consts, row, row + dp->meta.n_ckpt_rows, r_lds, 0};
+            row += ws_rows(*dp, b);
+            key.push_back(tapes[q]->id);
+            key.push_back(b);
+        }
+        size_t need = size_t(row * uint64_t(Lp) * sizeof(double));
+        if (need && (!ws || ws_bytes < need)) {
+            set_error("ndvm_grad_many: workspace too small");
+            return NDVM_E_NOMEM;
+        }
+        void *d_table = nullptr;
+        {
+            std::lock_guard<std::mutex> lk(g_table_mu);
+            auto it = g_tables.find(key);
+            if (it == g_tables.end()) {
+                if (hipMalloc(&d_table, table.size() * sizeof(ProgStatic)) != hipSuccess) {
+                    (void)hipGetLastError();
+                    set_error("hipMalloc of the program table failed");
+                    return NDVM_E_NOMEM;
+                }
+                if (hipMemcpyAsync(d_table, table.data(), table.size() * sizeof(ProgStatic), hipMemcpyHostToDevice,
+                                   s) != hipSuccess ||
+                    hipStreamSynchronize(s) != hipSuccess) {
+                    (void)hipFree(d_table);
+                    set_error("copy of the program table failed");
+                    return NDVM_E_DEVICE;
+                }
+                g_tables.emplace(key, d_table);
+            } else {
+                d_table = it->second;
+            }
+        }
+        LaunchArgs A{obs, params, loss, grad, static_cast<double *>(ws), ld_p, ld_g, L, Lp, prog_stride_p,
+                     prog_stride_g};
+        ProgStatic none{};
+        return check_stream_and_launch(A, static_cast<const ProgStatic *>(d_table), none, uint32_t(n_prog),
+                                       r_launch, s);
+    });
+}
+
+}  // extern "C"

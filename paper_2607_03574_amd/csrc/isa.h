@@ -1,0 +1,85 @@
+// Device program format executed by the replay kernel.  Produced by the
+// scheduler from a validated tape; not part of the public interface.
+//
+// A program is a sequence of 8-word instructions.  Each lane owns a file of
+// fp64 "registers" (lane values and adjoints); register r of lane l lives in
+// LDS when r < R_lds and in the workspace spill area otherwise.
+//
+//   w0 : op (bits 0-7) | mode (8-15) | nel (16-23)
+//   w1 : destination register (forward) / adjoint register g of the output
+//        (reverse)
+//   w2, w3 : operands a, b     w4 : operand c / output value z (reverse)
+//   w5 : operand d (select) / adjoint target of a (reverse)
+//   w6 : adjoint target of b (reverse)
+//   w7 : immediate (dims, element index, aux offset, checkpoint row, param)
+//
+// Operand words: bits 31-30 kind (0 register, 1 constant pool, 2 obs),
+// bits 29-0 index.  Adjoint target words: register | kInit (first
+// contribution: store instead of add), or kNone.
+#pragma once
+#include <cstdint>
+
+namespace ndvm {
+namespace isa {
+
+enum : uint32_t {
+    END = 0,
+    LDPARAM = 1,   // w1 dst, w7 param index
+    ST_LOSS = 2,   // w2 operand
+    CKPT_ST = 3,   // w2 src reg, w7 checkpoint row, nel
+    CKPT_LD = 4,   // w1 dst reg, w7 checkpoint row, nel
+    ZERO = 5,      // w1 dst reg, nel
+    SEED = 6,      // w5 target
+    ST_GRAD = 7,   // w2 src reg, w7 param index
+
+    F_ADD = 16, F_SUB, F_MUL, F_DIV, F_NEG, F_EXP, F_LOG, F_SQRT, F_SIN, F_COS, F_ABS, F_POW,
+    F_DOT, F_MATMUL, F_TRANSPOSE, F_TRACE, F_INV, F_DET, F_LOGDET, F_OUTER, F_PACK, F_INDEX,
+    F_SELECT,
+
+    R_ADD = 48, R_SUB, R_MUL, R_DIV, R_NEG, R_EXP, R_LOG, R_SQRT, R_SIN, R_COS, R_ABS, R_POW,
+    R_DOT, R_MATMUL, R_TRANSPOSE, R_TRACE, R_INV, R_DET, R_LOGDET, R_OUTER, R_PACK, R_INDEX,
+    R_SELECT,
+    OP_COUNT
+};
+
+// binary elementwise broadcast modes (w0 bits 8-15)
+enum : uint32_t { MODE_SAME = 0, MODE_A_SCALAR = 1, MODE_B_SCALAR = 2 };
+
+constexpr uint32_t kKindShift = 30;
+constexpr uint32_t kKindReg = 0, kKindConst = 1, kKindObs = 2;
+constexpr uint32_t kIndexMask = (1u << 30) - 1;
+constexpr uint32_t kInit = 0x80000000u;
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+constexpr uint32_t kWords = 8;
+
+inline uint32_t w0(uint32_t op, uint32_t mode, uint32_t nel) { return op | (mode << 8) | (nel << 16); }
+inline uint32_t dims(uint32_t m, uint32_t k, uint32_t n) { return m | (k << 8) | (n << 16); }
+
+}  // namespace isa
+
+// Per-program constants read by the kernel: the device program and where the
+// program's checkpoint and spill rows start in the workspace.  Depends only
+// on the program and the launch's register budget, never on per-call
+// pointers, so a table of these can be cached on the device.
+struct ProgStatic {
+    const uint32_t *prog;    // instruction words
+    const uint32_t *aux;     // operand / target lists
+    const double *consts;    // constant pool
+    uint64_t ckpt_row0;      // checkpoint row r of lane l at ws[(ckpt_row0 + r)*Lpad + l]
+    uint64_t spill_row0;     // register r_lds + r of lane l at ws[(spill_row0 + r)*Lpad + l]
+    uint32_t r_lds;          // registers held in LDS
+    uint32_t pad_;
+};
+
+// Per-call arguments.  Program q of a launch (blockIdx.y) reads
+// params + q*prog_stride_p and writes loss + q*L, grad + q*prog_stride_g.
+struct LaunchArgs {
+    const double *obs;
+    const double *params;
+    double *loss;
+    double *grad;
+    double *ws;
+    int64_t ld_p, ld_g, L, Lpad, prog_stride_p, prog_stride_g;
+};
+
+}  // namespace ndvm

@@ -1,0 +1,106 @@
+// Replay kernel: forward replay and reverse sweep of a scheduled tape, one
+// lane (parameter vector) per GPU thread (Section 3.5: one structural walk,
+// numeric payloads widened over the batch axis).
+//
+// Every instruction is wave-uniform: the opcode and operand words come from
+// the device program by scalar loads, so all 64 lanes of a wave follow the
+// same control and branch only on uniform values; per-lane numeric branches
+// were turned into selects by the trace producer.  Lane registers live in LDS
+// (register r of thread t at lds[r*64 + t], conflict-free 8-byte accesses)
+// and, beyond R_lds, in a lane-contiguous workspace area, so every global
+// access of a wave is one coalesced 512-byte row.  Small matrices (up to 4x4)
+// are loaded into VGPR arrays by fully unrolled code and multiplied with
+// fused multiply-add chains; nothing here is a dense contraction, so no
+// matrix cores are used.
+//
+#include <hip/hip_runtime.h>
+
+#include "isa.h"
+#include "replay.h"
+
+namespace ndvm {
+namespace {
+
+// Lane context on the GPU: register r of thread t at lds[r*64 + t] when
+// r < r_lds, else in the workspace spill rows; all addressing lane-contiguous.
+struct DevCtx {
+    double *lds;
+    double *spill;
+    const double *consts;
+    const double *obs;
+    const double *params;
+    double *loss, *grad, *ckpt;
+    int64_t lane, lc, Lpad, ld_p, ld_g;
+    uint32_t r_lds;
+    int t;
+    bool active;
+
+    __device__ __forceinline__ static uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+    __device__ __forceinline__ double ld(uint32_t r) const {
+        if (r < r_lds) return lds[r * 64u + t];
+        return spill[int64_t(r - r_lds) * Lpad + lane];
+    }
+    __device__ __forceinline__ void st(uint32_t r, double v) const {
+        if (r < r_lds)
+            lds[r * 64u + t] = v;
+        else
+            spill[int64_t(r - r_lds) * Lpad + lane] = v;
+    }
+    __device__ __forceinline__ double konst(uint32_t i) const { return consts[i]; }
+    __device__ __forceinline__ double obsv(uint32_t i) const { return obs[i]; }
+    __device__ __forceinline__ double param(uint32_t p) const { return params[lc * ld_p + p]; }
+    __device__ __forceinline__ void store_loss(double v) const {
+        if (active) loss[lane] = v;
+    }
+    __device__ __forceinline__ void store_grad(uint32_t p, double v) const {
+        if (active) grad[lane * ld_g + p] = v;
+    }
+    __device__ __forceinline__ void ckpt_st(uint32_t row, double v) const { ckpt[int64_t(row) * Lpad + lane] = v; }
+    __device__ __forceinline__ double ckpt_ld(uint32_t row) const { return ckpt[int64_t(row) * Lpad + lane]; }
+};
+
+}  // namespace
+
+extern "C" __global__ void __launch_bounds__(64)
+ndvm_replay(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
+    extern __shared__ double lds_regs[];
+    const uint32_t q = blockIdx.y;
+    const ProgStatic D = table ? table[q] : single;
+    DevCtx c;
+    c.t = threadIdx.x;
+    c.lane = int64_t(blockIdx.x) * 64 + c.t;
+    c.active = c.lane < A.L;
+    c.lc = c.active ? c.lane : A.L - 1;
+    c.lds = lds_regs;
+    c.spill = A.ws + int64_t(D.spill_row0) * A.Lpad;
+    c.ckpt = A.ws + int64_t(D.ckpt_row0) * A.Lpad;
+    c.consts = D.consts;
+    c.obs = A.obs;
+    c.params = A.params + int64_t(q) * A.prog_stride_p;
+    c.loss = A.loss + int64_t(q) * A.L;
+    c.grad = A.grad + int64_t(q) * A.prog_stride_g;
+    c.Lpad = A.Lpad;
+    c.ld_p = A.ld_p;
+    c.ld_g = A.ld_g;
+    c.r_lds = D.r_lds;
+    replay::run(c, D.prog, D.aux);
+}
+
+hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
+                         uint32_t r_lds, hipStream_t stream) {
+    static bool attr_set = false;
+    if (!attr_set) {
+        int dev = 0, max_smem = 0;
+        (void)hipGetDevice(&dev);
+        (void)hipDeviceGetAttribute(&max_smem, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&ndvm_replay),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
+        attr_set = true;
+    }
+    dim3 grid(uint32_t(A.Lpad / 64), n_prog), block(64);
+    size_t smem = size_t(r_lds) * 64 * sizeof(double);
+    hipLaunchKernelGGL(ndvm_replay, grid, block, smem, stream, A, d_table, single);
+    return hipGetLastError();
+}
+
+}  // namespace ndvm

@@ -1,0 +1,508 @@
+// Instruction handlers of the device program, shared by the GPU replay
+// kernel and the host-side emulator used to check the scheduler.
+//
+// A context type C supplies the lane's register file and memory:
+//   double ld(uint32_t r) const;  void st(uint32_t r, double v) const;
+//   double konst(uint32_t i) const;  double obsv(uint32_t i) const;
+//   static uint32_t uni(uint32_t x);          (wave-uniform value)
+//   double param(uint32_t p) const;  void store_loss(double) const;
+//   void store_grad(uint32_t p, double) const;
+//   void ckpt_st(uint32_t row, double) const;  double ckpt_ld(uint32_t row) const;
+//
+// Adjoint rules follow Appendix C, table tab:adjoints, with these readings:
+// contractions are fma chains over the summation index in ascending order
+// (first term a plain product); sqrt/log clamp at 1e-8 with no adjoint at or
+// below it; sign(0) = 0; the denominator adjoint of a division is g*z/b; a
+// node whose incoming adjoint is zero in every element leaves its inputs'
+// adjoints untouched (the gating that keeps an untaken select arm from
+// producing 0*inf); the first contribution to an adjoint stores 0 + x.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "isa.h"
+
+#define NDVM_HD __host__ __device__ __forceinline__
+
+namespace ndvm {
+namespace replay {
+
+using namespace isa;
+
+// scalar operand word: register, constant-pool entry or observation
+template <class C>
+NDVM_HD double opnd(const C &c, uint32_t w) {
+    uint32_t kind = w >> kKindShift, idx = w & kIndexMask;
+    if (kind == kKindReg) return c.ld(idx);
+    if (kind == kKindConst) return c.konst(idx);
+    return c.obsv(idx);
+}
+// element i of an operand (only registers hold more than one element)
+template <class C>
+NDVM_HD double elem(const C &c, uint32_t w, uint32_t i) {
+    return (w >> kKindShift) ? opnd(c, w) : c.ld(w + i);
+}
+// adjoint update of element i of target word tw with contribution x when
+// `on` holds for this lane; the first contribution stores (0 + x)
+template <class C>
+NDVM_HD void acc(const C &c, uint32_t tw, uint32_t i, double x, bool on) {
+    if (tw == kNone) return;
+    uint32_t r = (tw & ~kInit) + i;
+    if (tw & kInit) {
+        c.st(r, on ? 0.0 + x : 0.0);
+    } else {
+        double v = c.ld(r);
+        c.st(r, on ? v + x : v);
+    }
+}
+
+NDVM_HD double clampv(double x) { return x < 1e-8 ? 1e-8 : x; }
+
+// load an m x n row-major matrix stored at consecutive registers into M[i*4+j]
+template <class C>
+NDVM_HD void load_mat(const C &c, uint32_t base, uint32_t m, uint32_t n, double (&M)[16]) {
+#pragma unroll
+    for (uint32_t i = 0; i < 4; ++i)
+#pragma unroll
+        for (uint32_t j = 0; j < 4; ++j) M[i * 4 + j] = (i < m && j < n) ? c.ld(base + i * n + j) : 0.0;
+}
+
+NDVM_HD double det2(const double (&A)[16], uint32_t sz) {
+    if (sz == 1) return A[0];
+    double t1 = A[0] * A[5];
+    double t2 = A[1] * A[4];
+    return t1 - t2;
+}
+// inverse (adjugate times r = 1/det), packed into Ai[i*4+j]
+NDVM_HD void inv2(const double (&A)[16], uint32_t sz, double (&Ai)[16]) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) Ai[i] = 0.0;
+    if (sz == 1) {
+        Ai[0] = 1.0 / A[0];
+        return;
+    }
+    double r = 1.0 / det2(A, 2);
+    Ai[0] = A[5] * r;
+    Ai[1] = (-A[1]) * r;
+    Ai[4] = (-A[4]) * r;
+    Ai[5] = A[0] * r;
+}
+
+template <class C>
+NDVM_HD bool any_nz(const C &c, uint32_t g, uint32_t n) {
+    bool nz = false;
+    for (uint32_t i = 0; i < n; ++i) nz = nz || (c.ld(g + i) != 0.0);
+    return nz;
+}
+
+NDVM_HD double unary_fwd(uint32_t op, double x) {
+    switch (op) {
+    case F_NEG: return -x;
+    case F_EXP: return exp(x);
+    case F_LOG: return log(clampv(x));
+    case F_SQRT: return sqrt(clampv(x));
+    case F_SIN: return sin(x);
+    case F_COS: return cos(x);
+    default: return fabs(x);
+    }
+}
+
+template <class C>
+NDVM_HD void exec_fwd(const C &c, const uint32_t *aux, const uint32_t *w) {
+    const uint32_t op = w[0] & 0xFF, mode = (w[0] >> 8) & 0xFF, n = (w[0] >> 16) & 0xFF;
+    const uint32_t dst = w[1];
+    switch (op) {
+    case F_ADD: case F_SUB: case F_MUL: case F_DIV: {
+        for (uint32_t i = 0; i < n; ++i) {
+            double x = mode == MODE_A_SCALAR ? opnd(c, w[2]) : elem(c, w[2], i);
+            double y = mode == MODE_B_SCALAR ? opnd(c, w[3]) : elem(c, w[3], i);
+            double z = op == F_ADD ? x + y : op == F_SUB ? x - y : op == F_MUL ? x * y : x / y;
+            c.st(dst + i, z);
+        }
+        break;
+    }
+    case F_NEG: case F_EXP: case F_LOG: case F_SQRT: case F_SIN: case F_COS: case F_ABS:
+        for (uint32_t i = 0; i < n; ++i) c.st(dst + i, unary_fwd(op, elem(c, w[2], i)));
+        break;
+    case F_POW:
+        c.st(dst, pow(opnd(c, w[2]), opnd(c, w[3])));
+        break;
+    case F_DOT: {
+        double s = elem(c, w[2], 0) * elem(c, w[3], 0);
+        for (uint32_t i = 1; i < n; ++i) s = fma(elem(c, w[2], i), elem(c, w[3], i), s);
+        c.st(dst, s);
+        break;
+    }
+    case F_MATMUL: {
+        const uint32_t m = w[7] & 0xFF, k = (w[7] >> 8) & 0xFF, q = (w[7] >> 16) & 0xFF;
+        double A[16], B[16];
+        load_mat(c, w[2], m, k, A);
+        load_mat(c, w[3], k, q, B);
+#pragma unroll
+        for (uint32_t i = 0; i < 4; ++i)
+#pragma unroll
+            for (uint32_t j = 0; j < 4; ++j) {
+                if (i < m && j < q) {
+                    double s = A[i * 4] * B[j];
+#pragma unroll
+                    for (uint32_t p = 1; p < 4; ++p)
+                        if (p < k) s = fma(A[i * 4 + p], B[p * 4 + j], s);
+                    c.st(dst + i * q + j, s);
+                }
+            }
+        break;
+    }
+    case F_TRANSPOSE: {
+        const uint32_t m = w[7] & 0xFF, q = (w[7] >> 8) & 0xFF;   // input m x q
+        for (uint32_t i = 0; i < m; ++i)
+            for (uint32_t j = 0; j < q; ++j) c.st(dst + j * m + i, c.ld(w[2] + i * q + j));
+        break;
+    }
+    case F_TRACE: {
+        const uint32_t sz = w[7];
+        double s = c.ld(w[2]);
+        for (uint32_t i = 1; i < sz; ++i) s = s + c.ld(w[2] + i * sz + i);
+        c.st(dst, s);
+        break;
+    }
+    case F_INV: case F_DET: case F_LOGDET: {
+        const uint32_t sz = w[7];
+        double A[16], Ai[16];
+        load_mat(c, w[2], sz, sz, A);
+        if (op == F_INV) {
+            inv2(A, sz, Ai);
+#pragma unroll
+            for (uint32_t i = 0; i < 2; ++i)
+#pragma unroll
+                for (uint32_t j = 0; j < 2; ++j)
+                    if (i < sz && j < sz) c.st(dst + i * sz + j, Ai[i * 4 + j]);
+        } else {
+            double d = det2(A, sz);
+            c.st(dst, op == F_DET ? d : log(clampv(d)));
+        }
+        break;
+    }
+    case F_OUTER: {
+        const uint32_t m = w[7] & 0xFF, q = (w[7] >> 8) & 0xFF;
+        for (uint32_t i = 0; i < m; ++i) {
+            double a = elem(c, w[2], i);
+            for (uint32_t j = 0; j < q; ++j) c.st(dst + i * q + j, a * elem(c, w[3], j));
+        }
+        break;
+    }
+    case F_PACK:
+        for (uint32_t i = 0; i < n; ++i) c.st(dst + i, opnd(c, C::uni(aux[w[7] + i])));
+        break;
+    case F_INDEX:
+        c.st(dst, c.ld(w[2] + w[7]));
+        break;
+    case F_SELECT: {
+        const bool p = opnd(c, w[2]) < opnd(c, w[3]);
+        for (uint32_t i = 0; i < n; ++i) {
+            double x = elem(c, w[4], i), y = elem(c, w[5], i);
+            c.st(dst + i, p ? x : y);
+        }
+        break;
+    }
+    default:
+        break;
+    }
+}
+
+template <class C>
+NDVM_HD void exec_rev(const C &c, const uint32_t *aux, const uint32_t *w) {
+    const uint32_t op = w[0] & 0xFF, mode = (w[0] >> 8) & 0xFF, n = (w[0] >> 16) & 0xFF;
+    const uint32_t g = w[1], ta = w[5], tb = w[6];
+    switch (op) {
+    case R_ADD: case R_SUB: {
+        const bool nz = any_nz(c, g, n);
+        for (uint32_t i = 0; i < n; ++i) acc(c, ta, i, c.ld(g + i), nz);
+        for (uint32_t i = 0; i < n; ++i) {
+            double gi = c.ld(g + i);
+            acc(c, tb, i, op == R_ADD ? gi : -gi, nz);
+        }
+        break;
+    }
+    case R_MUL: {
+        const bool nz = any_nz(c, g, n);
+        if (mode == MODE_SAME) {
+            for (uint32_t i = 0; i < n; ++i) acc(c, ta, i, c.ld(g + i) * elem(c, w[3], i), nz);
+            for (uint32_t i = 0; i < n; ++i) acc(c, tb, i, c.ld(g + i) * elem(c, w[2], i), nz);
+        } else if (mode == MODE_A_SCALAR) {   // z = s * M
+            double s = c.ld(g) * elem(c, w[3], 0);
+            for (uint32_t i = 1; i < n; ++i) s = fma(c.ld(g + i), elem(c, w[3], i), s);
+            acc(c, ta, 0, s, nz);
+            const double a = opnd(c, w[2]);
+            for (uint32_t i = 0; i < n; ++i) acc(c, tb, i, c.ld(g + i) * a, nz);
+        } else {                             // z = M * s
+            const double b = opnd(c, w[3]);
+            for (uint32_t i = 0; i < n; ++i) acc(c, ta, i, c.ld(g + i) * b, nz);
+            double s = c.ld(g) * elem(c, w[2], 0);
+            for (uint32_t i = 1; i < n; ++i) s = fma(c.ld(g + i), elem(c, w[2], i), s);
+            acc(c, tb, 0, s, nz);
+        }
+        break;
+    }
+    case R_DIV: {
+        const bool nz = any_nz(c, g, n);
+        if (mode == MODE_SAME) {
+            for (uint32_t i = 0; i < n; ++i) acc(c, ta, i, c.ld(g + i) / elem(c, w[3], i), nz);
+            for (uint32_t i = 0; i < n; ++i)
+                acc(c, tb, i, -((c.ld(g + i) * elem(c, w[4], i)) / elem(c, w[3], i)), nz);
+        } else {                             // z = M / s
+            const double b = opnd(c, w[3]);
+            for (uint32_t i = 0; i < n; ++i) acc(c, ta, i, c.ld(g + i) / b, nz);
+            double s = c.ld(g) * c.ld(w[4]);
+            for (uint32_t i = 1; i < n; ++i) s = fma(c.ld(g + i), c.ld(w[4] + i), s);
+            acc(c, tb, 0, -(s / b), nz);
+        }
+        break;
+    }
+    case R_NEG: case R_EXP: case R_LOG: case R_SQRT: case R_SIN: case R_COS: case R_ABS: {
+        const bool nz = any_nz(c, g, n);
+        for (uint32_t i = 0; i < n; ++i) {
+            const double gi = c.ld(g + i);
+            double x = 0.0;
+            bool on = nz;
+            switch (op) {
+            case R_NEG: x = -gi; break;
+            case R_EXP: x = gi * c.ld(w[4] + i); break;
+            case R_LOG: {
+                const double a = elem(c, w[2], i);
+                on = on && a > 1e-8;
+                x = gi / a;
+                break;
+            }
+            case R_SQRT: {
+                const double a = elem(c, w[2], i);
+                on = on && a > 1e-8;
+                x = gi / (2.0 * c.ld(w[4] + i));
+                break;
+            }
+            case R_SIN: x = gi * cos(elem(c, w[2], i)); break;
+            case R_COS: x = -(gi * sin(elem(c, w[2], i))); break;
+            default: {
+                const double a = elem(c, w[2], i);
+                x = a > 0.0 ? gi : (a < 0.0 ? -gi : 0.0);
+            }
+            }
+            acc(c, ta, i, x, on);
+        }
+        break;
+    }
+    case R_POW: {
+        const double gv = c.ld(g), a = opnd(c, w[2]), b = opnd(c, w[3]), z = c.ld(w[4]);
+        const bool nz = gv != 0.0;
+        acc(c, ta, 0, ((gv * b) * z) / a, nz);
+        acc(c, tb, 0, (gv * z) * log(a), nz);
+        break;
+    }
+    case R_DOT: {
+        const double gv = c.ld(g);
+        const bool nz = gv != 0.0;
+        for (uint32_t i = 0; i < n; ++i) acc(c, ta, i, gv * elem(c, w[3], i), nz);
+        for (uint32_t i = 0; i < n; ++i) acc(c, tb, i, gv * elem(c, w[2], i), nz);
+        break;
+    }
+    case R_MATMUL: {
+        const uint32_t m = w[7] & 0xFF, k = (w[7] >> 8) & 0xFF, q = (w[7] >> 16) & 0xFF;
+        double G[16], A[16], B[16];
+        load_mat(c, g, m, q, G);
+        bool nz = false;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) nz = nz || G[i] != 0.0;
+        if (ta != kNone) {
+            load_mat(c, w[3], k, q, B);
+#pragma unroll
+            for (uint32_t i = 0; i < 4; ++i)
+#pragma unroll
+                for (uint32_t p = 0; p < 4; ++p) {
+                    if (i < m && p < k) {
+                        double s = G[i * 4] * B[p * 4];
+#pragma unroll
+                        for (uint32_t j = 1; j < 4; ++j)
+                            if (j < q) s = fma(G[i * 4 + j], B[p * 4 + j], s);
+                        acc(c, ta, i * k + p, s, nz);
+                    }
+                }
+        }
+        if (tb != kNone) {
+            load_mat(c, w[2], m, k, A);
+#pragma unroll
+            for (uint32_t p = 0; p < 4; ++p)
+#pragma unroll
+                for (uint32_t j = 0; j < 4; ++j) {
+                    if (p < k && j < q) {
+                        double s = A[p] * G[j];
+#pragma unroll
+                        for (uint32_t i = 1; i < 4; ++i)
+                            if (i < m) s = fma(A[i * 4 + p], G[i * 4 + j], s);
+                        acc(c, tb, p * q + j, s, nz);
+                    }
+                }
+        }
+        break;
+    }
+    case R_OUTER: {
+        const uint32_t m = w[7] & 0xFF, q = (w[7] >> 8) & 0xFF;
+        const bool nz = any_nz(c, g, n);
+        for (uint32_t i = 0; i < m; ++i) {
+            double s = c.ld(g + i * q) * elem(c, w[3], 0);
+            for (uint32_t j = 1; j < q; ++j) s = fma(c.ld(g + i * q + j), elem(c, w[3], j), s);
+            acc(c, ta, i, s, nz);
+        }
+        for (uint32_t j = 0; j < q; ++j) {
+            double s = c.ld(g + j) * elem(c, w[2], 0);
+            for (uint32_t i = 1; i < m; ++i) s = fma(c.ld(g + i * q + j), elem(c, w[2], i), s);
+            acc(c, tb, j, s, nz);
+        }
+        break;
+    }
+    case R_TRANSPOSE: {
+        const uint32_t m = w[7] & 0xFF, q = (w[7] >> 8) & 0xFF;   // input m x q, g is q x m
+        const bool nz = any_nz(c, g, n);
+        for (uint32_t i = 0; i < m; ++i)
+            for (uint32_t j = 0; j < q; ++j) acc(c, ta, i * q + j, c.ld(g + j * m + i), nz);
+        break;
+    }
+    case R_TRACE: {
+        const uint32_t sz = w[7];
+        const double gv = c.ld(g);
+        const bool nz = gv != 0.0;
+        for (uint32_t i = 0; i < sz; ++i)
+            for (uint32_t j = 0; j < sz; ++j) {
+                if (i == j)
+                    acc(c, ta, i * sz + j, gv, nz);
+                else if (ta != kNone && (ta & kInit))
+                    c.st((ta & ~kInit) + i * sz + j, 0.0);
+            }
+        break;
+    }
+    case R_INV: {
+        const uint32_t sz = w[7];
+        double G[16], B[16], M1[16];
+        load_mat(c, g, sz, sz, G);
+        load_mat(c, w[4], sz, sz, B);
+        bool nz = false;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) nz = nz || G[i] != 0.0;
+        // M1 = B^T G, M2 = M1 B^T, A -= M2
+#pragma unroll
+        for (uint32_t i = 0; i < 2; ++i)
+#pragma unroll
+            for (uint32_t j = 0; j < 2; ++j) {
+                double s = B[i] * G[j];
+                if (sz > 1) s = fma(B[4 + i], G[4 + j], s);
+                M1[i * 4 + j] = s;
+            }
+#pragma unroll
+        for (uint32_t i = 0; i < 2; ++i)
+#pragma unroll
+            for (uint32_t j = 0; j < 2; ++j) {
+                if (i < sz && j < sz) {
+                    double s = M1[i * 4] * B[j * 4];
+                    if (sz > 1) s = fma(M1[i * 4 + 1], B[j * 4 + 1], s);
+                    acc(c, ta, i * sz + j, -s, nz);
+                }
+            }
+        break;
+    }
+    case R_DET: case R_LOGDET: {
+        const uint32_t sz = w[7];
+        double A[16], Ai[16];
+        load_mat(c, w[2], sz, sz, A);
+        const double gv = c.ld(g);
+        bool on = gv != 0.0;
+        double scale;
+        if (op == R_DET) {
+            scale = gv * c.ld(w[4]);
+        } else {
+            on = on && det2(A, sz) > 1e-8;
+            scale = gv;
+        }
+        inv2(A, sz, Ai);
+#pragma unroll
+        for (uint32_t i = 0; i < 2; ++i)
+#pragma unroll
+            for (uint32_t j = 0; j < 2; ++j)
+                if (i < sz && j < sz) acc(c, ta, i * sz + j, scale * Ai[j * 4 + i], on);
+        break;
+    }
+    case R_PACK: {
+        const bool nz = any_nz(c, g, n);
+        for (uint32_t i = 0; i < n; ++i) acc(c, C::uni(aux[w[7] + i]), 0, c.ld(g + i), nz);
+        break;
+    }
+    case R_INDEX: {
+        const double gv = c.ld(g);
+        const bool nz = gv != 0.0;
+        if (ta != kNone && (ta & kInit)) {
+            for (uint32_t i = 0; i < n; ++i)
+                if (i != w[7]) c.st((ta & ~kInit) + i, 0.0);
+        }
+        acc(c, ta, w[7], gv, nz);
+        break;
+    }
+    case R_SELECT: {
+        const bool p = opnd(c, w[2]) < opnd(c, w[3]);
+        const bool nz = any_nz(c, g, n);
+        for (uint32_t i = 0; i < n; ++i) acc(c, ta, i, c.ld(g + i), nz && p);
+        for (uint32_t i = 0; i < n; ++i) acc(c, tb, i, c.ld(g + i), nz && !p);
+        break;
+    }
+    default:
+        break;
+    }
+}
+
+
+// Execute a device program from `pc` until END.
+template <class C>
+NDVM_HD void run(const C &c, const uint32_t *pc, const uint32_t *aux) {
+    for (;; pc += kWords) {
+        uint32_t w[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) w[i] = C::uni(pc[i]);
+        const uint32_t op = w[0] & 0xFF;
+        if (op >= R_ADD) {
+            exec_rev(c, aux, w);
+            continue;
+        }
+        if (op >= F_ADD) {
+            exec_fwd(c, aux, w);
+            continue;
+        }
+        const uint32_t n = (w[0] >> 16) & 0xFF;
+        switch (op) {
+        case END:
+            return;
+        case LDPARAM:
+            c.st(w[1], c.param(w[7]));
+            break;
+        case ST_LOSS:
+            c.store_loss(opnd(c, w[2]));
+            break;
+        case CKPT_ST:
+            for (uint32_t i = 0; i < n; ++i) c.ckpt_st(w[7] + i, c.ld(w[2] + i));
+            break;
+        case CKPT_LD:
+            for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, c.ckpt_ld(w[7] + i));
+            break;
+        case ZERO:
+            for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, 0.0);
+            break;
+        case SEED:
+            acc(c, w[5], 0, 1.0, true);
+            break;
+        case ST_GRAD:
+            c.store_grad(w[7], c.ld(w[2]));
+            break;
+        default:
+            return;
+        }
+    }
+}
+
+}  // namespace replay
+}  // namespace ndvm

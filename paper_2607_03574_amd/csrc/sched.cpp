@@ -1,0 +1,740 @@
+// Tape scheduler.
+//
+// The tape is replayed by one GPU thread per lane.  This file decides, once
+// per program and independently of L, where every lane value lives and what
+// the reverse sweep recomputes:
+//
+//  * liveness (ops that cannot reach the loss are dropped) and activity
+//    (values that do not depend on any parameter get no adjoint);
+//  * checkpoint segments: the tape is cut where few values cross the cut;
+//    the forward sweep stores the values a later segment needs at each cut,
+//    the reverse sweep restores them, recomputes inside the segment only what
+//    the segment's adjoint rules read, and applies the rules in reverse
+//    order (Section 3.4 replay; the save policy is this build's own choice);
+//  * values needed in many segments (loop invariants) stay resident instead
+//    of being checkpointed at every cut;
+//  * register allocation of values and adjoints on the instruction timeline
+//    (first fit, contiguous blocks for matrices), separately for the forward
+//    and the reverse phase;
+//  * first-contribution flags, so adjoint registers need no zeroing: the
+//    first write of an adjoint stores, later ones accumulate.
+#include "sched.h"
+
+#include <algorithm>
+#include <unordered_map>
+
+#include "isa.h"
+
+namespace ndvm {
+
+namespace {
+
+enum Kind : uint8_t { K_COMP = 0, K_CONST = 1, K_OBS = 2, K_PARAM = 3 };
+
+struct Info {
+    const Tape &t;
+    uint32_t N, P;
+    std::vector<uint8_t> kind, nel, live, active, has_adj, need_rev;
+    std::vector<uint32_t> last_use;  // last live consumer, or N when the slot is the loss
+
+    explicit Info(const Tape &tape) : t(tape), N(uint32_t(tape.ops.size())), P(tape.n_params) {}
+
+    template <class F>
+    void for_operands(uint32_t k, F f) const {
+        const TapeOp &o = t.ops[k];
+        switch (o.code) {
+        case tp::CONST: case tp::PARAM: case tp::OBS:
+            return;
+        case tp::PACK:
+            for (uint32_t i = 0; i < o.b; ++i) f(t.aux[o.a + i]);
+            return;
+        case tp::SELECT:
+            f(o.a); f(o.b); f(o.c); f(o.d);
+            return;
+        case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: case tp::POW: case tp::DOT:
+        case tp::MATMUL: case tp::OUTER:
+            f(o.a); f(o.b);
+            return;
+        default:
+            f(o.a);
+        }
+    }
+    // operands that receive an adjoint contribution from op k
+    template <class F>
+    void for_targets(uint32_t k, F f) const {
+        const TapeOp &o = t.ops[k];
+        switch (o.code) {
+        case tp::CONST: case tp::PARAM: case tp::OBS:
+            return;
+        case tp::PACK:
+            for (uint32_t i = 0; i < o.b; ++i) f(t.aux[o.a + i]);
+            return;
+        case tp::SELECT:
+            f(o.c); f(o.d);
+            return;
+        case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: case tp::POW: case tp::DOT:
+        case tp::MATMUL: case tp::OUTER:
+            f(o.a); f(o.b);
+            return;
+        default:
+            f(o.a);
+        }
+    }
+    // values the adjoint rule of op k reads (k itself = its output z)
+    template <class F>
+    void for_revreads(uint32_t k, F f) const {
+        const TapeOp &o = t.ops[k];
+        switch (o.code) {
+        case tp::MUL: case tp::DOT: case tp::MATMUL: case tp::OUTER: case tp::SELECT:
+            f(o.a); f(o.b);
+            return;
+        case tp::DIV: f(o.b); f(k); return;
+        case tp::EXP: f(k); return;
+        case tp::LOG: case tp::SIN: case tp::COS: case tp::ABS: case tp::LOGDET: f(o.a); return;
+        case tp::SQRT: f(o.a); f(k); return;
+        case tp::POW: f(o.a); f(o.b); f(k); return;
+        case tp::INV: f(k); return;
+        case tp::DET: f(o.a); f(k); return;
+        default: return;
+        }
+    }
+
+    void analyse() {
+        kind.assign(N, K_COMP);
+        nel.assign(N, 1);
+        for (uint32_t k = 0; k < N; ++k) {
+            uint16_t c = t.ops[k].code;
+            kind[k] = c == tp::CONST ? K_CONST : c == tp::OBS ? K_OBS : c == tp::PARAM ? K_PARAM : K_COMP;
+            nel[k] = uint8_t(t.nel(k));
+        }
+        live.assign(N, 0);
+        live[t.loss] = 1;
+        for (uint32_t k = N; k-- > 0;)
+            if (live[k]) for_operands(k, [&](uint32_t s) { live[s] = 1; });
+        last_use.assign(N, 0);
+        for (uint32_t k = 0; k < N; ++k)
+            if (live[k]) for_operands(k, [&](uint32_t s) { last_use[s] = k; });
+        last_use[t.loss] = N;
+        active.assign(N, 0);
+        for (uint32_t k = 0; k < N; ++k) {
+            if (kind[k] == K_PARAM) { active[k] = 1; continue; }
+            if (kind[k] != K_COMP) continue;
+            bool a = false;
+            for_targets(k, [&](uint32_t s) { a = a || active[s]; });
+            active[k] = a;
+        }
+        has_adj.assign(N, 0);
+        need_rev.assign(N, 0);
+        has_adj[t.loss] = active[t.loss];
+        for (uint32_t k = N; k-- > 0;) {
+            if (!live[k] || kind[k] != K_COMP || !has_adj[k] || !active[k]) continue;
+            need_rev[k] = 1;
+            for_targets(k, [&](uint32_t s) {
+                if (active[s]) has_adj[s] = 1;
+            });
+        }
+    }
+};
+
+// ------------------------------------------------------------------ allocation
+struct Interval {
+    uint32_t start, end, nel;
+    uint32_t reg;
+};
+
+// First-fit placement of intervals (sorted by start) into contiguous blocks.
+// Returns the register high-water mark; a register whose interval ends at t
+// is reusable from t + 1 on.
+uint32_t allocate(std::vector<Interval> &iv) {
+    std::vector<uint32_t> order(iv.size());
+    for (uint32_t i = 0; i < iv.size(); ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](uint32_t x, uint32_t y) { return iv[x].start < iv[y].start; });
+    std::vector<uint32_t> busy;  // first time the register is free again
+    uint32_t hwm = 0;
+    for (uint32_t id : order) {
+        Interval &v = iv[id];
+        uint32_t r = 0, run = 0, base = 0;
+        for (r = 0; r < busy.size(); ++r) {
+            if (busy[r] <= v.start) {
+                if (run == 0) base = r;
+                if (++run == v.nel) break;
+            } else {
+                run = 0;
+            }
+        }
+        if (run < v.nel) {
+            if (run == 0) base = uint32_t(busy.size());
+            busy.resize(base + v.nel, 0);
+        }
+        for (uint32_t i = 0; i < v.nel; ++i) busy[base + i] = v.end + 1;
+        v.reg = base;
+        hwm = std::max(hwm, base + v.nel);
+    }
+    return hwm;
+}
+
+uint32_t opnd_kind(uint32_t kind, uint32_t idx) { return (kind << isa::kKindShift) | idx; }
+
+uint32_t fwd_opcode(uint16_t c) {
+    switch (c) {
+    case tp::ADD: return isa::F_ADD;
+    case tp::SUB: return isa::F_SUB;
+    case tp::MUL: return isa::F_MUL;
+    case tp::DIV: return isa::F_DIV;
+    case tp::NEG: return isa::F_NEG;
+    case tp::EXP: return isa::F_EXP;
+    case tp::LOG: return isa::F_LOG;
+    case tp::SQRT: return isa::F_SQRT;
+    case tp::SIN: return isa::F_SIN;
+    case tp::COS: return isa::F_COS;
+    case tp::ABS: return isa::F_ABS;
+    case tp::POW: return isa::F_POW;
+    case tp::DOT: return isa::F_DOT;
+    case tp::MATMUL: return isa::F_MATMUL;
+    case tp::TRANSPOSE: return isa::F_TRANSPOSE;
+    case tp::TRACE: return isa::F_TRACE;
+    case tp::INV: return isa::F_INV;
+    case tp::DET: return isa::F_DET;
+    case tp::LOGDET: return isa::F_LOGDET;
+    case tp::OUTER: return isa::F_OUTER;
+    case tp::PACK: return isa::F_PACK;
+    case tp::INDEX: return isa::F_INDEX;
+    case tp::SELECT: return isa::F_SELECT;
+    }
+    return isa::END;
+}
+
+// ------------------------------------------------------------------ builder
+// Abstract instruction before register assignment.
+enum RIKind : uint8_t { I_LDP, I_CKST, I_FWD, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_STG };
+struct AI {
+    uint8_t kind;
+    uint32_t k;   // slot / param index
+    uint32_t j;   // segment (reverse phase) or checkpoint row
+};
+
+struct Builder {
+    const Info &I;
+    const Tape &t;
+    uint32_t N, P;
+    // plan
+    std::vector<uint32_t> cuts;       // segment starts, cuts[0] = 0
+    std::vector<uint32_t> seg_of;
+    std::vector<uint8_t> resident;
+    std::vector<std::vector<uint32_t>> livein, recomp, revops;
+    std::vector<uint32_t> res_off;    // resident slot -> offset in resident block
+    uint32_t res_elems = 0;
+
+    explicit Builder(const Info &info) : I(info), t(info.t), N(info.N), P(info.P) {}
+
+    bool comp_live(uint32_t s) const { return I.kind[s] == K_COMP && I.live[s]; }
+
+    void set_cuts(const std::vector<uint32_t> &c) {
+        cuts = c;
+        seg_of.assign(N, 0);
+        uint32_t j = 0;
+        for (uint32_t k = 0; k < N; ++k) {
+            while (j + 1 < cuts.size() && cuts[j + 1] <= k) ++j;
+            seg_of[k] = j;
+        }
+    }
+
+    void plan(bool with_residents) {
+        uint32_t m = uint32_t(cuts.size());
+        if (!with_residents) resident.assign(N, 0);
+        livein.assign(m, {});
+        recomp.assign(m, {});
+        revops.assign(m, {});
+        std::vector<uint32_t> mark(N, UINT32_MAX), inmark(N, UINT32_MAX), stack;
+        for (uint32_t j = 0; j < m; ++j) {
+            uint32_t lo = cuts[j], hi = j + 1 < m ? cuts[j + 1] : N;
+            auto need = [&](uint32_t s) {
+                if (I.kind[s] != K_COMP || resident[s]) return;
+                if (s >= lo) {
+                    if (mark[s] != j) { mark[s] = j; stack.push_back(s); }
+                } else if (inmark[s] != j) {
+                    inmark[s] = j;
+                    livein[j].push_back(s);
+                }
+            };
+            for (uint32_t k = hi; k-- > lo;)
+                if (I.need_rev[k]) {
+                    revops[j].push_back(k);
+                    I.for_revreads(k, need);
+                }
+            while (!stack.empty()) {
+                uint32_t s = stack.back();
+                stack.pop_back();
+                recomp[j].push_back(s);
+                I.for_operands(s, need);
+            }
+            std::sort(recomp[j].begin(), recomp[j].end());
+            std::sort(livein[j].begin(), livein[j].end());
+        }
+    }
+
+    void choose_residents(uint32_t K) {
+        std::vector<uint32_t> cnt(N, 0);
+        for (auto &v : livein)
+            for (uint32_t s : v) cnt[s]++;
+        resident.assign(N, 0);
+        res_off.assign(N, 0);
+        res_elems = 0;
+        for (uint32_t s = 0; s < N; ++s)
+            if (cnt[s] > K) {
+                resident[s] = 1;
+                res_off[s] = res_elems;
+                res_elems += I.nel[s];
+            }
+    }
+
+    std::vector<uint32_t> choose_cuts(uint64_t S) const {
+        std::vector<int64_t> diff(N + 2, 0);
+        for (uint32_t s = 0; s < N; ++s) {
+            if (!comp_live(s) || resident[s]) continue;
+            uint32_t lu = std::min(I.last_use[s], N);
+            if (lu > s) {
+                diff[s + 1] += I.nel[s];
+                diff[lu + 1] -= I.nel[s];
+            }
+        }
+        std::vector<int64_t> w(N + 1, 0);
+        int64_t run = 0;
+        for (uint32_t p = 0; p <= N; ++p) {
+            run += diff[p];
+            w[p] = run;
+        }
+        std::vector<uint32_t> c{0};
+        uint64_t acc = 0;
+        int64_t best = -1;
+        uint32_t start = 0;
+        for (uint32_t k = 0; k < N; ++k) {
+            if (comp_live(k)) acc += I.nel[k];
+            uint32_t p = k + 1;
+            if (p >= N) break;
+            if (acc * 2 >= S && p > start) {
+                if (best < 0 || w[p] <= w[best]) best = p;
+            }
+            if (acc >= S && best > 0) {
+                c.push_back(uint32_t(best));
+                start = uint32_t(best);
+                acc = 0;
+                for (uint32_t q = start; q <= k; ++q)
+                    if (comp_live(q)) acc += I.nel[q];
+                best = -1;
+            }
+        }
+        return c;
+    }
+};
+
+struct Emitter {
+    std::vector<uint32_t> code, aux;
+    void put(uint32_t a, uint32_t b = 0, uint32_t c = 0, uint32_t d = 0, uint32_t e = 0, uint32_t f = 0,
+             uint32_t g = 0, uint32_t h = 0) {
+        uint32_t w[8] = {a, b, c, d, e, f, g, h};
+        code.insert(code.end(), w, w + 8);
+    }
+};
+
+// Build the forward phase (shared by both programs) and, for the gradient
+// program, the reverse phase; returns the schedule with registers assigned.
+Schedule build(const Info &I, Builder &B, bool with_grad) {
+    const Tape &t = I.t;
+    const uint32_t N = I.N, P = I.P;
+    const uint32_t kStatic = 2 * P + B.res_elems;   // param values, param adjoints, residents
+    const uint32_t m = uint32_t(B.cuts.size());
+    Schedule S;
+    S.n_segments = with_grad ? m : 1;
+    S.static_regs = kStatic;
+
+    // ---- forward phase: abstract instructions + value intervals
+    std::vector<AI> fa;
+    std::vector<uint32_t> ckrow_of;   // per (segment, livein index) row, flattened
+    std::vector<uint32_t> ckrow_base(m + 1, 0);
+    if (with_grad) {
+        uint32_t row = 0;
+        for (uint32_t j = 0; j < m; ++j) {
+            ckrow_base[j] = row;
+            for (uint32_t s : B.livein[j]) row += I.nel[s];
+        }
+        ckrow_base[m] = row;
+        S.n_ckpt_rows = row;
+    }
+    for (uint32_t p = 0; p < P; ++p) fa.push_back({I_LDP, p, 0});
+    uint32_t next_cut = 1;
+    for (uint32_t k = 0; k < N; ++k) {
+        if (with_grad) {
+            while (next_cut < m && B.cuts[next_cut] == k) {
+                for (uint32_t i = 0; i < B.livein[next_cut].size(); ++i) fa.push_back({I_CKST, next_cut, i});
+                ++next_cut;
+            }
+        }
+        if (B.comp_live(k)) fa.push_back({I_FWD, k, 0});
+    }
+    fa.push_back({I_STLOSS, t.loss, 0});
+    // intervals for forward values
+    std::vector<Interval> fiv;
+    std::vector<int32_t> fiv_of(N, -1);
+    for (uint32_t ti = 0; ti < fa.size(); ++ti) {
+        const AI &a = fa[ti];
+        auto use = [&](uint32_t s) {
+            if (fiv_of[s] >= 0) fiv[fiv_of[s]].end = std::max(fiv[fiv_of[s]].end, ti);
+        };
+        if (a.kind == I_FWD) {
+            I.for_operands(a.k, use);
+            if (!(with_grad && B.resident[a.k])) {
+                fiv_of[a.k] = int32_t(fiv.size());
+                fiv.push_back({ti, ti, I.nel[a.k], 0});
+            }
+        } else if (a.kind == I_CKST) {
+            use(B.livein[a.k][a.j]);
+        } else if (a.kind == I_STLOSS) {
+            use(a.k);
+        }
+    }
+    uint32_t fhwm = allocate(fiv);
+    S.fwd_regs = fhwm;
+
+    auto res_reg = [&](uint32_t s) { return 2 * P + B.res_off[s]; };
+    auto fwd_operand = [&](uint32_t s) -> uint32_t {
+        switch (I.kind[s]) {
+        case K_CONST: return opnd_kind(isa::kKindConst, t.ops[s].imm);
+        case K_OBS: return opnd_kind(isa::kKindObs, t.ops[s].imm);
+        case K_PARAM: return t.ops[s].imm;
+        default:
+            if (with_grad && B.resident[s]) return res_reg(s);
+            return kStatic + fiv[fiv_of[s]].reg;
+        }
+    };
+
+    Emitter E;
+    auto emit_fwd = [&](uint32_t k, auto operand, uint32_t dst) {
+        const TapeOp &o = t.ops[k];
+        uint32_t op = fwd_opcode(o.code), n = I.nel[k];
+        switch (o.code) {
+        case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: {
+            uint32_t mode = isa::MODE_SAME;
+            if (I.nel[o.a] != I.nel[o.b] || t.ops[o.a].rows != t.ops[o.b].rows)
+                mode = I.nel[o.a] == 1 ? isa::MODE_A_SCALAR : isa::MODE_B_SCALAR;
+            E.put(isa::w0(op, mode, n), dst, operand(o.a), operand(o.b));
+            break;
+        }
+        case tp::POW:
+            E.put(isa::w0(op, 0, 1), dst, operand(o.a), operand(o.b));
+            break;
+        case tp::DOT:
+            E.put(isa::w0(op, 0, I.nel[o.a]), dst, operand(o.a), operand(o.b));
+            break;
+        case tp::MATMUL:
+            E.put(isa::w0(op, 0, n), dst, operand(o.a), operand(o.b), 0, 0, 0,
+                  isa::dims(t.ops[o.a].rows, t.ops[o.a].cols, t.ops[o.b].cols));
+            break;
+        case tp::TRANSPOSE: case tp::OUTER:
+            E.put(isa::w0(op, 0, n), dst, operand(o.a), o.code == tp::OUTER ? operand(o.b) : 0, 0, 0, 0,
+                  isa::dims(t.ops[o.a].rows, o.code == tp::OUTER ? t.ops[o.b].rows : t.ops[o.a].cols, 0));
+            break;
+        case tp::TRACE: case tp::INV: case tp::DET: case tp::LOGDET:
+            E.put(isa::w0(op, 0, n), dst, operand(o.a), 0, 0, 0, 0, t.ops[o.a].rows);
+            break;
+        case tp::PACK: {
+            uint32_t off = uint32_t(E.aux.size());
+            for (uint32_t i = 0; i < o.b; ++i) E.aux.push_back(operand(t.aux[o.a + i]));
+            E.put(isa::w0(op, 0, n), dst, 0, 0, 0, 0, 0, off);
+            break;
+        }
+        case tp::INDEX:
+            E.put(isa::w0(op, 0, 1), dst, operand(o.a), 0, 0, 0, 0, o.imm);
+            break;
+        case tp::SELECT:
+            E.put(isa::w0(op, 0, n), dst, operand(o.a), operand(o.b), operand(o.c), operand(o.d));
+            break;
+        default:  // elementwise unary
+            E.put(isa::w0(op, 0, n), dst, operand(o.a));
+        }
+    };
+
+    for (const AI &a : fa) {
+        switch (a.kind) {
+        case I_LDP: E.put(isa::w0(isa::LDPARAM, 0, 1), a.k, 0, 0, 0, 0, 0, a.k); break;
+        case I_CKST: {
+            uint32_t s = B.livein[a.k][a.j];
+            uint32_t row = ckrow_base[a.k];
+            for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
+            E.put(isa::w0(isa::CKPT_ST, 0, I.nel[s]), 0, fwd_operand(s), 0, 0, 0, 0, row);
+            S.ckpt_elems_stored += I.nel[s];
+            break;
+        }
+        case I_FWD:
+            emit_fwd(a.k, fwd_operand, fwd_operand(a.k) & isa::kIndexMask);
+            S.n_fwd_ops++;
+            break;
+        case I_STLOSS: E.put(isa::w0(isa::ST_LOSS, 0, 1), 0, fwd_operand(a.k)); break;
+        }
+    }
+    if (!with_grad) {
+        E.put(isa::w0(isa::END, 0, 0));
+        S.n_regs = kStatic + fhwm;
+        S.code = std::move(E.code);
+        S.aux = std::move(E.aux);
+        S.n_instr = S.code.size() / isa::kWords;
+        return S;
+    }
+
+    // ---- reverse phase
+    std::vector<AI> ra;
+    ra.push_back({I_ZEROP, 0, 0});
+    ra.push_back({I_SEED, t.loss, 0});
+    for (uint32_t j = m; j-- > 0;) {
+        for (uint32_t i = 0; i < B.livein[j].size(); ++i) ra.push_back({I_CKLD, j, i});
+        for (uint32_t s : B.recomp[j]) ra.push_back({I_FWD, s, j});
+        for (uint32_t k : B.revops[j]) ra.push_back({I_REV, k, j});
+    }
+    for (uint32_t p = 0; p < P; ++p) ra.push_back({I_STG, p, 0});
+
+    // value intervals keyed by (slot, segment); adjoint intervals keyed by slot
+    std::vector<Interval> riv;
+    std::unordered_map<uint64_t, uint32_t> val_of;
+    std::vector<int32_t> adj_of(N, -1);
+    auto key = [](uint32_t s, uint32_t j) { return (uint64_t(s) << 32) | j; };
+    auto vuse = [&](uint32_t s, uint32_t j, uint32_t ti) {
+        if (I.kind[s] != K_COMP || B.resident[s]) return;
+        auto it = val_of.find(key(s, j));
+        riv[it->second].end = std::max(riv[it->second].end, ti);
+    };
+    // first contribution flags: (instruction index, target position) -> init
+    std::vector<uint8_t> touched(N, 0);
+    auto contrib = [&](uint32_t s, uint32_t ti) {
+        if (I.kind[s] != K_COMP || !I.active[s]) return;
+        if (!touched[s]) {
+            touched[s] = 1;
+            adj_of[s] = int32_t(riv.size());
+            riv.push_back({ti, ti, I.nel[s], 0});
+        }
+    };
+    for (uint32_t ti = 0; ti < ra.size(); ++ti) {
+        const AI &a = ra[ti];
+        switch (a.kind) {
+        case I_SEED:
+            contrib(a.k, ti);
+            break;
+        case I_CKLD: {
+            uint32_t s = B.livein[a.k][a.j];
+            val_of[key(s, a.k)] = uint32_t(riv.size());
+            riv.push_back({ti, ti, I.nel[s], 0});
+            break;
+        }
+        case I_FWD:
+            I.for_operands(a.k, [&](uint32_t s) { vuse(s, a.j, ti); });
+            val_of[key(a.k, a.j)] = uint32_t(riv.size());
+            riv.push_back({ti, ti, I.nel[a.k], 0});
+            break;
+        case I_REV: {
+            I.for_revreads(a.k, [&](uint32_t s) { vuse(s, a.j, ti); });
+            I.for_targets(a.k, [&](uint32_t s) { contrib(s, ti); });
+            int32_t g = adj_of[a.k];
+            riv[g].end = std::max(riv[g].end, ti);
+            break;
+        }
+        default:
+            break;
+        }
+    }
+    uint32_t rhwm = allocate(riv);
+    S.rev_regs = rhwm;
+    S.n_regs = kStatic + std::max(fhwm, rhwm);
+
+    auto rev_operand = [&](uint32_t s, uint32_t j) -> uint32_t {
+        switch (I.kind[s]) {
+        case K_CONST: return opnd_kind(isa::kKindConst, t.ops[s].imm);
+        case K_OBS: return opnd_kind(isa::kKindObs, t.ops[s].imm);
+        case K_PARAM: return t.ops[s].imm;
+        default:
+            if (B.resident[s]) return res_reg(s);
+            return kStatic + riv[val_of.at(key(s, j))].reg;
+        }
+    };
+    std::fill(touched.begin(), touched.end(), 0);
+    auto target = [&](uint32_t s) -> uint32_t {
+        if (I.kind[s] == K_PARAM) return P + t.ops[s].imm;
+        if (I.kind[s] != K_COMP || !I.active[s]) return isa::kNone;
+        uint32_t r = kStatic + riv[adj_of[s]].reg;
+        if (!touched[s]) {
+            touched[s] = 1;
+            return r | isa::kInit;
+        }
+        return r;
+    };
+    auto adjreg = [&](uint32_t s) { return kStatic + riv[adj_of[s]].reg; };
+
+    for (const AI &a : ra) {
+        switch (a.kind) {
+        case I_ZEROP:
+            for (uint32_t p0 = 0; p0 < P; p0 += 16)
+                E.put(isa::w0(isa::ZERO, 0, std::min<uint32_t>(16, P - p0)), P + p0);
+            break;
+        case I_SEED:
+            if (I.kind[a.k] == K_PARAM || (I.kind[a.k] == K_COMP && I.active[a.k]))
+                E.put(isa::w0(isa::SEED, 0, 1), 0, 0, 0, 0, target(a.k));
+            break;
+        case I_CKLD: {
+            uint32_t s = B.livein[a.k][a.j];
+            uint32_t row = ckrow_base[a.k];
+            for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
+            E.put(isa::w0(isa::CKPT_LD, 0, I.nel[s]), rev_operand(s, a.k), 0, 0, 0, 0, 0, row);
+            S.ckpt_elems_loaded += I.nel[s];
+            break;
+        }
+        case I_FWD: {
+            auto opnd = [&](uint32_t s) { return rev_operand(s, a.j); };
+            emit_fwd(a.k, opnd, rev_operand(a.k, a.j));
+            S.n_recompute_ops++;
+            break;
+        }
+        case I_REV: {
+            const TapeOp &o = t.ops[a.k];
+            uint32_t k = a.k, j = a.j, n = I.nel[k];
+            uint32_t g = adjreg(k);
+            auto v = [&](uint32_t s) { return rev_operand(s, j); };
+            uint32_t op = fwd_opcode(o.code) - isa::F_ADD + isa::R_ADD;
+            S.n_rev_ops++;
+            switch (o.code) {
+            case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: {
+                uint32_t mode = isa::MODE_SAME;
+                if (I.nel[o.a] != I.nel[o.b] || t.ops[o.a].rows != t.ops[o.b].rows)
+                    mode = I.nel[o.a] == 1 ? isa::MODE_A_SCALAR : isa::MODE_B_SCALAR;
+                uint32_t va = (o.code == tp::MUL) ? v(o.a) : 0;
+                uint32_t vb = (o.code == tp::MUL || o.code == tp::DIV) ? v(o.b) : 0;
+                uint32_t vz = o.code == tp::DIV ? v(k) : 0;
+                uint32_t ta = target(o.a), tb = target(o.b);
+                E.put(isa::w0(op, mode, n), g, va, vb, vz, ta, tb);
+                break;
+            }
+            case tp::POW: {
+                uint32_t va = v(o.a), vb = v(o.b), vz = v(k);
+                uint32_t ta = target(o.a), tb = target(o.b);
+                E.put(isa::w0(op, 0, 1), g, va, vb, vz, ta, tb);
+                break;
+            }
+            case tp::DOT: {
+                uint32_t va = v(o.a), vb = v(o.b);
+                uint32_t ta = target(o.a), tb = target(o.b);
+                E.put(isa::w0(op, 0, I.nel[o.a]), g, va, vb, 0, ta, tb);
+                break;
+            }
+            case tp::MATMUL: {
+                uint32_t va = v(o.a), vb = v(o.b);
+                uint32_t ta = target(o.a), tb = target(o.b);
+                E.put(isa::w0(op, 0, n), g, va, vb, 0, ta, tb,
+                      isa::dims(t.ops[o.a].rows, t.ops[o.a].cols, t.ops[o.b].cols));
+                break;
+            }
+            case tp::OUTER: {
+                uint32_t va = v(o.a), vb = v(o.b);
+                uint32_t ta = target(o.a), tb = target(o.b);
+                E.put(isa::w0(op, 0, n), g, va, vb, 0, ta, tb, isa::dims(t.ops[o.a].rows, t.ops[o.b].rows, 0));
+                break;
+            }
+            case tp::TRANSPOSE:
+                E.put(isa::w0(op, 0, n), g, 0, 0, 0, target(o.a), 0,
+                      isa::dims(t.ops[o.a].rows, t.ops[o.a].cols, 0));
+                break;
+            case tp::TRACE:
+                E.put(isa::w0(op, 0, 1), g, 0, 0, 0, target(o.a), 0, t.ops[o.a].rows);
+                break;
+            case tp::INV:
+                E.put(isa::w0(op, 0, n), g, 0, 0, v(k), target(o.a), 0, t.ops[o.a].rows);
+                break;
+            case tp::DET: {
+                uint32_t va = v(o.a), vz = v(k);
+                E.put(isa::w0(op, 0, 1), g, va, 0, vz, target(o.a), 0, t.ops[o.a].rows);
+                break;
+            }
+            case tp::LOGDET:
+                E.put(isa::w0(op, 0, 1), g, v(o.a), 0, 0, target(o.a), 0, t.ops[o.a].rows);
+                break;
+            case tp::PACK: {
+                uint32_t off = uint32_t(E.aux.size());
+                for (uint32_t i = 0; i < o.b; ++i) E.aux.push_back(target(t.aux[o.a + i]));
+                E.put(isa::w0(op, 0, n), g, 0, 0, 0, 0, 0, off);
+                break;
+            }
+            case tp::INDEX:
+                E.put(isa::w0(op, 0, I.nel[o.a]), g, 0, 0, 0, target(o.a), 0, o.imm);
+                break;
+            case tp::SELECT: {
+                uint32_t va = v(o.a), vb = v(o.b);
+                uint32_t tc = target(o.c), td = target(o.d);
+                E.put(isa::w0(op, 0, n), g, va, vb, 0, tc, td);
+                break;
+            }
+            case tp::EXP: case tp::SQRT: {
+                uint32_t va = o.code == tp::SQRT ? v(o.a) : 0, vz = v(k);
+                E.put(isa::w0(op, 0, n), g, va, 0, vz, target(o.a));
+                break;
+            }
+            default:  // NEG, LOG, SIN, COS, ABS
+                E.put(isa::w0(op, 0, n), g, o.code == tp::NEG ? 0 : v(o.a), 0, 0, target(o.a));
+            }
+            break;
+        }
+        case I_STG:
+            E.put(isa::w0(isa::ST_GRAD, 0, 1), 0, P + a.k, 0, 0, 0, 0, a.k);
+            break;
+        default:
+            break;
+        }
+    }
+    E.put(isa::w0(isa::END, 0, 0));
+    S.code = std::move(E.code);
+    S.aux = std::move(E.aux);
+    S.n_instr = S.code.size() / isa::kWords;
+    return S;
+}
+
+}  // namespace
+
+Schedule schedule_forward(const Tape &t) {
+    Info I(t);
+    I.analyse();
+    Builder B(I);
+    B.set_cuts({0});
+    B.resident.assign(I.N, 0);
+    B.res_off.assign(I.N, 0);
+    return build(I, B, false);
+}
+
+Schedule schedule_grad(const Tape &t, uint32_t reg_budget) {
+    Info I(t);
+    I.analyse();
+    uint64_t total = 0;
+    for (uint32_t k = 0; k < I.N; ++k)
+        if (I.kind[k] == K_COMP && I.live[k]) total += I.nel[k];
+    const uint32_t kResidentAfter = 2;   // checkpointed in more segments -> keep resident
+    Schedule best;
+    bool have = false, best_fits = false;
+    uint64_t S = std::max<uint64_t>(total, 1);
+    for (;;) {
+        Builder B(I);
+        B.resident.assign(I.N, 0);
+        B.res_off.assign(I.N, 0);
+        B.set_cuts(B.choose_cuts(S));
+        B.plan(false);
+        B.choose_residents(kResidentAfter);
+        B.set_cuts(B.choose_cuts(S));
+        B.plan(true);
+        Schedule cand = build(I, B, true);
+        bool fits = cand.n_regs <= reg_budget;
+        if (!have || (fits && !best_fits) || (!fits && !best_fits && cand.n_regs < best.n_regs)) {
+            best = std::move(cand);
+            have = true;
+            best_fits = fits;
+        }
+        if (best_fits || S <= 4) break;
+        S /= 2;
+    }
+    return best;
+}
+
+}  // namespace ndvm

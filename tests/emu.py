@@ -1,0 +1,43 @@
+"""ctypes wrapper of libndvm_emu.so (host emulator of device programs; a
+scheduler-checking tool used by the CPU tests only)."""
+import ctypes
+import os
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+PATH = os.path.join(ROOT, "paper_2607_03574_amd", "libndvm_emu.so")
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        _lib = ctypes.CDLL(PATH)
+        f = _lib.ndvm_emu_run
+        vp, i64 = ctypes.c_void_p, ctypes.c_int64
+        f.restype = ctypes.c_int
+        f.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_uint32, vp, i64, i64,
+                      vp, i64, vp, vp, i64, vp]
+        _lib.ndvm_emu_error.restype = ctypes.c_char_p
+    return _lib
+
+
+STATS = ["n_regs", "n_ckpt_rows", "n_segments", "n_instr", "fwd_ops", "recompute_ops", "rev_ops",
+         "ckpt_stored"]
+
+
+def run(tape: bytes, params, obs, with_grad=True, budget=320):
+    params = np.ascontiguousarray(params, dtype=np.float64)
+    obs = np.ascontiguousarray(obs, dtype=np.float64)
+    L, P = params.shape
+    loss = np.empty(L)
+    grad = np.empty((L, P)) if with_grad else None
+    stats = (ctypes.c_uint64 * 8)()
+    rc = lib().ndvm_emu_run(tape, len(tape), int(with_grad), budget, params.ctypes.data, L, P,
+                            obs.ctypes.data, obs.size, loss.ctypes.data,
+                            grad.ctypes.data if grad is not None else None, P, stats)
+    if rc != 0:
+        raise RuntimeError(f"emulator rc={rc}: {lib().ndvm_emu_error().decode()}")
+    return loss, grad, dict(zip(STATS, list(stats)))

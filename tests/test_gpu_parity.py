@@ -1,0 +1,235 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Small sizes compare every lane; the full benchmark sizes (the launch
+configuration bench.py times) compare sampled lanes the oracle computes one by
+one, including the first, the last and the ragged tail.  Also: ragged lane
+counts, L = 0, poison-lane isolation, bitwise determinism, forward == the
+loss of the gradient call, many programs in one launch == one at a time, and
+every primitive.
+"""
+import numpy as np
+import pytest
+
+from parity import compare
+from workloads import configs
+from workloads.bytecode import Asm
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def nd():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_03574_amd as m
+    return m
+
+
+def run_gpu(nd, bc, params, obs, with_grad=True):
+    tape = nd.tape_upload(nd.tape_build(bc))
+    p = torch.tensor(np.asarray(params, dtype=np.float64), device="cuda")
+    o = torch.tensor(np.asarray(obs, dtype=np.float64), device="cuda")
+    if with_grad:
+        loss, g = nd.grad(tape, p, o)
+        torch.cuda.synchronize()
+        return loss.cpu().numpy(), g.cpu().numpy()
+    loss = nd.forward(tape, p, o)
+    torch.cuda.synchronize()
+    return loss.cpu().numpy(), None
+
+
+def sample_lanes(L, k, seed=0):
+    rng = np.random.default_rng(seed)
+    s = set(rng.choice(L, size=min(k, L), replace=False).tolist())
+    s |= {0, 1, L - 1, L - 2, (L // 64) * 64 - 1}
+    return np.array(sorted(x for x in s if 0 <= x < L))
+
+
+SMALL = [("exp_decay", dict()), ("logistic_euler", dict(L=300)),
+         ("lotka_volterra_rk4", dict(L=130)), ("kalman_cv4", dict(L=200)),
+         ("lotka_volterra_rk4", dict(L=70, T=7)), ("kalman_cv4", dict(L=65, T=3))]
+
+
+@pytest.mark.parametrize("name,kw", SMALL)
+def test_small_all_lanes(nd, oracle_mod, name, kw):
+    w = configs.build(name, **kw)
+    gl, gg = run_gpu(nd, w.bytecode, w.params, w.obs)
+    ol, og, _ = oracle_mod.run(w.bytecode, w.params, w.obs)
+    r = compare(gl, gg, ol, og)
+    print(name, kw, r)
+    fl, _ = run_gpu(nd, w.bytecode, w.params, w.obs, with_grad=False)
+    assert compare(fl, None, ol, None)["max_loss_err"] <= 1e-11
+
+
+@pytest.mark.parametrize("name", ["logistic_euler", "lotka_volterra_rk4", "kalman_cv4", "exp_decay"])
+def test_full_size_sampled(nd, oracle_mod, name):
+    w = configs.build(name)
+    gl, gg = run_gpu(nd, w.bytecode, w.params, w.obs)
+    L = w.params.shape[0]
+    idx = np.arange(L) if L <= 4096 else sample_lanes(L, 384)
+    ol, og, _ = oracle_mod.run(w.bytecode, w.params[idx], w.obs)
+    r = compare(gl[idx], gg[idx], ol, og)
+    print(name, "lanes", len(idx), r)
+
+
+def test_random_programs_full_size_sampled(nd, oracle_mod):
+    w = configs.random_programs()
+    tapes = [nd.tape_upload(nd.tape_build(bc)) for bc in w.programs]
+    p = torch.tensor(w.params, device="cuda")
+    o = torch.tensor(w.obs, device="cuda")
+    loss, grad = nd.grad_many(tapes, p, o)
+    torch.cuda.synchronize()
+    loss, grad = loss.cpu().numpy(), grad.cpu().numpy()
+    rng = np.random.default_rng(1)
+    progs = sorted(set(rng.choice(len(tapes), 40, replace=False).tolist()) | {0, len(tapes) - 1})
+    worst, amb = 0.0, 0
+    for q in progs:
+        P = w.n_params_each[q]
+        lanes = sample_lanes(w.L, 48, seed=q)
+        pp = w.params[q][lanes][:, :P]
+        ol, og, m = oracle_mod.run(w.programs[q], pp, w.obs, margin=True)
+        ole, oge, _ = oracle_mod.run(w.programs[q], pp, w.obs, extended=True)
+        r = compare(loss[q, lanes], grad[q, lanes, :P], ol, og, ole, oge, margin=m)
+        worst = max(worst, r["max_loss_err"], r["max_grad_err"])
+        amb += r["n_ambiguous"]
+    print("random programs: worst", worst, "ambiguous lanes", amb)
+    assert amb <= 5
+
+
+def test_random_programs_small_all_lanes_and_single_equals_many(nd, oracle_mod):
+    w = configs.random_programs(n_prog=16, L=100, n=128, seed=321)
+    tapes = [nd.tape_upload(nd.tape_build(bc)) for bc in w.programs]
+    p = torch.tensor(w.params, device="cuda")
+    o = torch.tensor(w.obs, device="cuda")
+    loss, grad = nd.grad_many(tapes, p, o)
+    torch.cuda.synchronize()
+    for q, bc in enumerate(w.programs):
+        P = w.n_params_each[q]
+        pq = w.params[q][:, :P]
+        ol, og, m = oracle_mod.run(bc, pq, w.obs, margin=True)
+        ole, oge, _ = oracle_mod.run(bc, pq, w.obs, extended=True)
+        compare(loss[q].cpu().numpy(), grad[q, :, :P].cpu().numpy(), ol, og, ole, oge, margin=m)
+        l1, g1 = nd.grad(tapes[q], p[q, :, :P].contiguous(), o)
+        torch.cuda.synchronize()
+        assert torch.equal(l1, loss[q]) and torch.equal(g1, grad[q, :, :P])
+
+
+@pytest.mark.parametrize("L", [1, 2, 63, 65, 129])
+def test_ragged_lane_counts(nd, oracle_mod, L):
+    w = configs.lotka_volterra(L=L, T=9)
+    gl, gg = run_gpu(nd, w.bytecode, w.params, w.obs)
+    ol, og, _ = oracle_mod.run(w.bytecode, w.params, w.obs)
+    compare(gl, gg, ol, og)
+
+
+def test_zero_lanes_is_noop(nd):
+    w = configs.exp_decay(L=1, n=4)
+    tape = nd.tape_upload(nd.tape_build(w.bytecode))
+    p = torch.empty((0, 3), dtype=torch.float64, device="cuda")
+    o = torch.tensor(w.obs, device="cuda")
+    loss, g = nd.grad(tape, p, o)
+    torch.cuda.synchronize()
+    assert loss.numel() == 0 and g.numel() == 0
+
+
+def test_poison_lane_isolation_and_determinism(nd):
+    w = configs.kalman(L=256, T=20)
+    a = run_gpu(nd, w.bytecode, w.params, w.obs)
+    b = run_gpu(nd, w.bytecode, w.params, w.obs)
+    assert a[0].tobytes() == b[0].tobytes() and a[1].tobytes() == b[1].tobytes()
+    p2 = w.params.copy()
+    p2[77, :] = np.nan
+    p2[130, 3] = np.inf
+    c = run_gpu(nd, w.bytecode, p2, w.obs)
+    keep = np.ones(256, bool)
+    keep[[77, 130]] = False
+    assert c[0][keep].tobytes() == a[0][keep].tobytes()
+    assert c[1][keep].tobytes() == a[1][keep].tobytes()
+    assert np.isnan(c[0][77])
+
+
+def test_forward_equals_grad_loss(nd):
+    w = configs.logistic(L=333, T=120)
+    fl, _ = run_gpu(nd, w.bytecode, w.params, w.obs, with_grad=False)
+    gl, _ = run_gpu(nd, w.bytecode, w.params, w.obs)
+    assert fl.tobytes() == gl.tobytes()
+
+
+def _primitive_programs():
+    import test_oracle_pins as T
+    out = []
+    for op, x in T.UNARY:
+        A = Asm(2, 0)
+        A.param(0).raw(op).param(1).mul().halt()
+        out.append((A.bytes(), [[x, -1.7], [x * 0.5, 2.0]]))
+    for op in T.BINARY:
+        A = Asm(3, 0)
+        A.param(0).param(1).raw(op).param(2).mul().halt()
+        out.append((A.bytes(), [[1.3, 0.6, -0.8], [0.7, 1.9, 1.1]]))
+    for m, k, n in [(2, 3, 2), (4, 4, 4), (4, 4, 1), (2, 4, 4), (4, 2, 2), (1, 2, 2), (3, 1, 2)]:
+        A = Asm(m * k + n * k, 0)
+        T._mat(A, m, k, 0)
+        T._mat(A, k, n, m * k)
+        A.matmul()
+        T._weights(A, m, n, 7)
+        A.dot().halt()
+        out.append((A.bytes(), [T._theta(m * k + n * k, s) for s in (1, 2)]))
+    for what in ["transpose", "trace", "outer", "dot", "index", "add", "sub", "hadamard", "ediv",
+                 "smul", "muls", "divs", "eexp", "esin", "elog"]:
+        A = Asm(13, 0)
+        if what == "transpose":
+            T._mat(A, 2, 3, 0); A.transpose(); T._weights(A, 3, 2, 3); A.dot()
+        elif what == "trace":
+            T._mat(A, 3, 3, 0); A.trace(); A.param(9).mul()
+        elif what == "outer":
+            T._mat(A, 3, 1, 0); T._mat(A, 2, 1, 3); A.outer(); T._weights(A, 3, 2, 4); A.dot()
+        elif what == "dot":
+            T._mat(A, 2, 3, 0); T._mat(A, 2, 3, 6); A.dot()
+        elif what == "index":
+            T._mat(A, 2, 3, 0); A.index(1, 2); A.param(0).mul()
+        elif what in ("add", "sub", "hadamard", "ediv"):
+            from workloads import bytecode as B
+            op = {"add": B.ADD, "sub": B.SUB, "hadamard": B.MUL, "ediv": B.DIV}[what]
+            T._mat(A, 2, 3, 0); T._mat(A, 2, 3, 6); A.raw(op); T._weights(A, 2, 3, 5); A.dot()
+        elif what == "smul":
+            A.param(12); T._mat(A, 2, 3, 0); A.mul(); T._weights(A, 2, 3, 6); A.dot()
+        elif what == "muls":
+            T._mat(A, 2, 3, 0); A.param(12); A.mul(); T._weights(A, 2, 3, 6); A.dot()
+        elif what == "divs":
+            T._mat(A, 2, 3, 0); A.param(12); A.div(); T._weights(A, 2, 3, 6); A.dot()
+        else:
+            from workloads import bytecode as B
+            op = {"eexp": B.EXP, "esin": B.SIN, "elog": B.LOG}[what]
+            T._mat(A, 2, 3, 0); A.raw(op); T._weights(A, 2, 3, 8); A.dot()
+        A.halt()
+        lo = 0.2 if what in ("elog", "ediv") else -1.0
+        out.append((A.bytes(), [T._theta(13, s, lo, 1.3) for s in (2, 3)]))
+    for n in (1, 2):
+        for op in ("inv", "det", "logdet"):
+            A = Asm(n * n + 1, 0)
+            T._mat(A, n, n, 0)
+            getattr(A, op)()
+            if op == "inv":
+                T._weights(A, n, n, 11)
+                A.dot()
+            else:
+                A.param(n * n).mul()
+            A.halt()
+            th = [1.4, 0.3, -0.2, 0.9][: n * n] + [1.1] if n == 2 else [1.6, 1.1]
+            out.append((A.bytes(), [th, [v * 0.9 for v in th]]))
+    out.append((T._select_prog(), [[1.0, 1.0, 5.0], [np.nan, 1.0, 5.0], [0.5, 1.0, 0.001], [2.0, 1.0, 5.0]]))
+    out.append((T._log_prog(0x19), [[1e-9], [-1.0], [1e-8], [2e-8]]))
+    out.append((T._log_prog(0x1A), [[1e-9], [-1.0], [1e-8], [2e-8]]))
+    A = Asm(1, 0)
+    A.param(0).abs().halt()
+    out.append((A.bytes(), [[0.0], [-2.0], [3.0]]))
+    return out
+
+
+def test_every_primitive(nd, oracle_mod):
+    for bc, params in _primitive_programs():
+        gl, gg = run_gpu(nd, bc, params, [])
+        ol, og, _ = oracle_mod.run(bc, params, [])
+        compare(gl, gg, ol, og)

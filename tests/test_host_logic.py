@@ -1,0 +1,182 @@
+"""Host-side logic of libndvm, no GPU needed.
+
+* the native trace producer matches the reference encoder byte for byte on
+  every benchmark program (and the SHA-256 goldens written from the reference
+  encoder), including error classes;
+* the C-ABI library loads and exports every symbol include/ndvm.h declares;
+  host-detectable argument errors are reported before any GPU work;
+* the scheduler's device programs, run through the shared instruction
+  handlers by the host emulator (bounds- and initialisation-checked), agree
+  with the oracle at several register budgets (forcing many checkpoint
+  segments) -- a check of the host logic, not a parity claim for the GPU.
+"""
+import ctypes
+import hashlib
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import emu
+from conftest import ROOT, lane_rel_err, rel_err
+from oracle import tape_ref
+from workloads import bytecode as B
+from workloads import configs
+from workloads.bytecode import Asm
+
+nd = pytest.importorskip("paper_2607_03574_amd")
+
+
+def test_library_exports_every_declared_symbol():
+    hdr = open(os.path.join(ROOT, "include", "ndvm.h")).read()
+    declared = sorted(set(re.findall(r"\b(ndvm_\w+)\s*\(", hdr)))
+    assert len(declared) >= 11
+    lib = ctypes.CDLL(nd.LIB_PATH)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(nd.EXPORTS) == declared
+
+
+@pytest.mark.parametrize("name", configs.ORDER[:4])
+def test_tape_bit_exact_and_golden(name):
+    w = configs.build(name, L=1)
+    tape = nd.tape_build(w.bytecode)
+    assert tape == tape_ref.encode(w.bytecode)
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "tape_sha256.json")))
+    assert hashlib.sha256(tape).hexdigest() == gold[name]
+    assert nd.tape_build(w.bytecode) == tape          # deterministic
+
+
+def test_random_program_tapes_golden():
+    w = configs.random_programs(L=1)
+    h = hashlib.sha256()
+    for i, bc in enumerate(w.programs):
+        t = nd.tape_build(bc)
+        if i < 48:
+            assert t == tape_ref.encode(bc)
+        h.update(t)
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "tape_sha256.json")))
+    assert h.hexdigest() == gold["random_programs"]
+
+
+def test_tape_constants_keep_bytecode_bit_patterns():
+    A = Asm(1, 0)
+    A.push(-0.0).push(float("nan")).push(5e-324).add().add().param(0).mul().halt()
+    bc = A.bytes()
+    hdr, consts, aux, ops = tape_ref.decode(nd.tape_build(bc))
+    import struct
+    n_instr = struct.unpack_from("<I", bc, 16)[0]
+    want = [struct.unpack_from("<Q", bc, 24 + 8 * n_instr + 8 * k)[0] for k in range(3)]
+    assert consts == want
+
+
+UNIT_PROGRAMS = [
+    Asm(3, 0).param(2).storel(0).param(0).param(1).iflt().loadl(0).exp().push(1.0).loadl(0).sin()
+    .storel(0).else_().loadl(0).push(1.0).endif().add().loadl(0).add().halt().bytes(),
+    Asm(1, 0).push(1.0).push(2.0).iflt().param(0).exp().else_().param(0).sin().endif().halt().bytes(),
+    Asm(1, 6).push(0.0).loop(2).loop(3).obs(0, 1, 3).add().endloop().endloop().halt().bytes(),
+    Asm(4, 0).param(0).param(1).param(2).param(3).pack(2, 2).dup().matmul().index(1, 0).halt().bytes(),
+]
+
+
+@pytest.mark.parametrize("k", range(len(UNIT_PROGRAMS)))
+def test_unit_tapes_bit_exact(k):
+    bc = UNIT_PROGRAMS[k]
+    assert nd.tape_build(bc) == tape_ref.encode(bc)
+
+
+@pytest.mark.parametrize("bc,code", [
+    (b"NOPE" + bytes(20), nd.E_BYTECODE),
+    (Asm(1, 0).param(0).loop(1).halt().bytes(), nd.E_BYTECODE),
+    (Asm(1, 0).add().halt().bytes(), nd.E_BYTECODE),
+    (Asm(1, 2).obs(2).halt().bytes(), nd.E_BYTECODE),
+    (Asm(1, 0).param(0).param(0).halt().bytes(), nd.E_BYTECODE),
+    (Asm(1, 0).param(0).param(0).iflt().param(0).param(0).else_().param(0).endif().add().halt().bytes(),
+     nd.E_STRUCT_DIVERGE),
+])
+def test_trace_errors_match_reference(bc, code):
+    with pytest.raises(nd.NdvmError) as e:
+        nd.tape_build(bc)
+    assert e.value.status == code
+    with pytest.raises(tape_ref.TapeError) as r:
+        tape_ref.encode(bc)
+    assert r.value.code == code
+
+
+def test_malformed_tape_rejected_before_gpu_work():
+    w = configs.exp_decay(L=1, n=4)
+    tape = bytearray(nd.tape_build(w.bytecode))
+    for bad in (bytes(tape[:-1]), b"XXXX" + bytes(tape[4:])):
+        with pytest.raises(nd.NdvmError) as e:
+            nd.tape_upload(bad, stream=0)
+        assert e.value.status == nd.E_TAPE
+    # forward reference in an op record
+    hdr, consts, aux, ops = tape_ref.decode(bytes(tape))
+    off = 32 + 8 * hdr["n_consts"] + 4 * hdr["n_aux"] + 24 * (len(ops) - 1) + 4
+    t2 = bytearray(tape)
+    t2[off:off + 4] = (len(ops) + 5).to_bytes(4, "little")
+    with pytest.raises(nd.NdvmError) as e:
+        nd.tape_upload(bytes(t2), stream=0)
+    assert e.value.status == nd.E_TAPE
+    with pytest.raises(nd.NdvmError) as e:
+        nd.tape_upload(bytes(tape), policy=99, stream=0)
+    assert e.value.status == nd.E_UNSUPPORTED
+
+
+CASES = [("exp_decay", dict(L=9)), ("logistic_euler", dict(L=9, T=60)),
+         ("lotka_volterra_rk4", dict(L=9, T=25)), ("kalman_cv4", dict(L=9, T=12))]
+
+
+@pytest.mark.parametrize("name,kw", CASES)
+@pytest.mark.parametrize("budget", [320, 48, 12])
+def test_emulated_programs_match_oracle(oracle_mod, name, kw, budget):
+    w = configs.build(name, **kw)
+    tape = nd.tape_build(w.bytecode)
+    lo, go, _ = oracle_mod.run(w.bytecode, w.params, w.obs)
+    le, ge, st = emu.run(tape, w.params, w.obs, True, budget)
+    lf, _, _ = emu.run(tape, w.params, w.obs, False, budget)
+    assert rel_err(le, lo).max() <= 1e-13
+    assert rel_err(lf, lo).max() <= 1e-13
+    assert lane_rel_err(ge, go).max() <= 1e-13
+    if budget < 100 and name != "exp_decay":
+        assert st["n_segments"] > 1
+
+
+def test_emulated_random_programs_match_oracle(oracle_mod):
+    w = configs.random_programs(n_prog=24, L=8, n=8, seed=99)
+    for i, bc in enumerate(w.programs):
+        P = w.n_params_each[i]
+        p = w.params[i][:, :P]
+        lo, go, m = oracle_mod.run(bc, p, w.obs, margin=True)
+        le, ge, _ = emu.run(nd.tape_build(bc), p, w.obs, True, 24)
+        ok = m > 1e-9
+        assert rel_err(le[ok], lo[ok]).max(initial=0) <= 1e-13
+        assert lane_rel_err(ge[ok], go[ok]).max(initial=0) <= 1e-12
+
+
+def test_emulated_edge_programs(oracle_mod):
+    progs = [
+        (Asm(3, 0).param(0).param(1).iflt().push(1000.0).param(2).mul().exp().else_().push(2.0)
+         .param(2).mul().endif().halt().bytes(),
+         [[1.0, 1.0, 5.0], [np.nan, 1.0, 5.0], [0.5, 1.0, 0.001], [2.0, 1.0, 5.0]]),
+        (Asm(1, 0).param(0).log().halt().bytes(), [[1e-9], [-1.0], [1e-8], [2e-8]]),
+        (Asm(1, 0).param(0).sqrt().halt().bytes(), [[1e-9], [4.0]]),
+        (Asm(1, 0).param(0).abs().halt().bytes(), [[0.0], [-2.0], [3.0]]),
+        (Asm(2, 0).param(1).halt().bytes(), [[3.0, 4.0]]),
+        (Asm(2, 0).push(2.5).halt().bytes(), [[3.0, 4.0]]),
+    ]
+    for bc, params in progs:
+        lo, go, _ = oracle_mod.run(bc, params, [])
+        le, ge, _ = emu.run(nd.tape_build(bc), params, [], True, 8)
+        np.testing.assert_array_equal(le, lo)
+        np.testing.assert_array_equal(ge, go)
+
+
+def test_schedule_is_deterministic():
+    w = configs.lotka_volterra(L=3, T=15)
+    tape = nd.tape_build(w.bytecode)
+    a = emu.run(tape, w.params, w.obs, True, 40)
+    b = emu.run(tape, w.params, w.obs, True, 40)
+    assert a[0].tobytes() == b[0].tobytes() and a[1].tobytes() == b[1].tobytes() and a[2] == b[2]
