@@ -24,7 +24,11 @@ SOURCES = ["frontend.cpp", "tape.cpp", "sched.cpp", "abi.cpp", "kernels.hip"]
 EMU_SOURCES = ["frontend.cpp", "tape.cpp", "sched.cpp", "emu.cpp"]
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-ffp-contract=off", "-fno-fast-math", "-Wall",
           "-Wno-unused-function"]
-DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          # the interpreter's dispatch branches are wave-uniform: leave such
+          # regions unstructured instead of routing every handler exit through
+          # a chain of flow blocks
+          "-mllvm", "-structurizecfg-skip-uniform-regions=true"]
 
 
 def _compile(src: str) -> str:

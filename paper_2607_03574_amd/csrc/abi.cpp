@@ -18,7 +18,7 @@
 
 namespace ndvm {
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, hipStream_t stream);
+                         uint32_t r_lds, bool spill, hipStream_t stream);
 }
 
 using namespace ndvm;
@@ -152,8 +152,8 @@ uint64_t ws_rows(const DevProg &dp, uint32_t b) {
 }
 
 ndvm_status check_stream_and_launch(const LaunchArgs &A, const ProgStatic *table, const ProgStatic &single,
-                                    uint32_t n_prog, uint32_t r_lds, hipStream_t stream) {
-    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, stream);
+                                    uint32_t n_prog, uint32_t r_lds, bool spill, hipStream_t stream) {
+    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, spill, stream);
     if (e != hipSuccess) {
         set_error(std::string("kernel launch failed: ") + hipGetErrorString(e));
         return NDVM_E_DEVICE;
@@ -356,7 +356,8 @@ ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
         }
         LaunchArgs A{obs, params, loss, loss, static_cast<double *>(ws), ld_p, 0, L, Lp, 0, 0};
         ProgStatic S{dp.code, dp.aux, dp.consts, 0, 0, r_lds, 0};
-        return check_stream_and_launch(A, nullptr, S, 1, r_lds, static_cast<hipStream_t>(stream));
+        return check_stream_and_launch(A, nullptr, S, 1, r_lds, dp.meta.n_regs > r_lds,
+                                       static_cast<hipStream_t>(stream));
     });
 }
 
@@ -387,7 +388,8 @@ ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L, in
         double *wsd = static_cast<double *>(ws);
         LaunchArgs A{obs, params, loss, grad, wsd, ld_p, ld_g, L, Lp, 0, 0};
         ProgStatic S{dp->code, dp->aux, dp->consts, 0, dp->meta.n_ckpt_rows, r_lds, 0};
-        return check_stream_and_launch(A, nullptr, S, 1, r_lds, static_cast<hipStream_t>(stream));
+        return check_stream_and_launch(A, nullptr, S, 1, r_lds, dp->meta.n_regs > r_lds,
+                                       static_cast<hipStream_t>(stream));
     });
 }
 
@@ -421,11 +423,13 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
         std::vector<uint64_t> key;
         uint64_t row = 0;
         uint32_t r_launch = 0;
+        bool spill = false;
         for (int q = 0; q < n_prog; ++q) {
             DevProg *dp;
             if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), b, s, &dp)) != NDVM_OK) return st;
             uint32_t r_lds = std::min(dp->meta.n_regs, b);
             r_launch = std::max(r_launch, r_lds);
+            spill = spill || dp->meta.n_regs > r_lds;
             table[q] = ProgStatic{dp->code, dp->aux, dp->consts, row, row + dp->meta.n_ckpt_rows, r_lds, 0};
             row += ws_rows(*dp, b);
             key.push_back(tapes[q]->id);
@@ -462,7 +466,7 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
                      prog_stride_g};
         ProgStatic none{};
         return check_stream_and_launch(A, static_cast<const ProgStatic *>(d_table), none, uint32_t(n_prog),
-                                       r_launch, s);
+                                       r_launch, spill, s);
     });
 }
 

@@ -31,12 +31,20 @@ struct HostCtx {
     int *fault;       // first problem seen: 1 register range, 2 unwritten read, 3 pool, 4 ckpt
 
     static uint32_t uni(uint32_t x) { return x; }
+    static void fetch(const uint32_t *pc, uint32_t (&w)[8]) {
+        for (int i = 0; i < 8; ++i) w[i] = pc[i];
+    }
+    static uint32_t aux_word(const uint32_t *aux, uint32_t i) { return aux[i]; }
     void flag(int code) const {
         if (*fault == 0) *fault = code;
     }
     double ld(uint32_t r) const {
         if (r >= n_regs) { flag(1); return NAN; }
         if (!written[r]) flag(2);
+        return regs[r];
+    }
+    double ld_raw(uint32_t r) const {
+        if (r >= n_regs) { flag(1); return NAN; }
         return regs[r];
     }
     void st(uint32_t r, double v) const {

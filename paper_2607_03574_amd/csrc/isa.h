@@ -13,9 +13,10 @@
 //   w6 : adjoint target of b (reverse)
 //   w7 : immediate (dims, element index, aux offset, checkpoint row, param)
 //
-// Operand words: bits 31-30 kind (0 register, 1 constant pool, 2 obs),
-// bits 29-0 index.  Adjoint target words: register | kInit (first
-// contribution: store instead of add), or kNone.
+// Operand words are register indices: constants are loaded into static
+// registers once (LDCONST) and observations by LDOBS where they are used.
+// Adjoint target words: register | kInit (first contribution: store instead
+// of add), or kNone (generic handlers; scalar handlers get a sink register).
 #pragma once
 #include <cstdint>
 
@@ -31,6 +32,8 @@ enum : uint32_t {
     ZERO = 5,      // w1 dst reg, nel
     SEED = 6,      // w5 target
     ST_GRAD = 7,   // w2 src reg, w7 param index
+    LDOBS = 8,     // w1 dst, w7 observation index
+    LDCONST = 9,   // w1 dst, w7 first pool entry, nel entries
 
     F_ADD = 16, F_SUB, F_MUL, F_DIV, F_NEG, F_EXP, F_LOG, F_SQRT, F_SIN, F_COS, F_ABS, F_POW,
     F_DOT, F_MATMUL, F_TRANSPOSE, F_TRACE, F_INV, F_DET, F_LOGDET, F_OUTER, F_PACK, F_INDEX,
@@ -39,14 +42,18 @@ enum : uint32_t {
     R_ADD = 48, R_SUB, R_MUL, R_DIV, R_NEG, R_EXP, R_LOG, R_SQRT, R_SIN, R_COS, R_ABS, R_POW,
     R_DOT, R_MATMUL, R_TRANSPOSE, R_TRACE, R_INV, R_DET, R_LOGDET, R_OUTER, R_PACK, R_INDEX,
     R_SELECT,
+
+    // scalar (1x1) fast paths of the elementwise ops and the select: no
+    // element loops, no broadcast modes
+    S_ADD = 96, S_SUB, S_MUL, S_DIV, S_NEG, S_EXP, S_LOG, S_SQRT, S_SIN, S_COS, S_ABS, S_SELECT,
+    SR_ADD = 112, SR_SUB, SR_MUL, SR_DIV, SR_NEG, SR_EXP, SR_LOG, SR_SQRT, SR_SIN, SR_COS, SR_ABS,
+    SR_SELECT,
     OP_COUNT
 };
 
 // binary elementwise broadcast modes (w0 bits 8-15)
 enum : uint32_t { MODE_SAME = 0, MODE_A_SCALAR = 1, MODE_B_SCALAR = 2 };
 
-constexpr uint32_t kKindShift = 30;
-constexpr uint32_t kKindReg = 0, kKindConst = 1, kKindObs = 2;
 constexpr uint32_t kIndexMask = (1u << 30) - 1;
 constexpr uint32_t kInit = 0x80000000u;
 constexpr uint32_t kNone = 0xFFFFFFFFu;

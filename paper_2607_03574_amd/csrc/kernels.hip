@@ -15,6 +15,8 @@
 //
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "isa.h"
 #include "replay.h"
 
@@ -23,25 +25,42 @@ namespace {
 
 // Lane context on the GPU: register r of thread t at lds[r*64 + t] when
 // r < r_lds, else in the workspace spill rows; all addressing lane-contiguous.
+// Every pointer carries its address space so that LDS, global and uniform
+// (scalar) accesses compile to ds_*, global_* and s_load instructions.
+#define AS_LDS __attribute__((address_space(3)))
+#define AS_GLOBAL __attribute__((address_space(1)))
+#define AS_CONST __attribute__((address_space(4)))
+
+template <bool kSpill>
 struct DevCtx {
-    double *lds;
-    double *spill;
-    const double *consts;
-    const double *obs;
-    const double *params;
-    double *loss, *grad, *ckpt;
+    AS_LDS double *lds;
+    AS_GLOBAL double *spill;
+    const AS_CONST double *consts;
+    const AS_CONST double *obs;
+    const AS_GLOBAL double *params;
+    AS_GLOBAL double *loss, *grad, *ckpt;
     int64_t lane, lc, Lpad, ld_p, ld_g;
     uint32_t r_lds;
     int t;
     bool active;
 
     __device__ __forceinline__ static uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+    // program words are wave-uniform and read-only: scalar loads
+    __device__ __forceinline__ static void fetch(const uint32_t *pc, uint32_t (&w)[8]) {
+        const AS_CONST uint32_t *p = (const AS_CONST uint32_t *)(pc);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) w[i] = p[i];
+    }
+    __device__ __forceinline__ static uint32_t aux_word(const uint32_t *aux, uint32_t i) {
+        return ((const AS_CONST uint32_t *)(aux))[i];
+    }
     __device__ __forceinline__ double ld(uint32_t r) const {
-        if (r < r_lds) return lds[r * 64u + t];
+        if (!kSpill || r < r_lds) return lds[r * 64u + t];
         return spill[int64_t(r - r_lds) * Lpad + lane];
     }
+    __device__ __forceinline__ double ld_raw(uint32_t r) const { return ld(r); }
     __device__ __forceinline__ void st(uint32_t r, double v) const {
-        if (r < r_lds)
+        if (!kSpill || r < r_lds)
             lds[r * 64u + t] = v;
         else
             spill[int64_t(r - r_lds) * Lpad + lane] = v;
@@ -59,26 +78,36 @@ struct DevCtx {
     __device__ __forceinline__ double ckpt_ld(uint32_t row) const { return ckpt[int64_t(row) * Lpad + lane]; }
 };
 
+template <class T>
+__device__ __forceinline__ AS_GLOBAL T *gptr(T *p) {
+    return (AS_GLOBAL T *)(p);
+}
+template <class T>
+__device__ __forceinline__ const AS_CONST T *cptr(const T *p) {
+    return (const AS_CONST T *)(p);
+}
+
 }  // namespace
 
-extern "C" __global__ void __launch_bounds__(64)
-ndvm_replay(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
+template <bool kSpill>
+__device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStatic *__restrict__ table,
+                                            const ProgStatic &single) {
     extern __shared__ double lds_regs[];
     const uint32_t q = blockIdx.y;
     const ProgStatic D = table ? table[q] : single;
-    DevCtx c;
+    DevCtx<kSpill> c;
     c.t = threadIdx.x;
     c.lane = int64_t(blockIdx.x) * 64 + c.t;
     c.active = c.lane < A.L;
     c.lc = c.active ? c.lane : A.L - 1;
-    c.lds = lds_regs;
-    c.spill = A.ws + int64_t(D.spill_row0) * A.Lpad;
-    c.ckpt = A.ws + int64_t(D.ckpt_row0) * A.Lpad;
-    c.consts = D.consts;
-    c.obs = A.obs;
-    c.params = A.params + int64_t(q) * A.prog_stride_p;
-    c.loss = A.loss + int64_t(q) * A.L;
-    c.grad = A.grad + int64_t(q) * A.prog_stride_g;
+    c.lds = (AS_LDS double *)lds_regs;
+    c.spill = gptr(A.ws + int64_t(D.spill_row0) * A.Lpad);
+    c.ckpt = gptr(A.ws + int64_t(D.ckpt_row0) * A.Lpad);
+    c.consts = cptr(D.consts);
+    c.obs = cptr(A.obs);
+    c.params = gptr(A.params + int64_t(q) * A.prog_stride_p);
+    c.loss = gptr(A.loss + int64_t(q) * A.L);
+    c.grad = gptr(A.grad + int64_t(q) * A.prog_stride_g);
     c.Lpad = A.Lpad;
     c.ld_p = A.ld_p;
     c.ld_g = A.ld_g;
@@ -86,20 +115,38 @@ ndvm_replay(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic singl
     replay::run(c, D.prog, D.aux);
 }
 
+// All lane registers in LDS (the usual case: the scheduler fits the register
+// file to the launch's LDS budget).
+extern "C" __global__ void __launch_bounds__(64)
+ndvm_replay(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
+    replay_body<false>(A, table, single);
+}
+
+// Registers beyond r_lds spill to lane-contiguous workspace rows.
+extern "C" __global__ void __launch_bounds__(64)
+ndvm_replay_spill(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
+    replay_body<true>(A, table, single);
+}
+
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, hipStream_t stream) {
-    static bool attr_set = false;
-    if (!attr_set) {
-        int dev = 0, max_smem = 0;
-        (void)hipGetDevice(&dev);
+                         uint32_t r_lds, bool spill, hipStream_t stream) {
+    static std::once_flag once[64];
+    int dev = 0;
+    (void)hipGetDevice(&dev);
+    std::call_once(once[dev & 63], [dev]() {
+        int max_smem = 0;
         (void)hipDeviceGetAttribute(&max_smem, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
         (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&ndvm_replay),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
-        attr_set = true;
-    }
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&ndvm_replay_spill),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
+    });
     dim3 grid(uint32_t(A.Lpad / 64), n_prog), block(64);
     size_t smem = size_t(r_lds) * 64 * sizeof(double);
-    hipLaunchKernelGGL(ndvm_replay, grid, block, smem, stream, A, d_table, single);
+    if (spill)
+        hipLaunchKernelGGL(ndvm_replay_spill, grid, block, smem, stream, A, d_table, single);
+    else
+        hipLaunchKernelGGL(ndvm_replay, grid, block, smem, stream, A, d_table, single);
     return hipGetLastError();
 }
 

@@ -3,8 +3,10 @@
 //
 // A context type C supplies the lane's register file and memory:
 //   double ld(uint32_t r) const;  void st(uint32_t r, double v) const;
-//   double konst(uint32_t i) const;  double obsv(uint32_t i) const;
+//   double ld_raw(uint32_t r) const;   (a read whose value may be discarded)
+//   double konst(uint32_t i) const;  double obsv(uint32_t i) const;  (uniform loads)
 //   static uint32_t uni(uint32_t x);          (wave-uniform value)
+//   static void fetch(const uint32_t *pc, uint32_t (&w)[8]);  (one instruction)
 //   double param(uint32_t p) const;  void store_loss(double) const;
 //   void store_grad(uint32_t p, double) const;
 //   void ckpt_st(uint32_t row, double) const;  double ckpt_ld(uint32_t row) const;
@@ -30,18 +32,15 @@ namespace replay {
 
 using namespace isa;
 
-// scalar operand word: register, constant-pool entry or observation
+// operand words are register indices
 template <class C>
 NDVM_HD double opnd(const C &c, uint32_t w) {
-    uint32_t kind = w >> kKindShift, idx = w & kIndexMask;
-    if (kind == kKindReg) return c.ld(idx);
-    if (kind == kKindConst) return c.konst(idx);
-    return c.obsv(idx);
+    return c.ld(w);
 }
-// element i of an operand (only registers hold more than one element)
+// element i of a register operand
 template <class C>
 NDVM_HD double elem(const C &c, uint32_t w, uint32_t i) {
-    return (w >> kKindShift) ? opnd(c, w) : c.ld(w + i);
+    return c.ld(w + i);
 }
 // adjoint update of element i of target word tw with contribution x when
 // `on` holds for this lane; the first contribution stores (0 + x)
@@ -192,7 +191,7 @@ NDVM_HD void exec_fwd(const C &c, const uint32_t *aux, const uint32_t *w) {
         break;
     }
     case F_PACK:
-        for (uint32_t i = 0; i < n; ++i) c.st(dst + i, opnd(c, C::uni(aux[w[7] + i])));
+        for (uint32_t i = 0; i < n; ++i) c.st(dst + i, opnd(c, C::aux_word(aux, w[7] + i)));
         break;
     case F_INDEX:
         c.st(dst, c.ld(w[2] + w[7]));
@@ -431,7 +430,7 @@ NDVM_HD void exec_rev(const C &c, const uint32_t *aux, const uint32_t *w) {
     }
     case R_PACK: {
         const bool nz = any_nz(c, g, n);
-        for (uint32_t i = 0; i < n; ++i) acc(c, C::uni(aux[w[7] + i]), 0, c.ld(g + i), nz);
+        for (uint32_t i = 0; i < n; ++i) acc(c, C::aux_word(aux, w[7] + i), 0, c.ld(g + i), nz);
         break;
     }
     case R_INDEX: {
@@ -457,14 +456,148 @@ NDVM_HD void exec_rev(const C &c, const uint32_t *aux, const uint32_t *w) {
 }
 
 
+// adjoint update of a scalar target (see acc); never kNone here (the
+// scheduler points unused targets at a sink register), so no branch
+template <class C>
+NDVM_HD void acc1(const C &c, uint32_t tw, double x, bool on) {
+    const uint32_t r = tw & ~kInit;
+    const double old = c.ld_raw(r);   // may be unset when the first contribution stores
+    const double base = (tw & kInit) ? 0.0 : old;
+    c.st(r, on ? base + x : base);
+}
+
+// Scalar handlers without any data-dependent control flow inside: kept in a
+// switch of their own so the compiler can leave that region's uniform
+// branches unstructured (a direct jump back to the dispatch).
+constexpr uint32_t kHotMask =
+    (1u << (S_ADD - S_ADD)) | (1u << (S_SUB - S_ADD)) | (1u << (S_MUL - S_ADD)) | (1u << (S_DIV - S_ADD)) |
+    (1u << (S_NEG - S_ADD)) | (1u << (S_ABS - S_ADD)) | (1u << (S_SELECT - S_ADD)) |
+    (1u << (SR_ADD - S_ADD)) | (1u << (SR_SUB - S_ADD)) | (1u << (SR_MUL - S_ADD)) |
+    (1u << (SR_DIV - S_ADD)) | (1u << (SR_NEG - S_ADD)) | (1u << (SR_EXP - S_ADD)) |
+    (1u << (SR_LOG - S_ADD)) | (1u << (SR_SQRT - S_ADD)) | (1u << (SR_ABS - S_ADD)) |
+    (1u << (SR_SELECT - S_ADD));
+
+template <class C>
+NDVM_HD void exec_hot(const C &c, const uint32_t *w, uint32_t op) {
+    switch (op) {
+    case S_ADD: c.st(w[1], c.ld(w[2]) + c.ld(w[3])); return;
+    case S_SUB: c.st(w[1], c.ld(w[2]) - c.ld(w[3])); return;
+    case S_MUL: c.st(w[1], c.ld(w[2]) * c.ld(w[3])); return;
+    case S_DIV: c.st(w[1], c.ld(w[2]) / c.ld(w[3])); return;
+    case S_NEG: c.st(w[1], -c.ld(w[2])); return;
+    case S_ABS: c.st(w[1], fabs(c.ld(w[2]))); return;
+    case S_SELECT: {
+        const bool p = c.ld(w[2]) < c.ld(w[3]);
+        const double x = c.ld(w[4]), y = c.ld(w[5]);
+        c.st(w[1], p ? x : y);
+        return;
+    }
+    case SR_ADD: {
+        const double g = c.ld(w[1]);
+        const bool nz = g != 0.0;
+        acc1(c, w[5], g, nz);
+        acc1(c, w[6], g, nz);
+        return;
+    }
+    case SR_SUB: {
+        const double g = c.ld(w[1]);
+        const bool nz = g != 0.0;
+        acc1(c, w[5], g, nz);
+        acc1(c, w[6], -g, nz);
+        return;
+    }
+    case SR_MUL: {
+        const double g = c.ld(w[1]), a = c.ld(w[2]), b = c.ld(w[3]);
+        const bool nz = g != 0.0;
+        acc1(c, w[5], g * b, nz);
+        acc1(c, w[6], g * a, nz);
+        return;
+    }
+    case SR_DIV: {
+        const double g = c.ld(w[1]), b = c.ld(w[3]), z = c.ld(w[4]);
+        const bool nz = g != 0.0;
+        acc1(c, w[5], g / b, nz);
+        acc1(c, w[6], -((g * z) / b), nz);
+        return;
+    }
+    case SR_NEG: {
+        const double g = c.ld(w[1]);
+        acc1(c, w[5], -g, g != 0.0);
+        return;
+    }
+    case SR_EXP: {
+        const double g = c.ld(w[1]);
+        acc1(c, w[5], g * c.ld(w[4]), g != 0.0);
+        return;
+    }
+    case SR_LOG: {
+        const double g = c.ld(w[1]), a = c.ld(w[2]);
+        acc1(c, w[5], g / a, g != 0.0 && a > 1e-8);
+        return;
+    }
+    case SR_SQRT: {
+        const double g = c.ld(w[1]), a = c.ld(w[2]);
+        acc1(c, w[5], g / (2.0 * c.ld(w[4])), g != 0.0 && a > 1e-8);
+        return;
+    }
+    case SR_ABS: {
+        const double g = c.ld(w[1]), a = c.ld(w[2]);
+        acc1(c, w[5], a > 0.0 ? g : (a < 0.0 ? -g : 0.0), g != 0.0);
+        return;
+    }
+    case SR_SELECT: {
+        const double g = c.ld(w[1]);
+        const bool nz = g != 0.0;
+        const bool p = c.ld(w[2]) < c.ld(w[3]);
+        acc1(c, w[5], g, nz && p);
+        acc1(c, w[6], g, nz && !p);
+        return;
+    }
+    default:
+        return;
+    }
+}
+
+// remaining scalar fast paths (transcendentals, whose library code branches
+// on the argument)
+template <class C>
+NDVM_HD void exec_scalar(const C &c, const uint32_t *w) {
+    const uint32_t op = w[0] & 0xFF;
+    switch (op) {
+    case S_EXP: c.st(w[1], exp(c.ld(w[2]))); return;
+    case S_LOG: c.st(w[1], log(clampv(c.ld(w[2])))); return;
+    case S_SQRT: c.st(w[1], sqrt(clampv(c.ld(w[2])))); return;
+    case S_SIN: c.st(w[1], sin(c.ld(w[2]))); return;
+    case S_COS: c.st(w[1], cos(c.ld(w[2]))); return;
+    case SR_SIN: {
+        const double g = c.ld(w[1]);
+        acc1(c, w[5], g * cos(c.ld(w[2])), g != 0.0);
+        return;
+    }
+    case SR_COS: {
+        const double g = c.ld(w[1]);
+        acc1(c, w[5], -(g * sin(c.ld(w[2]))), g != 0.0);
+        return;
+    }
+    default:
+        return;
+    }
+}
+
 // Execute a device program from `pc` until END.
 template <class C>
 NDVM_HD void run(const C &c, const uint32_t *pc, const uint32_t *aux) {
     for (;; pc += kWords) {
         uint32_t w[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) w[i] = C::uni(pc[i]);
+        C::fetch(pc, w);
         const uint32_t op = w[0] & 0xFF;
+        if (op >= S_ADD) {
+            if ((kHotMask >> (op - S_ADD)) & 1u)
+                exec_hot(c, w, op);
+            else
+                exec_scalar(c, w);
+            continue;
+        }
         if (op >= R_ADD) {
             exec_rev(c, aux, w);
             continue;
@@ -497,6 +630,12 @@ NDVM_HD void run(const C &c, const uint32_t *pc, const uint32_t *aux) {
             break;
         case ST_GRAD:
             c.store_grad(w[7], c.ld(w[2]));
+            break;
+        case LDOBS:
+            c.st(w[1], c.obsv(w[7]));
+            break;
+        case LDCONST:
+            for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, c.konst(w[7] + i));
             break;
         default:
             return;

@@ -174,7 +174,16 @@ uint32_t allocate(std::vector<Interval> &iv) {
     return hwm;
 }
 
-uint32_t opnd_kind(uint32_t kind, uint32_t idx) { return (kind << isa::kKindShift) | idx; }
+// elementwise ops and the select have scalar fast-path opcodes
+bool scalar_fast(uint16_t c) {
+    switch (c) {
+    case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: case tp::NEG: case tp::EXP: case tp::LOG:
+    case tp::SQRT: case tp::SIN: case tp::COS: case tp::ABS: case tp::SELECT:
+        return true;
+    }
+    return false;
+}
+bool binary_code(uint16_t c) { return c == tp::ADD || c == tp::SUB || c == tp::MUL || c == tp::DIV; }
 
 uint32_t fwd_opcode(uint16_t c) {
     switch (c) {
@@ -207,7 +216,7 @@ uint32_t fwd_opcode(uint16_t c) {
 
 // ------------------------------------------------------------------ builder
 // Abstract instruction before register assignment.
-enum RIKind : uint8_t { I_LDP, I_CKST, I_FWD, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_STG };
+enum RIKind : uint8_t { I_LDP, I_LDC, I_CKST, I_FWD, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_STG };
 struct AI {
     uint8_t kind;
     uint32_t k;   // slot / param index
@@ -250,6 +259,10 @@ struct Builder {
         for (uint32_t j = 0; j < m; ++j) {
             uint32_t lo = cuts[j], hi = j + 1 < m ? cuts[j + 1] : N;
             auto need = [&](uint32_t s) {
+                if (I.kind[s] == K_OBS) {   // observations are reloaded, never checkpointed
+                    if (mark[s] != j) { mark[s] = j; stack.push_back(s); }
+                    return;
+                }
                 if (I.kind[s] != K_COMP || resident[s]) return;
                 if (s >= lo) {
                     if (mark[s] != j) { mark[s] = j; stack.push_back(s); }
@@ -343,7 +356,11 @@ struct Emitter {
 Schedule build(const Info &I, Builder &B, bool with_grad) {
     const Tape &t = I.t;
     const uint32_t N = I.N, P = I.P;
-    const uint32_t kStatic = 2 * P + B.res_elems;   // param values, param adjoints, residents
+    // static registers: param values, param adjoints, a sink for adjoint
+    // contributions nobody needs, the constant pool, residents
+    const uint32_t nc = uint32_t(t.consts.size());
+    const uint32_t kSink = 2 * P, kConst0 = 2 * P + 1;
+    const uint32_t kStatic = 2 * P + 1 + nc + B.res_elems;
     const uint32_t m = uint32_t(B.cuts.size());
     Schedule S;
     S.n_segments = with_grad ? m : 1;
@@ -363,6 +380,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         S.n_ckpt_rows = row;
     }
     for (uint32_t p = 0; p < P; ++p) fa.push_back({I_LDP, p, 0});
+    for (uint32_t i = 0; i < nc; i += 255) fa.push_back({I_LDC, i, std::min<uint32_t>(255, nc - i)});
     uint32_t next_cut = 1;
     for (uint32_t k = 0; k < N; ++k) {
         if (with_grad) {
@@ -371,7 +389,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
                 ++next_cut;
             }
         }
-        if (B.comp_live(k)) fa.push_back({I_FWD, k, 0});
+        if (B.comp_live(k) || (I.kind[k] == K_OBS && I.live[k])) fa.push_back({I_FWD, k, 0});
     }
     fa.push_back({I_STLOSS, t.loss, 0});
     // intervals for forward values
@@ -397,11 +415,10 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     uint32_t fhwm = allocate(fiv);
     S.fwd_regs = fhwm;
 
-    auto res_reg = [&](uint32_t s) { return 2 * P + B.res_off[s]; };
+    auto res_reg = [&](uint32_t s) { return kConst0 + nc + B.res_off[s]; };
     auto fwd_operand = [&](uint32_t s) -> uint32_t {
         switch (I.kind[s]) {
-        case K_CONST: return opnd_kind(isa::kKindConst, t.ops[s].imm);
-        case K_OBS: return opnd_kind(isa::kKindObs, t.ops[s].imm);
+        case K_CONST: return kConst0 + t.ops[s].imm;
         case K_PARAM: return t.ops[s].imm;
         default:
             if (with_grad && B.resident[s]) return res_reg(s);
@@ -413,6 +430,18 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     auto emit_fwd = [&](uint32_t k, auto operand, uint32_t dst) {
         const TapeOp &o = t.ops[k];
         uint32_t op = fwd_opcode(o.code), n = I.nel[k];
+        if (o.code == tp::OBS) {
+            E.put(isa::w0(isa::LDOBS, 0, 1), dst, 0, 0, 0, 0, 0, o.imm);
+            return;
+        }
+        if (n == 1 && scalar_fast(o.code) && (o.code == tp::SELECT || I.nel[o.a] == 1)) {
+            uint32_t sop = op == isa::F_SELECT ? uint32_t(isa::S_SELECT) : op - isa::F_ADD + isa::S_ADD;
+            if (o.code == tp::SELECT)
+                E.put(isa::w0(sop, 0, 1), dst, operand(o.a), operand(o.b), operand(o.c), operand(o.d));
+            else
+                E.put(isa::w0(sop, 0, 1), dst, operand(o.a), binary_code(o.code) ? operand(o.b) : 0);
+            return;
+        }
         switch (o.code) {
         case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: {
             uint32_t mode = isa::MODE_SAME;
@@ -458,6 +487,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     for (const AI &a : fa) {
         switch (a.kind) {
         case I_LDP: E.put(isa::w0(isa::LDPARAM, 0, 1), a.k, 0, 0, 0, 0, 0, a.k); break;
+        case I_LDC: E.put(isa::w0(isa::LDCONST, 0, a.j), kConst0 + a.k, 0, 0, 0, 0, 0, a.k); break;
         case I_CKST: {
             uint32_t s = B.livein[a.k][a.j];
             uint32_t row = ckrow_base[a.k];
@@ -499,7 +529,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     std::vector<int32_t> adj_of(N, -1);
     auto key = [](uint32_t s, uint32_t j) { return (uint64_t(s) << 32) | j; };
     auto vuse = [&](uint32_t s, uint32_t j, uint32_t ti) {
-        if (I.kind[s] != K_COMP || B.resident[s]) return;
+        if ((I.kind[s] != K_COMP && I.kind[s] != K_OBS) || B.resident[s]) return;
         auto it = val_of.find(key(s, j));
         riv[it->second].end = std::max(riv[it->second].end, ti);
     };
@@ -547,8 +577,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
 
     auto rev_operand = [&](uint32_t s, uint32_t j) -> uint32_t {
         switch (I.kind[s]) {
-        case K_CONST: return opnd_kind(isa::kKindConst, t.ops[s].imm);
-        case K_OBS: return opnd_kind(isa::kKindObs, t.ops[s].imm);
+        case K_CONST: return kConst0 + t.ops[s].imm;
         case K_PARAM: return t.ops[s].imm;
         default:
             if (B.resident[s]) return res_reg(s);
@@ -556,7 +585,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         }
     };
     std::fill(touched.begin(), touched.end(), 0);
-    auto target = [&](uint32_t s) -> uint32_t {
+    auto target_word = [&](uint32_t s) -> uint32_t {
         if (I.kind[s] == K_PARAM) return P + t.ops[s].imm;
         if (I.kind[s] != K_COMP || !I.active[s]) return isa::kNone;
         uint32_t r = kStatic + riv[adj_of[s]].reg;
@@ -566,6 +595,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         }
         return r;
     };
+    auto target = target_word;
     auto adjreg = [&](uint32_t s) { return kStatic + riv[adj_of[s]].reg; };
 
     for (const AI &a : ra) {
@@ -599,6 +629,27 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             auto v = [&](uint32_t s) { return rev_operand(s, j); };
             uint32_t op = fwd_opcode(o.code) - isa::F_ADD + isa::R_ADD;
             S.n_rev_ops++;
+            if (n == 1 && scalar_fast(o.code) && (o.code == tp::SELECT || I.nel[o.a] == 1)) {
+                uint32_t sop = o.code == tp::SELECT ? uint32_t(isa::SR_SELECT)
+                                                    : fwd_opcode(o.code) - isa::F_ADD + isa::SR_ADD;
+                uint32_t va = 0, vb = 0, vz = 0, ta = isa::kNone, tb = isa::kNone;
+                auto target = [&](uint32_t s) {
+                    uint32_t x = target_word(s);
+                    return x == isa::kNone ? kSink : x;
+                };
+                switch (o.code) {
+                case tp::ADD: case tp::SUB: ta = target(o.a); tb = target(o.b); break;
+                case tp::MUL: va = v(o.a); vb = v(o.b); ta = target(o.a); tb = target(o.b); break;
+                case tp::DIV: vb = v(o.b); vz = v(k); ta = target(o.a); tb = target(o.b); break;
+                case tp::NEG: ta = target(o.a); break;
+                case tp::EXP: vz = v(k); ta = target(o.a); break;
+                case tp::SQRT: va = v(o.a); vz = v(k); ta = target(o.a); break;
+                case tp::SELECT: va = v(o.a); vb = v(o.b); ta = target(o.c); tb = target(o.d); break;
+                default: va = v(o.a); ta = target(o.a); break;   // LOG SIN COS ABS
+                }
+                E.put(isa::w0(sop, 0, 1), g, va, vb, vz, ta, tb);
+                break;
+            }
             switch (o.code) {
             case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: {
                 uint32_t mode = isa::MODE_SAME;

@@ -84,7 +84,7 @@ def test_random_programs_full_size_sampled(nd, oracle_mod):
     loss, grad = loss.cpu().numpy(), grad.cpu().numpy()
     rng = np.random.default_rng(1)
     progs = sorted(set(rng.choice(len(tapes), 40, replace=False).tolist()) | {0, len(tapes) - 1})
-    worst, amb = 0.0, 0
+    worst, amb, ill, n = 0.0, 0, 0, 0
     for q in progs:
         P = w.n_params_each[q]
         lanes = sample_lanes(w.L, 48, seed=q)
@@ -94,8 +94,11 @@ def test_random_programs_full_size_sampled(nd, oracle_mod):
         r = compare(loss[q, lanes], grad[q, lanes, :P], ol, og, ole, oge, margin=m)
         worst = max(worst, r["max_loss_err"], r["max_grad_err"])
         amb += r["n_ambiguous"]
-    print("random programs: worst", worst, "ambiguous lanes", amb)
-    assert amb <= 5
+        ill += r["n_ill_conditioned"]
+        n += r["n_lanes"]
+    print("random programs: lanes", n, "worst", worst, "excused near-tie lanes", amb,
+          "ill-conditioned lanes judged in extended precision", ill)
+    assert amb <= 5 and ill <= n // 50
 
 
 def test_random_programs_small_all_lanes_and_single_equals_many(nd, oracle_mod):
