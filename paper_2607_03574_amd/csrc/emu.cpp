@@ -31,8 +31,10 @@ struct HostCtx {
     int *fault;       // first problem seen: 1 register range, 2 unwritten read, 3 pool, 4 ckpt
 
     static uint32_t uni(uint32_t x) { return x; }
-    static void fetch(const uint32_t *pc, uint32_t (&w)[8]) {
-        for (int i = 0; i < 8; ++i) w[i] = pc[i];
+    using Fetch = const uint32_t *;
+    static Fetch prefetch(const uint32_t *pc) { return pc; }
+    static void decode(Fetch f, uint32_t (&w)[8]) {
+        for (int i = 0; i < 8; ++i) w[i] = f[i];
     }
     static uint32_t aux_word(const uint32_t *aux, uint32_t i) { return aux[i]; }
     void flag(int code) const {

@@ -45,11 +45,30 @@ struct DevCtx {
     bool active;
 
     __device__ __forceinline__ static uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
-    // program words are wave-uniform and read-only: scalar loads
-    __device__ __forceinline__ static void fetch(const uint32_t *pc, uint32_t (&w)[8]) {
-        const AS_CONST uint32_t *p = (const AS_CONST uint32_t *)(pc);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) w[i] = p[i];
+    // Program words are wave-uniform.  They are read with vector loads from a
+    // uniform address (one request per wave) so that a load issued two
+    // instructions ahead is tracked by the in-order vmcnt counter and does not
+    // hold up the LDS waits of the instructions in between.
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    struct Fetch {
+        u32x4 a, b;
+    };
+    __device__ __forceinline__ static Fetch prefetch(const uint32_t *pc) {
+        const AS_GLOBAL u32x4 *p = (const AS_GLOBAL u32x4 *)(pc);
+        Fetch f;
+        f.a = p[0];
+        f.b = p[1];
+        return f;
+    }
+    __device__ __forceinline__ static void decode(const Fetch &f, uint32_t (&w)[8]) {
+        w[0] = f.a.x;
+        w[1] = f.a.y;
+        w[2] = f.a.z;
+        w[3] = f.a.w;
+        w[4] = f.b.x;
+        w[5] = f.b.y;
+        w[6] = f.b.z;
+        w[7] = f.b.w;
     }
     __device__ __forceinline__ static uint32_t aux_word(const uint32_t *aux, uint32_t i) {
         return ((const AS_CONST uint32_t *)(aux))[i];

@@ -6,7 +6,7 @@
 //   double ld_raw(uint32_t r) const;   (a read whose value may be discarded)
 //   double konst(uint32_t i) const;  double obsv(uint32_t i) const;  (uniform loads)
 //   static uint32_t uni(uint32_t x);          (wave-uniform value)
-//   static void fetch(const uint32_t *pc, uint32_t (&w)[8]);  (one instruction)
+//   Fetch prefetch(const uint32_t *pc);  void decode(const Fetch&, uint32_t (&w)[8]);
 //   double param(uint32_t p) const;  void store_loss(double) const;
 //   void store_grad(uint32_t p, double) const;
 //   void ckpt_st(uint32_t row, double) const;  double ckpt_ld(uint32_t row) const;
@@ -584,62 +584,82 @@ NDVM_HD void exec_scalar(const C &c, const uint32_t *w) {
     }
 }
 
-// Execute a device program from `pc` until END.
+// Execute one instruction; false at END.  `wv` are the instruction words as
+// loaded (on the GPU: vector registers holding the same value in every
+// lane); the hot scalar handlers use them directly as LDS addresses, all
+// other paths first make every word an explicit scalar.
+template <class C>
+NDVM_HD bool step(const C &c, const uint32_t *wv, const uint32_t *aux) {
+    const uint32_t op = C::uni(wv[0]) & 0xFF;
+    if (op >= S_ADD && ((kHotMask >> (op - S_ADD)) & 1u)) {
+        exec_hot(c, wv, op);
+        return true;
+    }
+    uint32_t w[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = C::uni(wv[i]);
+    if (op >= S_ADD) {
+        exec_scalar(c, w);
+        return true;
+    }
+    if (op >= R_ADD) {
+        exec_rev(c, aux, w);
+        return true;
+    }
+    if (op >= F_ADD) {
+        exec_fwd(c, aux, w);
+        return true;
+    }
+    const uint32_t n = (w[0] >> 16) & 0xFF;
+    switch (op) {
+    case END:
+        return false;
+    case LDPARAM:
+        c.st(w[1], c.param(w[7]));
+        break;
+    case ST_LOSS:
+        c.store_loss(c.ld(w[2]));
+        break;
+    case CKPT_ST:
+        for (uint32_t i = 0; i < n; ++i) c.ckpt_st(w[7] + i, c.ld(w[2] + i));
+        break;
+    case CKPT_LD:
+        for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, c.ckpt_ld(w[7] + i));
+        break;
+    case ZERO:
+        for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, 0.0);
+        break;
+    case SEED:
+        acc(c, w[5], 0, 1.0, true);
+        break;
+    case ST_GRAD:
+        c.store_grad(w[7], c.ld(w[2]));
+        break;
+    case LDOBS:
+        c.st(w[1], c.obsv(w[7]));
+        break;
+    case LDCONST:
+        for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, c.konst(w[7] + i));
+        break;
+    default:
+        return false;
+    }
+    return true;
+}
+
+// Execute a device program from `pc` until END.  Instruction words are
+// fetched two instructions ahead (programs end with two padding words of
+// END so the look-ahead stays inside the program).
 template <class C>
 NDVM_HD void run(const C &c, const uint32_t *pc, const uint32_t *aux) {
+    typename C::Fetch f0 = C::prefetch(pc), f1 = C::prefetch(pc + kWords);
     for (;; pc += kWords) {
-        uint32_t w[8];
-        C::fetch(pc, w);
-        const uint32_t op = w[0] & 0xFF;
-        if (op >= S_ADD) {
-            if ((kHotMask >> (op - S_ADD)) & 1u)
-                exec_hot(c, w, op);
-            else
-                exec_scalar(c, w);
-            continue;
-        }
-        if (op >= R_ADD) {
-            exec_rev(c, aux, w);
-            continue;
-        }
-        if (op >= F_ADD) {
-            exec_fwd(c, aux, w);
-            continue;
-        }
-        const uint32_t n = (w[0] >> 16) & 0xFF;
-        switch (op) {
-        case END:
-            return;
-        case LDPARAM:
-            c.st(w[1], c.param(w[7]));
-            break;
-        case ST_LOSS:
-            c.store_loss(opnd(c, w[2]));
-            break;
-        case CKPT_ST:
-            for (uint32_t i = 0; i < n; ++i) c.ckpt_st(w[7] + i, c.ld(w[2] + i));
-            break;
-        case CKPT_LD:
-            for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, c.ckpt_ld(w[7] + i));
-            break;
-        case ZERO:
-            for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, 0.0);
-            break;
-        case SEED:
-            acc(c, w[5], 0, 1.0, true);
-            break;
-        case ST_GRAD:
-            c.store_grad(w[7], c.ld(w[2]));
-            break;
-        case LDOBS:
-            c.st(w[1], c.obsv(w[7]));
-            break;
-        case LDCONST:
-            for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, c.konst(w[7] + i));
-            break;
-        default:
-            return;
-        }
+        typename C::Fetch f2 = C::prefetch(pc + 2 * kWords);
+        uint32_t wv[8];
+        C::decode(f0, wv);
+        if (!step(c, wv, aux)) return;
+        f0 = f1;
+        f1 = f2;
     }
 }
 

@@ -504,7 +504,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         }
     }
     if (!with_grad) {
-        E.put(isa::w0(isa::END, 0, 0));
+        for (int pad = 0; pad < 3; ++pad) E.put(isa::w0(isa::END, 0, 0));   // END + look-ahead padding
         S.n_regs = kStatic + fhwm;
         S.code = std::move(E.code);
         S.aux = std::move(E.aux);
@@ -737,7 +737,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             break;
         }
     }
-    E.put(isa::w0(isa::END, 0, 0));
+    for (int pad = 0; pad < 3; ++pad) E.put(isa::w0(isa::END, 0, 0));   // END + look-ahead padding
     S.code = std::move(E.code);
     S.aux = std::move(E.aux);
     S.n_instr = S.code.size() / isa::kWords;
