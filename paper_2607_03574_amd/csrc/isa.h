@@ -46,6 +46,10 @@ enum : uint32_t {
     // scalar (1x1) fast paths of the elementwise ops and the select: no
     // element loops, no broadcast modes
     S_ADD = 96, S_SUB, S_MUL, S_DIV, S_NEG, S_EXP, S_LOG, S_SQRT, S_SIN, S_COS, S_ABS, S_SELECT,
+    // two independent scalar binary ops in one instruction: sub-ops (0 add,
+    // 1 sub, 2 mul, 3 div) in w0 bits 8-11 and 12-15; w1..w3 = d1, a1, b1,
+    // w4..w6 = d2, a2, b2
+    F2 = 108,
     SR_ADD = 112, SR_SUB, SR_MUL, SR_DIV, SR_NEG, SR_EXP, SR_LOG, SR_SQRT, SR_SIN, SR_COS, SR_ABS,
     SR_SELECT,
     OP_COUNT

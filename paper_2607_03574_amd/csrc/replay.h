@@ -471,15 +471,32 @@ NDVM_HD void acc1(const C &c, uint32_t tw, double x, bool on) {
 // branches unstructured (a direct jump back to the dispatch).
 constexpr uint32_t kHotMask =
     (1u << (S_ADD - S_ADD)) | (1u << (S_SUB - S_ADD)) | (1u << (S_MUL - S_ADD)) | (1u << (S_DIV - S_ADD)) |
-    (1u << (S_NEG - S_ADD)) | (1u << (S_ABS - S_ADD)) | (1u << (S_SELECT - S_ADD)) |
+    (1u << (S_NEG - S_ADD)) | (1u << (S_ABS - S_ADD)) | (1u << (S_SELECT - S_ADD)) | (1u << (F2 - S_ADD)) |
     (1u << (SR_ADD - S_ADD)) | (1u << (SR_SUB - S_ADD)) | (1u << (SR_MUL - S_ADD)) |
     (1u << (SR_DIV - S_ADD)) | (1u << (SR_NEG - S_ADD)) | (1u << (SR_EXP - S_ADD)) |
     (1u << (SR_LOG - S_ADD)) | (1u << (SR_SQRT - S_ADD)) | (1u << (SR_ABS - S_ADD)) |
     (1u << (SR_SELECT - S_ADD));
 
+// scalar binary op selected by a wave-uniform sub-op code
+NDVM_HD double binop(uint32_t sub, double a, double b) {
+    switch (sub) {
+    case 0: return a + b;
+    case 1: return a - b;
+    case 2: return a * b;
+    default: return a / b;
+    }
+}
+
 template <class C>
 NDVM_HD void exec_hot(const C &c, const uint32_t *w, uint32_t op) {
     switch (op) {
+    case F2: {
+        const uint32_t h = C::uni(w[0]);
+        const double a1 = c.ld(w[2]), b1 = c.ld(w[3]), a2 = c.ld(w[5]), b2 = c.ld(w[6]);
+        c.st(w[1], binop((h >> 8) & 15u, a1, b1));
+        c.st(w[4], binop((h >> 12) & 15u, a2, b2));
+        return;
+    }
     case S_ADD: c.st(w[1], c.ld(w[2]) + c.ld(w[3])); return;
     case S_SUB: c.st(w[1], c.ld(w[2]) - c.ld(w[3])); return;
     case S_MUL: c.st(w[1], c.ld(w[2]) * c.ld(w[3])); return;

@@ -216,11 +216,12 @@ uint32_t fwd_opcode(uint16_t c) {
 
 // ------------------------------------------------------------------ builder
 // Abstract instruction before register assignment.
-enum RIKind : uint8_t { I_LDP, I_LDC, I_CKST, I_FWD, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_STG };
+enum RIKind : uint8_t { I_LDP, I_LDC, I_CKST, I_FWD, I_FWD2, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_STG };
 struct AI {
     uint8_t kind;
     uint32_t k;   // slot / param index
     uint32_t j;   // segment (reverse phase) or checkpoint row
+    uint32_t k2;  // second op of a dual instruction (I_FWD2)
 };
 
 struct Builder {
@@ -342,6 +343,94 @@ struct Builder {
     }
 };
 
+// scalar binary ops that may share a dual instruction, and their sub-op code
+int dual_sub(const Info &I, uint32_t k) {
+    const TapeOp &o = I.t.ops[k];
+    if (I.kind[k] != K_COMP || I.nel[k] != 1) return -1;
+    switch (o.code) {
+    case tp::ADD: return 0;
+    case tp::SUB: return 1;
+    case tp::MUL: return 2;
+    case tp::DIV: return 3;
+    }
+    return -1;
+}
+
+// Reorder each run of forward instructions (list scheduling, earliest op
+// first, data dependences kept) and merge independent scalar binary ops into
+// dual instructions.  Every op still computes exactly what it computed
+// before, so results are unchanged bit for bit.
+std::vector<AI> pair_forward(const Info &I, const std::vector<AI> &in) {
+    std::vector<AI> out;
+    out.reserve(in.size());
+    const uint32_t kWindow = 24;
+    size_t i = 0;
+    std::vector<uint32_t> pos_of(I.N, UINT32_MAX);
+    while (i < in.size()) {
+        if (in[i].kind != I_FWD) {
+            out.push_back(in[i++]);
+            continue;
+        }
+        size_t e = i;
+        while (e < in.size() && in[e].kind == I_FWD && in[e].j == in[i].j) ++e;
+        const uint32_t n = uint32_t(e - i);
+        for (uint32_t q = 0; q < n; ++q) pos_of[in[i + q].k] = q;
+        std::vector<uint8_t> done(n, 0);
+        std::vector<uint32_t> pending(n, 0);   // operands still to be emitted
+        std::vector<uint32_t> ucnt(n + 1, 0), users;
+        for (uint32_t q = 0; q < n; ++q)
+            I.for_operands(in[i + q].k, [&](uint32_t s) {
+                if (pos_of[s] != UINT32_MAX) {
+                    pending[q]++;
+                    ucnt[pos_of[s] + 1]++;
+                }
+            });
+        for (uint32_t q = 0; q < n; ++q) ucnt[q + 1] += ucnt[q];
+        users.resize(ucnt[n]);
+        {
+            std::vector<uint32_t> fill(ucnt.begin(), ucnt.end() - 1);
+            for (uint32_t q = 0; q < n; ++q)
+                I.for_operands(in[i + q].k, [&](uint32_t s) {
+                    if (pos_of[s] != UINT32_MAX) users[fill[pos_of[s]]++] = q;
+                });
+        }
+        auto retire = [&](uint32_t q) {
+            done[q] = 1;
+            for (uint32_t u = ucnt[q]; u < ucnt[q + 1]; ++u) pending[users[u]]--;
+        };
+        uint32_t first = 0;
+        for (uint32_t emitted = 0; emitted < n;) {
+            while (done[first]) ++first;
+            uint32_t x = first;
+            while (pending[x] != 0) ++x;         // earliest ready op
+            int sx = dual_sub(I, in[i + x].k);
+            int32_t y = -1;
+            if (sx >= 0)
+                for (uint32_t r = x + 1; r < n && r < x + kWindow; ++r)
+                    if (!done[r] && pending[r] == 0 && dual_sub(I, in[i + r].k) >= 0) {
+                        y = int32_t(r);
+                        break;
+                    }
+            if (y >= 0) {
+                AI a = in[i + x];
+                a.kind = I_FWD2;
+                a.k2 = in[i + y].k;
+                out.push_back(a);
+                retire(x);
+                retire(uint32_t(y));
+                emitted += 2;
+            } else {
+                out.push_back(in[i + x]);
+                retire(x);
+                emitted += 1;
+            }
+        }
+        for (uint32_t q = 0; q < n; ++q) pos_of[in[i + q].k] = UINT32_MAX;
+        i = e;
+    }
+    return out;
+}
+
 struct Emitter {
     std::vector<uint32_t> code, aux;
     void put(uint32_t a, uint32_t b = 0, uint32_t c = 0, uint32_t d = 0, uint32_t e = 0, uint32_t f = 0,
@@ -392,6 +481,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         if (B.comp_live(k) || (I.kind[k] == K_OBS && I.live[k])) fa.push_back({I_FWD, k, 0});
     }
     fa.push_back({I_STLOSS, t.loss, 0});
+    fa = pair_forward(I, fa);
     // intervals for forward values
     std::vector<Interval> fiv;
     std::vector<int32_t> fiv_of(N, -1);
@@ -400,11 +490,13 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         auto use = [&](uint32_t s) {
             if (fiv_of[s] >= 0) fiv[fiv_of[s]].end = std::max(fiv[fiv_of[s]].end, ti);
         };
-        if (a.kind == I_FWD) {
+        if (a.kind == I_FWD || a.kind == I_FWD2) {
             I.for_operands(a.k, use);
-            if (!(with_grad && B.resident[a.k])) {
-                fiv_of[a.k] = int32_t(fiv.size());
-                fiv.push_back({ti, ti, I.nel[a.k], 0});
+            if (a.kind == I_FWD2) I.for_operands(a.k2, use);
+            for (uint32_t k : {a.k, a.kind == I_FWD2 ? a.k2 : a.k}) {
+                if (fiv_of[k] >= 0 || (with_grad && B.resident[k])) continue;
+                fiv_of[k] = int32_t(fiv.size());
+                fiv.push_back({ti, ti, I.nel[k], 0});
             }
         } else if (a.kind == I_CKST) {
             use(B.livein[a.k][a.j]);
@@ -484,6 +576,11 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         }
     };
 
+    auto emit_dual = [&](uint32_t k1, uint32_t k2, auto operand) {
+        const TapeOp &o1 = t.ops[k1], &o2 = t.ops[k2];
+        uint32_t w = isa::F2 | (uint32_t(dual_sub(I, k1)) << 8) | (uint32_t(dual_sub(I, k2)) << 12) | (1u << 16);
+        E.put(w, operand(k1), operand(o1.a), operand(o1.b), operand(k2), operand(o2.a), operand(o2.b));
+    };
     for (const AI &a : fa) {
         switch (a.kind) {
         case I_LDP: E.put(isa::w0(isa::LDPARAM, 0, 1), a.k, 0, 0, 0, 0, 0, a.k); break;
@@ -497,8 +594,13 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             break;
         }
         case I_FWD:
-            emit_fwd(a.k, fwd_operand, fwd_operand(a.k) & isa::kIndexMask);
+            emit_fwd(a.k, fwd_operand, fwd_operand(a.k));
             S.n_fwd_ops++;
+            break;
+        case I_FWD2:
+            emit_dual(a.k, a.k2, fwd_operand);
+            S.n_fwd_ops += 2;
+            S.n_dual++;
             break;
         case I_STLOSS: E.put(isa::w0(isa::ST_LOSS, 0, 1), 0, fwd_operand(a.k)); break;
         }
@@ -522,6 +624,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         for (uint32_t k : B.revops[j]) ra.push_back({I_REV, k, j});
     }
     for (uint32_t p = 0; p < P; ++p) ra.push_back({I_STG, p, 0});
+    ra = pair_forward(I, ra);
 
     // value intervals keyed by (slot, segment); adjoint intervals keyed by slot
     std::vector<Interval> riv;
@@ -555,10 +658,15 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             riv.push_back({ti, ti, I.nel[s], 0});
             break;
         }
-        case I_FWD:
+        case I_FWD: case I_FWD2:
             I.for_operands(a.k, [&](uint32_t s) { vuse(s, a.j, ti); });
+            if (a.kind == I_FWD2) I.for_operands(a.k2, [&](uint32_t s) { vuse(s, a.j, ti); });
             val_of[key(a.k, a.j)] = uint32_t(riv.size());
             riv.push_back({ti, ti, I.nel[a.k], 0});
+            if (a.kind == I_FWD2) {
+                val_of[key(a.k2, a.j)] = uint32_t(riv.size());
+                riv.push_back({ti, ti, I.nel[a.k2], 0});
+            }
             break;
         case I_REV: {
             I.for_revreads(a.k, [&](uint32_t s) { vuse(s, a.j, ti); });
@@ -620,6 +728,13 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             auto opnd = [&](uint32_t s) { return rev_operand(s, a.j); };
             emit_fwd(a.k, opnd, rev_operand(a.k, a.j));
             S.n_recompute_ops++;
+            break;
+        }
+        case I_FWD2: {
+            auto opnd = [&](uint32_t s) { return rev_operand(s, a.j); };
+            emit_dual(a.k, a.k2, opnd);
+            S.n_recompute_ops += 2;
+            S.n_dual++;
             break;
         }
         case I_REV: {

@@ -16,6 +16,7 @@ struct Schedule {
     uint32_t static_regs = 0, fwd_regs = 0, rev_regs = 0;
     uint64_t n_instr = 0, n_fwd_ops = 0, n_recompute_ops = 0, n_rev_ops = 0;
     uint64_t ckpt_elems_stored = 0, ckpt_elems_loaded = 0;
+    uint64_t n_dual = 0;          // dual (two-op) instructions
 };
 
 // Forward-only program (loss[L]).
