@@ -50,6 +50,11 @@ enum : uint32_t {
     // 1 sub, 2 mul, 3 div) in w0 bits 8-11 and 12-15; w1..w3 = d1, a1, b1,
     // w4..w6 = d2, a2, b2
     F2 = 108,
+    // two scalar adjoint rules (sub-ops 0 add, 1 sub, 2 mul, 3 div) with
+    // 16-bit fields: w1 = g1 | a1 << 16, w2 = b1 | z1 << 16,
+    // w3 = ta1 | tb1 << 16, w4..w6 the same for the second rule; a target
+    // field is a register below 2^15 with bit 15 = first contribution
+    R2 = 109,
     SR_ADD = 112, SR_SUB, SR_MUL, SR_DIV, SR_NEG, SR_EXP, SR_LOG, SR_SQRT, SR_SIN, SR_COS, SR_ABS,
     SR_SELECT,
     OP_COUNT
@@ -62,6 +67,7 @@ constexpr uint32_t kIndexMask = (1u << 30) - 1;
 constexpr uint32_t kInit = 0x80000000u;
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 constexpr uint32_t kWords = 8;
+constexpr uint32_t kR2MaxReg = 1u << 15;   // registers addressable by R2 fields
 
 inline uint32_t w0(uint32_t op, uint32_t mode, uint32_t nel) { return op | (mode << 8) | (nel << 16); }
 inline uint32_t dims(uint32_t m, uint32_t k, uint32_t n) { return m | (k << 8) | (n << 16); }

@@ -61,14 +61,19 @@ struct DevCtx {
         return f;
     }
     __device__ __forceinline__ static void decode(const Fetch &f, uint32_t (&w)[8]) {
-        w[0] = f.a.x;
-        w[1] = f.a.y;
-        w[2] = f.a.z;
-        w[3] = f.a.w;
-        w[4] = f.b.x;
-        w[5] = f.b.y;
-        w[6] = f.b.z;
-        w[7] = f.b.w;
+        // keep the words in vector registers up to this point, so no
+        // conversion to scalars (which waits for the load) is hoisted up to
+        // the prefetch
+        u32x4 a = f.a, b = f.b;
+        asm volatile("" : "+v"(a), "+v"(b));
+        w[0] = a.x;
+        w[1] = a.y;
+        w[2] = a.z;
+        w[3] = a.w;
+        w[4] = b.x;
+        w[5] = b.y;
+        w[6] = b.z;
+        w[7] = b.w;
     }
     __device__ __forceinline__ static uint32_t aux_word(const uint32_t *aux, uint32_t i) {
         return ((const AS_CONST uint32_t *)(aux))[i];

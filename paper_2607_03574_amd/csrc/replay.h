@@ -471,7 +471,7 @@ NDVM_HD void acc1(const C &c, uint32_t tw, double x, bool on) {
 // branches unstructured (a direct jump back to the dispatch).
 constexpr uint32_t kHotMask =
     (1u << (S_ADD - S_ADD)) | (1u << (S_SUB - S_ADD)) | (1u << (S_MUL - S_ADD)) | (1u << (S_DIV - S_ADD)) |
-    (1u << (S_NEG - S_ADD)) | (1u << (S_ABS - S_ADD)) | (1u << (S_SELECT - S_ADD)) | (1u << (F2 - S_ADD)) |
+    (1u << (S_NEG - S_ADD)) | (1u << (S_ABS - S_ADD)) | (1u << (S_SELECT - S_ADD)) | (1u << (F2 - S_ADD)) | (1u << (R2 - S_ADD)) |
     (1u << (SR_ADD - S_ADD)) | (1u << (SR_SUB - S_ADD)) | (1u << (SR_MUL - S_ADD)) |
     (1u << (SR_DIV - S_ADD)) | (1u << (SR_NEG - S_ADD)) | (1u << (SR_EXP - S_ADD)) |
     (1u << (SR_LOG - S_ADD)) | (1u << (SR_SQRT - S_ADD)) | (1u << (SR_ABS - S_ADD)) |
@@ -487,9 +487,50 @@ NDVM_HD double binop(uint32_t sub, double a, double b) {
     }
 }
 
+// contributions of one scalar binary adjoint rule (sub-op as in binop)
+template <class C>
+NDVM_HD void rev_binop(const C &c, uint32_t sub, uint32_t wg, uint32_t wa, uint32_t wb, uint32_t wz,
+                       uint32_t ta, uint32_t tb) {
+    const double g = c.ld(wg);
+    const bool nz = g != 0.0;
+    switch (sub) {
+    case 0:
+        acc1(c, ta, g, nz);
+        acc1(c, tb, g, nz);
+        return;
+    case 1:
+        acc1(c, ta, g, nz);
+        acc1(c, tb, -g, nz);
+        return;
+    case 2: {
+        const double a = c.ld(wa), b = c.ld(wb);
+        acc1(c, ta, g * b, nz);
+        acc1(c, tb, g * a, nz);
+        return;
+    }
+    default: {
+        const double b = c.ld(wb), z = c.ld(wz);
+        acc1(c, ta, g / b, nz);
+        acc1(c, tb, -((g * z) / b), nz);
+        return;
+    }
+    }
+}
+
+// a 16-bit target field as a target word
+NDVM_HD uint32_t t16(uint32_t f) { return (f & 0x7FFFu) | ((f & 0x8000u) << 16); }
+
 template <class C>
 NDVM_HD void exec_hot(const C &c, const uint32_t *w, uint32_t op) {
     switch (op) {
+    case R2: {
+        const uint32_t h = C::uni(w[0]);
+        rev_binop(c, (h >> 8) & 15u, w[1] & 0xFFFFu, w[1] >> 16, w[2] & 0xFFFFu, w[2] >> 16,
+                  t16(w[3] & 0xFFFFu), t16(w[3] >> 16));
+        rev_binop(c, (h >> 12) & 15u, w[4] & 0xFFFFu, w[4] >> 16, w[5] & 0xFFFFu, w[5] >> 16,
+                  t16(w[6] & 0xFFFFu), t16(w[6] >> 16));
+        return;
+    }
     case F2: {
         const uint32_t h = C::uni(w[0]);
         const double a1 = c.ld(w[2]), b1 = c.ld(w[3]), a2 = c.ld(w[5]), b2 = c.ld(w[6]);
@@ -664,9 +705,9 @@ NDVM_HD bool step(const C &c, const uint32_t *wv, const uint32_t *aux) {
     return true;
 }
 
-// Execute a device program from `pc` until END.  Instruction words are
-// fetched two instructions ahead (programs end with two padding words of
-// END so the look-ahead stays inside the program).
+// Execute a device program from `pc` until END.  Instructions are fetched two
+// ahead (programs end with padding instructions of END so the look-ahead stays
+// inside the program).
 template <class C>
 NDVM_HD void run(const C &c, const uint32_t *pc, const uint32_t *aux) {
     typename C::Fetch f0 = C::prefetch(pc), f1 = C::prefetch(pc + kWords);

@@ -216,7 +216,8 @@ uint32_t fwd_opcode(uint16_t c) {
 
 // ------------------------------------------------------------------ builder
 // Abstract instruction before register assignment.
-enum RIKind : uint8_t { I_LDP, I_LDC, I_CKST, I_FWD, I_FWD2, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_STG };
+enum RIKind : uint8_t { I_LDP, I_LDC, I_CKST, I_FWD, I_FWD2, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_REV2,
+                        I_STG };
 struct AI {
     uint8_t kind;
     uint32_t k;   // slot / param index
@@ -431,6 +432,95 @@ std::vector<AI> pair_forward(const Info &I, const std::vector<AI> &in) {
     return out;
 }
 
+// Pair scalar adjoint rules of each run of reverse instructions.  An op may be
+// hoisted next to an earlier one only when its own adjoint is complete (every
+// op contributing to it has been emitted) and no op it jumps over touches any
+// of its targets; so every adjoint still receives its contributions in the
+// same order and the results are unchanged bit for bit.
+std::vector<AI> pair_reverse(const Info &I, const std::vector<AI> &in) {
+    std::vector<AI> out;
+    out.reserve(in.size());
+    const uint32_t kWindow = 24;
+    auto tid = [&](uint32_t s) -> int64_t {   // adjoint identity of a target, -1 if none
+        if (I.kind[s] == K_PARAM) return int64_t(I.N) + I.t.ops[s].imm;
+        if (I.kind[s] == K_COMP && I.active[s]) return s;
+        return -1;
+    };
+    size_t i = 0;
+    while (i < in.size()) {
+        if (in[i].kind != I_REV) {
+            out.push_back(in[i++]);
+            continue;
+        }
+        size_t e = i;
+        while (e < in.size() && in[e].kind == I_REV && in[e].j == in[i].j) ++e;
+        const uint32_t n = uint32_t(e - i);
+        std::vector<std::vector<int64_t>> T(n);
+        std::unordered_map<int64_t, std::vector<uint32_t>> by_target;
+        for (uint32_t q = 0; q < n; ++q) {
+            I.for_targets(in[i + q].k, [&](uint32_t s) {
+                int64_t id = tid(s);
+                if (id >= 0) T[q].push_back(id);
+            });
+            for (int64_t id : T[q]) by_target[id].push_back(q);
+        }
+        std::vector<uint32_t> pend(n, 0);
+        for (uint32_t q = 0; q < n; ++q) {
+            auto it = by_target.find(int64_t(in[i + q].k));
+            if (it != by_target.end())
+                for (uint32_t p : it->second)
+                    if (p < q) pend[q]++;
+        }
+        std::vector<uint8_t> done(n, 0);
+        auto retire = [&](uint32_t q) {
+            done[q] = 1;
+            for (int64_t id : T[q]) {
+                if (id >= int64_t(I.N)) continue;
+                // ops in this run whose output is `id` lose one pending contributor
+                for (uint32_t r = q + 1; r < n && r < q + 4 * kWindow; ++r)
+                    if (int64_t(in[i + r].k) == id && pend[r] > 0) pend[r]--;
+            }
+        };
+        uint32_t first = 0;
+        std::vector<int64_t> skipped;
+        for (uint32_t emitted = 0; emitted < n;) {
+            while (done[first]) ++first;
+            const uint32_t x = first;
+            int32_t y = -1;
+            if (dual_sub(I, in[i + x].k) >= 0) {
+                skipped.clear();
+                for (uint32_t r = x + 1; r < n && r < x + kWindow; ++r) {
+                    if (done[r]) continue;
+                    bool clash = false;
+                    for (int64_t id : T[r])
+                        for (int64_t sid : skipped) clash = clash || id == sid;
+                    if (!clash && pend[r] == 0 && dual_sub(I, in[i + r].k) >= 0) {
+                        y = int32_t(r);
+                        break;
+                    }
+                    skipped.insert(skipped.end(), T[r].begin(), T[r].end());
+                    skipped.push_back(int64_t(in[i + r].k));
+                }
+            }
+            if (y >= 0) {
+                AI a = in[i + x];
+                a.kind = I_REV2;
+                a.k2 = in[i + y].k;
+                out.push_back(a);
+                retire(x);
+                retire(uint32_t(y));
+                emitted += 2;
+            } else {
+                out.push_back(in[i + x]);
+                retire(x);
+                emitted += 1;
+            }
+        }
+        i = e;
+    }
+    return out;
+}
+
 struct Emitter {
     std::vector<uint32_t> code, aux;
     void put(uint32_t a, uint32_t b = 0, uint32_t c = 0, uint32_t d = 0, uint32_t e = 0, uint32_t f = 0,
@@ -625,6 +715,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     }
     for (uint32_t p = 0; p < P; ++p) ra.push_back({I_STG, p, 0});
     ra = pair_forward(I, ra);
+    ra = pair_reverse(I, ra);
 
     // value intervals keyed by (slot, segment); adjoint intervals keyed by slot
     std::vector<Interval> riv;
@@ -668,11 +759,13 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
                 riv.push_back({ti, ti, I.nel[a.k2], 0});
             }
             break;
-        case I_REV: {
-            I.for_revreads(a.k, [&](uint32_t s) { vuse(s, a.j, ti); });
-            I.for_targets(a.k, [&](uint32_t s) { contrib(s, ti); });
-            int32_t g = adj_of[a.k];
-            riv[g].end = std::max(riv[g].end, ti);
+        case I_REV: case I_REV2: {
+            for (uint32_t k : {a.k, a.kind == I_REV2 ? a.k2 : a.k}) {
+                I.for_revreads(k, [&](uint32_t s) { vuse(s, a.j, ti); });
+                I.for_targets(k, [&](uint32_t s) { contrib(s, ti); });
+                int32_t g = adj_of[k];
+                riv[g].end = std::max(riv[g].end, ti);
+            }
             break;
         }
         default:
@@ -845,6 +938,42 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             }
             break;
         }
+        case I_REV2: {
+            uint32_t w[13];
+            int idx = 0;
+            uint32_t subs[2];
+            for (int h = 0; h < 2; ++h) {
+                const uint32_t k = h ? a.k2 : a.k;
+                const TapeOp &o = t.ops[k];
+                subs[h] = uint32_t(dual_sub(I, k));
+                uint32_t vg = adjreg(k);
+                uint32_t va = subs[h] == 2 ? rev_operand(o.a, a.j) : 0;
+                uint32_t vb = subs[h] >= 2 ? rev_operand(o.b, a.j) : 0;
+                uint32_t vz = subs[h] == 3 ? rev_operand(k, a.j) : 0;
+                uint32_t ta = target_word(o.a);
+                uint32_t tb = target_word(o.b);
+                ta = ta == isa::kNone ? kSink : ta;
+                tb = tb == isa::kNone ? kSink : tb;
+                uint32_t f[6] = {vg, va, vb, vz, ta, tb};
+                for (uint32_t v : f) w[idx++] = v;
+            }
+            S.n_rev_ops += 2;
+            bool fits = true;
+            for (int q = 0; q < 12; ++q) fits = fits && (w[q] & ~isa::kInit) < isa::kR2MaxReg;
+            if (!fits) {   // registers beyond the 16-bit fields: two single rules
+                static_assert(isa::SR_SUB == isa::SR_ADD + 1 && isa::SR_DIV == isa::SR_ADD + 3, "SR order");
+                for (int h = 0; h < 2; ++h)
+                    E.put(isa::w0(isa::SR_ADD + subs[h], 0, 1), w[6 * h], w[6 * h + 1], w[6 * h + 2],
+                          w[6 * h + 3], w[6 * h + 4], w[6 * h + 5]);
+                break;
+            }
+            S.n_dual++;
+            auto t16 = [](uint32_t tw) { return (tw & 0x7FFFu) | ((tw & isa::kInit) ? 0x8000u : 0u); };
+            auto pk = [](uint32_t lo, uint32_t hi) { return lo | (hi << 16); };
+            E.put(isa::R2 | (subs[0] << 8) | (subs[1] << 12) | (1u << 16), pk(w[0], w[1]), pk(w[2], w[3]),
+                  pk(t16(w[4]), t16(w[5])), pk(w[6], w[7]), pk(w[8], w[9]), pk(t16(w[10]), t16(w[11])));
+            break;
+        }
         case I_STG:
             E.put(isa::w0(isa::ST_GRAD, 0, 1), 0, P + a.k, 0, 0, 0, 0, a.k);
             break;
@@ -878,10 +1007,7 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget) {
     for (uint32_t k = 0; k < I.N; ++k)
         if (I.kind[k] == K_COMP && I.live[k]) total += I.nel[k];
     const uint32_t kResidentAfter = 2;   // checkpointed in more segments -> keep resident
-    Schedule best;
-    bool have = false, best_fits = false;
-    uint64_t S = std::max<uint64_t>(total, 1);
-    for (;;) {
+    auto trial = [&](uint64_t S) {
         Builder B(I);
         B.resident.assign(I.N, 0);
         B.res_off.assign(I.N, 0);
@@ -890,15 +1016,38 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget) {
         B.choose_residents(kResidentAfter);
         B.set_cuts(B.choose_cuts(S));
         B.plan(true);
-        Schedule cand = build(I, B, true);
-        bool fits = cand.n_regs <= reg_budget;
-        if (!have || (fits && !best_fits) || (!fits && !best_fits && cand.n_regs < best.n_regs)) {
-            best = std::move(cand);
-            have = true;
-            best_fits = fits;
+        return build(I, B, true);
+    };
+    // Largest segment size (in value elements) whose register file fits the
+    // budget: halve until it fits, then bisect between the fitting size and
+    // the one above it.  If nothing fits, keep the smallest register file.
+    uint64_t hi = std::max<uint64_t>(total, 1);
+    Schedule best = trial(hi);
+    if (best.n_regs <= reg_budget) return best;
+    uint64_t lo = hi;
+    bool found = false;
+    while (lo > 4) {
+        lo /= 2;
+        Schedule c = trial(lo);
+        if (c.n_regs <= reg_budget) {
+            best = std::move(c);
+            found = true;
+            break;
         }
-        if (best_fits || S <= 4) break;
-        S /= 2;
+        if (c.n_regs < best.n_regs) best = std::move(c);
+        hi = lo;
+    }
+    if (!found) return best;
+    // invariant: lo fits, hi does not
+    while (hi - lo > std::max<uint64_t>(8, lo / 16)) {
+        uint64_t mid = lo + (hi - lo) / 2;
+        Schedule c = trial(mid);
+        if (c.n_regs <= reg_budget) {
+            best = std::move(c);
+            lo = mid;
+        } else {
+            hi = mid;
+        }
     }
     return best;
 }

@@ -180,3 +180,26 @@ def test_schedule_is_deterministic():
     a = emu.run(tape, w.params, w.obs, True, 40)
     b = emu.run(tape, w.params, w.obs, True, 40)
     assert a[0].tobytes() == b[0].tobytes() and a[1].tobytes() == b[1].tobytes() and a[2] == b[2]
+
+
+def test_emulated_wide_program_beyond_packed_register_fields(oracle_mod):
+    # 17000 parameters put parameter adjoints above register 2^15, so reverse
+    # pairs whose registers do not fit the packed 16-bit fields must fall back
+    # to single rules; the gradient of sum_i p_i p_(i+1) is p_(i-1) + p_(i+1)
+    P = 17000
+    A = Asm(P, 0)
+    A.param(0).param(1).mul()
+    for i in range(1, P - 1):
+        A.param(i).param(i + 1).mul().add()
+    bc = A.halt().bytes()
+    rng = np.random.default_rng(5)
+    params = rng.uniform(-1, 1, (2, P))
+    le, ge, st = emu.run(nd.tape_build(bc), params, [], True, 320)
+    lo, go, _ = oracle_mod.run(bc, params, [])
+    assert st["n_regs"] > 2 ** 15
+    np.testing.assert_allclose(le, lo, rtol=1e-12)
+    want = np.zeros_like(params)
+    want[:, :-1] += params[:, 1:]
+    want[:, 1:] += params[:, :-1]
+    np.testing.assert_array_equal(ge, go)
+    np.testing.assert_allclose(ge, want, rtol=0, atol=0)
