@@ -98,8 +98,16 @@ struct ndvm_tape {
 namespace {
 
 ndvm_status upload_program(Schedule &&S, const Tape &t, hipStream_t stream, std::unique_ptr<DevProg> *out) {
+    // the kernel fetches whole chunks and reads one chunk past the END one
+    const uint64_t end_at = uint64_t(S.n_instr) - 1;   // index of the END instruction
+    if (S.code.size() % isa::kChunkWords != 0 || S.n_instr == 0 || end_at % isa::kChunkInstr != 0 ||
+        end_at + 2 * isa::kChunkInstr > S.code.size() / isa::kWords ||
+        (S.code[end_at * isa::kWords] & 0xFF) != isa::END) {
+        set_error("internal: device program is not padded to the fetch chunks");
+        return NDVM_E_TAPE;
+    }
     auto dp = std::make_unique<DevProg>();
-    size_t code_b = S.code.size() * 4, aux_b = S.aux.size() * 4, con_b = t.consts.size() * 8;
+    size_t code_b = S.code.size() * 4, aux_b = S.aux.size() * 4, con_b = S.consts.size() * 8;
     size_t aux_off = (code_b + 255) / 256 * 256, con_off = aux_off + (aux_b + 255) / 256 * 256;
     size_t total = con_off + std::max<size_t>(con_b, 8);
     if (hipMalloc(&dp->buf, total) != hipSuccess) {
@@ -111,7 +119,7 @@ ndvm_status upload_program(Schedule &&S, const Tape &t, hipStream_t stream, std:
     std::vector<uint8_t> host(total, 0);
     std::memcpy(host.data(), S.code.data(), code_b);
     if (aux_b) std::memcpy(host.data() + aux_off, S.aux.data(), aux_b);
-    if (con_b) std::memcpy(host.data() + con_off, t.consts.data(), con_b);
+    if (con_b) std::memcpy(host.data() + con_off, S.consts.data(), con_b);
     if (hipMemcpyAsync(dp->buf, host.data(), total, hipMemcpyHostToDevice, stream) != hipSuccess ||
         hipStreamSynchronize(stream) != hipSuccess) {
         set_error("copy of the device program failed");

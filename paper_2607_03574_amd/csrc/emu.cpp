@@ -8,6 +8,7 @@
 // of a never-written register reported.  That exposes register-allocation,
 // checkpoint and first-contribution mistakes without a GPU.
 #include <cmath>
+#include <algorithm>
 #include <cstdio>
 #include <vector>
 
@@ -20,6 +21,7 @@ using namespace ndvm;
 namespace {
 
 struct HostCtx {
+    const uint32_t *code_end;
     double *regs;
     uint8_t *written;
     uint32_t n_regs;
@@ -28,14 +30,16 @@ struct HostCtx {
     double *loss, *grad;
     double *ckpt;
     uint32_t n_ckpt;
-    int *fault;       // first problem seen: 1 register range, 2 unwritten read, 3 pool, 4 ckpt
+    int *fault;       // first problem seen: 1 register range, 2 unwritten read, 3 pool, 4 ckpt,
+                      // 5 program fetch beyond the padded program
 
     static uint32_t uni(uint32_t x) { return x; }
-    using Fetch = const uint32_t *;
-    static Fetch prefetch(const uint32_t *pc) { return pc; }
-    static void decode(Fetch f, uint32_t (&w)[8]) {
-        for (int i = 0; i < 8; ++i) w[i] = f[i];
+    using Chunk = const uint32_t *;
+    Chunk load_chunk(const uint32_t *p) const {
+        if (p + isa::kChunkWords > code_end) flag(5);
+        return p;
     }
+    static const uint32_t *instr(Chunk ch, uint32_t i) { return ch + i * isa::kWords; }
     static uint32_t aux_word(const uint32_t *aux, uint32_t i) { return aux[i]; }
     void flag(int code) const {
         if (*fault == 0) *fault = code;
@@ -110,8 +114,8 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
     for (int64_t l = 0; l < L; ++l) {
         std::fill(written.begin(), written.end(), 0);
         int fault = 0;
-        HostCtx c{regs.data(), written.data(), S.n_regs, t.consts.data(), obs, params + l * ld_p,
-                  uint32_t(t.consts.size()), uint32_t(n_obs), t.n_params, loss + l,
+        HostCtx c{S.code.data() + S.code.size(), regs.data(), written.data(), S.n_regs, S.consts.data(), obs, params + l * ld_p,
+                  uint32_t(S.consts.size()), uint32_t(n_obs), t.n_params, loss + l,
                   grad ? grad + l * ld_g : nullptr, ck.data(), S.n_ckpt_rows, &fault};
         replay::run(c, S.code.data(), S.aux.data());
         if (fault) {
@@ -122,6 +126,21 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
         }
     }
     return 0;
+}
+
+/*
+ * Copy the device program the scheduler makes for `tape` (words, isa::kWords
+ * per instruction, END-terminated) into `out` when it holds `cap` words;
+ * returns the number of words, or -1 on a parse error.
+ */
+int64_t ndvm_emu_program(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_budget, uint32_t *out,
+                         size_t cap) {
+    Tape t;
+    if (parse_tape(tape, len, &t) != NDVM_OK) return -1;
+    Schedule S = with_grad ? schedule_grad(t, reg_budget) : schedule_forward(t);
+    const size_t n = size_t(S.n_instr) * isa::kWords;
+    if (out && cap >= n) std::copy(S.code.begin(), S.code.begin() + n, out);
+    return int64_t(n);
 }
 
 const char *ndvm_emu_error(void) { return get_error(); }

@@ -13,8 +13,9 @@
 //   w6 : adjoint target of b (reverse)
 //   w7 : immediate (dims, element index, aux offset, checkpoint row, param)
 //
-// Operand words are register indices: constants are loaded into static
-// registers once (LDCONST) and observations by LDOBS where they are used.
+// Operand words are register indices: constants (the tape's pool and the
+// constants 1, -1, -0 that bundles use) are loaded into static registers once
+// (LDCONST) and observations by LDOBS where they are used.
 // Adjoint target words: register | kInit (first contribution: store instead
 // of add), or kNone (generic handlers; scalar handlers get a sink register).
 #pragma once
@@ -34,6 +35,7 @@ enum : uint32_t {
     ST_GRAD = 7,   // w2 src reg, w7 param index
     LDOBS = 8,     // w1 dst, w7 observation index
     LDCONST = 9,   // w1 dst, w7 first pool entry, nel entries
+    NOP = 10,      // padding before the END that opens the program's last chunk
 
     F_ADD = 16, F_SUB, F_MUL, F_DIV, F_NEG, F_EXP, F_LOG, F_SQRT, F_SIN, F_COS, F_ABS, F_POW,
     F_DOT, F_MATMUL, F_TRANSPOSE, F_TRACE, F_INV, F_DET, F_LOGDET, F_OUTER, F_PACK, F_INDEX,
@@ -46,17 +48,30 @@ enum : uint32_t {
     // scalar (1x1) fast paths of the elementwise ops and the select: no
     // element loops, no broadcast modes
     S_ADD = 96, S_SUB, S_MUL, S_DIV, S_NEG, S_EXP, S_LOG, S_SQRT, S_SIN, S_COS, S_ABS, S_SELECT,
-    // two independent scalar binary ops in one instruction: sub-ops (0 add,
-    // 1 sub, 2 mul, 3 div) in w0 bits 8-11 and 12-15; w1..w3 = d1, a1, b1,
-    // w4..w6 = d2, a2, b2
-    F2 = 108,
-    // two scalar adjoint rules (sub-ops 0 add, 1 sub, 2 mul, 3 div) with
-    // 16-bit fields: w1 = g1 | a1 << 16, w2 = b1 | z1 << 16,
-    // w3 = ta1 | tb1 << 16, w4..w6 the same for the second rule; a target
-    // field is a register below 2^15 with bit 15 = first contribution
-    R2 = 109,
     SR_ADD = 112, SR_SUB, SR_MUL, SR_DIV, SR_NEG, SR_EXP, SR_LOG, SR_SQRT, SR_SIN, SR_COS, SR_ABS,
     SR_SELECT,
+
+    // Bundles: N = 1..3 independent scalar ops or adjoint rules in one
+    // instruction, each a run of 16-bit register fields (field i < 14 is half
+    // i & 1 of word 1 + i / 2, field 14 the high half of w0).  A target field
+    // holds a register below 2^15 with bit 15 set on the first contribution.
+    // Sums, differences, products and negations all become one fused
+    // multiply-add against the constant registers 1, -1 and -0, which gives
+    // the same bits as the plain operation:
+    //   a + b = fma(a, 1, b)   a - b = fma(b, -1, a)   a * b = fma(a, b, -0)
+    //   -a = fma(a, -1, -0)
+    FB1 = 128, FB2, FB3,      // fields (d, x, y, w) per op: d = fma(x, y, w)
+    DB1, DB2, DB3,            // fields (d, a, b) per op: d = a / b
+    // linear adjoint rules, fields (g, ya, yb, ta, tb): ta += g * ya,
+    // tb += g * yb, gated on g != 0 (add: 1, 1; sub: 1, -1; mul: b, a;
+    // neg: -1 with tb the sink; exp: z with tb the sink)
+    LB1, LB2, LB3,
+    // division adjoint rules, fields (g, b, z, ta, tb): ta += g / b,
+    // tb += -((g * z) / b), gated on g != 0
+    RDB1, RDB2, RDB3,
+    // the same with targets that may repeat (x * x, or two rules feeding one
+    // adjoint): each target is read after the previous rule has written it
+    LBS1, LBS2, LBS3, RDBS1, RDBS2, RDBS3,
     OP_COUNT
 };
 
@@ -67,7 +82,14 @@ constexpr uint32_t kIndexMask = (1u << 30) - 1;
 constexpr uint32_t kInit = 0x80000000u;
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 constexpr uint32_t kWords = 8;
-constexpr uint32_t kR2MaxReg = 1u << 15;   // registers addressable by R2 fields
+// The program is fetched in chunks of 32 instructions (one 16-byte load per
+// thread of a wave).  Its END is the first instruction of a chunk (NOPs pad
+// the chunk before), and one more chunk of END follows, which the fetch reads
+// ahead; so the replay loop tests for END once per chunk.
+constexpr uint32_t kChunkInstr = 32;
+constexpr uint32_t kChunkWords = kChunkInstr * kWords;
+constexpr uint32_t kFieldMaxReg = 1u << 15;   // registers addressable by bundle fields
+constexpr uint32_t kFieldInit = 0x8000u;
 
 inline uint32_t w0(uint32_t op, uint32_t mode, uint32_t nel) { return op | (mode << 8) | (nel << 16); }
 inline uint32_t dims(uint32_t m, uint32_t k, uint32_t n) { return m | (k << 8) | (n << 16); }

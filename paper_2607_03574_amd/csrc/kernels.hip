@@ -2,9 +2,9 @@
 // lane (parameter vector) per GPU thread (Section 3.5: one structural walk,
 // numeric payloads widened over the batch axis).
 //
-// Every instruction is wave-uniform: the opcode and operand words come from
-// the device program by scalar loads, so all 64 lanes of a wave follow the
-// same control and branch only on uniform values; per-lane numeric branches
+// Every instruction is wave-uniform: the opcode and operand words of the
+// device program end up in scalar registers, so all 64 lanes of a wave follow
+// the same control and branch only on uniform values; per-lane numeric branches
 // were turned into selects by the trace producer.  Lane registers live in LDS
 // (register r of thread t at lds[r*64 + t], conflict-free 8-byte accesses)
 // and, beyond R_lds, in a lane-contiguous workspace area, so every global
@@ -45,36 +45,30 @@ struct DevCtx {
     bool active;
 
     __device__ __forceinline__ static uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
-    // Program words are wave-uniform.  They are read with vector loads from a
-    // uniform address (one request per wave) so that a load issued two
-    // instructions ahead is tracked by the in-order vmcnt counter and does not
-    // hold up the LDS waits of the instructions in between.
+    // Program chunks: thread t loads words 4t..4t+3 of a 32-instruction
+    // chunk (one coalesced 1 KiB load per wave), so instruction i lies in
+    // threads 2i (words 0-3) and 2i+1 (words 4-7) and v_readlane moves its
+    // words into scalar registers.  The chunk in flight sits in registers
+    // that nothing reads until the whole current chunk has executed.
     typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-    struct Fetch {
-        u32x4 a, b;
+    using Chunk = u32x4;
+    __device__ __forceinline__ Chunk load_chunk(const uint32_t *p) const {
+        return ((const AS_GLOBAL u32x4 *)(p))[t];
+    }
+    struct Words {
+        Chunk ch;
+        int l0;
+        __device__ __forceinline__ uint32_t operator[](int k) const {
+            const int lane = l0 + (k >> 2);
+            switch (k & 3) {
+            case 0: return uint32_t(__builtin_amdgcn_readlane(int(ch.x), lane));
+            case 1: return uint32_t(__builtin_amdgcn_readlane(int(ch.y), lane));
+            case 2: return uint32_t(__builtin_amdgcn_readlane(int(ch.z), lane));
+            default: return uint32_t(__builtin_amdgcn_readlane(int(ch.w), lane));
+            }
+        }
     };
-    __device__ __forceinline__ static Fetch prefetch(const uint32_t *pc) {
-        const AS_GLOBAL u32x4 *p = (const AS_GLOBAL u32x4 *)(pc);
-        Fetch f;
-        f.a = p[0];
-        f.b = p[1];
-        return f;
-    }
-    __device__ __forceinline__ static void decode(const Fetch &f, uint32_t (&w)[8]) {
-        // keep the words in vector registers up to this point, so no
-        // conversion to scalars (which waits for the load) is hoisted up to
-        // the prefetch
-        u32x4 a = f.a, b = f.b;
-        asm volatile("" : "+v"(a), "+v"(b));
-        w[0] = a.x;
-        w[1] = a.y;
-        w[2] = a.z;
-        w[3] = a.w;
-        w[4] = b.x;
-        w[5] = b.y;
-        w[6] = b.z;
-        w[7] = b.w;
-    }
+    __device__ __forceinline__ static Words instr(const Chunk &ch, uint32_t i) { return Words{ch, int(2 * i)}; }
     __device__ __forceinline__ static uint32_t aux_word(const uint32_t *aux, uint32_t i) {
         return ((const AS_CONST uint32_t *)(aux))[i];
     }

@@ -6,7 +6,8 @@
 //   double ld_raw(uint32_t r) const;   (a read whose value may be discarded)
 //   double konst(uint32_t i) const;  double obsv(uint32_t i) const;  (uniform loads)
 //   static uint32_t uni(uint32_t x);          (wave-uniform value)
-//   Fetch prefetch(const uint32_t *pc);  void decode(const Fetch&, uint32_t (&w)[8]);
+//   Chunk load_chunk(const uint32_t *p) const;   (kChunkInstr instructions)
+//   static Words instr(const Chunk&, uint32_t i);  (instruction i; Words[k] = word k, uniform)
 //   double param(uint32_t p) const;  void store_loss(double) const;
 //   void store_grad(uint32_t p, double) const;
 //   void ckpt_st(uint32_t row, double) const;  double ckpt_ld(uint32_t row) const;
@@ -466,153 +467,79 @@ NDVM_HD void acc1(const C &c, uint32_t tw, double x, bool on) {
     c.st(r, on ? base + x : base);
 }
 
-// Scalar handlers without any data-dependent control flow inside: kept in a
-// switch of their own so the compiler can leave that region's uniform
-// branches unstructured (a direct jump back to the dispatch).
-constexpr uint32_t kHotMask =
-    (1u << (S_ADD - S_ADD)) | (1u << (S_SUB - S_ADD)) | (1u << (S_MUL - S_ADD)) | (1u << (S_DIV - S_ADD)) |
-    (1u << (S_NEG - S_ADD)) | (1u << (S_ABS - S_ADD)) | (1u << (S_SELECT - S_ADD)) | (1u << (F2 - S_ADD)) | (1u << (R2 - S_ADD)) |
-    (1u << (SR_ADD - S_ADD)) | (1u << (SR_SUB - S_ADD)) | (1u << (SR_MUL - S_ADD)) |
-    (1u << (SR_DIV - S_ADD)) | (1u << (SR_NEG - S_ADD)) | (1u << (SR_EXP - S_ADD)) |
-    (1u << (SR_LOG - S_ADD)) | (1u << (SR_SQRT - S_ADD)) | (1u << (SR_ABS - S_ADD)) |
-    (1u << (SR_SELECT - S_ADD));
-
-// scalar binary op selected by a wave-uniform sub-op code
-NDVM_HD double binop(uint32_t sub, double a, double b) {
-    switch (sub) {
-    case 0: return a + b;
-    case 1: return a - b;
-    case 2: return a * b;
-    default: return a / b;
-    }
+// 16-bit field i of a bundle instruction
+template <class W>
+NDVM_HD uint32_t fld(const W &w, int i) {
+    return i == 14 ? (w[0] >> 16) : ((w[1 + (i >> 1)] >> ((i & 1) * 16)) & 0xFFFFu);
 }
 
-// contributions of one scalar binary adjoint rule (sub-op as in binop)
-template <class C>
-NDVM_HD void rev_binop(const C &c, uint32_t sub, uint32_t wg, uint32_t wa, uint32_t wb, uint32_t wz,
-                       uint32_t ta, uint32_t tb) {
-    const double g = c.ld(wg);
-    const bool nz = g != 0.0;
-    switch (sub) {
-    case 0:
-        acc1(c, ta, g, nz);
-        acc1(c, tb, g, nz);
-        return;
-    case 1:
-        acc1(c, ta, g, nz);
-        acc1(c, tb, -g, nz);
-        return;
-    case 2: {
-        const double a = c.ld(wa), b = c.ld(wb);
-        acc1(c, ta, g * b, nz);
-        acc1(c, tb, g * a, nz);
-        return;
+// d = fma(x, y, w) for N independent ops; all operands are read before any
+// result is written (the scheduler never bundles an op with one it reads)
+template <int N, class C, class W>
+NDVM_HD void fma_bundle(const C &c, const W &w) {
+    double x[N], y[N], z[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        x[k] = c.ld(fld(w, 4 * k + 1));
+        y[k] = c.ld(fld(w, 4 * k + 2));
+        z[k] = c.ld(fld(w, 4 * k + 3));
     }
-    default: {
-        const double b = c.ld(wb), z = c.ld(wz);
-        acc1(c, ta, g / b, nz);
-        acc1(c, tb, -((g * z) / b), nz);
-        return;
-    }
-    }
+#pragma unroll
+    for (int k = 0; k < N; ++k) c.st(fld(w, 4 * k), fma(x[k], y[k], z[k]));
 }
 
-// a 16-bit target field as a target word
-NDVM_HD uint32_t t16(uint32_t f) { return (f & 0x7FFFu) | ((f & 0x8000u) << 16); }
+template <int N, class C, class W>
+NDVM_HD void div_bundle(const C &c, const W &w) {
+    double a[N], b[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        a[k] = c.ld(fld(w, 3 * k + 1));
+        b[k] = c.ld(fld(w, 3 * k + 2));
+    }
+#pragma unroll
+    for (int k = 0; k < N; ++k) c.st(fld(w, 3 * k), a[k] / b[k]);
+}
 
-template <class C>
-NDVM_HD void exec_hot(const C &c, const uint32_t *w, uint32_t op) {
-    switch (op) {
-    case R2: {
-        const uint32_t h = C::uni(w[0]);
-        rev_binop(c, (h >> 8) & 15u, w[1] & 0xFFFFu, w[1] >> 16, w[2] & 0xFFFFu, w[2] >> 16,
-                  t16(w[3] & 0xFFFFu), t16(w[3] >> 16));
-        rev_binop(c, (h >> 12) & 15u, w[4] & 0xFFFFu, w[4] >> 16, w[5] & 0xFFFFu, w[5] >> 16,
-                  t16(w[6] & 0xFFFFu), t16(w[6] >> 16));
-        return;
+// adjoint rules of N bundled ops (kDiv: division rule, else linear).  Every
+// g and operand is read first.  With distinct targets (!kSeq) every target is
+// read before any is written; otherwise each target is read just before it is
+// written, after the earlier rules' updates (LDS accesses of a wave are
+// performed in order).
+template <int N, bool kDiv, bool kSeq, class C, class W>
+NDVM_HD void adj_bundle(const C &c, const W &w) {
+    double g[N], p[N], q[N], xa[N], xb[N], oa[N], ob[N];
+    uint32_t ta[N], tb[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        g[k] = c.ld(fld(w, 5 * k));
+        p[k] = c.ld(fld(w, 5 * k + 1));
+        q[k] = c.ld(fld(w, 5 * k + 2));
+        ta[k] = fld(w, 5 * k + 3);
+        tb[k] = fld(w, 5 * k + 4);
+        if (!kSeq) {
+            oa[k] = c.ld_raw(ta[k] & ~kFieldInit);   // may be unset on a first contribution
+            ob[k] = c.ld_raw(tb[k] & ~kFieldInit);
+        }
     }
-    case F2: {
-        const uint32_t h = C::uni(w[0]);
-        const double a1 = c.ld(w[2]), b1 = c.ld(w[3]), a2 = c.ld(w[5]), b2 = c.ld(w[6]);
-        c.st(w[1], binop((h >> 8) & 15u, a1, b1));
-        c.st(w[4], binop((h >> 12) & 15u, a2, b2));
-        return;
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        if (kDiv) {
+            xa[k] = g[k] / p[k];
+            xb[k] = -((g[k] * q[k]) / p[k]);
+        } else {
+            xa[k] = g[k] * p[k];
+            xb[k] = g[k] * q[k];
+        }
     }
-    case S_ADD: c.st(w[1], c.ld(w[2]) + c.ld(w[3])); return;
-    case S_SUB: c.st(w[1], c.ld(w[2]) - c.ld(w[3])); return;
-    case S_MUL: c.st(w[1], c.ld(w[2]) * c.ld(w[3])); return;
-    case S_DIV: c.st(w[1], c.ld(w[2]) / c.ld(w[3])); return;
-    case S_NEG: c.st(w[1], -c.ld(w[2])); return;
-    case S_ABS: c.st(w[1], fabs(c.ld(w[2]))); return;
-    case S_SELECT: {
-        const bool p = c.ld(w[2]) < c.ld(w[3]);
-        const double x = c.ld(w[4]), y = c.ld(w[5]);
-        c.st(w[1], p ? x : y);
-        return;
-    }
-    case SR_ADD: {
-        const double g = c.ld(w[1]);
-        const bool nz = g != 0.0;
-        acc1(c, w[5], g, nz);
-        acc1(c, w[6], g, nz);
-        return;
-    }
-    case SR_SUB: {
-        const double g = c.ld(w[1]);
-        const bool nz = g != 0.0;
-        acc1(c, w[5], g, nz);
-        acc1(c, w[6], -g, nz);
-        return;
-    }
-    case SR_MUL: {
-        const double g = c.ld(w[1]), a = c.ld(w[2]), b = c.ld(w[3]);
-        const bool nz = g != 0.0;
-        acc1(c, w[5], g * b, nz);
-        acc1(c, w[6], g * a, nz);
-        return;
-    }
-    case SR_DIV: {
-        const double g = c.ld(w[1]), b = c.ld(w[3]), z = c.ld(w[4]);
-        const bool nz = g != 0.0;
-        acc1(c, w[5], g / b, nz);
-        acc1(c, w[6], -((g * z) / b), nz);
-        return;
-    }
-    case SR_NEG: {
-        const double g = c.ld(w[1]);
-        acc1(c, w[5], -g, g != 0.0);
-        return;
-    }
-    case SR_EXP: {
-        const double g = c.ld(w[1]);
-        acc1(c, w[5], g * c.ld(w[4]), g != 0.0);
-        return;
-    }
-    case SR_LOG: {
-        const double g = c.ld(w[1]), a = c.ld(w[2]);
-        acc1(c, w[5], g / a, g != 0.0 && a > 1e-8);
-        return;
-    }
-    case SR_SQRT: {
-        const double g = c.ld(w[1]), a = c.ld(w[2]);
-        acc1(c, w[5], g / (2.0 * c.ld(w[4])), g != 0.0 && a > 1e-8);
-        return;
-    }
-    case SR_ABS: {
-        const double g = c.ld(w[1]), a = c.ld(w[2]);
-        acc1(c, w[5], a > 0.0 ? g : (a < 0.0 ? -g : 0.0), g != 0.0);
-        return;
-    }
-    case SR_SELECT: {
-        const double g = c.ld(w[1]);
-        const bool nz = g != 0.0;
-        const bool p = c.ld(w[2]) < c.ld(w[3]);
-        acc1(c, w[5], g, nz && p);
-        acc1(c, w[6], g, nz && !p);
-        return;
-    }
-    default:
-        return;
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        const bool nz = g[k] != 0.0;
+        if (kSeq) oa[k] = c.ld_raw(ta[k] & ~kFieldInit);
+        const double ba = (ta[k] & kFieldInit) ? 0.0 : oa[k];
+        c.st(ta[k] & ~kFieldInit, nz ? ba + xa[k] : ba);
+        if (kSeq) ob[k] = c.ld_raw(tb[k] & ~kFieldInit);
+        const double bb = (tb[k] & kFieldInit) ? 0.0 : ob[k];
+        c.st(tb[k] & ~kFieldInit, nz ? bb + xb[k] : bb);
     }
 }
 
@@ -642,36 +569,25 @@ NDVM_HD void exec_scalar(const C &c, const uint32_t *w) {
     }
 }
 
-// Execute one instruction; false at END.  `wv` are the instruction words as
-// loaded (on the GPU: vector registers holding the same value in every
-// lane); the hot scalar handlers use them directly as LDS addresses, all
-// other paths first make every word an explicit scalar.
+// Everything but END and the scalar/bundle fast paths: generic element
+// loops, scalar transcendentals, parameter, constant, observation, checkpoint
+// and gradient traffic.
 template <class C>
-NDVM_HD bool step(const C &c, const uint32_t *wv, const uint32_t *aux) {
-    const uint32_t op = C::uni(wv[0]) & 0xFF;
-    if (op >= S_ADD && ((kHotMask >> (op - S_ADD)) & 1u)) {
-        exec_hot(c, wv, op);
-        return true;
-    }
-    uint32_t w[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) w[i] = C::uni(wv[i]);
+NDVM_HD void exec_cold(const C &c, const uint32_t *w, uint32_t op, const uint32_t *aux) {
     if (op >= S_ADD) {
         exec_scalar(c, w);
-        return true;
+        return;
     }
     if (op >= R_ADD) {
         exec_rev(c, aux, w);
-        return true;
+        return;
     }
     if (op >= F_ADD) {
         exec_fwd(c, aux, w);
-        return true;
+        return;
     }
     const uint32_t n = (w[0] >> 16) & 0xFF;
     switch (op) {
-    case END:
-        return false;
     case LDPARAM:
         c.st(w[1], c.param(w[7]));
         break;
@@ -700,24 +616,130 @@ NDVM_HD bool step(const C &c, const uint32_t *wv, const uint32_t *aux) {
         for (uint32_t i = 0; i < n; ++i) c.st(w[1] + i, c.konst(w[7] + i));
         break;
     default:
-        return false;
+        break;
     }
-    return true;
 }
 
-// Execute a device program from `pc` until END.  Instructions are fetched two
-// ahead (programs end with padding instructions of END so the look-ahead stays
-// inside the program).
+// Execute a device program until END.  One flat switch over the opcodes in
+// a loop without exits, so every handler jumps straight back to the fetch.  `wv[k]` is word k of the
+// current instruction (wave-uniform); handlers read only the words they use.
+// The chunk after the current one is loaded when the current one starts, so
+// it has a whole chunk's worth of instructions to arrive (programs are padded
+// so this read-ahead stays inside the program).
 template <class C>
-NDVM_HD void run(const C &c, const uint32_t *pc, const uint32_t *aux) {
-    typename C::Fetch f0 = C::prefetch(pc), f1 = C::prefetch(pc + kWords);
-    for (;; pc += kWords) {
-        typename C::Fetch f2 = C::prefetch(pc + 2 * kWords);
-        uint32_t wv[8];
-        C::decode(f0, wv);
-        if (!step(c, wv, aux)) return;
-        f0 = f1;
-        f1 = f2;
+NDVM_HD void run(const C &c, const uint32_t *prog, const uint32_t *aux) {
+    typename C::Chunk cur = c.load_chunk(prog), nxt = c.load_chunk(prog + kChunkWords);
+    for (const uint32_t *ahead = prog + 2 * kChunkWords;; ahead += kChunkWords) {
+    // END only ever opens a chunk; the chunk registers change only below,
+    // outside the per-instruction loop, which has no exit of its own
+    if ((C::instr(cur, 0)[0] & 0xFF) == END) return;
+    for (uint32_t i = 0; i < kChunkInstr; ++i) {
+        const auto w = C::instr(cur, i);
+        const uint32_t op = w[0] & 0xFF;
+        switch (op) {
+        case END: case NOP: break;
+        case FB1: fma_bundle<1>(c, w); break;
+        case FB2: fma_bundle<2>(c, w); break;
+        case FB3: fma_bundle<3>(c, w); break;
+        case DB1: div_bundle<1>(c, w); break;
+        case DB2: div_bundle<2>(c, w); break;
+        case DB3: div_bundle<3>(c, w); break;
+        case LB1: adj_bundle<1, false, false>(c, w); break;
+        case LB2: adj_bundle<2, false, false>(c, w); break;
+        case LB3: adj_bundle<3, false, false>(c, w); break;
+        case RDB1: adj_bundle<1, true, false>(c, w); break;
+        case RDB2: adj_bundle<2, true, false>(c, w); break;
+        case RDB3: adj_bundle<3, true, false>(c, w); break;
+        case LBS1: adj_bundle<1, false, true>(c, w); break;
+        case LBS2: adj_bundle<2, false, true>(c, w); break;
+        case LBS3: adj_bundle<3, false, true>(c, w); break;
+        case RDBS1: adj_bundle<1, true, true>(c, w); break;
+        case RDBS2: adj_bundle<2, true, true>(c, w); break;
+        case RDBS3: adj_bundle<3, true, true>(c, w); break;
+        case S_ADD: c.st(w[1], c.ld(w[2]) + c.ld(w[3])); break;
+        case S_SUB: c.st(w[1], c.ld(w[2]) - c.ld(w[3])); break;
+        case S_MUL: c.st(w[1], c.ld(w[2]) * c.ld(w[3])); break;
+        case S_DIV: c.st(w[1], c.ld(w[2]) / c.ld(w[3])); break;
+        case S_NEG: c.st(w[1], -c.ld(w[2])); break;
+        case S_ABS: c.st(w[1], fabs(c.ld(w[2]))); break;
+        case S_SELECT: {
+            const bool p = c.ld(w[2]) < c.ld(w[3]);
+            const double x = c.ld(w[4]), y = c.ld(w[5]);
+            c.st(w[1], p ? x : y);
+            break;
+        }
+        case SR_ADD: {
+            const double g = c.ld(w[1]);
+            const bool nz = g != 0.0;
+            acc1(c, w[5], g, nz);
+            acc1(c, w[6], g, nz);
+            break;
+        }
+        case SR_SUB: {
+            const double g = c.ld(w[1]);
+            const bool nz = g != 0.0;
+            acc1(c, w[5], g, nz);
+            acc1(c, w[6], -g, nz);
+            break;
+        }
+        case SR_MUL: {
+            const double g = c.ld(w[1]), a = c.ld(w[2]), b = c.ld(w[3]);
+            const bool nz = g != 0.0;
+            acc1(c, w[5], g * b, nz);
+            acc1(c, w[6], g * a, nz);
+            break;
+        }
+        case SR_DIV: {
+            const double g = c.ld(w[1]), b = c.ld(w[3]), z = c.ld(w[4]);
+            const bool nz = g != 0.0;
+            acc1(c, w[5], g / b, nz);
+            acc1(c, w[6], -((g * z) / b), nz);
+            break;
+        }
+        case SR_NEG: {
+            const double g = c.ld(w[1]);
+            acc1(c, w[5], -g, g != 0.0);
+            break;
+        }
+        case SR_EXP: {
+            const double g = c.ld(w[1]);
+            acc1(c, w[5], g * c.ld(w[4]), g != 0.0);
+            break;
+        }
+        case SR_LOG: {
+            const double g = c.ld(w[1]), a = c.ld(w[2]);
+            acc1(c, w[5], g / a, g != 0.0 && a > 1e-8);
+            break;
+        }
+        case SR_SQRT: {
+            const double g = c.ld(w[1]), a = c.ld(w[2]);
+            acc1(c, w[5], g / (2.0 * c.ld(w[4])), g != 0.0 && a > 1e-8);
+            break;
+        }
+        case SR_ABS: {
+            const double g = c.ld(w[1]), a = c.ld(w[2]);
+            acc1(c, w[5], a > 0.0 ? g : (a < 0.0 ? -g : 0.0), g != 0.0);
+            break;
+        }
+        case SR_SELECT: {
+            const double g = c.ld(w[1]);
+            const bool nz = g != 0.0;
+            const bool p = c.ld(w[2]) < c.ld(w[3]);
+            acc1(c, w[5], g, nz && p);
+            acc1(c, w[6], g, nz && !p);
+            break;
+        }
+        default: {
+            uint32_t wc[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) wc[k] = w[k];
+            exec_cold(c, wc, op, aux);
+            break;
+        }
+        }
+    }
+        cur = nxt;
+        nxt = c.load_chunk(ahead);
     }
 }
 

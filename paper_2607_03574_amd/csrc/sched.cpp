@@ -216,13 +216,17 @@ uint32_t fwd_opcode(uint16_t c) {
 
 // ------------------------------------------------------------------ builder
 // Abstract instruction before register assignment.
-enum RIKind : uint8_t { I_LDP, I_LDC, I_CKST, I_FWD, I_FWD2, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_REV2,
-                        I_STG };
+enum RIKind : uint8_t { I_LDP, I_LDC, I_CKST, I_FWD, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_STG };
 struct AI {
     uint8_t kind;
     uint32_t k;   // slot / param index
     uint32_t j;   // segment (reverse phase) or checkpoint row
-    uint32_t k2;  // second op of a dual instruction (I_FWD2)
+    uint8_t nb = 0;          // further ops bundled with k (I_FWD, I_REV)
+    bool seq = false;        // reverse bundle whose rules' targets may repeat
+    uint32_t kb[2] = {0, 0};
+    // the ops of a forward or reverse instruction
+    uint32_t nops() const { return 1u + nb; }
+    uint32_t op(uint32_t i) const { return i == 0 ? k : kb[i - 1]; }
 };
 
 struct Builder {
@@ -344,27 +348,38 @@ struct Builder {
     }
 };
 
-// scalar binary ops that may share a dual instruction, and their sub-op code
-int dual_sub(const Info &I, uint32_t k) {
+// Bundle class of a scalar op in the forward program: 1 fused multiply-add
+// form (add, sub, mul, neg), 2 division, 0 none.
+int fwd_class(const Info &I, uint32_t k) {
     const TapeOp &o = I.t.ops[k];
-    if (I.kind[k] != K_COMP || I.nel[k] != 1) return -1;
+    if (I.kind[k] != K_COMP || I.nel[k] != 1 || I.nel[o.a] != 1) return 0;
     switch (o.code) {
-    case tp::ADD: return 0;
-    case tp::SUB: return 1;
-    case tp::MUL: return 2;
-    case tp::DIV: return 3;
+    case tp::ADD: case tp::SUB: case tp::MUL: case tp::NEG: return 1;
+    case tp::DIV: return 2;
     }
-    return -1;
+    return 0;
 }
+// Bundle class of a scalar op's adjoint rule: 1 linear (add, sub, mul, neg,
+// exp), 2 division, 0 none.
+int rev_class(const Info &I, uint32_t k) {
+    const TapeOp &o = I.t.ops[k];
+    if (I.kind[k] != K_COMP || I.nel[k] != 1 || I.nel[o.a] != 1) return 0;
+    switch (o.code) {
+    case tp::ADD: case tp::SUB: case tp::MUL: case tp::NEG: case tp::EXP: return 1;
+    case tp::DIV: return 2;
+    }
+    return 0;
+}
+constexpr uint32_t kBundleMax = 3;
+constexpr uint32_t kBundleWindow = 24;
 
-// Reorder each run of forward instructions (list scheduling, earliest op
-// first, data dependences kept) and merge independent scalar binary ops into
-// dual instructions.  Every op still computes exactly what it computed
-// before, so results are unchanged bit for bit.
-std::vector<AI> pair_forward(const Info &I, const std::vector<AI> &in) {
+// Reorder each run of forward instructions (list scheduling, earliest ready
+// op first, data dependences kept) and bundle up to kBundleMax independent
+// scalar ops of one class into one instruction.  Every op still computes
+// exactly what it computed before, so results are unchanged bit for bit.
+std::vector<AI> bundle_forward(const Info &I, const std::vector<AI> &in) {
     std::vector<AI> out;
     out.reserve(in.size());
-    const uint32_t kWindow = 24;
     size_t i = 0;
     std::vector<uint32_t> pos_of(I.N, UINT32_MAX);
     while (i < in.size()) {
@@ -404,27 +419,26 @@ std::vector<AI> pair_forward(const Info &I, const std::vector<AI> &in) {
             while (done[first]) ++first;
             uint32_t x = first;
             while (pending[x] != 0) ++x;         // earliest ready op
-            int sx = dual_sub(I, in[i + x].k);
-            int32_t y = -1;
-            if (sx >= 0)
-                for (uint32_t r = x + 1; r < n && r < x + kWindow; ++r)
-                    if (!done[r] && pending[r] == 0 && dual_sub(I, in[i + r].k) >= 0) {
-                        y = int32_t(r);
-                        break;
+            // a ready observation load in the window goes first: it is cheap
+            // and makes its users ready to be bundled
+            for (uint32_t r = x; r < n && r < x + kBundleWindow; ++r)
+                if (!done[r] && pending[r] == 0 && I.kind[in[i + r].k] == K_OBS) {
+                    x = r;
+                    break;
+                }
+            AI a = in[i + x];
+            const int cls = fwd_class(I, a.k);
+            if (cls)
+                for (uint32_t r = x + 1; r < n && r < x + kBundleWindow && a.nb + 1 < kBundleMax; ++r)
+                    if (!done[r] && pending[r] == 0 && fwd_class(I, in[i + r].k) == cls) {
+                        a.kb[a.nb++] = in[i + r].k;
+                        done[r] = 2;             // taken; retired with the bundle
                     }
-            if (y >= 0) {
-                AI a = in[i + x];
-                a.kind = I_FWD2;
-                a.k2 = in[i + y].k;
-                out.push_back(a);
-                retire(x);
-                retire(uint32_t(y));
-                emitted += 2;
-            } else {
-                out.push_back(in[i + x]);
-                retire(x);
-                emitted += 1;
-            }
+            retire(x);
+            for (uint32_t r = x + 1; r < n && r < x + kBundleWindow; ++r)
+                if (done[r] == 2) retire(r);
+            out.push_back(a);
+            emitted += a.nops();
         }
         for (uint32_t q = 0; q < n; ++q) pos_of[in[i + q].k] = UINT32_MAX;
         i = e;
@@ -432,15 +446,17 @@ std::vector<AI> pair_forward(const Info &I, const std::vector<AI> &in) {
     return out;
 }
 
-// Pair scalar adjoint rules of each run of reverse instructions.  An op may be
-// hoisted next to an earlier one only when its own adjoint is complete (every
-// op contributing to it has been emitted) and no op it jumps over touches any
-// of its targets; so every adjoint still receives its contributions in the
-// same order and the results are unchanged bit for bit.
-std::vector<AI> pair_reverse(const Info &I, const std::vector<AI> &in) {
+// Bundle scalar adjoint rules of each run of reverse instructions.  An op may
+// be hoisted next to an earlier one only when its own adjoint is complete
+// (every op contributing to it has been emitted) and no op it jumps over
+// touches any of its targets; so every adjoint still receives its
+// contributions in the same order and the results are unchanged bit for
+// bit.  Within a bundle the rules are applied in their original order; a
+// bundle whose targets repeat (x * x, or two rules feeding one adjoint) is
+// marked sequential, the others let the handler read every target first.
+std::vector<AI> bundle_reverse(const Info &I, const std::vector<AI> &in) {
     std::vector<AI> out;
     out.reserve(in.size());
-    const uint32_t kWindow = 24;
     auto tid = [&](uint32_t s) -> int64_t {   // adjoint identity of a target, -1 if none
         if (I.kind[s] == K_PARAM) return int64_t(I.N) + I.t.ops[s].imm;
         if (I.kind[s] == K_COMP && I.active[s]) return s;
@@ -456,11 +472,14 @@ std::vector<AI> pair_reverse(const Info &I, const std::vector<AI> &in) {
         while (e < in.size() && in[e].kind == I_REV && in[e].j == in[i].j) ++e;
         const uint32_t n = uint32_t(e - i);
         std::vector<std::vector<int64_t>> T(n);
+        std::vector<uint8_t> self_clash(n, 0);
         std::unordered_map<int64_t, std::vector<uint32_t>> by_target;
         for (uint32_t q = 0; q < n; ++q) {
             I.for_targets(in[i + q].k, [&](uint32_t s) {
                 int64_t id = tid(s);
-                if (id >= 0) T[q].push_back(id);
+                if (id < 0) return;
+                for (int64_t x : T[q]) self_clash[q] = self_clash[q] || x == id;
+                T[q].push_back(id);
             });
             for (int64_t id : T[q]) by_target[id].push_back(q);
         }
@@ -477,44 +496,45 @@ std::vector<AI> pair_reverse(const Info &I, const std::vector<AI> &in) {
             for (int64_t id : T[q]) {
                 if (id >= int64_t(I.N)) continue;
                 // ops in this run whose output is `id` lose one pending contributor
-                for (uint32_t r = q + 1; r < n && r < q + 4 * kWindow; ++r)
+                for (uint32_t r = q + 1; r < n && r < q + 4 * kBundleWindow; ++r)
                     if (int64_t(in[i + r].k) == id && pend[r] > 0) pend[r]--;
             }
         };
+        auto clashes = [&](uint32_t r, const std::vector<int64_t> &ids) {
+            for (int64_t id : T[r])
+                for (int64_t x : ids)
+                    if (id == x) return true;
+            return false;
+        };
         uint32_t first = 0;
-        std::vector<int64_t> skipped;
+        std::vector<int64_t> skipped, taken;
         for (uint32_t emitted = 0; emitted < n;) {
             while (done[first]) ++first;
             const uint32_t x = first;
-            int32_t y = -1;
-            if (dual_sub(I, in[i + x].k) >= 0) {
+            AI a = in[i + x];
+            const int cls = rev_class(I, a.k);
+            uint32_t picked[kBundleMax - 1];
+            a.seq = self_clash[x];
+            if (cls) {
                 skipped.clear();
-                for (uint32_t r = x + 1; r < n && r < x + kWindow; ++r) {
+                taken.assign(T[x].begin(), T[x].end());
+                for (uint32_t r = x + 1; r < n && r < x + kBundleWindow && a.nb + 1 < kBundleMax; ++r) {
                     if (done[r]) continue;
-                    bool clash = false;
-                    for (int64_t id : T[r])
-                        for (int64_t sid : skipped) clash = clash || id == sid;
-                    if (!clash && pend[r] == 0 && dual_sub(I, in[i + r].k) >= 0) {
-                        y = int32_t(r);
-                        break;
+                    if (pend[r] == 0 && rev_class(I, in[i + r].k) == cls && !clashes(r, skipped)) {
+                        a.seq = a.seq || self_clash[r] || clashes(r, taken);
+                        picked[a.nb] = r;
+                        a.kb[a.nb++] = in[i + r].k;
+                        taken.insert(taken.end(), T[r].begin(), T[r].end());
+                        continue;
                     }
                     skipped.insert(skipped.end(), T[r].begin(), T[r].end());
                     skipped.push_back(int64_t(in[i + r].k));
                 }
             }
-            if (y >= 0) {
-                AI a = in[i + x];
-                a.kind = I_REV2;
-                a.k2 = in[i + y].k;
-                out.push_back(a);
-                retire(x);
-                retire(uint32_t(y));
-                emitted += 2;
-            } else {
-                out.push_back(in[i + x]);
-                retire(x);
-                emitted += 1;
-            }
+            out.push_back(a);
+            retire(x);
+            for (uint32_t b = 0; b < a.nb; ++b) retire(picked[b]);
+            emitted += a.nops();
         }
         i = e;
     }
@@ -530,6 +550,16 @@ struct Emitter {
     }
 };
 
+// Terminate the program: NOPs up to the next fetch chunk, a chunk of END,
+// and the chunk the fetch reads ahead (also END).
+void finish(Emitter &E, Schedule &S) {
+    while (E.code.size() % isa::kChunkWords) E.put(isa::w0(isa::NOP, 0, 0));
+    S.n_instr = E.code.size() / isa::kWords + 1;   // through the END
+    for (uint32_t i = 0; i < 2 * isa::kChunkInstr; ++i) E.put(isa::w0(isa::END, 0, 0));
+    S.code = std::move(E.code);
+    S.aux = std::move(E.aux);
+}
+
 // Build the forward phase (shared by both programs) and, for the gradient
 // program, the reverse phase; returns the schedule with registers assigned.
 Schedule build(const Info &I, Builder &B, bool with_grad) {
@@ -537,13 +567,19 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     const uint32_t N = I.N, P = I.P;
     // static registers: param values, param adjoints, a sink for adjoint
     // contributions nobody needs, the constant pool, residents
-    const uint32_t nc = uint32_t(t.consts.size());
+    // the pool holds the tape's constants, then 1, -1 and -0 for bundles
+    const uint32_t nt = uint32_t(t.consts.size()), nc = nt + 3;
     const uint32_t kSink = 2 * P, kConst0 = 2 * P + 1;
+    const uint32_t kOne = kConst0 + nt, kMinusOne = kOne + 1, kNegZero = kOne + 2;
     const uint32_t kStatic = 2 * P + 1 + nc + B.res_elems;
     const uint32_t m = uint32_t(B.cuts.size());
     Schedule S;
     S.n_segments = with_grad ? m : 1;
     S.static_regs = kStatic;
+    S.consts = t.consts;
+    S.consts.push_back(1.0);
+    S.consts.push_back(-1.0);
+    S.consts.push_back(-0.0);
 
     // ---- forward phase: abstract instructions + value intervals
     std::vector<AI> fa;
@@ -571,7 +607,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         if (B.comp_live(k) || (I.kind[k] == K_OBS && I.live[k])) fa.push_back({I_FWD, k, 0});
     }
     fa.push_back({I_STLOSS, t.loss, 0});
-    fa = pair_forward(I, fa);
+    fa = bundle_forward(I, fa);
     // intervals for forward values
     std::vector<Interval> fiv;
     std::vector<int32_t> fiv_of(N, -1);
@@ -580,10 +616,10 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         auto use = [&](uint32_t s) {
             if (fiv_of[s] >= 0) fiv[fiv_of[s]].end = std::max(fiv[fiv_of[s]].end, ti);
         };
-        if (a.kind == I_FWD || a.kind == I_FWD2) {
-            I.for_operands(a.k, use);
-            if (a.kind == I_FWD2) I.for_operands(a.k2, use);
-            for (uint32_t k : {a.k, a.kind == I_FWD2 ? a.k2 : a.k}) {
+        if (a.kind == I_FWD) {
+            for (uint32_t b = 0; b < a.nops(); ++b) I.for_operands(a.op(b), use);
+            for (uint32_t b = 0; b < a.nops(); ++b) {
+                const uint32_t k = a.op(b);
                 if (fiv_of[k] >= 0 || (with_grad && B.resident[k])) continue;
                 fiv_of[k] = int32_t(fiv.size());
                 fiv.push_back({ti, ti, I.nel[k], 0});
@@ -666,10 +702,45 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         }
     };
 
-    auto emit_dual = [&](uint32_t k1, uint32_t k2, auto operand) {
-        const TapeOp &o1 = t.ops[k1], &o2 = t.ops[k2];
-        uint32_t w = isa::F2 | (uint32_t(dual_sub(I, k1)) << 8) | (uint32_t(dual_sub(I, k2)) << 12) | (1u << 16);
-        E.put(w, operand(k1), operand(o1.a), operand(o1.b), operand(k2), operand(o2.a), operand(o2.b));
+    // a forward bundle: the fused multiply-add form of each op, or divisions;
+    // single ops (and bundles naming registers beyond the 16-bit fields) use
+    // the one-op instructions
+    auto emit_bundle = [&](const AI &a, auto operand) {
+        const uint32_t nb = a.nops();
+        const int cls = nb > 1 ? fwd_class(I, a.k) : 0;
+        uint32_t f[15] = {};
+        uint32_t nf = 0;
+        bool fits = cls != 0;
+        for (uint32_t b = 0; b < nb && fits; ++b) {
+            const uint32_t k = a.op(b);
+            const TapeOp &o = t.ops[k];
+            uint32_t x[4];
+            if (cls == 2) {
+                x[0] = operand(k); x[1] = operand(o.a); x[2] = operand(o.b);
+            } else {
+                switch (o.code) {
+                case tp::ADD: x[1] = operand(o.a); x[2] = kOne; x[3] = operand(o.b); break;
+                case tp::SUB: x[1] = operand(o.b); x[2] = kMinusOne; x[3] = operand(o.a); break;
+                case tp::MUL: x[1] = operand(o.a); x[2] = operand(o.b); x[3] = kNegZero; break;
+                default: x[1] = operand(o.a); x[2] = kMinusOne; x[3] = kNegZero; break;   // NEG
+                }
+                x[0] = operand(k);
+            }
+            for (uint32_t q = 0; q < (cls == 2 ? 3u : 4u); ++q) {
+                fits = fits && x[q] < isa::kFieldMaxReg;
+                f[nf++] = x[q];
+            }
+        }
+        if (!fits) {
+            for (uint32_t b = 0; b < nb; ++b) emit_fwd(a.op(b), operand, operand(a.op(b)));
+            return;
+        }
+        const uint32_t op = (cls == 2 ? isa::DB1 : isa::FB1) + nb - 1;
+        uint32_t w[8] = {op, 0, 0, 0, 0, 0, 0, 0};
+        for (uint32_t q = 0; q < nf; ++q) w[1 + q / 2] |= f[q] << (16 * (q & 1));
+        E.put(w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]);
+        S.n_bundles++;
+        S.n_bundled_ops += nb;
     };
     for (const AI &a : fa) {
         switch (a.kind) {
@@ -684,23 +755,15 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             break;
         }
         case I_FWD:
-            emit_fwd(a.k, fwd_operand, fwd_operand(a.k));
-            S.n_fwd_ops++;
-            break;
-        case I_FWD2:
-            emit_dual(a.k, a.k2, fwd_operand);
-            S.n_fwd_ops += 2;
-            S.n_dual++;
+            emit_bundle(a, fwd_operand);
+            S.n_fwd_ops += a.nops();
             break;
         case I_STLOSS: E.put(isa::w0(isa::ST_LOSS, 0, 1), 0, fwd_operand(a.k)); break;
         }
     }
     if (!with_grad) {
-        for (int pad = 0; pad < 3; ++pad) E.put(isa::w0(isa::END, 0, 0));   // END + look-ahead padding
         S.n_regs = kStatic + fhwm;
-        S.code = std::move(E.code);
-        S.aux = std::move(E.aux);
-        S.n_instr = S.code.size() / isa::kWords;
+        finish(E, S);
         return S;
     }
 
@@ -714,8 +777,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         for (uint32_t k : B.revops[j]) ra.push_back({I_REV, k, j});
     }
     for (uint32_t p = 0; p < P; ++p) ra.push_back({I_STG, p, 0});
-    ra = pair_forward(I, ra);
-    ra = pair_reverse(I, ra);
+    ra = bundle_forward(I, ra);
+    ra = bundle_reverse(I, ra);
 
     // value intervals keyed by (slot, segment); adjoint intervals keyed by slot
     std::vector<Interval> riv;
@@ -749,18 +812,17 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             riv.push_back({ti, ti, I.nel[s], 0});
             break;
         }
-        case I_FWD: case I_FWD2:
-            I.for_operands(a.k, [&](uint32_t s) { vuse(s, a.j, ti); });
-            if (a.kind == I_FWD2) I.for_operands(a.k2, [&](uint32_t s) { vuse(s, a.j, ti); });
-            val_of[key(a.k, a.j)] = uint32_t(riv.size());
-            riv.push_back({ti, ti, I.nel[a.k], 0});
-            if (a.kind == I_FWD2) {
-                val_of[key(a.k2, a.j)] = uint32_t(riv.size());
-                riv.push_back({ti, ti, I.nel[a.k2], 0});
+        case I_FWD:
+            for (uint32_t b = 0; b < a.nops(); ++b)
+                I.for_operands(a.op(b), [&](uint32_t s) { vuse(s, a.j, ti); });
+            for (uint32_t b = 0; b < a.nops(); ++b) {
+                val_of[key(a.op(b), a.j)] = uint32_t(riv.size());
+                riv.push_back({ti, ti, I.nel[a.op(b)], 0});
             }
             break;
-        case I_REV: case I_REV2: {
-            for (uint32_t k : {a.k, a.kind == I_REV2 ? a.k2 : a.k}) {
+        case I_REV: {
+            for (uint32_t b = 0; b < a.nops(); ++b) {
+                const uint32_t k = a.op(b);
                 I.for_revreads(k, [&](uint32_t s) { vuse(s, a.j, ti); });
                 I.for_targets(k, [&](uint32_t s) { contrib(s, ti); });
                 int32_t g = adj_of[k];
@@ -799,40 +861,11 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     auto target = target_word;
     auto adjreg = [&](uint32_t s) { return kStatic + riv[adj_of[s]].reg; };
 
-    for (const AI &a : ra) {
-        switch (a.kind) {
-        case I_ZEROP:
-            for (uint32_t p0 = 0; p0 < P; p0 += 16)
-                E.put(isa::w0(isa::ZERO, 0, std::min<uint32_t>(16, P - p0)), P + p0);
-            break;
-        case I_SEED:
-            if (I.kind[a.k] == K_PARAM || (I.kind[a.k] == K_COMP && I.active[a.k]))
-                E.put(isa::w0(isa::SEED, 0, 1), 0, 0, 0, 0, target(a.k));
-            break;
-        case I_CKLD: {
-            uint32_t s = B.livein[a.k][a.j];
-            uint32_t row = ckrow_base[a.k];
-            for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
-            E.put(isa::w0(isa::CKPT_LD, 0, I.nel[s]), rev_operand(s, a.k), 0, 0, 0, 0, 0, row);
-            S.ckpt_elems_loaded += I.nel[s];
-            break;
-        }
-        case I_FWD: {
-            auto opnd = [&](uint32_t s) { return rev_operand(s, a.j); };
-            emit_fwd(a.k, opnd, rev_operand(a.k, a.j));
-            S.n_recompute_ops++;
-            break;
-        }
-        case I_FWD2: {
-            auto opnd = [&](uint32_t s) { return rev_operand(s, a.j); };
-            emit_dual(a.k, a.k2, opnd);
-            S.n_recompute_ops += 2;
-            S.n_dual++;
-            break;
-        }
-        case I_REV: {
-            const TapeOp &o = t.ops[a.k];
-            uint32_t k = a.k, j = a.j, n = I.nel[k];
+    // one op's adjoint rule as a single instruction
+    auto emit_rev1 = [&](uint32_t k, uint32_t j) {
+        do {
+            const TapeOp &o = t.ops[k];
+            const uint32_t n = I.nel[k];
             uint32_t g = adjreg(k);
             auto v = [&](uint32_t s) { return rev_operand(s, j); };
             uint32_t op = fwd_opcode(o.code) - isa::F_ADD + isa::R_ADD;
@@ -936,42 +969,105 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             default:  // NEG, LOG, SIN, COS, ABS
                 E.put(isa::w0(op, 0, n), g, o.code == tp::NEG ? 0 : v(o.a), 0, 0, target(o.a));
             }
+        } while (false);
+    };
+    // value (not adjoint-first) register of a target, without side effects
+    auto target_reg = [&](uint32_t s) -> uint32_t {
+        if (I.kind[s] == K_PARAM) return P + t.ops[s].imm;
+        if (I.kind[s] != K_COMP || !I.active[s]) return kSink;
+        return kStatic + riv[adj_of[s]].reg;
+    };
+
+
+    for (const AI &a : ra) {
+        switch (a.kind) {
+        case I_ZEROP:
+            for (uint32_t p0 = 0; p0 < P; p0 += 16)
+                E.put(isa::w0(isa::ZERO, 0, std::min<uint32_t>(16, P - p0)), P + p0);
+            break;
+        case I_SEED:
+            if (I.kind[a.k] == K_PARAM || (I.kind[a.k] == K_COMP && I.active[a.k]))
+                E.put(isa::w0(isa::SEED, 0, 1), 0, 0, 0, 0, target(a.k));
+            break;
+        case I_CKLD: {
+            uint32_t s = B.livein[a.k][a.j];
+            uint32_t row = ckrow_base[a.k];
+            for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
+            E.put(isa::w0(isa::CKPT_LD, 0, I.nel[s]), rev_operand(s, a.k), 0, 0, 0, 0, 0, row);
+            S.ckpt_elems_loaded += I.nel[s];
             break;
         }
-        case I_REV2: {
-            uint32_t w[13];
-            int idx = 0;
-            uint32_t subs[2];
-            for (int h = 0; h < 2; ++h) {
-                const uint32_t k = h ? a.k2 : a.k;
+        case I_FWD: {
+            auto opnd = [&](uint32_t s) { return rev_operand(s, a.j); };
+            emit_bundle(a, opnd);
+            S.n_recompute_ops += a.nops();
+            break;
+        }
+        case I_REV: {
+            const uint32_t nb = a.nops();
+            const int cls = nb > 1 || a.seq ? rev_class(I, a.k) : 0;
+            // the registers a rule reads: g, ya, yb
+            auto rule_regs = [&](uint32_t k, uint32_t (&r)[3]) {
                 const TapeOp &o = t.ops[k];
-                subs[h] = uint32_t(dual_sub(I, k));
-                uint32_t vg = adjreg(k);
-                uint32_t va = subs[h] == 2 ? rev_operand(o.a, a.j) : 0;
-                uint32_t vb = subs[h] >= 2 ? rev_operand(o.b, a.j) : 0;
-                uint32_t vz = subs[h] == 3 ? rev_operand(k, a.j) : 0;
-                uint32_t ta = target_word(o.a);
-                uint32_t tb = target_word(o.b);
-                ta = ta == isa::kNone ? kSink : ta;
-                tb = tb == isa::kNone ? kSink : tb;
-                uint32_t f[6] = {vg, va, vb, vz, ta, tb};
-                for (uint32_t v : f) w[idx++] = v;
+                auto v = [&](uint32_t s) { return rev_operand(s, a.j); };
+                r[0] = adjreg(k);
+                r[1] = kOne;
+                r[2] = kOne;
+                if (cls == 2) {
+                    r[1] = v(o.b);
+                    r[2] = v(k);
+                    return;
+                }
+                switch (o.code) {
+                case tp::SUB: r[2] = kMinusOne; break;
+                case tp::MUL: r[1] = v(o.b); r[2] = v(o.a); break;
+                case tp::NEG: r[1] = kMinusOne; break;
+                case tp::EXP: r[1] = v(k); break;
+                default: break;   // ADD
+                }
+            };
+            bool fits = cls != 0;
+            for (uint32_t b = 0; b < nb && fits; ++b) {
+                const uint32_t k = a.op(b);
+                const TapeOp &o = t.ops[k];
+                uint32_t r[3];
+                rule_regs(k, r);
+                fits = r[0] < isa::kFieldMaxReg && r[1] < isa::kFieldMaxReg && r[2] < isa::kFieldMaxReg &&
+                       target_reg(o.a) < isa::kFieldMaxReg &&
+                       (!binary_code(o.code) || target_reg(o.b) < isa::kFieldMaxReg);
             }
-            S.n_rev_ops += 2;
-            bool fits = true;
-            for (int q = 0; q < 12; ++q) fits = fits && (w[q] & ~isa::kInit) < isa::kR2MaxReg;
-            if (!fits) {   // registers beyond the 16-bit fields: two single rules
-                static_assert(isa::SR_SUB == isa::SR_ADD + 1 && isa::SR_DIV == isa::SR_ADD + 3, "SR order");
-                for (int h = 0; h < 2; ++h)
-                    E.put(isa::w0(isa::SR_ADD + subs[h], 0, 1), w[6 * h], w[6 * h + 1], w[6 * h + 2],
-                          w[6 * h + 3], w[6 * h + 4], w[6 * h + 5]);
+            if (!fits) {
+                for (uint32_t b = 0; b < nb; ++b) emit_rev1(a.op(b), a.j);
                 break;
             }
-            S.n_dual++;
-            auto t16 = [](uint32_t tw) { return (tw & 0x7FFFu) | ((tw & isa::kInit) ? 0x8000u : 0u); };
-            auto pk = [](uint32_t lo, uint32_t hi) { return lo | (hi << 16); };
-            E.put(isa::R2 | (subs[0] << 8) | (subs[1] << 12) | (1u << 16), pk(w[0], w[1]), pk(w[2], w[3]),
-                  pk(t16(w[4]), t16(w[5])), pk(w[6], w[7]), pk(w[8], w[9]), pk(t16(w[10]), t16(w[11])));
+            const uint32_t op0 = a.seq ? (cls == 2 ? isa::RDBS1 : isa::LBS1) : (cls == 2 ? isa::RDB1 : isa::LB1);
+            uint32_t w[8] = {op0 + nb - 1, 0, 0, 0, 0, 0, 0, 0};
+            auto put_field = [&](uint32_t i, uint32_t f) {
+                if (i == 14)
+                    w[0] |= f << 16;
+                else
+                    w[1 + i / 2] |= f << (16 * (i & 1));
+            };
+            auto tfield = [&](uint32_t s) {
+                const uint32_t x = target_word(s);
+                if (x == isa::kNone) return kSink;
+                return (x & ~isa::kInit) | ((x & isa::kInit) ? isa::kFieldInit : 0u);
+            };
+            for (uint32_t b = 0; b < nb; ++b) {
+                const uint32_t k = a.op(b);
+                const TapeOp &o = t.ops[k];
+                uint32_t r[3];
+                rule_regs(k, r);
+                put_field(5 * b, r[0]);
+                put_field(5 * b + 1, r[1]);
+                put_field(5 * b + 2, r[2]);
+                put_field(5 * b + 3, tfield(o.a));
+                put_field(5 * b + 4, binary_code(o.code) ? tfield(o.b) : kSink);
+            }
+            E.put(w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]);
+            S.n_rev_ops += nb;
+            S.n_bundles++;
+            S.n_bundled_ops += nb;
             break;
         }
         case I_STG:
@@ -981,10 +1077,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             break;
         }
     }
-    for (int pad = 0; pad < 3; ++pad) E.put(isa::w0(isa::END, 0, 0));   // END + look-ahead padding
-    S.code = std::move(E.code);
-    S.aux = std::move(E.aux);
-    S.n_instr = S.code.size() / isa::kWords;
+    finish(E, S);
     return S;
 }
 

@@ -21,6 +21,9 @@ def lib():
         f.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_uint32, vp, i64, i64,
                       vp, i64, vp, vp, i64, vp]
         _lib.ndvm_emu_error.restype = ctypes.c_char_p
+        g = _lib.ndvm_emu_program
+        g.restype = ctypes.c_int64
+        g.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_uint32, vp, ctypes.c_size_t]
     return _lib
 
 
@@ -41,3 +44,12 @@ def run(tape: bytes, params, obs, with_grad=True, budget=320):
     if rc != 0:
         raise RuntimeError(f"emulator rc={rc}: {lib().ndvm_emu_error().decode()}")
     return loss, grad, dict(zip(STATS, list(stats)))
+
+
+def program(tape: bytes, with_grad=True, budget=320):
+    """The scheduled device program as an (n_instr, 8) array of uint32 words."""
+    n = lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, None, 0)
+    assert n >= 0
+    out = np.empty(n, dtype=np.uint32)
+    lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, out.ctypes.data, n)
+    return out.reshape(-1, 8)
