@@ -467,6 +467,203 @@ NDVM_HD void acc1(const C &c, uint32_t tw, double x, bool on) {
     c.st(r, on ? base + x : base);
 }
 
+// ---- small-matrix fast paths: shapes known at compile time, so every loop
+// unrolls, element offsets become immediate LDS offsets and no per-element
+// branch remains.  Same arithmetic as the generic handlers: ascending fma
+// chains whose first term is a plain product.
+
+// adjoint update of register r (first contribution when `init`), as acc
+template <class C>
+NDVM_HD void accv(const C &c, uint32_t r, bool init, double x, bool on) {
+    const double old = c.ld_raw(r);   // may be unset on a first contribution
+    const double b = init ? 0.0 : old;
+    c.st(r, on ? b + x : b);
+}
+
+template <int M, int K, int N, class C>
+NDVM_HD void mm_fwd(const C &c, uint32_t d, uint32_t a, uint32_t b) {
+    double A[M * K], B[K * N];
+#pragma unroll
+    for (int i = 0; i < M * K; ++i) A[i] = c.ld(a + i);
+#pragma unroll
+    for (int i = 0; i < K * N; ++i) B[i] = c.ld(b + i);
+#pragma unroll
+    for (int i = 0; i < M; ++i)
+#pragma unroll
+        for (int j = 0; j < N; ++j) {
+            double s = A[i * K] * B[j];
+#pragma unroll
+            for (int p = 1; p < K; ++p) s = fma(A[i * K + p], B[p * N + j], s);
+            c.st(d + i * N + j, s);
+        }
+}
+
+// Z = A B with adjoint G: A += G B^T, B += A^T G, gated on any G != 0
+template <int M, int K, int N, class C>
+NDVM_HD void mm_rev(const C &c, uint32_t g, uint32_t a, uint32_t b, uint32_t ta, uint32_t tb) {
+    double G[M * N];
+    bool nz = false;
+#pragma unroll
+    for (int i = 0; i < M * N; ++i) {
+        G[i] = c.ld(g + i);
+        nz = nz || G[i] != 0.0;
+    }
+    if (ta != kNone) {
+        const uint32_t r = ta & ~kInit;
+        const bool init = (ta & kInit) != 0;
+        double B[K * N], T[M * K];
+#pragma unroll
+        for (int i = 0; i < K * N; ++i) B[i] = c.ld(b + i);
+#pragma unroll
+        for (int i = 0; i < M; ++i)
+#pragma unroll
+            for (int q = 0; q < K; ++q) {
+                double s = G[i * N] * B[q * N];
+#pragma unroll
+                for (int j = 1; j < N; ++j) s = fma(G[i * N + j], B[q * N + j], s);
+                T[i * K + q] = s;
+            }
+#pragma unroll
+        for (int e = 0; e < M * K; ++e) accv(c, r + e, init, T[e], nz);
+    }
+    if (tb != kNone) {
+        const uint32_t r = tb & ~kInit;
+        const bool init = (tb & kInit) != 0;
+        double A[M * K], T[K * N];
+#pragma unroll
+        for (int i = 0; i < M * K; ++i) A[i] = c.ld(a + i);
+#pragma unroll
+        for (int q = 0; q < K; ++q)
+#pragma unroll
+            for (int j = 0; j < N; ++j) {
+                double s = A[q] * G[j];
+#pragma unroll
+                for (int i = 1; i < M; ++i) s = fma(A[i * K + q], G[i * N + j], s);
+                T[q * N + j] = s;
+            }
+#pragma unroll
+        for (int e = 0; e < K * N; ++e) accv(c, r + e, init, T[e], nz);
+    }
+}
+
+#define NDVM_MM_SHAPES(X) \
+    X(1, 1, 1) X(1, 1, 2) X(1, 1, 4) X(1, 2, 1) X(1, 2, 2) X(1, 2, 4) X(1, 4, 1) X(1, 4, 2) X(1, 4, 4) \
+    X(2, 1, 1) X(2, 1, 2) X(2, 1, 4) X(2, 2, 1) X(2, 2, 2) X(2, 2, 4) X(2, 4, 1) X(2, 4, 2) X(2, 4, 4) \
+    X(4, 1, 1) X(4, 1, 2) X(4, 1, 4) X(4, 2, 1) X(4, 2, 2) X(4, 2, 4) X(4, 4, 1) X(4, 4, 2) X(4, 4, 4)
+
+// shapes with m, k, n in {1, 2, 4}; false for the generic handler
+template <class C, class W>
+NDVM_HD bool mm_fwd_fast(const C &c, const W &w) {
+    switch (w[7] & 0xFFFFFFu) {
+#define NDVM_X(m, k, n) \
+    case (m) | ((k) << 8) | ((n) << 16): mm_fwd<m, k, n>(c, w[1], w[2], w[3]); return true;
+        NDVM_MM_SHAPES(NDVM_X)
+#undef NDVM_X
+    }
+    return false;
+}
+template <class C, class W>
+NDVM_HD bool mm_rev_fast(const C &c, const W &w) {
+    switch (w[7] & 0xFFFFFFu) {
+#define NDVM_X(m, k, n) \
+    case (m) | ((k) << 8) | ((n) << 16): mm_rev<m, k, n>(c, w[1], w[2], w[3], w[5], w[6]); return true;
+        NDVM_MM_SHAPES(NDVM_X)
+#undef NDVM_X
+    }
+    return false;
+}
+
+// elementwise binary ops of two equal-shape operands, N elements
+template <int N, class C>
+NDVM_HD void ew_fwd(const C &c, uint32_t op, uint32_t d, uint32_t a, uint32_t b) {
+    double x[N], y[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        x[i] = c.ld(a + i);
+        y[i] = c.ld(b + i);
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const double z = op == F_ADD ? x[i] + y[i] : op == F_SUB ? x[i] - y[i] : op == F_MUL ? x[i] * y[i]
+                                                                                              : x[i] / y[i];
+        c.st(d + i, z);
+    }
+}
+// adjoints of an elementwise sum or difference, N elements
+template <int N, class C>
+NDVM_HD void ew_rev_addsub(const C &c, bool sub, uint32_t g, uint32_t ta, uint32_t tb) {
+    double G[N];
+    bool nz = false;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        G[i] = c.ld(g + i);
+        nz = nz || G[i] != 0.0;
+    }
+    if (ta != kNone) {
+        const uint32_t r = ta & ~kInit;
+        const bool init = (ta & kInit) != 0;
+#pragma unroll
+        for (int i = 0; i < N; ++i) accv(c, r + i, init, G[i], nz);
+    }
+    if (tb != kNone) {
+        const uint32_t r = tb & ~kInit;
+        const bool init = (tb & kInit) != 0;
+#pragma unroll
+        for (int i = 0; i < N; ++i) accv(c, r + i, init, sub ? -G[i] : G[i], nz);
+    }
+}
+
+template <class C, class W>
+NDVM_HD bool ew_fwd_fast(const C &c, const W &w, uint32_t op) {
+    const uint32_t w0 = w[0];
+    if (((w0 >> 8) & 0xFF) != MODE_SAME) return false;
+    switch ((w0 >> 16) & 0xFF) {
+    case 2: ew_fwd<2>(c, op, w[1], w[2], w[3]); return true;
+    case 4: ew_fwd<4>(c, op, w[1], w[2], w[3]); return true;
+    case 16: ew_fwd<16>(c, op, w[1], w[2], w[3]); return true;
+    }
+    return false;
+}
+template <class C, class W>
+NDVM_HD bool ew_rev_fast(const C &c, const W &w, uint32_t op) {
+    switch ((w[0] >> 16) & 0xFF) {
+    case 2: ew_rev_addsub<2>(c, op == R_SUB, w[1], w[5], w[6]); return true;
+    case 4: ew_rev_addsub<4>(c, op == R_SUB, w[1], w[5], w[6]); return true;
+    case 16: ew_rev_addsub<16>(c, op == R_SUB, w[1], w[5], w[6]); return true;
+    }
+    return false;
+}
+
+// checkpoint rows to registers and back, N elements: every load is issued
+// before the first store
+template <int N, class C>
+NDVM_HD void ckpt_load(const C &c, uint32_t d, uint32_t row) {
+    double v[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = c.ckpt_ld(row + i);
+#pragma unroll
+    for (int i = 0; i < N; ++i) c.st(d + i, v[i]);
+}
+template <int N, class C>
+NDVM_HD void ckpt_store(const C &c, uint32_t src, uint32_t row) {
+    double v[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = c.ld(src + i);
+#pragma unroll
+    for (int i = 0; i < N; ++i) c.ckpt_st(row + i, v[i]);
+}
+template <class C, class W>
+NDVM_HD bool ckpt_fast(const C &c, const W &w, bool load) {
+    const uint32_t n = (w[0] >> 16) & 0xFF;
+    switch (n) {
+    case 1: load ? ckpt_load<1>(c, w[1], w[7]) : ckpt_store<1>(c, w[2], w[7]); return true;
+    case 2: load ? ckpt_load<2>(c, w[1], w[7]) : ckpt_store<2>(c, w[2], w[7]); return true;
+    case 4: load ? ckpt_load<4>(c, w[1], w[7]) : ckpt_store<4>(c, w[2], w[7]); return true;
+    case 16: load ? ckpt_load<16>(c, w[1], w[7]) : ckpt_store<16>(c, w[2], w[7]); return true;
+    }
+    return false;
+}
+
 // 16-bit field i of a bundle instruction
 template <class W>
 NDVM_HD uint32_t fld(const W &w, int i) {
@@ -729,7 +926,27 @@ NDVM_HD void run(const C &c, const uint32_t *prog, const uint32_t *aux) {
             acc1(c, w[6], g, nz && !p);
             break;
         }
-        default: {
+        case F_MATMUL:
+            if (!mm_fwd_fast(c, w)) goto cold;
+            break;
+        case R_MATMUL:
+            if (!mm_rev_fast(c, w)) goto cold;
+            break;
+        case F_ADD: case F_SUB: case F_MUL: case F_DIV:
+            if (!ew_fwd_fast(c, w, op)) goto cold;
+            break;
+        case R_ADD: case R_SUB:
+            if (!ew_rev_fast(c, w, op)) goto cold;
+            break;
+        case CKPT_LD:
+            if (!ckpt_fast(c, w, true)) goto cold;
+            break;
+        case CKPT_ST:
+            if (!ckpt_fast(c, w, false)) goto cold;
+            break;
+        case LDOBS: c.st(w[1], c.obsv(w[7])); break;
+        default:
+        cold: {
             uint32_t wc[8];
 #pragma unroll
             for (int k = 0; k < 8; ++k) wc[k] = w[k];
