@@ -827,134 +827,134 @@ template <class C>
 NDVM_HD void run(const C &c, const uint32_t *prog, const uint32_t *aux) {
     typename C::Chunk cur = c.load_chunk(prog), nxt = c.load_chunk(prog + kChunkWords);
     for (const uint32_t *ahead = prog + 2 * kChunkWords;; ahead += kChunkWords) {
-    // END only ever opens a chunk; the chunk registers change only below,
-    // outside the per-instruction loop, which has no exit of its own
-    if ((C::instr(cur, 0)[0] & 0xFF) == END) return;
-    for (uint32_t i = 0; i < kChunkInstr; ++i) {
-        const auto w = C::instr(cur, i);
-        const uint32_t op = w[0] & 0xFF;
-        switch (op) {
-        case END: case NOP: break;
-        case FB1: fma_bundle<1>(c, w); break;
-        case FB2: fma_bundle<2>(c, w); break;
-        case FB3: fma_bundle<3>(c, w); break;
-        case DB1: div_bundle<1>(c, w); break;
-        case DB2: div_bundle<2>(c, w); break;
-        case DB3: div_bundle<3>(c, w); break;
-        case LB1: adj_bundle<1, false, false>(c, w); break;
-        case LB2: adj_bundle<2, false, false>(c, w); break;
-        case LB3: adj_bundle<3, false, false>(c, w); break;
-        case RDB1: adj_bundle<1, true, false>(c, w); break;
-        case RDB2: adj_bundle<2, true, false>(c, w); break;
-        case RDB3: adj_bundle<3, true, false>(c, w); break;
-        case LBS1: adj_bundle<1, false, true>(c, w); break;
-        case LBS2: adj_bundle<2, false, true>(c, w); break;
-        case LBS3: adj_bundle<3, false, true>(c, w); break;
-        case RDBS1: adj_bundle<1, true, true>(c, w); break;
-        case RDBS2: adj_bundle<2, true, true>(c, w); break;
-        case RDBS3: adj_bundle<3, true, true>(c, w); break;
-        case S_ADD: c.st(w[1], c.ld(w[2]) + c.ld(w[3])); break;
-        case S_SUB: c.st(w[1], c.ld(w[2]) - c.ld(w[3])); break;
-        case S_MUL: c.st(w[1], c.ld(w[2]) * c.ld(w[3])); break;
-        case S_DIV: c.st(w[1], c.ld(w[2]) / c.ld(w[3])); break;
-        case S_NEG: c.st(w[1], -c.ld(w[2])); break;
-        case S_ABS: c.st(w[1], fabs(c.ld(w[2]))); break;
-        case S_SELECT: {
-            const bool p = c.ld(w[2]) < c.ld(w[3]);
-            const double x = c.ld(w[4]), y = c.ld(w[5]);
-            c.st(w[1], p ? x : y);
-            break;
-        }
-        case SR_ADD: {
-            const double g = c.ld(w[1]);
-            const bool nz = g != 0.0;
-            acc1(c, w[5], g, nz);
-            acc1(c, w[6], g, nz);
-            break;
-        }
-        case SR_SUB: {
-            const double g = c.ld(w[1]);
-            const bool nz = g != 0.0;
-            acc1(c, w[5], g, nz);
-            acc1(c, w[6], -g, nz);
-            break;
-        }
-        case SR_MUL: {
-            const double g = c.ld(w[1]), a = c.ld(w[2]), b = c.ld(w[3]);
-            const bool nz = g != 0.0;
-            acc1(c, w[5], g * b, nz);
-            acc1(c, w[6], g * a, nz);
-            break;
-        }
-        case SR_DIV: {
-            const double g = c.ld(w[1]), b = c.ld(w[3]), z = c.ld(w[4]);
-            const bool nz = g != 0.0;
-            acc1(c, w[5], g / b, nz);
-            acc1(c, w[6], -((g * z) / b), nz);
-            break;
-        }
-        case SR_NEG: {
-            const double g = c.ld(w[1]);
-            acc1(c, w[5], -g, g != 0.0);
-            break;
-        }
-        case SR_EXP: {
-            const double g = c.ld(w[1]);
-            acc1(c, w[5], g * c.ld(w[4]), g != 0.0);
-            break;
-        }
-        case SR_LOG: {
-            const double g = c.ld(w[1]), a = c.ld(w[2]);
-            acc1(c, w[5], g / a, g != 0.0 && a > 1e-8);
-            break;
-        }
-        case SR_SQRT: {
-            const double g = c.ld(w[1]), a = c.ld(w[2]);
-            acc1(c, w[5], g / (2.0 * c.ld(w[4])), g != 0.0 && a > 1e-8);
-            break;
-        }
-        case SR_ABS: {
-            const double g = c.ld(w[1]), a = c.ld(w[2]);
-            acc1(c, w[5], a > 0.0 ? g : (a < 0.0 ? -g : 0.0), g != 0.0);
-            break;
-        }
-        case SR_SELECT: {
-            const double g = c.ld(w[1]);
-            const bool nz = g != 0.0;
-            const bool p = c.ld(w[2]) < c.ld(w[3]);
-            acc1(c, w[5], g, nz && p);
-            acc1(c, w[6], g, nz && !p);
-            break;
-        }
-        case F_MATMUL:
-            if (!mm_fwd_fast(c, w)) goto cold;
-            break;
-        case R_MATMUL:
-            if (!mm_rev_fast(c, w)) goto cold;
-            break;
-        case F_ADD: case F_SUB: case F_MUL: case F_DIV:
-            if (!ew_fwd_fast(c, w, op)) goto cold;
-            break;
-        case R_ADD: case R_SUB:
-            if (!ew_rev_fast(c, w, op)) goto cold;
-            break;
-        case CKPT_LD:
-            if (!ckpt_fast(c, w, true)) goto cold;
-            break;
-        case CKPT_ST:
-            if (!ckpt_fast(c, w, false)) goto cold;
-            break;
-        case LDOBS: c.st(w[1], c.obsv(w[7])); break;
-        default:
-        cold: {
-            uint32_t wc[8];
+        // END only ever opens a chunk; the chunk registers change only below,
+        // outside the per-instruction loop, which has no exit of its own
+        if ((C::instr(cur, 0)[0] & 0xFF) == END) return;
+        for (uint32_t i = 0; i < kChunkInstr; ++i) {
+            const auto w = C::instr(cur, i);
+            const uint32_t op = w[0] & 0xFF;
+            switch (op) {
+            case END: case NOP: break;
+            case FB1: fma_bundle<1>(c, w); break;
+            case FB2: fma_bundle<2>(c, w); break;
+            case FB3: fma_bundle<3>(c, w); break;
+            case DB1: div_bundle<1>(c, w); break;
+            case DB2: div_bundle<2>(c, w); break;
+            case DB3: div_bundle<3>(c, w); break;
+            case LB1: adj_bundle<1, false, false>(c, w); break;
+            case LB2: adj_bundle<2, false, false>(c, w); break;
+            case LB3: adj_bundle<3, false, false>(c, w); break;
+            case RDB1: adj_bundle<1, true, false>(c, w); break;
+            case RDB2: adj_bundle<2, true, false>(c, w); break;
+            case RDB3: adj_bundle<3, true, false>(c, w); break;
+            case LBS1: adj_bundle<1, false, true>(c, w); break;
+            case LBS2: adj_bundle<2, false, true>(c, w); break;
+            case LBS3: adj_bundle<3, false, true>(c, w); break;
+            case RDBS1: adj_bundle<1, true, true>(c, w); break;
+            case RDBS2: adj_bundle<2, true, true>(c, w); break;
+            case RDBS3: adj_bundle<3, true, true>(c, w); break;
+            case S_ADD: c.st(w[1], c.ld(w[2]) + c.ld(w[3])); break;
+            case S_SUB: c.st(w[1], c.ld(w[2]) - c.ld(w[3])); break;
+            case S_MUL: c.st(w[1], c.ld(w[2]) * c.ld(w[3])); break;
+            case S_DIV: c.st(w[1], c.ld(w[2]) / c.ld(w[3])); break;
+            case S_NEG: c.st(w[1], -c.ld(w[2])); break;
+            case S_ABS: c.st(w[1], fabs(c.ld(w[2]))); break;
+            case S_SELECT: {
+                const bool p = c.ld(w[2]) < c.ld(w[3]);
+                const double x = c.ld(w[4]), y = c.ld(w[5]);
+                c.st(w[1], p ? x : y);
+                break;
+            }
+            case SR_ADD: {
+                const double g = c.ld(w[1]);
+                const bool nz = g != 0.0;
+                acc1(c, w[5], g, nz);
+                acc1(c, w[6], g, nz);
+                break;
+            }
+            case SR_SUB: {
+                const double g = c.ld(w[1]);
+                const bool nz = g != 0.0;
+                acc1(c, w[5], g, nz);
+                acc1(c, w[6], -g, nz);
+                break;
+            }
+            case SR_MUL: {
+                const double g = c.ld(w[1]), a = c.ld(w[2]), b = c.ld(w[3]);
+                const bool nz = g != 0.0;
+                acc1(c, w[5], g * b, nz);
+                acc1(c, w[6], g * a, nz);
+                break;
+            }
+            case SR_DIV: {
+                const double g = c.ld(w[1]), b = c.ld(w[3]), z = c.ld(w[4]);
+                const bool nz = g != 0.0;
+                acc1(c, w[5], g / b, nz);
+                acc1(c, w[6], -((g * z) / b), nz);
+                break;
+            }
+            case SR_NEG: {
+                const double g = c.ld(w[1]);
+                acc1(c, w[5], -g, g != 0.0);
+                break;
+            }
+            case SR_EXP: {
+                const double g = c.ld(w[1]);
+                acc1(c, w[5], g * c.ld(w[4]), g != 0.0);
+                break;
+            }
+            case SR_LOG: {
+                const double g = c.ld(w[1]), a = c.ld(w[2]);
+                acc1(c, w[5], g / a, g != 0.0 && a > 1e-8);
+                break;
+            }
+            case SR_SQRT: {
+                const double g = c.ld(w[1]), a = c.ld(w[2]);
+                acc1(c, w[5], g / (2.0 * c.ld(w[4])), g != 0.0 && a > 1e-8);
+                break;
+            }
+            case SR_ABS: {
+                const double g = c.ld(w[1]), a = c.ld(w[2]);
+                acc1(c, w[5], a > 0.0 ? g : (a < 0.0 ? -g : 0.0), g != 0.0);
+                break;
+            }
+            case SR_SELECT: {
+                const double g = c.ld(w[1]);
+                const bool nz = g != 0.0;
+                const bool p = c.ld(w[2]) < c.ld(w[3]);
+                acc1(c, w[5], g, nz && p);
+                acc1(c, w[6], g, nz && !p);
+                break;
+            }
+            case F_MATMUL:
+                if (!mm_fwd_fast(c, w)) goto cold;
+                break;
+            case R_MATMUL:
+                if (!mm_rev_fast(c, w)) goto cold;
+                break;
+            case F_ADD: case F_SUB: case F_MUL: case F_DIV:
+                if (!ew_fwd_fast(c, w, op)) goto cold;
+                break;
+            case R_ADD: case R_SUB:
+                if (!ew_rev_fast(c, w, op)) goto cold;
+                break;
+            case CKPT_LD:
+                if (!ckpt_fast(c, w, true)) goto cold;
+                break;
+            case CKPT_ST:
+                if (!ckpt_fast(c, w, false)) goto cold;
+                break;
+            case LDOBS: c.st(w[1], c.obsv(w[7])); break;
+            default:
+            cold: {
+                uint32_t wc[8];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) wc[k] = w[k];
-            exec_cold(c, wc, op, aux);
-            break;
+                for (int k = 0; k < 8; ++k) wc[k] = w[k];
+                exec_cold(c, wc, op, aux);
+                break;
+            }
+            }
         }
-        }
-    }
         cur = nxt;
         nxt = c.load_chunk(ahead);
     }
