@@ -13,6 +13,7 @@ kernel (its average duration measured with HIP events on the launch stream)
 and the CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -28,6 +29,41 @@ from workloads import configs  # noqa: E402
 PEAK_FP64 = 78.6e12        # MI355X fp64 vector FLOP/s
 PEAK_HBM = 8.0e12          # MI355X HBM3E bytes/s
 DEFAULT_WORKLOAD = configs.ORDER[1]
+CSRC = os.path.join(ROOT, "paper_2607_03574_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_sources_sha256() -> str:
+    """Hash of every source that decides what the replay kernel does on the GPU
+    (front end, validator, scheduler, launch code, kernel); the host emulator is
+    left out."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".h", ".hip", ".cpp")) and name != "emu.cpp":
+            h.update(name.encode() + b"\0")
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload: str):
+    """HBM bytes per launch of the replay kernel for `workload`, from the
+    committed rocprofv3 summary (FETCH_SIZE + WRITE_SIZE, each scaled by a copy
+    calibration); None when there is no summary or the kernel sources changed
+    since its counters were taken."""
+    sha = kernel_sources_sha256()
+    for name in sorted(os.listdir(PROFILES)):
+        if not (name.startswith(f"ndvm_replay_{workload}_") and name.endswith(".md")):
+            continue
+        vals = {}
+        with open(os.path.join(PROFILES, name)) as f:
+            for line in f:
+                key, _, val = line.strip().partition(": ")
+                if key in ("traffic_bytes_per_launch", "kernel_sources_sha256"):
+                    vals[key] = val
+        if vals.get("kernel_sources_sha256") == sha and "traffic_bytes_per_launch" in vals:
+            return float(vals["traffic_bytes_per_launch"])
+    return None
 
 
 def tape_flops(tape_bytes: bytes) -> float:
@@ -185,7 +221,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": dict(workload=w.name, **meta),
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_FP64 / 1e12,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP64, "traffic": None,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP64,
+                     "traffic": profiled_traffic(args.workload),
                      "kernel": "ndvm_replay", "kernel_ms": kern_s * 1e3,
                      "alg_flops_per_launch": flops},
     }

@@ -203,3 +203,16 @@ def test_emulated_wide_program_beyond_packed_register_fields(oracle_mod):
     want[:, 1:] += params[:, :-1]
     np.testing.assert_array_equal(ge, go)
     np.testing.assert_allclose(ge, want, rtol=0, atol=0)
+
+
+def test_bench_traffic_only_for_matching_kernel_sources(tmp_path, monkeypatch):
+    import bench
+    sha = bench.kernel_sources_sha256()
+    (tmp_path / "ndvm_replay_logistic_euler_L4096.md").write_text(
+        f"text\n\n    traffic_bytes_per_launch: 12345\n    kernel_sources_sha256: {sha}\n")
+    (tmp_path / "ndvm_replay_kalman_cv4_L16384.md").write_text(
+        "    traffic_bytes_per_launch: 999\n    kernel_sources_sha256: " + "0" * 64 + "\n")
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    assert bench.profiled_traffic("logistic_euler") == 12345.0
+    assert bench.profiled_traffic("kalman_cv4") is None      # counters of another kernel build
+    assert bench.profiled_traffic("exp_decay") is None       # no summary
