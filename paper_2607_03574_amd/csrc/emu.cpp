@@ -53,6 +53,10 @@ struct HostCtx {
         if (r >= n_regs) { flag(1); return NAN; }
         return regs[r];
     }
+    static uint32_t half(uint32_t word, int hi) { return hi ? word >> 16 : word & 0xFFFFu; }
+    double ldh(uint32_t word, int hi) const { return ld(half(word, hi)); }
+    double ldh_raw(uint32_t word, int hi) const { return ld_raw(half(word, hi)); }
+    void sth(uint32_t word, int hi, double v) const { st(half(word, hi), v); }
     void st(uint32_t r, double v) const {
         if (r >= n_regs) { flag(1); return; }
         regs[r] = v;

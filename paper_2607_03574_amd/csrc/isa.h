@@ -53,8 +53,9 @@ enum : uint32_t {
 
     // Bundles: N = 1..3 independent scalar ops or adjoint rules in one
     // instruction, each a run of 16-bit register fields (field i < 14 is half
-    // i & 1 of word 1 + i / 2, field 14 the high half of w0).  A target field
-    // holds a register below 2^15 with bit 15 set on the first contribution.
+    // i & 1 of word 1 + i / 2, field 14 the high half of w0).  First
+    // contributions of adjoint rules are flagged in w0: bit 8 + 2k for rule
+    // k's target a, bit 9 + 2k for its target b.
     // Sums, differences, products and negations all become one fused
     // multiply-add against the constant registers 1, -1 and -0, which gives
     // the same bits as the plain operation:
@@ -88,8 +89,7 @@ constexpr uint32_t kWords = 8;
 // ahead; so the replay loop tests for END once per chunk.
 constexpr uint32_t kChunkInstr = 32;
 constexpr uint32_t kChunkWords = kChunkInstr * kWords;
-constexpr uint32_t kFieldMaxReg = 1u << 15;   // registers addressable by bundle fields
-constexpr uint32_t kFieldInit = 0x8000u;
+constexpr uint32_t kFieldMaxReg = 1u << 16;   // registers addressable by bundle fields
 
 inline uint32_t w0(uint32_t op, uint32_t mode, uint32_t nel) { return op | (mode << 8) | (nel << 16); }
 inline uint32_t dims(uint32_t m, uint32_t k, uint32_t n) { return m | (k << 8) | (n << 16); }

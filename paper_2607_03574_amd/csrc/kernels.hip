@@ -41,6 +41,8 @@ struct DevCtx {
     AS_GLOBAL double *loss, *grad, *ckpt;
     int64_t lane, lc, Lpad, ld_p, ld_g;
     uint32_t r_lds;
+    uint32_t lane_addr;   // LDS byte address of this thread's register 0
+    uint32_t k512;        // 512 (bytes between consecutive registers), kept in a VGPR
     int t;
     bool active;
 
@@ -77,6 +79,28 @@ struct DevCtx {
         return spill[int64_t(r - r_lds) * Lpad + lane];
     }
     __device__ __forceinline__ double ld_raw(uint32_t r) const { return ld(r); }
+    // Register named by the low (hi = 0) or high half of a scalar word.  In
+    // LDS its byte address is half * 512 + lane_addr, formed by one
+    // v_mad_u32_u16 that reads the half straight from the scalar word.
+    __device__ __forceinline__ AS_LDS double *half_ptr(uint32_t word, int hi) const {
+        uint32_t addr;
+        if (hi)
+            asm("v_mad_u32_u16 %0, %1, %2, %3 op_sel:[1,0,0,0]" : "=v"(addr) : "s"(word), "v"(k512), "v"(lane_addr));
+        else
+            asm("v_mad_u32_u16 %0, %1, %2, %3" : "=v"(addr) : "s"(word), "v"(k512), "v"(lane_addr));
+        return (AS_LDS double *)(size_t)addr;
+    }
+    __device__ __forceinline__ double ldh(uint32_t word, int hi) const {
+        if (kSpill) return ld(hi ? word >> 16 : word & 0xFFFFu);
+        return *half_ptr(word, hi);
+    }
+    __device__ __forceinline__ double ldh_raw(uint32_t word, int hi) const { return ldh(word, hi); }
+    __device__ __forceinline__ void sth(uint32_t word, int hi, double v) const {
+        if (kSpill)
+            st(hi ? word >> 16 : word & 0xFFFFu, v);
+        else
+            *half_ptr(word, hi) = v;
+    }
     __device__ __forceinline__ void st(uint32_t r, double v) const {
         if (!kSpill || r < r_lds)
             lds[r * 64u + t] = v;
@@ -119,6 +143,8 @@ __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStati
     c.active = c.lane < A.L;
     c.lc = c.active ? c.lane : A.L - 1;
     c.lds = (AS_LDS double *)lds_regs;
+    c.lane_addr = uint32_t(size_t(c.lds + c.t));
+    c.k512 = 512u;
     c.spill = gptr(A.ws + int64_t(D.spill_row0) * A.Lpad);
     c.ckpt = gptr(A.ws + int64_t(D.ckpt_row0) * A.Lpad);
     c.consts = cptr(D.consts);

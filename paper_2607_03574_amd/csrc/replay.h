@@ -6,6 +6,9 @@
 //   double ld_raw(uint32_t r) const;   (a read whose value may be discarded)
 //   double konst(uint32_t i) const;  double obsv(uint32_t i) const;  (uniform loads)
 //   static uint32_t uni(uint32_t x);          (wave-uniform value)
+//   double ldh(uint32_t word, int hi) const;  void sth(uint32_t word, int hi, double v) const;
+//   double ldh_raw(uint32_t word, int hi) const;
+//        (the register named by the low (hi = 0) or high half of `word`)
 //   Chunk load_chunk(const uint32_t *p) const;   (kChunkInstr instructions)
 //   static Words instr(const Chunk&, uint32_t i);  (instruction i; Words[k] = word k, uniform)
 //   double param(uint32_t p) const;  void store_loss(double) const;
@@ -664,11 +667,11 @@ NDVM_HD bool ckpt_fast(const C &c, const W &w, bool load) {
     return false;
 }
 
-// 16-bit field i of a bundle instruction
-template <class W>
-NDVM_HD uint32_t fld(const W &w, int i) {
-    return i == 14 ? (w[0] >> 16) : ((w[1 + (i >> 1)] >> ((i & 1) * 16)) & 0xFFFFu);
-}
+// Register named by 16-bit field i of a bundle instruction: word and half.
+// The context loads and stores through (word, half) so the GPU can form the
+// address from the scalar word in one instruction.
+#define NDVM_FW(i) ((i) == 14 ? w[0] : w[1 + ((i) >> 1)])
+#define NDVM_FH(i) ((i) == 14 ? 1 : ((i) & 1))
 
 // d = fma(x, y, w) for N independent ops; all operands are read before any
 // result is written (the scheduler never bundles an op with one it reads)
@@ -677,12 +680,12 @@ NDVM_HD void fma_bundle(const C &c, const W &w) {
     double x[N], y[N], z[N];
 #pragma unroll
     for (int k = 0; k < N; ++k) {
-        x[k] = c.ld(fld(w, 4 * k + 1));
-        y[k] = c.ld(fld(w, 4 * k + 2));
-        z[k] = c.ld(fld(w, 4 * k + 3));
+        x[k] = c.ldh(NDVM_FW(4 * k + 1), NDVM_FH(4 * k + 1));
+        y[k] = c.ldh(NDVM_FW(4 * k + 2), NDVM_FH(4 * k + 2));
+        z[k] = c.ldh(NDVM_FW(4 * k + 3), NDVM_FH(4 * k + 3));
     }
 #pragma unroll
-    for (int k = 0; k < N; ++k) c.st(fld(w, 4 * k), fma(x[k], y[k], z[k]));
+    for (int k = 0; k < N; ++k) c.sth(NDVM_FW(4 * k), NDVM_FH(4 * k), fma(x[k], y[k], z[k]));
 }
 
 template <int N, class C, class W>
@@ -690,11 +693,11 @@ NDVM_HD void div_bundle(const C &c, const W &w) {
     double a[N], b[N];
 #pragma unroll
     for (int k = 0; k < N; ++k) {
-        a[k] = c.ld(fld(w, 3 * k + 1));
-        b[k] = c.ld(fld(w, 3 * k + 2));
+        a[k] = c.ldh(NDVM_FW(3 * k + 1), NDVM_FH(3 * k + 1));
+        b[k] = c.ldh(NDVM_FW(3 * k + 2), NDVM_FH(3 * k + 2));
     }
 #pragma unroll
-    for (int k = 0; k < N; ++k) c.st(fld(w, 3 * k), a[k] / b[k]);
+    for (int k = 0; k < N; ++k) c.sth(NDVM_FW(3 * k), NDVM_FH(3 * k), a[k] / b[k]);
 }
 
 // adjoint rules of N bundled ops (kDiv: division rule, else linear).  Every
@@ -704,18 +707,16 @@ NDVM_HD void div_bundle(const C &c, const W &w) {
 // performed in order).
 template <int N, bool kDiv, bool kSeq, class C, class W>
 NDVM_HD void adj_bundle(const C &c, const W &w) {
+    const uint32_t w0 = w[0];
     double g[N], p[N], q[N], xa[N], xb[N], oa[N], ob[N];
-    uint32_t ta[N], tb[N];
 #pragma unroll
     for (int k = 0; k < N; ++k) {
-        g[k] = c.ld(fld(w, 5 * k));
-        p[k] = c.ld(fld(w, 5 * k + 1));
-        q[k] = c.ld(fld(w, 5 * k + 2));
-        ta[k] = fld(w, 5 * k + 3);
-        tb[k] = fld(w, 5 * k + 4);
-        if (!kSeq) {
-            oa[k] = c.ld_raw(ta[k] & ~kFieldInit);   // may be unset on a first contribution
-            ob[k] = c.ld_raw(tb[k] & ~kFieldInit);
+        g[k] = c.ldh(NDVM_FW(5 * k), NDVM_FH(5 * k));
+        p[k] = c.ldh(NDVM_FW(5 * k + 1), NDVM_FH(5 * k + 1));
+        q[k] = c.ldh(NDVM_FW(5 * k + 2), NDVM_FH(5 * k + 2));
+        if (!kSeq) {   // may be unset on a first contribution
+            oa[k] = c.ldh_raw(NDVM_FW(5 * k + 3), NDVM_FH(5 * k + 3));
+            ob[k] = c.ldh_raw(NDVM_FW(5 * k + 4), NDVM_FH(5 * k + 4));
         }
     }
 #pragma unroll
@@ -731,14 +732,16 @@ NDVM_HD void adj_bundle(const C &c, const W &w) {
 #pragma unroll
     for (int k = 0; k < N; ++k) {
         const bool nz = g[k] != 0.0;
-        if (kSeq) oa[k] = c.ld_raw(ta[k] & ~kFieldInit);
-        const double ba = (ta[k] & kFieldInit) ? 0.0 : oa[k];
-        c.st(ta[k] & ~kFieldInit, nz ? ba + xa[k] : ba);
-        if (kSeq) ob[k] = c.ld_raw(tb[k] & ~kFieldInit);
-        const double bb = (tb[k] & kFieldInit) ? 0.0 : ob[k];
-        c.st(tb[k] & ~kFieldInit, nz ? bb + xb[k] : bb);
+        if (kSeq) oa[k] = c.ldh_raw(NDVM_FW(5 * k + 3), NDVM_FH(5 * k + 3));
+        const double ba = (w0 >> (8 + 2 * k)) & 1u ? 0.0 : oa[k];
+        c.sth(NDVM_FW(5 * k + 3), NDVM_FH(5 * k + 3), nz ? ba + xa[k] : ba);
+        if (kSeq) ob[k] = c.ldh_raw(NDVM_FW(5 * k + 4), NDVM_FH(5 * k + 4));
+        const double bb = (w0 >> (9 + 2 * k)) & 1u ? 0.0 : ob[k];
+        c.sth(NDVM_FW(5 * k + 4), NDVM_FH(5 * k + 4), nz ? bb + xb[k] : bb);
     }
 }
+#undef NDVM_FW
+#undef NDVM_FH
 
 // remaining scalar fast paths (transcendentals, whose library code branches
 // on the argument)

@@ -1048,10 +1048,12 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
                 else
                     w[1 + i / 2] |= f << (16 * (i & 1));
             };
-            auto tfield = [&](uint32_t s) {
+            // target register; its first contribution sets flag bit `bit` of w0
+            auto tfield = [&](uint32_t s, uint32_t bit) {
                 const uint32_t x = target_word(s);
                 if (x == isa::kNone) return kSink;
-                return (x & ~isa::kInit) | ((x & isa::kInit) ? isa::kFieldInit : 0u);
+                if (x & isa::kInit) w[0] |= 1u << bit;
+                return x & ~isa::kInit;
             };
             for (uint32_t b = 0; b < nb; ++b) {
                 const uint32_t k = a.op(b);
@@ -1061,8 +1063,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
                 put_field(5 * b, r[0]);
                 put_field(5 * b + 1, r[1]);
                 put_field(5 * b + 2, r[2]);
-                put_field(5 * b + 3, tfield(o.a));
-                put_field(5 * b + 4, binary_code(o.code) ? tfield(o.b) : kSink);
+                put_field(5 * b + 3, tfield(o.a, 8 + 2 * b));
+                put_field(5 * b + 4, binary_code(o.code) ? tfield(o.b, 9 + 2 * b) : kSink);
             }
             E.put(w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]);
             S.n_rev_ops += nb;
