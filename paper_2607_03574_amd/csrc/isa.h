@@ -36,6 +36,8 @@ enum : uint32_t {
     LDOBS = 8,     // w1 dst, w7 observation index
     LDCONST = 9,   // w1 dst, w7 first pool entry, nel entries
     NOP = 10,      // padding before the END that opens the program's last chunk
+    // N = 2..4 observation loads: word k + 1 = destination | index << 16
+    OB2 = 11, OB3 = 12, OB4 = 13,
 
     F_ADD = 16, F_SUB, F_MUL, F_DIV, F_NEG, F_EXP, F_LOG, F_SQRT, F_SIN, F_COS, F_ABS, F_POW,
     F_DOT, F_MATMUL, F_TRANSPOSE, F_TRACE, F_INV, F_DET, F_LOGDET, F_OUTER, F_PACK, F_INDEX,

@@ -743,6 +743,17 @@ NDVM_HD void adj_bundle(const C &c, const W &w) {
 #undef NDVM_FW
 #undef NDVM_FH
 
+// N observation loads: word k + 1 = destination | observation index << 16;
+// every (scalar) load is issued before the first store
+template <int N, class C, class W>
+NDVM_HD void obs_bundle(const C &c, const W &w) {
+    double v[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) v[k] = c.obsv(w[1 + k] >> 16);
+#pragma unroll
+    for (int k = 0; k < N; ++k) c.sth(w[1 + k], 0, v[k]);
+}
+
 // remaining scalar fast paths (transcendentals, whose library code branches
 // on the argument)
 template <class C>
@@ -856,6 +867,9 @@ NDVM_HD void run(const C &c, const uint32_t *prog, const uint32_t *aux) {
             case RDBS1: adj_bundle<1, true, true>(c, w); break;
             case RDBS2: adj_bundle<2, true, true>(c, w); break;
             case RDBS3: adj_bundle<3, true, true>(c, w); break;
+            case OB2: obs_bundle<2>(c, w); break;
+            case OB3: obs_bundle<3>(c, w); break;
+            case OB4: obs_bundle<4>(c, w); break;
             case S_ADD: c.st(w[1], c.ld(w[2]) + c.ld(w[3])); break;
             case S_SUB: c.st(w[1], c.ld(w[2]) - c.ld(w[3])); break;
             case S_MUL: c.st(w[1], c.ld(w[2]) * c.ld(w[3])); break;

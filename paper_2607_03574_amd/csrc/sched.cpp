@@ -223,7 +223,7 @@ struct AI {
     uint32_t j;   // segment (reverse phase) or checkpoint row
     uint8_t nb = 0;          // further ops bundled with k (I_FWD, I_REV)
     bool seq = false;        // reverse bundle whose rules' targets may repeat
-    uint32_t kb[2] = {0, 0};
+    uint32_t kb[3] = {0, 0, 0};
     // the ops of a forward or reverse instruction
     uint32_t nops() const { return 1u + nb; }
     uint32_t op(uint32_t i) const { return i == 0 ? k : kb[i - 1]; }
@@ -348,10 +348,12 @@ struct Builder {
     }
 };
 
-// Bundle class of a scalar op in the forward program: 1 fused multiply-add
-// form (add, sub, mul, neg), 2 division, 0 none.
+// Bundle class of an op in the forward program: 1 fused multiply-add form of
+// a scalar op (add, sub, mul, neg), 2 scalar division, 3 observation load,
+// 0 none.
 int fwd_class(const Info &I, uint32_t k) {
     const TapeOp &o = I.t.ops[k];
+    if (I.kind[k] == K_OBS) return 3;
     if (I.kind[k] != K_COMP || I.nel[k] != 1 || I.nel[o.a] != 1) return 0;
     switch (o.code) {
     case tp::ADD: case tp::SUB: case tp::MUL: case tp::NEG: return 1;
@@ -371,6 +373,7 @@ int rev_class(const Info &I, uint32_t k) {
     return 0;
 }
 constexpr uint32_t kBundleMax = 3;
+constexpr uint32_t kObsBundleMax = 4;
 constexpr uint32_t kBundleWindow = 24;
 
 // Reorder each run of forward instructions (list scheduling, earliest ready
@@ -428,8 +431,9 @@ std::vector<AI> bundle_forward(const Info &I, const std::vector<AI> &in) {
                 }
             AI a = in[i + x];
             const int cls = fwd_class(I, a.k);
+            const uint32_t cap = cls == 3 ? kObsBundleMax : kBundleMax;
             if (cls)
-                for (uint32_t r = x + 1; r < n && r < x + kBundleWindow && a.nb + 1 < kBundleMax; ++r)
+                for (uint32_t r = x + 1; r < n && r < x + kBundleWindow && a.nb + 1u < cap; ++r)
                     if (!done[r] && pending[r] == 0 && fwd_class(I, in[i + r].k) == cls) {
                         a.kb[a.nb++] = in[i + r].k;
                         done[r] = 2;             // taken; retired with the bundle
@@ -708,6 +712,23 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     auto emit_bundle = [&](const AI &a, auto operand) {
         const uint32_t nb = a.nops();
         const int cls = nb > 1 ? fwd_class(I, a.k) : 0;
+        if (cls == 3) {   // observation loads: fields (d, observation index)
+            bool ok = true;
+            uint32_t w[8] = {isa::OB2 + nb - 2, 0, 0, 0, 0, 0, 0, 0};
+            for (uint32_t b = 0; b < nb; ++b) {
+                const uint32_t d = operand(a.op(b)), idx = t.ops[a.op(b)].imm;
+                ok = ok && d < isa::kFieldMaxReg && idx < isa::kFieldMaxReg;
+                w[1 + b] = d | (idx << 16);
+            }
+            if (ok) {
+                E.put(w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]);
+                S.n_bundles++;
+                S.n_bundled_ops += nb;
+                return;
+            }
+            for (uint32_t b = 0; b < nb; ++b) emit_fwd(a.op(b), operand, operand(a.op(b)));
+            return;
+        }
         uint32_t f[15] = {};
         uint32_t nf = 0;
         bool fits = cls != 0;
