@@ -92,6 +92,10 @@ constexpr uint32_t kWords = 8;
 constexpr uint32_t kChunkInstr = 32;
 constexpr uint32_t kChunkWords = kChunkInstr * kWords;
 constexpr uint32_t kFieldMaxReg = 1u << 16;   // registers addressable by bundle fields
+// Set on a bundle, observation bundle or matmul when the next instruction has
+// the same opcode and lies in the same fetch chunk: the handler runs it too,
+// without going back through the dispatch.
+constexpr uint32_t kRepeat = 1u << 15;
 
 inline uint32_t w0(uint32_t op, uint32_t mode, uint32_t nel) { return op | (mode << 8) | (nel << 16); }
 inline uint32_t dims(uint32_t m, uint32_t k, uint32_t n) { return m | (k << 8) | (n << 16); }

@@ -837,6 +837,28 @@ NDVM_HD void exec_cold(const C &c, const uint32_t *w, uint32_t op, const uint32_
 // The chunk after the current one is loaded when the current one starts, so
 // it has a whole chunk's worth of instructions to arrive (programs are padded
 // so this read-ahead stays inside the program).
+// all eight words of an instruction as an array
+struct Words8 {
+    uint32_t v[8];
+};
+template <class W>
+NDVM_HD Words8 words8(const W &w) {
+    Words8 r;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) r.v[k] = w[k];
+    return r;
+}
+
+// Run `body` (which reads the instruction through `w`) for instruction i and,
+// while its repeat bit is set, for the next instructions of the chunk (same
+// opcode), without going back through the dispatch; leaves i on the last one.
+#define NDVM_RUN(body)                             \
+    for (auto w = C::instr(cur, i);;) {            \
+        body;                                      \
+        if (!(w[0] & kRepeat)) break;              \
+        w = C::instr(cur, ++i);                    \
+    }
+
 template <class C>
 NDVM_HD void run(const C &c, const uint32_t *prog, const uint32_t *aux) {
     typename C::Chunk cur = c.load_chunk(prog), nxt = c.load_chunk(prog + kChunkWords);
@@ -849,27 +871,27 @@ NDVM_HD void run(const C &c, const uint32_t *prog, const uint32_t *aux) {
             const uint32_t op = w[0] & 0xFF;
             switch (op) {
             case END: case NOP: break;
-            case FB1: fma_bundle<1>(c, w); break;
-            case FB2: fma_bundle<2>(c, w); break;
-            case FB3: fma_bundle<3>(c, w); break;
-            case DB1: div_bundle<1>(c, w); break;
-            case DB2: div_bundle<2>(c, w); break;
-            case DB3: div_bundle<3>(c, w); break;
-            case LB1: adj_bundle<1, false, false>(c, w); break;
-            case LB2: adj_bundle<2, false, false>(c, w); break;
-            case LB3: adj_bundle<3, false, false>(c, w); break;
-            case RDB1: adj_bundle<1, true, false>(c, w); break;
-            case RDB2: adj_bundle<2, true, false>(c, w); break;
-            case RDB3: adj_bundle<3, true, false>(c, w); break;
-            case LBS1: adj_bundle<1, false, true>(c, w); break;
-            case LBS2: adj_bundle<2, false, true>(c, w); break;
-            case LBS3: adj_bundle<3, false, true>(c, w); break;
-            case RDBS1: adj_bundle<1, true, true>(c, w); break;
-            case RDBS2: adj_bundle<2, true, true>(c, w); break;
-            case RDBS3: adj_bundle<3, true, true>(c, w); break;
-            case OB2: obs_bundle<2>(c, w); break;
-            case OB3: obs_bundle<3>(c, w); break;
-            case OB4: obs_bundle<4>(c, w); break;
+            case FB1: NDVM_RUN((fma_bundle<1>(c, w))) break;
+            case FB2: NDVM_RUN((fma_bundle<2>(c, w))) break;
+            case FB3: NDVM_RUN((fma_bundle<3>(c, w))) break;
+            case DB1: NDVM_RUN((div_bundle<1>(c, w))) break;
+            case DB2: NDVM_RUN((div_bundle<2>(c, w))) break;
+            case DB3: NDVM_RUN((div_bundle<3>(c, w))) break;
+            case LB1: NDVM_RUN((adj_bundle<1, false, false>(c, w))) break;
+            case LB2: NDVM_RUN((adj_bundle<2, false, false>(c, w))) break;
+            case LB3: NDVM_RUN((adj_bundle<3, false, false>(c, w))) break;
+            case RDB1: NDVM_RUN((adj_bundle<1, true, false>(c, w))) break;
+            case RDB2: NDVM_RUN((adj_bundle<2, true, false>(c, w))) break;
+            case RDB3: NDVM_RUN((adj_bundle<3, true, false>(c, w))) break;
+            case LBS1: NDVM_RUN((adj_bundle<1, false, true>(c, w))) break;
+            case LBS2: NDVM_RUN((adj_bundle<2, false, true>(c, w))) break;
+            case LBS3: NDVM_RUN((adj_bundle<3, false, true>(c, w))) break;
+            case RDBS1: NDVM_RUN((adj_bundle<1, true, true>(c, w))) break;
+            case RDBS2: NDVM_RUN((adj_bundle<2, true, true>(c, w))) break;
+            case RDBS3: NDVM_RUN((adj_bundle<3, true, true>(c, w))) break;
+            case OB2: NDVM_RUN((obs_bundle<2>(c, w))) break;
+            case OB3: NDVM_RUN((obs_bundle<3>(c, w))) break;
+            case OB4: NDVM_RUN((obs_bundle<4>(c, w))) break;
             case S_ADD: c.st(w[1], c.ld(w[2]) + c.ld(w[3])); break;
             case S_SUB: c.st(w[1], c.ld(w[2]) - c.ld(w[3])); break;
             case S_MUL: c.st(w[1], c.ld(w[2]) * c.ld(w[3])); break;
@@ -944,10 +966,10 @@ NDVM_HD void run(const C &c, const uint32_t *prog, const uint32_t *aux) {
                 break;
             }
             case F_MATMUL:
-                if (!mm_fwd_fast(c, w)) goto cold;
+                NDVM_RUN(if (!mm_fwd_fast(c, w)) exec_fwd(c, aux, words8(w).v))
                 break;
             case R_MATMUL:
-                if (!mm_rev_fast(c, w)) goto cold;
+                NDVM_RUN(if (!mm_rev_fast(c, w)) exec_rev(c, aux, words8(w).v))
                 break;
             case F_ADD: case F_SUB: case F_MUL: case F_DIV:
                 if (!ew_fwd_fast(c, w, op)) goto cold;
@@ -976,6 +998,7 @@ NDVM_HD void run(const C &c, const uint32_t *prog, const uint32_t *aux) {
         nxt = c.load_chunk(ahead);
     }
 }
+#undef NDVM_RUN
 
 }  // namespace replay
 }  // namespace ndvm
