@@ -34,6 +34,7 @@ struct HostCtx {
                       // 5 program fetch beyond the padded program
 
     static uint32_t uni(uint32_t x) { return x; }
+    static bool all(bool b) { return b; }
     using Chunk = const uint32_t *;
     Chunk load_chunk(const uint32_t *p) const {
         if (p + isa::kChunkWords > code_end) flag(5);

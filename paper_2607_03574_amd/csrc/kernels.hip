@@ -47,6 +47,8 @@ struct DevCtx {
     bool active;
 
     __device__ __forceinline__ static uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+    // every thread of the workgroup (one wave, all threads active) has b
+    __device__ __forceinline__ static bool all(bool b) { return __all(b); }
     // Program chunks: thread t loads words 4t..4t+3 of a 32-instruction
     // chunk (one coalesced 1 KiB load per wave), so instruction i lies in
     // threads 2i (words 0-3) and 2i+1 (words 4-7) and v_readlane moves its

@@ -6,6 +6,7 @@
 //   double ld_raw(uint32_t r) const;   (a read whose value may be discarded)
 //   double konst(uint32_t i) const;  double obsv(uint32_t i) const;  (uniform loads)
 //   static uint32_t uni(uint32_t x);          (wave-uniform value)
+//   static bool all(bool b);                  (b holds in every lane of the wave)
 //   double ldh(uint32_t word, int hi) const;  void sth(uint32_t word, int hi, double v) const;
 //   double ldh_raw(uint32_t word, int hi) const;
 //        (the register named by the low (hi = 0) or high half of `word`)
@@ -483,6 +484,35 @@ NDVM_HD void accv(const C &c, uint32_t r, bool init, double x, bool on) {
     c.st(r, on ? b + x : b);
 }
 
+// Adjoint update of the E registers r.. with contributions T, gated per lane
+// on `nz`, as accv element by element.  `init` is uniform, so it selects a
+// code path instead of a value; when every lane of the wave has nz the gate
+// is the identity and its selects are skipped.
+template <int E, class C>
+NDVM_HD void acc_block(const C &c, uint32_t r, bool init, const double (&T)[E], bool nz) {
+    const bool all = C::all(nz);
+    if (init) {
+        if (all) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) c.st(r + e, 0.0 + T[e]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < E; ++e) c.st(r + e, nz ? 0.0 + T[e] : 0.0);
+        }
+        return;
+    }
+    double old[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) old[e] = c.ld(r + e);
+    if (all) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) c.st(r + e, old[e] + T[e]);
+    } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) c.st(r + e, nz ? old[e] + T[e] : old[e]);
+    }
+}
+
 template <int M, int K, int N, class C>
 NDVM_HD void mm_fwd(const C &c, uint32_t d, uint32_t a, uint32_t b) {
     double A[M * K], B[K * N];
@@ -526,8 +556,7 @@ NDVM_HD void mm_rev(const C &c, uint32_t g, uint32_t a, uint32_t b, uint32_t ta,
                 for (int j = 1; j < N; ++j) s = fma(G[i * N + j], B[q * N + j], s);
                 T[i * K + q] = s;
             }
-#pragma unroll
-        for (int e = 0; e < M * K; ++e) accv(c, r + e, init, T[e], nz);
+        acc_block<M * K>(c, r, init, T, nz);
     }
     if (tb != kNone) {
         const uint32_t r = tb & ~kInit;
@@ -544,8 +573,7 @@ NDVM_HD void mm_rev(const C &c, uint32_t g, uint32_t a, uint32_t b, uint32_t ta,
                 for (int i = 1; i < M; ++i) s = fma(A[i * K + q], G[i * N + j], s);
                 T[q * N + j] = s;
             }
-#pragma unroll
-        for (int e = 0; e < K * N; ++e) accv(c, r + e, init, T[e], nz);
+        acc_block<K * N>(c, r, init, T, nz);
     }
 }
 
@@ -602,17 +630,12 @@ NDVM_HD void ew_rev_addsub(const C &c, bool sub, uint32_t g, uint32_t ta, uint32
         G[i] = c.ld(g + i);
         nz = nz || G[i] != 0.0;
     }
-    if (ta != kNone) {
-        const uint32_t r = ta & ~kInit;
-        const bool init = (ta & kInit) != 0;
-#pragma unroll
-        for (int i = 0; i < N; ++i) accv(c, r + i, init, G[i], nz);
-    }
+    if (ta != kNone) acc_block<N>(c, ta & ~kInit, (ta & kInit) != 0, G, nz);
     if (tb != kNone) {
-        const uint32_t r = tb & ~kInit;
-        const bool init = (tb & kInit) != 0;
+        double H[N];
 #pragma unroll
-        for (int i = 0; i < N; ++i) accv(c, r + i, init, sub ? -G[i] : G[i], nz);
+        for (int i = 0; i < N; ++i) H[i] = sub ? -G[i] : G[i];
+        acc_block<N>(c, tb & ~kInit, (tb & kInit) != 0, H, nz);
     }
 }
 
