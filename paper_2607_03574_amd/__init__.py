@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import sys
 from typing import Optional, Sequence
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -91,10 +92,12 @@ class Tape:
     def __init__(self, handle: int):
         self.handle = handle
 
-    def __del__(self):
+    def __del__(self, _free_fn=_tape_free, _finalizing=sys.is_finalizing):
+        # at interpreter exit the device runtime may already be gone: leave
+        # the handle to the process teardown then
         h, self.handle = getattr(self, "handle", None), None
-        if h:
-            _tape_free(h)
+        if h and not _finalizing():
+            _free_fn(h)
 
     @property
     def info(self) -> dict:

@@ -236,3 +236,24 @@ def test_every_primitive(nd, oracle_mod):
         gl, gg = run_gpu(nd, bc, params, [])
         ol, og, _ = oracle_mod.run(bc, params, [])
         compare(gl, gg, ol, og)
+
+
+def test_wide_program_spills_and_unbundles(nd, oracle_mod):
+    # 17000 parameters: registers far beyond the LDS budget (spill kernel) and
+    # beyond the 16-bit bundle fields (single-op fallback); the gradient of
+    # sum_i p_i p_(i+1) is p_(i-1) + p_(i+1)
+    P = 17000
+    A = Asm(P, 0)
+    A.param(0).param(1).mul()
+    for i in range(1, P - 1):
+        A.param(i).param(i + 1).mul().add()
+    bc = A.halt().bytes()
+    rng = np.random.default_rng(11)
+    params = rng.uniform(-1, 1, (70, P))
+    gl, gg = run_gpu(nd, bc, params, [])
+    ol, og, _ = oracle_mod.run(bc, params, [])
+    compare(gl, gg, ol, og)
+    want = np.zeros_like(params)
+    want[:, :-1] += params[:, 1:]
+    want[:, 1:] += params[:, :-1]
+    np.testing.assert_array_equal(gg, want)
