@@ -18,7 +18,7 @@
 
 namespace ndvm {
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, bool spill, hipStream_t stream);
+                         uint32_t r_lds, int variant, hipStream_t stream);
 }
 
 using namespace ndvm;
@@ -160,8 +160,8 @@ uint64_t ws_rows(const DevProg &dp, uint32_t b) {
 }
 
 ndvm_status check_stream_and_launch(const LaunchArgs &A, const ProgStatic *table, const ProgStatic &single,
-                                    uint32_t n_prog, uint32_t r_lds, bool spill, hipStream_t stream) {
-    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, spill, stream);
+                                    uint32_t n_prog, uint32_t r_lds, int variant, hipStream_t stream) {
+    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, variant, stream);
     if (e != hipSuccess) {
         set_error(std::string("kernel launch failed: ") + hipGetErrorString(e));
         return NDVM_E_DEVICE;
@@ -363,8 +363,9 @@ ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
             return NDVM_E_NOMEM;
         }
         LaunchArgs A{obs, params, loss, loss, static_cast<double *>(ws), ld_p, 0, L, Lp, 0, 0};
-        ProgStatic S{dp.code, dp.aux, dp.consts, 0, 0, r_lds, 0};
-        return check_stream_and_launch(A, nullptr, S, 1, r_lds, dp.meta.n_regs > r_lds,
+        const bool spills = dp.meta.n_regs > r_lds;
+        ProgStatic S{dp.code, dp.aux, dp.consts, 0, 0, r_lds, spills};
+        return check_stream_and_launch(A, nullptr, S, 1, r_lds, spills ? kSpill : kLdsOnly,
                                        static_cast<hipStream_t>(stream));
     });
 }
@@ -395,8 +396,9 @@ ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L, in
         }
         double *wsd = static_cast<double *>(ws);
         LaunchArgs A{obs, params, loss, grad, wsd, ld_p, ld_g, L, Lp, 0, 0};
-        ProgStatic S{dp->code, dp->aux, dp->consts, 0, dp->meta.n_ckpt_rows, r_lds, 0};
-        return check_stream_and_launch(A, nullptr, S, 1, r_lds, dp->meta.n_regs > r_lds,
+        const bool spills = dp->meta.n_regs > r_lds;
+        ProgStatic S{dp->code, dp->aux, dp->consts, 0, dp->meta.n_ckpt_rows, r_lds, spills};
+        return check_stream_and_launch(A, nullptr, S, 1, r_lds, spills ? kSpill : kLdsOnly,
                                        static_cast<hipStream_t>(stream));
     });
 }
@@ -431,14 +433,15 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
         std::vector<uint64_t> key;
         uint64_t row = 0;
         uint32_t r_launch = 0;
-        bool spill = false;
+        int n_spill = 0;
         for (int q = 0; q < n_prog; ++q) {
             DevProg *dp;
             if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), b, s, &dp)) != NDVM_OK) return st;
             uint32_t r_lds = std::min(dp->meta.n_regs, b);
             r_launch = std::max(r_launch, r_lds);
-            spill = spill || dp->meta.n_regs > r_lds;
-            table[q] = ProgStatic{dp->code, dp->aux, dp->consts, row, row + dp->meta.n_ckpt_rows, r_lds, 0};
+            const bool spills = dp->meta.n_regs > r_lds;
+            n_spill += spills;
+            table[q] = ProgStatic{dp->code, dp->aux, dp->consts, row, row + dp->meta.n_ckpt_rows, r_lds, spills};
             row += ws_rows(*dp, b);
             key.push_back(tapes[q]->id);
             key.push_back(b);
@@ -473,8 +476,9 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
         LaunchArgs A{obs, params, loss, grad, static_cast<double *>(ws), ld_p, ld_g, L, Lp, prog_stride_p,
                      prog_stride_g};
         ProgStatic none{};
+        const int variant = n_spill == 0 ? kLdsOnly : n_spill == n_prog ? kSpill : kPerProgram;
         return check_stream_and_launch(A, static_cast<const ProgStatic *>(d_table), none, uint32_t(n_prog),
-                                       r_launch, spill, s);
+                                       r_launch, variant, s);
     });
 }
 

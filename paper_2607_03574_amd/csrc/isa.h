@@ -113,8 +113,12 @@ struct ProgStatic {
     uint64_t ckpt_row0;      // checkpoint row r of lane l at ws[(ckpt_row0 + r)*Lpad + l]
     uint64_t spill_row0;     // register r_lds + r of lane l at ws[(spill_row0 + r)*Lpad + l]
     uint32_t r_lds;          // registers held in LDS
-    uint32_t pad_;
+    uint32_t spills;         // nonzero when the program has registers beyond r_lds
 };
+
+// Kernel variant of a launch: every register in LDS, a spill tail for every
+// program, or chosen per program (many-program launches that mix the two).
+enum LaunchVariant : int { kLdsOnly = 0, kSpill = 1, kPerProgram = 2 };
 
 // Per-call arguments.  Program q of a launch (blockIdx.y) reads
 // params + q*prog_stride_p and writes loss + q*L, grad + q*prog_stride_g.

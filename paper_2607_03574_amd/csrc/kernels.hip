@@ -174,8 +174,19 @@ ndvm_replay_spill(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic
     replay_body<true>(A, table, single);
 }
 
+// Many programs in one launch, only some of which spill: each workgroup takes
+// the variant its program needs, so one spilling program does not slow the
+// others down.
+extern "C" __global__ void __launch_bounds__(64)
+ndvm_replay_per_program(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
+    if (table[blockIdx.y].spills)
+        replay_body<true>(A, table, single);
+    else
+        replay_body<false>(A, table, single);
+}
+
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, bool spill, hipStream_t stream) {
+                         uint32_t r_lds, int variant, hipStream_t stream) {
     static std::once_flag once[64];
     int dev = 0;
     (void)hipGetDevice(&dev);
@@ -186,10 +197,14 @@ hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const P
                                   hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
         (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&ndvm_replay_spill),
                                   hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
+        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&ndvm_replay_per_program),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
     });
     dim3 grid(uint32_t(A.Lpad / 64), n_prog), block(64);
     size_t smem = size_t(r_lds) * 64 * sizeof(double);
-    if (spill)
+    if (variant == kPerProgram && d_table)
+        hipLaunchKernelGGL(ndvm_replay_per_program, grid, block, smem, stream, A, d_table, single);
+    else if (variant == kSpill || variant == kPerProgram)
         hipLaunchKernelGGL(ndvm_replay_spill, grid, block, smem, stream, A, d_table, single);
     else
         hipLaunchKernelGGL(ndvm_replay, grid, block, smem, stream, A, d_table, single);

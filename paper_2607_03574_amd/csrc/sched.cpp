@@ -21,6 +21,7 @@
 #include "sched.h"
 
 #include <algorithm>
+#include <map>
 #include <unordered_map>
 
 #include "isa.h"
@@ -35,12 +36,26 @@ struct Info {
     const Tape &t;
     uint32_t N, P;
     std::vector<uint8_t> kind, nel, live, active, has_adj, need_rev;
-    std::vector<uint32_t> last_use;  // last live consumer, or N when the slot is the loss
+    // Value numbering: rep[k] is the first slot that computes the same value
+    // as slot k (same opcode, shape and immediate on the same operand values;
+    // every op is a deterministic function of its operands, so the bits are
+    // equal).  Only representatives are computed; every reader of a value
+    // reads its representative's register.  Adjoints stay per slot, so each
+    // slot keeps its own adjoint rule and the reverse sweep is unchanged.
+    std::vector<uint32_t> rep;
+    std::vector<uint8_t> vlive;      // representative whose value is needed
+    std::vector<uint32_t> last_use;  // last forward reader of a value, or N for the loss
 
     explicit Info(const Tape &tape) : t(tape), N(uint32_t(tape.ops.size())), P(tape.n_params) {}
 
+    // operand values of op k (as representatives)
     template <class F>
     void for_operands(uint32_t k, F f) const {
+        for_operands_raw(k, [&](uint32_t s) { f(rep[s]); });
+    }
+    // operand slots of op k as written in the tape
+    template <class F>
+    void for_operands_raw(uint32_t k, F f) const {
         const TapeOp &o = t.ops[k];
         switch (o.code) {
         case tp::CONST: case tp::PARAM: case tp::OBS:
@@ -80,9 +95,14 @@ struct Info {
             f(o.a);
         }
     }
-    // values the adjoint rule of op k reads (k itself = its output z)
+    // values the adjoint rule of op k reads (k itself = its output z), as
+    // representatives
     template <class F>
     void for_revreads(uint32_t k, F f) const {
+        for_revreads_raw(k, [&](uint32_t s) { f(rep[s]); });
+    }
+    template <class F>
+    void for_revreads_raw(uint32_t k, F f) const {
         const TapeOp &o = t.ops[k];
         switch (o.code) {
         case tp::MUL: case tp::DOT: case tp::MATMUL: case tp::OUTER: case tp::SELECT:
@@ -99,6 +119,19 @@ struct Info {
         }
     }
 
+    void number_values() {
+        rep.assign(N, 0);
+        std::map<std::vector<uint32_t>, uint32_t> first;
+        std::vector<uint32_t> key;
+        for (uint32_t k = 0; k < N; ++k) {
+            const TapeOp &o = t.ops[k];
+            key.assign({o.code, o.rows, o.cols, o.imm});
+            for_operands_raw(k, [&](uint32_t s) { key.push_back(rep[s]); });
+            auto it = first.emplace(key, k).first;
+            rep[k] = it->second;
+        }
+    }
+
     void analyse() {
         kind.assign(N, K_COMP);
         nel.assign(N, 1);
@@ -107,14 +140,13 @@ struct Info {
             kind[k] = c == tp::CONST ? K_CONST : c == tp::OBS ? K_OBS : c == tp::PARAM ? K_PARAM : K_COMP;
             nel[k] = uint8_t(t.nel(k));
         }
+        number_values();
+        // structure of the trace: slots the loss depends on (every one keeps
+        // its adjoint rule, duplicates included)
         live.assign(N, 0);
         live[t.loss] = 1;
         for (uint32_t k = N; k-- > 0;)
-            if (live[k]) for_operands(k, [&](uint32_t s) { live[s] = 1; });
-        last_use.assign(N, 0);
-        for (uint32_t k = 0; k < N; ++k)
-            if (live[k]) for_operands(k, [&](uint32_t s) { last_use[s] = k; });
-        last_use[t.loss] = N;
+            if (live[k]) for_operands_raw(k, [&](uint32_t s) { live[s] = 1; });
         active.assign(N, 0);
         for (uint32_t k = 0; k < N; ++k) {
             if (kind[k] == K_PARAM) { active[k] = 1; continue; }
@@ -133,6 +165,18 @@ struct Info {
                 if (active[s]) has_adj[s] = 1;
             });
         }
+        // values to compute: the loss, what the adjoint rules read, and what
+        // those depend on
+        vlive.assign(N, 0);
+        vlive[rep[t.loss]] = 1;
+        for (uint32_t k = N; k-- > 0;) {
+            if (need_rev[k]) for_revreads(k, [&](uint32_t s) { vlive[s] = 1; });
+            if (vlive[k] && rep[k] == k) for_operands(k, [&](uint32_t s) { vlive[s] = 1; });
+        }
+        last_use.assign(N, 0);
+        for (uint32_t k = 0; k < N; ++k)
+            if (vlive[k] && rep[k] == k) for_operands(k, [&](uint32_t s) { last_use[s] = k; });
+        last_use[rep[t.loss]] = N;
     }
 };
 
@@ -243,7 +287,8 @@ struct Builder {
 
     explicit Builder(const Info &info) : I(info), t(info.t), N(info.N), P(info.P) {}
 
-    bool comp_live(uint32_t s) const { return I.kind[s] == K_COMP && I.live[s]; }
+    // a computed value the program needs (representatives only)
+    bool comp_live(uint32_t s) const { return I.kind[s] == K_COMP && I.vlive[s]; }
 
     void set_cuts(const std::vector<uint32_t> &c) {
         cuts = c;
@@ -620,7 +665,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
                 ++next_cut;
             }
         }
-        if (B.comp_live(k) || (I.kind[k] == K_OBS && I.live[k])) fa.push_back({I_FWD, k, 0});
+        if (B.comp_live(k) || (I.kind[k] == K_OBS && I.vlive[k])) fa.push_back({I_FWD, k, 0});
     }
     fa.push_back({I_STLOSS, t.loss, 0});
     fa = bundle_forward(I, fa);
@@ -651,6 +696,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
 
     auto res_reg = [&](uint32_t s) { return kConst0 + nc + B.res_off[s]; };
     auto fwd_operand = [&](uint32_t s) -> uint32_t {
+        s = I.rep[s];
         switch (I.kind[s]) {
         case K_CONST: return kConst0 + t.ops[s].imm;
         case K_PARAM: return t.ops[s].imm;
@@ -872,6 +918,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     S.n_regs = kStatic + std::max(fhwm, rhwm);
 
     auto rev_operand = [&](uint32_t s, uint32_t j) -> uint32_t {
+        s = I.rep[s];
         switch (I.kind[s]) {
         case K_CONST: return kConst0 + t.ops[s].imm;
         case K_PARAM: return t.ops[s].imm;
@@ -1133,7 +1180,7 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget) {
     I.analyse();
     uint64_t total = 0;
     for (uint32_t k = 0; k < I.N; ++k)
-        if (I.kind[k] == K_COMP && I.live[k]) total += I.nel[k];
+        if (I.kind[k] == K_COMP && I.vlive[k]) total += I.nel[k];
     const uint32_t kResidentAfter = 2;   // checkpointed in more segments -> keep resident
     auto trial = [&](uint64_t S) {
         Builder B(I);
