@@ -13,12 +13,13 @@
 #include <new>
 
 #include "common.h"
-#include "isa.h"
+#include "slot.h"
 #include "sched.h"
 
 namespace ndvm {
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, int variant, hipStream_t stream);
+                         uint32_t r_lds, int variant, uint32_t slots, hipStream_t stream);
+bool slots_supported(uint32_t S);
 }
 
 using namespace ndvm;
@@ -56,24 +57,35 @@ ndvm_status device_props(DeviceProps *out) {
     return NDVM_OK;
 }
 
-constexpr size_t kRegBytes = 64 * sizeof(double);   // one register of one wave
-constexpr uint32_t kMaxWavesPerCuTarget = 8;
+constexpr uint32_t kMaxWavesPerCuTarget = 16;
+
+// Micro-ops per instruction (threads per lane) of a launch: 4 slots (16
+// lanes per wave), so each lane's independent micro-ops run side by side and
+// the launch has four times as many waves as lanes / 64.
+uint32_t choose_slots(const DeviceProps &p, int64_t L, int64_t n_prog) {
+    (void)p;
+    (void)L;
+    (void)n_prog;
+    return slot::kMaxSlots;
+}
+// bytes of one register of one wave (64/S lanes)
+size_t reg_bytes(uint32_t S) { return size_t(64 / S) * sizeof(double); }
+int64_t waves_of(int64_t L, int64_t n_prog, uint32_t S) { return (L + 64 / S - 1) / (64 / S) * n_prog; }
 
 // Registers per lane that may live in LDS for a launch of `waves` waves:
-// enough waves resident per CU to cover the launch (at most 8), LDS split
+// enough waves resident per CU to cover the launch (at most 16), LDS split
 // evenly between them.
-uint32_t reg_budget(const DeviceProps &p, int64_t waves) {
+uint32_t reg_budget(const DeviceProps &p, int64_t waves, uint32_t S) {
     int64_t per_cu = (waves + p.cus - 1) / p.cus;
     per_cu = std::max<int64_t>(1, std::min<int64_t>(per_cu, kMaxWavesPerCuTarget));
     size_t bytes = std::min(p.lds_per_cu / size_t(per_cu), p.lds_per_block);
-    return uint32_t(bytes / kRegBytes);
+    return uint32_t(bytes / reg_bytes(S));
 }
 
 struct DevProg {
-    Schedule meta;          // host copy of counts (code/aux vectors released)
-    void *buf = nullptr;    // device: code | aux | consts
+    Schedule meta;          // host copy of counts (code vector released)
+    void *buf = nullptr;    // device: code | consts
     const uint32_t *code = nullptr;
-    const uint32_t *aux = nullptr;
     const double *consts = nullptr;
     ~DevProg() {
         if (buf) (void)hipFree(buf);
@@ -91,24 +103,26 @@ struct ndvm_tape {
     uint32_t n_selects = 0;
     int policy = NDVM_POLICY_RECOMPUTE;
     std::mutex mu;
-    std::unique_ptr<DevProg> fwd;
-    std::map<uint32_t, std::unique_ptr<DevProg>> grad;   // keyed by register budget
+    std::map<uint32_t, std::unique_ptr<DevProg>> fwd;    // keyed by slot count
+    std::map<uint64_t, std::unique_ptr<DevProg>> grad;   // keyed by (slot count, register budget)
 };
 
 namespace {
 
 ndvm_status upload_program(Schedule &&S, const Tape &t, hipStream_t stream, std::unique_ptr<DevProg> *out) {
-    // the kernel fetches whole chunks and reads one chunk past the END one
+    // the kernel fetches whole chunks and reads two chunks past the one that
+    // holds END
     const uint64_t end_at = uint64_t(S.n_instr) - 1;   // index of the END instruction
-    if (S.code.size() % isa::kChunkWords != 0 || S.n_instr == 0 || end_at % isa::kChunkInstr != 0 ||
-        end_at + 2 * isa::kChunkInstr > S.code.size() / isa::kWords ||
-        (S.code[end_at * isa::kWords] & 0xFF) != isa::END) {
+    if (S.code.size() != uint64_t(S.n_chunks) * slot::kChunkWords || S.n_instr == 0 ||
+        end_at / slot::kChunk + 1 + slot::kFetchAhead > S.n_chunks ||
+        slot::form_of(S.code[end_at / slot::kChunk * slot::kChunkWords + (end_at % slot::kChunk) * 4]) !=
+            slot::END) {
         set_error("internal: device program is not padded to the fetch chunks");
         return NDVM_E_TAPE;
     }
     auto dp = std::make_unique<DevProg>();
-    size_t code_b = S.code.size() * 4, aux_b = S.aux.size() * 4, con_b = S.consts.size() * 8;
-    size_t aux_off = (code_b + 255) / 256 * 256, con_off = aux_off + (aux_b + 255) / 256 * 256;
+    size_t code_b = S.code.size() * 4, con_b = S.consts.size() * 8;
+    size_t con_off = (code_b + 255) / 256 * 256;
     size_t total = con_off + std::max<size_t>(con_b, 8);
     if (hipMalloc(&dp->buf, total) != hipSuccess) {
         (void)hipGetLastError();
@@ -118,7 +132,6 @@ ndvm_status upload_program(Schedule &&S, const Tape &t, hipStream_t stream, std:
     }
     std::vector<uint8_t> host(total, 0);
     std::memcpy(host.data(), S.code.data(), code_b);
-    if (aux_b) std::memcpy(host.data() + aux_off, S.aux.data(), aux_b);
     if (con_b) std::memcpy(host.data() + con_off, S.consts.data(), con_b);
     if (hipMemcpyAsync(dp->buf, host.data(), total, hipMemcpyHostToDevice, stream) != hipSuccess ||
         hipStreamSynchronize(stream) != hipSuccess) {
@@ -126,26 +139,58 @@ ndvm_status upload_program(Schedule &&S, const Tape &t, hipStream_t stream, std:
         return NDVM_E_DEVICE;
     }
     dp->code = reinterpret_cast<const uint32_t *>(dp->buf);
-    dp->aux = reinterpret_cast<const uint32_t *>(static_cast<uint8_t *>(dp->buf) + aux_off);
     dp->consts = reinterpret_cast<const double *>(static_cast<uint8_t *>(dp->buf) + con_off);
     S.code.clear();
     S.code.shrink_to_fit();
-    S.aux.clear();
-    S.aux.shrink_to_fit();
     dp->meta = std::move(S);
     *out = std::move(dp);
+    (void)t;
     return NDVM_OK;
 }
 
-// Device program of `tape` for gradient launches with register budget b.
-ndvm_status grad_program(ndvm_tape *tape, uint32_t b, hipStream_t stream, DevProg **out) {
+// Schedule a program, turning scheduler limits into a status.
+template <class F>
+ndvm_status scheduled(F f, Schedule *out) {
+    try {
+        *out = f();
+    } catch (const std::length_error &e) {
+        set_error(std::string("program too large for the device format: ") + e.what());
+        return NDVM_E_UNSUPPORTED;
+    }
+    return NDVM_OK;
+}
+
+// Device program of `tape` for gradient launches with S slots and register
+// budget b.
+ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, hipStream_t stream, DevProg **out) {
     std::lock_guard<std::mutex> lk(tape->mu);
-    auto it = tape->grad.find(b);
+    const uint64_t key = (uint64_t(S) << 32) | b;
+    auto it = tape->grad.find(key);
     if (it == tape->grad.end()) {
-        std::unique_ptr<DevProg> dp;
-        ndvm_status st = upload_program(schedule_grad(tape->tape, b), tape->tape, stream, &dp);
+        Schedule sch;
+        ndvm_status st = scheduled([&] { return schedule_grad(tape->tape, b, S); }, &sch);
         if (st != NDVM_OK) return st;
-        it = tape->grad.emplace(b, std::move(dp)).first;
+        std::unique_ptr<DevProg> dp;
+        st = upload_program(std::move(sch), tape->tape, stream, &dp);
+        if (st != NDVM_OK) return st;
+        it = tape->grad.emplace(key, std::move(dp)).first;
+    }
+    *out = it->second.get();
+    return NDVM_OK;
+}
+
+// Forward-only device program of `tape` with S slots.
+ndvm_status fwd_program(ndvm_tape *tape, uint32_t S, hipStream_t stream, DevProg **out) {
+    std::lock_guard<std::mutex> lk(tape->mu);
+    auto it = tape->fwd.find(S);
+    if (it == tape->fwd.end()) {
+        Schedule sch;
+        ndvm_status st = scheduled([&] { return schedule_forward(tape->tape, S); }, &sch);
+        if (st != NDVM_OK) return st;
+        std::unique_ptr<DevProg> dp;
+        st = upload_program(std::move(sch), tape->tape, stream, &dp);
+        if (st != NDVM_OK) return st;
+        it = tape->fwd.emplace(S, std::move(dp)).first;
     }
     *out = it->second.get();
     return NDVM_OK;
@@ -153,15 +198,17 @@ ndvm_status grad_program(ndvm_tape *tape, uint32_t b, hipStream_t stream, DevPro
 
 int64_t lpad_of(int64_t L) { return (L + 63) / 64 * 64; }
 
-// Workspace rows (fp64 per lane) of one program launched with LDS budget b.
+// Workspace rows (fp64 per lane) of one program launched with LDS budget b:
+// checkpoint rows, the trash row that unused slots store to, spill rows.
 uint64_t ws_rows(const DevProg &dp, uint32_t b) {
     uint32_t r_lds = std::min(dp.meta.n_regs, b);
-    return uint64_t(dp.meta.n_ckpt_rows) + (dp.meta.n_regs - r_lds);
+    return uint64_t(dp.meta.n_ckpt_rows) + 1 + (dp.meta.n_regs - r_lds);
 }
 
 ndvm_status check_stream_and_launch(const LaunchArgs &A, const ProgStatic *table, const ProgStatic &single,
-                                    uint32_t n_prog, uint32_t r_lds, int variant, hipStream_t stream) {
-    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, variant, stream);
+                                    uint32_t n_prog, uint32_t r_lds, int variant, uint32_t slots,
+                                    hipStream_t stream) {
+    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, variant, slots, stream);
     if (e != hipSuccess) {
         set_error(std::string("kernel launch failed: ") + hipGetErrorString(e));
         return NDVM_E_DEVICE;
@@ -232,7 +279,9 @@ ndvm_status ndvm_tape_upload(const uint8_t *bytes, size_t len, int policy, void 
         h->tape_bytes = len;
         h->policy = policy;
         for (const TapeOp &o : h->tape.ops) h->n_selects += o.code == tp::SELECT;
-        st = upload_program(schedule_forward(h->tape), h->tape, static_cast<hipStream_t>(stream), &h->fwd);
+        // schedule the forward program now: scheduling limits surface at upload
+        DevProg *fp = nullptr;
+        st = fwd_program(h.get(), 4, static_cast<hipStream_t>(stream), &fp);
         if (st != NDVM_OK) return st;
         *out = h.release();
         return NDVM_OK;
@@ -282,16 +331,19 @@ ndvm_status ndvm_workspace_bytes(const ndvm_tape *tape, int64_t L, int with_grad
         ndvm_status st = device_props(&p);
         if (st != NDVM_OK) return st;
         int64_t Lp = lpad_of(L);
-        uint32_t b = reg_budget(p, Lp / 64);
+        const uint32_t S = choose_slots(p, L, 1);
         uint64_t rows;
+        DevProg *dp;
         if (with_grad) {
-            DevProg *dp;
-            st = grad_program(const_cast<ndvm_tape *>(tape), b, nullptr, &dp);
+            uint32_t b = reg_budget(p, waves_of(L, 1, S), S);
+            st = grad_program(const_cast<ndvm_tape *>(tape), S, b, nullptr, &dp);
             if (st != NDVM_OK) return st;
             rows = ws_rows(*dp, b);
         } else {
-            uint32_t bf = uint32_t(p.lds_per_block / kRegBytes);
-            rows = ws_rows(*tape->fwd, bf);
+            uint32_t bf = uint32_t(p.lds_per_block / reg_bytes(S));
+            st = fwd_program(const_cast<ndvm_tape *>(tape), S, nullptr, &dp);
+            if (st != NDVM_OK) return st;
+            rows = ws_rows(*dp, bf);
         }
         *bytes = size_t(rows * uint64_t(Lp) * sizeof(double));
         return NDVM_OK;
@@ -308,7 +360,8 @@ ndvm_status ndvm_workspace_bytes_many(const ndvm_tape *const *tapes, int n_prog,
         ndvm_status st = device_props(&p);
         if (st != NDVM_OK) return st;
         int64_t Lp = lpad_of(L);
-        uint32_t b = reg_budget(p, Lp / 64 * n_prog);
+        const uint32_t S = choose_slots(p, L, n_prog);
+        uint32_t b = reg_budget(p, waves_of(L, n_prog, S), S);
         uint64_t rows = 0;
         for (int q = 0; q < n_prog; ++q) {
             if (!tapes[q]) {
@@ -316,7 +369,7 @@ ndvm_status ndvm_workspace_bytes_many(const ndvm_tape *const *tapes, int n_prog,
                 return NDVM_E_ARG;
             }
             DevProg *dp;
-            st = grad_program(const_cast<ndvm_tape *>(tapes[q]), b, nullptr, &dp);
+            st = grad_program(const_cast<ndvm_tape *>(tapes[q]), S, b, nullptr, &dp);
             if (st != NDVM_OK) return st;
             rows += ws_rows(*dp, b);
         }
@@ -354,8 +407,12 @@ ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
         if (L == 0) return NDVM_OK;
         DeviceProps p;
         if ((st = device_props(&p)) != NDVM_OK) return st;
-        const DevProg &dp = *tape->fwd;
-        uint32_t r_lds = std::min<uint32_t>(dp.meta.n_regs, uint32_t(p.lds_per_block / kRegBytes));
+        const uint32_t S = choose_slots(p, L, 1);
+        DevProg *fp;
+        if ((st = fwd_program(const_cast<ndvm_tape *>(tape), S, static_cast<hipStream_t>(stream), &fp)) != NDVM_OK)
+            return st;
+        const DevProg &dp = *fp;
+        uint32_t r_lds = std::min<uint32_t>(dp.meta.n_regs, uint32_t(p.lds_per_block / reg_bytes(S)));
         int64_t Lp = lpad_of(L);
         size_t need = size_t(ws_rows(dp, r_lds) * uint64_t(Lp) * sizeof(double));
         if (need && (!ws || ws_bytes < need)) {
@@ -364,8 +421,8 @@ ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
         }
         LaunchArgs A{obs, params, loss, loss, static_cast<double *>(ws), ld_p, 0, L, Lp, 0, 0};
         const bool spills = dp.meta.n_regs > r_lds;
-        ProgStatic S{dp.code, dp.aux, dp.consts, 0, 0, r_lds, spills};
-        return check_stream_and_launch(A, nullptr, S, 1, r_lds, spills ? kSpill : kLdsOnly,
+        ProgStatic D{dp.code, dp.consts, 0, uint64_t(dp.meta.n_ckpt_rows) + 1, r_lds, spills};
+        return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, S,
                                        static_cast<hipStream_t>(stream));
     });
 }
@@ -384,9 +441,10 @@ ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L, in
         DeviceProps p;
         if ((st = device_props(&p)) != NDVM_OK) return st;
         int64_t Lp = lpad_of(L);
-        uint32_t b = reg_budget(p, Lp / 64);
+        const uint32_t S = choose_slots(p, L, 1);
+        uint32_t b = reg_budget(p, waves_of(L, 1, S), S);
         DevProg *dp;
-        if ((st = grad_program(const_cast<ndvm_tape *>(tape), b, static_cast<hipStream_t>(stream), &dp)) != NDVM_OK)
+        if ((st = grad_program(const_cast<ndvm_tape *>(tape), S, b, static_cast<hipStream_t>(stream), &dp)) != NDVM_OK)
             return st;
         uint32_t r_lds = std::min(dp->meta.n_regs, b);
         size_t need = size_t(ws_rows(*dp, b) * uint64_t(Lp) * sizeof(double));
@@ -397,8 +455,8 @@ ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L, in
         double *wsd = static_cast<double *>(ws);
         LaunchArgs A{obs, params, loss, grad, wsd, ld_p, ld_g, L, Lp, 0, 0};
         const bool spills = dp->meta.n_regs > r_lds;
-        ProgStatic S{dp->code, dp->aux, dp->consts, 0, dp->meta.n_ckpt_rows, r_lds, spills};
-        return check_stream_and_launch(A, nullptr, S, 1, r_lds, spills ? kSpill : kLdsOnly,
+        ProgStatic D{dp->code, dp->consts, 0, uint64_t(dp->meta.n_ckpt_rows) + 1, r_lds, spills};
+        return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, S,
                                        static_cast<hipStream_t>(stream));
     });
 }
@@ -428,7 +486,8 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
         if (st != NDVM_OK) return st;
         hipStream_t s = static_cast<hipStream_t>(stream);
         int64_t Lp = lpad_of(L);
-        uint32_t b = reg_budget(p, Lp / 64 * n_prog);
+        const uint32_t S = choose_slots(p, L, n_prog);
+        uint32_t b = reg_budget(p, waves_of(L, n_prog, S), S);
         std::vector<ProgStatic> table(static_cast<size_t>(n_prog), ProgStatic{});
         std::vector<uint64_t> key;
         uint64_t row = 0;
@@ -436,15 +495,15 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
         int n_spill = 0;
         for (int q = 0; q < n_prog; ++q) {
             DevProg *dp;
-            if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), b, s, &dp)) != NDVM_OK) return st;
+            if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), S, b, s, &dp)) != NDVM_OK) return st;
             uint32_t r_lds = std::min(dp->meta.n_regs, b);
             r_launch = std::max(r_launch, r_lds);
             const bool spills = dp->meta.n_regs > r_lds;
             n_spill += spills;
-            table[q] = ProgStatic{dp->code, dp->aux, dp->consts, row, row + dp->meta.n_ckpt_rows, r_lds, spills};
+            table[q] = ProgStatic{dp->code, dp->consts, row, row + dp->meta.n_ckpt_rows + 1, r_lds, spills};
             row += ws_rows(*dp, b);
             key.push_back(tapes[q]->id);
-            key.push_back(b);
+            key.push_back((uint64_t(S) << 32) | b);
         }
         size_t need = size_t(row * uint64_t(Lp) * sizeof(double));
         if (need && (!ws || ws_bytes < need)) {
@@ -478,7 +537,7 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
         ProgStatic none{};
         const int variant = n_spill == 0 ? kLdsOnly : n_spill == n_prog ? kSpill : kPerProgram;
         return check_stream_and_launch(A, static_cast<const ProgStatic *>(d_table), none, uint32_t(n_prog),
-                                       r_launch, variant, s);
+                                       r_launch, variant, S, s);
     });
 }
 

@@ -1,67 +1,91 @@
-// Host emulator of the device program -- a checking tool for the scheduler,
-// built into its own library (libndvm_emu.so) that only the CPU tests load;
-// the product binding never calls it.
+// Host emulator of slot programs -- a checking tool for the scheduler, built
+// into its own library (libndvm_emu.so) that only the CPU tests load; the
+// product binding never calls it.
 //
 // It schedules a tape exactly as ndvm_tape_upload / ndvm_grad do and runs the
-// resulting program lane by lane through the same instruction handlers the
-// GPU kernel uses, with every register access bounds-checked and every read
-// of a never-written register reported.  That exposes register-allocation,
-// checkpoint and first-contribution mistakes without a GPU.
+// resulting program lane by lane through the same micro-op handlers the GPU
+// kernel uses.  Every slot of an instruction reads before any slot writes
+// (writes are buffered until the instruction ends, as on the GPU); every
+// register access is bounds-checked, every read of a never-written register
+// is reported, and so is a slot that reads or writes a register another slot
+// of the same instruction writes.  That exposes register-allocation,
+// checkpoint, packing and first-contribution mistakes without a GPU.
 #include <cmath>
 #include <algorithm>
 #include <cstdio>
 #include <vector>
 
 #include "common.h"
-#include "replay.h"
 #include "sched.h"
+#include "slot_exec.h"
 
 using namespace ndvm;
 
 namespace {
 
+struct P4 {
+    uint32_t x, y, z, w;
+    uint32_t u1() const { return y; }
+    uint32_t u2() const { return z; }
+    uint32_t u3() const { return w; }
+};
+
 struct HostCtx {
-    const uint32_t *code_end;
     double *regs;
     uint8_t *written;
-    uint32_t n_regs;
+    uint32_t n_regs, sink;
     const double *consts, *obs, *params;
     uint32_t n_consts, n_obs, n_params;
     double *loss, *grad;
     double *ckpt;
-    uint32_t n_ckpt;
-    int *fault;       // first problem seen: 1 register range, 2 unwritten read, 3 pool, 4 ckpt,
-                      // 5 program fetch beyond the padded program
+    uint32_t n_ckpt;   // rows including the trash row
+    int *fault;        // first problem seen: 1 register range, 2 unwritten read, 3 pool/param/obs index,
+                       // 4 ckpt row, 6 read of a register another slot writes, 7 two slots write one register,
+                       // 8 form differs between slots
+    uint32_t cur_slot = 0;
+    bool cur_dummy = false;   // an unused slot (result to the sink): its reads are never checked
+    std::vector<std::pair<uint32_t, double>> *pending;
+    std::vector<uint32_t> *pend_slot;
 
     static uint32_t uni(uint32_t x) { return x; }
-    static bool all(bool b) { return b; }
-    using Chunk = const uint32_t *;
-    Chunk load_chunk(const uint32_t *p) const {
-        if (p + isa::kChunkWords > code_end) flag(5);
-        return p;
-    }
-    static const uint32_t *instr(Chunk ch, uint32_t i) { return ch + i * isa::kWords; }
-    static uint32_t aux_word(const uint32_t *aux, uint32_t i) { return aux[i]; }
+    uint32_t slot() const { return cur_slot; }
     void flag(int code) const {
         if (*fault == 0) *fault = code;
     }
-    double ld(uint32_t r) const {
+    void check_pending_read(uint32_t r) const {
+        if (cur_dummy) return;
+        for (size_t i = 0; i < pending->size(); ++i)
+            if ((*pending)[i].first == r && (*pend_slot)[i] != cur_slot) flag(6);
+    }
+    double ld(uint32_t f) const {
+        const uint32_t r = f & slot::kFieldMask;
         if (r >= n_regs) { flag(1); return NAN; }
+        check_pending_read(r);
         if (!written[r]) flag(2);
         return regs[r];
     }
-    double ld_raw(uint32_t r) const {
+    double ld_raw(uint32_t f) const {
+        const uint32_t r = f & slot::kFieldMask;
         if (r >= n_regs) { flag(1); return NAN; }
+        if (r != sink) check_pending_read(r);
         return regs[r];
     }
-    static uint32_t half(uint32_t word, int hi) { return hi ? word >> 16 : word & 0xFFFFu; }
-    double ldh(uint32_t word, int hi) const { return ld(half(word, hi)); }
-    double ldh_raw(uint32_t word, int hi) const { return ld_raw(half(word, hi)); }
-    void sth(uint32_t word, int hi, double v) const { st(half(word, hi), v); }
-    void st(uint32_t r, double v) const {
+    void st(uint32_t f, double v) const {
+        const uint32_t r = f & slot::kFieldMask;
         if (r >= n_regs) { flag(1); return; }
-        regs[r] = v;
-        written[r] = 1;
+        if (r != sink)
+            for (const auto &pw : *pending)
+                if (pw.first == r) flag(7);
+        pending->push_back({r, v});
+        pend_slot->push_back(cur_slot);
+    }
+    void commit() const {
+        for (const auto &pw : *pending) {
+            regs[pw.first] = pw.second;
+            written[pw.first] = 1;
+        }
+        pending->clear();
+        pend_slot->clear();
     }
     double konst(uint32_t i) const {
         if (i >= n_consts) { flag(3); return NAN; }
@@ -75,20 +99,27 @@ struct HostCtx {
         if (p >= n_params) { flag(3); return NAN; }
         return params[p];
     }
-    void store_loss(double v) const { *loss = v; }
-    void store_grad(uint32_t p, double v) const {
+    void store_loss(double v, bool on) const {
+        if (on) *loss = v;
+    }
+    void store_grad(uint32_t p, double v, bool on) const {
+        if (!on) return;
         if (p >= n_params) { flag(3); return; }
         grad[p] = v;
     }
-    void ckpt_st(uint32_t row, double v) const {
+    void ckst(uint32_t row, double v) const {
         if (row >= n_ckpt) { flag(4); return; }
         ckpt[row] = v;
     }
-    double ckpt_ld(uint32_t row) const {
+    double ckld(uint32_t row) const {
         if (row >= n_ckpt) { flag(4); return NAN; }
         return ckpt[row];
     }
 };
+
+Schedule schedule(const Tape &t, int with_grad, uint32_t reg_budget, uint32_t slots) {
+    return with_grad ? schedule_grad(t, reg_budget, slots) : schedule_forward(t, slots);
+}
 
 }  // namespace
 
@@ -96,33 +127,74 @@ extern "C" {
 
 /*
  * Schedule `tape` (forward-only when with_grad == 0, else the gradient
- * program for `reg_budget` registers) and run it for L lanes on the host.
- * stats (optional, 8 entries): n_regs, n_ckpt_rows, n_segments, n_instr,
- * fwd ops, recompute ops, reverse ops, checkpoint elements stored.
+ * program for `reg_budget` registers) with `slots` micro-ops per instruction
+ * and run it for L lanes on the host.  stats (optional, 10 entries): n_regs,
+ * n_ckpt_rows, n_segments, n_instr, fwd ops, recompute ops, reverse ops,
+ * checkpoint elements stored, micro-ops, slots used.
  * Returns 0, an ndvm_status from parsing, or 100 + fault code.
  */
-int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_budget, const double *params,
-                 int64_t L, int64_t ld_p, const double *obs, int64_t n_obs, double *loss, double *grad,
-                 int64_t ld_g, uint64_t *stats) {
+int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_budget, uint32_t slots,
+                 const double *params, int64_t L, int64_t ld_p, const double *obs, int64_t n_obs, double *loss,
+                 double *grad, int64_t ld_g, uint64_t *stats) {
     Tape t;
     ndvm_status st = parse_tape(tape, len, &t);
     if (st != NDVM_OK) return st;
     if (n_obs != int64_t(t.n_obs)) return NDVM_E_ARG;
-    Schedule S = with_grad ? schedule_grad(t, reg_budget) : schedule_forward(t);
-    if (stats) {
-        uint64_t v[8] = {S.n_regs, S.n_ckpt_rows, S.n_segments, S.n_instr, S.n_fwd_ops,
-                         S.n_recompute_ops, S.n_rev_ops, S.ckpt_elems_stored};
-        for (int i = 0; i < 8; ++i) stats[i] = v[i];
+    if (slots != 1 && slots != 2 && slots != 4) return NDVM_E_ARG;
+    Schedule S;
+    try {
+        S = schedule(t, with_grad, reg_budget, slots);
+    } catch (const std::exception &e) {
+        set_error(e.what());
+        return NDVM_E_UNSUPPORTED;
     }
-    std::vector<double> regs(S.n_regs), ck(S.n_ckpt_rows);
+    if (stats) {
+        uint64_t v[10] = {S.n_regs, S.n_ckpt_rows, S.n_segments, S.n_instr, S.n_fwd_ops,
+                          S.n_recompute_ops, S.n_rev_ops, S.ckpt_elems_stored, S.n_uops, S.n_slots_used};
+        for (int i = 0; i < 10; ++i) stats[i] = v[i];
+    }
+    const uint32_t sink = 2 * t.n_params;
+    std::vector<double> regs(S.n_regs), ck(size_t(S.n_ckpt_rows) + 1);
     std::vector<uint8_t> written(S.n_regs);
+    std::vector<std::pair<uint32_t, double>> pending;
+    std::vector<uint32_t> pend_slot;
+    const uint32_t K = slot::kChunk;
     for (int64_t l = 0; l < L; ++l) {
         std::fill(written.begin(), written.end(), 0);
         int fault = 0;
-        HostCtx c{S.code.data() + S.code.size(), regs.data(), written.data(), S.n_regs, S.consts.data(), obs, params + l * ld_p,
+        HostCtx c{regs.data(), written.data(), S.n_regs, sink, S.consts.data(), obs, params + l * ld_p,
                   uint32_t(S.consts.size()), uint32_t(n_obs), t.n_params, loss + l,
-                  grad ? grad + l * ld_g : nullptr, ck.data(), S.n_ckpt_rows, &fault};
-        replay::run(c, S.code.data(), S.aux.data());
+                  grad ? grad + l * ld_g : nullptr, ck.data(), S.n_ckpt_rows + 1, &fault, 0, false, &pending,
+                  &pend_slot};
+        bool ended = false;
+        for (uint64_t i = 0; i < uint64_t(S.n_chunks) * K && !ended && !fault; ++i) {
+            // slot sl's words sit in rows sl * 4 / S ..; take the first
+            auto words = [&](uint32_t sl) {
+                const uint32_t r = sl * slot::kRows / slots;
+                const uint32_t *w = &S.code[size_t(i / K) * slot::kChunkWords + (size_t(r) * K + i % K) * 4];
+                return P4{w[0], w[1], w[2], w[3]};
+            };
+            const uint32_t form = slot::form_of(words(0).x);
+            if (form == slot::END) {
+                ended = true;
+                break;
+            }
+            for (uint32_t sl = 0; sl < slots; ++sl) {
+                const P4 p = words(sl);
+                if (slot::form_of(p.x) != form || (p.y >> 24) != (words(0).y >> 24) ||
+                    (p.z >> 24) != (words(0).z >> 24) || (p.w >> 24) != (words(0).w >> 24))
+                    c.flag(8);
+                c.cur_slot = sl;
+                c.cur_dummy = (slot::writes_a(form) && (p.x & slot::kFieldMask) == sink) ||
+                              (form == slot::CKST && (p.y & slot::kFieldMask) == S.n_ckpt_rows);
+                if (slot::is_hot(form))
+                    slotx::exec_hot(c, form, p);
+                else
+                    slotx::exec_cold(c, form, p);
+            }
+            c.commit();
+        }
+        if (!ended && !fault) fault = 5;
         if (fault) {
             char m[96];
             std::snprintf(m, sizeof m, "emulator fault %d in lane %lld", fault, (long long)l);
@@ -134,17 +206,23 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
 }
 
 /*
- * Copy the device program the scheduler makes for `tape` (words, isa::kWords
- * per instruction, END-terminated) into `out` when it holds `cap` words;
- * returns the number of words, or -1 on a parse error.
+ * Copy the device program the scheduler makes for `tape` (payload words,
+ * chunk-major: [chunk][row][instr][4], slot.h) into `out` when it holds `cap` words;
+ * returns the number of words, or -1 on an error.
  */
-int64_t ndvm_emu_program(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_budget, uint32_t *out,
-                         size_t cap) {
+int64_t ndvm_emu_program(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_budget, uint32_t slots,
+                         uint32_t *out, size_t cap) {
     Tape t;
     if (parse_tape(tape, len, &t) != NDVM_OK) return -1;
-    Schedule S = with_grad ? schedule_grad(t, reg_budget) : schedule_forward(t);
-    const size_t n = size_t(S.n_instr) * isa::kWords;
-    if (out && cap >= n) std::copy(S.code.begin(), S.code.begin() + n, out);
+    Schedule S;
+    try {
+        S = schedule(t, with_grad, reg_budget, slots);
+    } catch (const std::exception &e) {
+        set_error(e.what());
+        return -1;
+    }
+    const size_t n = S.code.size();
+    if (out && cap >= n) std::copy(S.code.begin(), S.code.end(), out);
     return int64_t(n);
 }
 

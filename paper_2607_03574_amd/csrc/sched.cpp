@@ -21,10 +21,12 @@
 #include "sched.h"
 
 #include <algorithm>
+#include <cstring>
 #include <map>
+#include <stdexcept>
 #include <unordered_map>
 
-#include "isa.h"
+#include "slot.h"
 
 namespace ndvm {
 
@@ -216,46 +218,6 @@ uint32_t allocate(std::vector<Interval> &iv) {
         hwm = std::max(hwm, base + v.nel);
     }
     return hwm;
-}
-
-// elementwise ops and the select have scalar fast-path opcodes
-bool scalar_fast(uint16_t c) {
-    switch (c) {
-    case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: case tp::NEG: case tp::EXP: case tp::LOG:
-    case tp::SQRT: case tp::SIN: case tp::COS: case tp::ABS: case tp::SELECT:
-        return true;
-    }
-    return false;
-}
-bool binary_code(uint16_t c) { return c == tp::ADD || c == tp::SUB || c == tp::MUL || c == tp::DIV; }
-
-uint32_t fwd_opcode(uint16_t c) {
-    switch (c) {
-    case tp::ADD: return isa::F_ADD;
-    case tp::SUB: return isa::F_SUB;
-    case tp::MUL: return isa::F_MUL;
-    case tp::DIV: return isa::F_DIV;
-    case tp::NEG: return isa::F_NEG;
-    case tp::EXP: return isa::F_EXP;
-    case tp::LOG: return isa::F_LOG;
-    case tp::SQRT: return isa::F_SQRT;
-    case tp::SIN: return isa::F_SIN;
-    case tp::COS: return isa::F_COS;
-    case tp::ABS: return isa::F_ABS;
-    case tp::POW: return isa::F_POW;
-    case tp::DOT: return isa::F_DOT;
-    case tp::MATMUL: return isa::F_MATMUL;
-    case tp::TRANSPOSE: return isa::F_TRANSPOSE;
-    case tp::TRACE: return isa::F_TRACE;
-    case tp::INV: return isa::F_INV;
-    case tp::DET: return isa::F_DET;
-    case tp::LOGDET: return isa::F_LOGDET;
-    case tp::OUTER: return isa::F_OUTER;
-    case tp::PACK: return isa::F_PACK;
-    case tp::INDEX: return isa::F_INDEX;
-    case tp::SELECT: return isa::F_SELECT;
-    }
-    return isa::END;
 }
 
 // ------------------------------------------------------------------ builder
@@ -590,61 +552,229 @@ std::vector<AI> bundle_reverse(const Info &I, const std::vector<AI> &in) {
     return out;
 }
 
-struct Emitter {
-    std::vector<uint32_t> code, aux;
-    void put(uint32_t a, uint32_t b = 0, uint32_t c = 0, uint32_t d = 0, uint32_t e = 0, uint32_t f = 0,
-             uint32_t g = 0, uint32_t h = 0) {
-        uint32_t w[8] = {a, b, c, d, e, f, g, h};
-        code.insert(code.end(), w, w + 8);
+// ------------------------------------------------------------------ micro-ops
+// One slot's micro-op before packing: its four payload words (slot.h).
+struct UOp {
+    uint32_t w[4];
+};
+
+// Keys of what a micro-op reads and writes: registers r, checkpoint rows
+// kKeyCkpt + row, the loss, gradient entries kKeyGrad + p.
+constexpr uint64_t kKeyCkpt = 1ull << 32, kKeyLoss = 2ull << 32, kKeyGrad = 3ull << 32;
+
+void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &wr) {
+    using namespace slot;
+    rd.clear();
+    wr.clear();
+    const uint32_t f = form_of(u.w[0]);
+    const uint32_t a = u.w[0] & kFieldMask, x = u.w[1] & kFieldMask, y = u.w[2] & kFieldMask,
+                   z = u.w[3] & kFieldMask;
+    const uint32_t i1 = u.w[1] >> 24, i2 = u.w[2] >> 24, i3 = u.w[3] >> 24;
+    const bool acc_base = !(u.w[0] & kFirst);   // adjoint forms read their target
+    switch (f) {
+    case MAC:
+        rd = {x, y, z};
+        wr = {a};
+        break;
+    case ACC:
+        rd = {x, y};
+        if (acc_base) rd.push_back(z);
+        wr = {a};
+        break;
+    case MACG: case ACCD: case ACCND: case ACCSEL: case ACCABS:
+        rd = {x, y, z};
+        if (acc_base) rd.push_back(a);
+        wr = {a};
+        break;
+    case DOT: case DOTACC:
+        for (uint32_t k = 0; k < (i1 & 0x7Fu); ++k) {
+            rd.push_back(x + k * i2);
+            rd.push_back(y + k * i3);
+        }
+        if (f == DOTACC) {
+            rd.push_back(z);
+            if (acc_base) rd.push_back(a);
+        }
+        wr = {a};
+        break;
+    case DIV: case CMPLT: case POW:
+        rd = {x, y};
+        wr = {a};
+        break;
+    case SELP: case GATEGT:
+        rd = {x, y, z};
+        wr = {a};
+        break;
+    case DET2:
+        rd = {x, x + 1, x + 2, x + 3};
+        wr = {a};
+        break;
+    case NZ:
+        for (uint32_t k = 0; k < i1; ++k) rd.push_back(x + k);
+        wr = {a};
+        break;
+    case SUMK:
+        for (uint32_t k = 0; k < i1; ++k) rd.push_back(x + k * i2);
+        wr = {a};
+        break;
+    case UN:
+        rd = {x};
+        wr = {a};
+        break;
+    case LDOBS: case LDPARAM: case LDCONST: case ZERO:
+        wr = {a};
+        break;
+    case CKST:
+        rd = {a};
+        wr = {kKeyCkpt + x};
+        break;
+    case CKLD:
+        rd = {kKeyCkpt + x};
+        wr = {a};
+        break;
+    case STLOSS:
+        rd = {a};
+        wr = {kKeyLoss};
+        break;
+    case STGRAD:
+        rd = {a};
+        wr = {kKeyGrad + x};
+        break;
+    default:
+        break;
+    }
+}
+
+// Instruction class of a micro-op: form and uniform immediates must agree
+// for micro-ops to share an instruction.
+uint32_t uop_class(const UOp &u) {
+    return slot::form_of(u.w[0]) | ((u.w[1] >> 24) << 6) | ((u.w[2] >> 24) << 14) | ((u.w[3] >> 24) << 22);
+}
+
+// Pack micro-ops (in program order) into instructions of at most S slots:
+// list scheduling in which the oldest unscheduled micro-op opens each
+// instruction and later micro-ops of the same class join it when every value
+// they read or overwrite is final (true and output dependences satisfied by
+// earlier instructions; a micro-op may overwrite a register that another slot
+// of the same instruction reads, since every slot reads before any writes).
+// Each register and memory cell therefore sees its reads and writes in
+// program order, so results are those of the sequential program.
+constexpr uint32_t kPackWindow = 160;
+
+std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S) {
+    const uint32_t n = uint32_t(ops.size());
+    std::vector<uint32_t> hard_off(n + 1, 0), soft_off(n + 1, 0), hard, soft;
+    {
+        std::unordered_map<uint64_t, uint32_t> dense;
+        std::vector<int64_t> last_w;
+        std::vector<std::vector<uint32_t>> readers;
+        std::vector<uint64_t> rd, wr;
+        auto id = [&](uint64_t key) {
+            auto it = dense.emplace(key, uint32_t(last_w.size())).first;
+            if (it->second == last_w.size()) {
+                last_w.push_back(-1);
+                readers.emplace_back();
+            }
+            return it->second;
+        };
+        for (uint32_t j = 0; j < n; ++j) {
+            uop_access(ops[j], rd, wr);
+            for (uint64_t r : rd) {
+                const uint32_t d = id(r);
+                if (last_w[d] >= 0) hard.push_back(uint32_t(last_w[d]));
+            }
+            for (uint64_t w : wr) {
+                const uint32_t d = id(w);
+                if (last_w[d] >= 0) hard.push_back(uint32_t(last_w[d]));
+                for (uint32_t p : readers[d])
+                    if (p != j) soft.push_back(p);
+            }
+            hard_off[j + 1] = uint32_t(hard.size());
+            soft_off[j + 1] = uint32_t(soft.size());
+            for (uint64_t r : rd) readers[id(r)].push_back(j);
+            for (uint64_t w : wr) {
+                const uint32_t d = id(w);
+                last_w[d] = j;
+                readers[d].clear();
+            }
+        }
+    }
+    std::vector<uint32_t> cls(n);
+    for (uint32_t j = 0; j < n; ++j) cls[j] = uop_class(ops[j]);
+    std::vector<int64_t> at(n, -1);
+    std::vector<std::vector<uint32_t>> out;
+    uint32_t front = 0;
+    while (front < n) {
+        const int64_t ni = int64_t(out.size());
+        std::vector<uint32_t> cur{front};
+        at[front] = ni;
+        for (uint32_t j = front + 1; j < n && j < front + kPackWindow && cur.size() < S; ++j) {
+            if (at[j] >= 0 || cls[j] != cls[front]) continue;
+            bool ok = true;
+            for (uint32_t q = hard_off[j]; q < hard_off[j + 1] && ok; ++q) ok = at[hard[q]] >= 0 && at[hard[q]] < ni;
+            for (uint32_t q = soft_off[j]; q < soft_off[j + 1] && ok; ++q) ok = at[soft[q]] >= 0;
+            if (ok) {
+                at[j] = ni;
+                cur.push_back(j);
+            }
+        }
+        out.push_back(std::move(cur));
+        while (front < n && at[front] >= 0) ++front;
+    }
+    return out;
+}
+
+// Micro-op emitter of one program: registers named by the scheduler, plus a
+// rotating pool of temporaries for values that live inside one op's
+// lowering (predicates, node gates, partial products, 2x2 inverses).
+struct UEmit {
+    std::vector<UOp> ops;
+    uint32_t tmp0 = 0, n_tmp = 0, next_tmp = 0;
+    void put(uint32_t form, uint32_t a, uint32_t flags, uint32_t x = 0, uint32_t y = 0, uint32_t z = 0,
+             uint32_t i1 = 0, uint32_t i2 = 0, uint32_t i3 = 0) {
+        if (a > slot::kMaxField || x > slot::kMaxField || y > slot::kMaxField || z > slot::kMaxField ||
+            i1 > 255 || i2 > 255 || i3 > 255)
+            throw std::length_error("register or index beyond the 24-bit fields of the device program");
+        ops.push_back({{slot::word0(form, a, flags), slot::fieldw(x, i1), slot::fieldw(y, i2), slot::fieldw(z, i3)}});
+    }
+    uint32_t used_tmp = 0;   // temporaries touched (0 when the program needs none)
+    // a block of n consecutive temporaries
+    uint32_t tmp(uint32_t n = 1) {
+        if (next_tmp + n > n_tmp) next_tmp = 0;
+        const uint32_t r = tmp0 + next_tmp;
+        next_tmp += n;
+        used_tmp = std::max(used_tmp, next_tmp);
+        return r;
     }
 };
 
-// Terminate the program: NOPs up to the next fetch chunk, a chunk of END,
-// and the chunk the fetch reads ahead (also END).
-bool repeatable(uint32_t op) {
-    return (op >= isa::FB1 && op <= isa::RDBS3) || (op >= isa::OB2 && op <= isa::OB4) || op == isa::F_MATMUL ||
-           op == isa::R_MATMUL;
-}
-
-void finish(Emitter &E, Schedule &S) {
-    const size_t n = E.code.size() / isa::kWords;
-    for (size_t k = 0; k + 1 < n; ++k) {
-        uint32_t &w0 = E.code[k * isa::kWords];
-        const uint32_t op = w0 & 0xFF;
-        if (repeatable(op) && (k + 1) % isa::kChunkInstr != 0 && (E.code[(k + 1) * isa::kWords] & 0xFF) == op)
-            w0 |= isa::kRepeat;
-    }
-    while (E.code.size() % isa::kChunkWords) E.put(isa::w0(isa::NOP, 0, 0));
-    S.n_instr = E.code.size() / isa::kWords + 1;   // through the END
-    for (uint32_t i = 0; i < 2 * isa::kChunkInstr; ++i) E.put(isa::w0(isa::END, 0, 0));
-    S.code = std::move(E.code);
-    S.aux = std::move(E.aux);
-}
+constexpr uint32_t kTemps = 24;
 
 // Build the forward phase (shared by both programs) and, for the gradient
-// program, the reverse phase; returns the schedule with registers assigned.
-Schedule build(const Info &I, Builder &B, bool with_grad) {
+// program, the reverse phase; returns the slot program with registers
+// assigned and micro-ops packed S to an instruction.
+Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
+    using namespace slot;
     const Tape &t = I.t;
     const uint32_t N = I.N, P = I.P;
-    // static registers: param values, param adjoints, a sink for adjoint
-    // contributions nobody needs, the constant pool, residents
-    // the pool holds the tape's constants, then 1, -1 and -0 for bundles
-    const uint32_t nt = uint32_t(t.consts.size()), nc = nt + 3;
+    // static registers: param values, param adjoints, a sink for results
+    // nobody needs, the constant pool, residents.  The pool holds the tape's
+    // constants, then 1, -1, -0, 2 and the clamp threshold 1e-8.
+    const uint32_t nt = uint32_t(t.consts.size()), nc = nt + 5;
     const uint32_t kSink = 2 * P, kConst0 = 2 * P + 1;
-    const uint32_t kOne = kConst0 + nt, kMinusOne = kOne + 1, kNegZero = kOne + 2;
+    const uint32_t kOne = kConst0 + nt, kMinusOne = kOne + 1, kNegZero = kOne + 2, kTwo = kOne + 3,
+                   kEps = kOne + 4;
     const uint32_t kStatic = 2 * P + 1 + nc + B.res_elems;
     const uint32_t m = uint32_t(B.cuts.size());
-    Schedule S;
-    S.n_segments = with_grad ? m : 1;
-    S.static_regs = kStatic;
-    S.consts = t.consts;
-    S.consts.push_back(1.0);
-    S.consts.push_back(-1.0);
-    S.consts.push_back(-0.0);
+    Schedule Sch;
+    Sch.slots = S;
+    Sch.n_segments = with_grad ? m : 1;
+    Sch.static_regs = kStatic;
+    Sch.consts = t.consts;
+    for (double v : {1.0, -1.0, -0.0, 2.0, 1e-8}) Sch.consts.push_back(v);
 
     // ---- forward phase: abstract instructions + value intervals
     std::vector<AI> fa;
-    std::vector<uint32_t> ckrow_of;   // per (segment, livein index) row, flattened
     std::vector<uint32_t> ckrow_base(m + 1, 0);
     if (with_grad) {
         uint32_t row = 0;
@@ -653,10 +783,10 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             for (uint32_t s : B.livein[j]) row += I.nel[s];
         }
         ckrow_base[m] = row;
-        S.n_ckpt_rows = row;
+        Sch.n_ckpt_rows = row;
     }
     for (uint32_t p = 0; p < P; ++p) fa.push_back({I_LDP, p, 0});
-    for (uint32_t i = 0; i < nc; i += 255) fa.push_back({I_LDC, i, std::min<uint32_t>(255, nc - i)});
+    fa.push_back({I_LDC, 0, nc});
     uint32_t next_cut = 1;
     for (uint32_t k = 0; k < N; ++k) {
         if (with_grad) {
@@ -669,7 +799,6 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
     }
     fa.push_back({I_STLOSS, t.loss, 0});
     fa = bundle_forward(I, fa);
-    // intervals for forward values
     std::vector<Interval> fiv;
     std::vector<int32_t> fiv_of(N, -1);
     for (uint32_t ti = 0; ti < fa.size(); ++ti) {
@@ -691,8 +820,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
             use(a.k);
         }
     }
-    uint32_t fhwm = allocate(fiv);
-    S.fwd_regs = fhwm;
+    const uint32_t fhwm = allocate(fiv);
+    Sch.fwd_regs = fhwm;
 
     auto res_reg = [&](uint32_t s) { return kConst0 + nc + B.res_off[s]; };
     auto fwd_operand = [&](uint32_t s) -> uint32_t {
@@ -706,476 +835,644 @@ Schedule build(const Info &I, Builder &B, bool with_grad) {
         }
     };
 
-    Emitter E;
+    UEmit E;
+    E.tmp0 = kStatic + fhwm;   // forward temporaries above the forward registers
+    E.n_tmp = kTemps;
+    auto mov = [&](uint32_t d, uint32_t x) { E.put(MAC, d, 0, x, kOne, kNegZero); };
+
+    // forward computation of op k into dst (registers from `operand`)
     auto emit_fwd = [&](uint32_t k, auto operand, uint32_t dst) {
         const TapeOp &o = t.ops[k];
-        uint32_t op = fwd_opcode(o.code), n = I.nel[k];
-        if (o.code == tp::OBS) {
-            E.put(isa::w0(isa::LDOBS, 0, 1), dst, 0, 0, 0, 0, 0, o.imm);
-            return;
-        }
-        if (n == 1 && scalar_fast(o.code) && (o.code == tp::SELECT || I.nel[o.a] == 1)) {
-            uint32_t sop = op == isa::F_SELECT ? uint32_t(isa::S_SELECT) : op - isa::F_ADD + isa::S_ADD;
-            if (o.code == tp::SELECT)
-                E.put(isa::w0(sop, 0, 1), dst, operand(o.a), operand(o.b), operand(o.c), operand(o.d));
-            else
-                E.put(isa::w0(sop, 0, 1), dst, operand(o.a), binary_code(o.code) ? operand(o.b) : 0);
-            return;
-        }
+        const uint32_t n = I.nel[k];
         switch (o.code) {
+        case tp::OBS:
+            E.put(LDOBS, dst, 0, o.imm);
+            return;
         case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: {
-            uint32_t mode = isa::MODE_SAME;
-            if (I.nel[o.a] != I.nel[o.b] || t.ops[o.a].rows != t.ops[o.b].rows)
-                mode = I.nel[o.a] == 1 ? isa::MODE_A_SCALAR : isa::MODE_B_SCALAR;
-            E.put(isa::w0(op, mode, n), dst, operand(o.a), operand(o.b));
-            break;
+            const uint32_t A = operand(o.a), Bv = operand(o.b);
+            const bool as = I.nel[o.a] == 1 && n > 1, bs = I.nel[o.b] == 1 && n > 1;
+            for (uint32_t i = 0; i < n; ++i) {
+                const uint32_t xa = as ? A : A + i, xb = bs ? Bv : Bv + i;
+                switch (o.code) {
+                case tp::ADD: E.put(MAC, dst + i, 0, xa, kOne, xb); break;
+                case tp::SUB: E.put(MAC, dst + i, 0, xb, kMinusOne, xa); break;
+                case tp::MUL: E.put(MAC, dst + i, 0, xa, xb, kNegZero); break;
+                default: E.put(DIV, dst + i, 0, xa, xb); break;
+                }
+            }
+            return;
+        }
+        case tp::NEG: {
+            const uint32_t A = operand(o.a);
+            for (uint32_t i = 0; i < n; ++i) E.put(MAC, dst + i, 0, A + i, kMinusOne, kNegZero);
+            return;
+        }
+        case tp::EXP: case tp::LOG: case tp::SQRT: case tp::SIN: case tp::COS: case tp::ABS: {
+            const uint32_t A = operand(o.a);
+            const uint32_t f = o.code == tp::EXP ? U_EXP : o.code == tp::LOG ? U_LOGC : o.code == tp::SQRT ? U_SQRTC
+                             : o.code == tp::SIN ? U_SIN : o.code == tp::COS ? U_COS : U_ABS;
+            for (uint32_t i = 0; i < n; ++i) E.put(UN, dst + i, 0, A + i, 0, 0, f);
+            return;
         }
         case tp::POW:
-            E.put(isa::w0(op, 0, 1), dst, operand(o.a), operand(o.b));
-            break;
+            E.put(POW, dst, 0, operand(o.a), operand(o.b));
+            return;
         case tp::DOT:
-            E.put(isa::w0(op, 0, I.nel[o.a]), dst, operand(o.a), operand(o.b));
-            break;
-        case tp::MATMUL:
-            E.put(isa::w0(op, 0, n), dst, operand(o.a), operand(o.b), 0, 0, 0,
-                  isa::dims(t.ops[o.a].rows, t.ops[o.a].cols, t.ops[o.b].cols));
-            break;
-        case tp::TRANSPOSE: case tp::OUTER:
-            E.put(isa::w0(op, 0, n), dst, operand(o.a), o.code == tp::OUTER ? operand(o.b) : 0, 0, 0, 0,
-                  isa::dims(t.ops[o.a].rows, o.code == tp::OUTER ? t.ops[o.b].rows : t.ops[o.a].cols, 0));
-            break;
-        case tp::TRACE: case tp::INV: case tp::DET: case tp::LOGDET:
-            E.put(isa::w0(op, 0, n), dst, operand(o.a), 0, 0, 0, 0, t.ops[o.a].rows);
-            break;
-        case tp::PACK: {
-            uint32_t off = uint32_t(E.aux.size());
-            for (uint32_t i = 0; i < o.b; ++i) E.aux.push_back(operand(t.aux[o.a + i]));
-            E.put(isa::w0(op, 0, n), dst, 0, 0, 0, 0, 0, off);
-            break;
+            E.put(DOT, dst, 0, operand(o.a), operand(o.b), 0, I.nel[o.a], 1, 1);
+            return;
+        case tp::MATMUL: {
+            const uint32_t A = operand(o.a), Bv = operand(o.b);
+            const uint32_t mm = t.ops[o.a].rows, kk = t.ops[o.a].cols, q = t.ops[o.b].cols;
+            for (uint32_t i = 0; i < mm; ++i)
+                for (uint32_t j = 0; j < q; ++j) E.put(DOT, dst + i * q + j, 0, A + i * kk, Bv + j, 0, kk, 1, q);
+            return;
         }
-        case tp::INDEX:
-            E.put(isa::w0(op, 0, 1), dst, operand(o.a), 0, 0, 0, 0, o.imm);
-            break;
-        case tp::SELECT:
-            E.put(isa::w0(op, 0, n), dst, operand(o.a), operand(o.b), operand(o.c), operand(o.d));
-            break;
-        default:  // elementwise unary
-            E.put(isa::w0(op, 0, n), dst, operand(o.a));
+        case tp::TRANSPOSE: {
+            const uint32_t A = operand(o.a), mm = t.ops[o.a].rows, q = t.ops[o.a].cols;
+            for (uint32_t i = 0; i < mm; ++i)
+                for (uint32_t j = 0; j < q; ++j) mov(dst + j * mm + i, A + i * q + j);
+            return;
         }
-    };
-
-    // a forward bundle: the fused multiply-add form of each op, or divisions;
-    // single ops (and bundles naming registers beyond the 16-bit fields) use
-    // the one-op instructions
-    auto emit_bundle = [&](const AI &a, auto operand) {
-        const uint32_t nb = a.nops();
-        const int cls = nb > 1 ? fwd_class(I, a.k) : 0;
-        if (cls == 3) {   // observation loads: fields (d, observation index)
-            bool ok = true;
-            uint32_t w[8] = {isa::OB2 + nb - 2, 0, 0, 0, 0, 0, 0, 0};
-            for (uint32_t b = 0; b < nb; ++b) {
-                const uint32_t d = operand(a.op(b)), idx = t.ops[a.op(b)].imm;
-                ok = ok && d < isa::kFieldMaxReg && idx < isa::kFieldMaxReg;
-                w[1 + b] = d | (idx << 16);
-            }
-            if (ok) {
-                E.put(w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]);
-                S.n_bundles++;
-                S.n_bundled_ops += nb;
+        case tp::TRACE: {
+            const uint32_t sz = t.ops[o.a].rows;
+            E.put(SUMK, dst, 0, operand(o.a), 0, 0, sz, sz + 1);
+            return;
+        }
+        case tp::INV: {
+            const uint32_t A = operand(o.a), sz = t.ops[o.a].rows;
+            if (sz == 1) {
+                E.put(DIV, dst, 0, kOne, A);
                 return;
             }
-            for (uint32_t b = 0; b < nb; ++b) emit_fwd(a.op(b), operand, operand(a.op(b)));
+            // adjugate times r = 1 / det; (-a) * r is computed as a * (-r),
+            // the same bits
+            const uint32_t d = E.tmp(), r = E.tmp(), nr = E.tmp();
+            E.put(DET2, d, 0, A);
+            E.put(DIV, r, 0, kOne, d);
+            E.put(MAC, nr, 0, r, kMinusOne, kNegZero);
+            E.put(MAC, dst + 0, 0, A + 3, r, kNegZero);
+            E.put(MAC, dst + 1, 0, A + 1, nr, kNegZero);
+            E.put(MAC, dst + 2, 0, A + 2, nr, kNegZero);
+            E.put(MAC, dst + 3, 0, A + 0, r, kNegZero);
             return;
         }
-        uint32_t f[15] = {};
-        uint32_t nf = 0;
-        bool fits = cls != 0;
-        for (uint32_t b = 0; b < nb && fits; ++b) {
-            const uint32_t k = a.op(b);
-            const TapeOp &o = t.ops[k];
-            uint32_t x[4];
-            if (cls == 2) {
-                x[0] = operand(k); x[1] = operand(o.a); x[2] = operand(o.b);
-            } else {
-                switch (o.code) {
-                case tp::ADD: x[1] = operand(o.a); x[2] = kOne; x[3] = operand(o.b); break;
-                case tp::SUB: x[1] = operand(o.b); x[2] = kMinusOne; x[3] = operand(o.a); break;
-                case tp::MUL: x[1] = operand(o.a); x[2] = operand(o.b); x[3] = kNegZero; break;
-                default: x[1] = operand(o.a); x[2] = kMinusOne; x[3] = kNegZero; break;   // NEG
-                }
-                x[0] = operand(k);
+        case tp::DET: case tp::LOGDET: {
+            const uint32_t A = operand(o.a), sz = t.ops[o.a].rows;
+            uint32_t d = A;
+            if (sz == 2) {
+                d = o.code == tp::DET ? dst : E.tmp();
+                E.put(DET2, d, 0, A);
+            } else if (o.code == tp::DET) {
+                mov(dst, A);
             }
-            for (uint32_t q = 0; q < (cls == 2 ? 3u : 4u); ++q) {
-                fits = fits && x[q] < isa::kFieldMaxReg;
-                f[nf++] = x[q];
-            }
-        }
-        if (!fits) {
-            for (uint32_t b = 0; b < nb; ++b) emit_fwd(a.op(b), operand, operand(a.op(b)));
+            if (o.code == tp::LOGDET) E.put(UN, dst, 0, d, 0, 0, U_LOGC);
             return;
         }
-        const uint32_t op = (cls == 2 ? isa::DB1 : isa::FB1) + nb - 1;
-        uint32_t w[8] = {op, 0, 0, 0, 0, 0, 0, 0};
-        for (uint32_t q = 0; q < nf; ++q) w[1 + q / 2] |= f[q] << (16 * (q & 1));
-        E.put(w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]);
-        S.n_bundles++;
-        S.n_bundled_ops += nb;
+        case tp::OUTER: {
+            const uint32_t A = operand(o.a), Bv = operand(o.b);
+            const uint32_t mm = t.ops[o.a].rows, q = t.ops[o.b].rows;
+            for (uint32_t i = 0; i < mm; ++i)
+                for (uint32_t j = 0; j < q; ++j) E.put(MAC, dst + i * q + j, 0, A + i, Bv + j, kNegZero);
+            return;
+        }
+        case tp::PACK:
+            for (uint32_t i = 0; i < o.b; ++i) mov(dst + i, operand(t.aux[o.a + i]));
+            return;
+        case tp::INDEX:
+            mov(dst, operand(o.a) + o.imm);
+            return;
+        case tp::SELECT: {
+            const uint32_t p = E.tmp();
+            E.put(CMPLT, p, 0, operand(o.a), operand(o.b));
+            const uint32_t C = operand(o.c), D = operand(o.d);
+            for (uint32_t i = 0; i < n; ++i) E.put(SELP, dst + i, 0, p, C + i, D + i);
+            return;
+        }
+        default:
+            throw std::logic_error("unknown tape op in the scheduler");
+        }
     };
+
     for (const AI &a : fa) {
         switch (a.kind) {
-        case I_LDP: E.put(isa::w0(isa::LDPARAM, 0, 1), a.k, 0, 0, 0, 0, 0, a.k); break;
-        case I_LDC: E.put(isa::w0(isa::LDCONST, 0, a.j), kConst0 + a.k, 0, 0, 0, 0, 0, a.k); break;
+        case I_LDP: E.put(LDPARAM, a.k, 0, a.k); break;
+        case I_LDC:
+            for (uint32_t i = 0; i < a.j; ++i) E.put(LDCONST, kConst0 + i, 0, i);
+            break;
         case I_CKST: {
-            uint32_t s = B.livein[a.k][a.j];
+            const uint32_t s = B.livein[a.k][a.j];
             uint32_t row = ckrow_base[a.k];
             for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
-            E.put(isa::w0(isa::CKPT_ST, 0, I.nel[s]), 0, fwd_operand(s), 0, 0, 0, 0, row);
-            S.ckpt_elems_stored += I.nel[s];
+            const uint32_t src = fwd_operand(s);
+            for (uint32_t e = 0; e < I.nel[s]; ++e) E.put(CKST, src + e, 0, row + e);
+            Sch.ckpt_elems_stored += I.nel[s];
             break;
         }
         case I_FWD:
-            emit_bundle(a, fwd_operand);
-            S.n_fwd_ops += a.nops();
+            for (uint32_t b = 0; b < a.nops(); ++b) emit_fwd(a.op(b), fwd_operand, fwd_operand(a.op(b)));
+            Sch.n_fwd_ops += a.nops();
             break;
-        case I_STLOSS: E.put(isa::w0(isa::ST_LOSS, 0, 1), 0, fwd_operand(a.k)); break;
+        case I_STLOSS: E.put(STLOSS, fwd_operand(a.k), 0); break;
         }
     }
-    if (!with_grad) {
-        S.n_regs = kStatic + fhwm;
-        finish(E, S);
-        return S;
+    std::vector<UOp> fwd_ops;
+    uint32_t rhwm = 0;
+    Sch.n_regs = kStatic + fhwm + E.used_tmp;
+    if (with_grad) {
+        fwd_ops = std::move(E.ops);
+        E.ops.clear();
     }
 
-    // ---- reverse phase
-    std::vector<AI> ra;
-    ra.push_back({I_ZEROP, 0, 0});
-    ra.push_back({I_SEED, t.loss, 0});
-    for (uint32_t j = m; j-- > 0;) {
-        for (uint32_t i = 0; i < B.livein[j].size(); ++i) ra.push_back({I_CKLD, j, i});
-        for (uint32_t s : B.recomp[j]) ra.push_back({I_FWD, s, j});
-        for (uint32_t k : B.revops[j]) ra.push_back({I_REV, k, j});
-    }
-    for (uint32_t p = 0; p < P; ++p) ra.push_back({I_STG, p, 0});
-    ra = bundle_forward(I, ra);
-    ra = bundle_reverse(I, ra);
+    if (with_grad) {
+        // ---- reverse phase
+        std::vector<AI> ra;
+        ra.push_back({I_ZEROP, 0, 0});
+        ra.push_back({I_SEED, t.loss, 0});
+        for (uint32_t j = m; j-- > 0;) {
+            for (uint32_t i = 0; i < B.livein[j].size(); ++i) ra.push_back({I_CKLD, j, i});
+            for (uint32_t s : B.recomp[j]) ra.push_back({I_FWD, s, j});
+            for (uint32_t k : B.revops[j]) ra.push_back({I_REV, k, j});
+        }
+        for (uint32_t p = 0; p < P; ++p) ra.push_back({I_STG, p, 0});
+        ra = bundle_forward(I, ra);
+        ra = bundle_reverse(I, ra);
 
-    // value intervals keyed by (slot, segment); adjoint intervals keyed by slot
-    std::vector<Interval> riv;
-    std::unordered_map<uint64_t, uint32_t> val_of;
-    std::vector<int32_t> adj_of(N, -1);
-    auto key = [](uint32_t s, uint32_t j) { return (uint64_t(s) << 32) | j; };
-    auto vuse = [&](uint32_t s, uint32_t j, uint32_t ti) {
-        if ((I.kind[s] != K_COMP && I.kind[s] != K_OBS) || B.resident[s]) return;
-        auto it = val_of.find(key(s, j));
-        riv[it->second].end = std::max(riv[it->second].end, ti);
-    };
-    // first contribution flags: (instruction index, target position) -> init
-    std::vector<uint8_t> touched(N, 0);
-    auto contrib = [&](uint32_t s, uint32_t ti) {
-        if (I.kind[s] != K_COMP || !I.active[s]) return;
-        if (!touched[s]) {
-            touched[s] = 1;
-            adj_of[s] = int32_t(riv.size());
-            riv.push_back({ti, ti, I.nel[s], 0});
-        }
-    };
-    for (uint32_t ti = 0; ti < ra.size(); ++ti) {
-        const AI &a = ra[ti];
-        switch (a.kind) {
-        case I_SEED:
-            contrib(a.k, ti);
-            break;
-        case I_CKLD: {
-            uint32_t s = B.livein[a.k][a.j];
-            val_of[key(s, a.k)] = uint32_t(riv.size());
-            riv.push_back({ti, ti, I.nel[s], 0});
-            break;
-        }
-        case I_FWD:
-            for (uint32_t b = 0; b < a.nops(); ++b)
-                I.for_operands(a.op(b), [&](uint32_t s) { vuse(s, a.j, ti); });
-            for (uint32_t b = 0; b < a.nops(); ++b) {
-                val_of[key(a.op(b), a.j)] = uint32_t(riv.size());
-                riv.push_back({ti, ti, I.nel[a.op(b)], 0});
+        // value intervals keyed by (slot, segment); adjoint intervals keyed by slot
+        std::vector<Interval> riv;
+        std::unordered_map<uint64_t, uint32_t> val_of;
+        std::vector<int32_t> adj_of(N, -1);
+        auto key = [](uint32_t s, uint32_t j) { return (uint64_t(s) << 32) | j; };
+        auto vuse = [&](uint32_t s, uint32_t j, uint32_t ti) {
+            if ((I.kind[s] != K_COMP && I.kind[s] != K_OBS) || B.resident[s]) return;
+            auto it = val_of.find(key(s, j));
+            riv[it->second].end = std::max(riv[it->second].end, ti);
+        };
+        std::vector<uint8_t> touched(N, 0);
+        auto contrib = [&](uint32_t s, uint32_t ti) {
+            if (I.kind[s] != K_COMP || !I.active[s]) return;
+            if (!touched[s]) {
+                touched[s] = 1;
+                adj_of[s] = int32_t(riv.size());
+                riv.push_back({ti, ti, I.nel[s], 0});
             }
-            break;
-        case I_REV: {
-            for (uint32_t b = 0; b < a.nops(); ++b) {
-                const uint32_t k = a.op(b);
-                I.for_revreads(k, [&](uint32_t s) { vuse(s, a.j, ti); });
-                I.for_targets(k, [&](uint32_t s) { contrib(s, ti); });
-                int32_t g = adj_of[k];
-                riv[g].end = std::max(riv[g].end, ti);
+        };
+        for (uint32_t ti = 0; ti < ra.size(); ++ti) {
+            const AI &a = ra[ti];
+            switch (a.kind) {
+            case I_SEED:
+                contrib(a.k, ti);
+                break;
+            case I_CKLD: {
+                const uint32_t s = B.livein[a.k][a.j];
+                val_of[key(s, a.k)] = uint32_t(riv.size());
+                riv.push_back({ti, ti, I.nel[s], 0});
+                break;
             }
-            break;
+            case I_FWD:
+                for (uint32_t b = 0; b < a.nops(); ++b)
+                    I.for_operands(a.op(b), [&](uint32_t s) { vuse(s, a.j, ti); });
+                for (uint32_t b = 0; b < a.nops(); ++b) {
+                    val_of[key(a.op(b), a.j)] = uint32_t(riv.size());
+                    riv.push_back({ti, ti, I.nel[a.op(b)], 0});
+                }
+                break;
+            case I_REV:
+                for (uint32_t b = 0; b < a.nops(); ++b) {
+                    const uint32_t k = a.op(b);
+                    I.for_revreads(k, [&](uint32_t s) { vuse(s, a.j, ti); });
+                    I.for_targets(k, [&](uint32_t s) { contrib(s, ti); });
+                    const int32_t g = adj_of[k];
+                    riv[g].end = std::max(riv[g].end, ti);
+                }
+                break;
+            default:
+                break;
+            }
         }
-        default:
-            break;
-        }
-    }
-    uint32_t rhwm = allocate(riv);
-    S.rev_regs = rhwm;
-    S.n_regs = kStatic + std::max(fhwm, rhwm);
+        rhwm = allocate(riv);
+        Sch.rev_regs = rhwm;
 
-    auto rev_operand = [&](uint32_t s, uint32_t j) -> uint32_t {
-        s = I.rep[s];
-        switch (I.kind[s]) {
-        case K_CONST: return kConst0 + t.ops[s].imm;
-        case K_PARAM: return t.ops[s].imm;
-        default:
-            if (B.resident[s]) return res_reg(s);
-            return kStatic + riv[val_of.at(key(s, j))].reg;
-        }
-    };
-    std::fill(touched.begin(), touched.end(), 0);
-    auto target_word = [&](uint32_t s) -> uint32_t {
-        if (I.kind[s] == K_PARAM) return P + t.ops[s].imm;
-        if (I.kind[s] != K_COMP || !I.active[s]) return isa::kNone;
-        uint32_t r = kStatic + riv[adj_of[s]].reg;
-        if (!touched[s]) {
-            touched[s] = 1;
-            return r | isa::kInit;
-        }
-        return r;
-    };
-    auto target = target_word;
-    auto adjreg = [&](uint32_t s) { return kStatic + riv[adj_of[s]].reg; };
+        auto rev_operand = [&](uint32_t s, uint32_t j) -> uint32_t {
+            s = I.rep[s];
+            switch (I.kind[s]) {
+            case K_CONST: return kConst0 + t.ops[s].imm;
+            case K_PARAM: return t.ops[s].imm;
+            default:
+                if (B.resident[s]) return res_reg(s);
+                return kStatic + riv[val_of.at(key(s, j))].reg;
+            }
+        };
+        std::fill(touched.begin(), touched.end(), 0);
+        // adjoint register of a target and whether this is its first
+        // contribution; kNone when the target has no adjoint
+        constexpr uint32_t kNone = 0xFFFFFFFFu;
+        auto target = [&](uint32_t s, uint32_t *flags) -> uint32_t {
+            *flags = 0;
+            if (I.kind[s] == K_PARAM) return P + t.ops[s].imm;
+            if (I.kind[s] != K_COMP || !I.active[s]) return kNone;
+            const uint32_t r = kStatic + riv[adj_of[s]].reg;
+            if (!touched[s]) {
+                touched[s] = 1;
+                *flags = kFirst;
+            }
+            return r;
+        };
+        auto adjreg = [&](uint32_t s) { return kStatic + riv[adj_of[s]].reg; };
 
-    // one op's adjoint rule as a single instruction
-    auto emit_rev1 = [&](uint32_t k, uint32_t j) {
-        do {
+        E.tmp0 = kStatic + std::max(fhwm, rhwm);
+        E.n_tmp = kTemps;
+        E.next_tmp = 0;
+        E.used_tmp = 0;
+
+        // adjoint rule of op k (Appendix C, table tab:adjoints)
+        auto emit_rev = [&](uint32_t k, uint32_t j) {
             const TapeOp &o = t.ops[k];
             const uint32_t n = I.nel[k];
-            uint32_t g = adjreg(k);
+            const uint32_t g = adjreg(k);
             auto v = [&](uint32_t s) { return rev_operand(s, j); };
-            uint32_t op = fwd_opcode(o.code) - isa::F_ADD + isa::R_ADD;
-            S.n_rev_ops++;
-            if (n == 1 && scalar_fast(o.code) && (o.code == tp::SELECT || I.nel[o.a] == 1)) {
-                uint32_t sop = o.code == tp::SELECT ? uint32_t(isa::SR_SELECT)
-                                                    : fwd_opcode(o.code) - isa::F_ADD + isa::SR_ADD;
-                uint32_t va = 0, vb = 0, vz = 0, ta = isa::kNone, tb = isa::kNone;
-                auto target = [&](uint32_t s) {
-                    uint32_t x = target_word(s);
-                    return x == isa::kNone ? kSink : x;
-                };
-                switch (o.code) {
-                case tp::ADD: case tp::SUB: ta = target(o.a); tb = target(o.b); break;
-                case tp::MUL: va = v(o.a); vb = v(o.b); ta = target(o.a); tb = target(o.b); break;
-                case tp::DIV: vb = v(o.b); vz = v(k); ta = target(o.a); tb = target(o.b); break;
-                case tp::NEG: ta = target(o.a); break;
-                case tp::EXP: vz = v(k); ta = target(o.a); break;
-                case tp::SQRT: va = v(o.a); vz = v(k); ta = target(o.a); break;
-                case tp::SELECT: va = v(o.a); vb = v(o.b); ta = target(o.c); tb = target(o.d); break;
-                default: va = v(o.a); ta = target(o.a); break;   // LOG SIN COS ABS
+            Sch.n_rev_ops++;
+            // gate of the node: its adjoint itself when scalar, else a flag
+            // register set when any element is nonzero
+            uint32_t gate = g;
+            auto node_gate = [&](uint32_t nel) {
+                if (nel > 1) {
+                    gate = E.tmp();
+                    E.put(NZ, gate, 0, g, 0, 0, nel);
+                } else {
+                    gate = g;
                 }
-                E.put(isa::w0(sop, 0, 1), g, va, vb, vz, ta, tb);
-                break;
-            }
+            };
+            // t += x * y under the node gate
+            auto acc = [&](uint32_t tr, uint32_t fl, uint32_t x, uint32_t y) {
+                if (tr == kNone) return;
+                if (gate == x)
+                    E.put(ACC, tr, fl | kGated, x, y, tr);
+                else
+                    E.put(MACG, tr, fl, x, y, gate);
+            };
+            uint32_t fa_ = 0, fb_ = 0;
             switch (o.code) {
-            case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: {
-                uint32_t mode = isa::MODE_SAME;
-                if (I.nel[o.a] != I.nel[o.b] || t.ops[o.a].rows != t.ops[o.b].rows)
-                    mode = I.nel[o.a] == 1 ? isa::MODE_A_SCALAR : isa::MODE_B_SCALAR;
-                uint32_t va = (o.code == tp::MUL) ? v(o.a) : 0;
-                uint32_t vb = (o.code == tp::MUL || o.code == tp::DIV) ? v(o.b) : 0;
-                uint32_t vz = o.code == tp::DIV ? v(k) : 0;
-                uint32_t ta = target(o.a), tb = target(o.b);
-                E.put(isa::w0(op, mode, n), g, va, vb, vz, ta, tb);
-                break;
+            case tp::ADD: case tp::SUB: {
+                node_gate(n);
+                const uint32_t ta = target(o.a, &fa_);
+                for (uint32_t i = 0; i < n; ++i) acc(ta == kNone ? kNone : ta + i, fa_, g + i, kOne);
+                const uint32_t tb = target(o.b, &fb_);
+                for (uint32_t i = 0; i < n; ++i)
+                    acc(tb == kNone ? kNone : tb + i, fb_, g + i, o.code == tp::ADD ? kOne : kMinusOne);
+                return;
+            }
+            case tp::MUL: {
+                node_gate(n);
+                const uint32_t A = v(o.a), Bv = v(o.b);
+                const bool as = I.nel[o.a] == 1 && n > 1, bs = I.nel[o.b] == 1 && n > 1;
+                const uint32_t ta = target(o.a, &fa_);
+                if (as) {   // z = s * M: ds = sum_i g_i M_i
+                    if (ta != kNone) E.put(DOTACC, ta, fa_, g, Bv, gate, n, 1, 1);
+                } else {
+                    for (uint32_t i = 0; i < n; ++i) acc(ta == kNone ? kNone : ta + i, fa_, g + i, bs ? Bv : Bv + i);
+                }
+                const uint32_t tb = target(o.b, &fb_);
+                if (bs) {   // z = M * s
+                    if (tb != kNone) E.put(DOTACC, tb, fb_, g, A, gate, n, 1, 1);
+                } else {
+                    for (uint32_t i = 0; i < n; ++i) acc(tb == kNone ? kNone : tb + i, fb_, g + i, as ? A : A + i);
+                }
+                return;
+            }
+            case tp::DIV: {
+                node_gate(n);
+                const uint32_t Bv = v(o.b), Z = v(k);
+                const bool bs = I.nel[o.b] == 1 && n > 1;
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta != kNone)
+                    for (uint32_t i = 0; i < n; ++i) E.put(ACCD, ta + i, fa_, g + i, bs ? Bv : Bv + i, gate);
+                const uint32_t tb = target(o.b, &fb_);
+                if (tb != kNone) {
+                    if (bs) {   // z = M / s: ds -= (sum_i g_i z_i) / s
+                        const uint32_t s = E.tmp();
+                        E.put(DOT, s, 0, g, Z, 0, n, 1, 1);
+                        E.put(ACCND, tb, fb_, s, Bv, gate);
+                    } else {
+                        for (uint32_t i = 0; i < n; ++i) {
+                            const uint32_t gz = E.tmp();
+                            E.put(MAC, gz, 0, g + i, Z + i, kNegZero);
+                            E.put(ACCND, tb + i, fb_, gz, Bv + i, gate);
+                        }
+                    }
+                }
+                return;
+            }
+            case tp::NEG: case tp::EXP: case tp::LOG: case tp::SQRT: case tp::SIN: case tp::COS: case tp::ABS: {
+                node_gate(n);
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta == kNone) return;
+                for (uint32_t i = 0; i < n; ++i) {
+                    const uint32_t tr = ta + i, gi = g + i;
+                    switch (o.code) {
+                    case tp::NEG: acc(tr, fa_, gi, kMinusOne); break;
+                    case tp::EXP: acc(tr, fa_, gi, v(k) + i); break;
+                    case tp::LOG: {
+                        const uint32_t fl = E.tmp();
+                        E.put(GATEGT, fl, 0, v(o.a) + i, kEps, gate);
+                        E.put(ACCD, tr, fa_, gi, v(o.a) + i, fl);
+                        break;
+                    }
+                    case tp::SQRT: {
+                        const uint32_t tz = E.tmp(), fl = E.tmp();
+                        E.put(MAC, tz, 0, kTwo, v(k) + i, kNegZero);
+                        E.put(GATEGT, fl, 0, v(o.a) + i, kEps, gate);
+                        E.put(ACCD, tr, fa_, gi, tz, fl);
+                        break;
+                    }
+                    case tp::SIN: {
+                        const uint32_t c = E.tmp();
+                        E.put(UN, c, 0, v(o.a) + i, 0, 0, U_COS);
+                        acc(tr, fa_, gi, c);
+                        break;
+                    }
+                    case tp::COS: {
+                        const uint32_t s = E.tmp(), ns = E.tmp();
+                        E.put(UN, s, 0, v(o.a) + i, 0, 0, U_SIN);
+                        E.put(MAC, ns, 0, s, kMinusOne, kNegZero);
+                        acc(tr, fa_, gi, ns);
+                        break;
+                    }
+                    default:
+                        E.put(ACCABS, tr, fa_, gi, v(o.a) + i, gate);
+                        break;
+                    }
+                }
+                return;
             }
             case tp::POW: {
-                uint32_t va = v(o.a), vb = v(o.b), vz = v(k);
-                uint32_t ta = target(o.a), tb = target(o.b);
-                E.put(isa::w0(op, 0, 1), g, va, vb, vz, ta, tb);
-                break;
+                const uint32_t A = v(o.a), Bv = v(o.b), Z = v(k);
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta != kNone) {   // a += ((g * b) * z) / a
+                    const uint32_t t1 = E.tmp(), t2 = E.tmp();
+                    E.put(MAC, t1, 0, g, Bv, kNegZero);
+                    E.put(MAC, t2, 0, t1, Z, kNegZero);
+                    E.put(ACCD, ta, fa_, t2, A, g);
+                }
+                const uint32_t tb = target(o.b, &fb_);
+                if (tb != kNone) {   // b += (g * z) * ln a
+                    const uint32_t t3 = E.tmp(), t4 = E.tmp();
+                    E.put(MAC, t3, 0, g, Z, kNegZero);
+                    E.put(UN, t4, 0, A, 0, 0, U_LOG);
+                    E.put(MACG, tb, fb_, t3, t4, g);
+                }
+                return;
             }
             case tp::DOT: {
-                uint32_t va = v(o.a), vb = v(o.b);
-                uint32_t ta = target(o.a), tb = target(o.b);
-                E.put(isa::w0(op, 0, I.nel[o.a]), g, va, vb, 0, ta, tb);
-                break;
+                gate = g;
+                const uint32_t A = v(o.a), Bv = v(o.b), ne = I.nel[o.a];
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta != kNone)
+                    for (uint32_t i = 0; i < ne; ++i) acc(ta + i, fa_, g, Bv + i);
+                const uint32_t tb = target(o.b, &fb_);
+                if (tb != kNone)
+                    for (uint32_t i = 0; i < ne; ++i) acc(tb + i, fb_, g, A + i);
+                return;
             }
             case tp::MATMUL: {
-                uint32_t va = v(o.a), vb = v(o.b);
-                uint32_t ta = target(o.a), tb = target(o.b);
-                E.put(isa::w0(op, 0, n), g, va, vb, 0, ta, tb,
-                      isa::dims(t.ops[o.a].rows, t.ops[o.a].cols, t.ops[o.b].cols));
-                break;
+                const uint32_t A = v(o.a), Bv = v(o.b);
+                const uint32_t mm = t.ops[o.a].rows, kk = t.ops[o.a].cols, q = t.ops[o.b].cols;
+                node_gate(mm * q);
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta != kNone)
+                    for (uint32_t i = 0; i < mm; ++i)
+                        for (uint32_t p = 0; p < kk; ++p)
+                            E.put(DOTACC, ta + i * kk + p, fa_, g + i * q, Bv + p * q, gate, q, 1, 1);
+                const uint32_t tb = target(o.b, &fb_);
+                if (tb != kNone)
+                    for (uint32_t p = 0; p < kk; ++p)
+                        for (uint32_t jj = 0; jj < q; ++jj)
+                            E.put(DOTACC, tb + p * q + jj, fb_, A + p, g + jj, gate, mm, kk, q);
+                return;
             }
             case tp::OUTER: {
-                uint32_t va = v(o.a), vb = v(o.b);
-                uint32_t ta = target(o.a), tb = target(o.b);
-                E.put(isa::w0(op, 0, n), g, va, vb, 0, ta, tb, isa::dims(t.ops[o.a].rows, t.ops[o.b].rows, 0));
-                break;
+                const uint32_t A = v(o.a), Bv = v(o.b);
+                const uint32_t mm = t.ops[o.a].rows, q = t.ops[o.b].rows;
+                node_gate(mm * q);
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta != kNone)
+                    for (uint32_t i = 0; i < mm; ++i) E.put(DOTACC, ta + i, fa_, g + i * q, Bv, gate, q, 1, 1);
+                const uint32_t tb = target(o.b, &fb_);
+                if (tb != kNone)
+                    for (uint32_t jj = 0; jj < q; ++jj) E.put(DOTACC, tb + jj, fb_, g + jj, A, gate, mm, q, 1);
+                return;
             }
-            case tp::TRANSPOSE:
-                E.put(isa::w0(op, 0, n), g, 0, 0, 0, target(o.a), 0,
-                      isa::dims(t.ops[o.a].rows, t.ops[o.a].cols, 0));
-                break;
-            case tp::TRACE:
-                E.put(isa::w0(op, 0, 1), g, 0, 0, 0, target(o.a), 0, t.ops[o.a].rows);
-                break;
-            case tp::INV:
-                E.put(isa::w0(op, 0, n), g, 0, 0, v(k), target(o.a), 0, t.ops[o.a].rows);
-                break;
-            case tp::DET: {
-                uint32_t va = v(o.a), vz = v(k);
-                E.put(isa::w0(op, 0, 1), g, va, 0, vz, target(o.a), 0, t.ops[o.a].rows);
-                break;
+            case tp::TRANSPOSE: {
+                const uint32_t mm = t.ops[o.a].rows, q = t.ops[o.a].cols;
+                node_gate(n);
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta != kNone)
+                    for (uint32_t i = 0; i < mm; ++i)
+                        for (uint32_t jj = 0; jj < q; ++jj) E.put(MACG, ta + i * q + jj, fa_, g + jj * mm + i, kOne, gate);
+                return;
             }
-            case tp::LOGDET:
-                E.put(isa::w0(op, 0, 1), g, v(o.a), 0, 0, target(o.a), 0, t.ops[o.a].rows);
-                break;
+            case tp::TRACE: {
+                gate = g;
+                const uint32_t sz = t.ops[o.a].rows;
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta == kNone) return;
+                for (uint32_t i = 0; i < sz; ++i)
+                    for (uint32_t jj = 0; jj < sz; ++jj) {
+                        if (i == jj)
+                            acc(ta + i * sz + jj, fa_, g, kOne);
+                        else if (fa_ & kFirst)
+                            E.put(ZERO, ta + i * sz + jj, 0);
+                    }
+                return;
+            }
+            case tp::INV: {
+                const uint32_t sz = t.ops[o.a].rows, Z = v(k);
+                node_gate(sz * sz);
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta == kNone) return;
+                // M1 = B^T G, then A -= M1 B^T  (B the inverse)
+                const uint32_t M1 = E.tmp(sz * sz);
+                for (uint32_t i = 0; i < sz; ++i)
+                    for (uint32_t jj = 0; jj < sz; ++jj) E.put(DOT, M1 + i * sz + jj, 0, Z + i, g + jj, 0, sz, sz, sz);
+                for (uint32_t i = 0; i < sz; ++i)
+                    for (uint32_t jj = 0; jj < sz; ++jj)
+                        E.put(DOTACC, ta + i * sz + jj, fa_, M1 + i * sz, Z + jj * sz, gate, sz | kNegate, 1, 1);
+                return;
+            }
+            case tp::DET: case tp::LOGDET: {
+                const uint32_t A = v(o.a), sz = t.ops[o.a].rows;
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta == kNone) return;
+                // the inverse of A, recomputed as in the forward op
+                const uint32_t Ai = E.tmp(sz * sz);
+                if (sz == 1) {
+                    E.put(DIV, Ai, 0, kOne, A);
+                } else {
+                    const uint32_t d = E.tmp(), r = E.tmp(), nr = E.tmp();
+                    E.put(DET2, d, 0, A);
+                    E.put(DIV, r, 0, kOne, d);
+                    E.put(MAC, nr, 0, r, kMinusOne, kNegZero);
+                    E.put(MAC, Ai + 0, 0, A + 3, r, kNegZero);
+                    E.put(MAC, Ai + 1, 0, A + 1, nr, kNegZero);
+                    E.put(MAC, Ai + 2, 0, A + 2, nr, kNegZero);
+                    E.put(MAC, Ai + 3, 0, A + 0, r, kNegZero);
+                }
+                uint32_t scale = g, on = g;
+                if (o.code == tp::DET) {   // d det / dA = det * A^-T
+                    scale = E.tmp();
+                    E.put(MAC, scale, 0, g, v(k), kNegZero);
+                } else {                   // d log det / dA = A^-T where det > 1e-8
+                    uint32_t d = A;
+                    if (sz == 2) {
+                        d = E.tmp();
+                        E.put(DET2, d, 0, A);
+                    }
+                    on = E.tmp();
+                    E.put(GATEGT, on, 0, d, kEps, g);
+                }
+                for (uint32_t i = 0; i < sz; ++i)
+                    for (uint32_t jj = 0; jj < sz; ++jj) E.put(MACG, ta + i * sz + jj, fa_, scale, Ai + jj * sz + i, on);
+                return;
+            }
             case tp::PACK: {
-                uint32_t off = uint32_t(E.aux.size());
-                for (uint32_t i = 0; i < o.b; ++i) E.aux.push_back(target(t.aux[o.a + i]));
-                E.put(isa::w0(op, 0, n), g, 0, 0, 0, 0, 0, off);
-                break;
+                node_gate(n);
+                for (uint32_t i = 0; i < o.b; ++i) {
+                    uint32_t fl;
+                    const uint32_t tr = target(t.aux[o.a + i], &fl);
+                    if (tr != kNone) E.put(MACG, tr, fl, g + i, kOne, gate);
+                }
+                return;
             }
-            case tp::INDEX:
-                E.put(isa::w0(op, 0, I.nel[o.a]), g, 0, 0, 0, target(o.a), 0, o.imm);
-                break;
+            case tp::INDEX: {
+                gate = g;
+                const uint32_t ne = I.nel[o.a];
+                const uint32_t ta = target(o.a, &fa_);
+                if (ta == kNone) return;
+                if (fa_ & kFirst)
+                    for (uint32_t i = 0; i < ne; ++i)
+                        if (i != o.imm) E.put(ZERO, ta + i, 0);
+                acc(ta + o.imm, fa_, g, kOne);
+                return;
+            }
             case tp::SELECT: {
-                uint32_t va = v(o.a), vb = v(o.b);
-                uint32_t tc = target(o.c), td = target(o.d);
-                E.put(isa::w0(op, 0, n), g, va, vb, 0, tc, td);
-                break;
+                node_gate(n);
+                const uint32_t p = E.tmp();
+                E.put(CMPLT, p, 0, v(o.a), v(o.b));
+                const uint32_t tc = target(o.c, &fa_);
+                if (tc != kNone)
+                    for (uint32_t i = 0; i < n; ++i) E.put(ACCSEL, tc + i, fa_, g + i, p, gate, 1);
+                const uint32_t td = target(o.d, &fb_);
+                if (td != kNone)
+                    for (uint32_t i = 0; i < n; ++i) E.put(ACCSEL, td + i, fb_, g + i, p, gate, 0);
+                return;
             }
-            case tp::EXP: case tp::SQRT: {
-                uint32_t va = o.code == tp::SQRT ? v(o.a) : 0, vz = v(k);
-                E.put(isa::w0(op, 0, n), g, va, 0, vz, target(o.a));
-                break;
+            default:
+                throw std::logic_error("unknown tape op in the reverse scheduler");
             }
-            default:  // NEG, LOG, SIN, COS, ABS
-                E.put(isa::w0(op, 0, n), g, o.code == tp::NEG ? 0 : v(o.a), 0, 0, target(o.a));
-            }
-        } while (false);
-    };
-    // value (not adjoint-first) register of a target, without side effects
-    auto target_reg = [&](uint32_t s) -> uint32_t {
-        if (I.kind[s] == K_PARAM) return P + t.ops[s].imm;
-        if (I.kind[s] != K_COMP || !I.active[s]) return kSink;
-        return kStatic + riv[adj_of[s]].reg;
-    };
+        };
 
-
-    for (const AI &a : ra) {
-        switch (a.kind) {
-        case I_ZEROP:
-            for (uint32_t p0 = 0; p0 < P; p0 += 16)
-                E.put(isa::w0(isa::ZERO, 0, std::min<uint32_t>(16, P - p0)), P + p0);
-            break;
-        case I_SEED:
-            if (I.kind[a.k] == K_PARAM || (I.kind[a.k] == K_COMP && I.active[a.k]))
-                E.put(isa::w0(isa::SEED, 0, 1), 0, 0, 0, 0, target(a.k));
-            break;
-        case I_CKLD: {
-            uint32_t s = B.livein[a.k][a.j];
-            uint32_t row = ckrow_base[a.k];
-            for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
-            E.put(isa::w0(isa::CKPT_LD, 0, I.nel[s]), rev_operand(s, a.k), 0, 0, 0, 0, 0, row);
-            S.ckpt_elems_loaded += I.nel[s];
-            break;
-        }
-        case I_FWD: {
-            auto opnd = [&](uint32_t s) { return rev_operand(s, a.j); };
-            emit_bundle(a, opnd);
-            S.n_recompute_ops += a.nops();
-            break;
-        }
-        case I_REV: {
-            const uint32_t nb = a.nops();
-            const int cls = nb > 1 || a.seq ? rev_class(I, a.k) : 0;
-            // the registers a rule reads: g, ya, yb
-            auto rule_regs = [&](uint32_t k, uint32_t (&r)[3]) {
-                const TapeOp &o = t.ops[k];
-                auto v = [&](uint32_t s) { return rev_operand(s, a.j); };
-                r[0] = adjreg(k);
-                r[1] = kOne;
-                r[2] = kOne;
-                if (cls == 2) {
-                    r[1] = v(o.b);
-                    r[2] = v(k);
-                    return;
-                }
-                switch (o.code) {
-                case tp::SUB: r[2] = kMinusOne; break;
-                case tp::MUL: r[1] = v(o.b); r[2] = v(o.a); break;
-                case tp::NEG: r[1] = kMinusOne; break;
-                case tp::EXP: r[1] = v(k); break;
-                default: break;   // ADD
-                }
-            };
-            bool fits = cls != 0;
-            for (uint32_t b = 0; b < nb && fits; ++b) {
-                const uint32_t k = a.op(b);
-                const TapeOp &o = t.ops[k];
-                uint32_t r[3];
-                rule_regs(k, r);
-                fits = r[0] < isa::kFieldMaxReg && r[1] < isa::kFieldMaxReg && r[2] < isa::kFieldMaxReg &&
-                       target_reg(o.a) < isa::kFieldMaxReg &&
-                       (!binary_code(o.code) || target_reg(o.b) < isa::kFieldMaxReg);
-            }
-            if (!fits) {
-                for (uint32_t b = 0; b < nb; ++b) emit_rev1(a.op(b), a.j);
+        for (const AI &a : ra) {
+            switch (a.kind) {
+            case I_ZEROP:
+                for (uint32_t p = 0; p < P; ++p) E.put(ZERO, P + p, 0);
+                break;
+            case I_SEED: {
+                uint32_t fl;
+                const uint32_t tr = target(a.k, &fl);
+                if (tr != kNone) E.put(ACC, tr, fl, kOne, kOne, tr);
                 break;
             }
-            const uint32_t op0 = a.seq ? (cls == 2 ? isa::RDBS1 : isa::LBS1) : (cls == 2 ? isa::RDB1 : isa::LB1);
-            uint32_t w[8] = {op0 + nb - 1, 0, 0, 0, 0, 0, 0, 0};
-            auto put_field = [&](uint32_t i, uint32_t f) {
-                if (i == 14)
-                    w[0] |= f << 16;
-                else
-                    w[1 + i / 2] |= f << (16 * (i & 1));
-            };
-            // target register; its first contribution sets flag bit `bit` of w0
-            auto tfield = [&](uint32_t s, uint32_t bit) {
-                const uint32_t x = target_word(s);
-                if (x == isa::kNone) return kSink;
-                if (x & isa::kInit) w[0] |= 1u << bit;
-                return x & ~isa::kInit;
-            };
-            for (uint32_t b = 0; b < nb; ++b) {
-                const uint32_t k = a.op(b);
-                const TapeOp &o = t.ops[k];
-                uint32_t r[3];
-                rule_regs(k, r);
-                put_field(5 * b, r[0]);
-                put_field(5 * b + 1, r[1]);
-                put_field(5 * b + 2, r[2]);
-                put_field(5 * b + 3, tfield(o.a, 8 + 2 * b));
-                put_field(5 * b + 4, binary_code(o.code) ? tfield(o.b, 9 + 2 * b) : kSink);
+            case I_CKLD: {
+                const uint32_t s = B.livein[a.k][a.j];
+                uint32_t row = ckrow_base[a.k];
+                for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
+                const uint32_t dst = rev_operand(s, a.k);
+                for (uint32_t e = 0; e < I.nel[s]; ++e) E.put(CKLD, dst + e, 0, row + e);
+                Sch.ckpt_elems_loaded += I.nel[s];
+                break;
             }
-            E.put(w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]);
-            S.n_rev_ops += nb;
-            S.n_bundles++;
-            S.n_bundled_ops += nb;
-            break;
+            case I_FWD: {
+                auto opnd = [&](uint32_t s) { return rev_operand(s, a.j); };
+                for (uint32_t b = 0; b < a.nops(); ++b) emit_fwd(a.op(b), opnd, opnd(a.op(b)));
+                Sch.n_recompute_ops += a.nops();
+                break;
+            }
+            case I_REV:
+                for (uint32_t b = 0; b < a.nops(); ++b) emit_rev(a.op(b), a.j);
+                break;
+            case I_STG:
+                E.put(STGRAD, P + a.k, 0, a.k);
+                break;
+            default:
+                break;
+            }
         }
-        case I_STG:
-            E.put(isa::w0(isa::ST_GRAD, 0, 1), 0, P + a.k, 0, 0, 0, 0, a.k);
-            break;
-        default:
-            break;
-        }
+        Sch.n_regs = std::max(Sch.n_regs, E.tmp0 + E.used_tmp);
     }
-    finish(E, S);
-    return S;
+
+    // ---- pack and encode: forward and reverse phases separately (the
+    // reverse phase starts after every forward store)
+    const uint32_t trash_row = Sch.n_ckpt_rows;
+    std::vector<std::vector<UOp>> phases;
+    if (with_grad) {
+        phases.push_back(std::move(fwd_ops));
+        phases.push_back(std::move(E.ops));
+    } else {
+        phases.push_back(std::move(E.ops));
+    }
+    std::vector<UOp> flat;
+    std::vector<std::pair<uint32_t, uint32_t>> spans;   // (first op, count) per instruction
+    for (auto &ph : phases) {
+        const auto groups = pack(ph, S);
+        for (const auto &gq : groups) {
+            spans.push_back({uint32_t(flat.size()), uint32_t(gq.size())});
+            for (uint32_t j : gq) flat.push_back(ph[j]);
+        }
+        Sch.n_uops += ph.size();
+    }
+    const uint32_t n_real = uint32_t(spans.size());
+    Sch.n_instr = n_real + 1;   // through the END
+    const uint32_t n_chunks = n_real / kChunk + 1 + kFetchAhead;
+    Sch.code.assign(size_t(n_chunks) * kChunkWords, 0);
+    // words of instruction i in row r
+    auto row_words = [&](uint32_t i, uint32_t r) -> uint32_t * {
+        return &Sch.code[size_t(i / kChunk) * kChunkWords + (size_t(r) * kChunk + i % kChunk) * 4];
+    };
+    for (uint32_t i = 0; i < n_chunks * kChunk; ++i) {
+        if (i >= n_real) {
+            for (uint32_t r = 0; r < kRows; ++r) row_words(i, r)[0] = word0(END, kSink);
+            continue;
+        }
+        const auto [first, cnt] = spans[i];
+        const UOp &u0 = flat[first];
+        const uint32_t f = form_of(u0.w[0]);
+        for (uint32_t sl = 0; sl < S; ++sl) {
+            UOp u = sl < cnt ? flat[first + sl] : u0;
+            if (sl >= cnt) {
+                if (writes_a(f)) u.w[0] = (u.w[0] & ~(kFieldMask | kFirst | kGated)) | kSink;
+                if (f == CKST) u.w[1] = (u.w[1] & ~kFieldMask) | trash_row;
+            }
+            if (f == STLOSS || f == STGRAD) u.w[1] = (u.w[1] & kFieldMask) | (cnt << 24);
+            for (uint32_t r = sl * kRows / S; r < (sl + 1) * kRows / S; ++r) std::memcpy(row_words(i, r), u.w, 16);
+        }
+        Sch.n_slots_used += cnt;
+    }
+    Sch.n_chunks = n_chunks;
+    return Sch;
 }
 
 }  // namespace
 
-Schedule schedule_forward(const Tape &t) {
+Schedule schedule_forward(const Tape &t, uint32_t slots) {
     Info I(t);
     I.analyse();
     Builder B(I);
     B.set_cuts({0});
     B.resident.assign(I.N, 0);
     B.res_off.assign(I.N, 0);
-    return build(I, B, false);
+    return build(I, B, false, slots);
 }
 
-Schedule schedule_grad(const Tape &t, uint32_t reg_budget) {
+Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
     Info I(t);
     I.analyse();
     uint64_t total = 0;
@@ -1191,7 +1488,7 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget) {
         B.choose_residents(kResidentAfter);
         B.set_cuts(B.choose_cuts(S));
         B.plan(true);
-        return build(I, B, true);
+        return build(I, B, true, slots);
     };
     // Largest segment size (in value elements) whose register file fits the
     // budget: halve until it fits, then bisect between the fitting size and

@@ -18,27 +18,28 @@ def lib():
         f = _lib.ndvm_emu_run
         vp, i64 = ctypes.c_void_p, ctypes.c_int64
         f.restype = ctypes.c_int
-        f.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_uint32, vp, i64, i64,
-                      vp, i64, vp, vp, i64, vp]
+        f.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, vp, i64,
+                      i64, vp, i64, vp, vp, i64, vp]
         _lib.ndvm_emu_error.restype = ctypes.c_char_p
         g = _lib.ndvm_emu_program
         g.restype = ctypes.c_int64
-        g.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_uint32, vp, ctypes.c_size_t]
+        g.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, vp,
+                      ctypes.c_size_t]
     return _lib
 
 
 STATS = ["n_regs", "n_ckpt_rows", "n_segments", "n_instr", "fwd_ops", "recompute_ops", "rev_ops",
-         "ckpt_stored"]
+         "ckpt_stored", "n_uops", "slots_used"]
 
 
-def run(tape: bytes, params, obs, with_grad=True, budget=320):
+def run(tape: bytes, params, obs, with_grad=True, budget=320, slots=4):
     params = np.ascontiguousarray(params, dtype=np.float64)
     obs = np.ascontiguousarray(obs, dtype=np.float64)
     L, P = params.shape
     loss = np.empty(L)
     grad = np.empty((L, P)) if with_grad else None
-    stats = (ctypes.c_uint64 * 8)()
-    rc = lib().ndvm_emu_run(tape, len(tape), int(with_grad), budget, params.ctypes.data, L, P,
+    stats = (ctypes.c_uint64 * 10)()
+    rc = lib().ndvm_emu_run(tape, len(tape), int(with_grad), budget, slots, params.ctypes.data, L, P,
                             obs.ctypes.data, obs.size, loss.ctypes.data,
                             grad.ctypes.data if grad is not None else None, P, stats)
     if rc != 0:
@@ -46,10 +47,12 @@ def run(tape: bytes, params, obs, with_grad=True, budget=320):
     return loss, grad, dict(zip(STATS, list(stats)))
 
 
-def program(tape: bytes, with_grad=True, budget=320):
-    """The scheduled device program as an (n_instr, 8) array of uint32 words."""
-    n = lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, None, 0)
+def program(tape: bytes, with_grad=True, budget=320, slots=4):
+    """The scheduled device program as an (n_instr, slots, 4) array of uint32
+    payload words, in instruction order (END instructions included)."""
+    n = lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, slots, None, 0)
     assert n >= 0
     out = np.empty(n, dtype=np.uint32)
-    lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, out.ctypes.data, n)
-    return out.reshape(-1, 8)
+    lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, slots, out.ctypes.data, n)
+    chunk = 4
+    return out.reshape(-1, slots, chunk, 4).transpose(0, 2, 1, 3).reshape(-1, slots, 4)
