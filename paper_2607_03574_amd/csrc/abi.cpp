@@ -60,8 +60,10 @@ ndvm_status device_props(DeviceProps *out) {
 constexpr uint32_t kMaxWavesPerCuTarget = 16;
 
 // Micro-ops per instruction (threads per lane) of a launch: 4 slots (16
-// lanes per wave), so each lane's independent micro-ops run side by side and
-// the launch has four times as many waves as lanes / 64.
+// lanes per wave).  Fewer slots would leave fewer unused slots per
+// instruction, but give each lane a quarter or half the LDS registers at the
+// same wave count (measured: the program population at 1 slot spills and
+// runs 3x slower), so the format keeps 4.
 uint32_t choose_slots(const DeviceProps &p, int64_t L, int64_t n_prog) {
     (void)p;
     (void)L;
@@ -113,10 +115,10 @@ ndvm_status upload_program(Schedule &&S, const Tape &t, hipStream_t stream, std:
     // the kernel fetches whole chunks and reads two chunks past the one that
     // holds END
     const uint64_t end_at = uint64_t(S.n_instr) - 1;   // index of the END instruction
-    if (S.code.size() != uint64_t(S.n_chunks) * slot::kChunkWords || S.n_instr == 0 ||
+    if (S.hdr_off != uint64_t(S.n_chunks) * slot::kChunkWords || S.n_instr == 0 ||
         end_at / slot::kChunk + 1 + slot::kFetchAhead > S.n_chunks ||
-        slot::form_of(S.code[end_at / slot::kChunk * slot::kChunkWords + (end_at % slot::kChunk) * 4]) !=
-            slot::END) {
+        S.hdr_off + (end_at / slot::kHeaderGroup + 1 + slot::kFetchAhead) * slot::kHeaderGroup > S.code.size() ||
+        (S.code[S.hdr_off + end_at] & slot::kFormMask) != slot::END) {
         set_error("internal: device program is not padded to the fetch chunks");
         return NDVM_E_TAPE;
     }
@@ -179,13 +181,20 @@ ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, hipStream_t st
     return NDVM_OK;
 }
 
+// Registers of a forward-only program: whatever one workgroup may hold.
+uint32_t fwd_budget(uint32_t S) {
+    DeviceProps p;
+    if (device_props(&p) != NDVM_OK) p = DeviceProps{};
+    return uint32_t(p.lds_per_block / reg_bytes(S));
+}
+
 // Forward-only device program of `tape` with S slots.
 ndvm_status fwd_program(ndvm_tape *tape, uint32_t S, hipStream_t stream, DevProg **out) {
     std::lock_guard<std::mutex> lk(tape->mu);
     auto it = tape->fwd.find(S);
     if (it == tape->fwd.end()) {
         Schedule sch;
-        ndvm_status st = scheduled([&] { return schedule_forward(tape->tape, S); }, &sch);
+        ndvm_status st = scheduled([&] { return schedule_forward(tape->tape, S, fwd_budget(S)); }, &sch);
         if (st != NDVM_OK) return st;
         std::unique_ptr<DevProg> dp;
         st = upload_program(std::move(sch), tape->tape, stream, &dp);
@@ -199,10 +208,10 @@ ndvm_status fwd_program(ndvm_tape *tape, uint32_t S, hipStream_t stream, DevProg
 int64_t lpad_of(int64_t L) { return (L + 63) / 64 * 64; }
 
 // Workspace rows (fp64 per lane) of one program launched with LDS budget b:
-// checkpoint rows, the trash row that unused slots store to, spill rows.
+// checkpoint rows, the trash rows that unused slots store to, spill rows.
 uint64_t ws_rows(const DevProg &dp, uint32_t b) {
     uint32_t r_lds = std::min(dp.meta.n_regs, b);
-    return uint64_t(dp.meta.n_ckpt_rows) + 1 + (dp.meta.n_regs - r_lds);
+    return uint64_t(dp.meta.n_ckpt_rows) + slot::kMaxBlock + (dp.meta.n_regs - r_lds);
 }
 
 ndvm_status check_stream_and_launch(const LaunchArgs &A, const ProgStatic *table, const ProgStatic &single,
@@ -421,7 +430,7 @@ ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
         }
         LaunchArgs A{obs, params, loss, loss, static_cast<double *>(ws), ld_p, 0, L, Lp, 0, 0};
         const bool spills = dp.meta.n_regs > r_lds;
-        ProgStatic D{dp.code, dp.consts, 0, uint64_t(dp.meta.n_ckpt_rows) + 1, r_lds, spills};
+        ProgStatic D{dp.code, dp.consts, 0, uint64_t(dp.meta.n_ckpt_rows) + slot::kMaxBlock, dp.meta.hdr_off, r_lds, spills};
         return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, S,
                                        static_cast<hipStream_t>(stream));
     });
@@ -455,7 +464,7 @@ ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L, in
         double *wsd = static_cast<double *>(ws);
         LaunchArgs A{obs, params, loss, grad, wsd, ld_p, ld_g, L, Lp, 0, 0};
         const bool spills = dp->meta.n_regs > r_lds;
-        ProgStatic D{dp->code, dp->consts, 0, uint64_t(dp->meta.n_ckpt_rows) + 1, r_lds, spills};
+        ProgStatic D{dp->code, dp->consts, 0, uint64_t(dp->meta.n_ckpt_rows) + slot::kMaxBlock, dp->meta.hdr_off, r_lds, spills};
         return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, S,
                                        static_cast<hipStream_t>(stream));
     });
@@ -500,7 +509,7 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
             r_launch = std::max(r_launch, r_lds);
             const bool spills = dp->meta.n_regs > r_lds;
             n_spill += spills;
-            table[q] = ProgStatic{dp->code, dp->consts, row, row + dp->meta.n_ckpt_rows + 1, r_lds, spills};
+            table[q] = ProgStatic{dp->code, dp->consts, row, row + dp->meta.n_ckpt_rows + slot::kMaxBlock, dp->meta.hdr_off, r_lds, spills};
             row += ws_rows(*dp, b);
             key.push_back(tapes[q]->id);
             key.push_back((uint64_t(S) << 32) | b);

@@ -23,11 +23,18 @@ using namespace ndvm;
 
 namespace {
 
+// Payload of one slot: register fields decoded from byte offsets into
+// register numbers (the host context's handles).
 struct P4 {
-    uint32_t x, y, z, w;
-    uint32_t u1() const { return y; }
-    uint32_t u2() const { return z; }
-    uint32_t u3() const { return w; }
+    uint32_t w[4], hdr, slot, reg_bytes;
+    uint32_t a() const { return w[0] / reg_bytes; }
+    uint32_t x() const { return w[1] / reg_bytes; }
+    uint32_t y() const { return w[2] / reg_bytes; }
+    uint32_t z() const { return w[3] / reg_bytes; }
+    uint32_t ix() const { return w[1]; }
+    uint32_t imm() const { return hdr >> slot::kImmShift; }
+    bool first() const { return (hdr >> (slot::kFirstShift + slot)) & 1u; }
+    bool gated() const { return (hdr >> (slot::kGatedShift + slot)) & 1u; }
 };
 
 struct HostCtx {
@@ -57,23 +64,21 @@ struct HostCtx {
         for (size_t i = 0; i < pending->size(); ++i)
             if ((*pending)[i].first == r && (*pend_slot)[i] != cur_slot) flag(6);
     }
-    double ld(uint32_t f) const {
-        const uint32_t r = f & slot::kFieldMask;
+    static uint32_t adv(uint32_t h, uint32_t n) { return h + n; }
+    double ld(uint32_t r) const {
         if (r >= n_regs) { flag(1); return NAN; }
         check_pending_read(r);
         if (!written[r]) flag(2);
         return regs[r];
     }
-    double ld_raw(uint32_t f) const {
-        const uint32_t r = f & slot::kFieldMask;
+    double ld_raw(uint32_t r) const {
         if (r >= n_regs) { flag(1); return NAN; }
-        if (r != sink) check_pending_read(r);
+        if (r < sink || r >= sink + slot::kMaxBlock) check_pending_read(r);
         return regs[r];
     }
-    void st(uint32_t f, double v) const {
-        const uint32_t r = f & slot::kFieldMask;
+    void st(uint32_t r, double v) const {
         if (r >= n_regs) { flag(1); return; }
-        if (r != sink)
+        if (r < sink || r >= sink + slot::kMaxBlock)
             for (const auto &pw : *pending)
                 if (pw.first == r) flag(7);
         pending->push_back({r, v});
@@ -118,7 +123,7 @@ struct HostCtx {
 };
 
 Schedule schedule(const Tape &t, int with_grad, uint32_t reg_budget, uint32_t slots) {
-    return with_grad ? schedule_grad(t, reg_budget, slots) : schedule_forward(t, slots);
+    return with_grad ? schedule_grad(t, reg_budget, slots) : schedule_forward(t, slots, reg_budget);
 }
 
 }  // namespace
@@ -154,39 +159,34 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
         for (int i = 0; i < 10; ++i) stats[i] = v[i];
     }
     const uint32_t sink = 2 * t.n_params;
-    std::vector<double> regs(S.n_regs), ck(size_t(S.n_ckpt_rows) + 1);
+    std::vector<double> regs(S.n_regs), ck(size_t(S.n_ckpt_rows) + slot::kMaxBlock);
     std::vector<uint8_t> written(S.n_regs);
     std::vector<std::pair<uint32_t, double>> pending;
     std::vector<uint32_t> pend_slot;
     const uint32_t K = slot::kChunk;
+    const uint32_t reg_bytes = 8 * (64 / slots);
     for (int64_t l = 0; l < L; ++l) {
         std::fill(written.begin(), written.end(), 0);
         int fault = 0;
         HostCtx c{regs.data(), written.data(), S.n_regs, sink, S.consts.data(), obs, params + l * ld_p,
                   uint32_t(S.consts.size()), uint32_t(n_obs), t.n_params, loss + l,
-                  grad ? grad + l * ld_g : nullptr, ck.data(), S.n_ckpt_rows + 1, &fault, 0, false, &pending,
+                  grad ? grad + l * ld_g : nullptr, ck.data(), S.n_ckpt_rows + slot::kMaxBlock, &fault, 0, false, &pending,
                   &pend_slot};
         bool ended = false;
         for (uint64_t i = 0; i < uint64_t(S.n_chunks) * K && !ended && !fault; ++i) {
-            // slot sl's words sit in rows sl * 4 / S ..; take the first
-            auto words = [&](uint32_t sl) {
-                const uint32_t r = sl * slot::kRows / slots;
-                const uint32_t *w = &S.code[size_t(i / K) * slot::kChunkWords + (size_t(r) * K + i % K) * 4];
-                return P4{w[0], w[1], w[2], w[3]};
-            };
-            const uint32_t form = slot::form_of(words(0).x);
+            const uint32_t hdr = S.code[S.hdr_off + i];
+            const uint32_t form = hdr & slot::kFormMask;
             if (form == slot::END) {
                 ended = true;
                 break;
             }
             for (uint32_t sl = 0; sl < slots; ++sl) {
-                const P4 p = words(sl);
-                if (slot::form_of(p.x) != form || (p.y >> 24) != (words(0).y >> 24) ||
-                    (p.z >> 24) != (words(0).z >> 24) || (p.w >> 24) != (words(0).w >> 24))
-                    c.flag(8);
+                // slot sl's words sit in rows sl * 4 / S ..; take the first
+                const uint32_t r = sl * slot::kRows / slots;
+                const uint32_t *w = &S.code[size_t(i / K) * slot::kChunkWords + (size_t(r) * K + i % K) * 4];
+                const P4 p{{w[0], w[1], w[2], w[3]}, hdr, sl, reg_bytes};
                 c.cur_slot = sl;
-                c.cur_dummy = (slot::writes_a(form) && (p.x & slot::kFieldMask) == sink) ||
-                              (form == slot::CKST && (p.y & slot::kFieldMask) == S.n_ckpt_rows);
+                c.cur_dummy = (slot::writes_a(form) && p.a() == sink) || (form == slot::CKST && p.ix() == S.n_ckpt_rows);
                 if (slot::is_hot(form))
                     slotx::exec_hot(c, form, p);
                 else
@@ -206,8 +206,9 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
 }
 
 /*
- * Copy the device program the scheduler makes for `tape` (payload words,
- * chunk-major: [chunk][row][instr][4], slot.h) into `out` when it holds `cap` words;
+ * Copy the device program the scheduler makes for `tape` (slot words,
+ * chunk-major ([chunk][row][instr][4]), then the headers; slot.h) into `out`
+ * when it holds `cap` words;
  * returns the number of words, or -1 on an error.
  */
 int64_t ndvm_emu_program(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_budget, uint32_t slots,

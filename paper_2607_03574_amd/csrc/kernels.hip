@@ -28,38 +28,33 @@ namespace {
 
 template <int S, bool kSpill>
 struct DevCtx {
-    static constexpr int LW = 64 / S;   // lanes per wave
+    static constexpr int LW = 64 / S;                        // lanes per wave
+    static constexpr uint32_t kStride = LW * sizeof(double); // bytes between consecutive registers
     AS_GLOBAL double *spill;
     const AS_GLOBAL double *consts, *obs, *params;
     AS_GLOBAL double *loss, *grad, *ckpt;
     int64_t lane, lc, Lpad, ld_p, ld_g;
-    uint32_t r_lds, lane_addr, stride, slot_;
+    uint32_t r_lds, lane_addr, slot_;
     bool active;
 
-    __device__ __forceinline__ static uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
     __device__ __forceinline__ uint32_t slot() const { return slot_; }
-    // LDS address of the register named by the low 24 bits of f: one
-    // v_mad_u32_u24, whose 24-bit multiply ignores the field's high byte
-    __device__ __forceinline__ AS_LDS double *rp(uint32_t f) const {
-        uint32_t a;
-        asm("v_mad_u32_u24 %0, %1, %2, %3" : "=v"(a) : "v"(f), "v"(stride), "v"(lane_addr));
-        return (AS_LDS double *)(size_t)a;
-    }
-    __device__ __forceinline__ double ld(uint32_t f) const {
-        if (!kSpill) return *rp(f);
-        const uint32_t r = f & slot::kFieldMask;
-        if (r < r_lds) return *rp(r);
+    // registers are named by their LDS byte address in this thread's lane
+    __device__ __forceinline__ static uint32_t adv(uint32_t h, uint32_t n) { return h + n * kStride; }
+    __device__ __forceinline__ double ld(uint32_t h) const {
+        if (!kSpill) return *(AS_LDS double *)(size_t)h;
+        const uint32_t r = (h - lane_addr) / kStride;
+        if (r < r_lds) return *(AS_LDS double *)(size_t)h;
         return spill[int64_t(r - r_lds) * Lpad + lane];
     }
-    __device__ __forceinline__ double ld_raw(uint32_t f) const { return ld(f); }
-    __device__ __forceinline__ void st(uint32_t f, double v) const {
+    __device__ __forceinline__ double ld_raw(uint32_t h) const { return ld(h); }
+    __device__ __forceinline__ void st(uint32_t h, double v) const {
         if (!kSpill) {
-            *rp(f) = v;
+            *(AS_LDS double *)(size_t)h = v;
             return;
         }
-        const uint32_t r = f & slot::kFieldMask;
+        const uint32_t r = (h - lane_addr) / kStride;
         if (r < r_lds)
-            *rp(r) = v;
+            *(AS_LDS double *)(size_t)h = v;
         else
             spill[int64_t(r - r_lds) * Lpad + lane] = v;
     }
@@ -82,74 +77,112 @@ template <int J>
 __device__ __forceinline__ uint32_t row_word(uint32_t v) {
     return uint32_t(__builtin_amdgcn_mov_dpp(int(v), 0x150 + J, 0xF, 0xF, false));
 }
-__device__ __forceinline__ uint32_t lane_word(uint32_t v, int lane) {
-    return uint32_t(__builtin_amdgcn_readlane(int(v), lane));
+__device__ __forceinline__ uint32_t lane_word(uint32_t v, uint32_t lane) {
+    return uint32_t(__builtin_amdgcn_readlane(int(v), int(lane)));
 }
 
-// Payload of instruction P of a chunk: this thread's words (row broadcasts);
-// the uniform words that carry the immediates are read from the chunk only
-// by the forms that use them.
+// LDS addresses of the four register fields of instruction P: each is the
+// broadcast byte offset plus this thread's lane address, one DPP-sourced add
+// per field (the s_nop covers the wait states a DPP read of a VGPR written
+// by a preceding VALU op needs).
+template <int P>
+__device__ __forceinline__ void field_addrs(uint32_t ch, uint32_t la, uint32_t &a, uint32_t &x, uint32_t &y,
+                                            uint32_t &z) {
+    asm("s_nop 1\n\t"
+        "v_add_u32_dpp %0, %4, %5 row_newbcast:%6 row_mask:0xf bank_mask:0xf\n\t"
+        "v_add_u32_dpp %1, %4, %5 row_newbcast:%7 row_mask:0xf bank_mask:0xf\n\t"
+        "v_add_u32_dpp %2, %4, %5 row_newbcast:%8 row_mask:0xf bank_mask:0xf\n\t"
+        "v_add_u32_dpp %3, %4, %5 row_newbcast:%9 row_mask:0xf bank_mask:0xf"
+        : "=&v"(a), "=&v"(x), "=&v"(y), "=&v"(z)
+        : "v"(ch), "v"(la), "i"(4 * P), "i"(4 * P + 1), "i"(4 * P + 2), "i"(4 * P + 3));
+}
+
+// Payload of instruction P of a chunk: register fields as LDS addresses,
+// the header supplies the immediate and this slot's flags.
 template <int P>
 struct ChunkPayload {
-    uint32_t x, y, z, w;
-    uint32_t ch;
-    __device__ __forceinline__ uint32_t u1() const { return lane_word(ch, 4 * P + 1); }
-    __device__ __forceinline__ uint32_t u2() const { return lane_word(ch, 4 * P + 2); }
-    __device__ __forceinline__ uint32_t u3() const { return lane_word(ch, 4 * P + 3); }
+    uint32_t ha, hx, hy, hz, ch, hdr, slot;
+    __device__ __forceinline__ uint32_t a() const { return ha; }
+    __device__ __forceinline__ uint32_t x() const { return hx; }
+    __device__ __forceinline__ uint32_t y() const { return hy; }
+    __device__ __forceinline__ uint32_t z() const { return hz; }
+    __device__ __forceinline__ uint32_t ix() const { return row_word<4 * P + 1>(ch); }
+    __device__ __forceinline__ uint32_t imm() const { return hdr >> slot::kImmShift; }
+    __device__ __forceinline__ bool first() const { return (hdr >> (slot::kFirstShift + slot)) & 1u; }
+    __device__ __forceinline__ bool gated() const { return (hdr >> (slot::kGatedShift + slot)) & 1u; }
 };
-// Payload of a cold instruction, immediates read out
+// Payload of a cold instruction, words read out
 struct Payload {
-    uint32_t x, y, z, w;
-    uint32_t v1, v2, v3;
-    __device__ __forceinline__ uint32_t u1() const { return v1; }
-    __device__ __forceinline__ uint32_t u2() const { return v2; }
-    __device__ __forceinline__ uint32_t u3() const { return v3; }
+    uint32_t w[4], hdr, slot, lane_addr;
+    __device__ __forceinline__ uint32_t a() const { return w[0] + lane_addr; }
+    __device__ __forceinline__ uint32_t x() const { return w[1] + lane_addr; }
+    __device__ __forceinline__ uint32_t y() const { return w[2] + lane_addr; }
+    __device__ __forceinline__ uint32_t z() const { return w[3] + lane_addr; }
+    __device__ __forceinline__ uint32_t ix() const { return w[1]; }
+    __device__ __forceinline__ uint32_t imm() const { return hdr >> slot::kImmShift; }
+    __device__ __forceinline__ bool first() const { return (hdr >> (slot::kFirstShift + slot)) & 1u; }
+    __device__ __forceinline__ bool gated() const { return (hdr >> (slot::kGatedShift + slot)) & 1u; }
 };
 
 // Cold micro-ops run out of line: their library code branches per lane, and
 // keeping those branches out of the replay loop leaves its hot part free of
-// divergent control flow.  Returns 1 for END.
+// divergent control flow.
 template <class C>
-__device__ __attribute__((noinline)) uint32_t cold_call(const C &c, uint32_t form, Payload p) {
-    if (form == slot::END) return 1;
+__device__ __attribute__((noinline)) void cold_call(const C &c, uint32_t form, Payload p) {
     slotx::exec_cold(c, form, p);
-    return 0;
 }
 
-// Instruction P of the chunk held in `ch` (one dword per thread); returns 1
-// when it is END.
+// Instruction P of the chunk held in `ch` (one dword per thread), header
+// lane hb + P of `hv`; returns 1 when it is END.
 template <int P, class C>
-__device__ __forceinline__ uint32_t step(const C &c, uint32_t ch) {
-    const uint32_t form = (lane_word(ch, 4 * P) >> slot::kFormShift) & 63u;
-    const ChunkPayload<P> p{row_word<4 * P>(ch), row_word<4 * P + 1>(ch), row_word<4 * P + 2>(ch),
-                            row_word<4 * P + 3>(ch), ch};
+__device__ __forceinline__ uint32_t step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb) {
+    const uint32_t hdr = lane_word(hv, hb + P);
+    const uint32_t form = hdr & slot::kFormMask;
     if (form < slot::HOT_END) {
+        ChunkPayload<P> p;
+        field_addrs<P>(ch, c.lane_addr, p.ha, p.hx, p.hy, p.hz);
+        p.ch = ch;
+        p.hdr = hdr;
+        p.slot = c.slot_;
         slotx::exec_hot(c, form, p);
         return 0;
     }
-    return cold_call(c, form, Payload{p.x, p.y, p.z, p.w, p.u1(), p.u2(), p.u3()});
+    if (form == slot::END) return 1;
+    cold_call(c, form,
+              Payload{{row_word<4 * P>(ch), row_word<4 * P + 1>(ch), row_word<4 * P + 2>(ch), row_word<4 * P + 3>(ch)},
+                      hdr, c.slot_, c.lane_addr});
+    return 0;
 }
 
 // Execute a slot program until END: the four instructions of each chunk in
-// straight-line code, chunk c + 2 requested when chunk c starts (two chunks
-// of END follow the program's END for this read-ahead; instructions after
-// END in its chunk are END too).
+// straight-line code, chunk c + 2 requested when chunk c starts, headers
+// 64 at a time with the next group in flight (the program is padded for
+// these read-aheads; instructions after END are END too).
 template <int S, bool kSpill>
-__device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *prog) {
-    static_assert(slot::kChunk == 4 && slot::kFetchAhead == 2, "the fetch below reads four-instruction chunks two ahead");
+__device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *prog, uint32_t hdr_off) {
+    static_assert(slot::kChunk == 4 && slot::kFetchAhead == 2 && slot::kHeaderGroup == 64,
+                  "the fetch below reads four-instruction chunks two ahead and 64 headers a group");
     const AS_GLOBAL uint32_t *pc = (const AS_GLOBAL uint32_t *)prog + threadIdx.x;
+    const AS_GLOBAL uint32_t *ph = (const AS_GLOBAL uint32_t *)prog + hdr_off + threadIdx.x;
     constexpr uint32_t W = slot::kChunkWords;
     uint32_t cur = pc[0], n1 = pc[W];
-    for (;;) {
+    uint32_t hv = ph[0], hn = ph[64];
+    for (uint32_t chunk = 0;; ++chunk) {
         pc += W;
         const uint32_t n2 = pc[W];
-        uint32_t ended = step<0>(c, cur);
-        ended |= step<1>(c, cur);
-        ended |= step<2>(c, cur);
-        ended |= step<3>(c, cur);
+        const uint32_t hb = (chunk & 15u) * 4;
+        uint32_t ended = step<0>(c, cur, hv, hb);
+        ended |= step<1>(c, cur, hv, hb);
+        ended |= step<2>(c, cur, hv, hb);
+        ended |= step<3>(c, cur, hv, hb);
         if (ended) return;
         cur = n1;
         n1 = n2;
+        if ((chunk & 15u) == 15u) {
+            ph += 64;
+            hv = hn;
+            hn = ph[64];
+        }
     }
 }
 
@@ -169,7 +202,6 @@ __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStati
     c.active = c.lane < A.L;
     c.lc = c.active ? c.lane : A.L - 1;
     c.lane_addr = uint32_t(size_t((AS_LDS double *)lds_regs + l));
-    c.stride = uint32_t(LW * sizeof(double));
     c.spill = (AS_GLOBAL double *)(A.ws + int64_t(D.spill_row0) * A.Lpad);
     c.ckpt = (AS_GLOBAL double *)(A.ws + int64_t(D.ckpt_row0) * A.Lpad);
     c.consts = (const AS_GLOBAL double *)D.consts;
@@ -181,7 +213,7 @@ __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStati
     c.ld_p = A.ld_p;
     c.ld_g = A.ld_g;
     c.r_lds = D.r_lds;
-    run(c, D.prog);
+    run(c, D.prog, D.hdr_off);
 }
 
 // All lane registers in LDS (the usual case: the scheduler fits the register
@@ -244,7 +276,7 @@ hipError_t launch_s(const LaunchArgs &A, const ProgStatic *d_table, const ProgSt
 }  // namespace
 
 // Slot counts the kernel is built for (micro-ops per instruction).
-bool slots_supported(uint32_t S) { return S == 1 || S == 2 || S == 4; }
+bool slots_supported(uint32_t S) { return S == 4; }
 
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
                          uint32_t r_lds, int variant, uint32_t slots, hipStream_t stream) {

@@ -188,18 +188,45 @@ struct Interval {
     uint32_t reg;
 };
 
-// First-fit placement of intervals (sorted by start) into contiguous blocks.
+// Placement of intervals (sorted by start) into registers.  A scalar takes
+// the next free register after the previous scalar's, cycling through a pool
+// of `pool` registers, so that values of independent computations land in
+// different registers for as long as the pool allows (immediate reuse would
+// tie their micro-ops together in the packer); a block takes the first free
+// run.  The file grows past the pool only when every pool register is busy.
+// Without `spread`, scalars also take the first free register (the most
+// compact placement).
 // Returns the register high-water mark; a register whose interval ends at t
 // is reusable from t + 1 on.
-uint32_t allocate(std::vector<Interval> &iv) {
+uint32_t allocate(std::vector<Interval> &iv, uint32_t pool, bool spread = true) {
     std::vector<uint32_t> order(iv.size());
     for (uint32_t i = 0; i < iv.size(); ++i) order[i] = i;
     std::stable_sort(order.begin(), order.end(),
                      [&](uint32_t x, uint32_t y) { return iv[x].start < iv[y].start; });
-    std::vector<uint32_t> busy;  // first time the register is free again
-    uint32_t hwm = 0;
+    std::vector<uint32_t> busy(pool, 0);  // first time the register is free again
+    uint32_t hwm = 0, cursor = 0;
     for (uint32_t id : order) {
         Interval &v = iv[id];
+        if (v.nel == 1 && spread) {
+            const uint32_t n = uint32_t(busy.size());
+            uint32_t r = UINT32_MAX;
+            for (uint32_t k = 0; k < n; ++k) {
+                const uint32_t c = (cursor + k) % n;
+                if (busy[c] <= v.start) {
+                    r = c;
+                    break;
+                }
+            }
+            if (r == UINT32_MAX) {
+                r = n;
+                busy.push_back(0);
+            }
+            busy[r] = v.end + 1;
+            v.reg = r;
+            cursor = r + 1;
+            hwm = std::max(hwm, r + 1);
+            continue;
+        }
         uint32_t r = 0, run = 0, base = 0;
         for (r = 0; r < busy.size(); ++r) {
             if (busy[r] <= v.start) {
@@ -553,9 +580,12 @@ std::vector<AI> bundle_reverse(const Info &I, const std::vector<AI> &in) {
 }
 
 // ------------------------------------------------------------------ micro-ops
-// One slot's micro-op before packing: its four payload words (slot.h).
+// One slot's micro-op before packing: form, flags (kUFirst, kUGated), the
+// immediate, and fields a, x, y, z as register numbers or indices.
+constexpr uint32_t kUFirst = 1, kUGated = 2;
 struct UOp {
-    uint32_t w[4];
+    uint32_t form, flags, imm;
+    uint32_t f[4];
 };
 
 // Keys of what a micro-op reads and writes: registers r, checkpoint rows
@@ -566,19 +596,17 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
     using namespace slot;
     rd.clear();
     wr.clear();
-    const uint32_t f = form_of(u.w[0]);
-    const uint32_t a = u.w[0] & kFieldMask, x = u.w[1] & kFieldMask, y = u.w[2] & kFieldMask,
-                   z = u.w[3] & kFieldMask;
-    const uint32_t i1 = u.w[1] >> 24, i2 = u.w[2] >> 24, i3 = u.w[3] >> 24;
-    const bool acc_base = !(u.w[0] & kFirst);   // adjoint forms read their target
+    const uint32_t f = u.form, im = u.imm;
+    const uint32_t a = u.f[0], x = u.f[1], y = u.f[2], z = u.f[3];
+    const bool acc_base = !(u.flags & kUFirst);   // adjoint forms read their target
     switch (f) {
-    case MAC:
+    case MAC: case SELP: case GATEGT:
         rd = {x, y, z};
         wr = {a};
         break;
     case ACC:
         rd = {x, y};
-        if (acc_base) rd.push_back(z);
+        if (acc_base) rd.push_back(a);
         wr = {a};
         break;
     case MACG: case ACCD: case ACCND: case ACCSEL: case ACCABS:
@@ -586,10 +614,11 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
         if (acc_base) rd.push_back(a);
         wr = {a};
         break;
-    case DOT: case DOTACC:
-        for (uint32_t k = 0; k < (i1 & 0x7Fu); ++k) {
-            rd.push_back(x + k * i2);
-            rd.push_back(y + k * i3);
+    case DOT: case DOTACC: {
+        const uint32_t K = im & 31u, sa = (im >> 6) & 63u, sb = (im >> 12) & 63u;
+        for (uint32_t k = 0; k < K; ++k) {
+            rd.push_back(x + k * sa);
+            rd.push_back(y + k * sb);
         }
         if (f == DOTACC) {
             rd.push_back(z);
@@ -597,12 +626,23 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
         }
         wr = {a};
         break;
+    }
+    case DOTB: case DOTBACC: {
+        const uint32_t K = im & 7u, N = (im >> 3) & 7u, sx = (im >> 6) & 7u, sy = (im >> 9) & 7u,
+                       sc = (im >> 12) & 7u;
+        for (uint32_t k = 0; k < K; ++k) {
+            rd.push_back(x + k * sx);
+            for (uint32_t j = 0; j < N; ++j) rd.push_back(y + k * sy + j * sc);
+        }
+        for (uint32_t j = 0; j < N; ++j) {
+            wr.push_back(a + j);
+            if (f == DOTBACC && acc_base) rd.push_back(a + j);
+        }
+        if (f == DOTBACC) rd.push_back(z);
+        break;
+    }
     case DIV: case CMPLT: case POW:
         rd = {x, y};
-        wr = {a};
-        break;
-    case SELP: case GATEGT:
-        rd = {x, y, z};
         wr = {a};
         break;
     case DET2:
@@ -610,11 +650,11 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
         wr = {a};
         break;
     case NZ:
-        for (uint32_t k = 0; k < i1; ++k) rd.push_back(x + k);
+        for (uint32_t k = 0; k < im; ++k) rd.push_back(x + k);
         wr = {a};
         break;
     case SUMK:
-        for (uint32_t k = 0; k < i1; ++k) rd.push_back(x + k * i2);
+        for (uint32_t k = 0; k < (im & 63u); ++k) rd.push_back(x + k * ((im >> 6) & 63u));
         wr = {a};
         break;
     case UN:
@@ -625,12 +665,16 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
         wr = {a};
         break;
     case CKST:
-        rd = {a};
-        wr = {kKeyCkpt + x};
+        for (uint32_t k = 0; k < im; ++k) {
+            rd.push_back(a + k);
+            wr.push_back(kKeyCkpt + x + k);
+        }
         break;
     case CKLD:
-        rd = {kKeyCkpt + x};
-        wr = {a};
+        for (uint32_t k = 0; k < im; ++k) {
+            rd.push_back(kKeyCkpt + x + k);
+            wr.push_back(a + k);
+        }
         break;
     case STLOSS:
         rd = {a};
@@ -645,25 +689,28 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
     }
 }
 
-// Instruction class of a micro-op: form and uniform immediates must agree
-// for micro-ops to share an instruction.
-uint32_t uop_class(const UOp &u) {
-    return slot::form_of(u.w[0]) | ((u.w[1] >> 24) << 6) | ((u.w[2] >> 24) << 14) | ((u.w[3] >> 24) << 22);
-}
+// Instruction class of a micro-op: form and immediate must agree for
+// micro-ops to share an instruction.
+uint64_t uop_class(const UOp &u) { return uint64_t(u.form) | uint64_t(u.imm) << 8; }
 
-// Pack micro-ops (in program order) into instructions of at most S slots:
-// list scheduling in which the oldest unscheduled micro-op opens each
-// instruction and later micro-ops of the same class join it when every value
-// they read or overwrite is final (true and output dependences satisfied by
-// earlier instructions; a micro-op may overwrite a register that another slot
-// of the same instruction reads, since every slot reads before any writes).
-// Each register and memory cell therefore sees its reads and writes in
-// program order, so results are those of the sequential program.
+// Pack micro-ops (in program order) into instructions of at most S slots
+// by list scheduling: each instruction takes the form (and immediate) with
+// the most ready micro-ops among the next kPackWindow unscheduled ones, and
+// up to S of those in program order.  A micro-op is ready when every value it
+// reads or overwrites is final: its true and output dependences lie in
+// earlier instructions, and the micro-ops that read a register it overwrites
+// are scheduled (possibly in the same instruction, since every slot reads
+// before any writes).  Each register and memory cell therefore sees its
+// reads and writes in program order, so results are those of the sequential
+// program.
 constexpr uint32_t kPackWindow = 160;
 
 std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S) {
     const uint32_t n = uint32_t(ops.size());
-    std::vector<uint32_t> hard_off(n + 1, 0), soft_off(n + 1, 0), hard, soft;
+    // successor lists: hard (true / output dependences), soft (overwrite
+    // after read)
+    std::vector<uint32_t> hard_cnt(n, 0), soft_cnt(n, 0);
+    std::vector<std::vector<uint32_t>> hard_succ(n), soft_succ(n);
     {
         std::unordered_map<uint64_t, uint32_t> dense;
         std::vector<int64_t> last_w;
@@ -677,20 +724,34 @@ std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S)
             }
             return it->second;
         };
+        std::vector<uint32_t> preds;
         for (uint32_t j = 0; j < n; ++j) {
             uop_access(ops[j], rd, wr);
+            preds.clear();
             for (uint64_t r : rd) {
                 const uint32_t d = id(r);
-                if (last_w[d] >= 0) hard.push_back(uint32_t(last_w[d]));
+                if (last_w[d] >= 0) preds.push_back(uint32_t(last_w[d]));
             }
             for (uint64_t w : wr) {
                 const uint32_t d = id(w);
-                if (last_w[d] >= 0) hard.push_back(uint32_t(last_w[d]));
-                for (uint32_t p : readers[d])
-                    if (p != j) soft.push_back(p);
+                if (last_w[d] >= 0) preds.push_back(uint32_t(last_w[d]));
             }
-            hard_off[j + 1] = uint32_t(hard.size());
-            soft_off[j + 1] = uint32_t(soft.size());
+            std::sort(preds.begin(), preds.end());
+            preds.erase(std::unique(preds.begin(), preds.end()), preds.end());
+            for (uint32_t p : preds) {
+                hard_succ[p].push_back(j);
+                hard_cnt[j]++;
+            }
+            preds.clear();
+            for (uint64_t w : wr)
+                for (uint32_t p : readers[id(w)])
+                    if (p != j) preds.push_back(p);
+            std::sort(preds.begin(), preds.end());
+            preds.erase(std::unique(preds.begin(), preds.end()), preds.end());
+            for (uint32_t p : preds) {
+                soft_succ[p].push_back(j);
+                soft_cnt[j]++;
+            }
             for (uint64_t r : rd) readers[id(r)].push_back(j);
             for (uint64_t w : wr) {
                 const uint32_t d = id(w);
@@ -699,27 +760,45 @@ std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S)
             }
         }
     }
-    std::vector<uint32_t> cls(n);
+    std::vector<uint64_t> cls(n);
     for (uint32_t j = 0; j < n; ++j) cls[j] = uop_class(ops[j]);
-    std::vector<int64_t> at(n, -1);
+    std::vector<uint8_t> done(n, 0);
     std::vector<std::vector<uint32_t>> out;
+    std::vector<std::pair<uint64_t, uint32_t>> counts;   // (class, ready micro-ops)
     uint32_t front = 0;
     while (front < n) {
-        const int64_t ni = int64_t(out.size());
-        std::vector<uint32_t> cur{front};
-        at[front] = ni;
-        for (uint32_t j = front + 1; j < n && j < front + kPackWindow && cur.size() < S; ++j) {
-            if (at[j] >= 0 || cls[j] != cls[front]) continue;
-            bool ok = true;
-            for (uint32_t q = hard_off[j]; q < hard_off[j + 1] && ok; ++q) ok = at[hard[q]] >= 0 && at[hard[q]] < ni;
-            for (uint32_t q = soft_off[j]; q < soft_off[j + 1] && ok; ++q) ok = at[soft[q]] >= 0;
-            if (ok) {
-                at[j] = ni;
-                cur.push_back(j);
-            }
+        const uint32_t end = std::min<uint32_t>(n, front + kPackWindow);
+        // the class with the most ready micro-ops (ties: the earliest)
+        counts.clear();
+        for (uint32_t j = front; j < end; ++j) {
+            if (done[j] || hard_cnt[j] || soft_cnt[j]) continue;
+            bool found = false;
+            for (auto &cc : counts)
+                if (cc.first == cls[j]) {
+                    cc.second++;
+                    found = true;
+                    break;
+                }
+            if (!found) counts.push_back({cls[j], 1});
         }
+        uint64_t best = counts[0].first;
+        uint32_t best_n = counts[0].second;
+        for (const auto &cc : counts)
+            if (std::min(cc.second, S) > std::min(best_n, S)) {
+                best = cc.first;
+                best_n = cc.second;
+            }
+        std::vector<uint32_t> cur;
+        for (uint32_t j = front; j < end && cur.size() < S; ++j) {
+            if (done[j] || cls[j] != best || hard_cnt[j] || soft_cnt[j]) continue;
+            done[j] = 1;
+            cur.push_back(j);
+            for (uint32_t s : soft_succ[j]) soft_cnt[s]--;   // may join this instruction
+        }
+        for (uint32_t j : cur)
+            for (uint32_t s : hard_succ[j]) hard_cnt[s]--;
         out.push_back(std::move(cur));
-        while (front < n && at[front] >= 0) ++front;
+        while (front < n && done[front]) ++front;
     }
     return out;
 }
@@ -731,11 +810,9 @@ struct UEmit {
     std::vector<UOp> ops;
     uint32_t tmp0 = 0, n_tmp = 0, next_tmp = 0;
     void put(uint32_t form, uint32_t a, uint32_t flags, uint32_t x = 0, uint32_t y = 0, uint32_t z = 0,
-             uint32_t i1 = 0, uint32_t i2 = 0, uint32_t i3 = 0) {
-        if (a > slot::kMaxField || x > slot::kMaxField || y > slot::kMaxField || z > slot::kMaxField ||
-            i1 > 255 || i2 > 255 || i3 > 255)
-            throw std::length_error("register or index beyond the 24-bit fields of the device program");
-        ops.push_back({{slot::word0(form, a, flags), slot::fieldw(x, i1), slot::fieldw(y, i2), slot::fieldw(z, i3)}});
+             uint32_t imm = 0) {
+        if (imm > slot::kMaxImm) throw std::length_error("immediate beyond the header field of the device program");
+        ops.push_back({form, flags, imm, {a, x, y, z}});
     }
     uint32_t used_tmp = 0;   // temporaries touched (0 when the program needs none)
     // a block of n consecutive temporaries
@@ -753,18 +830,21 @@ constexpr uint32_t kTemps = 24;
 // Build the forward phase (shared by both programs) and, for the gradient
 // program, the reverse phase; returns the slot program with registers
 // assigned and micro-ops packed S to an instruction.
-Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
+Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t reg_budget) {
     using namespace slot;
     const Tape &t = I.t;
     const uint32_t N = I.N, P = I.P;
-    // static registers: param values, param adjoints, a sink for results
-    // nobody needs, the constant pool, residents.  The pool holds the tape's
+    // static registers: param values, param adjoints, sinks for results of
+    // unused slots, the constant pool, residents.  The pool holds the tape's
     // constants, then 1, -1, -0, 2 and the clamp threshold 1e-8.
     const uint32_t nt = uint32_t(t.consts.size()), nc = nt + 5;
-    const uint32_t kSink = 2 * P, kConst0 = 2 * P + 1;
+    const uint32_t kSink = 2 * P, kConst0 = 2 * P + kMaxBlock;
     const uint32_t kOne = kConst0 + nt, kMinusOne = kOne + 1, kNegZero = kOne + 2, kTwo = kOne + 3,
                    kEps = kOne + 4;
-    const uint32_t kStatic = 2 * P + 1 + nc + B.res_elems;
+    const uint32_t kStatic = kConst0 + nc + B.res_elems;
+    // registers the value allocation may spread over: the budget less the
+    // static registers and the temporaries
+    const uint32_t pool = reg_budget > kStatic + kTemps ? reg_budget - kStatic - kTemps : 1;
     const uint32_t m = uint32_t(B.cuts.size());
     Schedule Sch;
     Sch.slots = S;
@@ -820,7 +900,10 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
             use(a.k);
         }
     }
-    const uint32_t fhwm = allocate(fiv);
+    // spread over the pool; compact when that does not fit (blocks need
+    // contiguous free registers, which spreading fragments)
+    uint32_t fhwm = allocate(fiv, pool);
+    if (fhwm > pool) fhwm = allocate(fiv, 0, false);
     Sch.fwd_regs = fhwm;
 
     auto res_reg = [&](uint32_t s) { return kConst0 + nc + B.res_off[s]; };
@@ -878,13 +961,13 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
             E.put(POW, dst, 0, operand(o.a), operand(o.b));
             return;
         case tp::DOT:
-            E.put(DOT, dst, 0, operand(o.a), operand(o.b), 0, I.nel[o.a], 1, 1);
+            E.put(DOT, dst, 0, operand(o.a), operand(o.b), 0, dot_imm(I.nel[o.a], 1, 1, false));
             return;
-        case tp::MATMUL: {
+        case tp::MATMUL: {   // one block of q outputs per row
             const uint32_t A = operand(o.a), Bv = operand(o.b);
             const uint32_t mm = t.ops[o.a].rows, kk = t.ops[o.a].cols, q = t.ops[o.b].cols;
             for (uint32_t i = 0; i < mm; ++i)
-                for (uint32_t j = 0; j < q; ++j) E.put(DOT, dst + i * q + j, 0, A + i * kk, Bv + j, 0, kk, 1, q);
+                E.put(DOTB, dst + i * q, 0, A + i * kk, Bv, 0, dotb_imm(kk, q, 1, q, 1, false));
             return;
         }
         case tp::TRANSPOSE: {
@@ -895,7 +978,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
         }
         case tp::TRACE: {
             const uint32_t sz = t.ops[o.a].rows;
-            E.put(SUMK, dst, 0, operand(o.a), 0, 0, sz, sz + 1);
+            E.put(SUMK, dst, 0, operand(o.a), 0, 0, sz | (sz + 1) << 6);
             return;
         }
         case tp::INV: {
@@ -964,7 +1047,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
             uint32_t row = ckrow_base[a.k];
             for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
             const uint32_t src = fwd_operand(s);
-            for (uint32_t e = 0; e < I.nel[s]; ++e) E.put(CKST, src + e, 0, row + e);
+            for (uint32_t e = 0; e < I.nel[s]; e += kMaxBlock)
+                E.put(CKST, src + e, 0, row + e, 0, 0, std::min(kMaxBlock, I.nel[s] - e));
             Sch.ckpt_elems_stored += I.nel[s];
             break;
         }
@@ -1049,7 +1133,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
                 break;
             }
         }
-        rhwm = allocate(riv);
+        rhwm = allocate(riv, pool);
+        if (rhwm > pool) rhwm = allocate(riv, 0, false);
         Sch.rev_regs = rhwm;
 
         auto rev_operand = [&](uint32_t s, uint32_t j) -> uint32_t {
@@ -1073,7 +1158,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
             const uint32_t r = kStatic + riv[adj_of[s]].reg;
             if (!touched[s]) {
                 touched[s] = 1;
-                *flags = kFirst;
+                *flags = kUFirst;
             }
             return r;
         };
@@ -1106,7 +1191,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
             auto acc = [&](uint32_t tr, uint32_t fl, uint32_t x, uint32_t y) {
                 if (tr == kNone) return;
                 if (gate == x)
-                    E.put(ACC, tr, fl | kGated, x, y, tr);
+                    E.put(ACC, tr, fl | kUGated, x, y);
                 else
                     E.put(MACG, tr, fl, x, y, gate);
             };
@@ -1127,13 +1212,13 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
                 const bool as = I.nel[o.a] == 1 && n > 1, bs = I.nel[o.b] == 1 && n > 1;
                 const uint32_t ta = target(o.a, &fa_);
                 if (as) {   // z = s * M: ds = sum_i g_i M_i
-                    if (ta != kNone) E.put(DOTACC, ta, fa_, g, Bv, gate, n, 1, 1);
+                    if (ta != kNone) E.put(DOTACC, ta, fa_, g, Bv, gate, dot_imm(n, 1, 1, false));
                 } else {
                     for (uint32_t i = 0; i < n; ++i) acc(ta == kNone ? kNone : ta + i, fa_, g + i, bs ? Bv : Bv + i);
                 }
                 const uint32_t tb = target(o.b, &fb_);
                 if (bs) {   // z = M * s
-                    if (tb != kNone) E.put(DOTACC, tb, fb_, g, A, gate, n, 1, 1);
+                    if (tb != kNone) E.put(DOTACC, tb, fb_, g, A, gate, dot_imm(n, 1, 1, false));
                 } else {
                     for (uint32_t i = 0; i < n; ++i) acc(tb == kNone ? kNone : tb + i, fb_, g + i, as ? A : A + i);
                 }
@@ -1150,7 +1235,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
                 if (tb != kNone) {
                     if (bs) {   // z = M / s: ds -= (sum_i g_i z_i) / s
                         const uint32_t s = E.tmp();
-                        E.put(DOT, s, 0, g, Z, 0, n, 1, 1);
+                        E.put(DOT, s, 0, g, Z, 0, dot_imm(n, 1, 1, false));
                         E.put(ACCND, tb, fb_, s, Bv, gate);
                     } else {
                         for (uint32_t i = 0; i < n; ++i) {
@@ -1237,16 +1322,16 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
                 const uint32_t A = v(o.a), Bv = v(o.b);
                 const uint32_t mm = t.ops[o.a].rows, kk = t.ops[o.a].cols, q = t.ops[o.b].cols;
                 node_gate(mm * q);
+                // dA[i, p] = sum_j G[i, j] B[p, j]: a block over p per row i
                 const uint32_t ta = target(o.a, &fa_);
                 if (ta != kNone)
                     for (uint32_t i = 0; i < mm; ++i)
-                        for (uint32_t p = 0; p < kk; ++p)
-                            E.put(DOTACC, ta + i * kk + p, fa_, g + i * q, Bv + p * q, gate, q, 1, 1);
+                        E.put(DOTBACC, ta + i * kk, fa_, g + i * q, Bv, gate, dotb_imm(q, kk, 1, 1, q, false));
+                // dB[p, j] = sum_i A[i, p] G[i, j]: a block over j per row p
                 const uint32_t tb = target(o.b, &fb_);
                 if (tb != kNone)
                     for (uint32_t p = 0; p < kk; ++p)
-                        for (uint32_t jj = 0; jj < q; ++jj)
-                            E.put(DOTACC, tb + p * q + jj, fb_, A + p, g + jj, gate, mm, kk, q);
+                        E.put(DOTBACC, tb + p * q, fb_, A + p, g, gate, dotb_imm(mm, q, kk, q, 1, false));
                 return;
             }
             case tp::OUTER: {
@@ -1255,10 +1340,10 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
                 node_gate(mm * q);
                 const uint32_t ta = target(o.a, &fa_);
                 if (ta != kNone)
-                    for (uint32_t i = 0; i < mm; ++i) E.put(DOTACC, ta + i, fa_, g + i * q, Bv, gate, q, 1, 1);
+                    for (uint32_t i = 0; i < mm; ++i) E.put(DOTACC, ta + i, fa_, g + i * q, Bv, gate, dot_imm(q, 1, 1, false));
                 const uint32_t tb = target(o.b, &fb_);
                 if (tb != kNone)
-                    for (uint32_t jj = 0; jj < q; ++jj) E.put(DOTACC, tb + jj, fb_, g + jj, A, gate, mm, q, 1);
+                    for (uint32_t jj = 0; jj < q; ++jj) E.put(DOTACC, tb + jj, fb_, g + jj, A, gate, dot_imm(mm, q, 1, false));
                 return;
             }
             case tp::TRANSPOSE: {
@@ -1279,7 +1364,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
                     for (uint32_t jj = 0; jj < sz; ++jj) {
                         if (i == jj)
                             acc(ta + i * sz + jj, fa_, g, kOne);
-                        else if (fa_ & kFirst)
+                        else if (fa_ & kUFirst)
                             E.put(ZERO, ta + i * sz + jj, 0);
                     }
                 return;
@@ -1292,10 +1377,10 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
                 // M1 = B^T G, then A -= M1 B^T  (B the inverse)
                 const uint32_t M1 = E.tmp(sz * sz);
                 for (uint32_t i = 0; i < sz; ++i)
-                    for (uint32_t jj = 0; jj < sz; ++jj) E.put(DOT, M1 + i * sz + jj, 0, Z + i, g + jj, 0, sz, sz, sz);
+                    for (uint32_t jj = 0; jj < sz; ++jj) E.put(DOT, M1 + i * sz + jj, 0, Z + i, g + jj, 0, dot_imm(sz, sz, sz, false));
                 for (uint32_t i = 0; i < sz; ++i)
                     for (uint32_t jj = 0; jj < sz; ++jj)
-                        E.put(DOTACC, ta + i * sz + jj, fa_, M1 + i * sz, Z + jj * sz, gate, sz | kNegate, 1, 1);
+                        E.put(DOTACC, ta + i * sz + jj, fa_, M1 + i * sz, Z + jj * sz, gate, dot_imm(sz, 1, 1, true));
                 return;
             }
             case tp::DET: case tp::LOGDET: {
@@ -1347,7 +1432,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
                 const uint32_t ne = I.nel[o.a];
                 const uint32_t ta = target(o.a, &fa_);
                 if (ta == kNone) return;
-                if (fa_ & kFirst)
+                if (fa_ & kUFirst)
                     for (uint32_t i = 0; i < ne; ++i)
                         if (i != o.imm) E.put(ZERO, ta + i, 0);
                 acc(ta + o.imm, fa_, g, kOne);
@@ -1378,7 +1463,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
             case I_SEED: {
                 uint32_t fl;
                 const uint32_t tr = target(a.k, &fl);
-                if (tr != kNone) E.put(ACC, tr, fl, kOne, kOne, tr);
+                if (tr != kNone) E.put(ACC, tr, fl, kOne, kOne);
                 break;
             }
             case I_CKLD: {
@@ -1386,7 +1471,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
                 uint32_t row = ckrow_base[a.k];
                 for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
                 const uint32_t dst = rev_operand(s, a.k);
-                for (uint32_t e = 0; e < I.nel[s]; ++e) E.put(CKLD, dst + e, 0, row + e);
+                for (uint32_t e = 0; e < I.nel[s]; e += kMaxBlock)
+                    E.put(CKLD, dst + e, 0, row + e, 0, 0, std::min(kMaxBlock, I.nel[s] - e));
                 Sch.ckpt_elems_loaded += I.nel[s];
                 break;
             }
@@ -1411,7 +1497,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
 
     // ---- pack and encode: forward and reverse phases separately (the
     // reverse phase starts after every forward store)
-    const uint32_t trash_row = Sch.n_ckpt_rows;
+    const uint32_t trash_row = Sch.n_ckpt_rows;   // kMaxBlock trash rows follow the checkpoints
+    const uint32_t reg_bytes = 8 * (64 / S);      // byte offset of register r: r * reg_bytes
     std::vector<std::vector<UOp>> phases;
     if (with_grad) {
         phases.push_back(std::move(fwd_ops));
@@ -1432,28 +1519,41 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
     const uint32_t n_real = uint32_t(spans.size());
     Sch.n_instr = n_real + 1;   // through the END
     const uint32_t n_chunks = n_real / kChunk + 1 + kFetchAhead;
-    Sch.code.assign(size_t(n_chunks) * kChunkWords, 0);
-    // words of instruction i in row r
-    auto row_words = [&](uint32_t i, uint32_t r) -> uint32_t * {
-        return &Sch.code[size_t(i / kChunk) * kChunkWords + (size_t(r) * kChunk + i % kChunk) * 4];
+    const uint32_t n_groups = n_real / kHeaderGroup + 1 + kFetchAhead;
+    const size_t hdr_off = size_t(n_chunks) * kChunkWords;
+    Sch.code.assign(hdr_off + size_t(n_groups) * kHeaderGroup, END);
+    Sch.hdr_off = uint32_t(hdr_off);
+    auto field = [&](uint64_t v) -> uint32_t {
+        if (v > 0xFFFFFFFFull) throw std::length_error("register or index beyond the 32-bit fields of the device program");
+        return uint32_t(v);
     };
     for (uint32_t i = 0; i < n_chunks * kChunk; ++i) {
+        uint32_t *row0 = &Sch.code[size_t(i / kChunk) * kChunkWords + (i % kChunk) * 4];
         if (i >= n_real) {
-            for (uint32_t r = 0; r < kRows; ++r) row_words(i, r)[0] = word0(END, kSink);
+            for (uint32_t r = 0; r < kRows; ++r) row0[r * kChunk * 4] = field(uint64_t(kSink) * reg_bytes);
             continue;
         }
         const auto [first, cnt] = spans[i];
         const UOp &u0 = flat[first];
-        const uint32_t f = form_of(u0.w[0]);
+        const uint32_t f = u0.form;
+        uint32_t hdr = f | u0.imm << kImmShift;
+        if (f == STLOSS || f == STGRAD) hdr = f | cnt << kImmShift;
         for (uint32_t sl = 0; sl < S; ++sl) {
             UOp u = sl < cnt ? flat[first + sl] : u0;
             if (sl >= cnt) {
-                if (writes_a(f)) u.w[0] = (u.w[0] & ~(kFieldMask | kFirst | kGated)) | kSink;
-                if (f == CKST) u.w[1] = (u.w[1] & ~kFieldMask) | trash_row;
+                if (writes_a(f)) u.f[0] = kSink;
+                if (f == CKST) u.f[1] = trash_row;
+                u.flags = 0;
             }
-            if (f == STLOSS || f == STGRAD) u.w[1] = (u.w[1] & kFieldMask) | (cnt << 24);
-            for (uint32_t r = sl * kRows / S; r < (sl + 1) * kRows / S; ++r) std::memcpy(row_words(i, r), u.w, 16);
+            hdr |= (u.flags & kUFirst ? 1u : 0u) << (kFirstShift + sl);
+            hdr |= (u.flags & kUGated ? 1u : 0u) << (kGatedShift + sl);
+            const uint32_t w[4] = {field(uint64_t(u.f[0]) * reg_bytes),
+                                   x_is_index(f) ? u.f[1] : field(uint64_t(u.f[1]) * reg_bytes),
+                                   field(uint64_t(u.f[2]) * reg_bytes), field(uint64_t(u.f[3]) * reg_bytes)};
+            for (uint32_t r = sl * kRows / S; r < (sl + 1) * kRows / S; ++r)
+                std::memcpy(row0 + r * kChunk * 4, w, 16);
         }
+        Sch.code[hdr_off + i] = hdr;
         Sch.n_slots_used += cnt;
     }
     Sch.n_chunks = n_chunks;
@@ -1462,14 +1562,14 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S) {
 
 }  // namespace
 
-Schedule schedule_forward(const Tape &t, uint32_t slots) {
+Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget) {
     Info I(t);
     I.analyse();
     Builder B(I);
     B.set_cuts({0});
     B.resident.assign(I.N, 0);
     B.res_off.assign(I.N, 0);
-    return build(I, B, false, slots);
+    return build(I, B, false, slots, reg_budget);
 }
 
 Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
@@ -1488,7 +1588,7 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
         B.choose_residents(kResidentAfter);
         B.set_cuts(B.choose_cuts(S));
         B.plan(true);
-        return build(I, B, true, slots);
+        return build(I, B, true, slots, reg_budget);
     };
     // Largest segment size (in value elements) whose register file fits the
     // budget: halve until it fits, then bisect between the fitting size and

@@ -8,21 +8,23 @@
 namespace ndvm {
 
 struct Schedule {
-    std::vector<uint32_t> code;   // payload words, chunk-major ([chunk][slot][instr][4], slot.h)
+    std::vector<uint32_t> code;   // slot words, chunk-major ([chunk][row][instr][4]), then headers (slot.h)
     std::vector<double> consts;   // constant pool: the tape's, then 1, -1, -0, 2, 1e-8
     uint32_t slots = 1;           // micro-ops per instruction (threads per lane)
     uint32_t n_regs = 0;          // lane registers used
-    uint32_t n_ckpt_rows = 0;     // checkpoint rows (fp64 per lane); one trash row follows
+    uint32_t n_ckpt_rows = 0;     // checkpoint rows (fp64 per lane); slot::kMaxBlock trash rows follow
     uint32_t n_segments = 1;
-    uint32_t n_chunks = 0;        // fetch chunks of the program, read-ahead chunk included
+    uint32_t n_chunks = 0;        // fetch chunks of the program, read-ahead chunks included
+    uint32_t hdr_off = 0;         // word offset of the headers in code
     uint32_t static_regs = 0, fwd_regs = 0, rev_regs = 0;
     uint64_t n_instr = 0, n_uops = 0, n_slots_used = 0;
     uint64_t n_fwd_ops = 0, n_recompute_ops = 0, n_rev_ops = 0;
     uint64_t ckpt_elems_stored = 0, ckpt_elems_loaded = 0;
 };
 
-// Forward-only program (loss[L]) with `slots` micro-ops per instruction.
-Schedule schedule_forward(const Tape &t, uint32_t slots);
+// Forward-only program (loss[L]) with `slots` micro-ops per instruction;
+// values spread over up to `reg_budget` registers.
+Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget);
 
 // Forward + reverse program (loss[L], grad[L, P]); cuts the tape into
 // checkpoint segments so that the lane register file fits `reg_budget`

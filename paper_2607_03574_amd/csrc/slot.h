@@ -14,16 +14,17 @@
 // fp64 result and writes it back.  All slots of an instruction read before
 // any slot writes, so the slots of one instruction never depend on each other.
 //
-// Per slot and instruction: four 32-bit words.
-//   w0: bits 0-23 register a (destination, adjoint target or stored source)
-//       bits 24-29 form (the same in every slot)
-//       bit 30 kGated: the contribution is skipped when operand x is zero
-//       bit 31 kFirst: first contribution to the target (store, do not add)
-//   w1..w3: bits 0-23 operand fields x, y, z (registers or indices)
-//       bits 24-31 uniform immediates i1, i2, i3 (the same in every slot)
+// Per instruction: a header word, the same for every slot:
+//   bits 0-5 form, bits 6-9 kFirst of slots 0-3 (first contribution to the
+//   target: store, do not add), bits 10-13 kGated of slots 0-3 (the
+//   contribution is skipped when operand x is zero), bits 14-31 the form's
+//   immediate;
+// and per slot four words a, x, y, z: a register named in a field is held as
+// its byte offset in a lane's register file (register * 8 * 64/S), an index
+// (observation, parameter, constant, checkpoint row) as itself.
 // Slots an instruction does not use hold a copy of slot 0's micro-op whose
-// result goes to the sink register (and whose checkpoint store goes to the
-// trash row); forms with side effects outside the register file mask them.
+// results go to the sink registers (and whose checkpoint stores go to the
+// trash rows); forms with side effects outside the register file mask them.
 #pragma once
 #include <cstdint>
 
@@ -38,67 +39,82 @@ enum Form : uint32_t {
     // products, negations and copies are this form against the constants
     // 1, -1, -0, with the bits of the plain operation.
     MAC = 1,
-    ACC,       // t = (!kGated || x != 0) ? base + x * y : base, z = t: the linear adjoint rule t += g * y
+    ACC,       // t = (!kGated || x != 0) ? base + x * y : base: the linear adjoint rule t += g * y
     MACG,      // t = gate(z) ? base + x * y : base          (explicit gate register z)
     DIV,       // d = x / y
     ACCD,      // t = gate(z) ? base + x / y : base
     ACCND,     // t = gate(z) ? base + -(x / y) : base
-    DOT,       // d = fma chain over k < i1 of A[x + k*i2] * B[y + k*i3], ascending, first term a product
-    DOTACC,    // t = gate(z) ? base + (+/-)dot : base   (dot as DOT; i1 bit 7 negates)
+    DOT,       // d = fma chain over k < K of A[x + k sa] * B[y + k sb], ascending, first term a product
+    DOTACC,    // t = gate(z) ? base + (+/-)dot : base   (dot as DOT)
     CMPLT,     // d = x < y ? 1 : 0   (unordered -> 0)
     SELP,      // d = p(x) != 0 ? y : z
-    ACCSEL,    // t = gate(z) != 0 && (p(y) != 0) == i1 ? base + x : base
+    ACCSEL,    // t = gate(z) != 0 && (p(y) != 0) == imm ? base + x : base
     DET2,      // d = A0 * A3 - A1 * A2 for the 2x2 matrix at x (two products, then difference)
-    NZ,        // d = any of x .. x + i1 - 1 nonzero ? 1 : 0
+    NZ,        // d = any of x .. x + imm - 1 nonzero ? 1 : 0
     GATEGT,    // d = gate(z) != 0 && x > y ? 1 : 0
     ACCABS,    // t = gate(z) ? base + (y > 0 ? x : y < 0 ? -x : 0) : base
-    SUMK,      // d = ((A[x] + A[x + i2]) + A[x + 2 i2]) ... over k < i1
-    LDOBS,     // d = obs[x]
-    LDPARAM,   // d = params[lane, x]
-    LDCONST,   // d = consts[x]
-    CKST,      // ckpt row x of this lane = register a
-    CKLD,      // d = ckpt row x of this lane
+    SUMK,      // d = ((A[x] + A[x + s]) + A[x + 2 s]) ... over k < K  (imm = K | s << 6)
     ZERO,      // d = +0
+    // block of N outputs d[c] = fma chain over k < K of X[x + k sx] * Y[y + k sy + c sc]
+    // (ascending, first term a product)
+    DOTB,
+    DOTBACC,   // t[c] = gate(z) ? base[c] + (+/-)dot[c] : base[c]
     HOT_END,
     // ---- cold forms: library transcendentals (per-lane branches) and
-    // stores outside the register file
-    UN = 40,   // d = f(x), f = i1: see Unary
+    // global memory traffic (kept out of the hot loop so that no hot form
+    // waits on the program fetch in flight)
+    LDOBS = 32,   // d = obs[x]
+    LDPARAM,   // d = params[lane, x]
+    LDCONST,   // d = consts[x]
+    CKST,      // ckpt rows x .. x + n - 1 of this lane = registers a .. a + n - 1  (imm = n)
+    CKLD,      // registers a .. a + n - 1 = ckpt rows x .. x + n - 1 of this lane
+    UN = 40,   // d = f(x), f = imm: see Unary
     POW,       // d = pow(x, y)
-    STLOSS,    // loss[lane] = register a          (slots < i1 only)
-    STGRAD,    // grad[lane, x] = register a       (slots < i1 only)
+    STLOSS,    // loss[lane] = register a          (slots < imm only)
+    STGRAD,    // grad[lane, x] = register a       (slots < imm only)
     END = 63,
 };
 
 enum Unary : uint32_t { U_EXP = 0, U_LOGC, U_SQRTC, U_SIN, U_COS, U_ABS, U_LOG };
 
-constexpr uint32_t kFieldMask = (1u << 24) - 1;
-constexpr uint32_t kGated = 1u << 30;
-constexpr uint32_t kFirst = 1u << 31;
-constexpr uint32_t kFormShift = 24;
-constexpr uint32_t kMaxField = kFieldMask;   // largest register / index a field holds
-constexpr uint32_t kNegate = 0x80;           // DOTACC: subtract the dot product
+constexpr uint32_t kFormMask = 63u;
+constexpr uint32_t kFirstShift = 6, kGatedShift = 10, kImmShift = 14;
+constexpr uint32_t kMaxImm = (1u << 18) - 1;
+constexpr uint32_t kMaxBlock = 4;            // outputs of a block form (sink and trash rows reserved)
 
-// Program fetch: a chunk holds kChunk instructions as 4 rows x kChunk x 4
-// words; row r (threads 16r .. 16r + 15 of a wave) carries the micro-ops of
-// slot r * S / 4, and thread 16r + j holds word j of its row (instruction
-// j / 4, word j % 4), so one coalesced dword load per thread fetches the
-// chunk and a row broadcast hands every thread of a slot its words.  The
-// program is padded so that the chunk holding END is followed by two more
-// chunks (the fetch reads two ahead).  Slot counts 1, 2 and 4 (a slot's
-// threads fill whole rows).
+// immediates: DOT / DOTACC: K | negate << 5 | sa << 6 | sb << 12;
+// DOTB / DOTBACC: K | N << 3 | sx << 6 | sy << 9 | sc << 12 | negate << 15
+inline uint32_t dot_imm(uint32_t K, uint32_t sa, uint32_t sb, bool neg) {
+    return K | uint32_t(neg) << 5 | sa << 6 | sb << 12;
+}
+inline uint32_t dotb_imm(uint32_t K, uint32_t N, uint32_t sx, uint32_t sy, uint32_t sc, bool neg) {
+    return K | N << 3 | sx << 6 | sy << 9 | sc << 12 | uint32_t(neg) << 15;
+}
+
+// Program fetch: the slot words come in chunks of kChunk instructions as
+// 4 rows x kChunk x 4 words; row r (threads 16r .. 16r + 15 of a wave)
+// carries the micro-ops of slot r * S / 4, and thread 16r + j holds word j
+// of its row (instruction j / 4, word j % 4), so one coalesced dword load per
+// thread fetches the chunk and a row broadcast hands every thread of a slot
+// its words.  The headers follow the chunks, kHeaderGroup at a time (thread
+// t of a wave holds header t of a group).  The chunk holding END is followed
+// by two more chunks and the header group holding it by two more groups (the
+// fetch reads two ahead).  Slot counts 1, 2 and 4 (a slot's threads fill
+// whole rows).
 constexpr uint32_t kChunk = 4;
 constexpr uint32_t kRows = 4;
 constexpr uint32_t kChunkWords = kRows * kChunk * 4;
 constexpr uint32_t kFetchAhead = 2;
+constexpr uint32_t kHeaderGroup = 64;
 constexpr uint32_t kMaxSlots = 4;
-
-inline uint32_t form_of(uint32_t w0) { return (w0 >> kFormShift) & 63u; }
-inline uint32_t word0(uint32_t form, uint32_t a, uint32_t flags = 0) { return a | (form << kFormShift) | flags; }
-inline uint32_t fieldw(uint32_t f, uint32_t imm = 0) { return f | (imm << 24); }
 
 inline bool is_hot(uint32_t form) { return form >= MAC && form < HOT_END; }
 // forms whose register a is written
 inline bool writes_a(uint32_t form) { return form != CKST && form != STLOSS && form != STGRAD && form != END; }
+// forms whose field x is an index rather than a register
+inline bool x_is_index(uint32_t form) {
+    return form == LDOBS || form == LDPARAM || form == LDCONST || form == CKST || form == CKLD || form == STGRAD;
+}
 
 }  // namespace slot
 
@@ -107,10 +123,11 @@ inline bool writes_a(uint32_t form) { return form != CKST && form != STLOSS && f
 // on the program and the launch's register budget, never on per-call
 // pointers, so a table of these can be cached on the device.
 struct ProgStatic {
-    const uint32_t *prog;    // payload words, chunk-major: [chunk][row][instr][4]
+    const uint32_t *prog;    // slot words, chunk-major ([chunk][row][instr][4]), then the headers
     const double *consts;    // constant pool
     uint64_t ckpt_row0;      // checkpoint row r of lane l at ws[(ckpt_row0 + r)*Lpad + l]
     uint64_t spill_row0;     // register r_lds + r of lane l at ws[(spill_row0 + r)*Lpad + l]
+    uint32_t hdr_off;        // word offset of the headers in prog
     uint32_t r_lds;          // registers held in LDS
     uint32_t spills;         // nonzero when the program has registers beyond r_lds
 };

@@ -2,18 +2,18 @@
 // the host emulator that checks the scheduler.  Each call executes the
 // micro-op of one slot of one lane.
 //
-// A context type C supplies the lane's register file and memory:
-//   double ld(uint32_t f) const;        register named by the low 24 bits of f
-//   double ld_raw(uint32_t f) const;    a read whose value may be discarded
-//   void st(uint32_t f, double v) const;
+// A context type C supplies the lane's register file and memory; registers
+// are named by handles (on the GPU an LDS byte address, on the host an
+// index):
+//   double ld(R h) const;  double ld_raw(R h) const;  (a read whose value may be discarded)
+//   void st(R h, double v) const;  R adv(R h, uint32_t n) const;  (n registers further)
 //   double obsv(uint32_t i) const;  double param(uint32_t p) const;  double konst(uint32_t i) const;
 //   double ckld(uint32_t row) const;  void ckst(uint32_t row, double v) const;
 //   void store_loss(double v, bool on) const;  void store_grad(uint32_t p, double v, bool on) const;
 //   uint32_t slot() const;
-//   static uint32_t uni(uint32_t x);   (a value that is the same in every thread of the wave)
-// and W is a payload with members x, y, z, w (this slot's words 0..3) and
-// u1(), u2(), u3() (words 1..3 of any slot, whose high bytes hold the
-// uniform immediates).
+// and W is the payload of this slot's micro-op: register handles a(), x(),
+// y(), z(), the raw field ix() (an index), the uniform immediate imm() and
+// this slot's flags first() and gated().
 //
 // Adjoint rules follow Appendix C, table tab:adjoints: contractions are fma
 // chains over the summation index in ascending order with a plain product as
@@ -37,31 +37,23 @@ using namespace slot;
 
 NDVM_HD double clampv(double x) { return x < 1e-8 ? 1e-8 : x; }
 
-// immediates of a payload (uniform)
-template <class C, class W>
-NDVM_HD uint32_t imm1(const W &p) { return p.u1() >> 24; }
-template <class C, class W>
-NDVM_HD uint32_t imm2(const W &p) { return p.u2() >> 24; }
-template <class C, class W>
-NDVM_HD uint32_t imm3(const W &p) { return p.u3() >> 24; }
-
-// base of an adjoint update of register a: +0 on the first contribution
-template <class C>
-NDVM_HD double base_of(const C &c, uint32_t w0) {
-    const double old = c.ld_raw(w0);
-    return (w0 & kFirst) ? 0.0 : old;
+// base of an adjoint update: +0 on the first contribution
+template <class C, class R>
+NDVM_HD double base_of(const C &c, R t, bool first) {
+    const double old = c.ld_raw(t);
+    return first ? 0.0 : old;
 }
 
-// fma chain of K terms A[x + k sa] * B[y + k sb]; every operand is read
-// before the chain starts (K <= 4 unrolled, longer chains in steps of 4)
-template <class C>
-NDVM_HD double dot_chain(const C &c, uint32_t x, uint32_t y, uint32_t K, uint32_t sa, uint32_t sb) {
+// fma chain of K terms A[x + k sa] * B[y + k sb]; operands read in groups of
+// four before their terms are added
+template <class C, class R>
+NDVM_HD double dot_chain(const C &c, R x, R y, uint32_t K, uint32_t sa, uint32_t sb) {
     double a[4], b[4];
 #pragma unroll
     for (uint32_t k = 0; k < 4; ++k) {
         if (k < K) {
-            a[k] = c.ld(x + k * sa);
-            b[k] = c.ld(y + k * sb);
+            a[k] = c.ld(c.adv(x, k * sa));
+            b[k] = c.ld(c.adv(y, k * sb));
         }
     }
     double s = a[0] * b[0];
@@ -72,8 +64,8 @@ NDVM_HD double dot_chain(const C &c, uint32_t x, uint32_t y, uint32_t K, uint32_
 #pragma unroll
         for (uint32_t k = 0; k < 4; ++k) {
             if (k0 + k < K) {
-                a[k] = c.ld(x + (k0 + k) * sa);
-                b[k] = c.ld(y + (k0 + k) * sb);
+                a[k] = c.ld(c.adv(x, (k0 + k) * sa));
+                b[k] = c.ld(c.adv(y, (k0 + k) * sb));
             }
         }
 #pragma unroll
@@ -83,139 +75,205 @@ NDVM_HD double dot_chain(const C &c, uint32_t x, uint32_t y, uint32_t K, uint32_
     return s;
 }
 
+// Block of N <= 4 dot products sharing the X operand: d[j] = chain over
+// k < K of X[k] * Y[k][j]; every operand is read before the chains start.
+template <uint32_t K, uint32_t N, class C, class W>
+NDVM_HD void dot_block_kn(const C &c, bool acc, const W &p, uint32_t sx, uint32_t sy, uint32_t sc, bool neg) {
+    const auto a = p.a(), x = p.x(), y = p.y();
+    double X[K], Y[K][N], base[N];
+#pragma unroll
+    for (uint32_t k = 0; k < K; ++k) {
+        X[k] = c.ld(c.adv(x, k * sx));
+#pragma unroll
+        for (uint32_t j = 0; j < N; ++j) Y[k][j] = c.ld(c.adv(y, k * sy + j * sc));
+    }
+    double g = 1.0;
+    const bool first = p.first();
+    if (acc) {
+        g = c.ld(p.z());
+#pragma unroll
+        for (uint32_t j = 0; j < N; ++j) base[j] = base_of(c, c.adv(a, j), first);
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < N; ++j) {
+        double s = X[0] * Y[0][j];
+#pragma unroll
+        for (uint32_t k = 1; k < K; ++k) s = fma(X[k], Y[k][j], s);
+        if (acc) {
+            if (neg) s = -s;
+            s = g != 0.0 ? base[j] + s : base[j];
+        }
+        c.st(c.adv(a, j), s);
+    }
+}
+
+// any K, N <= 7: the same arithmetic with uniform loop bounds
+template <class C, class W>
+NDVM_HD void dot_block_generic(const C &c, bool acc, const W &p, uint32_t K, uint32_t N, uint32_t sx, uint32_t sy,
+                               uint32_t sc, bool neg) {
+    const auto a = p.a(), x = p.x(), y = p.y();
+    const double g = acc ? c.ld(p.z()) : 1.0;
+    const bool first = p.first();
+    for (uint32_t j = 0; j < N; ++j) {
+        double s = c.ld(x) * c.ld(c.adv(y, j * sc));
+        for (uint32_t k = 1; k < K; ++k) s = fma(c.ld(c.adv(x, k * sx)), c.ld(c.adv(y, k * sy + j * sc)), s);
+        if (acc) {
+            if (neg) s = -s;
+            const double b = base_of(c, c.adv(a, j), first);
+            s = g != 0.0 ? b + s : b;
+        }
+        c.st(c.adv(a, j), s);
+    }
+}
+
+template <class C, class W>
+NDVM_HD void dot_block(const C &c, bool acc, const W &p) {
+    const uint32_t im = p.imm();
+    const uint32_t K = im & 7u, N = (im >> 3) & 7u, sx = (im >> 6) & 7u, sy = (im >> 9) & 7u,
+                   sc = (im >> 12) & 7u;
+    const bool neg = (im >> 15) & 1u;
+    // shapes of sides 1, 2 and 4 unrolled; others through the generic loops
+    switch (K * 8 + N) {
+#define NDVM_KN(k, n) \
+    case k * 8 + n: dot_block_kn<k, n>(c, acc, p, sx, sy, sc, neg); return;
+    NDVM_KN(1, 1) NDVM_KN(1, 2) NDVM_KN(1, 4)
+    NDVM_KN(2, 1) NDVM_KN(2, 2) NDVM_KN(2, 4)
+    NDVM_KN(4, 1) NDVM_KN(4, 2) NDVM_KN(4, 4)
+#undef NDVM_KN
+    default: dot_block_generic(c, acc, p, K, N, sx, sy, sc, neg); return;
+    }
+}
+
 // Hot micro-ops (forms below HOT_END): straight-line code, no per-lane
 // branches.
 template <class C, class W>
 NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
-    const uint32_t w0 = p.x;
     if (form == MAC) {   // the most frequent form first
-        const double x = c.ld(p.y), y = c.ld(p.z), z = c.ld(p.w);
-        c.st(w0, x * y + z);
+        const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+        c.st(p.a(), x * y + z);
         return;
     }
     switch (form) {
     case ACC: {
-        const double x = c.ld(p.y), y = c.ld(p.z), z = c.ld_raw(p.w);
-        const double base = (w0 & kFirst) ? 0.0 : z;
-        const bool on = (!(w0 & kGated)) | (x != 0.0);
-        c.st(w0, on ? base + x * y : base);
+        const auto a = p.a();
+        const double x = c.ld(p.x()), y = c.ld(p.y());
+        const double base = base_of(c, a, p.first());
+        const bool on = (!p.gated()) | (x != 0.0);
+        c.st(a, on ? base + x * y : base);
         return;
     }
     case MACG: {
-        const double x = c.ld(p.y), y = c.ld(p.z), g = c.ld(p.w);
-        const double base = base_of(c, w0);
-        c.st(w0, g != 0.0 ? base + x * y : base);
+        const auto a = p.a();
+        const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());
+        const double base = base_of(c, a, p.first());
+        c.st(a, g != 0.0 ? base + x * y : base);
         return;
     }
     case DIV:
-        c.st(w0, c.ld(p.y) / c.ld(p.z));
+        c.st(p.a(), c.ld(p.x()) / c.ld(p.y()));
         return;
     case ACCD: {
-        const double x = c.ld(p.y), y = c.ld(p.z), g = c.ld(p.w);
-        const double base = base_of(c, w0);
-        c.st(w0, g != 0.0 ? base + x / y : base);
+        const auto a = p.a();
+        const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());
+        const double base = base_of(c, a, p.first());
+        c.st(a, g != 0.0 ? base + x / y : base);
         return;
     }
     case ACCND: {
-        const double x = c.ld(p.y), y = c.ld(p.z), g = c.ld(p.w);
-        const double base = base_of(c, w0);
-        c.st(w0, g != 0.0 ? base + -(x / y) : base);
+        const auto a = p.a();
+        const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());
+        const double base = base_of(c, a, p.first());
+        c.st(a, g != 0.0 ? base + -(x / y) : base);
         return;
     }
     case DOT: {
-        const uint32_t i1 = imm1<C>(p);
-        c.st(w0, dot_chain(c, p.y, p.z, i1 & 0x7Fu, imm2<C>(p), imm3<C>(p)));
+        const uint32_t im = p.imm();
+        c.st(p.a(), dot_chain(c, p.x(), p.y(), im & 31u, (im >> 6) & 63u, (im >> 12) & 63u));
         return;
     }
     case DOTACC: {
-        const uint32_t i1 = imm1<C>(p);
-        double s = dot_chain(c, p.y, p.z, i1 & 0x7Fu, imm2<C>(p), imm3<C>(p));
-        if (i1 & kNegate) s = -s;
-        const double g = c.ld(p.w);
-        const double base = base_of(c, w0);
-        c.st(w0, g != 0.0 ? base + s : base);
+        const uint32_t im = p.imm();
+        const auto a = p.a();
+        double s = dot_chain(c, p.x(), p.y(), im & 31u, (im >> 6) & 63u, (im >> 12) & 63u);
+        if ((im >> 5) & 1u) s = -s;
+        const double g = c.ld(p.z());
+        const double base = base_of(c, a, p.first());
+        c.st(a, g != 0.0 ? base + s : base);
         return;
     }
     case CMPLT:
-        c.st(w0, c.ld(p.y) < c.ld(p.z) ? 1.0 : 0.0);
+        c.st(p.a(), c.ld(p.x()) < c.ld(p.y()) ? 1.0 : 0.0);
         return;
     case SELP: {
-        const double q = c.ld(p.y), y = c.ld(p.z), z = c.ld(p.w);
-        c.st(w0, q != 0.0 ? y : z);
+        const double q = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+        c.st(p.a(), q != 0.0 ? y : z);
         return;
     }
     case ACCSEL: {
-        const double x = c.ld(p.y), q = c.ld(p.z), g = c.ld(p.w);
-        const bool want = imm1<C>(p) != 0;
-        const double base = base_of(c, w0);
-        c.st(w0, ((g != 0.0) & ((q != 0.0) == want)) ? base + x : base);
+        const auto a = p.a();
+        const double x = c.ld(p.x()), q = c.ld(p.y()), g = c.ld(p.z());
+        const bool want = (p.imm() & 1u) != 0;
+        const double base = base_of(c, a, p.first());
+        c.st(a, ((g != 0.0) & ((q != 0.0) == want)) ? base + x : base);
         return;
     }
     case DET2: {
-        const double a0 = c.ld(p.y), a1 = c.ld(p.y + 1), a2 = c.ld(p.y + 2), a3 = c.ld(p.y + 3);
+        const auto x = p.x();
+        const double a0 = c.ld(x), a1 = c.ld(c.adv(x, 1)), a2 = c.ld(c.adv(x, 2)), a3 = c.ld(c.adv(x, 3));
         const double t1 = a0 * a3;
         const double t2 = a1 * a2;
-        c.st(w0, t1 - t2);
+        c.st(p.a(), t1 - t2);
         return;
     }
     case NZ: {
         // reads in groups of four; bitwise ors, so no lane skips a read
-        const uint32_t K = imm1<C>(p);
+        const uint32_t K = p.imm();
+        const auto x = p.x();
         bool nz = false;
         for (uint32_t k0 = 0; k0 < K; k0 += 4) {
             double v[4];
 #pragma unroll
-            for (uint32_t k = 0; k < 4; ++k) v[k] = k0 + k < K ? c.ld(p.y + k0 + k) : 0.0;
+            for (uint32_t k = 0; k < 4; ++k) v[k] = k0 + k < K ? c.ld(c.adv(x, k0 + k)) : 0.0;
 #pragma unroll
             for (uint32_t k = 0; k < 4; ++k) nz = nz | (v[k] != 0.0);
         }
-        c.st(w0, nz ? 1.0 : 0.0);
+        c.st(p.a(), nz ? 1.0 : 0.0);
         return;
     }
     case GATEGT: {
-        const double x = c.ld(p.y), y = c.ld(p.z), g = c.ld(p.w);
-        c.st(w0, ((g != 0.0) & (x > y)) ? 1.0 : 0.0);
+        const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());
+        c.st(p.a(), ((g != 0.0) & (x > y)) ? 1.0 : 0.0);
         return;
     }
     case ACCABS: {
-        const double x = c.ld(p.y), a = c.ld(p.z), g = c.ld(p.w);
-        const double v = a > 0.0 ? x : (a < 0.0 ? -x : 0.0);
-        const double base = base_of(c, w0);
-        c.st(w0, g != 0.0 ? base + v : base);
+        const auto a = p.a();
+        const double x = c.ld(p.x()), v = c.ld(p.y()), g = c.ld(p.z());
+        const double d = v > 0.0 ? x : (v < 0.0 ? -x : 0.0);
+        const double base = base_of(c, a, p.first());
+        c.st(a, g != 0.0 ? base + d : base);
         return;
     }
     case SUMK: {
         // reads in groups of four, then the sum in index order
-        const uint32_t K = imm1<C>(p), st = imm2<C>(p);
+        const uint32_t im = p.imm(), K = im & 63u, st = (im >> 6) & 63u;
+        const auto x = p.x();
         double s = 0.0;
         for (uint32_t k0 = 0; k0 < K; k0 += 4) {
             double v[4];
 #pragma unroll
-            for (uint32_t k = 0; k < 4; ++k) v[k] = k0 + k < K ? c.ld(p.y + (k0 + k) * st) : 0.0;
+            for (uint32_t k = 0; k < 4; ++k) v[k] = k0 + k < K ? c.ld(c.adv(x, (k0 + k) * st)) : 0.0;
 #pragma unroll
             for (uint32_t k = 0; k < 4; ++k)
                 if (k0 + k < K) s = (k0 + k == 0) ? v[0] : s + v[k];
         }
-        c.st(w0, s);
+        c.st(p.a(), s);
         return;
     }
-    case LDOBS:
-        c.st(w0, c.obsv(p.y & kFieldMask));
-        return;
-    case LDPARAM:
-        c.st(w0, c.param(p.y & kFieldMask));
-        return;
-    case LDCONST:
-        c.st(w0, c.konst(p.y & kFieldMask));
-        return;
-    case CKST:
-        c.ckst(p.y & kFieldMask, c.ld(w0));
-        return;
-    case CKLD:
-        c.st(w0, c.ckld(p.y & kFieldMask));
-        return;
     case ZERO:
-        c.st(w0, 0.0);
+        c.st(p.a(), 0.0);
+        return;
+    case DOTB: case DOTBACC:
+        dot_block(c, form == DOTBACC, p);
         return;
     default:
         return;
@@ -225,12 +283,11 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
 // Cold micro-ops (everything but END, which the caller handles).
 template <class C, class W>
 NDVM_HD void exec_cold(const C &c, uint32_t form, const W &p) {
-    const uint32_t w0 = p.x;
     switch (form) {
     case UN: {
-        const double x = c.ld(p.y);
+        const double x = c.ld(p.x());
         double r;
-        switch (imm1<C>(p)) {
+        switch (p.imm()) {
         case U_EXP: r = exp(x); break;
         case U_LOGC: r = log(clampv(x)); break;
         case U_SQRTC: r = sqrt(clampv(x)); break;
@@ -239,17 +296,50 @@ NDVM_HD void exec_cold(const C &c, uint32_t form, const W &p) {
         case U_ABS: r = fabs(x); break;
         default: r = log(x); break;
         }
-        c.st(w0, r);
+        c.st(p.a(), r);
         return;
     }
     case POW:
-        c.st(w0, pow(c.ld(p.y), c.ld(p.z)));
+        c.st(p.a(), pow(c.ld(p.x()), c.ld(p.y())));
         return;
+    case LDOBS:
+        c.st(p.a(), c.obsv(p.ix()));
+        return;
+    case LDPARAM:
+        c.st(p.a(), c.param(p.ix()));
+        return;
+    case LDCONST:
+        c.st(p.a(), c.konst(p.ix()));
+        return;
+    case CKST: {   // all loads issued before the first store
+        const uint32_t n = p.imm(), row = p.ix();
+        const auto a = p.a();
+        double v[kMaxBlock];
+#pragma unroll
+        for (uint32_t k = 0; k < kMaxBlock; ++k)
+            if (k < n) v[k] = c.ld(c.adv(a, k));
+#pragma unroll
+        for (uint32_t k = 0; k < kMaxBlock; ++k)
+            if (k < n) c.ckst(row + k, v[k]);
+        return;
+    }
+    case CKLD: {   // all loads issued before the first write
+        const uint32_t n = p.imm(), row = p.ix();
+        const auto a = p.a();
+        double v[kMaxBlock];
+#pragma unroll
+        for (uint32_t k = 0; k < kMaxBlock; ++k)
+            if (k < n) v[k] = c.ckld(row + k);
+#pragma unroll
+        for (uint32_t k = 0; k < kMaxBlock; ++k)
+            if (k < n) c.st(c.adv(a, k), v[k]);
+        return;
+    }
     case STLOSS:
-        c.store_loss(c.ld(w0), c.slot() < imm1<C>(p));
+        c.store_loss(c.ld(p.a()), c.slot() < p.imm());
         return;
     case STGRAD:
-        c.store_grad(p.y & kFieldMask, c.ld(w0), c.slot() < imm1<C>(p));
+        c.store_grad(p.ix(), c.ld(p.a()), c.slot() < p.imm());
         return;
     default:
         return;
