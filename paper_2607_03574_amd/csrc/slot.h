@@ -59,15 +59,14 @@ enum Form : uint32_t {
     // (ascending, first term a product)
     DOTB,
     DOTBACC,   // t[c] = gate(z) ? base[c] + (+/-)dot[c] : base[c]
-    HOT_END,
-    // ---- cold forms: library transcendentals (per-lane branches) and
-    // global memory traffic (kept out of the hot loop so that no hot form
-    // waits on the program fetch in flight)
-    LDOBS = 32,   // d = obs[x]
+    LDOBS,      // d = obs[x]
     LDPARAM,   // d = params[lane, x]
     LDCONST,   // d = consts[x]
     CKST,      // ckpt rows x .. x + n - 1 of this lane = registers a .. a + n - 1  (imm = n)
     CKLD,      // registers a .. a + n - 1 = ckpt rows x .. x + n - 1 of this lane
+    HOT_END,
+    // ---- cold forms: library transcendentals (per-lane branches) and the
+    // loss and gradient stores (masked per slot)
     UN = 40,   // d = f(x), f = imm: see Unary
     POW,       // d = pow(x, y)
     STLOSS,    // loss[lane] = register a          (slots < imm only)

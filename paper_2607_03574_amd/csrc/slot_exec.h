@@ -275,33 +275,6 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
     case DOTB: case DOTBACC:
         dot_block(c, form == DOTBACC, p);
         return;
-    default:
-        return;
-    }
-}
-
-// Cold micro-ops (everything but END, which the caller handles).
-template <class C, class W>
-NDVM_HD void exec_cold(const C &c, uint32_t form, const W &p) {
-    switch (form) {
-    case UN: {
-        const double x = c.ld(p.x());
-        double r;
-        switch (p.imm()) {
-        case U_EXP: r = exp(x); break;
-        case U_LOGC: r = log(clampv(x)); break;
-        case U_SQRTC: r = sqrt(clampv(x)); break;
-        case U_SIN: r = sin(x); break;
-        case U_COS: r = cos(x); break;
-        case U_ABS: r = fabs(x); break;
-        default: r = log(x); break;
-        }
-        c.st(p.a(), r);
-        return;
-    }
-    case POW:
-        c.st(p.a(), pow(c.ld(p.x()), c.ld(p.y())));
-        return;
     case LDOBS:
         c.st(p.a(), c.obsv(p.ix()));
         return;
@@ -335,6 +308,33 @@ NDVM_HD void exec_cold(const C &c, uint32_t form, const W &p) {
             if (k < n) c.st(c.adv(a, k), v[k]);
         return;
     }
+    default:
+        return;
+    }
+}
+
+// Cold micro-ops (everything but END, which the caller handles).
+template <class C, class W>
+NDVM_HD void exec_cold(const C &c, uint32_t form, const W &p) {
+    switch (form) {
+    case UN: {
+        const double x = c.ld(p.x());
+        double r;
+        switch (p.imm()) {
+        case U_EXP: r = exp(x); break;
+        case U_LOGC: r = log(clampv(x)); break;
+        case U_SQRTC: r = sqrt(clampv(x)); break;
+        case U_SIN: r = sin(x); break;
+        case U_COS: r = cos(x); break;
+        case U_ABS: r = fabs(x); break;
+        default: r = log(x); break;
+        }
+        c.st(p.a(), r);
+        return;
+    }
+    case POW:
+        c.st(p.a(), pow(c.ld(p.x()), c.ld(p.y())));
+        return;
     case STLOSS:
         c.store_loss(c.ld(p.a()), c.slot() < p.imm());
         return;
