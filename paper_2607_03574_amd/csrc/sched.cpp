@@ -641,7 +641,7 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
         if (f == DOTBACC) rd.push_back(z);
         break;
     }
-    case DIV: case CMPLT: case POW:
+    case DIV: case CMPLT: case POWF:
         rd = {x, y};
         wr = {a};
         break;
@@ -657,7 +657,7 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
         for (uint32_t k = 0; k < (im & 63u); ++k) rd.push_back(x + k * ((im >> 6) & 63u));
         wr = {a};
         break;
-    case UN:
+    case UN: case EXPF: case LOGCF: case LOGF: case SQRTCF: case ABSF:
         rd = {x};
         wr = {a};
         break;
@@ -950,15 +950,19 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             for (uint32_t i = 0; i < n; ++i) E.put(MAC, dst + i, 0, A + i, kMinusOne, kNegZero);
             return;
         }
-        case tp::EXP: case tp::LOG: case tp::SQRT: case tp::SIN: case tp::COS: case tp::ABS: {
+        case tp::EXP: case tp::LOG: case tp::SQRT: case tp::ABS: {
             const uint32_t A = operand(o.a);
-            const uint32_t f = o.code == tp::EXP ? U_EXP : o.code == tp::LOG ? U_LOGC : o.code == tp::SQRT ? U_SQRTC
-                             : o.code == tp::SIN ? U_SIN : o.code == tp::COS ? U_COS : U_ABS;
-            for (uint32_t i = 0; i < n; ++i) E.put(UN, dst + i, 0, A + i, 0, 0, f);
+            const uint32_t f = o.code == tp::EXP ? EXPF : o.code == tp::LOG ? LOGCF : o.code == tp::SQRT ? SQRTCF : ABSF;
+            for (uint32_t i = 0; i < n; ++i) E.put(f, dst + i, 0, A + i);
+            return;
+        }
+        case tp::SIN: case tp::COS: {
+            const uint32_t A = operand(o.a);
+            for (uint32_t i = 0; i < n; ++i) E.put(UN, dst + i, 0, A + i, 0, 0, o.code == tp::SIN ? U_SIN : U_COS);
             return;
         }
         case tp::POW:
-            E.put(POW, dst, 0, operand(o.a), operand(o.b));
+            E.put(POWF, dst, 0, operand(o.a), operand(o.b));
             return;
         case tp::DOT:
             E.put(DOT, dst, 0, operand(o.a), operand(o.b), 0, dot_imm(I.nel[o.a], 1, 1, false));
@@ -1008,7 +1012,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             } else if (o.code == tp::DET) {
                 mov(dst, A);
             }
-            if (o.code == tp::LOGDET) E.put(UN, dst, 0, d, 0, 0, U_LOGC);
+            if (o.code == tp::LOGDET) E.put(LOGCF, dst, 0, d);
             return;
         }
         case tp::OUTER: {
@@ -1302,7 +1306,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                 if (tb != kNone) {   // b += (g * z) * ln a
                     const uint32_t t3 = E.tmp(), t4 = E.tmp();
                     E.put(MAC, t3, 0, g, Z, kNegZero);
-                    E.put(UN, t4, 0, A, 0, 0, U_LOG);
+                    E.put(LOGF, t4, 0, A);
                     E.put(MACG, tb, fb_, t3, t4, g);
                 }
                 return;

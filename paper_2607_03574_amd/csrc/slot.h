@@ -59,22 +59,27 @@ enum Form : uint32_t {
     // (ascending, first term a product)
     DOTB,
     DOTBACC,   // t[c] = gate(z) ? base[c] + (+/-)dot[c] : base[c]
+    EXPF,      // d = exp(x)      (library functions without per-lane branches)
+    LOGCF,     // d = log(max(x, 1e-8)) with x < 1e-8 -> 1e-8 (NaN propagates)
+    LOGF,      // d = log(x)
+    SQRTCF,    // d = sqrt(max(x, 1e-8)), clamped as LOGCF
+    ABSF,      // d = |x|
     LDOBS,      // d = obs[x]
     LDPARAM,   // d = params[lane, x]
     LDCONST,   // d = consts[x]
     CKST,      // ckpt rows x .. x + n - 1 of this lane = registers a .. a + n - 1  (imm = n)
     CKLD,      // registers a .. a + n - 1 = ckpt rows x .. x + n - 1 of this lane
     HOT_END,
-    // ---- cold forms: library transcendentals (per-lane branches) and the
-    // loss and gradient stores (masked per slot)
+    // ---- cold forms: sine and cosine (their library code branches per
+    // lane), pow, and the loss and gradient stores (masked per slot)
     UN = 40,   // d = f(x), f = imm: see Unary
-    POW,       // d = pow(x, y)
+    POWF,      // d = pow(x, y)   (heavy: kept out of line to spare registers)
     STLOSS,    // loss[lane] = register a          (slots < imm only)
     STGRAD,    // grad[lane, x] = register a       (slots < imm only)
     END = 63,
 };
 
-enum Unary : uint32_t { U_EXP = 0, U_LOGC, U_SQRTC, U_SIN, U_COS, U_ABS, U_LOG };
+enum Unary : uint32_t { U_SIN = 0, U_COS };
 
 constexpr uint32_t kFormMask = 63u;
 constexpr uint32_t kFirstShift = 6, kGatedShift = 10, kImmShift = 14;

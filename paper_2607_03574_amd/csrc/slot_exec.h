@@ -275,6 +275,22 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
     case DOTB: case DOTBACC:
         dot_block(c, form == DOTBACC, p);
         return;
+    case EXPF:
+        c.st(p.a(), exp(c.ld(p.x())));
+        return;
+    case LOGCF:
+        c.st(p.a(), log(clampv(c.ld(p.x()))));
+        return;
+    case LOGF:
+        c.st(p.a(), log(c.ld(p.x())));
+        return;
+    case SQRTCF:
+        c.st(p.a(), sqrt(clampv(c.ld(p.x()))));
+        return;
+    case ABSF:
+        c.st(p.a(), fabs(c.ld(p.x())));
+        return;
+
     case LDOBS:
         c.st(p.a(), c.obsv(p.ix()));
         return;
@@ -313,26 +329,17 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
     }
 }
 
-// Cold micro-ops (everything but END, which the caller handles).
+// Cold micro-ops (everything but END, which the caller handles): sine,
+// cosine, pow, loss and gradient stores.
 template <class C, class W>
 NDVM_HD void exec_cold(const C &c, uint32_t form, const W &p) {
     switch (form) {
     case UN: {
         const double x = c.ld(p.x());
-        double r;
-        switch (p.imm()) {
-        case U_EXP: r = exp(x); break;
-        case U_LOGC: r = log(clampv(x)); break;
-        case U_SQRTC: r = sqrt(clampv(x)); break;
-        case U_SIN: r = sin(x); break;
-        case U_COS: r = cos(x); break;
-        case U_ABS: r = fabs(x); break;
-        default: r = log(x); break;
-        }
-        c.st(p.a(), r);
+        c.st(p.a(), p.imm() == U_SIN ? sin(x) : cos(x));
         return;
     }
-    case POW:
+    case POWF:
         c.st(p.a(), pow(c.ld(p.x()), c.ld(p.y())));
         return;
     case STLOSS:
