@@ -212,7 +212,7 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
  * returns the number of words, or -1 on an error.
  */
 int64_t ndvm_emu_program(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_budget, uint32_t slots,
-                         uint32_t *out, size_t cap) {
+                         uint32_t *out, size_t cap, uint32_t *hdr_off) {
     Tape t;
     if (parse_tape(tape, len, &t) != NDVM_OK) return -1;
     Schedule S;
@@ -224,6 +224,7 @@ int64_t ndvm_emu_program(const uint8_t *tape, size_t len, int with_grad, uint32_
     }
     const size_t n = S.code.size();
     if (out && cap >= n) std::copy(S.code.begin(), S.code.end(), out);
+    if (hdr_off) *hdr_off = S.hdr_off;
     return int64_t(n);
 }
 

@@ -24,7 +24,7 @@ def lib():
         g = _lib.ndvm_emu_program
         g.restype = ctypes.c_int64
         g.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, vp,
-                      ctypes.c_size_t]
+                      ctypes.c_size_t, vp]
     return _lib
 
 
@@ -48,11 +48,17 @@ def run(tape: bytes, params, obs, with_grad=True, budget=320, slots=4):
 
 
 def program(tape: bytes, with_grad=True, budget=320, slots=4):
-    """The scheduled device program as an (n_instr, slots, 4) array of uint32
-    payload words, in instruction order (END instructions included)."""
-    n = lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, slots, None, 0)
-    assert n >= 0
+    """The scheduled device program in instruction order: (headers[n_instr],
+    words[n_instr, 4 rows, 4]) as uint32 arrays (padding after END included).
+    The device layout is chunk-major ([chunk][row][instr][4] words), then the
+    header words."""
+    n = lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, slots, None, 0, None)
+    assert n >= 0, lib().ndvm_emu_error()
     out = np.empty(n, dtype=np.uint32)
-    lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, slots, out.ctypes.data, n)
-    chunk = 4
-    return out.reshape(-1, slots, chunk, 4).transpose(0, 2, 1, 3).reshape(-1, slots, 4)
+    hdr_off = ctypes.c_uint32(0)
+    lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, slots, out.ctypes.data, n,
+                           ctypes.byref(hdr_off))
+    k = hdr_off.value
+    words = out[:k].reshape(-1, 4, 4, 4).transpose(0, 2, 1, 3).reshape(-1, 4, 4)
+    headers = out[k:k + words.shape[0]]
+    return headers, words

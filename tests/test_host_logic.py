@@ -183,9 +183,9 @@ def test_schedule_is_deterministic():
 
 
 def test_emulated_wide_program_beyond_packed_register_fields(oracle_mod):
-    # 17000 parameters put parameter adjoints above register 2^15, so reverse
-    # pairs whose registers do not fit the packed 16-bit fields must fall back
-    # to single rules; the gradient of sum_i p_i p_(i+1) is p_(i-1) + p_(i+1)
+    # 17000 parameters put the register file far past any LDS budget (the
+    # tail spills to workspace rows) and register byte offsets past 16 bits;
+    # the gradient of sum_i p_i p_(i+1) is p_(i-1) + p_(i+1)
     P = 17000
     A = Asm(P, 0)
     A.param(0).param(1).mul()
@@ -203,6 +203,41 @@ def test_emulated_wide_program_beyond_packed_register_fields(oracle_mod):
     want[:, 1:] += params[:, :-1]
     np.testing.assert_array_equal(ge, go)
     np.testing.assert_allclose(ge, want, rtol=0, atol=0)
+
+
+# form numbers of the device program format (slot.h)
+HOT_FORMS = set(range(1, 30))
+COLD_FORMS = {40, 41, 42, 43}
+END = 63
+INDEX_X = {25, 26, 27, 28, 29, 43}      # LDOBS LDPARAM LDCONST CKST CKLD STGRAD
+NO_A = {28, 42, 43}                     # CKST STLOSS STGRAD (register a is read)
+
+
+@pytest.mark.parametrize("name,kw", CASES)
+def test_device_program_encoding(name, kw):
+    """The encoded program: known forms only, END once followed by END padding,
+    register fields as byte offsets of whole 16-lane registers inside the
+    register file, slot flags only where a slot exists."""
+    w = configs.build(name, **kw)
+    tape = nd.tape_build(w.bytecode)
+    budget = 48
+    _, _, st = emu.run(tape, w.params[:1], w.obs, True, budget)
+    headers, words = emu.program(tape, True, budget)
+    forms = headers & 63
+    n = int(np.argmax(forms == END)) + 1
+    assert n == st["n_instr"]
+    assert set(forms[n:len(words)].tolist()) <= {END}
+    assert set(forms[:n].tolist()) <= HOT_FORMS | COLD_FORMS | {END}
+    stride = 16 * 8
+    for k in range(n - 1):
+        f = int(forms[k])
+        regs = words[k, :, 0:1] if f in INDEX_X else words[k, :, [0, 2, 3]].T
+        if f in (1, 2, 3, 4, 5, 6):       # every field of these forms names a register
+            regs = words[k]
+        assert (regs % stride == 0).all(), (k, f)
+        assert (regs // stride < st["n_regs"] + 8).all(), (k, f)
+    # all four slots of every executed instruction carry a micro-op
+    assert st["n_uops"] <= 4 * st["n_instr"]
 
 
 def test_bench_traffic_only_for_matching_kernel_sources(tmp_path, monkeypatch):
