@@ -28,7 +28,11 @@ DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-p
           # the interpreter's dispatch branches are wave-uniform: leave such
           # regions unstructured instead of routing every handler exit through
           # a chain of flow blocks
-          "-mllvm", "-structurizecfg-skip-uniform-regions=true"]
+          "-mllvm", "-structurizecfg-skip-uniform-regions=true",
+          # keep every handler's final register store in the handler: sunk
+          # into a shared block it would wait there for the memory traffic
+          # of every other handler (the program prefetch included)
+          "-mllvm", "-sink-common-insts=false", "-mllvm", "-enable-tail-merge=false"]
 
 
 def _compile(src: str) -> str:

@@ -81,6 +81,12 @@ __device__ __forceinline__ uint32_t lane_word(uint32_t v, uint32_t lane) {
     return uint32_t(__builtin_amdgcn_readlane(int(v), int(lane)));
 }
 
+// A copy of a wave-uniform value that the compiler cannot see through.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+    asm("" : "+s"(v));
+    return v;
+}
+
 // LDS addresses of the four register fields of instruction P: each is the
 // broadcast byte offset plus this thread's lane address, one DPP-sourced add
 // per field (the s_nop covers the wait states a DPP read of a VGPR written
@@ -138,17 +144,31 @@ template <int P, class C>
 __device__ __forceinline__ uint32_t step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb) {
     const uint32_t hdr = lane_word(hv, hb + P);
     const uint32_t form = hdr & slot::kFormMask;
-    if (form < slot::HOT_END) {
-        ChunkPayload<P> p;
-        field_addrs<P>(ch, c.lane_addr, p.ha, p.hx, p.hy, p.hz);
-        p.ch = ch;
-        p.hdr = hdr;
-        p.slot = c.slot_;
-        slotx::exec_hot(c, form, p);
+    ChunkPayload<P> p;
+    field_addrs<P>(ch, c.lane_addr, p.ha, p.hx, p.hy, p.hz);
+    p.ch = ch;
+    p.hdr = hdr;
+    p.slot = c.slot_;
+    // multiply-add and the linear adjoint rule are tested one by one ahead
+    // of the dispatch tree; the empty asm hides that the later tests are on
+    // the same value, so the compiler cannot fold them into one balanced
+    // tree (which would put every form several compares deep)
+    if (form == slot::MAC) {
+        slotx::exec_mac(c, p);
         return 0;
     }
-    if (form == slot::END) return 1;
-    cold_call(c, form,
+    const uint32_t f1 = opaque(form);
+    if (f1 == slot::ACC) {
+        slotx::exec_acc(c, p);
+        return 0;
+    }
+    const uint32_t f2 = opaque(f1);
+    if (f2 < slot::HOT_END) {
+        slotx::exec_hot(c, f2, p);
+        return 0;
+    }
+    if (f2 == slot::END) return 1;
+    cold_call(c, f2,
               Payload{{row_word<4 * P>(ch), row_word<4 * P + 1>(ch), row_word<4 * P + 2>(ch), row_word<4 * P + 3>(ch)},
                       hdr, c.slot_, c.lane_addr});
     return 0;

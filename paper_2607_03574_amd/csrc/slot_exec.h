@@ -144,24 +144,33 @@ NDVM_HD void dot_block(const C &c, bool acc, const W &p) {
     }
 }
 
+// The two most frequent forms, also callable on their own (the kernel tests
+// for them ahead of the general dispatch).
+template <class C, class W>
+NDVM_HD void exec_mac(const C &c, const W &p) {
+    const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+    c.st(p.a(), x * y + z);
+}
+template <class C, class W>
+NDVM_HD void exec_acc(const C &c, const W &p) {
+    const auto a = p.a();
+    const double x = c.ld(p.x()), y = c.ld(p.y());
+    const double base = base_of(c, a, p.first());
+    const bool on = (!p.gated()) | (x != 0.0);
+    c.st(a, on ? base + x * y : base);
+}
+
 // Hot micro-ops (forms below HOT_END): straight-line code, no per-lane
 // branches.
 template <class C, class W>
 NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
-    if (form == MAC) {   // the most frequent form first
-        const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
-        c.st(p.a(), x * y + z);
-        return;
-    }
     switch (form) {
-    case ACC: {
-        const auto a = p.a();
-        const double x = c.ld(p.x()), y = c.ld(p.y());
-        const double base = base_of(c, a, p.first());
-        const bool on = (!p.gated()) | (x != 0.0);
-        c.st(a, on ? base + x * y : base);
+    case MAC:
+        exec_mac(c, p);
         return;
-    }
+    case ACC:
+        exec_acc(c, p);
+        return;
     case MACG: {
         const auto a = p.a();
         const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());
