@@ -116,6 +116,7 @@ struct HostCtx {
         if (row >= n_ckpt) { flag(4); return; }
         ckpt[row] = v;
     }
+    static void settle(double) {}
     double ckld(uint32_t row) const {
         if (row >= n_ckpt) { flag(4); return NAN; }
         return ckpt[row];

@@ -61,6 +61,7 @@ struct DevCtx {
     __device__ __forceinline__ double obsv(uint32_t i) const { return obs[i]; }
     __device__ __forceinline__ double konst(uint32_t i) const { return consts[i]; }
     __device__ __forceinline__ double param(uint32_t p) const { return params[lc * ld_p + p]; }
+    __device__ __forceinline__ static void settle(double v) { asm volatile("" ::"v"(v)); }
     __device__ __forceinline__ double ckld(uint32_t row) const { return ckpt[int64_t(row) * Lpad + lane]; }
     __device__ __forceinline__ void ckst(uint32_t row, double v) const { ckpt[int64_t(row) * Lpad + lane] = v; }
     __device__ __forceinline__ void store_loss(double v, bool on) const {

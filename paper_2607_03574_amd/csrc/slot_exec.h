@@ -9,6 +9,7 @@
 //   void st(R h, double v) const;  R adv(R h, uint32_t n) const;  (n registers further)
 //   double obsv(uint32_t i) const;  double param(uint32_t p) const;  double konst(uint32_t i) const;
 //   double ckld(uint32_t row) const;  void ckst(uint32_t row, double v) const;
+//   void settle(double v) const;  (a no-op use of v that waits for any load of v to land)
 //   void store_loss(double v, bool on) const;  void store_grad(uint32_t p, double v, bool on) const;
 //   uint32_t slot() const;
 // and W is the payload of this slot's micro-op: register handles a(), x(),
@@ -319,6 +320,8 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
 #pragma unroll
         for (uint32_t k = 0; k < kMaxBlock; ++k)
             if (k < n) c.ckst(row + k, v[k]);
+#pragma unroll
+        for (uint32_t k = 0; k < kMaxBlock; ++k) c.settle(v[k]);
         return;
     }
     case CKLD: {   // all loads issued before the first write
@@ -331,6 +334,10 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
 #pragma unroll
         for (uint32_t k = 0; k < kMaxBlock; ++k)
             if (k < n) c.st(c.adv(a, k), v[k]);
+        // every path leaves with all loads landed, so the next handler does
+        // not wait for the program prefetch before its own register reads
+#pragma unroll
+        for (uint32_t k = 0; k < kMaxBlock; ++k) c.settle(v[k]);
         return;
     }
     default:
