@@ -76,6 +76,19 @@ NDVM_HD double dot_chain(const C &c, R x, R y, uint32_t K, uint32_t sa, uint32_t
     return s;
 }
 
+// d = 1 if any of the K registers from x on is nonzero, else 0
+template <uint32_t K, class C, class W>
+NDVM_HD void any_nonzero(const C &c, const W &p) {
+    const auto x = p.x();
+    double v[K];
+#pragma unroll
+    for (uint32_t k = 0; k < K; ++k) v[k] = c.ld(c.adv(x, k));
+    bool nz = false;
+#pragma unroll
+    for (uint32_t k = 0; k < K; ++k) nz = nz | (v[k] != 0.0);
+    c.st(p.a(), nz ? 1.0 : 0.0);
+}
+
 // Block of N <= 4 dot products sharing the X operand: d[j] = chain over
 // k < K of X[k] * Y[k][j]; every operand is read before the chains start.
 template <uint32_t K, uint32_t N, class C, class W>
@@ -236,8 +249,16 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         return;
     }
     case NZ: {
-        // reads in groups of four; bitwise ors, so no lane skips a read
         const uint32_t K = p.imm();
+        switch (K) {   // the sizes of small matrices unrolled: every read issued at once
+        case 1: any_nonzero<1>(c, p); return;
+        case 2: any_nonzero<2>(c, p); return;
+        case 4: any_nonzero<4>(c, p); return;
+        case 8: any_nonzero<8>(c, p); return;
+        case 16: any_nonzero<16>(c, p); return;
+        default: break;
+        }
+        // other sizes: reads in groups of four; bitwise ors, so no lane skips a read
         const auto x = p.x();
         bool nz = false;
         for (uint32_t k0 = 0; k0 < K; k0 += 4) {
