@@ -91,8 +91,17 @@ NDVM_HD void any_nonzero(const C &c, const W &p) {
 
 // Block of N <= 4 dot products sharing the X operand: d[j] = chain over
 // k < K of X[k] * Y[k][j]; every operand is read before the chains start.
-template <uint32_t K, uint32_t N, class C, class W>
-NDVM_HD void dot_block_kn(const C &c, bool acc, const W &p, uint32_t sx, uint32_t sy, uint32_t sc, bool neg) {
+// ACC: the adjoint form (gate register z, base per output, negation).
+// Strides in registers: X[k] at x + k*sx, Y[k][j] at y + k*sy + j*sc; when
+// kStd they are the row-major ones (sx = 1, sy = N, sc = 1) and known here,
+// so register offsets fold into the reads.
+template <uint32_t K, uint32_t N, bool ACC, bool kStd, class C, class W>
+NDVM_HD void dot_block_kn(const C &c, const W &p, uint32_t sx, uint32_t sy, uint32_t sc, bool neg) {
+    if (kStd) {
+        sx = 1;
+        sy = N;
+        sc = 1;
+    }
     const auto a = p.a(), x = p.x(), y = p.y();
     double X[K], Y[K][N], base[N];
 #pragma unroll
@@ -102,8 +111,8 @@ NDVM_HD void dot_block_kn(const C &c, bool acc, const W &p, uint32_t sx, uint32_
         for (uint32_t j = 0; j < N; ++j) Y[k][j] = c.ld(c.adv(y, k * sy + j * sc));
     }
     double g = 1.0;
-    const bool first = p.first();
-    if (acc) {
+    if (ACC) {
+        const bool first = p.first();
         g = c.ld(p.z());
 #pragma unroll
         for (uint32_t j = 0; j < N; ++j) base[j] = base_of(c, c.adv(a, j), first);
@@ -113,7 +122,7 @@ NDVM_HD void dot_block_kn(const C &c, bool acc, const W &p, uint32_t sx, uint32_
         double s = X[0] * Y[0][j];
 #pragma unroll
         for (uint32_t k = 1; k < K; ++k) s = fma(X[k], Y[k][j], s);
-        if (acc) {
+        if (ACC) {
             if (neg) s = -s;
             s = g != 0.0 ? base[j] + s : base[j];
         }
@@ -122,16 +131,16 @@ NDVM_HD void dot_block_kn(const C &c, bool acc, const W &p, uint32_t sx, uint32_
 }
 
 // any K, N <= 7: the same arithmetic with uniform loop bounds
-template <class C, class W>
-NDVM_HD void dot_block_generic(const C &c, bool acc, const W &p, uint32_t K, uint32_t N, uint32_t sx, uint32_t sy,
+template <bool ACC, class C, class W>
+NDVM_HD void dot_block_generic(const C &c, const W &p, uint32_t K, uint32_t N, uint32_t sx, uint32_t sy,
                                uint32_t sc, bool neg) {
     const auto a = p.a(), x = p.x(), y = p.y();
-    const double g = acc ? c.ld(p.z()) : 1.0;
+    const double g = ACC ? c.ld(p.z()) : 1.0;
     const bool first = p.first();
     for (uint32_t j = 0; j < N; ++j) {
         double s = c.ld(x) * c.ld(c.adv(y, j * sc));
         for (uint32_t k = 1; k < K; ++k) s = fma(c.ld(c.adv(x, k * sx)), c.ld(c.adv(y, k * sy + j * sc)), s);
-        if (acc) {
+        if (ACC) {
             if (neg) s = -s;
             const double b = base_of(c, c.adv(a, j), first);
             s = g != 0.0 ? b + s : b;
@@ -140,22 +149,38 @@ NDVM_HD void dot_block_generic(const C &c, bool acc, const W &p, uint32_t K, uin
     }
 }
 
-template <class C, class W>
-NDVM_HD void dot_block(const C &c, bool acc, const W &p) {
+// Shapes with sides 1, 2 and 4 unrolled; others through the generic loops.
+// The forward form takes the row-major strides unrolled too (the layout the
+// scheduler gives forward products), the adjoint form its strides at run time.
+template <bool ACC, class C, class W>
+NDVM_HD void dot_block(const C &c, const W &p) {
     const uint32_t im = p.imm();
     const uint32_t K = im & 7u, N = (im >> 3) & 7u, sx = (im >> 6) & 7u, sy = (im >> 9) & 7u,
                    sc = (im >> 12) & 7u;
     const bool neg = (im >> 15) & 1u;
-    // shapes of sides 1, 2 and 4 unrolled; others through the generic loops
-    switch (K * 8 + N) {
+    const bool std_layout = !ACC && (K == 1 || sy == N) && (N == 1 || sc == 1) && (K == 1 || sx == 1);
+    if (std_layout) {
+        switch (K * 8 + N) {
 #define NDVM_KN(k, n) \
-    case k * 8 + n: dot_block_kn<k, n>(c, acc, p, sx, sy, sc, neg); return;
-    NDVM_KN(1, 1) NDVM_KN(1, 2) NDVM_KN(1, 4)
-    NDVM_KN(2, 1) NDVM_KN(2, 2) NDVM_KN(2, 4)
-    NDVM_KN(4, 1) NDVM_KN(4, 2) NDVM_KN(4, 4)
+    case k * 8 + n: dot_block_kn<k, n, ACC, true>(c, p, sx, sy, sc, neg); return;
+        NDVM_KN(1, 1) NDVM_KN(1, 2) NDVM_KN(1, 4)
+        NDVM_KN(2, 1) NDVM_KN(2, 2) NDVM_KN(2, 4)
+        NDVM_KN(4, 1) NDVM_KN(4, 2) NDVM_KN(4, 4)
 #undef NDVM_KN
-    default: dot_block_generic(c, acc, p, K, N, sx, sy, sc, neg); return;
+        default: break;
+        }
+    } else if (ACC) {
+        switch (K * 8 + N) {
+#define NDVM_KN(k, n) \
+    case k * 8 + n: dot_block_kn<k, n, ACC, false>(c, p, sx, sy, sc, neg); return;
+        NDVM_KN(1, 1) NDVM_KN(1, 2) NDVM_KN(1, 4)
+        NDVM_KN(2, 1) NDVM_KN(2, 2) NDVM_KN(2, 4)
+        NDVM_KN(4, 1) NDVM_KN(4, 2) NDVM_KN(4, 4)
+#undef NDVM_KN
+        default: break;
+        }
     }
+    dot_block_generic<ACC>(c, p, K, N, sx, sy, sc, neg);
 }
 
 // The two most frequent forms, also callable on their own (the kernel tests
@@ -303,8 +328,11 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
     case ZERO:
         c.st(p.a(), 0.0);
         return;
-    case DOTB: case DOTBACC:
-        dot_block(c, form == DOTBACC, p);
+    case DOTB:
+        dot_block<false>(c, p);
+        return;
+    case DOTBACC:
+        dot_block<true>(c, p);
         return;
     case EXPF:
         c.st(p.a(), exp(c.ld(p.x())));
