@@ -21,6 +21,7 @@
 #include "sched.h"
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <stdexcept>
@@ -694,9 +695,11 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
 uint64_t uop_class(const UOp &u) { return uint64_t(u.form) | uint64_t(u.imm) << 8; }
 
 // Pack micro-ops (in program order) into instructions of at most S slots
-// by list scheduling: each instruction takes the form (and immediate) with
-// the most ready micro-ops among the next kPackWindow unscheduled ones, and
-// up to S of those in program order.  A micro-op is ready when every value it
+// by list scheduling on the dependence graph: among the next kPackWindow
+// unscheduled micro-ops, each instruction takes the form (and immediate) of
+// the ready one with the longest chain of dependences after it, and up to S
+// ready micro-ops of that form, longest chains first, so the critical path
+// of a latency-bound lane goes first.  A micro-op is ready when every value it
 // reads or overwrites is final: its true and output dependences lie in
 // earlier instructions, and the micro-ops that read a register it overwrites
 // are scheduled (possibly in the same instruction, since every slot reads
@@ -762,38 +765,45 @@ std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S)
     }
     std::vector<uint64_t> cls(n);
     for (uint32_t j = 0; j < n; ++j) cls[j] = uop_class(ops[j]);
+    // height: instructions from a micro-op to the end of the longest chain
+    // of dependences through it (an overwrite after a read may share an
+    // instruction)
+    std::vector<uint32_t> height(n, 1);
+    for (uint32_t j = n; j-- > 0;) {
+        uint32_t h = 1;
+        for (uint32_t s : hard_succ[j]) h = std::max(h, height[s] + 1);
+        for (uint32_t s : soft_succ[j]) h = std::max(h, height[s]);
+        height[j] = h;
+    }
     std::vector<uint8_t> done(n, 0);
     std::vector<std::vector<uint32_t>> out;
-    std::vector<std::pair<uint64_t, uint32_t>> counts;   // (class, ready micro-ops)
     uint32_t front = 0;
     while (front < n) {
         const uint32_t end = std::min<uint32_t>(n, front + kPackWindow);
-        // the class with the most ready micro-ops (ties: the earliest)
-        counts.clear();
+        // list scheduling by height: the class of the ready micro-op with
+        // the greatest height (ties: the earliest), filled with the ready
+        // micro-ops of that class in order of height; an overwrite whose
+        // readers were just taken may join
+        uint64_t best = 0;
+        uint32_t hb = 0;
         for (uint32_t j = front; j < end; ++j) {
             if (done[j] || hard_cnt[j] || soft_cnt[j]) continue;
-            bool found = false;
-            for (auto &cc : counts)
-                if (cc.first == cls[j]) {
-                    cc.second++;
-                    found = true;
-                    break;
-                }
-            if (!found) counts.push_back({cls[j], 1});
-        }
-        uint64_t best = counts[0].first;
-        uint32_t best_n = counts[0].second;
-        for (const auto &cc : counts)
-            if (std::min(cc.second, S) > std::min(best_n, S)) {
-                best = cc.first;
-                best_n = cc.second;
+            if (height[j] > hb) {
+                hb = height[j];
+                best = cls[j];
             }
+        }
         std::vector<uint32_t> cur;
-        for (uint32_t j = front; j < end && cur.size() < S; ++j) {
-            if (done[j] || cls[j] != best || hard_cnt[j] || soft_cnt[j]) continue;
-            done[j] = 1;
-            cur.push_back(j);
-            for (uint32_t s : soft_succ[j]) soft_cnt[s]--;   // may join this instruction
+        while (cur.size() < S) {
+            uint32_t pick = n;
+            for (uint32_t j = front; j < end; ++j) {
+                if (done[j] || cls[j] != best || hard_cnt[j] || soft_cnt[j]) continue;
+                if (pick == n || height[j] > height[pick]) pick = j;
+            }
+            if (pick == n) break;
+            done[pick] = 1;
+            cur.push_back(pick);
+            for (uint32_t s : soft_succ[pick]) soft_cnt[s]--;
         }
         for (uint32_t j : cur)
             for (uint32_t s : hard_succ[j]) hard_cnt[s]--;
