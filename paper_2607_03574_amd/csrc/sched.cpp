@@ -48,12 +48,27 @@ struct Info {
     std::vector<uint32_t> rep;
     std::vector<uint8_t> vlive;      // representative whose value is needed
     std::vector<uint32_t> last_use;  // last forward reader of a value, or N for the loss
+    // Multiply-add fusion: fmul[c] = 1 + m when the product m is folded into
+    // the sum or difference c (c reads m's operands instead of m), else 0.
+    // m's value is then never formed: its only reader is c and no adjoint
+    // rule reads it.  x*y + z rounds the product and then the sum, so c
+    // keeps the bits of the two separate operations.
+    std::vector<uint32_t> fmul;
 
     explicit Info(const Tape &tape) : t(tape), N(uint32_t(tape.ops.size())), P(tape.n_params) {}
 
-    // operand values of op k (as representatives)
+    // operand values of op k (as representatives; a fused sum reads the
+    // product's operands, then its other operand)
     template <class F>
     void for_operands(uint32_t k, F f) const {
+        if (!fmul.empty() && fmul[k]) {
+            const uint32_t m = fmul[k] - 1;
+            const TapeOp &o = t.ops[k];
+            f(rep[t.ops[m].a]);
+            f(rep[t.ops[m].b]);
+            f(rep[rep[o.a] == m ? o.b : o.a]);
+            return;
+        }
         for_operands_raw(k, [&](uint32_t s) { f(rep[s]); });
     }
     // operand slots of op k as written in the tape
@@ -122,6 +137,33 @@ struct Info {
         }
     }
 
+    // Fold a product into the sum or difference that is its only reader,
+    // elementwise ops of one shape only (no broadcast operand).
+    void fuse_products() {
+        std::vector<uint32_t> readers(N, 0);
+        std::vector<uint8_t> rule_reads(N, 0);
+        for (uint32_t k = 0; k < N; ++k)
+            if (vlive[k] && rep[k] == k) for_operands(k, [&](uint32_t s) { readers[s]++; });
+        readers[rep[t.loss]]++;
+        for (uint32_t k = 0; k < N; ++k)
+            if (need_rev[k]) for_revreads(k, [&](uint32_t s) { rule_reads[s] = 1; });
+        fmul.assign(N, 0);
+        for (uint32_t c = 0; c < N; ++c) {
+            const TapeOp &o = t.ops[c];
+            if (!vlive[c] || rep[c] != c || kind[c] != K_COMP || (o.code != tp::ADD && o.code != tp::SUB)) continue;
+            for (uint32_t side = 0; side < 2; ++side) {
+                const uint32_t m = rep[side == 0 ? o.a : o.b], other = rep[side == 0 ? o.b : o.a];
+                if (kind[m] != K_COMP || t.ops[m].code != tp::MUL || rep[m] != m || !vlive[m]) continue;
+                if (readers[m] != 1 || rule_reads[m] || m == rep[t.loss] || m == other) continue;
+                const uint32_t n = nel[c];
+                if (nel[m] != n || nel[other] != n || nel[t.ops[m].a] != n || nel[t.ops[m].b] != n) continue;
+                fmul[c] = m + 1;
+                vlive[m] = 0;
+                break;
+            }
+        }
+    }
+
     void number_values() {
         rep.assign(N, 0);
         std::map<std::vector<uint32_t>, uint32_t> first;
@@ -176,6 +218,7 @@ struct Info {
             if (need_rev[k]) for_revreads(k, [&](uint32_t s) { vlive[s] = 1; });
             if (vlive[k] && rep[k] == k) for_operands(k, [&](uint32_t s) { vlive[s] = 1; });
         }
+        fuse_products();
         last_use.assign(N, 0);
         for (uint32_t k = 0; k < N; ++k)
             if (vlive[k] && rep[k] == k) for_operands(k, [&](uint32_t s) { last_use[s] = k; });
@@ -601,7 +644,7 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
     const uint32_t a = u.f[0], x = u.f[1], y = u.f[2], z = u.f[3];
     const bool acc_base = !(u.flags & kUFirst);   // adjoint forms read their target
     switch (f) {
-    case MAC: case SELP: case GATEGT:
+    case MAC: case SELP: case GATEGT: case MSUB: case RSUB:
         rd = {x, y, z};
         wr = {a};
         break;
@@ -776,6 +819,7 @@ std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S)
         height[j] = h;
     }
     std::vector<uint8_t> done(n, 0);
+    if (getenv("NDVM_HEIGHT")) fprintf(stderr, "pack: %u micro-ops, critical path %u\n", n, n ? *std::max_element(height.begin(), height.end()) : 0);
     std::vector<std::vector<uint32_t>> out;
     uint32_t front = 0;
     while (front < n) {
@@ -942,6 +986,14 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             E.put(LDOBS, dst, 0, o.imm);
             return;
         case tp::ADD: case tp::SUB: case tp::MUL: case tp::DIV: {
+            if (I.fmul[k]) {   // product folded in: x*y + z, x*y - z or z - x*y
+                const uint32_t mm = I.fmul[k] - 1;
+                const bool m_first = I.rep[o.a] == mm;
+                const uint32_t X = operand(t.ops[mm].a), Y = operand(t.ops[mm].b), Z = operand(m_first ? o.b : o.a);
+                const uint32_t f = o.code == tp::ADD ? MAC : m_first ? MSUB : RSUB;
+                for (uint32_t i = 0; i < n; ++i) E.put(f, dst + i, 0, X + i, Y + i, Z + i);
+                return;
+            }
             const uint32_t A = operand(o.a), Bv = operand(o.b);
             const bool as = I.nel[o.a] == 1 && n > 1, bs = I.nel[o.b] == 1 && n > 1;
             for (uint32_t i = 0; i < n; ++i) {

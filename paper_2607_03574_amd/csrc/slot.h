@@ -69,6 +69,8 @@ enum Form : uint32_t {
     LDCONST,   // d = consts[x]
     CKST,      // ckpt rows x .. x + n - 1 of this lane = registers a .. a + n - 1  (imm = n)
     CKLD,      // registers a .. a + n - 1 = ckpt rows x .. x + n - 1 of this lane
+    MSUB,      // d = x * y - z  (product rounded, then difference rounded)
+    RSUB,      // d = z - x * y  (product rounded, then difference rounded)
     HOT_END,
     // ---- cold forms: sine and cosine (their library code branches per
     // lane), pow, and the loss and gradient stores (masked per slot)

@@ -220,6 +220,16 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
     case DIV:
         c.st(p.a(), c.ld(p.x()) / c.ld(p.y()));
         return;
+    case MSUB: {
+        const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+        c.st(p.a(), x * y - z);
+        return;
+    }
+    case RSUB: {
+        const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+        c.st(p.a(), z - x * y);
+        return;
+    }
     case ACCD: {
         const auto a = p.a();
         const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());

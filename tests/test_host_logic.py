@@ -206,7 +206,7 @@ def test_emulated_wide_program_beyond_packed_register_fields(oracle_mod):
 
 
 # form numbers of the device program format (slot.h)
-HOT_FORMS = set(range(1, 30))
+HOT_FORMS = set(range(1, 32))
 COLD_FORMS = {40, 41, 42, 43}
 END = 63
 INDEX_X = {25, 26, 27, 28, 29, 43}      # LDOBS LDPARAM LDCONST CKST CKLD STGRAD
@@ -232,7 +232,7 @@ def test_device_program_encoding(name, kw):
     for k in range(n - 1):
         f = int(forms[k])
         regs = words[k, :, 0:1] if f in INDEX_X else words[k, :, [0, 2, 3]].T
-        if f in (1, 2, 3, 4, 5, 6):       # every field of these forms names a register
+        if f in (1, 2, 3, 4, 5, 6, 30, 31):   # every field of these forms names a register
             regs = words[k]
         assert (regs % stride == 0).all(), (k, f)
         assert (regs // stride < st["n_regs"] + 8).all(), (k, f)
