@@ -34,7 +34,6 @@ struct P4 {
     uint32_t ix() const { return w[1]; }
     uint32_t imm() const { return hdr >> slot::kImmShift; }
     bool first() const { return (hdr >> (slot::kFirstShift + slot)) & 1u; }
-    bool gated() const { return (hdr >> (slot::kGatedShift + slot)) & 1u; }
 };
 
 struct HostCtx {

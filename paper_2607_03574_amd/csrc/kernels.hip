@@ -116,7 +116,6 @@ struct ChunkPayload {
     __device__ __forceinline__ uint32_t ix() const { return row_word<4 * P + 1>(ch); }
     __device__ __forceinline__ uint32_t imm() const { return hdr >> slot::kImmShift; }
     __device__ __forceinline__ bool first() const { return (hdr >> (slot::kFirstShift + slot)) & 1u; }
-    __device__ __forceinline__ bool gated() const { return (hdr >> (slot::kGatedShift + slot)) & 1u; }
 };
 // Payload of a cold instruction, words read out
 struct Payload {
@@ -128,7 +127,6 @@ struct Payload {
     __device__ __forceinline__ uint32_t ix() const { return w[1]; }
     __device__ __forceinline__ uint32_t imm() const { return hdr >> slot::kImmShift; }
     __device__ __forceinline__ bool first() const { return (hdr >> (slot::kFirstShift + slot)) & 1u; }
-    __device__ __forceinline__ bool gated() const { return (hdr >> (slot::kGatedShift + slot)) & 1u; }
 };
 
 // Cold micro-ops run out of line: their library code branches per lane, and

@@ -624,9 +624,9 @@ std::vector<AI> bundle_reverse(const Info &I, const std::vector<AI> &in) {
 }
 
 // ------------------------------------------------------------------ micro-ops
-// One slot's micro-op before packing: form, flags (kUFirst, kUGated), the
+// One slot's micro-op before packing: form, flags (kUFirst), the
 // immediate, and fields a, x, y, z as register numbers or indices.
-constexpr uint32_t kUFirst = 1, kUGated = 2;
+constexpr uint32_t kUFirst = 1;
 struct UOp {
     uint32_t form, flags, imm;
     uint32_t f[4];
@@ -1257,7 +1257,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             auto acc = [&](uint32_t tr, uint32_t fl, uint32_t x, uint32_t y) {
                 if (tr == kNone) return;
                 if (gate == x)
-                    E.put(ACC, tr, fl | kUGated, x, y);
+                    E.put(ACC, tr, fl, x, y);
                 else
                     E.put(MACG, tr, fl, x, y, gate);
             };
@@ -1529,7 +1529,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             case I_SEED: {
                 uint32_t fl;
                 const uint32_t tr = target(a.k, &fl);
-                if (tr != kNone) E.put(ACC, tr, fl, kOne, kOne);
+                if (tr != kNone) E.put(ACC, tr, fl, kOne, kOne);   // 1 * 1 (its gate, x = 1, is open)
                 break;
             }
             case I_CKLD: {
@@ -1612,7 +1612,6 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                 u.flags = 0;
             }
             hdr |= (u.flags & kUFirst ? 1u : 0u) << (kFirstShift + sl);
-            hdr |= (u.flags & kUGated ? 1u : 0u) << (kGatedShift + sl);
             const uint32_t w[4] = {field(uint64_t(u.f[0]) * reg_bytes),
                                    x_is_index(f) ? u.f[1] : field(uint64_t(u.f[1]) * reg_bytes),
                                    field(uint64_t(u.f[2]) * reg_bytes), field(uint64_t(u.f[3]) * reg_bytes)};

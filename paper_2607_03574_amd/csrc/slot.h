@@ -16,8 +16,7 @@
 //
 // Per instruction: a header word, the same for every slot:
 //   bits 0-5 form, bits 6-9 kFirst of slots 0-3 (first contribution to the
-//   target: store, do not add), bits 10-13 kGated of slots 0-3 (the
-//   contribution is skipped when operand x is zero), bits 14-31 the form's
+//   target: store, do not add), bits 10-13 zero, bits 14-31 the form's
 //   immediate;
 // and per slot four words a, x, y, z: a register named in a field is held as
 // its byte offset in a lane's register file (register * 8 * 64/S), an index
@@ -39,7 +38,7 @@ enum Form : uint32_t {
     // products, negations and copies are this form against the constants
     // 1, -1, -0, with the bits of the plain operation.
     MAC = 1,
-    ACC,       // t = (!kGated || x != 0) ? base + x * y : base: the linear adjoint rule t += g * y
+    ACC,       // t = x != 0 ? base + x * y : base: the linear adjoint rule t += g * y, gated on g
     MACG,      // t = gate(z) ? base + x * y : base          (explicit gate register z)
     DIV,       // d = x / y
     ACCD,      // t = gate(z) ? base + x / y : base
@@ -84,7 +83,7 @@ enum Form : uint32_t {
 enum Unary : uint32_t { U_SIN = 0, U_COS };
 
 constexpr uint32_t kFormMask = 63u;
-constexpr uint32_t kFirstShift = 6, kGatedShift = 10, kImmShift = 14;
+constexpr uint32_t kFirstShift = 6, kImmShift = 14;
 constexpr uint32_t kMaxImm = (1u << 18) - 1;
 constexpr uint32_t kMaxBlock = 4;            // outputs of a block form (sink and trash rows reserved)
 

@@ -14,7 +14,7 @@
 //   uint32_t slot() const;
 // and W is the payload of this slot's micro-op: register handles a(), x(),
 // y(), z(), the raw field ix() (an index), the uniform immediate imm() and
-// this slot's flags first() and gated().
+// this slot's first-contribution flag first().
 //
 // Adjoint rules follow Appendix C, table tab:adjoints: contractions are fma
 // chains over the summation index in ascending order with a plain product as
@@ -195,8 +195,7 @@ NDVM_HD void exec_acc(const C &c, const W &p) {
     const auto a = p.a();
     const double x = c.ld(p.x()), y = c.ld(p.y());
     const double base = base_of(c, a, p.first());
-    const bool on = (!p.gated()) | (x != 0.0);
-    c.st(a, on ? base + x * y : base);
+    c.st(a, x != 0.0 ? base + x * y : base);
 }
 
 // Hot micro-ops (forms below HOT_END): straight-line code, no per-lane
