@@ -11,6 +11,12 @@ the timed region.
 Prints one JSON line with the metric, a roofline object for the replay
 kernel (its average duration measured with HIP events on the launch stream)
 and the CPU oracle timed on a bounded sample of the same workload.
+
+    python bench.py --calibrate N [--workload NAME] [--steps K]
+
+instead measures calibrations per second: every lane of the workload is one
+N-step Adam fit (ndvm_grad + ndvm_adam_step per step, tape uploaded once), as
+in the paper's Kalman maximum-likelihood fit (default workload kalman_cv4).
 """
 import argparse
 import hashlib
@@ -168,17 +174,91 @@ def cpu_baseline(w, progs, budget_s=10.0):
                        f"program(s) of {w.name}, {passes} pass(es)), {dt:.1f} s wall")
 
 
+def calibration_bench(args):
+    """Calibrations per second: all L lanes fitted at once with args.calibrate
+    Adam steps each; a timed step is one whole fit of the population."""
+    import torch
+    import paper_2607_03574_amd as nd
+    from paper_2607_03574_amd import torch_api
+    name = args.workload if args.workload_given else "kalman_cv4"
+    w = configs.build(name)
+    if name == "random_programs":
+        raise SystemExit("the calibration benchmark takes a single-program workload")
+    n_steps, lr = args.calibrate, 1e-6
+    device = torch.device("cuda:0")
+    stream = torch.cuda.Stream(device=device)
+    with torch.cuda.stream(stream):
+        tape_b = nd.tape_build(w.bytecode)
+        tape = nd.tape_upload(tape_b)
+        obs = torch.tensor(w.obs, device=device)
+        p0 = torch.tensor(w.params, device=device)
+        L = p0.shape[0]
+        ws = torch.empty(max(nd.workspace_bytes(tape, L, True), 8), dtype=torch.uint8, device=device)
+        p = p0.clone()
+    torch.cuda.synchronize()
+
+    def fit():
+        p.copy_(p0)
+        return torch_api.calibrate(tape, p, obs, n_steps, lr, workspace=ws, stream=stream)
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            fit()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        for _ in range(args.steps):
+            hist = fit()
+        ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / args.steps
+    gpu_s = ev0.elapsed_time(ev1) / 1e3 / args.steps
+    flops = tape_flops(tape_b) * L * n_steps
+    improved = float((hist[-1] < hist[0]).double().mean().item())
+    out = {
+        "metric": f"calibrations/sec ({n_steps}-step Adam fits, one per lane) on 1 MI355X",
+        "value": L / wall, "unit": "calibrations/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": wall * 1e3, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64", "data": "synthetic",
+        "config": {"workload": w.name, "lanes": L, "adam_steps": n_steps, "lr": lr,
+                   "lanes_improved": improved},
+        "roofline": {"bound": "alu", "achieved": flops / gpu_s / 1e12, "peak": PEAK_FP64 / 1e12,
+                     "unit": "TFLOP/s", "frac": flops / gpu_s / PEAK_FP64, "traffic": None,
+                     "kernel": "ndvm_replay + ndvm_adam", "kernel_ms": gpu_s * 1e3},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import adam
+        lanes = 32
+        t0 = time.perf_counter()
+        done = 0
+        while time.perf_counter() - t0 < 10.0:
+            adam.calibrate(w.bytecode, w.params[:lanes], w.obs, n_steps, lr, threads=16)
+            done += lanes
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = dict(value=done / dt, unit="calibrations/s", cores=min(os.cpu_count() or 1, 16),
+                                   kind="oracle",
+                                   sample=f"{done} calibrations ({n_steps} Adam steps each) of the first "
+                                          f"{lanes} lanes of {w.name}, {dt:.1f} s wall")
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=configs.ORDER)
+    ap.add_argument("--workload", default=None, choices=configs.ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run a plain device-to-device copy of this many "
                          "MiB (reference for the FETCH_SIZE / WRITE_SIZE counter scale)")
+    ap.add_argument("--calibrate", type=int, default=0, metavar="N",
+                    help="measure calibrations/s: every lane is one N-step Adam fit")
     args = ap.parse_args()
+    args.workload_given = args.workload is not None
+    if args.workload is None:
+        args.workload = DEFAULT_WORKLOAD
     if args.copy_calibration:
         import torch
         n = args.copy_calibration * (1 << 20) // 8
@@ -193,6 +273,8 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
                           "(the path shards by lanes or programs, see the design notes)"}))
         sys.exit(2)
+    if args.calibrate:
+        return calibration_bench(args)
     import torch
     device = torch.device("cuda:0")
     stream = torch.cuda.Stream(device=device)

@@ -16,9 +16,11 @@
  * Here the structural walk happens once per program on the host
  * (ndvm_tape_build) and yields a lane-invariant tape in which numeric
  * branches are per-lane selects.  ndvm_tape_upload schedules the tape for the
- * GPU; ndvm_forward / ndvm_grad replay it on the device for L lanes, one lane
- * per GPU thread, and ndvm_grad_many does so for many programs in a single
- * launch.
+ * GPU; ndvm_forward / ndvm_grad replay it on the device for L lanes (16
+ * lanes per wave, each lane's independent operations spread over 4 threads),
+ * and ndvm_grad_many does so for many programs in a single launch.
+ * ndvm_adam_step is the optimiser step of a calibration loop driven by
+ * ndvm_grad.
  *
  * Conventions for every entry point:
  *  - All functions return ndvm_status; on a non-OK status a message is
@@ -170,6 +172,28 @@ void ndvm_free(void *p);
 
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char *ndvm_last_error(void);
+
+/*
+ * One Adam step for a population of parameter vectors (calibration: an
+ * optimiser fits every lane's parameters with the exact gradients of
+ * ndvm_grad, as in the paper's Kalman maximum-likelihood fit, Section "From
+ * buckets to phases").  Adam with bias correction (Kingma and Ba, 2015):
+ *   m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g*g;
+ *   p = p - lr * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ * evaluated in that order in fp64; beta1^t and beta2^t are computed on the
+ * host with pow.
+ *   params : device fp64, element (l, k) at params[l*ld_p + k], updated in place
+ *   grad   : device fp64, element (l, k) at grad[l*ld_g + k] (ndvm_grad's output)
+ *   m, v   : device fp64 moment buffers, [L, P] contiguous, zero before step t = 1;
+ *            owned by the caller, updated in place
+ *   t      : step number, >= 1
+ * Errors (synchronous): NDVM_E_ARG for a null buffer with L*P > 0, L < 0, P < 0,
+ * ld_p < P, ld_g < P, t < 1, or beta1, beta2 outside [0, 1); NDVM_E_DEVICE for a
+ * launch failure.
+ */
+ndvm_status ndvm_adam_step(double *params, const double *grad, double *m, double *v, int64_t L, int64_t P,
+                           int64_t ld_p, int64_t ld_g, int64_t t, double lr, double beta1, double beta2,
+                           double eps, void *stream);
 
 #ifdef __cplusplus
 }

@@ -23,7 +23,7 @@ POLICY_RECOMPUTE = 2
 # exported symbols of include/ndvm.h
 EXPORTS = ["ndvm_tape_build", "ndvm_tape_upload", "ndvm_tape_info_get", "ndvm_workspace_bytes",
            "ndvm_forward", "ndvm_grad", "ndvm_grad_many", "ndvm_workspace_bytes_many",
-           "ndvm_tape_free", "ndvm_free", "ndvm_last_error"]
+           "ndvm_tape_free", "ndvm_free", "ndvm_last_error", "ndvm_adam_step"]
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_03574_amd/build.py "
@@ -58,6 +58,9 @@ _grad_many = _sig("ndvm_grad_many", _int, [ctypes.POINTER(_vp), _int, _vp, _i64,
 _tape_free = _sig("ndvm_tape_free", None, [_vp])
 _free = _sig("ndvm_free", None, [_vp])
 _last_error = _sig("ndvm_last_error", ctypes.c_char_p, [])
+_f64 = ctypes.c_double
+_adam = _sig("ndvm_adam_step", _int, [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _f64, _f64, _f64, _f64,
+                                      _vp])
 
 
 class NdvmError(RuntimeError):
@@ -210,3 +213,21 @@ def grad_many(tapes: Sequence[Tape], params, obs, loss=None, grad_out=None, work
                       obs.numel(), loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(1),
                       grad_out.stride(0), ws.data_ptr(), nbytes, _stream_ptr(stream)), "ndvm_grad_many")
     return loss, grad_out
+
+
+def adam_step(params, grad_in, m, v, t: int, lr: float, beta1: float = 0.9, beta2: float = 0.999,
+              eps: float = 1e-8, stream=None):
+    """One Adam step for params[L, P] in place (ndvm_adam_step); m and v are
+    [L, P] contiguous moment buffers, zero before step t = 1."""
+    for name, x in (("params", params), ("grad", grad_in), ("m", m), ("v", v)):
+        _dev_f64(x, name)
+    if params.dim() != 2 or params.stride(1) != 1 or grad_in.stride(1) != 1:
+        raise ValueError("params and grad must be [L, P] with unit inner stride")
+    L, P = params.shape
+    if tuple(grad_in.shape) != (L, P) or tuple(m.shape) != (L, P) or tuple(v.shape) != (L, P) \
+            or not m.is_contiguous() or not v.is_contiguous():
+        raise ValueError("grad, m and v must match params [L, P]; m and v contiguous")
+    _check(_adam(params.data_ptr(), grad_in.data_ptr(), m.data_ptr(), v.data_ptr(), L, P, params.stride(0),
+                 grad_in.stride(0), int(t), float(lr), float(beta1), float(beta2), float(eps),
+                 _stream_ptr(stream)), "ndvm_adam_step")
+    return params

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <map>
@@ -20,6 +21,14 @@ namespace ndvm {
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
                          uint32_t r_lds, int variant, uint32_t slots, hipStream_t stream);
 bool slots_supported(uint32_t S);
+struct AdamArgs {
+    double *p;
+    const double *g;
+    double *m, *v;
+    int64_t L, P, ld_p, ld_g;
+    double lr, b1, b2, eps, c1, c2;
+};
+hipError_t launch_adam(const AdamArgs &a, hipStream_t stream);
 }
 
 using namespace ndvm;
@@ -247,6 +256,31 @@ ndvm_status guarded(F f) {
 extern "C" {
 
 const char *ndvm_last_error(void) { return get_error(); }
+
+ndvm_status ndvm_adam_step(double *params, const double *grad, double *m, double *v, int64_t L, int64_t P,
+                           int64_t ld_p, int64_t ld_g, int64_t t, double lr, double beta1, double beta2,
+                           double eps, void *stream) {
+    return guarded([&]() -> ndvm_status {
+        if (L < 0 || P < 0 || ld_p < P || ld_g < P || t < 1 || !(beta1 >= 0.0 && beta1 < 1.0) ||
+            !(beta2 >= 0.0 && beta2 < 1.0)) {
+            set_error("ndvm_adam_step: bad size, stride, step or beta");
+            return NDVM_E_ARG;
+        }
+        if (L * P == 0) return NDVM_OK;
+        if (!params || !grad || !m || !v) {
+            set_error("ndvm_adam_step: null buffer");
+            return NDVM_E_ARG;
+        }
+        const AdamArgs a{params, grad, m, v, L, P, ld_p, ld_g, lr, beta1, beta2, eps,
+                         1.0 - std::pow(beta1, double(t)), 1.0 - std::pow(beta2, double(t))};
+        const hipError_t e = launch_adam(a, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) {
+            set_error(std::string("ndvm_adam_step: launch failed: ") + hipGetErrorString(e));
+            return NDVM_E_DEVICE;
+        }
+        return NDVM_OK;
+    });
+}
 
 void ndvm_free(void *p) { std::free(p); }
 
