@@ -5,7 +5,7 @@ configuration bench.py times) compare sampled lanes the oracle computes one by
 one, including the first, the last and the ragged tail.  Also: ragged lane
 counts, L = 0, poison-lane isolation, bitwise determinism, forward == the
 loss of the gradient call, many programs in one launch == one at a time, and
-every primitive.
+every primitive, products folded into sums (bit for bit).
 """
 import numpy as np
 import pytest
@@ -257,3 +257,18 @@ def test_wide_program_spills_and_unbundles(nd, oracle_mod):
     want[:, :-1] += params[:, 1:]
     want[:, 1:] += params[:, :-1]
     np.testing.assert_array_equal(gg, want)
+
+
+def test_product_folding_bit_exact(nd, oracle_mod):
+    """Products folded into sums and differences keep the bits of the two
+    separate operations (signed zeros included)."""
+    from fusion_cases import fusion_programs
+    rng = np.random.default_rng(21)
+    for bc, P, _ in fusion_programs():
+        params = rng.uniform(-2, 2, (70, P))
+        params[0, :] = 0.0
+        params[1, :] = -0.0
+        gl, gg = run_gpu(nd, bc, params, [])
+        ol, og, _ = oracle_mod.run(bc, params, [])
+        np.testing.assert_array_equal(gl, ol)
+        np.testing.assert_array_equal(gg, og)

@@ -20,6 +20,7 @@ import numpy as np
 import pytest
 
 import emu
+from fusion_cases import fusion_programs
 from conftest import ROOT, lane_rel_err, rel_err
 from oracle import tape_ref
 from workloads import bytecode as B
@@ -251,3 +252,20 @@ def test_bench_traffic_only_for_matching_kernel_sources(tmp_path, monkeypatch):
     assert bench.profiled_traffic("logistic_euler") == 12345.0
     assert bench.profiled_traffic("kalman_cv4") is None      # counters of another kernel build
     assert bench.profiled_traffic("exp_decay") is None       # no summary
+
+
+def test_emulated_product_folding_is_bit_exact(oracle_mod):
+    rng = np.random.default_rng(21)
+    for bc, P, must in fusion_programs():
+        params = rng.uniform(-2, 2, (6, P))
+        params[0, :] = 0.0                      # signed zeros: +0 * +0 - +0
+        params[1, :] = -0.0
+        lo, go, _ = oracle_mod.run(bc, params, [])
+        tape = nd.tape_build(bc)
+        for budget in (320, 8):
+            le, ge, _ = emu.run(tape, params, [], True, budget)
+            np.testing.assert_array_equal(le, lo)
+            np.testing.assert_array_equal(ge, go)
+        headers, _ = emu.program(tape, True, 320)
+        forms = set((headers & 63).tolist())
+        assert must <= forms, (must, forms)
