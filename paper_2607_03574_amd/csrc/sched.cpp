@@ -648,9 +648,8 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
         rd = {x, y, z};
         wr = {a};
         break;
-    case ACC:
-        rd = {x, y};
-        if (acc_base) rd.push_back(a);
+    case ACC:   // base in z: the target itself, or +0 for a first contribution
+        rd = {x, y, z};
         wr = {a};
         break;
     case MACG: case ACCD: case ACCND: case ACCSEL: case ACCABS:
@@ -890,11 +889,11 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
     const uint32_t N = I.N, P = I.P;
     // static registers: param values, param adjoints, sinks for results of
     // unused slots, the constant pool, residents.  The pool holds the tape's
-    // constants, then 1, -1, -0, 2 and the clamp threshold 1e-8.
-    const uint32_t nt = uint32_t(t.consts.size()), nc = nt + 5;
+    // constants, then 1, -1, -0, 2, the clamp threshold 1e-8 and +0.
+    const uint32_t nt = uint32_t(t.consts.size()), nc = nt + 6;
     const uint32_t kSink = 2 * P, kConst0 = 2 * P + kMaxBlock;
     const uint32_t kOne = kConst0 + nt, kMinusOne = kOne + 1, kNegZero = kOne + 2, kTwo = kOne + 3,
-                   kEps = kOne + 4;
+                   kEps = kOne + 4, kZeroC = kOne + 5;
     const uint32_t kStatic = kConst0 + nc + B.res_elems;
     // registers the value allocation may spread over: the budget less the
     // static registers and the temporaries
@@ -905,7 +904,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
     Sch.n_segments = with_grad ? m : 1;
     Sch.static_regs = kStatic;
     Sch.consts = t.consts;
-    for (double v : {1.0, -1.0, -0.0, 2.0, 1e-8}) Sch.consts.push_back(v);
+    for (double v : {1.0, -1.0, -0.0, 2.0, 1e-8, 0.0}) Sch.consts.push_back(v);
 
     // ---- forward phase: abstract instructions + value intervals
     std::vector<AI> fa;
@@ -1257,7 +1256,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             auto acc = [&](uint32_t tr, uint32_t fl, uint32_t x, uint32_t y) {
                 if (tr == kNone) return;
                 if (gate == x)
-                    E.put(ACC, tr, fl, x, y);
+                    E.put(ACC, tr, 0, x, y, (fl & kUFirst) ? kZeroC : tr);
                 else
                     E.put(MACG, tr, fl, x, y, gate);
             };
@@ -1529,7 +1528,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             case I_SEED: {
                 uint32_t fl;
                 const uint32_t tr = target(a.k, &fl);
-                if (tr != kNone) E.put(ACC, tr, fl, kOne, kOne);   // 1 * 1 (its gate, x = 1, is open)
+                if (tr != kNone) E.put(ACC, tr, 0, kOne, kOne, (fl & kUFirst) ? kZeroC : tr);   // 1 * 1, gate open
                 break;
             }
             case I_CKLD: {

@@ -9,7 +9,7 @@ namespace ndvm {
 
 struct Schedule {
     std::vector<uint32_t> code;   // slot words, chunk-major ([chunk][row][instr][4]), then headers (slot.h)
-    std::vector<double> consts;   // constant pool: the tape's, then 1, -1, -0, 2, 1e-8
+    std::vector<double> consts;   // constant pool: the tape's, then 1, -1, -0, 2, 1e-8, +0
     uint32_t slots = 1;           // micro-ops per instruction (threads per lane)
     uint32_t n_regs = 0;          // lane registers used
     uint32_t n_ckpt_rows = 0;     // checkpoint rows (fp64 per lane); slot::kMaxBlock trash rows follow

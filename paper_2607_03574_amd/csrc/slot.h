@@ -38,7 +38,8 @@ enum Form : uint32_t {
     // products, negations and copies are this form against the constants
     // 1, -1, -0, with the bits of the plain operation.
     MAC = 1,
-    ACC,       // t = x != 0 ? base + x * y : base: the linear adjoint rule t += g * y, gated on g
+    ACC,       // d = x != 0 ? z + x * y : z: the linear adjoint rule t += g * y gated on g, with
+               // z = t, or z = a register holding +0 for the first contribution (d = t)
     MACG,      // t = gate(z) ? base + x * y : base          (explicit gate register z)
     DIV,       // d = x / y
     ACCD,      // t = gate(z) ? base + x / y : base

@@ -192,10 +192,8 @@ NDVM_HD void exec_mac(const C &c, const W &p) {
 }
 template <class C, class W>
 NDVM_HD void exec_acc(const C &c, const W &p) {
-    const auto a = p.a();
-    const double x = c.ld(p.x()), y = c.ld(p.y());
-    const double base = base_of(c, a, p.first());
-    c.st(a, x != 0.0 ? base + x * y : base);
+    const double x = c.ld(p.x()), y = c.ld(p.y()), base = c.ld(p.z());
+    c.st(p.a(), x != 0.0 ? base + x * y : base);
 }
 
 // Hot micro-ops (forms below HOT_END): straight-line code, no per-lane
