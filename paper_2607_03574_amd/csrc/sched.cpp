@@ -818,7 +818,6 @@ std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S)
         height[j] = h;
     }
     std::vector<uint8_t> done(n, 0);
-    if (getenv("NDVM_HEIGHT")) fprintf(stderr, "pack: %u micro-ops, critical path %u\n", n, n ? *std::max_element(height.begin(), height.end()) : 0);
     std::vector<std::vector<uint32_t>> out;
     uint32_t front = 0;
     while (front < n) {
@@ -883,7 +882,7 @@ constexpr uint32_t kTemps = 24;
 // Build the forward phase (shared by both programs) and, for the gradient
 // program, the reverse phase; returns the slot program with registers
 // assigned and micro-ops packed S to an instruction.
-Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t reg_budget) {
+Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t reg_budget, uint32_t n_temps) {
     using namespace slot;
     const Tape &t = I.t;
     const uint32_t N = I.N, P = I.P;
@@ -897,7 +896,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
     const uint32_t kStatic = kConst0 + nc + B.res_elems;
     // registers the value allocation may spread over: the budget less the
     // static registers and the temporaries
-    const uint32_t pool = reg_budget > kStatic + kTemps ? reg_budget - kStatic - kTemps : 1;
+    const uint32_t pool = reg_budget > kStatic + n_temps ? reg_budget - kStatic - n_temps : 1;
     const uint32_t m = uint32_t(B.cuts.size());
     Schedule Sch;
     Sch.slots = S;
@@ -973,7 +972,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
 
     UEmit E;
     E.tmp0 = kStatic + fhwm;   // forward temporaries above the forward registers
-    E.n_tmp = kTemps;
+    E.n_tmp = n_temps;
     auto mov = [&](uint32_t d, uint32_t x) { E.put(MAC, d, 0, x, kOne, kNegZero); };
 
     // forward computation of op k into dst (registers from `operand`)
@@ -1127,6 +1126,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
     std::vector<UOp> fwd_ops;
     uint32_t rhwm = 0;
     Sch.n_regs = kStatic + fhwm + E.used_tmp;
+    Sch.n_temps_used = E.used_tmp;
     if (with_grad) {
         fwd_ops = std::move(E.ops);
         E.ops.clear();
@@ -1230,7 +1230,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
         auto adjreg = [&](uint32_t s) { return kStatic + riv[adj_of[s]].reg; };
 
         E.tmp0 = kStatic + std::max(fhwm, rhwm);
-        E.n_tmp = kTemps;
+        E.n_tmp = n_temps;
         E.next_tmp = 0;
         E.used_tmp = 0;
 
@@ -1558,6 +1558,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             }
         }
         Sch.n_regs = std::max(Sch.n_regs, E.tmp0 + E.used_tmp);
+        Sch.n_temps_used = std::max(Sch.n_temps_used, E.used_tmp);
     }
 
     // ---- pack and encode: forward and reverse phases separately (the
@@ -1624,6 +1625,17 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
     return Sch;
 }
 
+// Build with kTemps temporaries reserved; a program that uses none is built
+// again with their registers given to the value pool (a wider spread of
+// values means fewer reuses of one register, which would order otherwise
+// independent micro-ops).  Deterministic: the lowering does not depend on
+// the reservation.
+Schedule build_fit(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t reg_budget) {
+    Schedule s = build(I, B, with_grad, S, reg_budget, kTemps);
+    if (s.n_temps_used == 0) s = build(I, B, with_grad, S, reg_budget, 0);
+    return s;
+}
+
 }  // namespace
 
 Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget) {
@@ -1633,7 +1645,7 @@ Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget) {
     B.set_cuts({0});
     B.resident.assign(I.N, 0);
     B.res_off.assign(I.N, 0);
-    return build(I, B, false, slots, reg_budget);
+    return build_fit(I, B, false, slots, reg_budget);
 }
 
 Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
@@ -1652,7 +1664,7 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
         B.choose_residents(kResidentAfter);
         B.set_cuts(B.choose_cuts(S));
         B.plan(true);
-        return build(I, B, true, slots, reg_budget);
+        return build_fit(I, B, true, slots, reg_budget);
     };
     // Largest segment size (in value elements) whose register file fits the
     // budget: halve until it fits, then bisect between the fitting size and

@@ -17,6 +17,7 @@ struct Schedule {
     uint32_t n_chunks = 0;        // fetch chunks of the program, read-ahead chunks included
     uint32_t hdr_off = 0;         // word offset of the headers in code
     uint32_t static_regs = 0, fwd_regs = 0, rev_regs = 0;
+    uint32_t n_temps_used = 0;    // temporaries the lowering used (0: their registers went to the value pool)
     uint64_t n_instr = 0, n_uops = 0, n_slots_used = 0;
     uint64_t n_fwd_ops = 0, n_recompute_ops = 0, n_rev_ops = 0;
     uint64_t ckpt_elems_stored = 0, ckpt_elems_loaded = 0;
