@@ -627,6 +627,9 @@ std::vector<AI> bundle_reverse(const Info &I, const std::vector<AI> &in) {
 // One slot's micro-op before packing: form, flags (kUFirst), the
 // immediate, and fields a, x, y, z as register numbers or indices.
 constexpr uint32_t kUFirst = 1;
+// a MAC whose x is a nonzero constant: the linear adjoint form (gated on x,
+// which is then open) computes the same bits, so it may be packed with them
+constexpr uint32_t kUAltAcc = 2;
 struct UOp {
     uint32_t form, flags, imm;
     uint32_t f[4];
@@ -750,7 +753,7 @@ uint64_t uop_class(const UOp &u) { return uint64_t(u.form) | uint64_t(u.imm) << 
 // program.
 constexpr uint32_t kPackWindow = 160;
 
-std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S) {
+std::vector<std::vector<uint32_t>> pack(std::vector<UOp> &ops, uint32_t S) {
     const uint32_t n = uint32_t(ops.size());
     // successor lists: hard (true / output dependences), soft (overwrite
     // after read)
@@ -805,8 +808,11 @@ std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S)
             }
         }
     }
-    std::vector<uint64_t> cls(n);
-    for (uint32_t j = 0; j < n; ++j) cls[j] = uop_class(ops[j]);
+    std::vector<uint64_t> cls(n), alt(n, ~0ull);
+    for (uint32_t j = 0; j < n; ++j) {
+        cls[j] = uop_class(ops[j]);
+        if (ops[j].flags & kUAltAcc) alt[j] = uop_class(UOp{slot::ACC, 0, 0, {0, 0, 0, 0}});
+    }
     // height: instructions from a micro-op to the end of the longest chain
     // of dependences through it (an overwrite after a read may share an
     // instruction)
@@ -827,24 +833,36 @@ std::vector<std::vector<uint32_t>> pack(const std::vector<UOp> &ops, uint32_t S)
         // micro-ops of that class in order of height; an overwrite whose
         // readers were just taken may join
         uint64_t best = 0;
-        uint32_t hb = 0;
+        uint32_t hb = 0, top = n;
         for (uint32_t j = front; j < end; ++j) {
             if (done[j] || hard_cnt[j] || soft_cnt[j]) continue;
             if (height[j] > hb) {
                 hb = height[j];
                 best = cls[j];
+                top = j;
             }
+        }
+        // a micro-op that may take either form: the one with more ready company
+        if (top < n && alt[top] != ~0ull) {
+            uint32_t c0 = 0, c1 = 0;
+            for (uint32_t j = front; j < end; ++j) {
+                if (done[j] || hard_cnt[j] || soft_cnt[j]) continue;
+                c0 += cls[j] == cls[top] || alt[j] == cls[top];
+                c1 += cls[j] == alt[top] || alt[j] == alt[top];
+            }
+            if (c1 > c0) best = alt[top];
         }
         std::vector<uint32_t> cur;
         while (cur.size() < S) {
             uint32_t pick = n;
             for (uint32_t j = front; j < end; ++j) {
-                if (done[j] || cls[j] != best || hard_cnt[j] || soft_cnt[j]) continue;
+                if (done[j] || (cls[j] != best && alt[j] != best) || hard_cnt[j] || soft_cnt[j]) continue;
                 if (pick == n || height[j] > height[pick]) pick = j;
             }
             if (pick == n) break;
             done[pick] = 1;
             cur.push_back(pick);
+            if (cls[pick] != best) ops[pick].form = slot::ACC;   // the alternative form
             for (uint32_t s : soft_succ[pick]) soft_cnt[s]--;
         }
         for (uint32_t j : cur)
@@ -973,7 +991,21 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
     UEmit E;
     E.tmp0 = kStatic + fhwm;   // forward temporaries above the forward registers
     E.n_tmp = n_temps;
-    auto mov = [&](uint32_t d, uint32_t x) { E.put(MAC, d, 0, x, kOne, kNegZero); };
+    // x*y + z.  When a multiplier is a nonzero constant it goes to x and the
+    // micro-op is marked kUAltAcc: the linear adjoint form computes the same
+    // bits then (its gate, that constant, is open; the product and the sum
+    // commute), so the packer may place it among adjoint rules.
+    auto nz_const = [&](uint32_t s) {
+        s = I.rep[s];
+        return I.kind[s] == K_CONST && t.consts[t.ops[s].imm] != 0.0;
+    };
+    auto put_mac = [&](uint32_t d, uint32_t x, uint32_t y, uint32_t z, bool xc, bool yc) {
+        if (xc || yc)
+            E.put(MAC, d, kUAltAcc, xc ? x : y, xc ? y : x, z);
+        else
+            E.put(MAC, d, 0, x, y, z);
+    };
+    auto mov = [&](uint32_t d, uint32_t x) { put_mac(d, x, kOne, kNegZero, false, true); };
 
     // forward computation of op k into dst (registers from `operand`)
     auto emit_fwd = [&](uint32_t k, auto operand, uint32_t dst) {
@@ -988,7 +1020,12 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                 const uint32_t mm = I.fmul[k] - 1;
                 const bool m_first = I.rep[o.a] == mm;
                 const uint32_t X = operand(t.ops[mm].a), Y = operand(t.ops[mm].b), Z = operand(m_first ? o.b : o.a);
-                const uint32_t f = o.code == tp::ADD ? MAC : m_first ? MSUB : RSUB;
+                if (o.code == tp::ADD) {
+                    const bool xc = nz_const(t.ops[mm].a), yc = nz_const(t.ops[mm].b);
+                    for (uint32_t i = 0; i < n; ++i) put_mac(dst + i, X + i, Y + i, Z + i, xc, yc);
+                    return;
+                }
+                const uint32_t f = m_first ? MSUB : RSUB;
                 for (uint32_t i = 0; i < n; ++i) E.put(f, dst + i, 0, X + i, Y + i, Z + i);
                 return;
             }
@@ -997,9 +1034,9 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             for (uint32_t i = 0; i < n; ++i) {
                 const uint32_t xa = as ? A : A + i, xb = bs ? Bv : Bv + i;
                 switch (o.code) {
-                case tp::ADD: E.put(MAC, dst + i, 0, xa, kOne, xb); break;
-                case tp::SUB: E.put(MAC, dst + i, 0, xb, kMinusOne, xa); break;
-                case tp::MUL: E.put(MAC, dst + i, 0, xa, xb, kNegZero); break;
+                case tp::ADD: put_mac(dst + i, xa, kOne, xb, false, true); break;
+                case tp::SUB: put_mac(dst + i, xb, kMinusOne, xa, false, true); break;
+                case tp::MUL: put_mac(dst + i, xa, xb, kNegZero, nz_const(o.a), nz_const(o.b)); break;
                 default: E.put(DIV, dst + i, 0, xa, xb); break;
                 }
             }
@@ -1007,7 +1044,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
         }
         case tp::NEG: {
             const uint32_t A = operand(o.a);
-            for (uint32_t i = 0; i < n; ++i) E.put(MAC, dst + i, 0, A + i, kMinusOne, kNegZero);
+            for (uint32_t i = 0; i < n; ++i) put_mac(dst + i, A + i, kMinusOne, kNegZero, false, true);
             return;
         }
         case tp::EXP: case tp::LOG: case tp::SQRT: case tp::ABS: {
@@ -1056,7 +1093,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             const uint32_t d = E.tmp(), r = E.tmp(), nr = E.tmp();
             E.put(DET2, d, 0, A);
             E.put(DIV, r, 0, kOne, d);
-            E.put(MAC, nr, 0, r, kMinusOne, kNegZero);
+            put_mac(nr, r, kMinusOne, kNegZero, false, true);
             E.put(MAC, dst + 0, 0, A + 3, r, kNegZero);
             E.put(MAC, dst + 1, 0, A + 1, nr, kNegZero);
             E.put(MAC, dst + 2, 0, A + 2, nr, kNegZero);
@@ -1329,7 +1366,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                     }
                     case tp::SQRT: {
                         const uint32_t tz = E.tmp(), fl = E.tmp();
-                        E.put(MAC, tz, 0, kTwo, v(k) + i, kNegZero);
+                        put_mac(tz, kTwo, v(k) + i, kNegZero, true, false);
                         E.put(GATEGT, fl, 0, v(o.a) + i, kEps, gate);
                         E.put(ACCD, tr, fa_, gi, tz, fl);
                         break;
@@ -1343,7 +1380,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                     case tp::COS: {
                         const uint32_t s = E.tmp(), ns = E.tmp();
                         E.put(UN, s, 0, v(o.a) + i, 0, 0, U_SIN);
-                        E.put(MAC, ns, 0, s, kMinusOne, kNegZero);
+                        put_mac(ns, s, kMinusOne, kNegZero, false, true);
                         acc(tr, fa_, gi, ns);
                         break;
                     }
@@ -1460,7 +1497,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                     const uint32_t d = E.tmp(), r = E.tmp(), nr = E.tmp();
                     E.put(DET2, d, 0, A);
                     E.put(DIV, r, 0, kOne, d);
-                    E.put(MAC, nr, 0, r, kMinusOne, kNegZero);
+                    put_mac(nr, r, kMinusOne, kNegZero, false, true);
                     E.put(MAC, Ai + 0, 0, A + 3, r, kNegZero);
                     E.put(MAC, Ai + 1, 0, A + 1, nr, kNegZero);
                     E.put(MAC, Ai + 2, 0, A + 2, nr, kNegZero);
