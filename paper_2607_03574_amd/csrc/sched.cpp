@@ -455,9 +455,14 @@ constexpr uint32_t kObsBundleMax = 4;
 constexpr uint32_t kBundleWindow = 24;
 
 // Reorder each run of forward instructions (list scheduling, earliest ready
-// op first, data dependences kept) and bundle up to kBundleMax independent
-// scalar ops of one class into one instruction.  Every op still computes
-// exactly what it computed before, so results are unchanged bit for bit.
+// op first, data dependences kept) and group up to kBundleMax independent
+// scalar ops of one class at one position.  The groups only order the
+// abstract instructions, and with them the value intervals the registers are
+// allocated from: independent ops placed side by side get distinct
+// registers, which leaves the micro-op packer free to put them in one
+// instruction (without this order the logistic program needs 21% more
+// instructions).  Every op still computes exactly what it computed before,
+// so results are unchanged bit for bit.
 std::vector<AI> bundle_forward(const Info &I, const std::vector<AI> &in) {
     std::vector<AI> out;
     out.reserve(in.size());
@@ -528,7 +533,9 @@ std::vector<AI> bundle_forward(const Info &I, const std::vector<AI> &in) {
     return out;
 }
 
-// Bundle scalar adjoint rules of each run of reverse instructions.  An op may
+// Group scalar adjoint rules of each run of reverse instructions (for the
+// same reason as the forward groups: the order of the abstract instructions
+// is the order the registers are allocated in).  An op may
 // be hoisted next to an earlier one only when its own adjoint is complete
 // (every op contributing to it has been emitted) and no op it jumps over
 // touches any of its targets; so every adjoint still receives its
