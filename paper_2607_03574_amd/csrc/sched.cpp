@@ -452,7 +452,7 @@ int rev_class(const Info &I, uint32_t k) {
 }
 constexpr uint32_t kBundleMax = 3;
 constexpr uint32_t kObsBundleMax = 4;
-constexpr uint32_t kBundleWindow = 24;
+constexpr uint32_t kBundleWindow = 48;
 
 // Reorder each run of forward instructions (list scheduling, earliest ready
 // op first, data dependences kept) and group up to kBundleMax independent
