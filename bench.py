@@ -116,36 +116,47 @@ def tape_flops(tape_bytes: bytes) -> float:
 
 
 def build_inputs(name, torch, device):
+    """The workload's device inputs and one step.  Also times the host work
+    per program that the lane-gradient rate leaves out: trace production
+    (bytecode -> tape), upload (validation, copy) and scheduling for the
+    launch's register budget (done once per program and lane count)."""
     import paper_2607_03574_amd as nd
     w = configs.build(name)
     o = torch.tensor(w.obs, device=device)
     p = torch.tensor(w.params, device=device)
+    bcs = w.programs if name == "random_programs" else [w.bytecode]
+    t0 = time.perf_counter()
+    tapes_b = [nd.tape_build(bc) for bc in bcs]
+    t1 = time.perf_counter()
+    tapes = [nd.tape_upload(t) for t in tapes_b]
+    t2 = time.perf_counter()
     if name == "random_programs":
-        tapes_b = [nd.tape_build(bc) for bc in w.programs]
-        tapes = [nd.tape_upload(t) for t in tapes_b]
         n_prog, L, P = p.shape
+        ws_bytes = nd.workspace_bytes_many(tapes, L)
+    else:
+        n_prog, (L, P) = 1, p.shape
+        ws_bytes = nd.workspace_bytes(tapes[0], L, True)
+    t3 = time.perf_counter()
+    host = {"trace_us_per_program": (t1 - t0) / n_prog * 1e6, "upload_us_per_program": (t2 - t1) / n_prog * 1e6,
+            "schedule_us_per_program": (t3 - t2) / n_prog * 1e6}
+    ws = torch.empty(max(ws_bytes, 8), dtype=torch.uint8, device=device)
+    flops = sum(tape_flops(t) for t in tapes_b) * L
+    if name == "random_programs":
         loss = torch.empty((n_prog, L), dtype=torch.float64, device=device)
         grad = torch.zeros((n_prog, L, P), dtype=torch.float64, device=device)
-        ws = torch.empty(max(nd.workspace_bytes_many(tapes, L), 8), dtype=torch.uint8, device=device)
-        flops = sum(tape_flops(t) for t in tapes_b) * L
 
         def step(stream):
             nd.grad_many(tapes, p, o, loss, grad, ws, stream)
-        lanes = n_prog * L
         meta = dict(programs=n_prog, lanes_per_program=L)
-        return w, step, lanes, flops, meta, (w.programs, w.params, w.n_params_each)
-    tape_b = nd.tape_build(w.bytecode)
-    tape = nd.tape_upload(tape_b)
-    L, P = p.shape
+        return w, step, n_prog * L, flops, meta, (w.programs, w.params, w.n_params_each), host
+    tape = tapes[0]
     loss = torch.empty(L, dtype=torch.float64, device=device)
     grad = torch.empty((L, P), dtype=torch.float64, device=device)
-    ws = torch.empty(max(nd.workspace_bytes(tape, L, True), 8), dtype=torch.uint8, device=device)
-    flops = tape_flops(tape_b) * L
 
     def step(stream):
         nd.grad(tape, p, o, loss, grad, ws, stream)
     meta = dict(lanes=L, params=P, tape_ops=nd.tape_info(tape)["n_ops"])
-    return w, step, L, flops, meta, ([w.bytecode], w.params[None], [P])
+    return w, step, L, flops, meta, ([w.bytecode], w.params[None], [P]), host
 
 
 def cpu_baseline(w, progs, budget_s=10.0):
@@ -279,7 +290,7 @@ def main():
     device = torch.device("cuda:0")
     stream = torch.cuda.Stream(device=device)
     with torch.cuda.stream(stream):
-        w, step, lanes, flops, meta, progs = build_inputs(args.workload, torch, device)
+        w, step, lanes, flops, meta, progs, host = build_inputs(args.workload, torch, device)
     torch.cuda.synchronize()
     for _ in range(args.warmup):
         step(stream)
@@ -307,6 +318,7 @@ def main():
                      "traffic": profiled_traffic(args.workload),
                      "kernel": "ndvm_replay", "kernel_ms": kern_s * 1e3,
                      "alg_flops_per_launch": flops},
+        "host": host,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, progs)

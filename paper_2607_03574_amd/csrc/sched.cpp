@@ -242,49 +242,89 @@ struct Interval {
 // compact placement).
 // Returns the register high-water mark; a register whose interval ends at t
 // is reusable from t + 1 on.
+// Free times of the register file, with a min tree over them so that the
+// first register at or after an index that is free by a given time is found
+// in O(log n).  Registers past the file's end read as never free.
+struct FreeTimes {
+    uint32_t n = 0, cap = 1;
+    std::vector<uint32_t> t{UINT32_MAX, UINT32_MAX};
+    explicit FreeTimes(uint32_t pool) { resize(pool); }
+    uint32_t size() const { return n; }
+    uint32_t get(uint32_t i) const { return t[cap + i]; }
+    void set(uint32_t i, uint32_t v) {
+        i += cap;
+        t[i] = v;
+        for (i >>= 1; i; i >>= 1) t[i] = std::min(t[2 * i], t[2 * i + 1]);
+    }
+    void resize(uint32_t m) {  // new registers start free at time 0
+        if (m > cap) {
+            uint32_t c = cap;
+            while (c < m) c *= 2;
+            std::vector<uint32_t> u(2 * c, UINT32_MAX);
+            for (uint32_t i = 0; i < n; ++i) u[c + i] = t[cap + i];
+            cap = c;
+            t.swap(u);
+            for (uint32_t i = cap - 1; i; --i) t[i] = std::min(t[2 * i], t[2 * i + 1]);
+        }
+        for (uint32_t i = n; i < m; ++i) set(i, 0);
+        n = std::max(n, m);
+    }
+    // first i >= lo with free time <= x, or UINT32_MAX
+    uint32_t first(uint32_t lo, uint32_t x) const {
+        if (lo >= n) return UINT32_MAX;
+        uint32_t i = cap + lo;
+        if (t[i] <= x) return lo;
+        // climb until a right sibling subtree holds a candidate
+        for (;;) {
+            if (i == 1) return UINT32_MAX;
+            if (!(i & 1) && t[i + 1] <= x) {
+                i = i + 1;
+                break;
+            }
+            i >>= 1;
+        }
+        while (i < cap) i = t[2 * i] <= x ? 2 * i : 2 * i + 1;
+        return i - cap;
+    }
+};
+
+// Returns the register high-water mark; a register whose interval ends at t
+// is reusable from t + 1 on.
 uint32_t allocate(std::vector<Interval> &iv, uint32_t pool, bool spread = true) {
     std::vector<uint32_t> order(iv.size());
     for (uint32_t i = 0; i < iv.size(); ++i) order[i] = i;
     std::stable_sort(order.begin(), order.end(),
                      [&](uint32_t x, uint32_t y) { return iv[x].start < iv[y].start; });
-    std::vector<uint32_t> busy(pool, 0);  // first time the register is free again
+    FreeTimes busy(pool);  // first time each register is free again
     uint32_t hwm = 0, cursor = 0;
     for (uint32_t id : order) {
         Interval &v = iv[id];
-        if (v.nel == 1 && spread) {
-            const uint32_t n = uint32_t(busy.size());
-            uint32_t r = UINT32_MAX;
-            for (uint32_t k = 0; k < n; ++k) {
-                const uint32_t c = (cursor + k) % n;
-                if (busy[c] <= v.start) {
-                    r = c;
-                    break;
-                }
-            }
+        if (v.nel == 1) {
+            // round robin from the cursor when spreading, else lowest free
+            uint32_t r = busy.first(spread ? cursor : 0, v.start);
+            if (r == UINT32_MAX && spread) r = busy.first(0, v.start);
             if (r == UINT32_MAX) {
-                r = n;
-                busy.push_back(0);
+                r = busy.size();
+                busy.resize(r + 1);
             }
-            busy[r] = v.end + 1;
+            busy.set(r, v.end + 1);
             v.reg = r;
-            cursor = r + 1;
+            if (spread) cursor = r + 1;
             hwm = std::max(hwm, r + 1);
             continue;
         }
-        uint32_t r = 0, run = 0, base = 0;
-        for (r = 0; r < busy.size(); ++r) {
-            if (busy[r] <= v.start) {
-                if (run == 0) base = r;
-                if (++run == v.nel) break;
-            } else {
-                run = 0;
-            }
+        // lowest run of nel registers free by the start; a run cut off by
+        // the file's end is extended
+        uint32_t base = busy.first(0, v.start);
+        while (base != UINT32_MAX) {
+            uint32_t k = 1;
+            while (k < v.nel && base + k < busy.size() && busy.get(base + k) <= v.start) ++k;
+            if (k == v.nel || base + k == busy.size()) break;
+            base = busy.first(base + k + 1, v.start);
         }
-        if (run < v.nel) {
-            if (run == 0) base = uint32_t(busy.size());
-            busy.resize(base + v.nel, 0);
-        }
-        for (uint32_t i = 0; i < v.nel; ++i) busy[base + i] = v.end + 1;
+        if (base == UINT32_MAX) base = busy.size();
+        if (base + v.nel > busy.size()) busy.resize(base + v.nel);
+        for (uint32_t i = 0; i < v.nel; ++i) busy.set(base + i, v.end + 1);
         v.reg = base;
         hwm = std::max(hwm, base + v.nel);
     }
@@ -907,7 +947,11 @@ constexpr uint32_t kTemps = 24;
 // Build the forward phase (shared by both programs) and, for the gradient
 // program, the reverse phase; returns the slot program with registers
 // assigned and micro-ops packed S to an instruction.
-Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t reg_budget, uint32_t n_temps) {
+// Without `full`, stops once the registers are known (n_regs,
+// n_temps_used and the counts of the lowering): what the search over
+// segment sizes needs, without packing and encoding.
+Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t reg_budget, uint32_t n_temps,
+               bool full) {
     using namespace slot;
     const Tape &t = I.t;
     const uint32_t N = I.N, P = I.P;
@@ -1605,6 +1649,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
         Sch.n_temps_used = std::max(Sch.n_temps_used, E.used_tmp);
     }
 
+    if (!full) return Sch;
+
     // ---- pack and encode: forward and reverse phases separately (the
     // reverse phase starts after every forward store)
     const uint32_t trash_row = Sch.n_ckpt_rows;   // kMaxBlock trash rows follow the checkpoints
@@ -1674,10 +1720,11 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
 // values means fewer reuses of one register, which would order otherwise
 // independent micro-ops).  Deterministic: the lowering does not depend on
 // the reservation.
-Schedule build_fit(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t reg_budget) {
-    Schedule s = build(I, B, with_grad, S, reg_budget, kTemps);
-    if (s.n_temps_used == 0) s = build(I, B, with_grad, S, reg_budget, 0);
-    return s;
+Schedule build_fit(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t reg_budget, bool full) {
+    Schedule s = build(I, B, with_grad, S, reg_budget, kTemps, false);
+    const uint32_t temps = s.n_temps_used ? kTemps : 0;
+    if (temps == kTemps && !full) return s;
+    return build(I, B, with_grad, S, reg_budget, temps, full);
 }
 
 }  // namespace
@@ -1689,7 +1736,7 @@ Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget) {
     B.set_cuts({0});
     B.resident.assign(I.N, 0);
     B.res_off.assign(I.N, 0);
-    return build_fit(I, B, false, slots, reg_budget);
+    return build_fit(I, B, false, slots, reg_budget, true);
 }
 
 Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
@@ -1699,7 +1746,8 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
     for (uint32_t k = 0; k < I.N; ++k)
         if (I.kind[k] == K_COMP && I.vlive[k]) total += I.nel[k];
     const uint32_t kResidentAfter = 2;   // checkpointed in more segments -> keep resident
-    auto trial = [&](uint64_t S) {
+    // the search sizes registers only; the chosen size is built in full
+    auto trial = [&](uint64_t S, bool full = false) {
         Builder B(I);
         B.resident.assign(I.N, 0);
         B.res_off.assign(I.N, 0);
@@ -1708,14 +1756,15 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
         B.choose_residents(kResidentAfter);
         B.set_cuts(B.choose_cuts(S));
         B.plan(true);
-        return build_fit(I, B, true, slots, reg_budget);
+        return build_fit(I, B, true, slots, reg_budget, full);
     };
     // Largest segment size (in value elements) whose register file fits the
     // budget: halve until it fits, then bisect between the fitting size and
     // the one above it.  If nothing fits, keep the smallest register file.
     uint64_t hi = std::max<uint64_t>(total, 1);
     Schedule best = trial(hi);
-    if (best.n_regs <= reg_budget) return best;
+    uint64_t best_size = hi;
+    if (best.n_regs <= reg_budget) return trial(best_size, true);
     uint64_t lo = hi;
     bool found = false;
     while (lo > 4) {
@@ -1723,25 +1772,30 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
         Schedule c = trial(lo);
         if (c.n_regs <= reg_budget) {
             best = std::move(c);
+            best_size = lo;
             found = true;
             break;
         }
-        if (c.n_regs < best.n_regs) best = std::move(c);
+        if (c.n_regs < best.n_regs) {
+            best = std::move(c);
+            best_size = lo;
+        }
         hi = lo;
     }
-    if (!found) return best;
+    if (!found) return trial(best_size, true);
     // invariant: lo fits, hi does not
     while (hi - lo > std::max<uint64_t>(8, lo / 16)) {
         uint64_t mid = lo + (hi - lo) / 2;
         Schedule c = trial(mid);
         if (c.n_regs <= reg_budget) {
             best = std::move(c);
+            best_size = mid;
             lo = mid;
         } else {
             hi = mid;
         }
     }
-    return best;
+    return trial(best_size, true);
 }
 
 }  // namespace ndvm
