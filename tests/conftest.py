@@ -13,7 +13,7 @@ if HERE not in sys.path:
 
 
 def pytest_configure(config):
-    config.addinivalue_line("markers", "gpu: needs an MI355X (run on the GPU box)")
+    config.addinivalue_line("markers", "gpu: needs an MI355X (HIP device visible)")
     config.addinivalue_line("markers", "slow: longer CPU test")
 
 
