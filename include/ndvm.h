@@ -152,6 +152,7 @@ ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L,
  *   grad   : grad + q*prog_stride_g, element (l, p) at [l*ld_g + p]
  * All programs read the same obs[n_obs] and must declare that n_obs; ld_p and
  * ld_g must cover the largest P.  Workspace: ndvm_workspace_bytes_many.
+ * More than 65,535 programs are enqueued as several launches on `stream`.
  */
 ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const double *params,
                            int64_t L, int64_t ld_p, int64_t prog_stride_p, const double *obs,

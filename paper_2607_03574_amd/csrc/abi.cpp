@@ -67,6 +67,8 @@ ndvm_status device_props(DeviceProps *out) {
 }
 
 constexpr uint32_t kMaxWavesPerCuTarget = 16;
+// programs per many-program launch (the grid's y extent)
+constexpr int kMaxProgPerLaunch = 65535;
 
 // Micro-ops per instruction (threads per lane) of a launch: 4 slots (16
 // lanes per wave).  Fewer slots would leave fewer unused slots per
@@ -575,12 +577,21 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
                 d_table = it->second;
             }
         }
-        LaunchArgs A{obs, params, loss, grad, static_cast<double *>(ws), ld_p, ld_g, L, Lp, prog_stride_p,
-                     prog_stride_g};
         ProgStatic none{};
         const int variant = n_spill == 0 ? kLdsOnly : n_spill == n_prog ? kSpill : kPerProgram;
-        return check_stream_and_launch(A, static_cast<const ProgStatic *>(d_table), none, uint32_t(n_prog),
-                                       r_launch, variant, S, s);
+        // programs run on the grid's y axis, at most kMaxProgPerLaunch per launch;
+        // later launches see their programs' parameters, outputs and table rows
+        // from their first program on (workspace rows are absolute in the table)
+        for (int q0 = 0; q0 < n_prog; q0 += kMaxProgPerLaunch) {
+            const int nq = std::min(kMaxProgPerLaunch, n_prog - q0);
+            LaunchArgs A{obs, params + q0 * prog_stride_p, loss + int64_t(q0) * L,
+                         grad ? grad + q0 * prog_stride_g : nullptr, static_cast<double *>(ws), ld_p, ld_g, L, Lp,
+                         prog_stride_p, prog_stride_g};
+            st = check_stream_and_launch(A, static_cast<const ProgStatic *>(d_table) + q0, none, uint32_t(nq),
+                                         r_launch, variant, S, s);
+            if (st != NDVM_OK) return st;
+        }
+        return NDVM_OK;
     });
 }
 

@@ -119,6 +119,24 @@ def test_random_programs_small_all_lanes_and_single_equals_many(nd, oracle_mod):
         assert torch.equal(l1, loss[q]) and torch.equal(g1, grad[q, :, :P])
 
 
+def test_many_programs_beyond_one_launch(nd):
+    """More programs than one launch's grid holds (65,535): the call runs
+    several launches; every program's loss and gradient is checked against
+    the closed form of loss = p0 * p1 + p0."""
+    n_prog = 70001
+    tape = nd.tape_upload(nd.tape_build(Asm(2, 0).param(0).param(1).mul().param(0).add().halt().bytes()))
+    rng = np.random.default_rng(7)
+    pv = rng.uniform(-2.0, 2.0, size=(n_prog, 1, 2))
+    p = torch.tensor(pv, device="cuda")
+    o = torch.zeros(0, dtype=torch.float64, device="cuda")
+    loss, grad = nd.grad_many([tape] * n_prog, p, o)
+    torch.cuda.synchronize()
+    a, b = pv[:, 0, 0], pv[:, 0, 1]
+    np.testing.assert_array_equal(loss[:, 0].cpu().numpy(), a * b + a)
+    np.testing.assert_array_equal(grad[:, 0, 0].cpu().numpy(), b + 1.0)
+    np.testing.assert_array_equal(grad[:, 0, 1].cpu().numpy(), a)
+
+
 @pytest.mark.parametrize("L", [1, 2, 63, 65, 129])
 def test_ragged_lane_counts(nd, oracle_mod, L):
     w = configs.lotka_volterra(L=L, T=9)
