@@ -281,7 +281,7 @@ def main():
         print(json.dumps({"copy_bytes_each_way": n * 8, "launches": 3}))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
+        print(json.dumps({"error": "the replay runs on one GPU per process; --gpus must be 1 "
                           "(the path shards by lanes or programs, see the design notes)"}))
         sys.exit(2)
     if args.calibrate:
