@@ -282,7 +282,7 @@ def main():
         return
     if args.gpus != 1:
         print(json.dumps({"error": "the replay runs on one GPU per process; --gpus must be 1 "
-                          "(the path shards by lanes or programs, see the design notes)"}))
+                          "(lanes and programs are independent, so several GPUs would each take a slice; not implemented)"}))
         sys.exit(2)
     if args.calibrate:
         return calibration_bench(args)
