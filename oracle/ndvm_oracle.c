@@ -16,7 +16,7 @@
  * list in reverse applying the vector-Jacobian products of Appendix C, table
  * tab:adjoints, to obtain d loss / d theta_l along the realized trace.
  *
- * Readings where the paper leaves freedom (listed in the design notes):
+ * Readings where the paper leaves freedom:
  *  - sqrt/log clamp at 1e-8 in the forward, adjoint only when the argument
  *    is strictly above the clamp (table tab:adjoints caption);
  *  - single-argument sub/div are negation/reciprocal; binary div adjoint of
