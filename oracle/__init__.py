@@ -6,8 +6,11 @@ may import this package.  The GPU path never calls it.
 ``run`` evaluates a stack-bytecode program for L parameter vectors with the
 plain C interpreter in ``ndvm_oracle.c`` (per-lane realized trace, Wengert
 list, reverse sweep; paper Section 3.4 and Appendix C table tab:adjoints).
-``run_ld`` is the same source evaluated in x87 extended precision, used to
-estimate how strongly rounding disturbs a lane's fp64 result.
+``run(..., extended=True)`` is the same source evaluated in x87 extended
+precision, used to estimate how strongly rounding disturbs a lane's fp64
+result.  ``run_ties`` also lists each lane's near-tie branch encounters, and
+``run(..., flip=...)`` evaluates a lane with one of them decided the other
+way (both are exact results of a realized trace, Section 4 Property 1).
 """
 from __future__ import annotations
 
@@ -49,7 +52,8 @@ def _lib(ld: bool):
             fn.restype = ctypes.c_int
             fn.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64,
                            ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
-                           ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int]
+                           ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                           ctypes.c_double, ctypes.c_void_p, ctypes.c_int]
             err = getattr(lib, "ndvm_oracle_error_ld" if ld else "ndvm_oracle_error")
             err.restype = ctypes.c_char_p
             _libs[key] = (lib, fn, err)
@@ -66,9 +70,28 @@ def _ptr(a):
     return a.ctypes.data if a is not None else None
 
 
+MAX_TIES = 8
+
+
 def run(bytecode: bytes, params, obs, grad: bool = True, threads: int = 0,
-        margin: bool = False, extended: bool = False):
-    """Return (loss[L], grad[L, P] or None, margin[L] or None)."""
+        margin: bool = False, extended: bool = False, flip=None):
+    """Return (loss[L], grad[L, P] or None, margin[L] or None).
+
+    flip: optional int array [L]; lane l inverts the decision of its
+    flip[l]-th IFLT encounter (counted from 0 in walk order; -1: none)."""
+    loss, g, m, _ = _run(bytecode, params, obs, grad, threads, margin, extended, flip, None)
+    return loss, g, m
+
+
+def run_ties(bytecode: bytes, params, obs, tie_tol: float = 1e-9, grad: bool = True,
+             threads: int = 0, extended: bool = False):
+    """Return (loss, grad, margin, ties): ties[L, 8] lists per lane the IFLT
+    encounters whose relative gap |a-b|/max(|a|,|b|) is at most tie_tol,
+    closest first, -1 padded."""
+    return _run(bytecode, params, obs, grad, threads, True, extended, None, tie_tol)
+
+
+def _run(bytecode, params, obs, grad, threads, margin, extended, flip, tie_tol):
     _, fn, err = _lib(extended)
     params = np.ascontiguousarray(params, dtype=np.float64)
     if params.ndim == 1:
@@ -78,10 +101,15 @@ def run(bytecode: bytes, params, obs, grad: bool = True, threads: int = 0,
     loss = np.empty(L)
     g = np.empty((L, P)) if grad else None
     m = np.empty(L) if margin else None
+    ties = np.empty((L, MAX_TIES), dtype=np.int64) if tie_tol is not None else None
+    if flip is not None:
+        flip = np.ascontiguousarray(flip, dtype=np.int64)
+        if flip.shape != (L,):
+            raise ValueError("flip must have one entry per lane")
     if threads <= 0:
         threads = max(1, min(os.cpu_count() or 1, 16))
     rc = fn(bytecode, len(bytecode), _ptr(params), L, P, _ptr(obs), obs.size,
-            _ptr(loss), _ptr(g), P, _ptr(m), threads)
+            _ptr(loss), _ptr(g), P, _ptr(m), _ptr(ties), float(tie_tol or 0.0), _ptr(flip), threads)
     if rc != 0:
         raise OracleError(rc, err().decode(errors="replace"))
-    return loss, g, m
+    return loss, g, m, ties

@@ -398,8 +398,39 @@ static int arity(int op) {
 }
 
 /* Run one lane forward; returns 0 and the loss node id in *loss_id. */
+/* Branch bookkeeping of one lane's walk: numeric IFLTs are counted in the
+ * order the walk meets them (a loop body's IFLT counts once per trip). */
+#define MAX_TIES 8
+typedef struct {
+    real margin;       /* smallest relative gap |a-b|/max(|a|,|b|) met so far */
+    int64_t seen;      /* encounters so far */
+    int64_t flip;      /* encounter whose decision is inverted (-1: none) */
+    real tie_tol;      /* gaps at or below this are recorded as near ties */
+    int n_ties;        /* recorded near ties, closest first */
+    int64_t tie_at[MAX_TIES];
+    real tie_m[MAX_TIES];
+} Branches;
+
+/* keep the MAX_TIES smallest gaps at or below tie_tol, in ascending order
+ * (equal gaps in the order met) */
+static void note_tie(Branches *br, real m, int64_t at) {
+    if (!(m <= br->tie_tol)) return;
+    int k = br->n_ties < MAX_TIES ? br->n_ties++ : MAX_TIES;
+    if (k == MAX_TIES) {
+        if (!(m < br->tie_m[MAX_TIES - 1])) return;
+        k = MAX_TIES - 1;
+    }
+    while (k > 0 && m < br->tie_m[k - 1]) {
+        br->tie_m[k] = br->tie_m[k - 1];
+        br->tie_at[k] = br->tie_at[k - 1];
+        --k;
+    }
+    br->tie_m[k] = m;
+    br->tie_at[k] = at;
+}
+
 static int run_forward(const Prog *P, Lane *S, const real *theta, const double *obs,
-                       int *loss_id, real *margin) {
+                       int *loss_id, Branches *br) {
     S->n_nodes = 0;
     S->sp = 0;
     S->n_pack = 0;
@@ -544,13 +575,20 @@ static int run_forward(const Prog *P, Lane *S, const real *theta, const double *
             int bi = S->stack[--S->sp], ai = S->stack[--S->sp];
             if (!is_scalar(&S->nodes[ai].v) || !is_scalar(&S->nodes[bi].v)) { set_err("IFLT on a non-scalar", pc); return E_RUNTIME; }
             real a = S->nodes[ai].v.e[0], b = S->nodes[bi].v.e[0];
-            if (margin) {
+            int take_then = a < b;
+            if (br) {
                 real den = R_FABS(a) > R_FABS(b) ? R_FABS(a) : R_FABS(b);
                 real m = den > 0 ? R_FABS(a - b) / den : 0;
                 if (a != a || b != b) m = 0;
-                if (m < *margin) *margin = m;
+                if (m < br->margin) br->margin = m;
+                note_tie(br, m, br->seen);
+                /* the other arm of an encounter whose operands sit within
+                 * rounding of a tie is the realized trace of an equally
+                 * valid evaluation (Property 1: exact on either path) */
+                if (br->seen == br->flip) take_then = !take_then;
+                br->seen++;
             }
-            if (a < b) break;                 /* then-arm follows */
+            if (take_then) break;             /* then-arm follows */
             pc = P->match[pc] + 1;            /* first word after ELSE */
             continue;
         }
@@ -762,6 +800,9 @@ typedef struct {
     const double *params, *obs;
     int64_t ld_p, ld_g, l0, l1;
     double *loss, *grad, *margin;
+    int64_t *ties;
+    double tie_tol;
+    const int64_t *flip;
     int status;
 } Job;
 
@@ -776,11 +817,17 @@ static void *worker(void *arg) {
     for (int64_t l = J->l0; l < J->l1; ++l) {
         for (uint32_t i = 0; i < P->n_params; ++i) theta[i] = (real)J->params[l * J->ld_p + i];
         int loss_id = -1;
-        real m = (real)INFINITY;
-        int st = run_forward(P, &S, theta, J->obs, &loss_id, J->margin ? &m : NULL);
+        Branches br;
+        memset(&br, 0, sizeof br);
+        br.margin = (real)INFINITY;
+        br.flip = J->flip ? J->flip[l] : -1;
+        br.tie_tol = (real)J->tie_tol;
+        int st = run_forward(P, &S, theta, J->obs, &loss_id, &br);
         if (st != OK) { J->status = st; break; }
         J->loss[l] = (double)S.nodes[loss_id].v.e[0];
-        if (J->margin) J->margin[l] = (double)m;
+        if (J->margin) J->margin[l] = (double)br.margin;
+        if (J->ties)
+            for (int k = 0; k < MAX_TIES; ++k) J->ties[l * MAX_TIES + k] = k < br.n_ties ? br.tie_at[k] : -1;
         if (J->grad) {
             if (S.cap_adj < S.n_nodes) {
                 free(S.adj);
@@ -806,13 +853,20 @@ static void *worker(void *arg) {
  * params: lane l, parameter i at params[l*ld_p + i]; grad likewise with ld_g.
  * margin (optional): per lane, the smallest relative gap |a-b|/max(|a|,|b|)
  * seen at any IFLT, +inf when the lane meets none.
+ * ties (optional, [L, 8]): per lane, the encounters (IFLTs counted from 0 in
+ * the order the lane's walk meets them) whose gap is at most tie_tol, the 8
+ * smallest gaps in ascending order, -1 padded.
+ * flip (optional): per lane, one encounter whose decision is inverted (-1:
+ * none): the lane's realized trace had that comparison gone the other way.
+ * Used to judge lanes whose comparison is a near tie.
  * Lanes are split into nthreads contiguous blocks; results do not depend on
  * the thread count.  Returns 0, or an error code with a message in
  * ndvm_oracle_error().
  */
 int ENTRY(ndvm_oracle_run)(const uint8_t *bc, size_t bc_len, const double *params, int64_t L,
                            int64_t ld_p, const double *obs, int64_t n_obs, double *loss,
-                           double *grad, int64_t ld_g, double *margin, int nthreads) {
+                           double *grad, int64_t ld_g, double *margin, int64_t *ties,
+                           double tie_tol, const int64_t *flip, int nthreads) {
     Prog P;
     if (!bc || L < 0 || !loss || (L > 0 && !params)) { set_err("bad arguments", -1); return E_ARG; }
     if (parse(bc, bc_len, &P)) return E_BYTECODE;
@@ -829,7 +883,7 @@ int ENTRY(ndvm_oracle_run)(const uint8_t *bc, size_t bc_len, const double *param
     pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
     for (int t = 0; t < nthreads; ++t) {
         jobs[t] = (Job){&P, params, obs, ld_p, ld_g, L * t / nthreads, L * (t + 1) / nthreads,
-                        loss, grad, margin, OK};
+                        loss, grad, margin, ties, tie_tol, flip, OK};
         pthread_create(&th[t], NULL, worker, &jobs[t]);
     }
     int st = OK;
