@@ -30,9 +30,15 @@
  *    work is enqueued (NDVM_E_ARG).
  *  - Device pointers are plain HIP device addresses (for example a torch
  *    tensor's data_ptr()).  `stream` is a hipStream_t passed as void*; NULL
- *    means the default stream.  Compute calls only enqueue work; faults inside
- *    a kernel surface at the caller's next synchronisation, launch failures
- *    as NDVM_E_DEVICE.
+ *    means the default stream.  Compute calls (ndvm_forward, ndvm_grad,
+ *    ndvm_grad_many, ndvm_adam_step) only enqueue work on `stream`: they never
+ *    schedule on the host, allocate or synchronise.  The device program of a
+ *    gradient launch depends on the lane count (it sets each lane's register
+ *    budget) and is scheduled and copied to the device by the sizing calls
+ *    ndvm_workspace_bytes / ndvm_workspace_bytes_many, which a caller needs
+ *    anyway to size the workspace; a compute call for a lane count that was
+ *    never sized returns NDVM_E_ARG.  Faults inside a kernel surface at the
+ *    caller's next synchronisation, launch failures as NDVM_E_DEVICE.
  *  - The caller owns every buffer it passes and must keep it alive until the
  *    enqueued work has completed.  The library keeps no caller pointer after
  *    a call returns.  Tape handles are owned by the library until
@@ -62,7 +68,8 @@ typedef enum {
     NDVM_E_TAPE = 4,            /* malformed tape bytes */
     NDVM_E_NOMEM = 5,           /* host or device allocation failed / workspace too small */
     NDVM_E_DEVICE = 6,          /* HIP runtime error */
-    NDVM_E_UNSUPPORTED = 7      /* valid input outside what this build handles */
+    NDVM_E_UNSUPPORTED = 7,     /* valid input outside what this build handles */
+    NDVM_E_INTERNAL = 8         /* a fault inside the library (a bug), not a caller error */
 } ndvm_status;
 
 /* Save policies for the reverse sweep (argument `policy` of ndvm_tape_upload). */
@@ -103,14 +110,21 @@ ndvm_status ndvm_tape_build(const uint8_t *bytecode, size_t bytecode_len,
 ndvm_status ndvm_tape_upload(const uint8_t *tape, size_t tape_len, int policy,
                              void *stream, ndvm_tape **out);
 
-/* Sizes of an uploaded tape.  Errors: NDVM_E_ARG. */
+/* Sizes of an uploaded tape.  Library infrastructure (no passage of the
+ * paper defines it): counts the caller may want for logging or sizing.
+ * Errors: NDVM_E_ARG. */
 ndvm_status ndvm_tape_info_get(const ndvm_tape *tape, ndvm_tape_info *out);
 
 /*
  * Bytes of device workspace ndvm_forward (with_grad = 0) or ndvm_grad
- * (with_grad = 1) needs for L lanes.  The workspace holds segment
- * checkpoints and any lane registers that do not fit in LDS.
- * Errors: NDVM_E_ARG (null handle/pointer, L < 0).
+ * (with_grad = 1) needs for L lanes.  Library infrastructure (no passage of
+ * the paper defines it): the workspace holds segment checkpoints and any lane
+ * registers that do not fit in LDS.  This is the preparation call of a lane
+ * count: with with_grad = 1 it schedules the tape for that launch shape and
+ * copies the device program to the GPU (synchronously; once per tape and
+ * register budget, then cached), so that ndvm_grad itself only enqueues.
+ * Errors: NDVM_E_ARG (null handle/pointer, L < 0), NDVM_E_NOMEM,
+ * NDVM_E_DEVICE, NDVM_E_UNSUPPORTED (program too large for the device format).
  */
 ndvm_status ndvm_workspace_bytes(const ndvm_tape *tape, int64_t L, int with_grad,
                                  size_t *bytes);
@@ -123,8 +137,9 @@ ndvm_status ndvm_workspace_bytes(const ndvm_tape *tape, int64_t L, int with_grad
  *   loss   : device fp64 [L]
  *   workspace : device buffer of at least ndvm_workspace_bytes(tape, L, 0)
  *               bytes (may be NULL when that size is 0), 256-byte aligned
- * L = 0 is a no-op.  Errors: NDVM_E_ARG, NDVM_E_NOMEM (workspace too small),
- * NDVM_E_DEVICE.
+ * L = 0 is a no-op.  Errors: NDVM_E_ARG (null tape or buffer, L < 0,
+ * ld_p < P, n_obs different from the tape's), NDVM_E_NOMEM (workspace too
+ * small), NDVM_E_DEVICE.
  */
 ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
                          int64_t ld_p, const double *obs, int64_t n_obs, double *loss,
@@ -137,7 +152,8 @@ ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
  * no gradient; a node whose incoming adjoint is exactly zero contributes
  * nothing, so untaken select arms cannot poison gradients.
  * Same argument rules as ndvm_forward plus ld_g >= P; the workspace must
- * hold ndvm_workspace_bytes(tape, L, 1) bytes.
+ * hold ndvm_workspace_bytes(tape, L, 1) bytes, and that call must have been
+ * made for this L (else NDVM_E_ARG).
  */
 ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L,
                       int64_t ld_p, const double *obs, int64_t n_obs, double *loss,
@@ -151,8 +167,11 @@ ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L,
  *   loss   : loss + q*L
  *   grad   : grad + q*prog_stride_g, element (l, p) at [l*ld_g + p]
  * All programs read the same obs[n_obs] and must declare that n_obs; ld_p and
- * ld_g must cover the largest P.  Workspace: ndvm_workspace_bytes_many.
+ * ld_g must cover the largest P.  Workspace: ndvm_workspace_bytes_many, which
+ * must have been called for the same program list and L (else NDVM_E_ARG).
  * More than 65,535 programs are enqueued as several launches on `stream`.
+ * Errors: as ndvm_grad, plus NDVM_E_ARG for n_prog < 0, a null tape or
+ * program strides smaller than L*ld_p / L*ld_g.
  */
 ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const double *params,
                            int64_t L, int64_t ld_p, int64_t prog_stride_p, const double *obs,
@@ -160,7 +179,10 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
                            int64_t prog_stride_g, void *workspace, size_t workspace_bytes,
                            void *stream);
 
-/* Workspace bytes for ndvm_grad_many.  Errors: NDVM_E_ARG. */
+/* Workspace bytes for ndvm_grad_many; the preparation call of a program set
+ * and lane count (schedules every program for the launch's register budget
+ * and copies the programs and the launch's program table to the GPU).
+ * Errors: NDVM_E_ARG, NDVM_E_NOMEM, NDVM_E_DEVICE, NDVM_E_UNSUPPORTED. */
 ndvm_status ndvm_workspace_bytes_many(const ndvm_tape *const *tapes, int n_prog, int64_t L,
                                       size_t *bytes);
 

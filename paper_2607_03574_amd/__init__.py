@@ -15,9 +15,10 @@ from typing import Optional, Sequence
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libndvm.so")
 
-OK, E_ARG, E_BYTECODE, E_STRUCT_DIVERGE, E_TAPE, E_NOMEM, E_DEVICE, E_UNSUPPORTED = range(8)
+OK, E_ARG, E_BYTECODE, E_STRUCT_DIVERGE, E_TAPE, E_NOMEM, E_DEVICE, E_UNSUPPORTED, E_INTERNAL = range(9)
 STATUS_NAMES = {0: "NDVM_OK", 1: "NDVM_E_ARG", 2: "NDVM_E_BYTECODE", 3: "NDVM_E_STRUCT_DIVERGE",
-                4: "NDVM_E_TAPE", 5: "NDVM_E_NOMEM", 6: "NDVM_E_DEVICE", 7: "NDVM_E_UNSUPPORTED"}
+                4: "NDVM_E_TAPE", 5: "NDVM_E_NOMEM", 6: "NDVM_E_DEVICE", 7: "NDVM_E_UNSUPPORTED",
+                8: "NDVM_E_INTERNAL"}
 POLICY_RECOMPUTE = 2
 
 # exported symbols of include/ndvm.h
@@ -114,6 +115,22 @@ def _stream_ptr(stream):
     return getattr(stream, "cuda_stream", stream)
 
 
+def _launch_stream(stream, device):
+    """The torch stream a call launches on: the current stream when `stream`
+    is None, else `stream` (a torch stream or a raw hipStream_t handle).
+    Temporaries a call allocates (workspace, default outputs) are allocated
+    and filled under this stream, so the caching allocator orders their reuse
+    after the launch and a fill cannot land after the kernel's writes.  Inputs
+    the caller produced on another stream are the caller's to order (as for
+    any torch kernel launched on a side stream)."""
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream(device)
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream), device=device)
+
+
 def tape_upload(tape_bytes: bytes, policy: int = POLICY_RECOMPUTE, stream=None) -> Tape:
     h = _vp()
     _check(_tape_upload(tape_bytes, len(tape_bytes), policy, _stream_ptr(stream), ctypes.byref(h)),
@@ -165,11 +182,14 @@ def forward(tape: Tape, params, obs, loss=None, workspace=None, stream=None):
     if params.dim() != 2 or params.stride(1) != 1 or not obs.is_contiguous():
         raise ValueError("params must be [L, P] with unit inner stride; obs contiguous")
     L = params.shape[0]
-    if loss is None:
-        loss = torch.empty(L, dtype=torch.float64, device=params.device)
-    ws, nbytes = _workspace(workspace_bytes(tape, L, False), params.device, workspace)
-    _check(_forward(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
-                    loss.data_ptr(), ws.data_ptr(), nbytes, _stream_ptr(stream)), "ndvm_forward")
+    need = workspace_bytes(tape, L, False)
+    s = _launch_stream(stream, params.device)
+    with torch.cuda.stream(s):
+        if loss is None:
+            loss = torch.empty(L, dtype=torch.float64, device=params.device)
+        ws, nbytes = _workspace(need, params.device, workspace)
+        _check(_forward(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
+                        loss.data_ptr(), ws.data_ptr(), nbytes, s.cuda_stream), "ndvm_forward")
     return loss
 
 
@@ -181,14 +201,17 @@ def grad(tape: Tape, params, obs, loss=None, grad_out=None, workspace=None, stre
     if params.dim() != 2 or params.stride(1) != 1 or not obs.is_contiguous():
         raise ValueError("params must be [L, P] with unit inner stride; obs contiguous")
     L, P = params.shape
-    if loss is None:
-        loss = torch.empty(L, dtype=torch.float64, device=params.device)
-    if grad_out is None:
-        grad_out = torch.empty((L, P), dtype=torch.float64, device=params.device)
-    ws, nbytes = _workspace(workspace_bytes(tape, L, True), params.device, workspace)
-    _check(_grad(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
-                 loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(0), ws.data_ptr(), nbytes,
-                 _stream_ptr(stream)), "ndvm_grad")
+    need = workspace_bytes(tape, L, True)
+    s = _launch_stream(stream, params.device)
+    with torch.cuda.stream(s):
+        if loss is None:
+            loss = torch.empty(L, dtype=torch.float64, device=params.device)
+        if grad_out is None:
+            grad_out = torch.empty((L, P), dtype=torch.float64, device=params.device)
+        ws, nbytes = _workspace(need, params.device, workspace)
+        _check(_grad(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
+                     loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(0), ws.data_ptr(), nbytes,
+                     s.cuda_stream), "ndvm_grad")
     return loss, grad_out
 
 
@@ -203,15 +226,18 @@ def grad_many(tapes: Sequence[Tape], params, obs, loss=None, grad_out=None, work
     n_prog, L, P = params.shape
     if n_prog != len(tapes):
         raise ValueError("one tape per program row")
-    if loss is None:
-        loss = torch.empty((n_prog, L), dtype=torch.float64, device=params.device)
-    if grad_out is None:
-        grad_out = torch.zeros((n_prog, L, P), dtype=torch.float64, device=params.device)
-    ws, nbytes = _workspace(workspace_bytes_many(tapes, L), params.device, workspace)
-    arr = (_vp * n_prog)(*[t.handle for t in tapes])
-    _check(_grad_many(arr, n_prog, params.data_ptr(), L, params.stride(1), params.stride(0), obs.data_ptr(),
-                      obs.numel(), loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(1),
-                      grad_out.stride(0), ws.data_ptr(), nbytes, _stream_ptr(stream)), "ndvm_grad_many")
+    need = workspace_bytes_many(tapes, L)
+    s = _launch_stream(stream, params.device)
+    with torch.cuda.stream(s):
+        if loss is None:
+            loss = torch.empty((n_prog, L), dtype=torch.float64, device=params.device)
+        if grad_out is None:
+            grad_out = torch.zeros((n_prog, L, P), dtype=torch.float64, device=params.device)
+        ws, nbytes = _workspace(need, params.device, workspace)
+        arr = (_vp * n_prog)(*[t.handle for t in tapes])
+        _check(_grad_many(arr, n_prog, params.data_ptr(), L, params.stride(1), params.stride(0), obs.data_ptr(),
+                          obs.numel(), loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(1),
+                          grad_out.stride(0), ws.data_ptr(), nbytes, s.cuda_stream), "ndvm_grad_many")
     return loss, grad_out
 
 

@@ -174,12 +174,20 @@ ndvm_status scheduled(F f, Schedule *out) {
 }
 
 // Device program of `tape` for gradient launches with S slots and register
-// budget b.
-ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, hipStream_t stream, DevProg **out) {
+// budget b.  Scheduling and the program's upload happen only in the sizing
+// calls (build = true); a compute call finds the program or fails, so it
+// never schedules on the host or waits for a copy.
+ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, bool build, DevProg **out) {
     std::lock_guard<std::mutex> lk(tape->mu);
     const uint64_t key = (uint64_t(S) << 32) | b;
     auto it = tape->grad.find(key);
+    if (it == tape->grad.end() && !build) {
+        set_error("the tape has no device program for this lane count: size the workspace with "
+                  "ndvm_workspace_bytes (ndvm_workspace_bytes_many) for the same lane count first");
+        return NDVM_E_ARG;
+    }
     if (it == tape->grad.end()) {
+        const hipStream_t stream = nullptr;
         Schedule sch;
         ndvm_status st = scheduled([&] { return schedule_grad(tape->tape, b, S); }, &sch);
         if (st != NDVM_OK) return st;
@@ -240,6 +248,74 @@ ndvm_status check_stream_and_launch(const LaunchArgs &A, const ProgStatic *table
 std::mutex g_table_mu;
 std::map<std::vector<uint64_t>, void *> g_tables;
 
+// A many-program launch: per-program device programs for the launch's
+// register budget, their table of ProgStatic on the device (cached per
+// program set) and workspace rows.  With build = false (compute calls)
+// nothing is scheduled, allocated or copied: everything must have been
+// prepared by ndvm_workspace_bytes_many for the same lane count.
+struct ManyLaunch {
+    uint32_t S = 0, r_launch = 0;
+    int variant = kLdsOnly;
+    uint64_t rows = 0;
+    void *d_table = nullptr;
+};
+
+ndvm_status many_launch(const ndvm_tape *const *tapes, int n_prog, int64_t L, bool build, ManyLaunch *out) {
+    DeviceProps p;
+    ndvm_status st = device_props(&p);
+    if (st != NDVM_OK) return st;
+    const uint32_t S = choose_slots(p, L, n_prog);
+    const uint32_t b = reg_budget(p, waves_of(L, n_prog, S), S);
+    std::vector<ProgStatic> table(static_cast<size_t>(n_prog), ProgStatic{});
+    std::vector<uint64_t> key;
+    uint64_t row = 0;
+    uint32_t r_launch = 0;
+    int n_spill = 0;
+    for (int q = 0; q < n_prog; ++q) {
+        DevProg *dp;
+        if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), S, b, build, &dp)) != NDVM_OK) return st;
+        uint32_t r_lds = std::min(dp->meta.n_regs, b);
+        r_launch = std::max(r_launch, r_lds);
+        const bool spills = dp->meta.n_regs > r_lds;
+        n_spill += spills;
+        table[q] = ProgStatic{dp->code, dp->consts, row, row + dp->meta.n_ckpt_rows + slot::kMaxBlock,
+                              dp->meta.hdr_off, r_lds, spills};
+        row += ws_rows(*dp, b);
+        key.push_back(tapes[q]->id);
+        key.push_back((uint64_t(S) << 32) | b);
+    }
+    out->S = S;
+    out->r_launch = r_launch;
+    out->rows = row;
+    out->variant = n_spill == 0 ? kLdsOnly : n_spill == n_prog ? kSpill : kPerProgram;
+    if (n_prog == 0) return NDVM_OK;
+    std::lock_guard<std::mutex> lk(g_table_mu);
+    auto it = g_tables.find(key);
+    if (it != g_tables.end()) {
+        out->d_table = it->second;
+        return NDVM_OK;
+    }
+    if (!build) {
+        set_error("no program table for this program set and lane count: size the workspace with "
+                  "ndvm_workspace_bytes_many for the same programs and lane count first");
+        return NDVM_E_ARG;
+    }
+    void *d_table = nullptr;
+    if (hipMalloc(&d_table, table.size() * sizeof(ProgStatic)) != hipSuccess) {
+        (void)hipGetLastError();
+        set_error("hipMalloc of the program table failed");
+        return NDVM_E_NOMEM;
+    }
+    if (hipMemcpy(d_table, table.data(), table.size() * sizeof(ProgStatic), hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(d_table);
+        set_error("copy of the program table failed");
+        return NDVM_E_DEVICE;
+    }
+    g_tables.emplace(key, d_table);
+    out->d_table = d_table;
+    return NDVM_OK;
+}
+
 template <class F>
 ndvm_status guarded(F f) {
     try {
@@ -249,7 +325,7 @@ ndvm_status guarded(F f) {
         return NDVM_E_NOMEM;
     } catch (const std::exception &e) {
         set_error(std::string("internal error: ") + e.what());
-        return NDVM_E_ARG;
+        return NDVM_E_INTERNAL;
     }
 }
 
@@ -381,7 +457,7 @@ ndvm_status ndvm_workspace_bytes(const ndvm_tape *tape, int64_t L, int with_grad
         DevProg *dp;
         if (with_grad) {
             uint32_t b = reg_budget(p, waves_of(L, 1, S), S);
-            st = grad_program(const_cast<ndvm_tape *>(tape), S, b, nullptr, &dp);
+            st = grad_program(const_cast<ndvm_tape *>(tape), S, b, true, &dp);
             if (st != NDVM_OK) return st;
             rows = ws_rows(*dp, b);
         } else {
@@ -401,24 +477,15 @@ ndvm_status ndvm_workspace_bytes_many(const ndvm_tape *const *tapes, int n_prog,
             set_error("ndvm_workspace_bytes_many: bad argument");
             return NDVM_E_ARG;
         }
-        DeviceProps p;
-        ndvm_status st = device_props(&p);
-        if (st != NDVM_OK) return st;
-        int64_t Lp = lpad_of(L);
-        const uint32_t S = choose_slots(p, L, n_prog);
-        uint32_t b = reg_budget(p, waves_of(L, n_prog, S), S);
-        uint64_t rows = 0;
-        for (int q = 0; q < n_prog; ++q) {
+        for (int q = 0; q < n_prog; ++q)
             if (!tapes[q]) {
                 set_error("ndvm_workspace_bytes_many: null tape");
                 return NDVM_E_ARG;
             }
-            DevProg *dp;
-            st = grad_program(const_cast<ndvm_tape *>(tapes[q]), S, b, nullptr, &dp);
-            if (st != NDVM_OK) return st;
-            rows += ws_rows(*dp, b);
-        }
-        *bytes = size_t(rows * uint64_t(Lp) * sizeof(double));
+        ManyLaunch ml;
+        ndvm_status st = many_launch(tapes, n_prog, L, true, &ml);
+        if (st != NDVM_OK) return st;
+        *bytes = size_t(ml.rows * uint64_t(lpad_of(L)) * sizeof(double));
         return NDVM_OK;
     });
 }
@@ -489,8 +556,7 @@ ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L, in
         const uint32_t S = choose_slots(p, L, 1);
         uint32_t b = reg_budget(p, waves_of(L, 1, S), S);
         DevProg *dp;
-        if ((st = grad_program(const_cast<ndvm_tape *>(tape), S, b, static_cast<hipStream_t>(stream), &dp)) != NDVM_OK)
-            return st;
+        if ((st = grad_program(const_cast<ndvm_tape *>(tape), S, b, false, &dp)) != NDVM_OK) return st;
         uint32_t r_lds = std::min(dp->meta.n_regs, b);
         size_t need = size_t(ws_rows(*dp, b) * uint64_t(Lp) * sizeof(double));
         if (need && (!ws || ws_bytes < need)) {
@@ -526,59 +592,20 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
             set_error("ndvm_grad_many: bad strides");
             return NDVM_E_ARG;
         }
-        DeviceProps p;
-        ndvm_status st = device_props(&p);
-        if (st != NDVM_OK) return st;
         hipStream_t s = static_cast<hipStream_t>(stream);
-        int64_t Lp = lpad_of(L);
-        const uint32_t S = choose_slots(p, L, n_prog);
-        uint32_t b = reg_budget(p, waves_of(L, n_prog, S), S);
-        std::vector<ProgStatic> table(static_cast<size_t>(n_prog), ProgStatic{});
-        std::vector<uint64_t> key;
-        uint64_t row = 0;
-        uint32_t r_launch = 0;
-        int n_spill = 0;
-        for (int q = 0; q < n_prog; ++q) {
-            DevProg *dp;
-            if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), S, b, s, &dp)) != NDVM_OK) return st;
-            uint32_t r_lds = std::min(dp->meta.n_regs, b);
-            r_launch = std::max(r_launch, r_lds);
-            const bool spills = dp->meta.n_regs > r_lds;
-            n_spill += spills;
-            table[q] = ProgStatic{dp->code, dp->consts, row, row + dp->meta.n_ckpt_rows + slot::kMaxBlock, dp->meta.hdr_off, r_lds, spills};
-            row += ws_rows(*dp, b);
-            key.push_back(tapes[q]->id);
-            key.push_back((uint64_t(S) << 32) | b);
-        }
-        size_t need = size_t(row * uint64_t(Lp) * sizeof(double));
+        const int64_t Lp = lpad_of(L);
+        ManyLaunch ml;
+        ndvm_status st = many_launch(tapes, n_prog, L, false, &ml);
+        if (st != NDVM_OK) return st;
+        size_t need = size_t(ml.rows * uint64_t(Lp) * sizeof(double));
         if (need && (!ws || ws_bytes < need)) {
             set_error("ndvm_grad_many: workspace too small");
             return NDVM_E_NOMEM;
         }
-        void *d_table = nullptr;
-        {
-            std::lock_guard<std::mutex> lk(g_table_mu);
-            auto it = g_tables.find(key);
-            if (it == g_tables.end()) {
-                if (hipMalloc(&d_table, table.size() * sizeof(ProgStatic)) != hipSuccess) {
-                    (void)hipGetLastError();
-                    set_error("hipMalloc of the program table failed");
-                    return NDVM_E_NOMEM;
-                }
-                if (hipMemcpyAsync(d_table, table.data(), table.size() * sizeof(ProgStatic), hipMemcpyHostToDevice,
-                                   s) != hipSuccess ||
-                    hipStreamSynchronize(s) != hipSuccess) {
-                    (void)hipFree(d_table);
-                    set_error("copy of the program table failed");
-                    return NDVM_E_DEVICE;
-                }
-                g_tables.emplace(key, d_table);
-            } else {
-                d_table = it->second;
-            }
-        }
+        const uint32_t S = ml.S, r_launch = ml.r_launch;
+        const int variant = ml.variant;
+        void *d_table = ml.d_table;
         ProgStatic none{};
-        const int variant = n_spill == 0 ? kLdsOnly : n_spill == n_prog ? kSpill : kPerProgram;
         // programs run on the grid's y axis, at most kMaxProgPerLaunch per launch;
         // later launches see their programs' parameters, outputs and table rows
         // from their first program on (workspace rows are absolute in the table)

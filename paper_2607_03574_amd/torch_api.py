@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import torch
 
-from . import Tape, adam_step, grad
+from . import Tape, _launch_stream, adam_step, grad
 
 
 class ReplayLoss(torch.autograd.Function):
@@ -40,11 +40,15 @@ def calibrate(tape: Tape, params, obs, steps: int, lr: float, beta1: float = 0.9
     Returns the loss of every lane before each step, [steps, L]."""
     L, P = params.shape
     dev = params.device
-    m = torch.zeros((L, P), dtype=torch.float64, device=dev)
-    v = torch.zeros((L, P), dtype=torch.float64, device=dev)
-    g = torch.empty((L, P), dtype=torch.float64, device=dev)
-    hist = torch.empty((steps, L), dtype=torch.float64, device=dev)
-    for t in range(1, steps + 1):
-        grad(tape, params, obs, loss=hist[t - 1], grad_out=g, workspace=workspace, stream=stream)
-        adam_step(params, g, m, v, t, lr, beta1, beta2, eps, stream=stream)
+    s = _launch_stream(stream, dev)
+    # moments and buffers are allocated and zeroed on the stream the replay
+    # and the optimiser steps run on, so the fills are ordered before them
+    with torch.cuda.stream(s):
+        m = torch.zeros((L, P), dtype=torch.float64, device=dev)
+        v = torch.zeros((L, P), dtype=torch.float64, device=dev)
+        g = torch.empty((L, P), dtype=torch.float64, device=dev)
+        hist = torch.empty((steps, L), dtype=torch.float64, device=dev)
+        for t in range(1, steps + 1):
+            grad(tape, params, obs, loss=hist[t - 1], grad_out=g, workspace=workspace, stream=s)
+            adam_step(params, g, m, v, t, lr, beta1, beta2, eps, stream=s)
     return hist

@@ -52,3 +52,16 @@ def oracle_mod():
     import oracle
     oracle.build(force=False)
     return oracle
+
+
+def record(name, **fields):
+    """Print a parity record and, when NDVM_PARITY_LOG names a file, append
+    it there as one JSON line (the GPU runs collect these into a summary)."""
+    import json
+    rec = dict(test=name, **fields)
+    print("PARITY", json.dumps(rec, sort_keys=True), flush=True)
+    path = os.environ.get("NDVM_PARITY_LOG")
+    if path:
+        os.makedirs(os.path.dirname(os.path.abspath(path)), exist_ok=True)
+        with open(path, "a") as f:
+            f.write(json.dumps(rec, sort_keys=True) + "\n")
