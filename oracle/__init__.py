@@ -11,6 +11,9 @@ precision, used to estimate how strongly rounding disturbs a lane's fp64
 result.  ``run_ties`` also lists each lane's near-tie branch encounters, and
 ``run(..., flip=...)`` evaluates a lane with one of them decided the other
 way (both are exact results of a realized trace, Section 4 Property 1).
+``run(..., perturb=(seed, ulps))`` moves every library transcendental result
+by a few ulps, to measure how strongly another math library's last-ulp
+differences move a lane's result.
 """
 from __future__ import annotations
 
@@ -53,7 +56,7 @@ def _lib(ld: bool):
             fn.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64,
                            ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                            ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
-                           ctypes.c_double, ctypes.c_void_p, ctypes.c_int]
+                           ctypes.c_double, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int, ctypes.c_int]
             err = getattr(lib, "ndvm_oracle_error_ld" if ld else "ndvm_oracle_error")
             err.restype = ctypes.c_char_p
             _libs[key] = (lib, fn, err)
@@ -74,12 +77,14 @@ MAX_TIES = 8
 
 
 def run(bytecode: bytes, params, obs, grad: bool = True, threads: int = 0,
-        margin: bool = False, extended: bool = False, flip=None):
+        margin: bool = False, extended: bool = False, flip=None, perturb=None):
     """Return (loss[L], grad[L, P] or None, margin[L] or None).
 
     flip: optional int array [L]; lane l inverts the decision of its
-    flip[l]-th IFLT encounter (counted from 0 in walk order; -1: none)."""
-    loss, g, m, _ = _run(bytecode, params, obs, grad, threads, margin, extended, flip, None)
+    flip[l]-th IFLT encounter (counted from 0 in walk order; -1: none).
+    perturb: optional (seed, ulps); every library transcendental result is
+    moved by a pseudo-random whole number of ulps in [-ulps, ulps]."""
+    loss, g, m, _ = _run(bytecode, params, obs, grad, threads, margin, extended, flip, None, perturb)
     return loss, g, m
 
 
@@ -88,10 +93,10 @@ def run_ties(bytecode: bytes, params, obs, tie_tol: float = 1e-9, grad: bool = T
     """Return (loss, grad, margin, ties): ties[L, 8] lists per lane the IFLT
     encounters whose relative gap |a-b|/max(|a|,|b|) is at most tie_tol,
     closest first, -1 padded."""
-    return _run(bytecode, params, obs, grad, threads, True, extended, None, tie_tol)
+    return _run(bytecode, params, obs, grad, threads, True, extended, None, tie_tol, None)
 
 
-def _run(bytecode, params, obs, grad, threads, margin, extended, flip, tie_tol):
+def _run(bytecode, params, obs, grad, threads, margin, extended, flip, tie_tol, perturb):
     _, fn, err = _lib(extended)
     params = np.ascontiguousarray(params, dtype=np.float64)
     if params.ndim == 1:
@@ -109,7 +114,8 @@ def _run(bytecode, params, obs, grad, threads, margin, extended, flip, tie_tol):
     if threads <= 0:
         threads = max(1, min(os.cpu_count() or 1, 16))
     rc = fn(bytecode, len(bytecode), _ptr(params), L, P, _ptr(obs), obs.size,
-            _ptr(loss), _ptr(g), P, _ptr(m), _ptr(ties), float(tie_tol or 0.0), _ptr(flip), threads)
+            _ptr(loss), _ptr(g), P, _ptr(m), _ptr(ties), float(tie_tol or 0.0), _ptr(flip),
+            int(perturb[0]) if perturb else 0, int(perturb[1]) if perturb else 0, threads)
     if rc != 0:
         raise OracleError(rc, err().decode(errors="replace"))
     return loss, g, m, ties

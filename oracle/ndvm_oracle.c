@@ -238,6 +238,38 @@ static int is_scalar(const Val *v) { return v->rows == 1 && v->cols == 1; }
 static int nel(const Val *v) { return v->rows * v->cols; }
 static real clampv(real x) { return x < CLAMP_EPS ? CLAMP_EPS : x; }
 
+/* Optional perturbation of library transcendental results (exp, log, sin,
+ * cos, pow; forward values and those inside adjoint rules) by a
+ * pseudo-random whole number of units in the last place in [-ulps, ulps],
+ * drawn per evaluation from a counter-based hash of (seed, lane, count).
+ * Another correct math library differs from this one's results by about that
+ * much, so the spread of a lane's result over a few seeds measures how
+ * strongly library last-ulp differences move it (its conditioning with
+ * respect to transcendental rounding).  Off (ulps = 0) by default. */
+typedef struct { int ulps; uint64_t key, count; } Perturb;
+static __thread Perturb g_pt;
+
+static uint64_t mix64(uint64_t z) {     /* splitmix64 finaliser (Steele, Lea, Flood 2014) */
+    z += 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+static real tr(real y) {
+    if (g_pt.ulps <= 0 || !(y == y) || y - y != 0) return y;
+    uint64_t h = mix64(g_pt.key ^ mix64(g_pt.count++));
+    int d = (int)(h % (uint64_t)(2 * g_pt.ulps + 1)) - g_pt.ulps;
+#ifdef ORACLE_LONG_DOUBLE
+    for (; d > 0; --d) y = nextafterl(y, (real)INFINITY);
+    for (; d < 0; ++d) y = nextafterl(y, -(real)INFINITY);
+#else
+    for (; d > 0; --d) y = nextafter(y, INFINITY);
+    for (; d < 0; ++d) y = nextafter(y, -INFINITY);
+#endif
+    return y;
+}
+
 /* Z = X Y with an fma chain over the inner index, ascending. */
 static void matmul(const Val *X, const Val *Y, Val *Z) {
     int m = X->rows, k = X->cols, n = Y->cols;
@@ -326,11 +358,11 @@ static int forward_op(int op, const Val *a, const Val *b, Val *z) {
             real x = a->e[i];
             switch (op) {
             case B_NEG: z->e[i] = -x; break;
-            case B_EXP: z->e[i] = R_EXP(x); break;
-            case B_LOG: z->e[i] = R_LOG(clampv(x)); break;
+            case B_EXP: z->e[i] = tr(R_EXP(x)); break;
+            case B_LOG: z->e[i] = tr(R_LOG(clampv(x))); break;
             case B_SQRT: z->e[i] = R_SQRT(clampv(x)); break;
-            case B_SIN: z->e[i] = R_SIN(x); break;
-            case B_COS: z->e[i] = R_COS(x); break;
+            case B_SIN: z->e[i] = tr(R_SIN(x)); break;
+            case B_COS: z->e[i] = tr(R_COS(x)); break;
             default: z->e[i] = R_FABS(x); break;
             }
         }
@@ -338,7 +370,7 @@ static int forward_op(int op, const Val *a, const Val *b, Val *z) {
     case B_POW:
         if (!is_scalar(a) || !is_scalar(b)) return -1;
         z->rows = z->cols = 1;
-        z->e[0] = R_POW(a->e[0], b->e[0]);
+        z->e[0] = tr(R_POW(a->e[0], b->e[0]));
         return 0;
     case B_DOT:
         if (a->rows != b->rows || a->cols != b->cols) return -1;
@@ -372,7 +404,7 @@ static int forward_op(int op, const Val *a, const Val *b, Val *z) {
     case B_LOGDET:
         if (!shape_ok_small_square(a)) return -1;
         z->rows = z->cols = 1;
-        z->e[0] = R_LOG(clampv(det_of(a)));
+        z->e[0] = tr(R_LOG(clampv(det_of(a))));
         return 0;
     case B_OUTER:
         if (a->cols != 1 || b->cols != 1) return -1;
@@ -702,10 +734,10 @@ static void run_reverse(const Prog *P, Lane *S, int loss_id) {
                 if (a->e[i] > CLAMP_EPS) ga->e[i] = ga->e[i] + g->e[i] / ((real)2 * z->e[i]);
             break;
         case B_SIN:
-            for (int i = 0; i < n; ++i) ga->e[i] = ga->e[i] + g->e[i] * R_COS(a->e[i]);
+            for (int i = 0; i < n; ++i) ga->e[i] = ga->e[i] + g->e[i] * tr(R_COS(a->e[i]));
             break;
         case B_COS:
-            for (int i = 0; i < n; ++i) ga->e[i] = ga->e[i] - g->e[i] * R_SIN(a->e[i]);
+            for (int i = 0; i < n; ++i) ga->e[i] = ga->e[i] - g->e[i] * tr(R_SIN(a->e[i]));
             break;
         case B_ABS:
             for (int i = 0; i < n; ++i) {
@@ -715,7 +747,7 @@ static void run_reverse(const Prog *P, Lane *S, int loss_id) {
             break;
         case B_POW:
             ga->e[0] = ga->e[0] + ((g->e[0] * b->e[0]) * z->e[0]) / a->e[0];
-            gb->e[0] = gb->e[0] + (g->e[0] * z->e[0]) * R_LOG(a->e[0]);
+            gb->e[0] = gb->e[0] + (g->e[0] * z->e[0]) * tr(R_LOG(a->e[0]));
             break;
         case B_DOT: {
             int m = nel(a);
@@ -803,6 +835,8 @@ typedef struct {
     int64_t *ties;
     double tie_tol;
     const int64_t *flip;
+    uint64_t perturb_seed;
+    int perturb_ulps;
     int status;
 } Job;
 
@@ -822,6 +856,9 @@ static void *worker(void *arg) {
         br.margin = (real)INFINITY;
         br.flip = J->flip ? J->flip[l] : -1;
         br.tie_tol = (real)J->tie_tol;
+        g_pt.ulps = J->perturb_ulps;
+        g_pt.key = mix64(J->perturb_seed) ^ (uint64_t)l;
+        g_pt.count = 0;
         int st = run_forward(P, &S, theta, J->obs, &loss_id, &br);
         if (st != OK) { J->status = st; break; }
         J->loss[l] = (double)S.nodes[loss_id].v.e[0];
@@ -859,6 +896,10 @@ static void *worker(void *arg) {
  * flip (optional): per lane, one encounter whose decision is inverted (-1:
  * none): the lane's realized trace had that comparison gone the other way.
  * Used to judge lanes whose comparison is a near tie.
+ * perturb_ulps > 0: every library transcendental result is moved by a
+ * pseudo-random whole number of ulps in [-perturb_ulps, perturb_ulps]
+ * (counter-based hash of perturb_seed, the lane and the evaluation count);
+ * used to measure a lane's sensitivity to math-library rounding.
  * Lanes are split into nthreads contiguous blocks; results do not depend on
  * the thread count.  Returns 0, or an error code with a message in
  * ndvm_oracle_error().
@@ -866,7 +907,8 @@ static void *worker(void *arg) {
 int ENTRY(ndvm_oracle_run)(const uint8_t *bc, size_t bc_len, const double *params, int64_t L,
                            int64_t ld_p, const double *obs, int64_t n_obs, double *loss,
                            double *grad, int64_t ld_g, double *margin, int64_t *ties,
-                           double tie_tol, const int64_t *flip, int nthreads) {
+                           double tie_tol, const int64_t *flip, uint64_t perturb_seed,
+                           int perturb_ulps, int nthreads) {
     Prog P;
     if (!bc || L < 0 || !loss || (L > 0 && !params)) { set_err("bad arguments", -1); return E_ARG; }
     if (parse(bc, bc_len, &P)) return E_BYTECODE;
@@ -883,7 +925,7 @@ int ENTRY(ndvm_oracle_run)(const uint8_t *bc, size_t bc_len, const double *param
     pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
     for (int t = 0; t < nthreads; ++t) {
         jobs[t] = (Job){&P, params, obs, ld_p, ld_g, L * t / nthreads, L * (t + 1) / nthreads,
-                        loss, grad, margin, ties, tie_tol, flip, OK};
+                        loss, grad, margin, ties, tie_tol, flip, perturb_seed, perturb_ulps, OK};
         pthread_create(&th[t], NULL, worker, &jobs[t]);
     }
     int st = OK;

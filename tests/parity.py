@@ -13,6 +13,12 @@ the oracle computed; nothing is excused:
   in x87 extended precision differs from its fp64 result) passes when the GPU
   is within max(2 |o - o_ext|, 1e-11 scale) of the extended-precision value:
   rounding, not the method, decides its last digits;
+* a lane whose result is sensitive to the last ulp of library
+  transcendentals (the GPU's math library and the host's round exp, log,
+  sin, cos and pow differently by an ulp or two) passes when the GPU's
+  deviation from the oracle is within twice the largest deviation of four
+  oracle evaluations with every transcendental result moved by a
+  pseudo-random whole number of ulps in [-2, 2];
 * a lane with a numeric branch whose operands sit within 1e-9 relative of a
   tie (the oracle lists such encounters) may have taken the other arm under
   last-ulp differences of the library transcendentals; it passes when the GPU
@@ -49,6 +55,24 @@ def _ext_ok(gl, gg, ol, og, ole, oge, tol=TOL):
     return ok
 
 
+PERTURB_ULPS = 2
+PERTURB_SEEDS = (101, 202, 303, 404)
+
+
+def _perturb_ok(oracle_mod, bytecode, params, obs, gl, gg, ol, og, tol=TOL):
+    """GPU deviation from the oracle within twice the spread the oracle shows
+    under +-2-ulp perturbations of its transcendental results."""
+    el, eg = _errs(gl, gg, ol, og)
+    sl = np.zeros_like(el)
+    sg = np.zeros_like(eg)
+    for seed in PERTURB_SEEDS:
+        pl, pg, _ = oracle_mod.run(bytecode, params, obs, grad=gg is not None, perturb=(seed, PERTURB_ULPS))
+        a, b = _errs(pl, pg, ol, og)
+        sl = np.maximum(sl, a)
+        sg = np.maximum(sg, b)
+    return (el <= np.maximum(2 * sl, tol)) & (eg <= np.maximum(2 * sg, tol))
+
+
 def compare(gl, gg, ol, og, tol=TOL):
     """Strict bar on every lane (programs without numeric branches, or
     results that must match one evaluation exactly); returns the worst
@@ -75,13 +99,19 @@ def judge(oracle_mod, bytecode, params, obs, gl, gg, tol=TOL, tie_tol=TIE_TOL):
     out = dict(n_lanes=int(el.size), n_strict=int(el.size - pending.size),
                max_loss_err=float(np.max(np.where((el > tol) | (eg > tol), 0, el), initial=0)),
                max_grad_err=float(np.max(np.where((el > tol) | (eg > tol), 0, eg), initial=0)),
-               n_ill_conditioned=0, n_other_arm=0, n_near_tie_lanes=int((ties[:, 0] >= 0).sum()))
+               n_ill_conditioned=0, n_libm_sensitive=0, n_other_arm=0,
+               n_near_tie_lanes=int((ties[:, 0] >= 0).sum()))
     if pending.size:
         sub = params[pending]
         ole, oge, _ = oracle_mod.run(bytecode, sub, obs, grad=with_grad, extended=True)
         ok = _ext_ok(gl[pending], gg[pending] if with_grad else None, ol[pending],
                      og[pending] if with_grad else None, ole, oge, tol)
         out["n_ill_conditioned"] = int(ok.sum())
+        pending = pending[~ok]
+    if pending.size:
+        ok = _perturb_ok(oracle_mod, bytecode, params[pending], obs, gl[pending],
+                         gg[pending] if with_grad else None, ol[pending], og[pending] if with_grad else None, tol)
+        out["n_libm_sensitive"] = int(ok.sum())
         pending = pending[~ok]
     for k in range(ties.shape[1]):
         if not pending.size:

@@ -230,3 +230,65 @@ def test_flip_counts_loop_trips(oracle_mod):
         assert lf[0] == want and gf[0, 1] == want / 3.0, trip
     _, _, _, ties = oracle_mod.run_ties(bc, [[2.0, 3.0]], obs, tie_tol=0.0)
     assert list(ties[0][:3]) == [1, 3, -1]      # exact ties on trips 1 and 3, in walk order
+
+
+# ------------------------------------------------- transcendental perturbation
+def test_perturb_zero_ulps_and_no_transcendentals_are_identity(oracle_mod):
+    w = configs.random_programs(n_prog=3, L=16, n=8, seed=5)
+    for q, bc in enumerate(w.programs):
+        P = w.n_params_each[q]
+        a = oracle_mod.run(bc, w.params[q][:, :P], w.obs)
+        b = oracle_mod.run(bc, w.params[q][:, :P], w.obs, perturb=(7, 0))
+        assert a[0].tobytes() == b[0].tobytes() and a[1].tobytes() == b[1].tobytes()
+    lv = configs.lotka_volterra(L=4, T=20)             # no library transcendental at all
+    a = oracle_mod.run(lv.bytecode, lv.params, lv.obs)
+    b = oracle_mod.run(lv.bytecode, lv.params, lv.obs, perturb=(3, 4))
+    assert a[0].tobytes() == b[0].tobytes() and a[1].tobytes() == b[1].tobytes()
+
+
+def _ulp_moves(y, k):
+    out = {}
+    for d in range(-k, k + 1):
+        v = y
+        for _ in range(abs(d)):
+            v = np.nextafter(v, np.inf if d > 0 else -np.inf)
+        out[float(v)] = d
+    return out
+
+
+@pytest.mark.parametrize("op", [B.EXP, B.LOG, B.SIN, B.COS])
+def test_perturb_moves_each_result_by_at_most_k_ulps(oracle_mod, op):
+    """loss = f(p0) * p1 with p1 = 1: every lane's loss is f(p0) moved by a
+    whole number of ulps in [-2, 2]; over many lanes every move occurs; the
+    gradient of p1 is that same perturbed value (the rule reads z or a fresh
+    evaluation of the derivative, itself perturbed)."""
+    A = Asm(2, 0)
+    A.param(0).raw(op).param(1).mul().halt()
+    L = 400
+    params = np.column_stack([np.full(L, 0.7), np.ones(L)])
+    loss, g, _ = oracle_mod.run(A.bytes(), params, [], perturb=(11, 2))
+    f = {B.EXP: math.exp, B.LOG: math.log, B.SIN: math.sin, B.COS: math.cos}[op]
+    moves = _ulp_moves(f(0.7), 2)
+    seen = set()
+    for l in range(L):
+        assert float(loss[l]) in moves, (l, loss[l])
+        seen.add(moves[float(loss[l])])
+        assert g[l, 1] == loss[l]
+    assert seen == {-2, -1, 0, 1, 2}
+    # different seeds give different draws; the same seed the same ones
+    loss2, _, _ = oracle_mod.run(A.bytes(), params, [], perturb=(12, 2))
+    loss3, _, _ = oracle_mod.run(A.bytes(), params, [], perturb=(11, 2))
+    assert loss3.tobytes() == loss.tobytes() and loss2.tobytes() != loss.tobytes()
+
+
+def test_perturb_reaches_adjoint_rule_evaluations(oracle_mod):
+    """sin's adjoint evaluates cos(x): with the forward value unused by the
+    loss's derivative path (loss = sin(p0)), the gradient moves in ulps of
+    cos(p0)."""
+    A = Asm(1, 0)
+    A.param(0).sin().halt()
+    L = 200
+    loss, g, _ = oracle_mod.run(A.bytes(), np.full((L, 1), 0.3), [], perturb=(5, 1))
+    moves = _ulp_moves(math.cos(0.3), 1)
+    assert all(float(v) in moves for v in g[:, 0])
+    assert len({float(v) for v in g[:, 0]}) == 3
