@@ -3,14 +3,23 @@ sweep) on one MI355X, for one of the five synthetic workloads.
 
 A step is one ndvm_grad call (ndvm_grad_many for the program population) that
 produces loss[L] and grad[L, P] for a batch of L parameter vectors whose
-inputs are already resident in HBM.  Tape production and upload happen before
-the timed region.
+inputs are already resident in HBM.  Tape production, upload and scheduling
+happen before the timed region (reported apart, in the `host` object).  The
+default workload is the largest: the Lotka-Volterra RK4 population (1000
+steps, 65,536 lanes).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
 Prints one JSON line with the metric, a roofline object for the replay
-kernel (its average duration measured with HIP events on the launch stream)
-and the CPU oracle timed on a bounded sample of the same workload.
+kernel (its launch durations measured with HIP events on the launch stream,
+against the algorithmic bytes and flops of one launch) and the CPU oracle
+timed on a bounded sample of the same workload (all host threads up to 16,
+and one thread).
+
+    python bench.py --sweep [--workload NAME]
+
+prints one JSON line per lane count (powers of two from 2^12 to 2^18) of the
+same workload: the lane sweep that shows where a launch fills the GPU.
 
     python bench.py --calibrate N [--workload NAME] [--steps K]
 
@@ -34,7 +43,16 @@ from workloads import configs  # noqa: E402
 
 PEAK_FP64 = 78.6e12        # MI355X fp64 vector FLOP/s
 PEAK_HBM = 8.0e12          # MI355X HBM3E bytes/s
-DEFAULT_WORKLOAD = configs.ORDER[1]
+DEFAULT_WORKLOAD = "lotka_volterra_rk4"
+
+# Doubles of loop-carried state per step and the step count: the values a
+# one-level checkpoint of each step must keep for the reverse sweep (the
+# predator and prey densities; the filter's state mean and covariance, 4 + 16;
+# the logistic state).  The running loss sum needs no checkpoint (its adjoint
+# is 1 whatever its value).  The exponential-decay and tree programs are sums
+# of independent terms with nothing carried.
+STATE_PER_STEP = {"lotka_volterra_rk4": (2, 1000), "kalman_cv4": (20, 200), "logistic_euler": (1, 500),
+                  "exp_decay": (0, 0), "random_programs": (0, 0)}
 CSRC = os.path.join(ROOT, "paper_2607_03574_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
 
@@ -138,7 +156,7 @@ def build_inputs(name, torch, device):
         ws_bytes = nd.workspace_bytes(tapes[0], L, True)
     t3 = time.perf_counter()
     host = {"trace_us_per_program": (t1 - t0) / n_prog * 1e6, "upload_us_per_program": (t2 - t1) / n_prog * 1e6,
-            "schedule_us_per_program": (t3 - t2) / n_prog * 1e6}
+            "schedule_us_per_program": (t3 - t2) / n_prog * 1e6, "total_host_s": t3 - t0, "programs": n_prog}
     ws = torch.empty(max(ws_bytes, 8), dtype=torch.uint8, device=device)
     flops = sum(tape_flops(t) for t in tapes_b) * L
     if name == "random_programs":
@@ -159,30 +177,79 @@ def build_inputs(name, torch, device):
     return w, step, L, flops, meta, ([w.bytecode], w.params[None], [P]), host
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, progs, budget_s=10.0):
     """The oracle, as it stands, on a bounded sample of the same workload:
-    lanes of the benchmark's own parameter population, repeated passes until
-    about `budget_s` seconds of wall time have been spent."""
+    lanes of the benchmark's own parameter population (the first 256 of each
+    program, programs in order), repeated until about `budget_s` seconds of
+    wall time have been spent with every host thread up to 16 (the host share
+    of one GPU), then about a third of that on one thread."""
     import oracle
     bcs, params, nps = progs
-    threads = max(1, min(os.cpu_count() or 1, 16))
-    lanes = min(params.shape[1], 256)
-    t0 = time.perf_counter()
-    done, passes = 0, 0
-    while True:
-        for q in range(len(bcs)):
-            sub = params[q][:lanes, :nps[q]]
-            oracle.run(bcs[q], sub, w.obs, threads=threads)
-            done += sub.shape[0]
-            if time.perf_counter() - t0 > budget_s:
+    nproc = os.cpu_count() or 1
+    threads = max(1, min(nproc, 16))
+
+    def rate(nthreads, budget, lanes):
+        t0 = time.perf_counter()
+        done, progs_run = 0, 0
+        while True:
+            for q in range(len(bcs)):
+                sub = params[q][:lanes, :nps[q]]
+                oracle.run(bcs[q], sub, w.obs, threads=nthreads)
+                done += sub.shape[0]
+                progs_run = max(progs_run, q + 1)
+                if time.perf_counter() - t0 > budget:
+                    break
+            if time.perf_counter() - t0 > budget:
                 break
-        passes += 1
         dt = time.perf_counter() - t0
-        if dt > budget_s or (len(bcs) > 1 and dt > budget_s / 2):
-            break
-    return dict(value=done / dt, unit="lane-gradient evals/s", cores=threads, kind="oracle",
-                sample=f"{done} lane evaluations (first {lanes} lanes of {min(len(bcs), q + 1)} "
-                       f"program(s) of {w.name}, {passes} pass(es)), {dt:.1f} s wall")
+        return done / dt, done, dt, progs_run
+
+    lanes = min(params.shape[1], 256)
+    v_all, n_all, dt_all, pr_all = rate(threads, budget_s, lanes)
+    v_one, n_one, dt_one, pr_one = rate(1, budget_s / 3, min(lanes, 16))
+    return dict(value=v_all, unit="lane-gradient evals/s", cores=threads, kind="oracle",
+                sample=f"{n_all} lane evaluations (first {lanes} lanes of {pr_all} program(s) of {w.name}, "
+                       f"repeated), {dt_all:.1f} s wall on {threads} threads",
+                nproc=nproc, cpu_model=cpu_model(), value_1_core=v_one,
+                sample_1_core=f"{n_one} lane evaluations (first {min(lanes, 16)} lanes of {pr_one} program(s), "
+                              f"repeated), {dt_one:.1f} s wall on 1 thread")
+
+
+def env_info(torch):
+    """What the numbers were measured with."""
+    import subprocess
+    info = {"gpu": torch.cuda.get_device_name(0), "torch": torch.__version__,
+            "hip_runtime": getattr(torch.version, "hip", None)}
+    try:
+        r = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short=12", "HEAD"], capture_output=True, text=True)
+        info["git_commit"] = r.stdout.strip() or None
+    except OSError:
+        info["git_commit"] = None
+    try:
+        with open("/opt/rocm/.info/version") as f:
+            info["rocm"] = f.read().strip()
+    except OSError:
+        info["rocm"] = None
+    return info
+
+
+def alg_bytes(name, L, P, n_prog=1):
+    """Algorithmic HBM bytes of one launch: parameters read, loss and gradient
+    written (8 (2P + 1) per lane), plus a store and a load of every double of
+    loop-carried state per step (16 S T per lane)."""
+    S, T = STATE_PER_STEP[name]
+    return float(n_prog * L * (8 * (2 * P + 1) + 16 * S * T))
 
 
 def calibration_bench(args):
@@ -261,6 +328,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=None, choices=configs.ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true", help="lane sweep 2^12 .. 2^18 of the workload")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run a plain device-to-device copy of this many "
                          "MiB (reference for the FETCH_SIZE / WRITE_SIZE counter scale)")
@@ -287,42 +355,112 @@ def main():
     if args.calibrate:
         return calibration_bench(args)
     import torch
+    if args.sweep:
+        return sweep(args, torch)
     device = torch.device("cuda:0")
     stream = torch.cuda.Stream(device=device)
     with torch.cuda.stream(stream):
         w, step, lanes, flops, meta, progs, host = build_inputs(args.workload, torch, device)
     torch.cuda.synchronize()
-    for _ in range(args.warmup):
-        step(stream)
-    torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        step(stream)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    kern_s = ev0.elapsed_time(ev1) / 1e3 / args.steps
-    ms_per_step = wall / args.steps * 1e3
-    value = lanes / (wall / args.steps)
-    achieved = flops / kern_s
+    res = time_steps(torch, stream, step, args.steps, args.warmup)
+    kern_s = res["kernel_mean_s"]
+    ms_per_step = res["wall_s"] / args.steps * 1e3
+    value = lanes / (res["wall_s"] / args.steps)
+    if args.workload == "random_programs":
+        host["end_to_end_s"] = host["total_host_s"] + kern_s
+    B = alg_bytes(args.workload, meta.get("lanes", meta.get("lanes_per_program")), meta.get("params", 0),
+                  meta.get("programs", 1)) if args.workload != "random_programs" else \
+        float(sum(8 * (2 * P + 1) for P in progs[2]) * meta["lanes_per_program"])
+    roof = roofline(B, flops, kern_s, profiled_traffic(args.workload))
+    roof.update(kernel="ndvm_replay", kernel_ms=kern_s * 1e3, kernel_ms_median=res["kernel_median_s"] * 1e3,
+                kernel_ms_iqr=res["kernel_iqr_s"] * 1e3)
     out = {
         "metric": "lane-gradient evals/sec (fwd+rev) on 1 MI355X",
         "value": value, "unit": "lane-gradient evals/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
-        "config": dict(workload=w.name, **meta),
-        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_FP64 / 1e12,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP64,
-                     "traffic": profiled_traffic(args.workload),
-                     "kernel": "ndvm_replay", "kernel_ms": kern_s * 1e3,
-                     "alg_flops_per_launch": flops},
+        "config": dict(workload=w.name, policy="recompute", **meta),
+        "roofline": roof,
         "host": host,
+        "env": env_info(torch),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, progs)
     print(json.dumps(out), flush=True)
+
+
+def time_steps(torch, stream, step, steps, warmup):
+    """Run `warmup` untimed steps, then `steps` timed ones bracketed by device
+    synchronisation; every launch is also bracketed by HIP events on the
+    launch stream (the kernel's own duration)."""
+    for _ in range(warmup):
+        step(stream)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    t0 = time.perf_counter()
+    evs[0].record(stream)
+    for k in range(steps):
+        step(stream)
+        evs[k + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    d = np.array([evs[k].elapsed_time(evs[k + 1]) / 1e3 for k in range(steps)])
+    q1, q3 = np.percentile(d, [25, 75])
+    return dict(wall_s=wall, kernel_mean_s=float(d.mean()), kernel_median_s=float(np.median(d)),
+                kernel_iqr_s=float(q3 - q1))
+
+
+def roofline(B, F, t, traffic):
+    """Roofline of one launch: the algorithmic bytes B and flops F against
+    MI355X's HBM and fp64 vector peaks; the bound is whichever would take
+    longer at peak, and frac = that time / the measured time t."""
+    t_hbm, t_alu = B / PEAK_HBM, F / PEAK_FP64
+    if t_hbm >= t_alu:
+        r = {"bound": "hbm", "achieved": B / t / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s"}
+    else:
+        r = {"bound": "alu", "achieved": F / t / 1e12, "peak": PEAK_FP64 / 1e12, "unit": "TFLOP/s"}
+    r["frac"] = r["achieved"] / r["peak"]
+    r["traffic"] = traffic
+    r.update(alg_bytes_per_launch=B, alg_flops_per_launch=F, t_at_hbm_peak_ms=t_hbm * 1e3,
+             t_at_fp64_peak_ms=t_alu * 1e3, alg_frac=max(t_hbm, t_alu) / t,
+             fp64_tflops=F / t / 1e12, alg_hbm_gbps=B / t / 1e9,
+             counter_hbm_gbps=(traffic / t / 1e9) if traffic else None)
+    return r
+
+
+def sweep(args, torch):
+    """Lane sweep of one workload: lane-grads/s and the roofline fraction at
+    L = 2^12 .. 2^18 (parameters drawn by the workload's own recipe)."""
+    import paper_2607_03574_amd as nd
+    name = args.workload
+    if name == "random_programs":
+        raise SystemExit("the sweep takes a single-program workload")
+    device = torch.device("cuda:0")
+    stream = torch.cuda.Stream(device=device)
+    for e in range(12, 19):
+        L = 1 << e
+        with torch.cuda.stream(stream):
+            w = configs.build(name, L=L)
+            tb = nd.tape_build(w.bytecode)
+            tape = nd.tape_upload(tb)
+            p = torch.tensor(w.params, device=device)
+            o = torch.tensor(w.obs, device=device)
+            P = p.shape[1]
+            ws = torch.empty(max(nd.workspace_bytes(tape, L, True), 8), dtype=torch.uint8, device=device)
+            loss = torch.empty(L, dtype=torch.float64, device=device)
+            grad = torch.empty((L, P), dtype=torch.float64, device=device)
+        torch.cuda.synchronize()
+
+        def step(s):
+            nd.grad(tape, p, o, loss, grad, ws, s)
+        res = time_steps(torch, stream, step, args.steps, args.warmup)
+        t = res["kernel_mean_s"]
+        roof = roofline(alg_bytes(name, L, P), tape_flops(tb) * L, t, None)
+        print(json.dumps({"workload": name, "lanes": L, "lane_grads_per_s": L / t, "kernel_ms": t * 1e3,
+                          "kernel_ms_median": res["kernel_median_s"] * 1e3, "bound": roof["bound"],
+                          "frac": roof["frac"], "alg_frac": roof["alg_frac"],
+                          "fp64_tflops": roof["fp64_tflops"], "alg_hbm_gbps": roof["alg_hbm_gbps"]}), flush=True)
+        del tape, p, ws, loss, grad
 
 
 if __name__ == "__main__":

@@ -99,8 +99,8 @@ def test_random_programs_full_size_every_program(nd, oracle_mod):
     loss, grad = nd.grad_many(tapes, p, o)
     torch.cuda.synchronize()
     loss, grad = loss.cpu().numpy(), grad.cpu().numpy()
-    tot = dict(n_lanes=0, n_strict=0, n_ill_conditioned=0, n_other_arm=0, n_near_tie_lanes=0,
-               max_loss_err=0.0, max_grad_err=0.0)
+    tot = dict(n_lanes=0, n_strict=0, n_ill_conditioned=0, n_libm_sensitive=0, n_other_arm=0,
+               n_near_tie_lanes=0, max_loss_err=0.0, max_grad_err=0.0)
     rng = np.random.default_rng(1)
     failures = []
     for q in range(len(tapes)):
