@@ -161,6 +161,27 @@ ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L,
                       void *stream);
 
 /*
+ * ndvm_grad without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  The call allocates nothing (no hipMalloc, hipFree
+ * or allocating library routine): the launch's checkpoint, trash and spill
+ * rows live in a static device array of NDVM_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every GPU it runs on until the process ends.  Arguments,
+ * results and errors as ndvm_grad, with the same preparation
+ * (ndvm_workspace_bytes(tape, L, 1) for this L, made beforehand, where
+ * allocation is allowed); a launch whose workspace would exceed the array is
+ * rejected with NDVM_E_NOMEM before anything is enqueued.  Nothing in the
+ * array needs to start at zero (every row is written before it is read), and
+ * it keeps the last call's contents.  All calls on one GPU share the array:
+ * calls that can overlap on one GPU (several streams, several threads) race
+ * and must be serialised by the caller.
+ */
+#define NDVM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+ndvm_status ndvm_grad_noalloc(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p,
+                              const double *obs, int64_t n_obs, double *loss, double *grad, int64_t ld_g,
+                              void *stream);
+
+/*
  * Many programs in one launch (candidate-level parallelism of Section 6,
  * "Across cores", mapped onto the GPU grid): program q uses
  *   params : params + q*prog_stride_p, element (l, p) at [l*ld_p + p]

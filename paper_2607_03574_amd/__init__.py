@@ -20,11 +20,12 @@ STATUS_NAMES = {0: "NDVM_OK", 1: "NDVM_E_ARG", 2: "NDVM_E_BYTECODE", 3: "NDVM_E_
                 4: "NDVM_E_TAPE", 5: "NDVM_E_NOMEM", 6: "NDVM_E_DEVICE", 7: "NDVM_E_UNSUPPORTED",
                 8: "NDVM_E_INTERNAL"}
 POLICY_RECOMPUTE = 2
+NOALLOC_SCRATCH_BYTES = 64 << 20    # NDVM_NOALLOC_SCRATCH_BYTES
 
 # exported symbols of include/ndvm.h
 EXPORTS = ["ndvm_tape_build", "ndvm_tape_upload", "ndvm_tape_info_get", "ndvm_workspace_bytes",
            "ndvm_forward", "ndvm_grad", "ndvm_grad_many", "ndvm_workspace_bytes_many",
-           "ndvm_tape_free", "ndvm_free", "ndvm_last_error", "ndvm_adam_step"]
+           "ndvm_tape_free", "ndvm_free", "ndvm_last_error", "ndvm_adam_step", "ndvm_grad_noalloc"]
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_03574_amd/build.py "
@@ -54,6 +55,7 @@ _ws_bytes = _sig("ndvm_workspace_bytes", _int, [_vp, _i64, _int, ctypes.POINTER(
 _ws_bytes_many = _sig("ndvm_workspace_bytes_many", _int, [ctypes.POINTER(_vp), _int, _i64, ctypes.POINTER(_sz)])
 _forward = _sig("ndvm_forward", _int, [_vp, _vp, _i64, _i64, _vp, _i64, _vp, _vp, _sz, _vp])
 _grad = _sig("ndvm_grad", _int, [_vp, _vp, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp, _sz, _vp])
+_grad_noalloc = _sig("ndvm_grad_noalloc", _int, [_vp, _vp, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp])
 _grad_many = _sig("ndvm_grad_many", _int, [ctypes.POINTER(_vp), _int, _vp, _i64, _i64, _i64, _vp, _i64, _vp,
                                             _vp, _i64, _i64, _vp, _sz, _vp])
 _tape_free = _sig("ndvm_tape_free", None, [_vp])
@@ -212,6 +214,23 @@ def grad(tape: Tape, params, obs, loss=None, grad_out=None, workspace=None, stre
         _check(_grad(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
                      loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(0), ws.data_ptr(), nbytes,
                      s.cuda_stream), "ndvm_grad")
+    return loss, grad_out
+
+
+def grad_noalloc(tape: Tape, params, obs, loss, grad_out, stream=None):
+    """ndvm_grad_noalloc: (loss[L], grad[L, P]) into the caller's buffers with
+    no workspace (the library's static scratch array serves).  The lane count
+    must have been prepared with workspace_bytes(tape, L, True)."""
+    for name, x in (("params", params), ("obs", obs), ("loss", loss), ("grad", grad_out)):
+        _dev_f64(x, name)
+    if params.dim() != 2 or params.stride(1) != 1 or not obs.is_contiguous() or grad_out.stride(1) != 1:
+        raise ValueError("params and grad must be [L, P] with unit inner stride; obs contiguous")
+    L = params.shape[0]
+    if loss.numel() < L or grad_out.shape[0] < L:
+        raise ValueError("loss and grad must hold L rows")
+    _check(_grad_noalloc(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
+                         loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(0), _stream_ptr(stream)),
+           "ndvm_grad_noalloc")
     return loss, grad_out
 
 

@@ -21,6 +21,8 @@ namespace ndvm {
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
                          uint32_t r_lds, int variant, uint32_t slots, hipStream_t stream);
 bool slots_supported(uint32_t S);
+size_t scratch_bytes();
+hipError_t scratch_address(void **out);
 struct AdamArgs {
     double *p;
     const double *g;
@@ -539,36 +541,69 @@ ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
     });
 }
 
+// ndvm_grad and its allocation-free variant: `ws` is the caller's workspace
+// or the static scratch array's device address.
+static ndvm_status grad_impl(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p,
+                             const double *obs, int64_t n_obs, double *loss, double *grad, int64_t ld_g, void *ws,
+                             size_t ws_bytes, bool static_ws, void *stream, const char *who) {
+    ndvm_status st = check_common(tape, params, L, ld_p, obs, n_obs, loss, who);
+    if (st != NDVM_OK) return st;
+    if (ld_g < int64_t(tape->tape.n_params) || ld_g < 0 || (L > 0 && tape->tape.n_params > 0 && !grad)) {
+        set_error(std::string(who) + ": bad grad buffer or ld_g");
+        return NDVM_E_ARG;
+    }
+    if (L == 0) return NDVM_OK;
+    DeviceProps p;
+    if ((st = device_props(&p)) != NDVM_OK) return st;
+    int64_t Lp = lpad_of(L);
+    const uint32_t S = choose_slots(p, L, 1);
+    uint32_t b = reg_budget(p, waves_of(L, 1, S), S);
+    DevProg *dp;
+    if ((st = grad_program(const_cast<ndvm_tape *>(tape), S, b, false, &dp)) != NDVM_OK) return st;
+    uint32_t r_lds = std::min(dp->meta.n_regs, b);
+    size_t need = size_t(ws_rows(*dp, b) * uint64_t(Lp) * sizeof(double));
+    if (static_ws) {
+        if (need > scratch_bytes()) {
+            set_error(std::string(who) + ": this launch needs " + std::to_string(need) +
+                      " bytes of workspace, more than the static scratch of " + std::to_string(scratch_bytes()) +
+                      " bytes; use ndvm_grad with a caller workspace");
+            return NDVM_E_NOMEM;
+        }
+        const hipError_t e = scratch_address(&ws);
+        if (e != hipSuccess) {
+            set_error(std::string(who) + ": hipGetSymbolAddress of the scratch array failed: " +
+                      hipGetErrorString(e));
+            return NDVM_E_DEVICE;
+        }
+        ws_bytes = scratch_bytes();
+    }
+    if (need && (!ws || ws_bytes < need)) {
+        set_error(std::string(who) + ": workspace too small");
+        return NDVM_E_NOMEM;
+    }
+    double *wsd = static_cast<double *>(ws);
+    LaunchArgs A{obs, params, loss, grad, wsd, ld_p, ld_g, L, Lp, 0, 0};
+    const bool spills = dp->meta.n_regs > r_lds;
+    ProgStatic D{dp->code, dp->consts, 0, uint64_t(dp->meta.n_ckpt_rows) + slot::kMaxBlock, dp->meta.hdr_off, r_lds, spills};
+    return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, S,
+                                   static_cast<hipStream_t>(stream));
+}
+
 ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p, const double *obs,
                       int64_t n_obs, double *loss, double *grad, int64_t ld_g, void *ws, size_t ws_bytes,
                       void *stream) {
     return guarded([&]() -> ndvm_status {
-        ndvm_status st = check_common(tape, params, L, ld_p, obs, n_obs, loss, "ndvm_grad");
-        if (st != NDVM_OK) return st;
-        if (ld_g < int64_t(tape->tape.n_params) || ld_g < 0 || (L > 0 && tape->tape.n_params > 0 && !grad)) {
-            set_error("ndvm_grad: bad grad buffer or ld_g");
-            return NDVM_E_ARG;
-        }
-        if (L == 0) return NDVM_OK;
-        DeviceProps p;
-        if ((st = device_props(&p)) != NDVM_OK) return st;
-        int64_t Lp = lpad_of(L);
-        const uint32_t S = choose_slots(p, L, 1);
-        uint32_t b = reg_budget(p, waves_of(L, 1, S), S);
-        DevProg *dp;
-        if ((st = grad_program(const_cast<ndvm_tape *>(tape), S, b, false, &dp)) != NDVM_OK) return st;
-        uint32_t r_lds = std::min(dp->meta.n_regs, b);
-        size_t need = size_t(ws_rows(*dp, b) * uint64_t(Lp) * sizeof(double));
-        if (need && (!ws || ws_bytes < need)) {
-            set_error("ndvm_grad: workspace too small");
-            return NDVM_E_NOMEM;
-        }
-        double *wsd = static_cast<double *>(ws);
-        LaunchArgs A{obs, params, loss, grad, wsd, ld_p, ld_g, L, Lp, 0, 0};
-        const bool spills = dp->meta.n_regs > r_lds;
-        ProgStatic D{dp->code, dp->consts, 0, uint64_t(dp->meta.n_ckpt_rows) + slot::kMaxBlock, dp->meta.hdr_off, r_lds, spills};
-        return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, S,
-                                       static_cast<hipStream_t>(stream));
+        return grad_impl(tape, params, L, ld_p, obs, n_obs, loss, grad, ld_g, ws, ws_bytes, false, stream,
+                         "ndvm_grad");
+    });
+}
+
+ndvm_status ndvm_grad_noalloc(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p,
+                              const double *obs, int64_t n_obs, double *loss, double *grad, int64_t ld_g,
+                              void *stream) {
+    return guarded([&]() -> ndvm_status {
+        return grad_impl(tape, params, L, ld_p, obs, n_obs, loss, grad, ld_g, nullptr, 0, true, stream,
+                         "ndvm_grad_noalloc");
     });
 }
 

@@ -17,6 +17,7 @@
 
 #include <mutex>
 
+#include "../../include/ndvm.h"
 #include "slot.h"
 #include "slot_exec.h"
 
@@ -296,6 +297,38 @@ hipError_t launch_s(const LaunchArgs &A, const ProgStatic *d_table, const ProgSt
 
 // Slot counts the kernel is built for (micro-ops per instruction).
 bool slots_supported(uint32_t S) { return S == 4; }
+
+// Static workspace of the allocation-free gradient entry point: checkpoint,
+// trash and spill rows of one launch live here instead of in a caller
+// workspace.  Each GPU the library runs on holds its own copy from module load
+// until the process ends.  Host code never passes `scratch` itself to a
+// kernel: in host code the name is a host-side stand-in, not a device
+// address; the device address comes from hipGetSymbolAddress, once per device.
+constexpr size_t kScratchBytes = NDVM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) double scratch[kScratchBytes / sizeof(double)];
+
+size_t scratch_bytes() { return kScratchBytes; }
+
+// Device address of `scratch` on the current device, looked up on the first
+// call per device (with that device current) and cached.
+hipError_t scratch_address(void **out) {
+    static std::mutex mu;
+    static void *addr[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!addr[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!ptr) return hipErrorInvalidSymbol;
+        addr[dev] = ptr;
+    }
+    *out = addr[dev];
+    return hipSuccess;
+}
 
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
                          uint32_t r_lds, int variant, uint32_t slots, hipStream_t stream) {
