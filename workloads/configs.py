@@ -70,6 +70,19 @@ def exp_decay_program(n: int) -> bytes:
     return A.bytes()
 
 
+def exp_decay_term_program() -> bytes:
+    """One data point of the exponential-decay loss, for the flattened data
+    axis: obs = [t, y] of the lane's point; params (a, b, c); term = r^2 with
+    r = a * exp(-(b t)) + c - y, the same operations in the same order as one
+    trip of exp_decay_program's loop."""
+    A = Asm(3, 2)
+    A.param(0).param(1).obs(0).mul().neg().exp().mul()
+    A.param(2).add()
+    A.obs(1).sub()
+    A.dup().mul()
+    return A.halt().bytes()
+
+
 def exp_decay(L: int = 256, n: int = 64, seed: int = 1001, noise: float = 0.01):
     r_data, r_lane, _ = _rngs(seed)
     t = np.linspace(0.0, 5.0, n)
@@ -311,6 +324,22 @@ def tree_program(tree, n_params: int, n: int) -> bytes:
     A.endloop()
     A.loadl(0).push(1.0 / n).mul().halt()
     return A.bytes()
+
+
+def tree_term_program(tree, n_params: int) -> bytes:
+    """One data point of a tree program's loss, for the flattened data axis:
+    obs = [x, y] of the lane's point; term = (tree(x) - y)^2, the same
+    operations in the same order as one trip of tree_program's loop."""
+    A = Asm(n_params, 2)
+    randtree.emit(A, tree, x_obs=(0,))
+    A.obs(1).sub().dup().mul()
+    return A.halt().bytes()
+
+
+def points_of(obs: np.ndarray, n: int, width: int = 2) -> np.ndarray:
+    """Observations [f_0..f_{n-1}, g_0..g_{n-1}, ...] as point-major rows
+    [[f_0, g_0, ...], ...] (the layout of the flattened data axis)."""
+    return np.ascontiguousarray(np.asarray(obs, dtype=np.float64).reshape(width, n).T)
 
 
 def random_programs(n_prog: int = 1024, L: int = 1024, n: int = 128,

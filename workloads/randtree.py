@@ -142,49 +142,50 @@ def evaluate(t, consts, x: float) -> float:
     raise ValueError(op)
 
 
-def emit(A, t):
+def emit(A, t, x_obs=(0, 1)):
     """Append postfix bytecode evaluating the tree for the current loop
-    counter (x = OBS 0 with stride 1, constant j = PARAM j)."""
+    counter (x = OBS 0 with stride 1, constant j = PARAM j); x_obs gives the
+    OBS word's base and strides (x_obs=(0,) reads obs[0] outside any loop)."""
     op = t[0]
     if op == "x":
-        A.obs(0, 1)
+        A.obs(*x_obs)
         return
     if op == "c":
         A.param(t[1])
         return
     k = t[1:]
     if op in ("add", "sub", "mul"):
-        emit(A, k[0])
-        emit(A, k[1])
+        emit(A, k[0], x_obs)
+        emit(A, k[1], x_obs)
         getattr(A, op)()
     elif op == "pdiv":
-        emit(A, k[0])
+        emit(A, k[0], x_obs)
         A.push(1.0)
-        emit(A, k[1])
+        emit(A, k[1], x_obs)
         A.dup().mul().add().div()
     elif op == "ppow":
         A.push(1.0)
-        emit(A, k[0])
+        emit(A, k[0], x_obs)
         A.dup().mul().add()
-        emit(A, k[1])
+        emit(A, k[1], x_obs)
         A.sin().pow()
     elif op == "sin":
-        emit(A, k[0])
+        emit(A, k[0], x_obs)
         A.sin()
     elif op == "pexp":
-        emit(A, k[0])
+        emit(A, k[0], x_obs)
         A.sin().exp()
     elif op == "plog":
         A.push(1.0)
-        emit(A, k[0])
+        emit(A, k[0], x_obs)
         A.dup().mul().add().log()
     elif op == "iflt":
-        emit(A, k[0])
-        emit(A, k[1])
+        emit(A, k[0], x_obs)
+        emit(A, k[1], x_obs)
         A.iflt()
-        emit(A, k[2])
+        emit(A, k[2], x_obs)
         A.else_()
-        emit(A, k[3])
+        emit(A, k[3], x_obs)
         A.endif()
     else:
         raise ValueError(op)
