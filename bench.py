@@ -21,6 +21,11 @@ and one thread).
 prints one JSON line per lane count (powers of two from 2^12 to 2^18) of the
 same workload: the lane sweep that shows where a launch fills the GPU.
 
+    python bench.py --flatten --workload exp_decay|random_programs
+
+times the flattened data axis (one lane per parameter vector and data point,
+ndvm_grad_points) against the ordinary replay of the same workload.
+
     python bench.py --calibrate N [--workload NAME] [--steps K]
 
 instead measures calibrations per second: every lane of the workload is one
@@ -131,6 +136,42 @@ def tape_flops(tape_bytes: bytes) -> float:
         if active[k]:
             rev += fr
     return fwd + rev
+
+
+def build_flattened(name, torch, device):
+    """The exponential-decay workload or the program population with the
+    data axis flattened into the lanes (ndvm_grad_points: one lane per
+    parameter vector and data point, then a fold over the points); one step
+    produces the same loss[L] and grad[L, P] per program as the unflattened
+    step."""
+    import paper_2607_03574_amd as nd
+    w = configs.build(name)
+    if name == "exp_decay":
+        n = w.meta["n_obs_points"]
+        terms = [configs.exp_decay_term_program()]
+        params = [w.params]
+    elif name == "random_programs":
+        n = w.meta["n"]
+        terms = [configs.tree_term_program(t, c) for t, c in zip(w.meta["trees"], w.n_params_each)]
+        params = [np.ascontiguousarray(w.params[q][:, :c]) for q, c in enumerate(w.n_params_each)]
+    else:
+        raise SystemExit("--flatten takes exp_decay or random_programs")
+    pts = torch.tensor(configs.points_of(w.obs, n), device=device)
+    t0 = time.perf_counter()
+    tapes = [nd.tape_upload(nd.tape_build(t)) for t in terms]
+    ps = [torch.tensor(p, device=device) for p in params]
+    L = ps[0].shape[0]
+    need = max(nd.workspace_bytes_points(t, L, n) for t in tapes)
+    host = {"total_host_s": time.perf_counter() - t0, "programs": len(tapes)}
+    ws = torch.empty(need, dtype=torch.uint8, device=device)
+    outs = [(torch.empty(L, dtype=torch.float64, device=device),
+             torch.empty((L, p.shape[1]), dtype=torch.float64, device=device)) for p in ps]
+
+    def step(stream):
+        for tape, p, (lo, go) in zip(tapes, ps, outs):
+            nd.grad_points(tape, p, pts, 1.0 / n, lo, go, ws, stream)
+    meta = dict(programs=len(tapes), lanes_per_program=L, data_points=n, flattened_lanes=L * n)
+    return w, step, L * len(tapes), meta, host
 
 
 def build_inputs(name, torch, device):
@@ -329,6 +370,8 @@ def main():
     ap.add_argument("--workload", default=None, choices=configs.ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true", help="lane sweep 2^12 .. 2^18 of the workload")
+    ap.add_argument("--flatten", action="store_true",
+                    help="data axis flattened into the lanes (exp_decay, random_programs), against the unflattened step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run a plain device-to-device copy of this many "
                          "MiB (reference for the FETCH_SIZE / WRITE_SIZE counter scale)")
@@ -357,6 +400,8 @@ def main():
     import torch
     if args.sweep:
         return sweep(args, torch)
+    if args.flatten:
+        return flattened_bench(args, torch)
     device = torch.device("cuda:0")
     stream = torch.cuda.Stream(device=device)
     with torch.cuda.stream(stream):
@@ -386,6 +431,30 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, progs)
+    print(json.dumps(out), flush=True)
+
+
+def flattened_bench(args, torch):
+    """The flattened data axis against the unflattened replay on the same
+    workload: lane-grads/s of each (the unflattened figure from a run of the
+    ordinary step in the same process)."""
+    device = torch.device("cuda:0")
+    stream = torch.cuda.Stream(device=device)
+    with torch.cuda.stream(stream):
+        w, step, lanes, meta, host = build_flattened(args.workload, torch, device)
+    torch.cuda.synchronize()
+    res = time_steps(torch, stream, step, args.steps, args.warmup)
+    with torch.cuda.stream(stream):
+        _, ustep, ulanes, _, _, _, _ = build_inputs(args.workload, torch, device)
+    torch.cuda.synchronize()
+    ures = time_steps(torch, stream, ustep, args.steps, args.warmup)
+    out = {"metric": "lane-gradient evals/sec (fwd+rev) on 1 MI355X, data axis flattened", "workload": w.name,
+           "value": lanes / (res["wall_s"] / args.steps), "unit": "lane-gradient evals/s",
+           "ms_per_step": res["wall_s"] / args.steps * 1e3, "kernel_ms_mean": res["kernel_mean_s"] * 1e3,
+           "unflattened_value": ulanes / (ures["wall_s"] / args.steps),
+           "unflattened_ms_per_step": ures["wall_s"] / args.steps * 1e3,
+           "speedup": ures["wall_s"] / res["wall_s"], "dtype": "f64", "data": "synthetic",
+           "config": meta, "host": host, "steps": args.steps, "warmup": args.warmup}
     print(json.dumps(out), flush=True)
 
 

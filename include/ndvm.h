@@ -182,6 +182,39 @@ ndvm_status ndvm_grad_noalloc(const ndvm_tape *tape, const double *params, int64
                               void *stream);
 
 /*
+ * Flattened data axis (Section 3.5, named axes flattened into the batch
+ * dimension): for a loss that is a scaled sum over N data points of a
+ * per-point term, `tape` is the per-point term program, reading its point's
+ * observation row (the tape's n_obs values), and the launch runs one lane
+ * per (parameter vector, data point), L*N lanes.  Then
+ *   loss[l]         = scale * ((((0 + t_0) + t_1) + ...) + t_{N-1})
+ *   grad[l*ld_g+p]  = scale * ((((0 + g_0p) + g_1p) + ...) + g_{N-1,p})
+ * with t_i and g_i the term and its gradient along lane (l, i)'s realized
+ * trace: a left fold over the points in ascending order, then one
+ * multiplication (a second, small kernel on `stream`).
+ *   params : device fp64, element (l, p) at params[l*ld_p + p], ld_p >= P
+ *   points : device fp64, observation k of point i at points[i*ld_pt + k],
+ *            ld_pt >= the tape's n_obs
+ *   loss   : device fp64 [L];  grad : element (l, p) at grad[l*ld_g + p]
+ *   workspace : ndvm_workspace_bytes_points(tape, L, n_points) bytes (the
+ *               replay's rows for L*N lanes plus the per-point terms and term
+ *               gradients); that call prepares the launch and must precede
+ * L = 0 is a no-op.  Errors: NDVM_E_ARG (null tape or buffer, L < 0,
+ * n_points < 1, a stride too small, L*N overflowing, a lane count never
+ * prepared), NDVM_E_NOMEM (workspace too small), NDVM_E_DEVICE.
+ */
+ndvm_status ndvm_grad_points(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p,
+                             const double *points, int64_t n_points, int64_t ld_pt, double scale, double *loss,
+                             double *grad, int64_t ld_g, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes of ndvm_grad_points for L parameter vectors and n_points
+ * data points; the preparation call of that launch shape (schedules the term
+ * program for L*n_points lanes and copies it to the GPU).  Library
+ * infrastructure.  Errors: NDVM_E_ARG, NDVM_E_NOMEM, NDVM_E_DEVICE,
+ * NDVM_E_UNSUPPORTED. */
+ndvm_status ndvm_workspace_bytes_points(const ndvm_tape *tape, int64_t L, int64_t n_points, size_t *bytes);
+
+/*
  * Many programs in one launch (candidate-level parallelism of Section 6,
  * "Across cores", mapped onto the GPU grid): program q uses
  *   params : params + q*prog_stride_p, element (l, p) at [l*ld_p + p]

@@ -25,7 +25,8 @@ NOALLOC_SCRATCH_BYTES = 64 << 20    # NDVM_NOALLOC_SCRATCH_BYTES
 # exported symbols of include/ndvm.h
 EXPORTS = ["ndvm_tape_build", "ndvm_tape_upload", "ndvm_tape_info_get", "ndvm_workspace_bytes",
            "ndvm_forward", "ndvm_grad", "ndvm_grad_many", "ndvm_workspace_bytes_many",
-           "ndvm_tape_free", "ndvm_free", "ndvm_last_error", "ndvm_adam_step", "ndvm_grad_noalloc"]
+           "ndvm_tape_free", "ndvm_free", "ndvm_last_error", "ndvm_adam_step", "ndvm_grad_noalloc",
+           "ndvm_grad_points", "ndvm_workspace_bytes_points"]
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_03574_amd/build.py "
@@ -56,6 +57,9 @@ _ws_bytes_many = _sig("ndvm_workspace_bytes_many", _int, [ctypes.POINTER(_vp), _
 _forward = _sig("ndvm_forward", _int, [_vp, _vp, _i64, _i64, _vp, _i64, _vp, _vp, _sz, _vp])
 _grad = _sig("ndvm_grad", _int, [_vp, _vp, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp, _sz, _vp])
 _grad_noalloc = _sig("ndvm_grad_noalloc", _int, [_vp, _vp, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp])
+_grad_points = _sig("ndvm_grad_points", _int, [_vp, _vp, _i64, _i64, _vp, _i64, _i64, ctypes.c_double, _vp, _vp,
+                                                _i64, _vp, _sz, _vp])
+_ws_bytes_points = _sig("ndvm_workspace_bytes_points", _int, [_vp, _i64, _i64, ctypes.POINTER(_sz)])
 _grad_many = _sig("ndvm_grad_many", _int, [ctypes.POINTER(_vp), _int, _vp, _i64, _i64, _i64, _vp, _i64, _vp,
                                             _vp, _i64, _i64, _vp, _sz, _vp])
 _tape_free = _sig("ndvm_tape_free", None, [_vp])
@@ -166,6 +170,13 @@ def _dev_f64(t, name):
     return t
 
 
+def _ld(t, dim=0):
+    """Leading dimension of a row-major 2-D view: its row stride, or the row
+    length when there is only one row (torch reports any stride for a
+    dimension of size one)."""
+    return t.stride(dim) if t.shape[dim] > 1 else max(t.shape[dim + 1], 1)
+
+
 def _workspace(tape_or_bytes, device, workspace):
     import torch
     need = tape_or_bytes
@@ -190,7 +201,7 @@ def forward(tape: Tape, params, obs, loss=None, workspace=None, stream=None):
         if loss is None:
             loss = torch.empty(L, dtype=torch.float64, device=params.device)
         ws, nbytes = _workspace(need, params.device, workspace)
-        _check(_forward(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
+        _check(_forward(tape.handle, params.data_ptr(), L, _ld(params), obs.data_ptr(), obs.numel(),
                         loss.data_ptr(), ws.data_ptr(), nbytes, s.cuda_stream), "ndvm_forward")
     return loss
 
@@ -211,8 +222,8 @@ def grad(tape: Tape, params, obs, loss=None, grad_out=None, workspace=None, stre
         if grad_out is None:
             grad_out = torch.empty((L, P), dtype=torch.float64, device=params.device)
         ws, nbytes = _workspace(need, params.device, workspace)
-        _check(_grad(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
-                     loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(0), ws.data_ptr(), nbytes,
+        _check(_grad(tape.handle, params.data_ptr(), L, _ld(params), obs.data_ptr(), obs.numel(),
+                     loss.data_ptr(), grad_out.data_ptr(), _ld(grad_out), ws.data_ptr(), nbytes,
                      s.cuda_stream), "ndvm_grad")
     return loss, grad_out
 
@@ -228,9 +239,40 @@ def grad_noalloc(tape: Tape, params, obs, loss, grad_out, stream=None):
     L = params.shape[0]
     if loss.numel() < L or grad_out.shape[0] < L:
         raise ValueError("loss and grad must hold L rows")
-    _check(_grad_noalloc(tape.handle, params.data_ptr(), L, params.stride(0), obs.data_ptr(), obs.numel(),
-                         loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(0), _stream_ptr(stream)),
+    _check(_grad_noalloc(tape.handle, params.data_ptr(), L, _ld(params), obs.data_ptr(), obs.numel(),
+                         loss.data_ptr(), grad_out.data_ptr(), _ld(grad_out), _stream_ptr(stream)),
            "ndvm_grad_noalloc")
+    return loss, grad_out
+
+
+def workspace_bytes_points(tape: Tape, L: int, n_points: int) -> int:
+    n = _sz()
+    _check(_ws_bytes_points(tape.handle, L, n_points, ctypes.byref(n)), "ndvm_workspace_bytes_points")
+    return n.value
+
+
+def grad_points(tape: Tape, params, points, scale: float, loss=None, grad_out=None, workspace=None, stream=None):
+    """Flattened data axis (ndvm_grad_points): `tape` is the per-point term
+    program; points[N, D] holds each data point's observation row; returns
+    (loss[L], grad[L, P]) of scale * sum over points of the term."""
+    import torch
+    _dev_f64(params, "params")
+    _dev_f64(points, "points")
+    if params.dim() != 2 or params.stride(1) != 1 or points.dim() != 2 or points.stride(1) != 1:
+        raise ValueError("params [L, P] and points [N, D] need unit inner stride")
+    L, P = params.shape
+    N = points.shape[0]
+    need = workspace_bytes_points(tape, L, N)
+    s = _launch_stream(stream, params.device)
+    with torch.cuda.stream(s):
+        if loss is None:
+            loss = torch.empty(L, dtype=torch.float64, device=params.device)
+        if grad_out is None:
+            grad_out = torch.empty((L, P), dtype=torch.float64, device=params.device)
+        ws, nbytes = _workspace(need, params.device, workspace)
+        _check(_grad_points(tape.handle, params.data_ptr(), L, _ld(params), points.data_ptr(), N,
+                            _ld(points), float(scale), loss.data_ptr(), grad_out.data_ptr(), _ld(grad_out),
+                            ws.data_ptr(), nbytes, s.cuda_stream), "ndvm_grad_points")
     return loss, grad_out
 
 
@@ -254,9 +296,12 @@ def grad_many(tapes: Sequence[Tape], params, obs, loss=None, grad_out=None, work
             grad_out = torch.zeros((n_prog, L, P), dtype=torch.float64, device=params.device)
         ws, nbytes = _workspace(need, params.device, workspace)
         arr = (_vp * n_prog)(*[t.handle for t in tapes])
-        _check(_grad_many(arr, n_prog, params.data_ptr(), L, params.stride(1), params.stride(0), obs.data_ptr(),
-                          obs.numel(), loss.data_ptr(), grad_out.data_ptr(), grad_out.stride(1),
-                          grad_out.stride(0), ws.data_ptr(), nbytes, s.cuda_stream), "ndvm_grad_many")
+        ldp, ldg = _ld(params, 1), _ld(grad_out, 1)
+        sp = params.stride(0) if n_prog > 1 else L * ldp
+        sg = grad_out.stride(0) if n_prog > 1 else L * ldg
+        _check(_grad_many(arr, n_prog, params.data_ptr(), L, ldp, sp, obs.data_ptr(),
+                          obs.numel(), loss.data_ptr(), grad_out.data_ptr(), ldg,
+                          sg, ws.data_ptr(), nbytes, s.cuda_stream), "ndvm_grad_many")
     return loss, grad_out
 
 
@@ -272,7 +317,7 @@ def adam_step(params, grad_in, m, v, t: int, lr: float, beta1: float = 0.9, beta
     if tuple(grad_in.shape) != (L, P) or tuple(m.shape) != (L, P) or tuple(v.shape) != (L, P) \
             or not m.is_contiguous() or not v.is_contiguous():
         raise ValueError("grad, m and v must match params [L, P]; m and v contiguous")
-    _check(_adam(params.data_ptr(), grad_in.data_ptr(), m.data_ptr(), v.data_ptr(), L, P, params.stride(0),
-                 grad_in.stride(0), int(t), float(lr), float(beta1), float(beta2), float(eps),
+    _check(_adam(params.data_ptr(), grad_in.data_ptr(), m.data_ptr(), v.data_ptr(), L, P, _ld(params),
+                 _ld(grad_in), int(t), float(lr), float(beta1), float(beta2), float(eps),
                  _stream_ptr(stream)), "ndvm_adam_step")
     return params

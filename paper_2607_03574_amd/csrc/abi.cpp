@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <climits>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -22,6 +23,8 @@ hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const P
                          uint32_t r_lds, int variant, uint32_t slots, hipStream_t stream);
 bool slots_supported(uint32_t S);
 size_t scratch_bytes();
+hipError_t launch_fold_points(const double *term, const double *tgrad, int64_t L, int64_t N, int64_t P,
+                              double scale, double *loss, double *grad, int64_t ld_g, hipStream_t stream);
 hipError_t scratch_address(void **out);
 struct AdamArgs {
     double *p;
@@ -604,6 +607,85 @@ ndvm_status ndvm_grad_noalloc(const ndvm_tape *tape, const double *params, int64
     return guarded([&]() -> ndvm_status {
         return grad_impl(tape, params, L, ld_p, obs, n_obs, loss, grad, ld_g, nullptr, 0, true, stream,
                          "ndvm_grad_noalloc");
+    });
+}
+
+// Flattened data axis: L * N lanes.  Workspace: the replay's rows for L*N
+// lanes, then the per-point terms [L*N] and term gradients [L*N, P].
+static ndvm_status points_layout(const ndvm_tape *tape, int64_t L, int64_t N, bool build, DevProg **dp,
+                                 uint32_t *b, uint64_t *replay_bytes, uint64_t *total) {
+    DeviceProps p;
+    ndvm_status st = device_props(&p);
+    if (st != NDVM_OK) return st;
+    const int64_t F = L * N;
+    const uint32_t S = choose_slots(p, F, 1);
+    *b = reg_budget(p, waves_of(F, 1, S), S);
+    if ((st = grad_program(const_cast<ndvm_tape *>(tape), S, *b, build, dp)) != NDVM_OK) return st;
+    *replay_bytes = ws_rows(**dp, *b) * uint64_t(lpad_of(F)) * sizeof(double);
+    *total = *replay_bytes + uint64_t(F) * (1 + tape->tape.n_params) * sizeof(double);
+    return NDVM_OK;
+}
+
+ndvm_status ndvm_workspace_bytes_points(const ndvm_tape *tape, int64_t L, int64_t n_points, size_t *bytes) {
+    return guarded([&]() -> ndvm_status {
+        if (!tape || !bytes || L < 0 || n_points < 1 || (L > 0 && n_points > INT64_MAX / L)) {
+            set_error("ndvm_workspace_bytes_points: bad argument");
+            return NDVM_E_ARG;
+        }
+        DevProg *dp;
+        uint32_t b;
+        uint64_t rb, total;
+        ndvm_status st = points_layout(tape, L, n_points, true, &dp, &b, &rb, &total);
+        if (st != NDVM_OK) return st;
+        *bytes = size_t(total);
+        return NDVM_OK;
+    });
+}
+
+ndvm_status ndvm_grad_points(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p,
+                             const double *points, int64_t n_points, int64_t ld_pt, double scale, double *loss,
+                             double *grad, int64_t ld_g, void *ws, size_t ws_bytes, void *stream) {
+    return guarded([&]() -> ndvm_status {
+        const char *who = "ndvm_grad_points";
+        if (!tape) {
+            set_error("ndvm_grad_points: null tape");
+            return NDVM_E_ARG;
+        }
+        const int64_t P = tape->tape.n_params, D = tape->tape.n_obs;
+        if (L < 0 || n_points < 1 || ld_pt < D || ld_p < P || ld_g < P || (L > 0 && n_points > INT64_MAX / L) ||
+            (L > 0 && (!loss || (P > 0 && (!params || !grad)) || (D > 0 && !points)))) {
+            set_error(std::string(who) + ": bad lane or point count, stride or null buffer");
+            return NDVM_E_ARG;
+        }
+        if (L == 0) return NDVM_OK;
+        DevProg *dp;
+        uint32_t b;
+        uint64_t rb, total;
+        ndvm_status st = points_layout(tape, L, n_points, false, &dp, &b, &rb, &total);
+        if (st != NDVM_OK) return st;
+        if (!ws || ws_bytes < total) {
+            set_error(std::string(who) + ": workspace too small");
+            return NDVM_E_NOMEM;
+        }
+        const int64_t F = L * n_points;
+        double *wsd = static_cast<double *>(ws);
+        double *term = wsd + rb / sizeof(double), *tgrad = term + F;
+        LaunchArgs A{points, params, term, tgrad, wsd, ld_p, P, F, lpad_of(F), 0, 0, n_points, ld_pt};
+        const uint32_t r_lds = std::min(dp->meta.n_regs, b);
+        const bool spills = dp->meta.n_regs > r_lds;
+        ProgStatic D_{dp->code, dp->consts, 0, uint64_t(dp->meta.n_ckpt_rows) + slot::kMaxBlock, dp->meta.hdr_off,
+                      r_lds, spills};
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        DeviceProps pr;
+        if ((st = device_props(&pr)) != NDVM_OK) return st;
+        st = check_stream_and_launch(A, nullptr, D_, 1, r_lds, spills ? kSpill : kLdsOnly, choose_slots(pr, F, 1), s);
+        if (st != NDVM_OK) return st;
+        const hipError_t e = launch_fold_points(term, tgrad, L, n_points, P, scale, loss, grad, ld_g, s);
+        if (e != hipSuccess) {
+            set_error(std::string(who) + ": fold launch failed: " + hipGetErrorString(e));
+            return NDVM_E_DEVICE;
+        }
+        return NDVM_OK;
     });
 }
 

@@ -221,11 +221,16 @@ __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStati
     c.lane = int64_t(blockIdx.x) * LW + l;
     c.active = c.lane < A.L;
     c.lc = c.active ? c.lane : A.L - 1;
+    const AS_GLOBAL double *obs_row = (const AS_GLOBAL double *)A.obs;
+    if (A.n_points > 0) {   // flattened data axis: parameter row and data point of the lane
+        obs_row += (c.lc % A.n_points) * A.obs_stride;
+        c.lc = c.lc / A.n_points;
+    }
     c.lane_addr = uint32_t(size_t((AS_LDS double *)lds_regs + l));
     c.spill = (AS_GLOBAL double *)(A.ws + int64_t(D.spill_row0) * A.Lpad);
     c.ckpt = (AS_GLOBAL double *)(A.ws + int64_t(D.ckpt_row0) * A.Lpad);
     c.consts = (const AS_GLOBAL double *)D.consts;
-    c.obs = (const AS_GLOBAL double *)A.obs;
+    c.obs = obs_row;
     c.params = (const AS_GLOBAL double *)(A.params + int64_t(q) * A.prog_stride_p);
     c.loss = (AS_GLOBAL double *)(A.loss + int64_t(q) * A.L);
     c.grad = (AS_GLOBAL double *)(A.grad + int64_t(q) * A.prog_stride_g);
@@ -294,6 +299,39 @@ hipError_t launch_s(const LaunchArgs &A, const ProgStatic *d_table, const ProgSt
 }
 
 }  // namespace
+
+// Reduction of the flattened data axis: loss[l] = scale * left fold over the
+// points in ascending order of term[l*N + i], and likewise every gradient
+// entry; one thread per (parameter row, output), consecutive threads on the
+// outputs of one row.  Each thread reads its own N terms in order (the fold
+// order is part of the result's definition).
+__global__ void __launch_bounds__(256) ndvm_fold_points(const double *__restrict__ term,
+                                                        const double *__restrict__ tgrad, int64_t L, int64_t N,
+                                                        int64_t P, double scale, double *__restrict__ loss,
+                                                        double *__restrict__ grad, int64_t ld_g) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= L * (P + 1)) return;
+    const int64_t l = i / (P + 1), k = i % (P + 1);
+    double acc = 0.0;
+    if (k == P) {
+        const double *t = term + l * N;
+        for (int64_t j = 0; j < N; ++j) acc = acc + t[j];
+        loss[l] = acc * scale;
+    } else {
+        const double *g = tgrad + l * N * P + k;
+        for (int64_t j = 0; j < N; ++j) acc = acc + g[j * P];
+        grad[l * ld_g + k] = acc * scale;
+    }
+}
+
+hipError_t launch_fold_points(const double *term, const double *tgrad, int64_t L, int64_t N, int64_t P,
+                              double scale, double *loss, double *grad, int64_t ld_g, hipStream_t stream) {
+    const int64_t n = L * (P + 1);
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(ndvm_fold_points, dim3(uint32_t((n + 255) / 256)), dim3(256), 0, stream, term, tgrad, L, N,
+                       P, scale, loss, grad, ld_g);
+    return hipGetLastError();
+}
 
 // Slot counts the kernel is built for (micro-ops per instruction).
 bool slots_supported(uint32_t S) { return S == 4; }

@@ -144,6 +144,10 @@ enum LaunchVariant : int { kLdsOnly = 0, kSpill = 1, kPerProgram = 2 };
 
 // Per-call arguments.  Program q of a launch (blockIdx.y) reads
 // params + q*prog_stride_p and writes loss + q*L, grad + q*prog_stride_g.
+// With n_points > 0 the data axis is flattened into the lanes: lane f serves
+// parameter row f / n_points and data point f % n_points, whose observation
+// row starts at obs + (f % n_points) * obs_stride; loss[f] and
+// grad[f*ld_g + p] are then that point's term and term gradient.
 struct LaunchArgs {
     const double *obs;
     const double *params;
@@ -151,6 +155,7 @@ struct LaunchArgs {
     double *grad;
     double *ws;
     int64_t ld_p, ld_g, L, Lpad, prog_stride_p, prog_stride_g;
+    int64_t n_points = 0, obs_stride = 0;
 };
 
 }  // namespace ndvm
