@@ -195,6 +195,11 @@ def forward(tape: Tape, params, obs, loss=None, workspace=None, stream=None):
     if params.dim() != 2 or params.stride(1) != 1 or not obs.is_contiguous():
         raise ValueError("params must be [L, P] with unit inner stride; obs contiguous")
     L = params.shape[0]
+    if workspace is not None and loss is not None:     # nothing to allocate: launch directly
+        _check(_forward(tape.handle, params.data_ptr(), L, _ld(params), obs.data_ptr(), obs.numel(),
+                        loss.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                        _stream_ptr(stream)), "ndvm_forward")
+        return loss
     need = workspace_bytes(tape, L, False)
     s = _launch_stream(stream, params.device)
     with torch.cuda.stream(s):
@@ -214,6 +219,11 @@ def grad(tape: Tape, params, obs, loss=None, grad_out=None, workspace=None, stre
     if params.dim() != 2 or params.stride(1) != 1 or not obs.is_contiguous():
         raise ValueError("params must be [L, P] with unit inner stride; obs contiguous")
     L, P = params.shape
+    if workspace is not None and loss is not None and grad_out is not None:   # launch directly
+        _check(_grad(tape.handle, params.data_ptr(), L, _ld(params), obs.data_ptr(), obs.numel(),
+                     loss.data_ptr(), grad_out.data_ptr(), _ld(grad_out), workspace.data_ptr(),
+                     workspace.numel() * workspace.element_size(), _stream_ptr(stream)), "ndvm_grad")
+        return loss, grad_out
     need = workspace_bytes(tape, L, True)
     s = _launch_stream(stream, params.device)
     with torch.cuda.stream(s):
@@ -262,6 +272,11 @@ def grad_points(tape: Tape, params, points, scale: float, loss=None, grad_out=No
         raise ValueError("params [L, P] and points [N, D] need unit inner stride")
     L, P = params.shape
     N = points.shape[0]
+    if workspace is not None and loss is not None and grad_out is not None:   # launch directly
+        _check(_grad_points(tape.handle, params.data_ptr(), L, _ld(params), points.data_ptr(), N, _ld(points),
+                            float(scale), loss.data_ptr(), grad_out.data_ptr(), _ld(grad_out), workspace.data_ptr(),
+                            workspace.numel() * workspace.element_size(), _stream_ptr(stream)), "ndvm_grad_points")
+        return loss, grad_out
     need = workspace_bytes_points(tape, L, N)
     s = _launch_stream(stream, params.device)
     with torch.cuda.stream(s):

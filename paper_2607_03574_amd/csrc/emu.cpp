@@ -78,8 +78,8 @@ struct HostCtx {
     void st(uint32_t r, double v) const {
         if (r >= n_regs) { flag(1); return; }
         if (r < sink || r >= sink + slot::kMaxBlock)
-            for (const auto &pw : *pending)
-                if (pw.first == r) flag(7);
+            for (size_t i = 0; i < pending->size(); ++i)
+                if ((*pending)[i].first == r && (*pend_slot)[i] != cur_slot) flag(7);
         pending->push_back({r, v});
         pend_slot->push_back(cur_slot);
     }
@@ -186,7 +186,8 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
                 const uint32_t *w = &S.code[size_t(i / K) * slot::kChunkWords + (size_t(r) * K + i % K) * 4];
                 const P4 p{{w[0], w[1], w[2], w[3]}, hdr, sl, reg_bytes};
                 c.cur_slot = sl;
-                c.cur_dummy = (slot::writes_a(form) && p.a() == sink) || (form == slot::CKST && p.ix() == S.n_ckpt_rows);
+                c.cur_dummy = (slot::writes_a(form) && p.a() == sink) ||
+                              (form == slot::CKST && (p.ix() & slot::kCkRowMask) == S.n_ckpt_rows);
                 if (slot::is_hot(form))
                     slotx::exec_hot(c, form, p);
                 else

@@ -682,6 +682,13 @@ struct UOp {
     uint32_t f[4];
 };
 
+// index field of a checkpoint move of n rows from `row` on
+uint32_t ck_row(uint32_t row, uint32_t n) {
+    if (row > slot::kCkRowMask || n == 0 || n > slot::kMaxCk)
+        throw std::length_error("checkpoint row beyond the index field of the device program");
+    return slot::ck_field(row, n);
+}
+
 // Keys of what a micro-op reads and writes: registers r, checkpoint rows
 // kKeyCkpt + row, the loss, gradient entries kKeyGrad + p.
 constexpr uint64_t kKeyCkpt = 1ull << 32, kKeyLoss = 2ull << 32, kKeyGrad = 3ull << 32;
@@ -758,14 +765,14 @@ void uop_access(const UOp &u, std::vector<uint64_t> &rd, std::vector<uint64_t> &
         wr = {a};
         break;
     case CKST:
-        for (uint32_t k = 0; k < im; ++k) {
+        for (uint32_t k = 0; k <= (x >> kCkRowBits); ++k) {
             rd.push_back(a + k);
-            wr.push_back(kKeyCkpt + x + k);
+            wr.push_back(kKeyCkpt + (x & kCkRowMask) + k);
         }
         break;
     case CKLD:
-        for (uint32_t k = 0; k < im; ++k) {
-            rd.push_back(kKeyCkpt + x + k);
+        for (uint32_t k = 0; k <= (x >> kCkRowBits); ++k) {
+            rd.push_back(kKeyCkpt + (x & kCkRowMask) + k);
             wr.push_back(a + k);
         }
         break;
@@ -1199,8 +1206,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             uint32_t row = ckrow_base[a.k];
             for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
             const uint32_t src = fwd_operand(s);
-            for (uint32_t e = 0; e < I.nel[s]; e += kMaxBlock)
-                E.put(CKST, src + e, 0, row + e, 0, 0, std::min(kMaxBlock, I.nel[s] - e));
+            for (uint32_t e = 0; e < I.nel[s]; e += kMaxCk)
+                E.put(CKST, src + e, 0, ck_row(row + e, std::min(kMaxCk, I.nel[s] - e)));
             Sch.ckpt_elems_stored += I.nel[s];
             break;
         }
@@ -1225,8 +1232,25 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
         std::vector<AI> ra;
         ra.push_back({I_ZEROP, 0, 0});
         ra.push_back({I_SEED, t.loss, 0});
+        // Checkpoint restores wait for HBM inside their instruction, so the
+        // restores of consecutive segments are issued together when their
+        // moves fit one instruction (S slots): the later segments' values
+        // then wait in registers while the earlier segment runs.
+        auto ck_moves = [&](uint32_t j) {
+            uint32_t n = 0;
+            for (uint32_t s : B.livein[j]) n += (I.nel[s] + kMaxCk - 1) / kMaxCk;
+            return n;
+        };
+        std::vector<uint8_t> restored(m, 0);
         for (uint32_t j = m; j-- > 0;) {
-            for (uint32_t i = 0; i < B.livein[j].size(); ++i) ra.push_back({I_CKLD, j, i});
+            if (!restored[j]) {
+                uint32_t moves = ck_moves(j), last = j;
+                while (last > 0 && moves + ck_moves(last - 1) <= S && ck_moves(last - 1) > 0) moves += ck_moves(--last);
+                for (uint32_t q = j + 1; q-- > last;) {
+                    for (uint32_t i = 0; i < B.livein[q].size(); ++i) ra.push_back({I_CKLD, q, i});
+                    restored[q] = 1;
+                }
+            }
             for (uint32_t s : B.recomp[j]) ra.push_back({I_FWD, s, j});
             for (uint32_t k : B.revops[j]) ra.push_back({I_REV, k, j});
         }
@@ -1624,8 +1648,8 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                 uint32_t row = ckrow_base[a.k];
                 for (uint32_t i = 0; i < a.j; ++i) row += I.nel[B.livein[a.k][i]];
                 const uint32_t dst = rev_operand(s, a.k);
-                for (uint32_t e = 0; e < I.nel[s]; e += kMaxBlock)
-                    E.put(CKLD, dst + e, 0, row + e, 0, 0, std::min(kMaxBlock, I.nel[s] - e));
+                for (uint32_t e = 0; e < I.nel[s]; e += kMaxCk)
+                    E.put(CKLD, dst + e, 0, ck_row(row + e, std::min(kMaxCk, I.nel[s] - e)));
                 Sch.ckpt_elems_loaded += I.nel[s];
                 break;
             }
@@ -1694,11 +1718,16 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
         const uint32_t f = u0.form;
         uint32_t hdr = f | u0.imm << kImmShift;
         if (f == STLOSS || f == STGRAD) hdr = f | cnt << kImmShift;
+        if (is_ckmove(f)) {   // the largest row count of the instruction's slots
+            uint32_t mx = 1;
+            for (uint32_t sl = 0; sl < cnt; ++sl) mx = std::max(mx, (flat[first + sl].f[1] >> kCkRowBits) + 1);
+            hdr = f | mx << kImmShift;
+        }
         for (uint32_t sl = 0; sl < S; ++sl) {
             UOp u = sl < cnt ? flat[first + sl] : u0;
             if (sl >= cnt) {
                 if (writes_a(f)) u.f[0] = kSink;
-                if (f == CKST) u.f[1] = trash_row;
+                if (is_ckmove(f)) u.f[0] = kSink, u.f[1] = ck_row(trash_row, 1);
                 u.flags = 0;
             }
             hdr |= (u.flags & kUFirst ? 1u : 0u) << (kFirstShift + sl);

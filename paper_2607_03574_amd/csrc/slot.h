@@ -67,8 +67,8 @@ enum Form : uint32_t {
     LDOBS,      // d = obs[x]
     LDPARAM,   // d = params[lane, x]
     LDCONST,   // d = consts[x]
-    CKST,      // ckpt rows x .. x + n - 1 of this lane = registers a .. a + n - 1  (imm = n)
-    CKLD,      // registers a .. a + n - 1 = ckpt rows x .. x + n - 1 of this lane
+    CKST,      // ckpt rows r .. r + n - 1 of this lane = registers a .. a + n - 1   (x = ck_field(r, n))
+    CKLD,      // registers a .. a + n - 1 = ckpt rows r .. r + n - 1 of this lane   (x = ck_field(r, n))
     MSUB,      // d = x * y - z  (product rounded, then difference rounded)
     RSUB,      // d = z - x * y  (product rounded, then difference rounded)
     HOT_END,
@@ -87,6 +87,18 @@ constexpr uint32_t kFormMask = 63u;
 constexpr uint32_t kFirstShift = 6, kImmShift = 14;
 constexpr uint32_t kMaxImm = (1u << 18) - 1;
 constexpr uint32_t kMaxBlock = 4;            // outputs of a block form (sink and trash rows reserved)
+
+// Checkpoint moves (CKST, CKLD) carry their own row count per slot, up to
+// kMaxCk rows, in the index field: x = row | (n - 1) << kCkRowBits; the
+// header immediate is the largest count of the instruction's slots, and a
+// slot with fewer rows repeats its last move (same register, same row, same
+// value), so every slot runs the same uniform loop.  Slots an instruction
+// does not use move one row between a sink register and a trash row.
+constexpr uint32_t kMaxCk = 16;
+constexpr uint32_t kCkRowBits = 28;
+constexpr uint32_t kCkRowMask = (1u << kCkRowBits) - 1;
+inline uint32_t ck_field(uint32_t row, uint32_t n) { return row | (n - 1) << kCkRowBits; }
+inline bool is_ckmove(uint32_t form) { return form == CKST || form == CKLD; }
 
 // immediates: DOT / DOTACC: K | negate << 5 | sa << 6 | sb << 12;
 // DOTB / DOTBACC: K | N << 3 | sx << 6 | sy << 9 | sc << 12 | negate << 15

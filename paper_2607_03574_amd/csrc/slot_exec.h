@@ -367,33 +367,33 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         c.st(p.a(), c.konst(p.ix()));
         return;
     case CKST: {   // all loads issued before the first store
-        const uint32_t n = p.imm(), row = p.ix();
+        const uint32_t m = p.imm(), f = p.ix(), row = f & kCkRowMask, n1 = f >> kCkRowBits;
         const auto a = p.a();
-        double v[kMaxBlock];
+        double v[kMaxCk];
 #pragma unroll
-        for (uint32_t k = 0; k < kMaxBlock; ++k)
-            if (k < n) v[k] = c.ld(c.adv(a, k));
+        for (uint32_t k = 0; k < kMaxCk; ++k)
+            if (k < m) v[k] = c.ld(c.adv(a, k < n1 ? k : n1));
 #pragma unroll
-        for (uint32_t k = 0; k < kMaxBlock; ++k)
-            if (k < n) c.ckst(row + k, v[k]);
+        for (uint32_t k = 0; k < kMaxCk; ++k)
+            if (k < m) c.ckst(row + (k < n1 ? k : n1), v[k]);
 #pragma unroll
-        for (uint32_t k = 0; k < kMaxBlock; ++k) c.settle(v[k]);
+        for (uint32_t k = 0; k < kMaxCk; ++k) c.settle(v[k]);
         return;
     }
     case CKLD: {   // all loads issued before the first write
-        const uint32_t n = p.imm(), row = p.ix();
+        const uint32_t m = p.imm(), f = p.ix(), row = f & kCkRowMask, n1 = f >> kCkRowBits;
         const auto a = p.a();
-        double v[kMaxBlock];
+        double v[kMaxCk];
 #pragma unroll
-        for (uint32_t k = 0; k < kMaxBlock; ++k)
-            if (k < n) v[k] = c.ckld(row + k);
+        for (uint32_t k = 0; k < kMaxCk; ++k)
+            if (k < m) v[k] = c.ckld(row + (k < n1 ? k : n1));
 #pragma unroll
-        for (uint32_t k = 0; k < kMaxBlock; ++k)
-            if (k < n) c.st(c.adv(a, k), v[k]);
+        for (uint32_t k = 0; k < kMaxCk; ++k)
+            if (k < m) c.st(c.adv(a, k < n1 ? k : n1), v[k]);
         // every path leaves with all loads landed, so the next handler does
         // not wait for the program prefetch before its own register reads
 #pragma unroll
-        for (uint32_t k = 0; k < kMaxBlock; ++k) c.settle(v[k]);
+        for (uint32_t k = 0; k < kMaxCk; ++k) c.settle(v[k]);
         return;
     }
     default:
