@@ -174,7 +174,10 @@ def build_flattened(name, torch, device):
     return w, step, L * len(tapes), meta, host
 
 
-def build_inputs(name, torch, device):
+POLICIES = {"recompute": 2, "save": 1}   # NDVM_POLICY_RECOMPUTE, NDVM_POLICY_SAVE
+
+
+def build_inputs(name, torch, device, policy="recompute"):
     """The workload's device inputs and one step.  Also times the host work
     per program that the lane-gradient rate leaves out: trace production
     (bytecode -> tape), upload (validation, copy) and scheduling for the
@@ -187,7 +190,7 @@ def build_inputs(name, torch, device):
     t0 = time.perf_counter()
     tapes_b = [nd.tape_build(bc) for bc in bcs]
     t1 = time.perf_counter()
-    tapes = [nd.tape_upload(t) for t in tapes_b]
+    tapes = [nd.tape_upload(t, policy=POLICIES[policy]) for t in tapes_b]
     t2 = time.perf_counter()
     if name == "random_programs":
         n_prog, L, P = p.shape
@@ -197,7 +200,8 @@ def build_inputs(name, torch, device):
         ws_bytes = nd.workspace_bytes(tapes[0], L, True)
     t3 = time.perf_counter()
     host = {"trace_us_per_program": (t1 - t0) / n_prog * 1e6, "upload_us_per_program": (t2 - t1) / n_prog * 1e6,
-            "schedule_us_per_program": (t3 - t2) / n_prog * 1e6, "total_host_s": t3 - t0, "programs": n_prog}
+            "schedule_us_per_program": (t3 - t2) / n_prog * 1e6, "total_host_s": t3 - t0, "programs": n_prog,
+            "workspace_bytes": int(ws_bytes)}
     ws = torch.empty(max(ws_bytes, 8), dtype=torch.uint8, device=device)
     flops = sum(tape_flops(t) for t in tapes_b) * L
     if name == "random_programs":
@@ -370,6 +374,9 @@ def main():
     ap.add_argument("--workload", default=None, choices=configs.ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true", help="lane sweep 2^12 .. 2^18 of the workload")
+    ap.add_argument("--policy", default="recompute", choices=sorted(POLICIES),
+                    help="save policy of the reverse sweep: recompute (segment inputs stored, values recomputed) "
+                         "or save (every value the adjoint rules read stored)")
     ap.add_argument("--flatten", action="store_true",
                     help="data axis flattened into the lanes (exp_decay, random_programs), against the unflattened step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -405,7 +412,7 @@ def main():
     device = torch.device("cuda:0")
     stream = torch.cuda.Stream(device=device)
     with torch.cuda.stream(stream):
-        w, step, lanes, flops, meta, progs, host = build_inputs(args.workload, torch, device)
+        w, step, lanes, flops, meta, progs, host = build_inputs(args.workload, torch, device, args.policy)
     torch.cuda.synchronize()
     res = time_steps(torch, stream, step, args.steps, args.warmup)
     kern_s = res["kernel_mean_s"]
@@ -416,6 +423,14 @@ def main():
     B = alg_bytes(args.workload, meta.get("lanes", meta.get("lanes_per_program")), meta.get("params", 0),
                   meta.get("programs", 1)) if args.workload != "random_programs" else \
         float(sum(8 * (2 * P + 1) for P in progs[2]) * meta["lanes_per_program"])
+    if args.policy == "save" and args.workload != "random_programs":
+        # the save policy needs a store and a load of every value the adjoint
+        # rules read: the schedule's checkpoint rows (workspace rows less the
+        # trash rows; no spills at these budgets)
+        L, P = meta["lanes"], meta["params"]
+        rows = host["workspace_bytes"] // (8 * ((L + 63) // 64 * 64)) - 4
+        B = float(L * (8 * (2 * P + 1) + 16 * rows))
+        meta["saved_doubles_per_lane"] = int(rows)
     roof = roofline(B, flops, kern_s, profiled_traffic(args.workload))
     roof.update(kernel="ndvm_replay", kernel_ms=kern_s * 1e3, kernel_ms_median=res["kernel_median_s"] * 1e3,
                 kernel_ms_iqr=res["kernel_iqr_s"] * 1e3)
@@ -424,7 +439,7 @@ def main():
         "value": value, "unit": "lane-gradient evals/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
-        "config": dict(workload=w.name, policy="recompute", **meta),
+        "config": dict(workload=w.name, policy=args.policy, **meta),
         "roofline": roof,
         "host": host,
         "env": env_info(torch),

@@ -72,8 +72,14 @@ typedef enum {
     NDVM_E_INTERNAL = 8         /* a fault inside the library (a bug), not a caller error */
 } ndvm_status;
 
-/* Save policies for the reverse sweep (argument `policy` of ndvm_tape_upload). */
-#define NDVM_POLICY_RECOMPUTE 2  /* checkpoint segment inputs, recompute inside segments */
+/* Save policies for the reverse sweep (argument `policy` of ndvm_tape_upload;
+ * Section 3.4: the tape keeps the payloads the reverse sweep reads).  Both
+ * give the same bits: a recomputed value is computed by the same operations
+ * on the same inputs as the stored one. */
+#define NDVM_POLICY_SAVE 1       /* store every value an adjoint rule reads when the forward sweep computes it;
+                                    the reverse sweep restores them and recomputes nothing */
+#define NDVM_POLICY_RECOMPUTE 2  /* store segment inputs only; each segment's reverse sweep recomputes the
+                                    values its rules read from them */
 
 typedef struct {
     uint32_t n_params;    /* P: parameters per lane */
@@ -102,7 +108,8 @@ ndvm_status ndvm_tape_build(const uint8_t *bytecode, size_t bytecode_len,
  * Validate a serialized tape (host bytes), schedule it for the device and
  * copy the device program to GPU memory on `stream` (Section 3.4 replay;
  * the schedule decides register placement, checkpoint segments and what is
- * recomputed in the reverse sweep).  `policy` is NDVM_POLICY_RECOMPUTE.
+ * recomputed in the reverse sweep).  `policy` is NDVM_POLICY_SAVE or
+ * NDVM_POLICY_RECOMPUTE.
  * On success *out receives a handle owned by the library.
  * Errors: NDVM_E_ARG, NDVM_E_TAPE (malformed tape), NDVM_E_NOMEM,
  * NDVM_E_DEVICE, NDVM_E_UNSUPPORTED (unknown policy).

@@ -19,7 +19,8 @@ OK, E_ARG, E_BYTECODE, E_STRUCT_DIVERGE, E_TAPE, E_NOMEM, E_DEVICE, E_UNSUPPORTE
 STATUS_NAMES = {0: "NDVM_OK", 1: "NDVM_E_ARG", 2: "NDVM_E_BYTECODE", 3: "NDVM_E_STRUCT_DIVERGE",
                 4: "NDVM_E_TAPE", 5: "NDVM_E_NOMEM", 6: "NDVM_E_DEVICE", 7: "NDVM_E_UNSUPPORTED",
                 8: "NDVM_E_INTERNAL"}
-POLICY_RECOMPUTE = 2
+POLICY_SAVE = 1        # store what the reverse sweep reads, recompute nothing
+POLICY_RECOMPUTE = 2   # store segment inputs, recompute inside segments
 NOALLOC_SCRATCH_BYTES = 64 << 20    # NDVM_NOALLOC_SCRATCH_BYTES
 
 # exported symbols of include/ndvm.h

@@ -194,7 +194,8 @@ ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, bool build, De
     if (it == tape->grad.end()) {
         const hipStream_t stream = nullptr;
         Schedule sch;
-        ndvm_status st = scheduled([&] { return schedule_grad(tape->tape, b, S); }, &sch);
+        ndvm_status st = scheduled(
+            [&] { return schedule_grad(tape->tape, b, S, tape->policy == NDVM_POLICY_SAVE); }, &sch);
         if (st != NDVM_OK) return st;
         std::unique_ptr<DevProg> dp;
         st = upload_program(std::move(sch), tape->tape, stream, &dp);
@@ -394,7 +395,7 @@ ndvm_status ndvm_tape_upload(const uint8_t *bytes, size_t len, int policy, void 
             set_error("ndvm_tape_upload: null argument");
             return NDVM_E_ARG;
         }
-        if (policy != NDVM_POLICY_RECOMPUTE) {
+        if (policy != NDVM_POLICY_RECOMPUTE && policy != NDVM_POLICY_SAVE) {
             set_error("ndvm_tape_upload: unsupported save policy");
             return NDVM_E_UNSUPPORTED;
         }

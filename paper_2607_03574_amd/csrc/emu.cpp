@@ -55,8 +55,12 @@ struct HostCtx {
 
     static uint32_t uni(uint32_t x) { return x; }
     uint32_t slot() const { return cur_slot; }
-    void flag(int code) const {
-        if (*fault == 0) *fault = code;
+    uint32_t *fault_reg = nullptr;   // register of the first fault (when it concerns one)
+    void flag(int code, uint32_t r = 0xFFFFFFFFu) const {
+        if (*fault == 0) {
+            *fault = code;
+            if (fault_reg) *fault_reg = r;
+        }
     }
     void check_pending_read(uint32_t r) const {
         if (cur_dummy) return;
@@ -67,7 +71,7 @@ struct HostCtx {
     double ld(uint32_t r) const {
         if (r >= n_regs) { flag(1); return NAN; }
         check_pending_read(r);
-        if (!written[r]) flag(2);
+        if (!written[r] && !cur_dummy) flag(2, r);   // an unused slot may read an unwritten sink
         return regs[r];
     }
     double ld_raw(uint32_t r) const {
@@ -122,8 +126,9 @@ struct HostCtx {
     }
 };
 
+// with_grad: 0 forward only, 1 gradient (recompute policy), 2 gradient (save policy)
 Schedule schedule(const Tape &t, int with_grad, uint32_t reg_budget, uint32_t slots) {
-    return with_grad ? schedule_grad(t, reg_budget, slots) : schedule_forward(t, slots, reg_budget);
+    return with_grad ? schedule_grad(t, reg_budget, slots, with_grad == 2) : schedule_forward(t, slots, reg_budget);
 }
 
 }  // namespace
@@ -172,10 +177,15 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
                   uint32_t(S.consts.size()), uint32_t(n_obs), t.n_params, loss + l,
                   grad ? grad + l * ld_g : nullptr, ck.data(), S.n_ckpt_rows + slot::kMaxBlock, &fault, 0, false, &pending,
                   &pend_slot};
+        uint32_t fault_reg = 0xFFFFFFFFu, fault_form = 0;
+        uint64_t fault_instr = 0;
+        c.fault_reg = &fault_reg;
         bool ended = false;
         for (uint64_t i = 0; i < uint64_t(S.n_chunks) * K && !ended && !fault; ++i) {
             const uint32_t hdr = S.code[S.hdr_off + i];
             const uint32_t form = hdr & slot::kFormMask;
+            fault_instr = i;
+            fault_form = form;
             if (form == slot::END) {
                 ended = true;
                 break;
@@ -197,8 +207,9 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
         }
         if (!ended && !fault) fault = 5;
         if (fault) {
-            char m[96];
-            std::snprintf(m, sizeof m, "emulator fault %d in lane %lld", fault, (long long)l);
+            char m[160];
+            std::snprintf(m, sizeof m, "emulator fault %d in lane %lld at instruction %llu (form %u), register %u",
+                          fault, (long long)l, (unsigned long long)fault_instr, fault_form, fault_reg);
             set_error(m);
             return 100 + fault;
         }

@@ -357,6 +357,9 @@ struct Builder {
     std::vector<std::vector<uint32_t>> livein, recomp, revops;
     std::vector<uint32_t> res_off;    // resident slot -> offset in resident block
     uint32_t res_elems = 0;
+    // save policy: values the adjoint rules read are stored in the forward
+    // sweep (as segment inputs of their own segment) instead of recomputed
+    bool save_reads = false;
 
     explicit Builder(const Info &info) : I(info), t(info.t), N(info.N), P(info.P) {}
 
@@ -388,7 +391,7 @@ struct Builder {
                     return;
                 }
                 if (I.kind[s] != K_COMP || resident[s]) return;
-                if (s >= lo) {
+                if (s >= lo && !save_reads) {
                     if (mark[s] != j) { mark[s] = j; stack.push_back(s); }
                 } else if (inmark[s] != j) {
                     inmark[s] = j;
@@ -997,7 +1000,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
     fa.push_back({I_LDC, 0, nc});
     uint32_t next_cut = 1;
     for (uint32_t k = 0; k < N; ++k) {
-        if (with_grad) {
+        if (with_grad && !B.save_reads) {
             while (next_cut < m && B.cuts[next_cut] == k) {
                 for (uint32_t i = 0; i < B.livein[next_cut].size(); ++i) fa.push_back({I_CKST, next_cut, i});
                 ++next_cut;
@@ -1007,6 +1010,25 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
     }
     fa.push_back({I_STLOSS, t.loss, 0});
     fa = bundle_forward(I, fa);
+    if (with_grad && B.save_reads) {
+        // save policy: every stored value is stored right after the forward
+        // instruction that computes it, so no value stays live for its store
+        std::unordered_map<uint32_t, std::vector<std::pair<uint32_t, uint32_t>>> saves_of;
+        for (uint32_t j = 0; j < m; ++j)
+            for (uint32_t i = 0; i < B.livein[j].size(); ++i) saves_of[B.livein[j][i]].push_back({j, i});
+        std::vector<AI> out;
+        out.reserve(fa.size() + saves_of.size());
+        for (const AI &a : fa) {
+            out.push_back(a);
+            if (a.kind != I_FWD) continue;
+            for (uint32_t b = 0; b < a.nops(); ++b) {
+                auto it = saves_of.find(a.op(b));
+                if (it == saves_of.end()) continue;
+                for (const auto &ji : it->second) out.push_back({I_CKST, ji.first, ji.second});
+            }
+        }
+        fa = std::move(out);
+    }
     std::vector<Interval> fiv;
     std::vector<int32_t> fiv_of(N, -1);
     for (uint32_t ti = 0; ti < fa.size(); ++ti) {
@@ -1768,7 +1790,7 @@ Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget) {
     return build_fit(I, B, false, slots, reg_budget, true);
 }
 
-Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
+Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots, bool save_reads) {
     Info I(t);
     I.analyse();
     uint64_t total = 0;
@@ -1778,6 +1800,7 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots) {
     // the search sizes registers only; the chosen size is built in full
     auto trial = [&](uint64_t S, bool full = false) {
         Builder B(I);
+        B.save_reads = save_reads;
         B.resident.assign(I.N, 0);
         B.res_off.assign(I.N, 0);
         B.set_cuts(B.choose_cuts(S));

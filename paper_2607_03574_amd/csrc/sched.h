@@ -29,7 +29,10 @@ Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget);
 
 // Forward + reverse program (loss[L], grad[L, P]); cuts the tape into
 // checkpoint segments so that the lane register file fits `reg_budget`
-// registers when possible.
-Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots);
+// registers when possible.  With save_reads, every value an adjoint rule
+// reads is stored when the forward sweep computes it and restored for its
+// segment's reverse sweep, so nothing is recomputed; otherwise only segment
+// inputs are stored and each segment recomputes what its rules read.
+Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots, bool save_reads = false);
 
 }  // namespace ndvm

@@ -32,14 +32,17 @@ STATS = ["n_regs", "n_ckpt_rows", "n_segments", "n_instr", "fwd_ops", "recompute
          "ckpt_stored", "n_uops", "slots_used"]
 
 
-def run(tape: bytes, params, obs, with_grad=True, budget=320, slots=4):
+def run(tape: bytes, params, obs, with_grad=True, budget=320, slots=4, save=False):
+    """with_grad: gradient program (loss and grad); save: the save policy
+    (values the adjoint rules read are stored, nothing recomputed)."""
     params = np.ascontiguousarray(params, dtype=np.float64)
     obs = np.ascontiguousarray(obs, dtype=np.float64)
     L, P = params.shape
     loss = np.empty(L)
     grad = np.empty((L, P)) if with_grad else None
     stats = (ctypes.c_uint64 * 10)()
-    rc = lib().ndvm_emu_run(tape, len(tape), int(with_grad), budget, slots, params.ctypes.data, L, P,
+    mode = (2 if save else 1) if with_grad else 0
+    rc = lib().ndvm_emu_run(tape, len(tape), mode, budget, slots, params.ctypes.data, L, P,
                             obs.ctypes.data, obs.size, loss.ctypes.data,
                             grad.ctypes.data if grad is not None else None, P, stats)
     if rc != 0:
@@ -47,16 +50,17 @@ def run(tape: bytes, params, obs, with_grad=True, budget=320, slots=4):
     return loss, grad, dict(zip(STATS, list(stats)))
 
 
-def program(tape: bytes, with_grad=True, budget=320, slots=4):
+def program(tape: bytes, with_grad=True, budget=320, slots=4, save=False):
     """The scheduled device program in instruction order: (headers[n_instr],
     words[n_instr, 4 rows, 4]) as uint32 arrays (padding after END included).
     The device layout is chunk-major ([chunk][row][instr][4] words), then the
     header words."""
-    n = lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, slots, None, 0, None)
+    mode = (2 if save else 1) if with_grad else 0
+    n = lib().ndvm_emu_program(tape, len(tape), mode, budget, slots, None, 0, None)
     assert n >= 0, lib().ndvm_emu_error()
     out = np.empty(n, dtype=np.uint32)
     hdr_off = ctypes.c_uint32(0)
-    lib().ndvm_emu_program(tape, len(tape), int(with_grad), budget, slots, out.ctypes.data, n,
+    lib().ndvm_emu_program(tape, len(tape), mode, budget, slots, out.ctypes.data, n,
                            ctypes.byref(hdr_off))
     k = hdr_off.value
     words = out[:k].reshape(-1, 4, 4, 4).transpose(0, 2, 1, 3).reshape(-1, 4, 4)

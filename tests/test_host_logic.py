@@ -145,6 +145,21 @@ def test_emulated_programs_match_oracle(oracle_mod, name, kw, budget):
         assert st["n_segments"] > 1
 
 
+@pytest.mark.parametrize("name,kw", CASES)
+@pytest.mark.parametrize("budget", [320, 48])
+def test_emulated_save_policy_equals_recompute(oracle_mod, name, kw, budget):
+    """The save policy (every value an adjoint rule reads stored, nothing
+    recomputed) gives the recompute policy's bits, and recomputes nothing."""
+    w = configs.build(name, **kw)
+    tape = nd.tape_build(w.bytecode)
+    lr, gr, _ = emu.run(tape, w.params, w.obs, True, budget)
+    ls, gs, st = emu.run(tape, w.params, w.obs, True, budget, save=True)
+    assert lr.tobytes() == ls.tobytes() and gr.tobytes() == gs.tobytes()
+    assert st["recompute_ops"] <= st["fwd_ops"] // 10 + 64   # observation reloads only
+    lo, go, _ = oracle_mod.run(w.bytecode, w.params, w.obs)
+    assert lane_rel_err(gs, go).max() <= 1e-13
+
+
 def test_emulated_random_programs_match_oracle(oracle_mod):
     w = configs.random_programs(n_prog=24, L=8, n=8, seed=99)
     for i, bc in enumerate(w.programs):
