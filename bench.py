@@ -177,7 +177,7 @@ def build_flattened(name, torch, device):
 POLICIES = {"recompute": 2, "save": 1}   # NDVM_POLICY_RECOMPUTE, NDVM_POLICY_SAVE
 
 
-def build_inputs(name, torch, device, policy="recompute"):
+def build_inputs(name, torch, device, policy="recompute", branch_skip=False):
     """The workload's device inputs and one step.  Also times the host work
     per program that the lane-gradient rate leaves out: trace production
     (bytecode -> tape), upload (validation, copy) and scheduling for the
@@ -190,7 +190,7 @@ def build_inputs(name, torch, device, policy="recompute"):
     t0 = time.perf_counter()
     tapes_b = [nd.tape_build(bc) for bc in bcs]
     t1 = time.perf_counter()
-    tapes = [nd.tape_upload(t, policy=POLICIES[policy]) for t in tapes_b]
+    tapes = [nd.tape_upload(t, policy=POLICIES[policy] | (nd.BRANCH_SKIP if branch_skip else 0)) for t in tapes_b]
     t2 = time.perf_counter()
     if name == "random_programs":
         n_prog, L, P = p.shape
@@ -377,6 +377,11 @@ def main():
     ap.add_argument("--policy", default="recompute", choices=sorted(POLICIES),
                     help="save policy of the reverse sweep: recompute (segment inputs stored, values recomputed) "
                          "or save (every value the adjoint rules read stored)")
+    ap.add_argument("--branch-skip", action="store_true",
+                    help="tapes uploaded with the BRANCH_SKIP option (waves skip branch arms none of their lanes takes)")
+    ap.add_argument("--branch-study", action="store_true",
+                    help="branch skipping on programs with heavy arms: lanes ordered by the predicate or "
+                         "interleaved, with and without the option")
     ap.add_argument("--flatten", action="store_true",
                     help="data axis flattened into the lanes (exp_decay, random_programs), against the unflattened step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -409,10 +414,15 @@ def main():
         return sweep(args, torch)
     if args.flatten:
         return flattened_bench(args, torch)
+    if args.branch_study:
+        return branch_study(args, torch)
     device = torch.device("cuda:0")
     stream = torch.cuda.Stream(device=device)
     with torch.cuda.stream(stream):
-        w, step, lanes, flops, meta, progs, host = build_inputs(args.workload, torch, device, args.policy)
+        w, step, lanes, flops, meta, progs, host = build_inputs(args.workload, torch, device, args.policy,
+                                                                args.branch_skip)
+    if args.branch_skip:
+        meta["branch_skip"] = True
     torch.cuda.synchronize()
     res = time_steps(torch, stream, step, args.steps, args.warmup)
     kern_s = res["kernel_mean_s"]
@@ -471,6 +481,42 @@ def flattened_bench(args, torch):
            "speedup": ures["wall_s"] / res["wall_s"], "dtype": "f64", "data": "synthetic",
            "config": meta, "host": host, "steps": args.steps, "warmup": args.warmup}
     print(json.dumps(out), flush=True)
+
+
+def branch_study(args, torch):
+    """Wave-level branch skipping on tree programs with heavy arms (16,384
+    and 65,536 lanes, 128 points): the same lanes ordered by the branch's
+    predicate (waves decide alike) or interleaved (every wave runs both
+    arms), and populations whose lanes all take one arm, each with and
+    without the BRANCH_SKIP option; one JSON line per run."""
+    import paper_2607_03574_amd as nd
+    device = torch.device("cuda:0")
+    stream = torch.cuda.Stream(device=device)
+    runs = [(c, n_l, o) for n_l in (16384, 65536) for c in range(len(configs.BRANCH_TREES))
+            for o in ("sorted", "mixed", "all_then", "all_else")]
+    for case, n_lanes, order in runs:
+        w = configs.branch_population(case, L=n_lanes, order=order)
+        L, P = w.params.shape
+        tb = nd.tape_build(w.bytecode)
+        for skip in (False, True):
+            with torch.cuda.stream(stream):
+                tape = nd.tape_upload(tb, policy=nd.POLICY_RECOMPUTE | (nd.BRANCH_SKIP if skip else 0))
+                p = torch.tensor(w.params, device=device)
+                o = torch.tensor(w.obs, device=device)
+                ws = torch.empty(max(nd.workspace_bytes(tape, L, True), 8), dtype=torch.uint8, device=device)
+                loss = torch.empty(L, dtype=torch.float64, device=device)
+                grad = torch.empty((L, P), dtype=torch.float64, device=device)
+            torch.cuda.synchronize()
+
+            def step(s):
+                nd.grad(tape, p, o, loss, grad, ws, s)
+            res = time_steps(torch, stream, step, args.steps, args.warmup)
+            t = res["kernel_mean_s"]
+            print(json.dumps({"study": "branch_skip", "case": case, "order": order, "branch_skip": skip,
+                              "lanes": L, "points": w.meta["n"], "kernel_ms": t * 1e3,
+                              "kernel_ms_median": res["kernel_median_s"] * 1e3,
+                              "lane_grads_per_s": L / t}), flush=True)
+            del tape, ws
 
 
 def time_steps(torch, stream, step, steps, warmup):

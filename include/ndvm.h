@@ -80,6 +80,17 @@ typedef enum {
                                     the reverse sweep restores them and recomputes nothing */
 #define NDVM_POLICY_RECOMPUTE 2  /* store segment inputs only; each segment's reverse sweep recomputes the
                                     values its rules read from them */
+/* Option OR'd into `policy`: wave-level branch skipping (Section 6 lane
+ * masking, decided per wave).  The arm of a numeric branch that only that
+ * arm's select reads is laid out behind a skip test; a wave in which every
+ * lane decides the branch the other way does not run the arm, in the forward
+ * sweep or the reverse sweep.  Results are bit for bit those without the
+ * option (a skipped arm would only have produced values the selects discard
+ * and adjoint contributions of exactly zero).  It pays when the lanes of a
+ * wave (64 / slots consecutive lanes) tend to decide alike, e.g. a population
+ * ordered by the branch's predicate; with lanes that decide at random it
+ * costs a few percent (the skip tests, and arms packed apart). */
+#define NDVM_BRANCH_SKIP 0x100
 
 typedef struct {
     uint32_t n_params;    /* P: parameters per lane */
@@ -109,7 +120,7 @@ ndvm_status ndvm_tape_build(const uint8_t *bytecode, size_t bytecode_len,
  * copy the device program to GPU memory on `stream` (Section 3.4 replay;
  * the schedule decides register placement, checkpoint segments and what is
  * recomputed in the reverse sweep).  `policy` is NDVM_POLICY_SAVE or
- * NDVM_POLICY_RECOMPUTE.
+ * NDVM_POLICY_RECOMPUTE, optionally OR'd with NDVM_BRANCH_SKIP.
  * On success *out receives a handle owned by the library.
  * Errors: NDVM_E_ARG, NDVM_E_TAPE (malformed tape), NDVM_E_NOMEM,
  * NDVM_E_DEVICE, NDVM_E_UNSUPPORTED (unknown policy).

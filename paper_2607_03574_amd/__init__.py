@@ -21,6 +21,7 @@ STATUS_NAMES = {0: "NDVM_OK", 1: "NDVM_E_ARG", 2: "NDVM_E_BYTECODE", 3: "NDVM_E_
                 8: "NDVM_E_INTERNAL"}
 POLICY_SAVE = 1        # store what the reverse sweep reads, recompute nothing
 POLICY_RECOMPUTE = 2   # store segment inputs, recompute inside segments
+BRANCH_SKIP = 0x100    # option OR'd into the policy: waves skip branch arms none of their lanes takes
 NOALLOC_SCRATCH_BYTES = 64 << 20    # NDVM_NOALLOC_SCRATCH_BYTES
 
 # exported symbols of include/ndvm.h

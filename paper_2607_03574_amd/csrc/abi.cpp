@@ -20,7 +20,7 @@
 
 namespace ndvm {
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, int variant, uint32_t slots, hipStream_t stream);
+                         uint32_t r_lds, int variant, bool skips, uint32_t slots, hipStream_t stream);
 bool slots_supported(uint32_t S);
 size_t scratch_bytes();
 hipError_t launch_fold_points(const double *term, const double *tgrad, int64_t L, int64_t N, int64_t P,
@@ -120,6 +120,7 @@ struct ndvm_tape {
     uint64_t tape_bytes = 0;
     uint32_t n_selects = 0;
     int policy = NDVM_POLICY_RECOMPUTE;
+    bool arms = false;   // NDVM_BRANCH_SKIP: branch arms behind wave skip tests
     std::mutex mu;
     std::map<uint32_t, std::unique_ptr<DevProg>> fwd;    // keyed by slot count
     std::map<uint64_t, std::unique_ptr<DevProg>> grad;   // keyed by (slot count, register budget)
@@ -195,7 +196,11 @@ ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, bool build, De
         const hipStream_t stream = nullptr;
         Schedule sch;
         ndvm_status st = scheduled(
-            [&] { return schedule_grad(tape->tape, b, S, tape->policy == NDVM_POLICY_SAVE); }, &sch);
+            [&] {
+                return schedule_grad(tape->tape, b, S, tape->policy == NDVM_POLICY_SAVE,
+                                     tape->arms ? kArmMinElems : 0);
+            },
+            &sch);
         if (st != NDVM_OK) return st;
         std::unique_ptr<DevProg> dp;
         st = upload_program(std::move(sch), tape->tape, stream, &dp);
@@ -219,7 +224,8 @@ ndvm_status fwd_program(ndvm_tape *tape, uint32_t S, hipStream_t stream, DevProg
     auto it = tape->fwd.find(S);
     if (it == tape->fwd.end()) {
         Schedule sch;
-        ndvm_status st = scheduled([&] { return schedule_forward(tape->tape, S, fwd_budget(S)); }, &sch);
+        ndvm_status st =
+            scheduled([&] { return schedule_forward(tape->tape, S, fwd_budget(S), tape->arms ? kArmMinElems : 0); }, &sch);
         if (st != NDVM_OK) return st;
         std::unique_ptr<DevProg> dp;
         st = upload_program(std::move(sch), tape->tape, stream, &dp);
@@ -240,9 +246,9 @@ uint64_t ws_rows(const DevProg &dp, uint32_t b) {
 }
 
 ndvm_status check_stream_and_launch(const LaunchArgs &A, const ProgStatic *table, const ProgStatic &single,
-                                    uint32_t n_prog, uint32_t r_lds, int variant, uint32_t slots,
+                                    uint32_t n_prog, uint32_t r_lds, int variant, bool skips, uint32_t slots,
                                     hipStream_t stream) {
-    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, variant, slots, stream);
+    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, variant, skips, slots, stream);
     if (e != hipSuccess) {
         set_error(std::string("kernel launch failed: ") + hipGetErrorString(e));
         return NDVM_E_DEVICE;
@@ -262,6 +268,7 @@ std::map<std::vector<uint64_t>, void *> g_tables;
 struct ManyLaunch {
     uint32_t S = 0, r_launch = 0;
     int variant = kLdsOnly;
+    bool skips = false;     // some program has skippable branch arms
     uint64_t rows = 0;
     void *d_table = nullptr;
 };
@@ -284,6 +291,7 @@ ndvm_status many_launch(const ndvm_tape *const *tapes, int n_prog, int64_t L, bo
         r_launch = std::max(r_launch, r_lds);
         const bool spills = dp->meta.n_regs > r_lds;
         n_spill += spills;
+        out->skips = out->skips || dp->meta.n_skips > 0;
         table[q] = ProgStatic{dp->code, dp->consts, row, row + dp->meta.n_ckpt_rows + slot::kMaxBlock,
                               dp->meta.hdr_off, r_lds, spills};
         row += ws_rows(*dp, b);
@@ -395,7 +403,8 @@ ndvm_status ndvm_tape_upload(const uint8_t *bytes, size_t len, int policy, void 
             set_error("ndvm_tape_upload: null argument");
             return NDVM_E_ARG;
         }
-        if (policy != NDVM_POLICY_RECOMPUTE && policy != NDVM_POLICY_SAVE) {
+        const int save = policy & ~NDVM_BRANCH_SKIP;
+        if (save != NDVM_POLICY_RECOMPUTE && save != NDVM_POLICY_SAVE) {
             set_error("ndvm_tape_upload: unsupported save policy");
             return NDVM_E_UNSUPPORTED;
         }
@@ -404,7 +413,8 @@ ndvm_status ndvm_tape_upload(const uint8_t *bytes, size_t len, int policy, void 
         if (st != NDVM_OK) return st;
         h->id = g_next_id++;
         h->tape_bytes = len;
-        h->policy = policy;
+        h->policy = save;
+        h->arms = (policy & NDVM_BRANCH_SKIP) != 0;
         for (const TapeOp &o : h->tape.ops) h->n_selects += o.code == tp::SELECT;
         // schedule the forward program now: scheduling limits surface at upload
         DevProg *fp = nullptr;
@@ -540,7 +550,7 @@ ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
         LaunchArgs A{obs, params, loss, loss, static_cast<double *>(ws), ld_p, 0, L, Lp, 0, 0};
         const bool spills = dp.meta.n_regs > r_lds;
         ProgStatic D{dp.code, dp.consts, 0, uint64_t(dp.meta.n_ckpt_rows) + slot::kMaxBlock, dp.meta.hdr_off, r_lds, spills};
-        return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, S,
+        return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, dp.meta.n_skips > 0, S,
                                        static_cast<hipStream_t>(stream));
     });
 }
@@ -589,7 +599,7 @@ static ndvm_status grad_impl(const ndvm_tape *tape, const double *params, int64_
     LaunchArgs A{obs, params, loss, grad, wsd, ld_p, ld_g, L, Lp, 0, 0};
     const bool spills = dp->meta.n_regs > r_lds;
     ProgStatic D{dp->code, dp->consts, 0, uint64_t(dp->meta.n_ckpt_rows) + slot::kMaxBlock, dp->meta.hdr_off, r_lds, spills};
-    return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, S,
+    return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, dp->meta.n_skips > 0, S,
                                    static_cast<hipStream_t>(stream));
 }
 
@@ -679,7 +689,8 @@ ndvm_status ndvm_grad_points(const ndvm_tape *tape, const double *params, int64_
         hipStream_t s = static_cast<hipStream_t>(stream);
         DeviceProps pr;
         if ((st = device_props(&pr)) != NDVM_OK) return st;
-        st = check_stream_and_launch(A, nullptr, D_, 1, r_lds, spills ? kSpill : kLdsOnly, choose_slots(pr, F, 1), s);
+        st = check_stream_and_launch(A, nullptr, D_, 1, r_lds, spills ? kSpill : kLdsOnly, dp->meta.n_skips > 0,
+                                     choose_slots(pr, F, 1), s);
         if (st != NDVM_OK) return st;
         const hipError_t e = launch_fold_points(term, tgrad, L, n_points, P, scale, loss, grad, ld_g, s);
         if (e != hipSuccess) {
@@ -733,7 +744,7 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
                          grad ? grad + q0 * prog_stride_g : nullptr, static_cast<double *>(ws), ld_p, ld_g, L, Lp,
                          prog_stride_p, prog_stride_g};
             st = check_stream_and_launch(A, static_cast<const ProgStatic *>(d_table) + q0, none, uint32_t(nq),
-                                         r_launch, variant, S, s);
+                                         r_launch, variant, ml.skips, S, s);
             if (st != NDVM_OK) return st;
         }
         return NDVM_OK;

@@ -47,7 +47,7 @@ struct HostCtx {
     uint32_t n_ckpt;   // rows including the trash row
     int *fault;        // first problem seen: 1 register range, 2 unwritten read, 3 pool/param/obs index,
                        // 4 ckpt row, 6 read of a register another slot writes, 7 two slots write one register,
-                       // 8 form differs between slots
+                       // 8 form differs between slots, 9 output store or skip test inside a skipped arm
     uint32_t cur_slot = 0;
     bool cur_dummy = false;   // an unused slot (result to the sink): its reads are never checked
     std::vector<std::pair<uint32_t, double>> *pending;
@@ -81,6 +81,10 @@ struct HostCtx {
     }
     void st(uint32_t r, double v) const {
         if (r >= n_regs) { flag(1); return; }
+        if (poison) {
+            if (cur_accum) return;
+            v = NAN;
+        }
         if (r < sink || r >= sink + slot::kMaxBlock)
             for (size_t i = 0; i < pending->size(); ++i)
                 if ((*pending)[i].first == r && (*pend_slot)[i] != cur_slot) flag(7);
@@ -108,28 +112,67 @@ struct HostCtx {
         return params[p];
     }
     void store_loss(double v, bool on) const {
+        if (poison) flag(9);
         if (on) *loss = v;
     }
     void store_grad(uint32_t p, double v, bool on) const {
+        if (poison) flag(9);
         if (!on) return;
         if (p >= n_params) { flag(3); return; }
         grad[p] = v;
     }
     void ckst(uint32_t row, double v) const {
         if (row >= n_ckpt) { flag(4); return; }
-        ckpt[row] = v;
+        ckpt[row] = poison ? NAN : v;
     }
     static void settle(double) {}
+    void check_written(uint32_t r) const {
+        if (r < n_regs && !written[r] && !cur_dummy) flag(2, r);
+    }
+    // SKIP, one lane at a time: the lane skips the arm it does not take (the
+    // most skipping any wave of lanes could do)
+    mutable uint32_t skip = 0;
+    bool never_skip = false;
+    // An instruction of an arm this lane skips.  On the GPU its registers
+    // keep whatever they held; here every value it would form anew (forward
+    // values, temporaries, first contributions) is set to NaN and every
+    // adjoint it would add to keeps its value, so a result that depends on a
+    // skipped arm comes out NaN or differs from the run without skipping.
+    bool poison = false;
+    bool cur_accum = false;   // the slot's writes add to their own register (not formed anew)
+    void skip_arm(bool then_taken, uint32_t imm) const {
+        const bool else_arm = (imm >> slot::kSkipSideShift) & 1u;
+        if (poison) flag(9);
+        if (!never_skip && (else_arm ? then_taken : !then_taken)) skip = imm & slot::kSkipCountMask;
+    }
     double ckld(uint32_t row) const {
         if (row >= n_ckpt) { flag(4); return NAN; }
         return ckpt[row];
     }
 };
 
-// with_grad: 0 forward only, 1 gradient (recompute policy), 2 gradient (save policy)
-Schedule schedule(const Tape &t, int with_grad, uint32_t reg_budget, uint32_t slots) {
-    return with_grad ? schedule_grad(t, reg_budget, slots, with_grad == 2) : schedule_forward(t, slots, reg_budget);
+// forms whose writes add to the register written (an adjoint update that is
+// not the first contribution)
+bool accumulates(uint32_t form, const P4 &p) {
+    switch (form) {
+    case slot::ACC: return p.z() == p.a();
+    case slot::MACG: case slot::ACCD: case slot::ACCND: case slot::DOTACC: case slot::ACCSEL: case slot::ACCABS:
+    case slot::DOTBACC:
+        return !p.first();
+    default:
+        return false;
+    }
 }
+
+// with_grad: 0 forward only, 1 gradient (recompute policy), 2 gradient (save
+// policy); arm_min: smallest arm behind a skip test (0: none)
+Schedule schedule(const Tape &t, int with_grad, uint32_t reg_budget, uint32_t slots, uint32_t arm_min) {
+    return with_grad ? schedule_grad(t, reg_budget, slots, with_grad == 2, arm_min)
+                     : schedule_forward(t, slots, reg_budget, arm_min);
+}
+// mode bits 8 / 16: arms as the NDVM_BRANCH_SKIP option lays them out / every
+// arm however small
+uint32_t arm_min_of(int mode) { return (mode & 16) ? 1 : (mode & 8) ? kArmMinElems : 0; }
 
 }  // namespace
 
@@ -138,14 +181,21 @@ extern "C" {
 /*
  * Schedule `tape` (forward-only when with_grad == 0, else the gradient
  * program for `reg_budget` registers) with `slots` micro-ops per instruction
- * and run it for L lanes on the host.  stats (optional, 10 entries): n_regs,
- * n_ckpt_rows, n_segments, n_instr, fwd ops, recompute ops, reverse ops,
- * checkpoint elements stored, micro-ops, slots used.
+ * and run it for L lanes on the host.  with_grad: 0 forward only, 1 gradient
+ * (recompute policy), 2 gradient (save policy); + 4: never skip a branch arm;
+ * + 8: branch arms behind skip tests (as the NDVM_BRANCH_SKIP option lays
+ * them out); + 16: every branch arm behind a skip test, however small.
+ * stats (optional, 11 entries): n_regs, n_ckpt_rows, n_segments, n_instr, fwd
+ * ops, recompute ops, reverse ops, checkpoint elements stored, micro-ops,
+ * slots used, skippable arms.
  * Returns 0, an ndvm_status from parsing, or 100 + fault code.
  */
 int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_budget, uint32_t slots,
                  const double *params, int64_t L, int64_t ld_p, const double *obs, int64_t n_obs, double *loss,
                  double *grad, int64_t ld_g, uint64_t *stats) {
+    const bool never_skip = (with_grad & 4) != 0;   // run both arms of every branch
+    const uint32_t arm_min = arm_min_of(with_grad);
+    with_grad &= 3;
     Tape t;
     ndvm_status st = parse_tape(tape, len, &t);
     if (st != NDVM_OK) return st;
@@ -153,15 +203,16 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
     if (slots != 1 && slots != 2 && slots != 4) return NDVM_E_ARG;
     Schedule S;
     try {
-        S = schedule(t, with_grad, reg_budget, slots);
+        S = schedule(t, with_grad, reg_budget, slots, arm_min);
     } catch (const std::exception &e) {
         set_error(e.what());
         return NDVM_E_UNSUPPORTED;
     }
     if (stats) {
-        uint64_t v[10] = {S.n_regs, S.n_ckpt_rows, S.n_segments, S.n_instr, S.n_fwd_ops,
-                          S.n_recompute_ops, S.n_rev_ops, S.ckpt_elems_stored, S.n_uops, S.n_slots_used};
-        for (int i = 0; i < 10; ++i) stats[i] = v[i];
+        uint64_t v[11] = {S.n_regs, S.n_ckpt_rows, S.n_segments, S.n_instr, S.n_fwd_ops,
+                          S.n_recompute_ops, S.n_rev_ops, S.ckpt_elems_stored, S.n_uops, S.n_slots_used,
+                          S.n_skips};
+        for (int i = 0; i < 11; ++i) stats[i] = v[i];
     }
     const uint32_t sink = 2 * t.n_params;
     std::vector<double> regs(S.n_regs), ck(size_t(S.n_ckpt_rows) + slot::kMaxBlock);
@@ -180,8 +231,12 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
         uint32_t fault_reg = 0xFFFFFFFFu, fault_form = 0;
         uint64_t fault_instr = 0;
         c.fault_reg = &fault_reg;
+        c.never_skip = never_skip;
         bool ended = false;
+        uint32_t skipped = 0;   // instructions of a skipped arm still to come
         for (uint64_t i = 0; i < uint64_t(S.n_chunks) * K && !ended && !fault; ++i) {
+            c.poison = skipped > 0;
+            if (skipped) --skipped;
             const uint32_t hdr = S.code[S.hdr_off + i];
             const uint32_t form = hdr & slot::kFormMask;
             fault_instr = i;
@@ -196,14 +251,19 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
                 const uint32_t *w = &S.code[size_t(i / K) * slot::kChunkWords + (size_t(r) * K + i % K) * 4];
                 const P4 p{{w[0], w[1], w[2], w[3]}, hdr, sl, reg_bytes};
                 c.cur_slot = sl;
-                c.cur_dummy = (slot::writes_a(form) && p.a() == sink) ||
+                c.cur_dummy = c.poison || (slot::writes_a(form) && p.a() == sink) ||
                               (form == slot::CKST && (p.ix() & slot::kCkRowMask) == S.n_ckpt_rows);
+                c.cur_accum = accumulates(form, p);
                 if (slot::is_hot(form))
                     slotx::exec_hot(c, form, p);
                 else
                     slotx::exec_cold(c, form, p);
             }
             c.commit();
+            if (c.skip) {   // the arm's instructions run poisoned
+                skipped = c.skip;
+                c.skip = 0;
+            }
         }
         if (!ended && !fault) fault = 5;
         if (fault) {
@@ -229,7 +289,7 @@ int64_t ndvm_emu_program(const uint8_t *tape, size_t len, int with_grad, uint32_
     if (parse_tape(tape, len, &t) != NDVM_OK) return -1;
     Schedule S;
     try {
-        S = schedule(t, with_grad, reg_budget, slots);
+        S = schedule(t, with_grad & 3, reg_budget, slots, arm_min_of(with_grad));
     } catch (const std::exception &e) {
         set_error(e.what());
         return -1;

@@ -63,6 +63,16 @@ struct DevCtx {
     __device__ __forceinline__ double konst(uint32_t i) const { return consts[i]; }
     __device__ __forceinline__ double param(uint32_t p) const { return params[lc * ld_p + p]; }
     __device__ __forceinline__ static void settle(double v) { asm volatile("" ::"v"(v)); }
+    __device__ __forceinline__ static void check_written(uint32_t) {}
+    // SKIP: the next n instructions are skipped when every lane of the wave
+    // decides the branch the other way (a ballot over the wave's threads; the
+    // threads of a lane's slots hold the same predicate)
+    mutable uint32_t skip = 0;
+    __device__ __forceinline__ void skip_arm(bool then_taken, uint32_t imm) const {
+        const uint64_t m = __ballot(then_taken);
+        const bool else_arm = (imm >> slot::kSkipSideShift) & 1u;
+        if (else_arm ? m == ~uint64_t(0) : m == 0) skip = imm & slot::kSkipCountMask;
+    }
     __device__ __forceinline__ double ckld(uint32_t row) const { return ckpt[int64_t(row) * Lpad + lane]; }
     __device__ __forceinline__ void ckst(uint32_t row, double v) const { ckpt[int64_t(row) * Lpad + lane] = v; }
     __device__ __forceinline__ void store_loss(double v, bool on) const {
@@ -140,8 +150,12 @@ __device__ __attribute__((noinline)) void cold_call(const C &c, uint32_t form, P
 
 // Instruction P of the chunk held in `ch` (one dword per thread), header
 // lane hb + P of `hv`; returns 1 when it is END.
-template <int P, class C>
+template <int P, bool kSkip, class C>
 __device__ __forceinline__ uint32_t step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb) {
+    if (kSkip && c.skip) {   // inside a skipped arm (never holds END)
+        --c.skip;
+        return 0;
+    }
     const uint32_t hdr = lane_word(hv, hb + P);
     const uint32_t form = hdr & slot::kFormMask;
     ChunkPayload<P> p;
@@ -178,7 +192,7 @@ __device__ __forceinline__ uint32_t step(const C &c, uint32_t ch, uint32_t hv, u
 // straight-line code, chunk c + 2 requested when chunk c starts, headers
 // 64 at a time with the next group in flight (the program is padded for
 // these read-aheads; instructions after END are END too).
-template <int S, bool kSpill>
+template <bool kSkip, int S, bool kSpill>
 __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *prog, uint32_t hdr_off) {
     static_assert(slot::kChunk == 4 && slot::kFetchAhead == 2 && slot::kHeaderGroup == 64,
                   "the fetch below reads four-instruction chunks two ahead and 64 headers a group");
@@ -191,10 +205,10 @@ __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *
         pc += W;
         const uint32_t n2 = pc[W];
         const uint32_t hb = (chunk & 15u) * 4;
-        uint32_t ended = step<0>(c, cur, hv, hb);
-        ended |= step<1>(c, cur, hv, hb);
-        ended |= step<2>(c, cur, hv, hb);
-        ended |= step<3>(c, cur, hv, hb);
+        uint32_t ended = step<0, kSkip>(c, cur, hv, hb);
+        ended |= step<1, kSkip>(c, cur, hv, hb);
+        ended |= step<2, kSkip>(c, cur, hv, hb);
+        ended |= step<3, kSkip>(c, cur, hv, hb);
         if (ended) return;
         cur = n1;
         n1 = n2;
@@ -208,7 +222,7 @@ __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *
 
 }  // namespace
 
-template <int S, bool kSpill>
+template <int S, bool kSpill, bool kSkip>
 __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStatic *__restrict__ table,
                                             const ProgStatic &single) {
     extern __shared__ double lds_regs[];
@@ -238,63 +252,70 @@ __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStati
     c.ld_p = A.ld_p;
     c.ld_g = A.ld_g;
     c.r_lds = D.r_lds;
-    run(c, D.prog, D.hdr_off);
+    run<kSkip>(c, D.prog, D.hdr_off);
 }
 
 // All lane registers in LDS (the usual case: the scheduler fits the register
-// file to the launch's LDS budget).
-template <int S>
+// file to the launch's LDS budget).  kSkip: the program has skippable branch
+// arms (every instruction then tests the skip counter first).
+template <int S, bool kSkip>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4)))
 ndvm_replay(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
-    replay_body<S, false>(A, table, single);
+    replay_body<S, false, kSkip>(A, table, single);
 }
 
 // Registers beyond r_lds spill to lane-contiguous workspace rows.
 template <int S>
 __global__ void __launch_bounds__(64)
 ndvm_replay_spill(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
-    replay_body<S, true>(A, table, single);
+    replay_body<S, true, true>(A, table, single);
 }
 
 // Many programs in one launch, only some of which spill: each workgroup takes
 // the variant its program needs, so one spilling program does not slow the
 // others down.
-template <int S>
+template <int S, bool kSkip>
 __global__ void __launch_bounds__(64)
 ndvm_replay_per_program(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
     if (table[blockIdx.y].spills)
-        replay_body<S, true>(A, table, single);
+        replay_body<S, true, true>(A, table, single);
     else
-        replay_body<S, false>(A, table, single);
+        replay_body<S, false, kSkip>(A, table, single);
 }
 
 namespace {
 
 template <int S>
 hipError_t launch_s(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                    uint32_t r_lds, int variant, hipStream_t stream) {
+                    uint32_t r_lds, int variant, bool skips, hipStream_t stream) {
     static std::once_flag once[64];
     int dev = 0;
     (void)hipGetDevice(&dev);
     std::call_once(once[dev & 63], [dev]() {
         int max_smem = 0;
         (void)hipDeviceGetAttribute(&max_smem, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&ndvm_replay<S>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
-        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&ndvm_replay_spill<S>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
-        (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&ndvm_replay_per_program<S>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
+        for (const void *f : {reinterpret_cast<const void *>(&ndvm_replay<S, false>),
+                              reinterpret_cast<const void *>(&ndvm_replay<S, true>),
+                              reinterpret_cast<const void *>(&ndvm_replay_spill<S>),
+                              reinterpret_cast<const void *>(&ndvm_replay_per_program<S, false>),
+                              reinterpret_cast<const void *>(&ndvm_replay_per_program<S, true>)})
+            (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
     });
     constexpr int LW = 64 / S;
     dim3 grid(uint32_t((A.L + LW - 1) / LW), n_prog), block(64);
     size_t smem = size_t(r_lds) * LW * sizeof(double);
-    if (variant == kPerProgram && d_table)
-        hipLaunchKernelGGL(ndvm_replay_per_program<S>, grid, block, smem, stream, A, d_table, single);
-    else if (variant == kSpill || variant == kPerProgram)
+    if (variant == kPerProgram && d_table) {
+        if (skips)
+            hipLaunchKernelGGL((ndvm_replay_per_program<S, true>), grid, block, smem, stream, A, d_table, single);
+        else
+            hipLaunchKernelGGL((ndvm_replay_per_program<S, false>), grid, block, smem, stream, A, d_table, single);
+    } else if (variant == kSpill || variant == kPerProgram) {
         hipLaunchKernelGGL(ndvm_replay_spill<S>, grid, block, smem, stream, A, d_table, single);
-    else
-        hipLaunchKernelGGL(ndvm_replay<S>, grid, block, smem, stream, A, d_table, single);
+    } else if (skips) {
+        hipLaunchKernelGGL((ndvm_replay<S, true>), grid, block, smem, stream, A, d_table, single);
+    } else {
+        hipLaunchKernelGGL((ndvm_replay<S, false>), grid, block, smem, stream, A, d_table, single);
+    }
     return hipGetLastError();
 }
 
@@ -369,9 +390,9 @@ hipError_t scratch_address(void **out) {
 }
 
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, int variant, uint32_t slots, hipStream_t stream) {
+                         uint32_t r_lds, int variant, bool skips, uint32_t slots, hipStream_t stream) {
     switch (slots) {
-    case 4: return launch_s<4>(A, d_table, single, n_prog, r_lds, variant, stream);
+    case 4: return launch_s<4>(A, d_table, single, n_prog, r_lds, variant, skips, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -25,6 +25,7 @@
 #include <cstring>
 #include <map>
 #include <stdexcept>
+#include <string>
 #include <unordered_map>
 
 #include "slot.h"
@@ -223,7 +224,184 @@ struct Info {
         for (uint32_t k = 0; k < N; ++k)
             if (vlive[k] && rep[k] == k) for_operands(k, [&](uint32_t s) { last_use[s] = k; });
         last_use[rep[t.loss]] = N;
+        // no skippable arms unless find_arms finds them
+        cone_of.assign(N, -1);
+        sel_group.assign(N, -1);
+        arm_of.assign(N, -1);
+        hoist.assign(N, 0);
+        groups.clear();
     }
+
+    // ---- arms of numeric branches that a wave may skip (Section 6 lane
+    // masking, taken per wave: when every lane of a wave decides a branch
+    // the same way, the other arm's forward values and adjoint rules are not
+    // run).  A group is one branch: a run of consecutive SELECT slots with the
+    // same predicate operands.  Its cone on side 0 (then) / 1 (else) is the
+    // set of values whose every reader is in that cone or is a select of the
+    // group reading it through that side's input: values no lane needs when
+    // the wave takes the other arm.  Groups inside another group's cone are
+    // not skipped on their own (they are part of the outer arm).
+    struct Group {
+        std::vector<uint32_t> sel;       // SELECT slots, ascending
+        uint32_t a = 0, b = 0;           // predicate operand slots
+        std::vector<uint32_t> cone[2];   // representatives, ascending
+        uint32_t lo = 0, hi = 0;         // tape range of its cones and selects
+        std::vector<uint32_t> hoisted;   // observation loads laid out before the arms
+    };
+    std::vector<Group> groups;
+    std::vector<int32_t> cone_of;        // representative -> 2 * group + side, or -1
+    std::vector<int32_t> sel_group;      // SELECT slot -> group, or -1
+    std::vector<int32_t> arm_of;         // slot -> 2 * group + side of the arm holding its rule, or -1
+    std::vector<uint8_t> hoist;          // observation loads laid out with an earlier branch's arms
+
+    void find_arms(uint32_t arm_min, uint32_t merge) {
+        cone_of.assign(N, -1);
+        sel_group.assign(N, -1);
+        groups.clear();
+        std::vector<uint32_t> readers(N, 0);
+        for (uint32_t k = 0; k < N; ++k)
+            if (vlive[k] && rep[k] == k) for_operands(k, [&](uint32_t s) { readers[s]++; });
+        readers[rep[t.loss]]++;
+        std::vector<Group> all;
+        for (uint32_t k = 0; k < N;) {
+            const TapeOp &o = t.ops[k];
+            if (o.code != tp::SELECT) { ++k; continue; }
+            Group g;
+            g.a = o.a;
+            g.b = o.b;
+            uint32_t e = k;
+            while (e < N && t.ops[e].code == tp::SELECT && rep[t.ops[e].a] == rep[o.a] && rep[t.ops[e].b] == rep[o.b])
+                g.sel.push_back(e++);
+            k = e;
+            bool live = false;
+            for (uint32_t q : g.sel) live = live || (vlive[q] && rep[q] == q);
+            if (!live) continue;
+            for (uint32_t side = 0; side < 2; ++side) {
+                std::vector<uint32_t> cnt(N, 0);   // readers accounted for by the cone
+                uint32_t top = 0;
+                for (uint32_t q : g.sel) {
+                    if (!(vlive[q] && rep[q] == q)) continue;
+                    const TapeOp &so = t.ops[q];
+                    const uint32_t in = rep[side == 0 ? so.c : so.d];
+                    cnt[in]++;
+                    top = std::max(top, in);
+                }
+                for (uint32_t v = top + 1; v-- > 0;) {
+                    if (!cnt[v] || cnt[v] != readers[v] || rep[v] != v || !vlive[v] || kind[v] != K_COMP) continue;
+                    // a select of the branch itself (one reading another) stays with the selects
+                    if (std::find(g.sel.begin(), g.sel.end(), v) != g.sel.end()) continue;
+                    g.cone[side].push_back(v);
+                    for_operands(v, [&](uint32_t s2) { cnt[s2]++; });
+                }
+                std::reverse(g.cone[side].begin(), g.cone[side].end());
+                // arms below arm_min elements stay unmarked
+                uint32_t elems = 0;
+                for (uint32_t v : g.cone[side]) elems += nel[v];
+                if (elems < arm_min) g.cone[side].clear();
+            }
+            if (g.cone[0].empty() && g.cone[1].empty()) continue;
+            all.push_back(std::move(g));
+        }
+        std::vector<int32_t> in_cone(N, -1);
+        for (uint32_t gi = 0; gi < all.size(); ++gi)
+            for (uint32_t side = 0; side < 2; ++side)
+                for (uint32_t v : all[gi].cone[side]) in_cone[v] = int32_t(gi);
+        std::vector<Group> kept;
+        for (uint32_t gi = 0; gi < all.size(); ++gi) {
+            bool nested = false;
+            for (uint32_t q : all[gi].sel) nested = nested || (in_cone[rep[q]] >= 0 && in_cone[rep[q]] != int32_t(gi));
+            if (!nested) kept.push_back(std::move(all[gi]));
+        }
+        // Branches on the same predicate value one after another (the trips
+        // of a loop around a branch) share one skip test: the later arms'
+        // values are computed with the first branch's, so the arms of up to
+        // `merge` branches are independent chains the packer can put side
+        // by side (one arm alone is mostly a dependent chain).  A later arm
+        // qualifies when every value it reads from outside itself is a
+        // constant, a parameter, an observation (its load moves up before
+        // the skip test) or a value computed before the first branch's arm.
+        hoist.assign(N, 0);
+        for (size_t gi = 0; gi < kept.size();) {
+            Group g = std::move(kept[gi]);
+            const uint32_t at = g.sel.front();   // where the arms are laid out
+            size_t e = gi + 1;
+            std::vector<uint32_t> loads;
+            for (uint32_t members = 1; e < kept.size() && members < merge; ++e, ++members) {
+                const Group &h = kept[e];
+                if (rep[h.a] != rep[g.a] || rep[h.b] != rep[g.b]) break;
+                bool ok = true;
+                std::vector<uint32_t> hl;
+                for (uint32_t side = 0; side < 2 && ok; ++side)
+                    for (uint32_t v : h.cone[side]) {
+                        for_operands(v, [&](uint32_t u) {
+                            if (std::binary_search(h.cone[side].begin(), h.cone[side].end(), u)) return;
+                            if (kind[u] == K_CONST || kind[u] == K_PARAM) return;
+                            if (kind[u] == K_OBS) {
+                                if (u > at) hl.push_back(u);
+                                return;
+                            }
+                            if (u >= at || cone_of[u] >= 0) ok = false;
+                        });
+                        // the arm's adjoint rules run after the first branch's
+                        // select rules: every slot they add to outside the arm
+                        // must have its own rule run later (lie before it)
+                        const uint32_t fused = (!fmul.empty() && fmul[v]) ? fmul[v] - 1 : N;   // in the arm too
+                        auto raw_ok = [&](uint32_t r) {
+                            if (kind[r] != K_COMP) return;
+                            if (std::binary_search(h.cone[side].begin(), h.cone[side].end(), rep[r])) return;
+                            if (r >= at && r != fused) ok = false;
+                        };
+                        for_operands_raw(v, raw_ok);
+                        if (!fmul.empty() && fmul[v]) for_operands_raw(fmul[v] - 1, raw_ok);
+                    }
+                if (!ok) break;
+                for (uint32_t side = 0; side < 2; ++side) {
+                    g.cone[side].insert(g.cone[side].end(), h.cone[side].begin(), h.cone[side].end());
+                    std::sort(g.cone[side].begin(), g.cone[side].end());
+                }
+                g.sel.insert(g.sel.end(), h.sel.begin(), h.sel.end());
+                loads.insert(loads.end(), hl.begin(), hl.end());
+            }
+            gi = e;
+            std::sort(loads.begin(), loads.end());
+            loads.erase(std::unique(loads.begin(), loads.end()), loads.end());
+            for (uint32_t u : loads) hoist[u] = 1;
+            g.hoisted = std::move(loads);
+            const int32_t id = int32_t(groups.size());
+            g.lo = g.sel.front();
+            g.hi = g.sel.back();
+            for (uint32_t side = 0; side < 2; ++side)
+                for (uint32_t v : g.cone[side]) {
+                    cone_of[v] = 2 * id + int32_t(side);
+                    g.lo = std::min(g.lo, v);
+                }
+            for (uint32_t q : g.sel) sel_group[q] = id;
+            groups.push_back(std::move(g));
+        }
+        // Slots whose adjoint rules lie in an arm: the cone's values; a
+        // product folded into a cone value's sum (its value is never formed,
+        // its rule is); duplicates of a cone value up to the branch's last
+        // select (an adjoint rule there may contribute to a cone value, so it
+        // must run before that value's rule).  A duplicate after the last
+        // select is laid out before the arm as usual; when the wave skips the
+        // arm its adjoint is exactly zero (only selects of the same predicate
+        // and the arm's own values reach it), so its gated contributions are
+        // nothing whatever stale values it reads.
+        arm_of.assign(N, -1);
+        for (uint32_t k = 0; k < N; ++k) {
+            const int32_t c = cone_of[rep[k]];
+            if (c >= 0 && k <= groups[uint32_t(c) / 2].hi) arm_of[k] = c;
+        }
+        for (uint32_t c = 0; c < N; ++c)
+            if (!fmul.empty() && fmul[c] && arm_of[c] >= 0) {
+                const uint32_t m = fmul[c] - 1;
+                arm_of[m] = arm_of[c];
+                Group &g = groups[uint32_t(arm_of[c]) / 2];
+                g.lo = std::min(g.lo, m);
+            }
+    }
+    // the cone (2 * group + side) a slot's adjoint rule or value belongs to, or -1
+    int32_t cone_of_slot(uint32_t k) const { return arm_of[k]; }
 };
 
 // ------------------------------------------------------------------ allocation
@@ -333,7 +511,11 @@ uint32_t allocate(std::vector<Interval> &iv, uint32_t pool, bool spread = true) 
 
 // ------------------------------------------------------------------ builder
 // Abstract instruction before register assignment.
-enum RIKind : uint8_t { I_LDP, I_LDC, I_CKST, I_FWD, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_STG };
+enum RIKind : uint8_t { I_LDP, I_LDC, I_CKST, I_FWD, I_STLOSS, I_ZEROP, I_SEED, I_CKLD, I_REV, I_STG,
+                        I_SKIP,      // a skippable arm starts: group k, side nb, segment j
+                        I_SKIPEND,   // the arm ends
+                        I_ZERO };    // adjoint of slot k set to +0 (segment j): its first contribution is in a
+                                     // skippable arm
 struct AI {
     uint8_t kind;
     uint32_t k;   // slot / param index
@@ -445,6 +627,11 @@ struct Builder {
             run += diff[p];
             w[p] = run;
         }
+        // no cut inside a skippable branch: its arms are laid out next to
+        // its selects, after the positions their ops had in the tape
+        std::vector<uint8_t> nocut(N + 1, 0);
+        for (const auto &g : I.groups)
+            for (uint32_t p = g.lo + 1; p <= g.hi; ++p) nocut[p] = 1;
         std::vector<uint32_t> c{0};
         uint64_t acc = 0;
         int64_t best = -1;
@@ -453,7 +640,7 @@ struct Builder {
             if (comp_live(k)) acc += I.nel[k];
             uint32_t p = k + 1;
             if (p >= N) break;
-            if (acc * 2 >= S && p > start) {
+            if (acc * 2 >= S && p > start && !nocut[p]) {
                 if (best < 0 || w[p] <= w[best]) best = p;
             }
             if (acc >= S && best > 0) {
@@ -684,6 +871,12 @@ struct UOp {
     uint32_t form, flags, imm;
     uint32_t f[4];
 };
+
+// Pseudo micro-ops that bound a skippable arm in a phase's micro-op list:
+// begin carries the predicate register in f[1] and the side (0 then, 1 else)
+// in imm.  They never reach the packer: each phase is packed block by block
+// between them, and the encoder puts a SKIP instruction before each arm.
+constexpr uint32_t kMarkBegin = 0x7FFF0001u, kMarkEnd = 0x7FFF0002u;
 
 // index field of a checkpoint move of n rows from `row` on
 uint32_t ck_row(uint32_t row, uint32_t n) {
@@ -1006,6 +1199,23 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                 ++next_cut;
             }
         }
+        if (I.cone_of_slot(k) >= 0 && B.comp_live(k)) continue;   // laid out with its branch's selects
+        if (I.hoist[k]) continue;                                  // loaded before an earlier branch's arms
+        if (I.sel_group[k] >= 0 && I.groups[uint32_t(I.sel_group[k])].sel.front() == k) {
+            // the branch's arms, each behind a skip test: its cone's values
+            // in tape order, right before the selects (the observations the
+            // arms of later branches on the same predicate read first)
+            const uint32_t gi = uint32_t(I.sel_group[k]);
+            for (uint32_t u : I.groups[gi].hoisted) fa.push_back({I_FWD, u, 0});
+            for (uint8_t side = 0; side < 2; ++side) {
+                if (I.groups[gi].cone[side].empty()) continue;
+                AI sk{I_SKIP, gi, 0};
+                sk.nb = side;
+                fa.push_back(sk);
+                for (uint32_t v : I.groups[gi].cone[side]) fa.push_back({I_FWD, v, 0});
+                fa.push_back({I_SKIPEND, gi, 0});
+            }
+        }
         if (B.comp_live(k) || (I.kind[k] == K_OBS && I.vlive[k])) fa.push_back({I_FWD, k, 0});
     }
     fa.push_back({I_STLOSS, t.loss, 0});
@@ -1048,6 +1258,9 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             use(B.livein[a.k][a.j]);
         } else if (a.kind == I_STLOSS) {
             use(a.k);
+        } else if (a.kind == I_SKIP) {
+            use(I.rep[I.groups[a.k].a]);
+            use(I.rep[I.groups[a.k].b]);
         }
     }
     // spread over the pool; compact when that does not fit (blocks need
@@ -1238,6 +1451,14 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             Sch.n_fwd_ops += a.nops();
             break;
         case I_STLOSS: E.put(STLOSS, fwd_operand(a.k), 0); break;
+        case I_SKIP: {   // predicate of the branch, then the arm's opening mark
+            const auto &g = I.groups[a.k];
+            const uint32_t pt = E.tmp();
+            E.put(CMPLT, pt, 0, fwd_operand(g.a), fwd_operand(g.b));
+            E.ops.push_back({kMarkBegin, 0, a.nb, {0, pt, 0, 0}});
+            break;
+        }
+        case I_SKIPEND: E.ops.push_back({kMarkEnd, 0, 0, {0, 0, 0, 0}}); break;
         }
     }
     std::vector<UOp> fwd_ops;
@@ -1264,6 +1485,15 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             return n;
         };
         std::vector<uint8_t> restored(m, 0);
+        // adjoints whose first contribution has been laid out (the first
+        // contribution stores instead of adding)
+        std::vector<uint8_t> touched_sim(N, 0);
+        auto mark_touched = [&](uint32_t k) {
+            I.for_targets(k, [&](uint32_t tg) {
+                if (I.kind[tg] == K_COMP && I.active[tg]) touched_sim[tg] = 1;
+            });
+        };
+        if (I.kind[t.loss] == K_COMP) touched_sim[t.loss] = 1;
         for (uint32_t j = m; j-- > 0;) {
             if (!restored[j]) {
                 uint32_t moves = ck_moves(j), last = j;
@@ -1274,7 +1504,47 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                 }
             }
             for (uint32_t s : B.recomp[j]) ra.push_back({I_FWD, s, j});
-            for (uint32_t k : B.revops[j]) ra.push_back({I_REV, k, j});
+            // position of each branch's last select rule in this segment
+            std::unordered_map<int32_t, uint32_t> last_sel;
+            for (uint32_t qi = 0; qi < B.revops[j].size(); ++qi)
+                if (I.sel_group[B.revops[j][qi]] >= 0) last_sel[I.sel_group[B.revops[j][qi]]] = qi;
+            for (uint32_t qi = 0; qi < B.revops[j].size(); ++qi) {
+                const uint32_t k = B.revops[j][qi];
+                if (I.cone_of_slot(k) >= 0) continue;   // applied in its arm, after the branch's selects
+                ra.push_back({I_REV, k, j});
+                mark_touched(k);
+                const int32_t gsel = I.sel_group[k];
+                if (gsel < 0) continue;
+                // after the branch's last select rule: each arm's rules behind a
+                // skip test (descending slot order, as in the tape's reverse;
+                // with several branches on one predicate, after the last
+                // select rule of the first)
+                const uint32_t gi = uint32_t(gsel);
+                if (last_sel.at(gsel) != qi) continue;
+                for (uint8_t side = 2; side-- > 0;) {
+                    std::vector<uint32_t> arm;   // the segment's rules of the arm, descending
+                    for (uint32_t q = 0; q < B.revops[j].size(); ++q)
+                        if (I.cone_of_slot(B.revops[j][q]) == int32_t(2 * gi + side)) arm.push_back(B.revops[j][q]);
+                    if (arm.empty()) continue;
+                    // an adjoint outside the arm whose first contribution the arm
+                    // would make starts at +0 before the arm instead
+                    for (uint32_t r : arm)
+                        I.for_targets(r, [&](uint32_t tg) {
+                            if (I.kind[tg] != K_COMP || !I.active[tg] || touched_sim[tg]) return;
+                            if (I.cone_of_slot(tg) == int32_t(2 * gi + side)) return;
+                            ra.push_back({I_ZERO, tg, j});
+                            touched_sim[tg] = 1;
+                        });
+                    AI sk{I_SKIP, gi, j};
+                    sk.nb = side;
+                    ra.push_back(sk);
+                    for (uint32_t r : arm) {
+                        ra.push_back({I_REV, r, j});
+                        mark_touched(r);
+                    }
+                    ra.push_back({I_SKIPEND, gi, j});
+                }
+            }
         }
         for (uint32_t p = 0; p < P; ++p) ra.push_back({I_STG, p, 0});
         ra = bundle_forward(I, ra);
@@ -1325,8 +1595,16 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
                     I.for_revreads(k, [&](uint32_t s) { vuse(s, a.j, ti); });
                     I.for_targets(k, [&](uint32_t s) { contrib(s, ti); });
                     const int32_t g = adj_of[k];
+                    if (g < 0) throw std::logic_error("adjoint rule laid out before any contribution to it");
                     riv[g].end = std::max(riv[g].end, ti);
                 }
+                break;
+            case I_ZERO:
+                contrib(a.k, ti);
+                break;
+            case I_SKIP:
+                vuse(I.rep[I.groups[a.k].a], a.j, ti);
+                vuse(I.rep[I.groups[a.k].b], a.j, ti);
                 break;
             default:
                 break;
@@ -1687,6 +1965,22 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
             case I_STG:
                 E.put(STGRAD, P + a.k, 0, a.k);
                 break;
+            case I_ZERO: {   // +0 before the arm that would make the first contribution
+                uint32_t fl;
+                const uint32_t tr = target(a.k, &fl);
+                for (uint32_t i = 0; i < I.nel[a.k]; ++i) E.put(ZERO, tr + i, 0);
+                break;
+            }
+            case I_SKIP: {
+                const auto &g = I.groups[a.k];
+                const uint32_t pt = E.tmp();
+                E.put(CMPLT, pt, 0, rev_operand(g.a, a.j), rev_operand(g.b, a.j));
+                E.ops.push_back({kMarkBegin, 0, a.nb, {0, pt, 0, 0}});
+                break;
+            }
+            case I_SKIPEND:
+                E.ops.push_back({kMarkEnd, 0, 0, {0, 0, 0, 0}});
+                break;
             default:
                 break;
             }
@@ -1711,14 +2005,51 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
     std::vector<UOp> flat;
     std::vector<std::pair<uint32_t, uint32_t>> spans;   // (first op, count) per instruction
     for (auto &ph : phases) {
-        const auto groups = pack(ph, S);
-        for (const auto &gq : groups) {
-            spans.push_back({uint32_t(flat.size()), uint32_t(gq.size())});
-            for (uint32_t j : gq) flat.push_back(ph[j]);
+        // blocks between arm marks are packed apart; each arm is preceded by
+        // a SKIP instruction that reads the predicate and jumps over the
+        // arm's instructions when every lane of the wave decides the other way
+        size_t b0 = 0;
+        std::vector<UOp> block;
+        UOp skip{};
+        bool in_arm = false;
+        auto flush = [&](size_t end) {
+            block.assign(ph.begin() + b0, ph.begin() + end);
+            const auto groups = pack(block, S);
+            if (in_arm) {
+                if (groups.size() > kSkipCountMask) throw std::length_error("skippable arm beyond the immediate field");
+                skip.imm = uint32_t(groups.size()) | uint32_t(skip.flags) << kSkipSideShift;
+                skip.flags = 0;
+                spans.push_back({uint32_t(flat.size()), 1});
+                flat.push_back(skip);
+            }
+            for (const auto &gq : groups) {
+                spans.push_back({uint32_t(flat.size()), uint32_t(gq.size())});
+                for (uint32_t j : gq) flat.push_back(block[j]);
+            }
+            Sch.n_uops += block.size();
+        };
+        for (size_t i = 0; i < ph.size(); ++i) {
+            if (ph[i].form != kMarkBegin && ph[i].form != kMarkEnd) continue;
+            flush(i);
+            in_arm = ph[i].form == kMarkBegin;
+            if (in_arm) {
+                skip = UOp{SKIP, ph[i].imm, 0, {0, ph[i].f[1], 0, 0}};
+                Sch.n_skips++;
+            }
+            b0 = i + 1;
         }
-        Sch.n_uops += ph.size();
+        flush(ph.size());
     }
     const uint32_t n_real = uint32_t(spans.size());
+    // a skipped span ends before the END and holds no other skip test (the
+    // device skips by counting instructions and never looks for END there)
+    for (uint32_t i = 0, open_end = 0; i < n_real; ++i) {
+        const UOp &u = flat[spans[i].first];
+        if (u.form != SKIP) continue;
+        const uint32_t n = u.imm & kSkipCountMask;
+        if (i < open_end || uint64_t(i) + n >= n_real) throw std::logic_error("skipped span out of place");
+        open_end = i + n + 1;
+    }
     Sch.n_instr = n_real + 1;   // through the END
     const uint32_t n_chunks = n_real / kChunk + 1 + kFetchAhead;
     const uint32_t n_groups = n_real / kHeaderGroup + 1 + kFetchAhead;
@@ -1778,11 +2109,10 @@ Schedule build_fit(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32
     return build(I, B, with_grad, S, reg_budget, temps, full);
 }
 
-}  // namespace
-
-Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget) {
+Schedule forward_fit(const Tape &t, uint32_t slots, uint32_t reg_budget, uint32_t arm_min, uint32_t merge) {
     Info I(t);
     I.analyse();
+    if (arm_min) I.find_arms(arm_min, merge);
     Builder B(I);
     B.set_cuts({0});
     B.resident.assign(I.N, 0);
@@ -1790,9 +2120,11 @@ Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget) {
     return build_fit(I, B, false, slots, reg_budget, true);
 }
 
-Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots, bool save_reads) {
+Schedule grad_fit(const Tape &t, uint32_t reg_budget, uint32_t slots, bool save_reads, uint32_t arm_min,
+                  uint32_t merge) {
     Info I(t);
     I.analyse();
+    if (arm_min) I.find_arms(arm_min, merge);
     uint64_t total = 0;
     for (uint32_t k = 0; k < I.N; ++k)
         if (I.kind[k] == K_COMP && I.vlive[k]) total += I.nel[k];
@@ -1848,6 +2180,37 @@ Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots, bool 
         }
     }
     return trial(best_size, true);
+}
+
+}  // namespace
+
+// Arms behind skip tests are an option of the layout, never a reason to
+// exceed the register budget (or, where nothing fits it, the register file
+// of the program without arms): with fewer branches per skip test (each
+// merge keeps values live longer and forbids checkpoint cuts across it), and
+// at last with no arms, until the register file fits.
+namespace {
+template <class F>
+Schedule with_arms(uint32_t arm_min, uint32_t reg_budget, F fit) {
+    Schedule plain = fit(0u, 1u);
+    if (!arm_min) return plain;
+    const uint32_t limit = std::max(reg_budget, plain.n_regs);
+    for (uint32_t merge : {4u, 2u, 1u}) {
+        Schedule s = fit(arm_min, merge);
+        if (s.n_regs <= limit) return s;
+    }
+    return plain;
+}
+}  // namespace
+
+Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget, uint32_t arm_min) {
+    return with_arms(arm_min, reg_budget,
+                     [&](uint32_t a, uint32_t m) { return forward_fit(t, slots, reg_budget, a, m); });
+}
+
+Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots, bool save_reads, uint32_t arm_min) {
+    return with_arms(arm_min, reg_budget,
+                     [&](uint32_t a, uint32_t m) { return grad_fit(t, reg_budget, slots, save_reads, a, m); });
 }
 
 }  // namespace ndvm

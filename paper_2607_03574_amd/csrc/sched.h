@@ -21,11 +21,20 @@ struct Schedule {
     uint64_t n_instr = 0, n_uops = 0, n_slots_used = 0;
     uint64_t n_fwd_ops = 0, n_recompute_ops = 0, n_rev_ops = 0;
     uint64_t ckpt_elems_stored = 0, ckpt_elems_loaded = 0;
+    uint32_t n_skips = 0;         // skippable branch arms (SKIP instructions)
 };
 
+// Smallest branch arm (in value elements) laid out behind a skip test: a
+// smaller one costs more in its skip test and in the packing it breaks than
+// a wave could save by skipping it.
+constexpr uint32_t kArmMinElems = 8;
+
 // Forward-only program (loss[L]) with `slots` micro-ops per instruction;
-// values spread over up to `reg_budget` registers.
-Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget);
+// values spread over up to `reg_budget` registers.  With arm_min > 0, the
+// arms of numeric branches with at least arm_min value elements are laid out
+// behind skip tests (a wave whose lanes all decide a branch one way skips the
+// other arm).
+Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget, uint32_t arm_min = 0);
 
 // Forward + reverse program (loss[L], grad[L, P]); cuts the tape into
 // checkpoint segments so that the lane register file fits `reg_budget`
@@ -33,6 +42,8 @@ Schedule schedule_forward(const Tape &t, uint32_t slots, uint32_t reg_budget);
 // reads is stored when the forward sweep computes it and restored for its
 // segment's reverse sweep, so nothing is recomputed; otherwise only segment
 // inputs are stored and each segment recomputes what its rules read.
-Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots, bool save_reads = false);
+// arm_min as for schedule_forward (both sweeps).
+Schedule schedule_grad(const Tape &t, uint32_t reg_budget, uint32_t slots, bool save_reads = false,
+                       uint32_t arm_min = 0);
 
 }  // namespace ndvm

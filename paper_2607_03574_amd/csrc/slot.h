@@ -71,6 +71,9 @@ enum Form : uint32_t {
     CKLD,      // registers a .. a + n - 1 = ckpt rows r .. r + n - 1 of this lane   (x = ck_field(r, n))
     MSUB,      // d = x * y - z  (product rounded, then difference rounded)
     RSUB,      // d = z - x * y  (product rounded, then difference rounded)
+    SKIP,      // skip the next n instructions (n = imm & kSkipCountMask) when every lane of the wave has
+               // predicate register x == 0 (side bit clear: the then-arm follows) or every lane has it
+               // nonzero (side bit set: the else-arm follows); the skipped arm's results are never read
     HOT_END,
     // ---- cold forms: sine and cosine (their library code branches per
     // lane), pow, and the loss and gradient stores (masked per slot)
@@ -84,6 +87,7 @@ enum Form : uint32_t {
 enum Unary : uint32_t { U_SIN = 0, U_COS };
 
 constexpr uint32_t kFormMask = 63u;
+constexpr uint32_t kSkipSideShift = 17, kSkipCountMask = (1u << kSkipSideShift) - 1;
 constexpr uint32_t kFirstShift = 6, kImmShift = 14;
 constexpr uint32_t kMaxImm = (1u << 18) - 1;
 constexpr uint32_t kMaxBlock = 4;            // outputs of a block form (sink and trash rows reserved)
@@ -128,7 +132,9 @@ constexpr uint32_t kMaxSlots = 4;
 
 inline bool is_hot(uint32_t form) { return form >= MAC && form < HOT_END; }
 // forms whose register a is written
-inline bool writes_a(uint32_t form) { return form != CKST && form != STLOSS && form != STGRAD && form != END; }
+inline bool writes_a(uint32_t form) {
+    return form != CKST && form != STLOSS && form != STGRAD && form != SKIP && form != END;
+}
 // forms whose field x is an index rather than a register
 inline bool x_is_index(uint32_t form) {
     return form == LDOBS || form == LDPARAM || form == LDCONST || form == CKST || form == CKLD || form == STGRAD;

@@ -10,6 +10,10 @@
 //   double obsv(uint32_t i) const;  double param(uint32_t p) const;  double konst(uint32_t i) const;
 //   double ckld(uint32_t row) const;  void ckst(uint32_t row, double v) const;
 //   void settle(double v) const;  (a no-op use of v that waits for any load of v to land)
+//   void check_written(R h) const;  (the host emulator checks h holds a written value; no-op on the GPU)
+//   void skip_arm(bool then_taken, uint32_t imm) const;  (SKIP: this lane's predicate; the context
+//       decides, over the lanes that share control, whether the next imm & kSkipCountMask
+//       instructions are skipped)
 //   void store_loss(double v, bool on) const;  void store_grad(uint32_t p, double v, bool on) const;
 //   uint32_t slot() const;
 // and W is the payload of this slot's micro-op: register handles a(), x(),
@@ -259,11 +263,15 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
     case CMPLT:
         c.st(p.a(), c.ld(p.x()) < c.ld(p.y()) ? 1.0 : 0.0);
         return;
-    case SELP: {
-        const double q = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+    case SELP: {   // the untaken arm's register may hold anything (its arm may have been skipped)
+        const double q = c.ld(p.x()), y = c.ld_raw(p.y()), z = c.ld_raw(p.z());
+        c.check_written(q != 0.0 ? p.y() : p.z());
         c.st(p.a(), q != 0.0 ? y : z);
         return;
     }
+    case SKIP:   // wave-level branch skipping: every lane takes the other arm
+        c.skip_arm(c.ld(p.x()) != 0.0, p.imm());
+        return;
     case ACCSEL: {
         const auto a = p.a();
         const double x = c.ld(p.x()), q = c.ld(p.y()), g = c.ld(p.z());

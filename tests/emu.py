@@ -29,19 +29,25 @@ def lib():
 
 
 STATS = ["n_regs", "n_ckpt_rows", "n_segments", "n_instr", "fwd_ops", "recompute_ops", "rev_ops",
-         "ckpt_stored", "n_uops", "slots_used"]
+         "ckpt_stored", "n_uops", "slots_used", "n_skips"]
 
 
-def run(tape: bytes, params, obs, with_grad=True, budget=320, slots=4, save=False):
+_ARMS = {False: 0, None: 0, "option": 8, "all": 16}
+
+
+def run(tape: bytes, params, obs, with_grad=True, budget=320, slots=4, save=False, arms=False, skip=True):
     """with_grad: gradient program (loss and grad); save: the save policy
-    (values the adjoint rules read are stored, nothing recomputed)."""
+    (values the adjoint rules read are stored, nothing recomputed); arms:
+    branch arms laid out behind skip tests, "option" as the BRANCH_SKIP
+    option lays them out, "all" every arm however small; skip: then each lane
+    skips the arms it does not take (else every arm runs)."""
     params = np.ascontiguousarray(params, dtype=np.float64)
     obs = np.ascontiguousarray(obs, dtype=np.float64)
     L, P = params.shape
     loss = np.empty(L)
     grad = np.empty((L, P)) if with_grad else None
-    stats = (ctypes.c_uint64 * 10)()
-    mode = (2 if save else 1) if with_grad else 0
+    stats = (ctypes.c_uint64 * 11)()
+    mode = ((2 if save else 1) if with_grad else 0) | (0 if skip else 4) | _ARMS[arms]
     rc = lib().ndvm_emu_run(tape, len(tape), mode, budget, slots, params.ctypes.data, L, P,
                             obs.ctypes.data, obs.size, loss.ctypes.data,
                             grad.ctypes.data if grad is not None else None, P, stats)
@@ -50,12 +56,12 @@ def run(tape: bytes, params, obs, with_grad=True, budget=320, slots=4, save=Fals
     return loss, grad, dict(zip(STATS, list(stats)))
 
 
-def program(tape: bytes, with_grad=True, budget=320, slots=4, save=False):
+def program(tape: bytes, with_grad=True, budget=320, slots=4, save=False, arms=False):
     """The scheduled device program in instruction order: (headers[n_instr],
     words[n_instr, 4 rows, 4]) as uint32 arrays (padding after END included).
     The device layout is chunk-major ([chunk][row][instr][4] words), then the
     header words."""
-    mode = (2 if save else 1) if with_grad else 0
+    mode = ((2 if save else 1) if with_grad else 0) | _ARMS[arms]
     n = lib().ndvm_emu_program(tape, len(tape), mode, budget, slots, None, 0, None)
     assert n >= 0, lib().ndvm_emu_error()
     out = np.empty(n, dtype=np.uint32)

@@ -172,6 +172,81 @@ def test_emulated_random_programs_match_oracle(oracle_mod):
         assert lane_rel_err(ge[ok], go[ok]).max(initial=0) <= 1e-12
 
 
+@pytest.mark.parametrize("seed", [3, 8])
+def test_emulated_branch_skipping_is_exact(oracle_mod, seed):
+    """Branch arms behind skip tests: every lane skips the arms it does not
+    take (the most skipping any wave could do); every value a skipped arm
+    would form is NaN for that lane.  Results must equal, bit for bit, the
+    run of both arms and the program without skip tests, at two register
+    budgets and under both policies, and the oracle wherever no branch is
+    near a tie."""
+    w = configs.random_programs(n_prog=120, L=16, n=8, seed=seed)
+    n_arms = 0
+    for i, bc in enumerate(w.programs):
+        P = w.n_params_each[i]
+        p = np.ascontiguousarray(w.params[i][:, :P])
+        tape = nd.tape_build(bc)
+        lo, go, m = oracle_mod.run(bc, p, w.obs, margin=True)
+        ok = m > 1e-9
+        for budget in (320, 24):
+            for save in (False, True):
+                la, ga, _ = emu.run(tape, p, w.obs, True, budget, save=save, arms="all", skip=False)
+                lb, gb, st = emu.run(tape, p, w.obs, True, budget, save=save, arms="all", skip=True)
+                lc, gc, _ = emu.run(tape, p, w.obs, True, budget, save=save)
+                np.testing.assert_array_equal(lc, la, err_msg=f"program {i} budget {budget} save {save}")
+                np.testing.assert_array_equal(gc, ga, err_msg=f"program {i} budget {budget} save {save}")
+                np.testing.assert_array_equal(lb, la, err_msg=f"program {i} budget {budget} save {save}")
+                np.testing.assert_array_equal(gb, ga, err_msg=f"program {i} budget {budget} save {save}")
+                assert rel_err(lb[ok], lo[ok]).max(initial=0) <= 1e-13
+                assert lane_rel_err(gb[ok], go[ok]).max(initial=0) <= 1e-12
+                n_arms += st["n_skips"]
+    assert n_arms > 0
+
+
+@pytest.mark.parametrize("tree", [
+    ("iflt", ("x",), ("x",), ("c", 0), ("iflt", ("x",), ("x",), ("x",), ("c", 1))),
+    ("iflt", ("x",), ("c", 2), ("c", 0), ("iflt", ("x",), ("c", 2), ("c", 3), ("c", 1))),
+    ("iflt", ("x",), ("c", 2), ("iflt", ("x",), ("c", 2), ("c", 3), ("c", 1)), ("c", 0)),
+    ("iflt", ("x",), ("x",), ("sub", ("c", 0), ("x",)), ("iflt", ("x",), ("x",), ("x",), ("c", 1))),
+    ("mul", ("iflt", ("c", 0), ("c", 1), ("pdiv", ("c", 2), ("c", 3)), ("c", 4)),
+     ("iflt", ("c", 0), ("c", 1), ("pdiv", ("c", 2), ("c", 3)), ("x",))),
+])
+def test_emulated_nested_and_repeated_branches(oracle_mod, tree):
+    """A select reading another select of the same predicate, a branch whose
+    arm values recur after it (duplicates), exact ties: skipping and not
+    skipping agree bit for bit and with the oracle."""
+    from workloads import randtree
+    nc = randtree.n_consts(tree)
+    rng = np.random.default_rng(7)
+    n = 8
+    obs = np.concatenate([rng.uniform(-2, 2, n), rng.uniform(-1, 1, n)])
+    p = rng.uniform(-2, 2, (16, nc))
+    bc = configs.tree_program(tree, nc, n)
+    lo, go, _ = oracle_mod.run(bc, p, obs)
+    for budget in (320, 12):
+        for save in (False, True):
+            for skip in (False, True):
+                le, ge, _ = emu.run(nd.tape_build(bc), p, obs, True, budget, save=save, arms="all", skip=skip)
+                assert rel_err(le, lo).max() <= 1e-13, (budget, save, skip)
+                assert lane_rel_err(ge, go).max() <= 1e-12, (budget, save, skip)
+
+
+@pytest.mark.parametrize("case", range(len(configs.BRANCH_TREES)))
+def test_branch_population_programs_have_skippable_arms(oracle_mod, case):
+    """The programs the GPU skipping tests and the skipping study run have
+    arms the BRANCH_SKIP option marks; ordered and interleaved lanes, with
+    per-lane skipping, give the oracle's results."""
+    for order in ("sorted", "mixed", "all_then", "all_else"):
+        w = configs.branch_population(case, L=64, n=8, order=order)
+        tape = nd.tape_build(w.bytecode)
+        lo, go, _ = oracle_mod.run(w.bytecode, w.params, w.obs)
+        for save in (False, True):
+            le, ge, st = emu.run(tape, w.params, w.obs, True, 320, save=save, arms="option")
+            assert st["n_skips"] > 0
+            assert rel_err(le, lo).max() <= 1e-13
+            assert lane_rel_err(ge, go).max() <= 1e-12
+
+
 def test_emulated_edge_programs(oracle_mod):
     progs = [
         (Asm(3, 0).param(0).param(1).iflt().push(1000.0).param(2).mul().exp().else_().push(2.0)

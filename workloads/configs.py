@@ -375,6 +375,63 @@ def random_programs(n_prog: int = 1024, L: int = 1024, n: int = 128,
     return w
 
 
+# Programs whose numeric branches have heavy arms (eight value elements or
+# more each side that is heavy), for wave-level branch skipping: the same
+# lanes ordered by the branch's predicate (the waves decide alike and skip
+# arms) or interleaved (every wave runs both arms).
+_HA = ("pexp", ("ppow", ("add", ("x",), ("c", 2)), ("sin", ("mul", ("c", 3), ("x",)))))
+_HB = ("plog", ("add", ("pdiv", ("c", 4), ("x",)), ("ppow", ("x",), ("c", 2))))
+_HC = ("pdiv", ("pexp", ("mul", ("c", 2), ("c", 3))), ("plog", ("sub", ("c", 4), ("pexp", ("c", 3)))))
+BRANCH_TREES = [
+    # predicate c0 < c1, arms depend on x
+    ("add", ("iflt", ("c", 0), ("c", 1), _HA, _HB), ("x",)),
+    # a branch that does not depend on x: later loop trips repeat its values
+    ("mul", ("ppow", ("x",), ("iflt", ("c", 0), ("c", 1), _HC, ("c", 4))), ("sin", ("x",))),
+    # a select reading another select of the same predicate
+    ("iflt", ("c", 0), ("c", 1), ("c", 2), ("iflt", ("c", 0), ("c", 1), _HA, _HB)),
+    # predicate x < c0 (lanes ordered by c0 decide alike on most trips)
+    ("iflt", ("x",), ("c", 0), ("sin", _HA), _HB),
+]
+
+
+def branch_population(case: int = 0, L: int = 65536, n: int = 128, seed: int = 6006, order: str = "sorted"):
+    """Tree program BRANCH_TREES[case] (mean squared error over n points) on L
+    lanes of parameters uniform in [-2, 2], ordered so that consecutive lanes
+    decide the branch alike ("sorted") or alternately ("mixed"), or with c0
+    moved so that every lane takes the first arm ("all_then") or the second
+    ("all_else"); meta["order"] maps lane i to its index in the unordered
+    draw."""
+    tree = BRANCH_TREES[case]
+    nc = randtree.n_consts(tree)
+    r_data, r_lane, _ = _rngs(seed)
+    xs = r_data.uniform(-2.0, 2.0, n)
+    ys = r_data.uniform(-1.0, 1.0, n)
+    p = r_lane.uniform(-2.0, 2.0, (L, nc))
+    if order in ("all_then", "all_else"):
+        then = order == "all_then"
+        if case == 3:   # x < c0 with x in [-2, 2]
+            p[:, 0] = 2.5 if then else -2.5
+        else:           # c0 < c1
+            p[:, 0] = p[:, 1] - 1.0 if then else p[:, 1] + 1.0
+    key = p[:, 0] if case == 3 else (p[:, 0] < p[:, 1]).astype(np.float64)
+    idx = np.argsort(key, kind="stable")
+    if order in ("all_then", "all_else"):
+        idx = np.arange(L)
+    elif order == "mixed":
+        half = L // 2
+        mixed = np.empty(L, dtype=np.int64)
+        mixed[0:2 * half:2] = idx[:half]
+        mixed[1:2 * half:2] = idx[half:2 * half]
+        if L % 2:
+            mixed[-1] = idx[-1]
+        idx = mixed
+    elif order != "sorted":
+        raise ValueError(order)
+    return Workload("branch_population", tree_program(tree, nc, n), np.concatenate([xs, ys]),
+                    np.ascontiguousarray(p[idx]), None,
+                    meta=dict(case=case, L=L, n=n, seed=seed, order_kind=order, order=idx, tree=tree))
+
+
 BUILDERS = {
     "exp_decay": exp_decay,
     "logistic_euler": logistic,
