@@ -62,35 +62,39 @@ CSRC = os.path.join(ROOT, "paper_2607_03574_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
 
 
+# every source that decides what the replay kernel does on the GPU (front
+# end, validator, scheduler, launch code, kernel)
+REPLAY_SOURCES = ("abi.cpp", "common.h", "frontend.cpp", "kernels.hip", "sched.cpp", "sched.h", "slot.h",
+                  "slot_exec.h", "tape.cpp")
+
+
 def kernel_sources_sha256() -> str:
-    """Hash of every source that decides what the replay kernel does on the GPU
-    (front end, validator, scheduler, launch code, kernel); the host emulator is
-    left out."""
+    """Hash of the replay kernel's sources (REPLAY_SOURCES)."""
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
-        if name.endswith((".h", ".hip", ".cpp")) and name != "emu.cpp":
-            h.update(name.encode() + b"\0")
-            with open(os.path.join(CSRC, name), "rb") as f:
-                h.update(f.read())
+    for name in sorted(REPLAY_SOURCES):
+        h.update(name.encode() + b"\0")
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
 
 
-def profiled_traffic(workload: str):
-    """HBM bytes per launch of the replay kernel for `workload`, from the
-    committed rocprofv3 summary (FETCH_SIZE + WRITE_SIZE, each scaled by a copy
-    calibration); None when there is no summary or the kernel sources changed
-    since its counters were taken."""
+def profiled_traffic(workload: str, policy: str = "recompute"):
+    """HBM bytes per launch of the replay kernel for `workload` under a save
+    policy, from the committed rocprofv3 summary (FETCH_SIZE + WRITE_SIZE, each
+    scaled by a copy calibration); None when there is no summary or the kernel
+    sources changed since its counters were taken."""
     sha = kernel_sources_sha256()
     for name in sorted(os.listdir(PROFILES)):
         if not (name.startswith(f"ndvm_replay_{workload}_") and name.endswith(".md")):
             continue
-        vals = {}
+        vals = {"policy": "recompute"}
         with open(os.path.join(PROFILES, name)) as f:
             for line in f:
                 key, _, val = line.strip().partition(": ")
-                if key in ("traffic_bytes_per_launch", "kernel_sources_sha256"):
+                if key in ("traffic_bytes_per_launch", "kernel_sources_sha256", "policy"):
                     vals[key] = val
-        if vals.get("kernel_sources_sha256") == sha and "traffic_bytes_per_launch" in vals:
+        if vals.get("kernel_sources_sha256") == sha and "traffic_bytes_per_launch" in vals \
+                and vals["policy"] == policy:
             return float(vals["traffic_bytes_per_launch"])
     return None
 
@@ -441,7 +445,7 @@ def main():
         rows = host["workspace_bytes"] // (8 * ((L + 63) // 64 * 64)) - 4
         B = float(L * (8 * (2 * P + 1) + 16 * rows))
         meta["saved_doubles_per_lane"] = int(rows)
-    roof = roofline(B, flops, kern_s, profiled_traffic(args.workload))
+    roof = roofline(B, flops, kern_s, None if args.branch_skip else profiled_traffic(args.workload, args.policy))
     roof.update(kernel="ndvm_replay", kernel_ms=kern_s * 1e3, kernel_ms_median=res["kernel_median_s"] * 1e3,
                 kernel_ms_iqr=res["kernel_iqr_s"] * 1e3)
     out = {

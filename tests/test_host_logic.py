@@ -338,8 +338,11 @@ def test_bench_traffic_only_for_matching_kernel_sources(tmp_path, monkeypatch):
         f"text\n\n    traffic_bytes_per_launch: 12345\n    kernel_sources_sha256: {sha}\n")
     (tmp_path / "ndvm_replay_kalman_cv4_L16384.md").write_text(
         "    traffic_bytes_per_launch: 999\n    kernel_sources_sha256: " + "0" * 64 + "\n")
+    (tmp_path / "ndvm_replay_logistic_euler_L4096_save.md").write_text(
+        f"    policy: save\n    traffic_bytes_per_launch: 777\n    kernel_sources_sha256: {sha}\n")
     monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
     assert bench.profiled_traffic("logistic_euler") == 12345.0
+    assert bench.profiled_traffic("logistic_euler", "save") == 777.0
     assert bench.profiled_traffic("kalman_cv4") is None      # counters of another kernel build
     assert bench.profiled_traffic("exp_decay") is None       # no summary
 
