@@ -386,6 +386,9 @@ def main():
     ap.add_argument("--branch-study", action="store_true",
                     help="branch skipping on programs with heavy arms: lanes ordered by the predicate or "
                          "interleaved, with and without the option")
+    ap.add_argument("--walk", action="store_true",
+                    help="the device walker (structural walk on the GPU, no tape, no scheduling) on the workload, "
+                         "against the scheduled replay, host work included")
     ap.add_argument("--flatten", action="store_true",
                     help="data axis flattened into the lanes (exp_decay, random_programs), against the unflattened step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -420,6 +423,8 @@ def main():
         return flattened_bench(args, torch)
     if args.branch_study:
         return branch_study(args, torch)
+    if args.walk:
+        return walk_bench(args, torch)
     device = torch.device("cuda:0")
     stream = torch.cuda.Stream(device=device)
     with torch.cuda.stream(stream):
@@ -484,6 +489,52 @@ def flattened_bench(args, torch):
            "unflattened_ms_per_step": ures["wall_s"] / args.steps * 1e3,
            "speedup": ures["wall_s"] / res["wall_s"], "dtype": "f64", "data": "synthetic",
            "config": meta, "host": host, "steps": args.steps, "warmup": args.warmup}
+    print(json.dumps(out), flush=True)
+
+
+def walk_bench(args, torch):
+    """The device walker on the workload (scalar programs): host work
+    (validation, measurement and one copy of the bytecode), the walk's kernel
+    time (HIP events over the timed steps) and lane-grads/s, next to the
+    scheduled replay's host work (trace, upload, scheduling) and kernel time
+    on the same inputs.  One JSON line."""
+    import paper_2607_03574_amd as nd
+    device = torch.device("cuda:0")
+    stream = torch.cuda.Stream(device=device)
+    w = configs.build(args.workload)
+    progs = w.programs if args.workload == "random_programs" else [w.bytecode]
+    params = w.params if args.workload == "random_programs" else w.params[None]
+    n_prog, L, P = params.shape
+    with torch.cuda.stream(stream):
+        t0 = time.perf_counter()
+        ws = nd.walk_prepare(progs, stream=stream)
+        t1 = time.perf_counter()
+        need = nd.walk_workspace_bytes(ws, L)
+        p = torch.tensor(params, device=device)
+        o = torch.tensor(w.obs, device=device)
+        work = torch.empty(max(need, 8), dtype=torch.uint8, device=device)
+        loss = torch.empty((n_prog, L), dtype=torch.float64, device=device)
+        grad = torch.zeros((n_prog, L, P), dtype=torch.float64, device=device)
+    torch.cuda.synchronize()
+
+    def step(s):
+        nd.walk_grad(ws, p, o, loss, grad, work, s)
+    res = time_steps(torch, stream, step, args.steps, args.warmup)
+    nd.walk_status(work, stream)
+    kern = res["kernel_mean_s"]
+    with torch.cuda.stream(stream):
+        _, rstep, _, _, _, _, host = build_inputs(args.workload, torch, device)
+    torch.cuda.synchronize()
+    rres = time_steps(torch, stream, rstep, args.steps, args.warmup)
+    out = {"metric": "lane-gradient evals/sec (fwd+rev) on 1 MI355X, device walker", "workload": w.name,
+           "value": n_prog * L / (res["wall_s"] / args.steps), "unit": "lane-gradient evals/s",
+           "kernel_ms": kern * 1e3, "kernel_ms_median": res["kernel_median_s"] * 1e3,
+           "host_prepare_s": t1 - t0, "workspace_bytes": int(need),
+           "end_to_end_s": (t1 - t0) + kern,
+           "replay_kernel_ms": rres["kernel_mean_s"] * 1e3, "replay_host_s": host["total_host_s"],
+           "replay_end_to_end_s": host["total_host_s"] + rres["kernel_mean_s"],
+           "dtype": "f64", "data": "synthetic", "programs": n_prog, "lanes_per_program": L,
+           "steps": args.steps, "warmup": args.warmup}
     print(json.dumps(out), flush=True)
 
 

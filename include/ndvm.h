@@ -258,6 +258,84 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
 ndvm_status ndvm_workspace_bytes_many(const ndvm_tape *const *tapes, int n_prog, int64_t L,
                                       size_t *bytes);
 
+/*
+ * Device walker (Section 9, "What remains designed and unbuilt", and
+ * Appendix A: the structural walk on the device under wave-ballot lane
+ * masks; Section 3.4 define-by-run tape; Section 6 lane masking; Appendix C
+ * adjoints).  No tape is built and nothing is scheduled on the host: the
+ * host only validates the bytecode and measures its structure (stack depth,
+ * locals, nesting, a bound on the nodes a walk records) without unrolling
+ * it, then copies the program set to the GPU once.  One wave walks a program
+ * for 64 lanes; a numeric IFLT runs each arm under the mask of the lanes that
+ * take it (one ballot; an arm no lane takes is not walked) and merges what
+ * the two arms left different, per lane.  Per lane the result is the loss
+ * and exact gradient of that lane's realized trace (Section 4, Property 1),
+ * the values ndvm_grad returns for the same program.
+ *
+ * Scalar programs only: bytecode with a matrix word (DOT, MATMUL, TRANSPOSE,
+ * INV, DET, LOGDET, TRACE, OUTER, PACK, INDEX) is NDVM_E_UNSUPPORTED.  Every
+ * IFLT's arms must leave the same stack depth and set the same locals
+ * (NDVM_E_STRUCT_DIVERGE), also where both operands are constants (the tape
+ * path resolves such a branch on the host and accepts any arms).
+ */
+typedef struct ndvm_walk ndvm_walk;
+
+/* Validate `n_prog` bytecode programs (bytecodes[q], lens[q] bytes each, all
+ * with the same observation count) and copy them to the current device on
+ * `stream` (synchronised before returning).  *out receives a handle owned by
+ * the library (ndvm_walk_free).  Errors: NDVM_E_ARG (null pointers, n_prog
+ * <= 0, differing observation counts), NDVM_E_BYTECODE, NDVM_E_STRUCT_DIVERGE,
+ * NDVM_E_UNSUPPORTED (matrix words, limits: stack depth 256, 256 locals,
+ * nesting 64, 2^24 nodes), NDVM_E_NOMEM, NDVM_E_DEVICE; the message names
+ * the program. */
+ndvm_status ndvm_walk_prepare(const uint8_t *const *bytecodes, const size_t *lens, int n_prog, void *stream,
+                              ndvm_walk **out);
+
+typedef struct {
+    uint32_t n_params, n_obs;
+    uint64_t n_nodes;     /* bound on the nodes one wave's walk records (parameters included) */
+    uint32_t depth;       /* largest operand stack depth */
+    uint32_t n_locals;    /* locals referenced */
+    uint32_t n_frames;    /* deepest IFLT nesting */
+    uint32_t n_loops;     /* deepest LOOP nesting */
+} ndvm_walk_info;
+
+/* Host only: the validation and structural measurement ndvm_walk_prepare
+ * applies to one program, without touching a device.  Library
+ * infrastructure.  Errors: as ndvm_walk_prepare for one program. */
+ndvm_status ndvm_walk_measure(const uint8_t *bytecode, size_t len, ndvm_walk_info *out);
+
+/* Workspace bytes of ndvm_walk_grad for L lanes per program: a status word
+ * and, per wave slot of the launch (enough waves to fill the GPU, at most one
+ * per 64 lanes of every program), 1,048 bytes per node the largest program
+ * can record (values and adjoints of 64 lanes, the node record).  Host only.
+ * Errors: NDVM_E_ARG. */
+ndvm_status ndvm_walk_workspace_bytes(const ndvm_walk *w, int64_t L, size_t *bytes);
+
+/* The walk of every program of the set for L lanes each, on `stream`.
+ * params: program q, lane l, parameter p at params[q*prog_stride_p + l*ld_p
+ * + p]; ld_p and ld_g at least the largest parameter count; the strides are
+ * read only when the set has more than one program.  obs[n_obs] is shared.
+ * loss[q*L + l]; grad as params with ld_g, prog_stride_g (columns beyond a
+ * program's own parameter count are not written).  workspace: device memory
+ * of ndvm_walk_workspace_bytes bytes (its status word is cleared on
+ * `stream`).  Enqueues only.  Errors: NDVM_E_ARG (null pointers, L < 0,
+ * n_obs mismatch, leading dimensions or strides too small, another current
+ * device), NDVM_E_NOMEM (workspace too small), NDVM_E_DEVICE. */
+ndvm_status ndvm_walk_grad(const ndvm_walk *w, const double *params, int64_t L, int64_t ld_p,
+                           int64_t prog_stride_p, const double *obs, int64_t n_obs, double *loss, double *grad,
+                           int64_t ld_g, int64_t prog_stride_g, void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/* Synchronise `stream` and read the status word of a workspace ndvm_walk_grad
+ * used: NDVM_E_INTERNAL if a wave met a bound the validation should have
+ * excluded (its lanes then hold NaN), else NDVM_OK.  Library
+ * infrastructure.  Errors: NDVM_E_ARG, NDVM_E_DEVICE, NDVM_E_INTERNAL. */
+ndvm_status ndvm_walk_status(const void *workspace, void *stream);
+
+/* Release a walker program set (NULL is ignored); as ndvm_tape_free. */
+void ndvm_walk_free(ndvm_walk *w);
+
 /* Release a tape handle (NULL is ignored).  Waits for nothing: the caller
  * must not free a tape while work that uses it is still pending. */
 void ndvm_tape_free(ndvm_tape *tape);

@@ -28,7 +28,8 @@ NOALLOC_SCRATCH_BYTES = 64 << 20    # NDVM_NOALLOC_SCRATCH_BYTES
 EXPORTS = ["ndvm_tape_build", "ndvm_tape_upload", "ndvm_tape_info_get", "ndvm_workspace_bytes",
            "ndvm_forward", "ndvm_grad", "ndvm_grad_many", "ndvm_workspace_bytes_many",
            "ndvm_tape_free", "ndvm_free", "ndvm_last_error", "ndvm_adam_step", "ndvm_grad_noalloc",
-           "ndvm_grad_points", "ndvm_workspace_bytes_points"]
+           "ndvm_grad_points", "ndvm_workspace_bytes_points", "ndvm_walk_prepare", "ndvm_walk_measure", "ndvm_walk_workspace_bytes",
+           "ndvm_walk_grad", "ndvm_walk_status", "ndvm_walk_free"]
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_03574_amd/build.py "
@@ -64,6 +65,22 @@ _grad_points = _sig("ndvm_grad_points", _int, [_vp, _vp, _i64, _i64, _vp, _i64, 
 _ws_bytes_points = _sig("ndvm_workspace_bytes_points", _int, [_vp, _i64, _i64, ctypes.POINTER(_sz)])
 _grad_many = _sig("ndvm_grad_many", _int, [ctypes.POINTER(_vp), _int, _vp, _i64, _i64, _i64, _vp, _i64, _vp,
                                             _vp, _i64, _i64, _vp, _sz, _vp])
+_walk_prepare = _sig("ndvm_walk_prepare", _int, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_sz), _int, _vp,
+                                                  ctypes.POINTER(_vp)])
+_walk_ws_bytes = _sig("ndvm_walk_workspace_bytes", _int, [_vp, _i64, ctypes.POINTER(_sz)])
+_walk_grad = _sig("ndvm_walk_grad", _int, [_vp, _vp, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _i64, _vp, _sz,
+                                            _vp])
+_walk_status = _sig("ndvm_walk_status", _int, [_vp, _vp])
+_walk_free = _sig("ndvm_walk_free", None, [_vp])
+
+
+class _WalkInfo(ctypes.Structure):
+    _fields_ = [("n_params", ctypes.c_uint32), ("n_obs", ctypes.c_uint32), ("n_nodes", ctypes.c_uint64),
+                ("depth", ctypes.c_uint32), ("n_locals", ctypes.c_uint32), ("n_frames", ctypes.c_uint32),
+                ("n_loops", ctypes.c_uint32)]
+
+
+_walk_measure = _sig("ndvm_walk_measure", _int, [ctypes.c_char_p, _sz, ctypes.POINTER(_WalkInfo)])
 _tape_free = _sig("ndvm_tape_free", None, [_vp])
 _free = _sig("ndvm_free", None, [_vp])
 _last_error = _sig("ndvm_last_error", ctypes.c_char_p, [])
@@ -320,6 +337,81 @@ def grad_many(tapes: Sequence[Tape], params, obs, loss=None, grad_out=None, work
                           obs.numel(), loss.data_ptr(), grad_out.data_ptr(), ldg,
                           sg, ws.data_ptr(), nbytes, s.cuda_stream), "ndvm_grad_many")
     return loss, grad_out
+
+
+class WalkSet:
+    """Owner of a program set prepared for the device walker."""
+
+    def __init__(self, handle: int, n_prog: int):
+        self.handle = handle
+        self.n_prog = n_prog
+
+    def __del__(self, _free_fn=_walk_free, _finalizing=sys.is_finalizing):
+        h, self.handle = getattr(self, "handle", None), None
+        if h and not _finalizing():
+            _free_fn(h)
+
+
+def walk_prepare(bytecodes: Sequence[bytes], stream=None) -> WalkSet:
+    """Validate stack-bytecode programs and copy them to the GPU for the
+    device walker (ndvm_walk_prepare): no tape, no scheduling."""
+    n = len(bytecodes)
+    arr = (ctypes.c_char_p * n)(*bytecodes)
+    lens = (_sz * n)(*[len(b) for b in bytecodes])
+    h = _vp()
+    _check(_walk_prepare(arr, lens, n, _stream_ptr(stream), ctypes.byref(h)), "ndvm_walk_prepare")
+    return WalkSet(h.value, n)
+
+
+def walk_measure(bytecode: bytes) -> dict:
+    """Host-only validation and structural measurement of one program for the
+    device walker (ndvm_walk_measure)."""
+    info = _WalkInfo()
+    _check(_walk_measure(bytecode, len(bytecode), ctypes.byref(info)), "ndvm_walk_measure")
+    return {k: getattr(info, k) for k, _ in _WalkInfo._fields_}
+
+
+def walk_workspace_bytes(ws: WalkSet, L: int) -> int:
+    n = _sz()
+    _check(_walk_ws_bytes(ws.handle, int(L), ctypes.byref(n)), "ndvm_walk_workspace_bytes")
+    return n.value
+
+
+def walk_grad(ws: WalkSet, params, obs, loss=None, grad_out=None, workspace=None, stream=None):
+    """The device walk of every program of the set: params[n_prog, L, Pmax]
+    (or [L, P] for one program) -> loss, grad of the same leading shape
+    (entries beyond a program's own P are left as is)."""
+    import torch
+    _dev_f64(params, "params")
+    _dev_f64(obs, "obs")
+    single = params.dim() == 2
+    p3 = params.unsqueeze(0) if single else params
+    if p3.dim() != 3 or p3.stride(2) != 1 or not obs.is_contiguous():
+        raise ValueError("params must be [n_prog, L, Pmax] (or [L, P]) with unit inner stride")
+    n_prog, L, P = p3.shape
+    if n_prog != ws.n_prog:
+        raise ValueError("one parameter block per program of the set")
+    need = walk_workspace_bytes(ws, L)
+    s = _launch_stream(stream, params.device)
+    with torch.cuda.stream(s):
+        if loss is None:
+            loss = torch.empty((n_prog, L) if not single else (L,), dtype=torch.float64, device=params.device)
+        if grad_out is None:
+            grad_out = torch.zeros(tuple(params.shape), dtype=torch.float64, device=params.device)
+        g3 = grad_out.unsqueeze(0) if single else grad_out
+        work, nbytes = _workspace(need, params.device, workspace)
+        ldp, ldg = _ld(p3, 1), _ld(g3, 1)
+        sp = p3.stride(0) if n_prog > 1 else L * ldp
+        sg = g3.stride(0) if n_prog > 1 else L * ldg
+        _check(_walk_grad(ws.handle, p3.data_ptr(), L, ldp, sp, obs.data_ptr(), obs.numel(), loss.data_ptr(),
+                          g3.data_ptr(), ldg, sg, work.data_ptr(), nbytes, s.cuda_stream), "ndvm_walk_grad")
+    return loss, grad_out
+
+
+def walk_status(workspace, stream=None):
+    """Synchronise `stream` and raise if a walk that used `workspace` met a
+    bound its validation should have excluded (ndvm_walk_status)."""
+    _check(_walk_status(workspace.data_ptr(), _stream_ptr(stream)), "ndvm_walk_status")
 
 
 def adam_step(params, grad_in, m, v, t: int, lr: float, beta1: float = 0.9, beta2: float = 0.999,

@@ -20,7 +20,7 @@ BUILD = os.path.join(HERE, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["frontend.cpp", "tape.cpp", "sched.cpp", "abi.cpp", "kernels.hip", "optim.hip"]
+SOURCES = ["frontend.cpp", "tape.cpp", "sched.cpp", "abi.cpp", "kernels.hip", "optim.hip", "walk_host.cpp", "walk.hip"]
 EMU_SOURCES = ["frontend.cpp", "tape.cpp", "sched.cpp", "emu.cpp"]
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-ffp-contract=off", "-fno-fast-math", "-Wall",
           "-Wno-unused-function"]

@@ -1,0 +1,88 @@
+// Device walker: definitions shared by its host part (walk_host.cpp) and its
+// kernel (walk.hip).
+//
+// The walker runs the structural walk of a stack-bytecode program on the
+// GPU -- the device interpreter the paper leaves as designed but unbuilt
+// (Section 9, "What remains designed and unbuilt"; Appendix A): one wave
+// walks the program for 64 lanes.  Structure (program counter, operand stack, locals,
+// loop counters) is the same for every lane and is kept once per wave; each
+// numeric word records one node whose per-lane value goes to the wave's
+// value rows in HBM (define-by-run, Section 3.4).  A numeric IFLT runs each
+// arm under the mask of the lanes that take it (one ballot; an arm no lane
+// takes is skipped), and at ENDIF every stack position and local the two
+// arms left different becomes a MERGE node that picks, per lane, the value
+// of the arm the lane took (Section 6, lane-masked divergent control).  The
+// reverse sweep walks the recorded nodes backwards with per-lane adjoints
+// (Appendix C, table tab:adjoints).
+#pragma once
+#include <cstdint>
+
+namespace ndvm {
+namespace walk {
+
+// One program in the device buffer.  Offsets count 32-bit words from the
+// start of the buffer; the constants start 8-byte aligned.
+struct ProgDesc {
+    uint32_t code_off;    // n_instr instruction words, 2 x u32 each: op | a << 8 | b << 16, imm
+    uint32_t match_off;   // n_instr int32: LOOP -> ENDLOOP, IFLT -> ELSE, ELSE -> ENDIF, else -1
+    uint32_t const_off;   // n_consts doubles
+    uint32_t n_instr;
+    uint32_t n_params, n_obs;
+    uint32_t n_nodes;     // bound on the nodes one wave records (parameters included)
+    uint32_t depth;       // bound on the operand stack depth
+    uint32_t n_locals;    // locals referenced (largest index + 1)
+    uint32_t n_frames;    // bound on IFLT nesting
+    uint32_t n_loops;     // bound on LOOP nesting
+    uint32_t n_steps;     // bound on the words one walk executes (the walk stops there)
+};
+
+// Node kinds beyond the bytecode's numeric opcodes (which keep their numbers).
+constexpr uint32_t kLeaf = 0x01;    // constant or observation: takes no adjoint
+constexpr uint32_t kParam = 0x02;   // parameter p = node p
+constexpr uint32_t kMerge = 0x40;   // per-lane pick of two arms' values (a if the lane took the first arm)
+
+// Recorded node (one per node and wave, 24 bytes): its operand nodes and,
+// for a MERGE, the ballot word of the lanes that took the first arm.
+struct Node {
+    uint32_t op, a, b, pad;
+    uint64_t mask;
+};
+
+// Per-wave workspace: values[n_nodes][64], adjoints[n_nodes][64] (fp64),
+// nodes[n_nodes].
+constexpr uint64_t ws_bytes_per_node() { return 64 * 8 * 2 + sizeof(Node); }
+
+// Words of LDS one wave uses for its structural state: stack, locals, loop
+// frames (start, trips, counter), IFLT frames (masks, phase, two snapshots of
+// stack + locals), and two flag bits per node (leaf, adjoint touched).
+constexpr uint32_t kFrameFixed = 8;
+inline uint32_t lds_words(uint32_t depth, uint32_t n_locals, uint32_t n_loops, uint32_t n_frames,
+                          uint32_t n_nodes) {
+    const uint32_t snap = depth + n_locals;
+    return depth + n_locals + 3 * n_loops + n_frames * (kFrameFixed + 2 * snap) + (n_nodes + 15) / 16;
+}
+
+// Limits the host validator enforces.
+constexpr uint32_t kMaxDepth = 256, kMaxLocals = 256, kMaxFrames = 64, kMaxLoops = 64;
+constexpr uint64_t kMaxNodes = 1u << 24;
+
+struct Args {
+    const uint32_t *buf;        // device buffer: ProgDesc[n_prog] then code, matches, constants
+    uint32_t n_prog;
+    int64_t L;                  // lanes per program
+    const double *params;       // [n_prog][L][ld_p] (program stride prog_stride_p)
+    int64_t ld_p, prog_stride_p;
+    const double *obs;          // shared by every program
+    double *loss;               // [n_prog][L]
+    double *grad;               // [n_prog][L][ld_g] (program stride prog_stride_g)
+    int64_t ld_g, prog_stride_g;
+    uint8_t *ws;                // per wave slot: n_nodes_max * ws_bytes_per_node() bytes
+    uint32_t n_nodes_max;       // nodes per wave slot
+    uint32_t lds_words;         // LDS words per wave
+    uint32_t depth, n_locals, n_loops, n_frames;   // LDS layout bounds (maxima over the programs)
+    uint64_t n_items;           // work items: n_prog * ceil(L / 64)
+    int *status;                // device word: 0, or a nonzero code when a wave met a bound it must not pass
+};
+
+}  // namespace walk
+}  // namespace ndvm
