@@ -285,9 +285,11 @@ typedef struct ndvm_walk ndvm_walk;
  * `stream` (synchronised before returning).  *out receives a handle owned by
  * the library (ndvm_walk_free).  Errors: NDVM_E_ARG (null pointers, n_prog
  * <= 0, differing observation counts), NDVM_E_BYTECODE, NDVM_E_STRUCT_DIVERGE,
- * NDVM_E_UNSUPPORTED (matrix words, limits: stack depth 256, 256 locals,
- * nesting 64, 2^24 nodes), NDVM_E_NOMEM, NDVM_E_DEVICE; the message names
- * the program. */
+ * NDVM_E_UNSUPPORTED (matrix words; limits: stack depth 64, 32 locals,
+ * nesting 32, 2^24 nodes, and the wave's structural state -- value rows of
+ * the parameters and of the stack and locals, node numbers, frames and two
+ * flag bits per node -- within 64 KiB of LDS), NDVM_E_NOMEM, NDVM_E_DEVICE;
+ * the message names the program. */
 ndvm_status ndvm_walk_prepare(const uint8_t *const *bytecodes, const size_t *lens, int n_prog, void *stream,
                               ndvm_walk **out);
 

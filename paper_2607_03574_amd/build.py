@@ -24,20 +24,26 @@ SOURCES = ["frontend.cpp", "tape.cpp", "sched.cpp", "abi.cpp", "kernels.hip", "o
 EMU_SOURCES = ["frontend.cpp", "tape.cpp", "sched.cpp", "emu.cpp"]
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-ffp-contract=off", "-fno-fast-math", "-Wall",
           "-Wno-unused-function"]
-DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          # the interpreter's dispatch branches are wave-uniform: leave such
-          # regions unstructured instead of routing every handler exit through
-          # a chain of flow blocks
-          "-mllvm", "-structurizecfg-skip-uniform-regions=true",
-          # keep every handler's final register store in the handler: sunk
-          # into a shared block it would wait there for the memory traffic
-          # of every other handler (the program prefetch included)
-          "-mllvm", "-sink-common-insts=false", "-mllvm", "-enable-tail-merge=false"]
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# the replay kernel's options
+REPLAY = [
+    # the interpreter's dispatch branches are wave-uniform: leave such
+    # regions unstructured instead of routing every handler exit through a
+    # chain of flow blocks
+    "-mllvm", "-structurizecfg-skip-uniform-regions=true",
+    # keep every handler's final register store in the handler: sunk into a
+    # shared block it would wait there for the memory traffic of every other
+    # handler (the program prefetch included)
+    "-mllvm", "-sink-common-insts=false", "-mllvm", "-enable-tail-merge=false"]
+# sources built with the replay kernel's options (the device walker is not:
+# with its loops the first option makes the code generator fail)
+REPLAY_OPTIONS_FOR = {"frontend.cpp", "tape.cpp", "sched.cpp", "abi.cpp", "kernels.hip", "optim.hip", "emu.cpp"}
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC] + COMMON + DEVICE + ["-c", os.path.join(CSRC, src), "-o", obj]
+    extra = REPLAY if src in REPLAY_OPTIONS_FOR else []
+    cmd = [HIPCC] + COMMON + DEVICE + extra + ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     err = "\n".join(l for l in (r.stderr or "").splitlines() if noise not in l)

@@ -52,18 +52,30 @@ struct Node {
 // nodes[n_nodes].
 constexpr uint64_t ws_bytes_per_node() { return 64 * 8 * 2 + sizeof(Node); }
 
-// Words of LDS one wave uses for its structural state: stack, locals, loop
-// frames (start, trips, counter), IFLT frames (masks, phase, two snapshots of
-// stack + locals), and two flag bits per node (leaf, adjoint touched).
+// LDS of one wave.  Rows of 64 doubles first: the parameters' values, then
+// the operand stack's and the locals' values during the forward walk, whose
+// rows the parameters' adjoints take over in the reverse sweep.  Then 32-bit
+// words: the operand stack's and locals' node numbers, loop frames (start,
+// trips, counter), IFLT frames (masks, phase, two snapshots of stack +
+// locals node numbers), and two flag bits per node (leaf, adjoint touched).
 constexpr uint32_t kFrameFixed = 8;
-inline uint32_t lds_words(uint32_t depth, uint32_t n_locals, uint32_t n_loops, uint32_t n_frames,
+constexpr uint32_t lds_rows(uint32_t depth, uint32_t n_locals, uint32_t n_params) {
+    const uint32_t fwd = depth + n_locals;
+    return n_params + (fwd > n_params ? fwd : n_params);
+}
+constexpr uint32_t lds_words(uint32_t depth, uint32_t n_locals, uint32_t n_loops, uint32_t n_frames,
                           uint32_t n_nodes) {
     const uint32_t snap = depth + n_locals;
     return depth + n_locals + 3 * n_loops + n_frames * (kFrameFixed + 2 * snap) + (n_nodes + 15) / 16;
 }
+constexpr uint64_t lds_bytes(uint32_t depth, uint32_t n_locals, uint32_t n_loops, uint32_t n_frames, uint32_t n_nodes,
+                          uint32_t n_params) {
+    return 512ull * lds_rows(depth, n_locals, n_params) + 4ull * lds_words(depth, n_locals, n_loops, n_frames, n_nodes);
+}
 
 // Limits the host validator enforces.
-constexpr uint32_t kMaxDepth = 256, kMaxLocals = 256, kMaxFrames = 64, kMaxLoops = 64;
+constexpr uint32_t kMaxDepth = 64, kMaxLocals = 32, kMaxFrames = 32, kMaxLoops = 32;
+constexpr uint64_t kMaxLdsBytes = 64 * 1024;   // a workgroup's LDS
 constexpr uint64_t kMaxNodes = 1u << 24;
 
 struct Args {
@@ -78,8 +90,8 @@ struct Args {
     int64_t ld_g, prog_stride_g;
     uint8_t *ws;                // per wave slot: n_nodes_max * ws_bytes_per_node() bytes
     uint32_t n_nodes_max;       // nodes per wave slot
-    uint32_t lds_words;         // LDS words per wave
-    uint32_t depth, n_locals, n_loops, n_frames;   // LDS layout bounds (maxima over the programs)
+    uint32_t lds_bytes;         // LDS bytes per wave
+    uint32_t depth, n_locals, n_loops, n_frames, n_params;   // LDS layout bounds (maxima over the programs)
     uint64_t n_items;           // work items: n_prog * ceil(L / 64)
     int *status;                // device word: 0, or a nonzero code when a wave met a bound it must not pass
 };

@@ -5,16 +5,19 @@
 // Control is the same for every lane of a wave: program counter, operand
 // stack (node numbers), locals, loop counters and branch frames live once
 // per wave in LDS and are read back as wave-uniform values.  Numbers are
-// per lane: node k's values are a coalesced row of 64 doubles in the wave's
-// HBM slot.  A numeric IFLT takes one ballot: each arm runs under the mask
-// of the lanes that take it, an arm no lane takes is not walked at all, and
-// when both arms ran their differing stack positions and locals become MERGE
-// nodes (Section 6, lane masking).  The reverse sweep visits the recorded
-// nodes from last to first and applies the adjoint rules of Appendix C,
-// table tab:adjoints, per lane, gated on a nonzero incoming adjoint; an
-// adjoint row is written in full by its first contribution (zero where the
-// rule does not apply), so no row is cleared beforehand, and a node no rule
-// reached is skipped without a read.
+// per lane.  The forward walk keeps the operand stack's and the locals'
+// values in LDS rows (one double per lane), so a word reads its operands
+// there; every node it records is also stored, as a coalesced row of 64
+// doubles, to the wave's slot in HBM for the reverse sweep.  A numeric IFLT
+// takes one ballot: each arm runs under the mask of the lanes that take it,
+// an arm no lane takes is not walked at all, and when both arms ran their
+// differing stack positions and locals become MERGE nodes (Section 6, lane
+// masking).  The reverse sweep visits the recorded nodes from last to first
+// and applies the adjoint rules of Appendix C, table tab:adjoints, per lane,
+// gated on a nonzero incoming adjoint; an adjoint row is written in full by
+// its first contribution (zero where the rule does not apply), so no row is
+// cleared beforehand, and a node no rule reached is skipped without a read.
+// The parameters' values and adjoints stay in LDS.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -31,6 +34,16 @@ using walk::ProgDesc;
 
 constexpr uint32_t kUnset = 0xFFFFFFFFu;
 
+// Read-only inputs (the program buffer, the observations) are read through
+// the constant address space, so wave-uniform reads become scalar loads that
+// wait for nothing else (a vector load would wait for every store the walk
+// has in flight before it).
+#define AS_CONST __attribute__((address_space(4)))
+template <class T>
+__device__ __forceinline__ const AS_CONST T *cst(const T *p) {
+    return (const AS_CONST T *)(p);
+}
+
 __device__ __forceinline__ uint32_t uni(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ uint64_t uni64(uint64_t v) {
     return uint64_t(uni(uint32_t(v))) | uint64_t(uni(uint32_t(v >> 32))) << 32;
@@ -42,6 +55,18 @@ __device__ __forceinline__ bool is_binary(uint32_t op) {
     return op == bc::ADD || op == bc::SUB || op == bc::MUL || op == bc::DIV || op == bc::POW;
 }
 
+// Library transcendentals out of line: inlined in both sweeps they would
+// hold the walk's registers (and its occupancy) hostage.
+__device__ __noinline__ double transcendental(uint32_t op, double x, double y) {
+    switch (op) {
+    case bc::EXP: return exp(x);
+    case bc::LOG: return log(x);
+    case bc::SIN: return sin(x);
+    case bc::COS: return cos(x);
+    default: return pow(x, y);
+    }
+}
+
 // forward value of a scalar word
 __device__ __forceinline__ double forward(uint32_t op, double x, double y) {
     switch (op) {
@@ -50,13 +75,10 @@ __device__ __forceinline__ double forward(uint32_t op, double x, double y) {
     case bc::MUL: return x * y;
     case bc::DIV: return x / y;
     case bc::NEG: return -x;
-    case bc::EXP: return exp(x);
-    case bc::LOG: return log(clampv(x));
     case bc::SQRT: return sqrt(clampv(x));
-    case bc::SIN: return sin(x);
-    case bc::COS: return cos(x);
     case bc::ABS: return fabs(x);
-    default: return pow(x, y);   // POW
+    case bc::LOG: return transcendental(bc::LOG, clampv(x), 0.0);
+    default: return transcendental(op, x, y);   // EXP SIN COS POW
     }
 }
 
@@ -76,8 +98,16 @@ __device__ __forceinline__ void stack_effect(uint32_t op, uint32_t *pops, uint32
 
 struct Wave {
     uint32_t lane;
+    uint32_t P;   // parameters of the current program
+    // LDS: value rows (64 doubles each)
+    double *VP;   // parameters' values
+    double *VS;   // operand stack values (forward)
+    double *VL;   // locals' values (forward)
+    double *GP;   // parameters' adjoints (reverse; the rows of VS and VL)
+    // LDS: structural words
     uint32_t *stk, *loc, *lps, *frm, *flg;
     uint32_t snap, fsz, depth;
+    // HBM slot of the wave
     double *V, *G;
     Node *E;
 
@@ -87,8 +117,15 @@ struct Wave {
         const uint32_t w = uni(flg[k >> 4]);
         flg[k >> 4] = w | bit << ((k & 15) * 2);
     }
-    __device__ __forceinline__ double &v(uint32_t k) const { return V[uint64_t(k) * 64 + lane]; }
-    __device__ __forceinline__ double &g(uint32_t k) const { return G[uint64_t(k) * 64 + lane]; }
+    __device__ __forceinline__ double &s(uint32_t i) const { return VS[i * 64 + lane]; }
+    __device__ __forceinline__ double &l(uint32_t j) const { return VL[j * 64 + lane]; }
+    // value and adjoint of node k (parameters in LDS, the others in HBM)
+    __device__ __forceinline__ double &v(uint32_t k) const {
+        return k < P ? VP[k * 64 + lane] : V[uint64_t(k) * 64 + lane];
+    }
+    __device__ __forceinline__ double &g(uint32_t k) const {
+        return k < P ? GP[k * 64 + lane] : G[uint64_t(k) * 64 + lane];
+    }
 
     // adjoint of node j += c (or -= c) where `apply`; the first contribution
     // writes the whole row (0 + c, or 0 where the rule does not apply)
@@ -108,30 +145,49 @@ struct Wave {
 
 // Walk one work item (64 lanes of one program); returns false when a bound
 // the host validation guarantees was not met (the lanes then hold NaN).
-__device__ bool walk_item(const Args &A, const Wave &W, const ProgDesc &D, uint32_t q, int64_t l0) {
+__device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q, int64_t l0) {
     const uint32_t lane = W.lane;
     const int64_t lg = l0 + lane;
     const bool active = lg < A.L;
     const int64_t lc = active ? lg : A.L - 1;
-    const uint32_t *code = A.buf + D.code_off;
-    const int32_t *match = reinterpret_cast<const int32_t *>(A.buf + D.match_off);
-    const double *K = reinterpret_cast<const double *>(A.buf + D.const_off);
+    const AS_CONST uint32_t *code = cst(A.buf + D.code_off);
+    const AS_CONST int32_t *match = cst(reinterpret_cast<const int32_t *>(A.buf + D.match_off));
+    const AS_CONST double *K = cst(reinterpret_cast<const double *>(A.buf + D.const_off));
+    const AS_CONST double *obs = cst(A.obs);
     const double *prm = A.params + int64_t(q) * A.prog_stride_p + lc * A.ld_p;
     const uint32_t n_nodes = D.n_nodes, P = D.n_params;
     if (n_nodes > A.n_nodes_max || D.depth > A.depth || D.n_locals > A.n_locals || D.n_loops > A.n_loops ||
-        D.n_frames > A.n_frames)
+        D.n_frames > A.n_frames || P > A.n_params)
         return false;
+    W.P = P;
 
     for (uint32_t i = lane; i < (n_nodes + 15) / 16; i += 64) W.flg[i] = 0;
     for (uint32_t i = lane; i < D.n_locals; i += 64) W.loc[i] = kUnset;
-    for (uint32_t p = 0; p < P; ++p) W.v(p) = prm[p];
+    for (uint32_t p = 0; p < P; ++p) W.VP[p * 64 + lane] = prm[p];
 
     uint64_t mask = uni64(__ballot(active));
     uint32_t n = P, sp = 0, lp = 0, fp = 0, pc = 0, steps = 0;
-    auto node = [&](uint32_t op, uint32_t a, uint32_t b) {
-        Node e{op, a, b, 0, 0};
-        W.E[n] = e;   // every lane stores the same record (each later reads its own store)
+    // record node n (every lane stores the same record: each later reads its own store)
+    auto record = [&](uint32_t op, uint32_t a, uint32_t b, double val) {
+        W.V[uint64_t(n) * 64 + lane] = val;
+        W.E[n] = Node{op, a, b, 0, 0};
         return n++;
+    };
+    // restore the stack and locals values of an IFLT's entry state (node
+    // numbers in the frame snapshot) wherever the current state differs
+    auto restore = [&](const uint32_t *snap_ids, uint32_t sp0, uint32_t sp_now) {
+        for (uint32_t i = 0; i < sp0; ++i) {
+            const uint32_t x = uni(snap_ids[i]);
+            if (i < sp_now && uni(W.stk[i]) == x) continue;
+            W.stk[i] = x;
+            W.s(i) = W.v(x);
+        }
+        for (uint32_t j = 0; j < D.n_locals; ++j) {
+            const uint32_t x = uni(snap_ids[W.depth + j]);
+            if (uni(W.loc[j]) == x) continue;
+            W.loc[j] = x;
+            if (x != kUnset) W.l(j) = W.v(x);
+        }
     };
 
     for (;;) {
@@ -144,50 +200,63 @@ __device__ bool walk_item(const Args &A, const Wave &W, const ProgDesc &D, uint3
         stack_effect(op, &pops, &pushes);
         if (sp < pops || sp - pops + pushes > W.depth || (op == bc::LOOP && lp >= A.n_loops) ||
             (op == bc::IFLT && fp >= A.n_frames) || ((op == bc::ELSE || op == bc::ENDIF) && fp == 0) ||
-            (op == bc::ENDLOOP && lp == 0))
+            (op == bc::ENDLOOP && lp == 0) || ((op == bc::LOADL || op == bc::STOREL) && imm >= D.n_locals) ||
+            (op == bc::PARAM && imm >= P))
             return false;
         switch (op) {
         case bc::HALT:
             goto reverse;
-        case bc::PUSH:
+        case bc::PUSH: {
             if (n >= n_nodes) return false;
-            W.v(n) = K[imm];
+            const double x = K[imm];
             W.set_flag(n, 1u);
-            W.stk[sp++] = node(walk::kLeaf, 0, 0);
+            W.s(sp) = x;
+            W.stk[sp++] = record(walk::kLeaf, 0, 0, x);
             break;
+        }
         case bc::OBS: {
             if (n >= n_nodes || wa > lp) return false;
             int64_t idx = imm;
             for (uint32_t d = 0; d < wa; ++d)
                 idx += int64_t(int32_t(code[2 * (pc + 1 + d) + 1])) * int64_t(uni(W.lps[3 * (lp - 1 - d) + 2]));
-            W.v(n) = A.obs[idx];
+            const double x = obs[idx];
             W.set_flag(n, 1u);
-            W.stk[sp++] = node(walk::kLeaf, 0, 0);
+            W.s(sp) = x;
+            W.stk[sp++] = record(walk::kLeaf, 0, 0, x);
             pc += wa;
             break;
         }
         case bc::PARAM:
+            W.s(sp) = W.VP[imm * 64 + lane];
             W.stk[sp++] = imm;
             break;
         case bc::LOADL: {
             const uint32_t id = uni(W.loc[imm]);
             if (id == kUnset) return false;
+            W.s(sp) = W.l(imm);
             W.stk[sp++] = id;
             break;
         }
         case bc::STOREL:
-            W.loc[imm] = uni(W.stk[--sp]);
+            --sp;
+            W.l(imm) = W.s(sp);
+            W.loc[imm] = uni(W.stk[sp]);
             break;
         case bc::DUP:
+            W.s(sp) = W.s(sp - 1);
             W.stk[sp] = uni(W.stk[sp - 1]);
             ++sp;
             break;
         case bc::OVER:
+            W.s(sp) = W.s(sp - 2);
             W.stk[sp] = uni(W.stk[sp - 2]);
             ++sp;
             break;
         case bc::SWAP: {
+            const double x = W.s(sp - 1), y = W.s(sp - 2);
             const uint32_t t = uni(W.stk[sp - 1]), u = uni(W.stk[sp - 2]);
+            W.s(sp - 1) = y;
+            W.s(sp - 2) = x;
             W.stk[sp - 1] = u;
             W.stk[sp - 2] = t;
             break;
@@ -216,11 +285,11 @@ __device__ bool walk_item(const Args &A, const Wave &W, const ProgDesc &D, uint3
             break;
         }
         case bc::IFLT: {
-            const uint32_t bi = uni(W.stk[sp - 1]), ai = uni(W.stk[sp - 2]);
             sp -= 2;
-            const uint64_t tm = uni64(__ballot(W.v(ai) < W.v(bi))) & mask, em = mask & ~tm;
+            const uint64_t tm = uni64(__ballot(W.s(sp) < W.s(sp + 1))) & mask, em = mask & ~tm;
             // frame: outer mask, first-arm mask, second-arm mask, phase, entry
             // depth, then the entry snapshot and the first arm's exit snapshot
+            // (node numbers of stack positions and locals)
             uint32_t *f = W.frm + fp * W.fsz;
             ++fp;
             f[0] = uint32_t(mask);
@@ -248,9 +317,9 @@ __device__ bool walk_item(const Args &A, const Wave &W, const ProgDesc &D, uint3
             for (uint32_t i = lane; i < sp; i += 64) f[walk::kFrameFixed + W.snap + i] = W.stk[i];
             for (uint32_t i = lane; i < D.n_locals; i += 64) f[walk::kFrameFixed + W.snap + W.depth + i] = W.loc[i];
             if (em) {   // the second arm starts from the entry state
-                sp = uni(f[7]);
-                for (uint32_t i = lane; i < sp; i += 64) W.stk[i] = f[walk::kFrameFixed + i];
-                for (uint32_t i = lane; i < D.n_locals; i += 64) W.loc[i] = f[walk::kFrameFixed + W.depth + i];
+                const uint32_t sp0 = uni(f[7]);
+                restore(f + walk::kFrameFixed, sp0, sp);
+                sp = sp0;
                 mask = em;
                 break;
             }
@@ -269,16 +338,20 @@ __device__ bool walk_item(const Args &A, const Wave &W, const ProgDesc &D, uint3
                     const uint32_t x = uni(f[walk::kFrameFixed + W.snap + i]), y = uni(W.stk[i]);
                     if (x == y) continue;
                     if (n >= n_nodes) return false;
-                    W.v(n) = first ? W.v(x) : W.v(y);
+                    const double val = first ? W.v(x) : W.s(i);
+                    W.V[uint64_t(n) * 64 + lane] = val;
                     W.E[n] = Node{walk::kMerge, x, y, 0, tm};
+                    W.s(i) = val;
                     W.stk[i] = n++;
                 }
                 for (uint32_t j = 0; j < D.n_locals; ++j) {
                     const uint32_t x = uni(f[walk::kFrameFixed + W.snap + W.depth + j]), y = uni(W.loc[j]);
                     if (x == y) continue;
                     if (x == kUnset || y == kUnset || n >= n_nodes) return false;
-                    W.v(n) = first ? W.v(x) : W.v(y);
+                    const double val = first ? W.v(x) : W.l(j);
+                    W.V[uint64_t(n) * 64 + lane] = val;
                     W.E[n] = Node{walk::kMerge, x, y, 0, tm};
+                    W.l(j) = val;
                     W.loc[j] = n++;
                 }
             }
@@ -291,9 +364,11 @@ __device__ bool walk_item(const Args &A, const Wave &W, const ProgDesc &D, uint3
             const bool bin = is_binary(op);
             const uint32_t bi = bin ? uni(W.stk[sp - 1]) : 0u;
             const uint32_t ai = uni(W.stk[sp - (bin ? 2 : 1)]);
+            const double x = W.s(sp - (bin ? 2 : 1)), y = bin ? W.s(sp - 1) : 0.0;
             sp -= bin ? 2 : 1;
-            W.v(n) = forward(op, W.v(ai), bin ? W.v(bi) : 0.0);
-            W.stk[sp++] = node(op, ai, bi);
+            const double z = forward(op, x, y);
+            W.s(sp) = z;
+            W.stk[sp++] = record(op, ai, bi, z);
         }
         }
         ++pc;
@@ -301,11 +376,14 @@ __device__ bool walk_item(const Args &A, const Wave &W, const ProgDesc &D, uint3
 
 reverse: {
     const uint32_t loss_id = uni(W.stk[0]);
-    const double loss = W.v(loss_id);
+    const double loss = W.s(0);
     W.contribute(loss_id, true, 1.0, false);   // seed: 0 + 1
+    // the next node's record is loaded one node ahead
+    Node nx = n > P ? W.E[n - 1] : Node{};
     for (uint32_t k = n; k-- > P;) {
+        const Node e = nx;
+        if (k > P) nx = W.E[k - 1];
         if (W.flags(k) != 2u) continue;   // a leaf, or no adjoint reached it
-        const Node e = W.E[k];
         const uint32_t op = uni(e.op), a = uni(e.a), b = uni(e.b);
         const double g = W.g(k);
         const bool on = g != 0.0;
@@ -353,10 +431,10 @@ reverse: {
             break;
         }
         case bc::SIN:
-            W.contribute(a, on, g * cos(W.v(a)), false);
+            W.contribute(a, on, g * transcendental(bc::COS, W.v(a), 0.0), false);
             break;
         case bc::COS:
-            W.contribute(a, on, g * sin(W.v(a)), true);
+            W.contribute(a, on, g * transcendental(bc::SIN, W.v(a), 0.0), true);
             break;
         case bc::ABS: {
             const double x = W.v(a);
@@ -366,27 +444,32 @@ reverse: {
         default: {   // POW
             const double x = W.v(a), y = W.v(b), z = W.v(k);
             W.contribute(a, on, ((g * y) * z) / x, false);
-            W.contribute(b, on, (g * z) * log(x), false);
+            W.contribute(b, on, (g * z) * transcendental(bc::LOG, x, 0.0), false);
         }
         }
     }
     if (active) {
         A.loss[int64_t(q) * A.L + lg] = loss;
         double *gr = A.grad + int64_t(q) * A.prog_stride_g + lg * A.ld_g;
-        for (uint32_t p = 0; p < P; ++p) gr[p] = (W.flags(p) & 2u) ? W.g(p) : 0.0;
+        for (uint32_t p = 0; p < P; ++p) gr[p] = (W.flags(p) & 2u) ? W.GP[p * 64 + lane] : 0.0;
     }
 }
     return true;
 }
 
 __global__ void __launch_bounds__(64) ndvm_walk(Args A) {
-    extern __shared__ uint32_t sh[];
+    extern __shared__ double sh[];
     Wave W;
     W.lane = threadIdx.x;
     W.depth = A.depth;
     W.snap = A.depth + A.n_locals;
     W.fsz = walk::kFrameFixed + 2 * W.snap;
-    W.stk = sh;
+    W.VP = sh;
+    W.VS = W.VP + A.n_params * 64;
+    W.VL = W.VS + A.depth * 64;
+    W.GP = W.VS;
+    uint32_t *words = reinterpret_cast<uint32_t *>(sh + walk::lds_rows(A.depth, A.n_locals, A.n_params) * 64);
+    W.stk = words;
     W.loc = W.stk + A.depth;
     W.lps = W.loc + A.n_locals;
     W.frm = W.lps + 3 * A.n_loops;
@@ -396,11 +479,13 @@ __global__ void __launch_bounds__(64) ndvm_walk(Args A) {
     W.G = W.V + uint64_t(A.n_nodes_max) * 64;
     W.E = reinterpret_cast<Node *>(W.G + uint64_t(A.n_nodes_max) * 64);
     const uint64_t per_prog = uint64_t((A.L + 63) / 64);
-    const ProgDesc *descs = reinterpret_cast<const ProgDesc *>(A.buf);
+    const AS_CONST uint32_t *descs = cst(A.buf);   // ProgDesc records, word by word
     for (uint64_t item = blockIdx.x; item < A.n_items; item += gridDim.x) {
         const uint32_t q = uint32_t(item / per_prog);
         const int64_t l0 = int64_t(item % per_prog) * 64;
-        const ProgDesc D = descs[q];
+        ProgDesc D;
+        uint32_t *dw = reinterpret_cast<uint32_t *>(&D);
+        for (uint32_t i = 0; i < sizeof(ProgDesc) / 4; ++i) dw[i] = descs[uint64_t(q) * (sizeof(ProgDesc) / 4) + i];
         if (!walk_item(A, W, D, q, l0)) {
             // a bound the validation guarantees was not met: report it and
             // leave this item's lanes NaN
@@ -419,7 +504,7 @@ __global__ void __launch_bounds__(64) ndvm_walk(Args A) {
 
 hipError_t launch_walk(const walk::Args &A, uint32_t grid, hipStream_t stream) {
     if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL(ndvm_walk, dim3(grid), dim3(64), size_t(A.lds_words) * 4, stream, A);
+    hipLaunchKernelGGL(ndvm_walk, dim3(grid), dim3(64), size_t(A.lds_bytes), stream, A);
     return hipGetLastError();
 }
 

@@ -314,6 +314,9 @@ class Measure {
         nodes = sat_add(block(0, code.size(), s, true, 0, &halted, &steps), n_params);
         if (nodes > walk::kMaxNodes) fail(NDVM_E_UNSUPPORTED, "program records more nodes than the device walker holds");
         if (steps >= 0xFFFFFFFFull) fail(NDVM_E_UNSUPPORTED, "program executes more words than the device walker counts");
+        if (walk::lds_bytes(uint32_t(max_depth), n_locals, max_loops, max_frames, uint32_t(nodes), n_params) >
+            walk::kMaxLdsBytes)
+            fail(NDVM_E_UNSUPPORTED, "the walk's structural state exceeds a workgroup's LDS");
     }
 };
 
@@ -345,7 +348,7 @@ uint32_t wave_slots(const ndvm_walk &w, uint64_t items) {
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess && v > 0)
             lds = v;
     }
-    const uint64_t lds_wave = 4ull * walk::lds_words(w.depth, w.n_locals, w.n_loops, w.n_frames, w.n_nodes);
+    const uint64_t lds_wave = walk::lds_bytes(w.depth, w.n_locals, w.n_loops, w.n_frames, w.n_nodes, w.max_params);
     const uint64_t per_cu = std::max<uint64_t>(1, std::min<uint64_t>(16, uint64_t(lds) / std::max<uint64_t>(lds_wave, 1)));
     return uint32_t(std::min<uint64_t>(items, per_cu * uint64_t(cus)));
 }
@@ -416,6 +419,9 @@ ndvm_status ndvm_walk_prepare(const uint8_t *const *bytecodes, const size_t *len
             w->n_frames = std::max(w->n_frames, d.n_frames);
         }
         if (buf.size() > 0xFFFFFFFFull) fail(NDVM_E_UNSUPPORTED, "program set beyond the device buffer's 32-bit offsets");
+        if (walk::lds_bytes(w->depth, w->n_locals, w->n_loops, w->n_frames, w->n_nodes, w->max_params) >
+            walk::kMaxLdsBytes)
+            fail(NDVM_E_UNSUPPORTED, "the program set's structural state exceeds a workgroup's LDS");
         std::memcpy(buf.data(), w->descs.data(), sizeof(walk::ProgDesc) * size_t(n_prog));
         if (hipGetDevice(&w->device) != hipSuccess) {
             set_error("hipGetDevice failed");
@@ -519,7 +525,8 @@ ndvm_status ndvm_walk_grad(const ndvm_walk *w, const double *params, int64_t L, 
         A.n_locals = w->n_locals;
         A.n_loops = w->n_loops;
         A.n_frames = w->n_frames;
-        A.lds_words = walk::lds_words(w->depth, w->n_locals, w->n_loops, w->n_frames, w->n_nodes);
+        A.n_params = w->max_params;
+        A.lds_bytes = uint32_t(walk::lds_bytes(w->depth, w->n_locals, w->n_loops, w->n_frames, w->n_nodes, w->max_params));
         A.n_items = uint64_t(w->n_prog) * uint64_t((L + 63) / 64);
         A.status = static_cast<int *>(workspace);
         const hipStream_t s = static_cast<hipStream_t>(stream);

@@ -79,13 +79,13 @@ def test_rejected_programs(bc, status):
 
 def test_loops_are_measured_without_unrolling():
     # a loop body that deepens the stack: depth and nodes grow with the trips
-    bc = Asm(1, 0).param(0).loop(200).push(1.0).endloop().loop(200).add().endloop().halt().bytes()
+    bc = Asm(1, 0).param(0).loop(60).push(1.0).endloop().loop(60).add().endloop().halt().bytes()
     info = nd.walk_measure(bc)
-    assert info["depth"] == 201
-    assert info["n_nodes"] >= 200 + 200 + 1
+    assert info["depth"] == 61
+    assert info["n_nodes"] >= 60 + 60 + 1
     with pytest.raises(nd.NdvmError):
-        # deeper than the walker's operand stack limit
-        nd.walk_measure(Asm(1, 0).param(0).loop(300).push(1.0).endloop().loop(300).add().endloop().halt().bytes())
+        # deeper than the walker's operand stack limit (64)
+        nd.walk_measure(Asm(1, 0).param(0).loop(70).push(1.0).endloop().loop(70).add().endloop().halt().bytes())
     info = nd.walk_measure(Asm(1, 3).push(0.0).storel(0).loop(3).loadl(0).obs(0, 1).add().storel(0).endloop()
                            .loadl(0).halt().bytes())
     assert info["n_loops"] == 1 and info["depth"] == 2 and info["n_nodes"] == 1 + 1 + 3 * 2
