@@ -23,7 +23,7 @@ namespace walk {
 // One program in the device buffer.  Offsets count 32-bit words from the
 // start of the buffer; the constants start 8-byte aligned.
 struct ProgDesc {
-    uint32_t code_off;    // n_instr instruction words, 2 x u32 each: op | a << 8 | b << 16, imm
+    uint32_t code_off;    // n_instr instruction words, 2 x u32 each: op | a << 8 | pops << 16 | pushes << 18, imm
     uint32_t match_off;   // n_instr int32: LOOP -> ENDLOOP, IFLT -> ELSE, ELSE -> ENDIF, else -1
     uint32_t const_off;   // n_consts doubles
     uint32_t n_instr;
@@ -36,28 +36,32 @@ struct ProgDesc {
     uint32_t n_steps;     // bound on the words one walk executes (the walk stops there)
 };
 
+// A node number with this bit set on the operand stack, in a local or as a
+// recorded operand is a constant or observation: it takes no adjoint.
+constexpr uint32_t kLeafBit = 0x80000000u;
+
 // Node kinds beyond the bytecode's numeric opcodes (which keep their numbers).
 constexpr uint32_t kLeaf = 0x01;    // constant or observation: takes no adjoint
 constexpr uint32_t kParam = 0x02;   // parameter p = node p
 constexpr uint32_t kMerge = 0x40;   // per-lane pick of two arms' values (a if the lane took the first arm)
 
-// Recorded node (one per node and wave, 24 bytes): its operand nodes and,
-// for a MERGE, the ballot word of the lanes that took the first arm.
+// Recorded node (one per node and wave, 16 bytes): its kind and operand
+// nodes; for a MERGE, `mask` indexes the ballot word of the lanes that took
+// the first arm (stored after the node records).
 struct Node {
-    uint32_t op, a, b, pad;
-    uint64_t mask;
+    uint32_t op, a, b, mask;
 };
 
 // Per-wave workspace: values[n_nodes][64], adjoints[n_nodes][64] (fp64),
-// nodes[n_nodes].
-constexpr uint64_t ws_bytes_per_node() { return 64 * 8 * 2 + sizeof(Node); }
+// nodes[n_nodes], ballot words[n_nodes] (u64, MERGE nodes only).
+constexpr uint64_t ws_bytes_per_node() { return 64 * 8 * 2 + sizeof(Node) + 8; }
 
 // LDS of one wave.  Rows of 64 doubles first: the parameters' values, then
 // the operand stack's and the locals' values during the forward walk, whose
 // rows the parameters' adjoints take over in the reverse sweep.  Then 32-bit
 // words: the operand stack's and locals' node numbers, loop frames (start,
 // trips, counter), IFLT frames (masks, phase, two snapshots of stack +
-// locals node numbers), and two flag bits per node (leaf, adjoint touched).
+// locals node numbers), and one flag bit per node (adjoint row written).
 constexpr uint32_t kFrameFixed = 8;
 constexpr uint32_t lds_rows(uint32_t depth, uint32_t n_locals, uint32_t n_params) {
     const uint32_t fwd = depth + n_locals;
@@ -66,7 +70,7 @@ constexpr uint32_t lds_rows(uint32_t depth, uint32_t n_locals, uint32_t n_params
 constexpr uint32_t lds_words(uint32_t depth, uint32_t n_locals, uint32_t n_loops, uint32_t n_frames,
                           uint32_t n_nodes) {
     const uint32_t snap = depth + n_locals;
-    return depth + n_locals + 3 * n_loops + n_frames * (kFrameFixed + 2 * snap) + (n_nodes + 15) / 16;
+    return depth + n_locals + 3 * n_loops + n_frames * (kFrameFixed + 2 * snap) + (n_nodes + 31) / 32;
 }
 constexpr uint64_t lds_bytes(uint32_t depth, uint32_t n_locals, uint32_t n_loops, uint32_t n_frames, uint32_t n_nodes,
                           uint32_t n_params) {
@@ -76,7 +80,7 @@ constexpr uint64_t lds_bytes(uint32_t depth, uint32_t n_locals, uint32_t n_loops
 // Limits the host validator enforces.
 constexpr uint32_t kMaxDepth = 64, kMaxLocals = 32, kMaxFrames = 32, kMaxLoops = 32;
 constexpr uint64_t kMaxLdsBytes = 64 * 1024;   // a workgroup's LDS
-constexpr uint64_t kMaxNodes = 1u << 24;
+constexpr uint64_t kMaxNodes = 1u << 22;   // node * 64 + lane fits 32 bits
 
 struct Args {
     const uint32_t *buf;        // device buffer: ProgDesc[n_prog] then code, matches, constants

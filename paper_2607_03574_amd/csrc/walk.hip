@@ -82,20 +82,6 @@ __device__ __forceinline__ double forward(uint32_t op, double x, double y) {
     }
 }
 
-// operand stack words a bytecode word pops and pushes
-__device__ __forceinline__ void stack_effect(uint32_t op, uint32_t *pops, uint32_t *pushes) {
-    switch (op) {
-    case bc::PUSH: case bc::OBS: case bc::PARAM: case bc::LOADL: *pops = 0; *pushes = 1; return;
-    case bc::STOREL: case bc::DROP: *pops = 1; *pushes = 0; return;
-    case bc::DUP: *pops = 1; *pushes = 2; return;
-    case bc::OVER: *pops = 2; *pushes = 3; return;
-    case bc::SWAP: *pops = 2; *pushes = 2; return;
-    case bc::IFLT: *pops = 2; *pushes = 0; return;
-    case bc::HALT: case bc::LOOP: case bc::ENDLOOP: case bc::ELSE: case bc::ENDIF: *pops = 0; *pushes = 0; return;
-    default: *pops = is_binary(op) ? 2 : 1; *pushes = 1; return;
-    }
-}
-
 struct Wave {
     uint32_t lane;
     uint32_t P;   // parameters of the current program
@@ -110,33 +96,35 @@ struct Wave {
     // HBM slot of the wave
     double *V, *G;
     Node *E;
+    uint64_t *M;   // ballot words of MERGE nodes
 
-    // two flag bits per node in LDS: bit 0 leaf, bit 1 adjoint row written
-    __device__ __forceinline__ uint32_t flags(uint32_t k) const { return uni(flg[k >> 4]) >> ((k & 15) * 2) & 3u; }
-    __device__ __forceinline__ void set_flag(uint32_t k, uint32_t bit) const {
-        const uint32_t w = uni(flg[k >> 4]);
-        flg[k >> 4] = w | bit << ((k & 15) * 2);
+    // one flag bit per node in LDS: its adjoint row has been written
+    __device__ __forceinline__ bool touched(uint32_t k) const { return (uni(flg[k >> 5]) >> (k & 31)) & 1u; }
+    __device__ __forceinline__ void touch(uint32_t k) const {
+        const uint32_t w = uni(flg[k >> 5]);
+        flg[k >> 5] = w | 1u << (k & 31);
     }
     __device__ __forceinline__ double &s(uint32_t i) const { return VS[i * 64 + lane]; }
     __device__ __forceinline__ double &l(uint32_t j) const { return VL[j * 64 + lane]; }
-    // value and adjoint of node k (parameters in LDS, the others in HBM)
+    // value and adjoint of node k (parameters in LDS, the others in HBM;
+    // a leaf's number carries kLeafBit)
     __device__ __forceinline__ double &v(uint32_t k) const {
-        return k < P ? VP[k * 64 + lane] : V[uint64_t(k) * 64 + lane];
+        k &= ~walk::kLeafBit;
+        return k < P ? VP[k * 64 + lane] : V[k * 64u + lane];
     }
     __device__ __forceinline__ double &g(uint32_t k) const {
-        return k < P ? GP[k * 64 + lane] : G[uint64_t(k) * 64 + lane];
+        return k < P ? GP[k * 64 + lane] : G[k * 64u + lane];
     }
 
     // adjoint of node j += c (or -= c) where `apply`; the first contribution
     // writes the whole row (0 + c, or 0 where the rule does not apply)
     __device__ __forceinline__ void contribute(uint32_t j, bool apply, double c, bool neg) const {
-        const uint32_t f = flags(j);
-        if (f & 1u) return;   // constants and observations take no adjoint
+        if (j & walk::kLeafBit) return;   // constants and observations take no adjoint
         double base = 0.0;
-        if (f & 2u) {
+        if (touched(j)) {
             base = g(j);
         } else {
-            set_flag(j, 2u);
+            touch(j);
         }
         const double nv = neg ? base - c : base + c;
         g(j) = apply ? nv : base;
@@ -161,7 +149,7 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
         return false;
     W.P = P;
 
-    for (uint32_t i = lane; i < (n_nodes + 15) / 16; i += 64) W.flg[i] = 0;
+    for (uint32_t i = lane; i < (n_nodes + 31) / 32; i += 64) W.flg[i] = 0;
     for (uint32_t i = lane; i < D.n_locals; i += 64) W.loc[i] = kUnset;
     for (uint32_t p = 0; p < P; ++p) W.VP[p * 64 + lane] = prm[p];
 
@@ -169,8 +157,8 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
     uint32_t n = P, sp = 0, lp = 0, fp = 0, pc = 0, steps = 0;
     // record node n (every lane stores the same record: each later reads its own store)
     auto record = [&](uint32_t op, uint32_t a, uint32_t b, double val) {
-        W.V[uint64_t(n) * 64 + lane] = val;
-        W.E[n] = Node{op, a, b, 0, 0};
+        W.V[n * 64u + lane] = val;
+        W.E[n] = Node{op, a, b, 0};
         return n++;
     };
     // restore the stack and locals values of an IFLT's entry state (node
@@ -195,23 +183,18 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
         const uint32_t w0 = code[2 * pc], imm = code[2 * pc + 1];
         const uint32_t op = w0 & 0xFFu, wa = (w0 >> 8) & 0xFFu;
         // bounds the host validation guarantees (kept so that a broken
-        // guarantee can only give NaN lanes, never an access out of bounds)
-        uint32_t pops = 0, pushes = 0;
-        stack_effect(op, &pops, &pushes);
-        if (sp < pops || sp - pops + pushes > W.depth || (op == bc::LOOP && lp >= A.n_loops) ||
-            (op == bc::IFLT && fp >= A.n_frames) || ((op == bc::ELSE || op == bc::ENDIF) && fp == 0) ||
-            (op == bc::ENDLOOP && lp == 0) || ((op == bc::LOADL || op == bc::STOREL) && imm >= D.n_locals) ||
-            (op == bc::PARAM && imm >= P))
-            return false;
+        // guarantee can only give NaN lanes, never an access out of bounds);
+        // the host packs each word's stack effect into it
+        const uint32_t pops = (w0 >> 16) & 3u, pushes = (w0 >> 18) & 3u;
+        if (sp < pops || sp - pops + pushes > W.depth) return false;   // the other bounds: in their words
         switch (op) {
         case bc::HALT:
             goto reverse;
         case bc::PUSH: {
             if (n >= n_nodes) return false;
             const double x = K[imm];
-            W.set_flag(n, 1u);
             W.s(sp) = x;
-            W.stk[sp++] = record(walk::kLeaf, 0, 0, x);
+            W.stk[sp++] = record(walk::kLeaf, 0, 0, x) | walk::kLeafBit;
             break;
         }
         case bc::OBS: {
@@ -220,17 +203,18 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
             for (uint32_t d = 0; d < wa; ++d)
                 idx += int64_t(int32_t(code[2 * (pc + 1 + d) + 1])) * int64_t(uni(W.lps[3 * (lp - 1 - d) + 2]));
             const double x = obs[idx];
-            W.set_flag(n, 1u);
             W.s(sp) = x;
-            W.stk[sp++] = record(walk::kLeaf, 0, 0, x);
+            W.stk[sp++] = record(walk::kLeaf, 0, 0, x) | walk::kLeafBit;
             pc += wa;
             break;
         }
         case bc::PARAM:
+            if (imm >= P) return false;
             W.s(sp) = W.VP[imm * 64 + lane];
             W.stk[sp++] = imm;
             break;
         case bc::LOADL: {
+            if (imm >= D.n_locals) return false;
             const uint32_t id = uni(W.loc[imm]);
             if (id == kUnset) return false;
             W.s(sp) = W.l(imm);
@@ -238,6 +222,7 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
             break;
         }
         case bc::STOREL:
+            if (imm >= D.n_locals) return false;
             --sp;
             W.l(imm) = W.s(sp);
             W.loc[imm] = uni(W.stk[sp]);
@@ -265,6 +250,7 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
             --sp;
             break;
         case bc::LOOP:
+            if (lp >= A.n_loops) return false;
             if (imm == 0) {
                 pc = uni(uint32_t(match[pc])) + 1;
                 continue;
@@ -275,6 +261,7 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
             ++lp;
             break;
         case bc::ENDLOOP: {
+            if (lp == 0) return false;
             const uint32_t k = uni(W.lps[3 * (lp - 1) + 2]) + 1;
             if (k < uni(W.lps[3 * (lp - 1) + 1])) {
                 W.lps[3 * (lp - 1) + 2] = k;
@@ -285,6 +272,7 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
             break;
         }
         case bc::IFLT: {
+            if (fp >= A.n_frames) return false;
             sp -= 2;
             const uint64_t tm = uni64(__ballot(W.s(sp) < W.s(sp + 1))) & mask, em = mask & ~tm;
             // frame: outer mask, first-arm mask, second-arm mask, phase, entry
@@ -311,6 +299,7 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
             continue;
         }
         case bc::ELSE: {   // end of a walked first arm
+            if (fp == 0) return false;
             uint32_t *f = W.frm + (fp - 1) * W.fsz;
             const uint64_t em = uint64_t(uni(f[4])) | uint64_t(uni(f[5])) << 32;
             f[6] = 1u | sp << 1;
@@ -327,6 +316,7 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
             continue;
         }
         case bc::ENDIF: {
+            if (fp == 0) return false;
             const uint32_t *f = W.frm + (fp - 1) * W.fsz;
             const uint32_t ph = uni(f[6]);
             const uint64_t tm = uint64_t(uni(f[2])) | uint64_t(uni(f[3])) << 32;
@@ -339,8 +329,9 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
                     if (x == y) continue;
                     if (n >= n_nodes) return false;
                     const double val = first ? W.v(x) : W.s(i);
-                    W.V[uint64_t(n) * 64 + lane] = val;
-                    W.E[n] = Node{walk::kMerge, x, y, 0, tm};
+                    W.V[n * 64u + lane] = val;
+                    W.E[n] = Node{walk::kMerge, x, y, 0};
+                    W.M[n] = tm;
                     W.s(i) = val;
                     W.stk[i] = n++;
                 }
@@ -349,8 +340,9 @@ __device__ bool walk_item(const Args &A, Wave &W, const ProgDesc &D, uint32_t q,
                     if (x == y) continue;
                     if (x == kUnset || y == kUnset || n >= n_nodes) return false;
                     const double val = first ? W.v(x) : W.l(j);
-                    W.V[uint64_t(n) * 64 + lane] = val;
-                    W.E[n] = Node{walk::kMerge, x, y, 0, tm};
+                    W.V[n * 64u + lane] = val;
+                    W.E[n] = Node{walk::kMerge, x, y, 0};
+                    W.M[n] = tm;
                     W.l(j) = val;
                     W.loc[j] = n++;
                 }
@@ -383,13 +375,13 @@ reverse: {
     for (uint32_t k = n; k-- > P;) {
         const Node e = nx;
         if (k > P) nx = W.E[k - 1];
-        if (W.flags(k) != 2u) continue;   // a leaf, or no adjoint reached it
+        if (!W.touched(k)) continue;   // a leaf, or no adjoint reached it
         const uint32_t op = uni(e.op), a = uni(e.a), b = uni(e.b);
         const double g = W.g(k);
         const bool on = g != 0.0;
         switch (op) {
         case walk::kMerge: {
-            const bool first = (uni64(e.mask) >> lane) & 1u;
+            const bool first = (uni64(W.M[k]) >> lane) & 1u;
             W.contribute(a, on && first, g, false);
             W.contribute(b, on && !first, g, false);
             break;
@@ -451,7 +443,7 @@ reverse: {
     if (active) {
         A.loss[int64_t(q) * A.L + lg] = loss;
         double *gr = A.grad + int64_t(q) * A.prog_stride_g + lg * A.ld_g;
-        for (uint32_t p = 0; p < P; ++p) gr[p] = (W.flags(p) & 2u) ? W.GP[p * 64 + lane] : 0.0;
+        for (uint32_t p = 0; p < P; ++p) gr[p] = W.touched(p) ? W.GP[p * 64 + lane] : 0.0;
     }
 }
     return true;
@@ -478,6 +470,7 @@ __global__ void __launch_bounds__(64) ndvm_walk(Args A) {
     W.V = reinterpret_cast<double *>(slot);
     W.G = W.V + uint64_t(A.n_nodes_max) * 64;
     W.E = reinterpret_cast<Node *>(W.G + uint64_t(A.n_nodes_max) * 64);
+    W.M = reinterpret_cast<uint64_t *>(W.E + A.n_nodes_max);
     const uint64_t per_prog = uint64_t((A.L + 63) / 64);
     const AS_CONST uint32_t *descs = cst(A.buf);   // ProgDesc records, word by word
     for (uint64_t item = blockIdx.x; item < A.n_items; item += gridDim.x) {

@@ -75,6 +75,23 @@ bool matrix_word(uint8_t op) {
     return false;
 }
 
+// operand stack words a (scalar) bytecode word pops and pushes
+void stack_effect(uint8_t op, uint32_t *pops, uint32_t *pushes) {
+    switch (op) {
+    case bc::PUSH: case bc::OBS: case bc::PARAM: case bc::LOADL: *pops = 0; *pushes = 1; return;
+    case bc::STOREL: case bc::DROP: *pops = 1; *pushes = 0; return;
+    case bc::DUP: *pops = 1; *pushes = 2; return;
+    case bc::OVER: *pops = 2; *pushes = 3; return;
+    case bc::SWAP: *pops = 2; *pushes = 2; return;
+    case bc::IFLT: *pops = 2; *pushes = 0; return;
+    default:
+        if (scalar_binary(op)) { *pops = 2; *pushes = 1; return; }
+        if (scalar_unary(op)) { *pops = 1; *pushes = 1; return; }
+        *pops = 0;   // HALT, LOOP, ENDLOOP, ELSE, ENDIF, OBSX
+        *pushes = 0;
+    }
+}
+
 // Structural measurement of one program: what one wave's walk can reach,
 // found by following the block structure once (a loop body is measured at
 // its first and last trip, whose entry depths bound every trip's).
@@ -398,7 +415,9 @@ ndvm_status ndvm_walk_prepare(const uint8_t *const *bytecodes, const size_t *len
             d.n_steps = uint32_t(m.steps);
             d.code_off = uint32_t(buf.size());
             for (const Word &x : m.code) {
-                buf.push_back(uint32_t(x.op) | uint32_t(x.a) << 8 | uint32_t(x.b) << 16);
+                uint32_t pops = 0, pushes = 0;
+                stack_effect(x.op, &pops, &pushes);
+                buf.push_back(uint32_t(x.op) | uint32_t(x.a) << 8 | pops << 16 | pushes << 18);
                 buf.push_back(x.imm);
             }
             d.match_off = uint32_t(buf.size());
