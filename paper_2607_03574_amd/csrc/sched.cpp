@@ -2179,7 +2179,17 @@ Schedule grad_fit(const Tape &t, uint32_t reg_budget, uint32_t slots, bool save_
             hi = mid;
         }
     }
-    return trial(best_size, true);
+    // A size that divides the trace evenly into as many segments cuts every
+    // step of a loop at the same point (the largest fitting size drifts
+    // through the steps): of the two, keep the schedule with fewer
+    // instructions (Lotka-Volterra: 61,020 against 63,523).
+    Schedule full = trial(best_size, true);
+    const uint64_t even = total / std::max<uint32_t>(1, full.n_segments);
+    if (even > 0 && even != best_size) {
+        Schedule alt = trial(even, true);
+        if (alt.n_regs <= reg_budget && alt.n_instr < full.n_instr) return alt;
+    }
+    return full;
 }
 
 }  // namespace
