@@ -378,67 +378,92 @@ reverse: {
         if (k > P) nx = W.E[k - 1];
         if (!W.touched(k)) continue;   // a leaf, or no adjoint reached it
         const uint32_t op = uni(e.op), a = uni(e.a), b = uni(e.b);
+        // Every load the node's rules need is issued before the first
+        // contribution is formed (the incoming adjoint, the values the rule
+        // reads, the targets' adjoint rows), so the node waits on memory
+        // once; a target named twice (x * x) takes its second contribution
+        // on top of the first.
+        const bool two = is_binary(op) || op == walk::kMerge;
+        const bool need_x = op == bc::MUL || op == bc::LOG || op == bc::SQRT || op == bc::SIN || op == bc::COS ||
+                            op == bc::ABS || op == bc::POW;
+        const bool need_y = op == bc::MUL || op == bc::DIV || op == bc::POW;
+        const bool need_z = op == bc::DIV || op == bc::EXP || op == bc::SQRT || op == bc::POW;
         const double g = W.g(k);
+        const double x = need_x ? W.v(a) : 0.0, y = need_y ? W.v(b) : 0.0, z = need_z ? W.v(k) : 0.0;
+        const bool has_a = !(a & walk::kLeafBit), has_b = two && !(b & walk::kLeafBit);
+        const bool ta = has_a && W.touched(a), tb = has_b && b != a && W.touched(b);
+        const double ga = ta ? W.g(a) : 0.0, gb = tb ? W.g(b) : 0.0;
         const bool on = g != 0.0;
+        // contributions: value, where it applies, subtracted
+        double ca = 0.0, cb = 0.0;
+        bool pa = on, pb = on, na = false, nb = false;
         switch (op) {
         case walk::kMerge: {
             const bool first = (uni64(W.M[k]) >> lane) & 1u;
-            W.contribute(a, on && first, g, false);
-            W.contribute(b, on && !first, g, false);
+            ca = cb = g;
+            pa = on && first;
+            pb = on && !first;
             break;
         }
         case bc::ADD:
-            W.contribute(a, on, g, false);
-            W.contribute(b, on, g, false);
+            ca = cb = g;
             break;
         case bc::SUB:
-            W.contribute(a, on, g, false);
-            W.contribute(b, on, g, true);
+            ca = cb = g;
+            nb = true;
             break;
-        case bc::MUL: {
-            const double x = W.v(a), y = W.v(b);
-            W.contribute(a, on, g * y, false);
-            W.contribute(b, on, g * x, false);
+        case bc::MUL:
+            ca = g * y;
+            cb = g * x;
             break;
-        }
-        case bc::DIV: {
-            const double y = W.v(b), z = W.v(k);
-            W.contribute(a, on, g / y, false);
-            W.contribute(b, on, (g * z) / y, true);
+        case bc::DIV:
+            ca = g / y;
+            cb = (g * z) / y;
+            nb = true;
             break;
-        }
         case bc::NEG:
-            W.contribute(a, on, g, true);
+            ca = g;
+            na = true;
             break;
         case bc::EXP:
-            W.contribute(a, on, g * W.v(k), false);
+            ca = g * z;
             break;
-        case bc::LOG: {
-            const double x = W.v(a);
-            W.contribute(a, on && x > 1e-8, g / x, false);
+        case bc::LOG:
+            pa = on && x > 1e-8;
+            ca = g / x;
             break;
-        }
-        case bc::SQRT: {
-            const double x = W.v(a);
-            W.contribute(a, on && x > 1e-8, g / (2.0 * W.v(k)), false);
+        case bc::SQRT:
+            pa = on && x > 1e-8;
+            ca = g / (2.0 * z);
             break;
-        }
         case bc::SIN:
-            W.contribute(a, on, g * transcendental(bc::COS, W.v(a), 0.0), false);
+            ca = g * transcendental(bc::COS, x, 0.0);
             break;
         case bc::COS:
-            W.contribute(a, on, g * transcendental(bc::SIN, W.v(a), 0.0), true);
+            ca = g * transcendental(bc::SIN, x, 0.0);
+            na = true;
             break;
-        case bc::ABS: {
-            const double x = W.v(a);
-            W.contribute(a, on, x > 0.0 ? g : (x < 0.0 ? -g : 0.0), false);
+        case bc::ABS:
+            ca = x > 0.0 ? g : (x < 0.0 ? -g : 0.0);
             break;
+        default:   // POW
+            ca = ((g * y) * z) / x;
+            cb = (g * z) * transcendental(bc::LOG, x, 0.0);
         }
-        default: {   // POW
-            const double x = W.v(a), y = W.v(b), z = W.v(k);
-            W.contribute(a, on, ((g * y) * z) / x, false);
-            W.contribute(b, on, (g * z) * transcendental(bc::LOG, x, 0.0), false);
+        // the first contribution to a row writes it whole (0 + c, or 0
+        // where the rule does not apply)
+        double ra = 0.0;
+        if (has_a) {
+            if (!ta) W.touch(a);
+            const double nv = na ? ga - ca : ga + ca;
+            ra = pa ? nv : ga;
+            W.g(a) = ra;
         }
+        if (has_b) {
+            const double base = b == a ? ra : gb;
+            if (b != a && !tb) W.touch(b);
+            const double nv = nb ? base - cb : base + cb;
+            W.g(b) = pb ? nv : base;
         }
     }
     if (active) {
