@@ -211,6 +211,30 @@ ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, bool build, De
     return NDVM_OK;
 }
 
+// Register budget and device program of a single-program gradient launch.
+// The budget first sizes LDS so that every wave of the launch is resident
+// (at most 16 per CU).  A program whose register file does not fit that
+// budget would keep its excess registers in HBM rows; it is scheduled again
+// for the budget of as many resident waves per CU as its register file
+// leaves room for, and the launch runs in several rounds of waves instead
+// (Kalman at 32,768 lanes needs 314 registers against a budget of 160).
+// Deterministic in (tape, L), so sizing and compute calls agree.
+ndvm_status single_grad_program(ndvm_tape *tape, const DeviceProps &p, int64_t L, uint32_t S, bool build,
+                                DevProg **dp, uint32_t *b) {
+    *b = reg_budget(p, waves_of(L, 1, S), S);
+    ndvm_status st = grad_program(tape, S, *b, build, dp);
+    if (st != NDVM_OK || (*dp)->meta.n_regs <= *b) return st;
+    const size_t need = size_t((*dp)->meta.n_regs) * reg_bytes(S);
+    const size_t per_cu = std::max<size_t>(1, p.lds_per_cu / need);
+    const uint32_t b2 = uint32_t(std::min(p.lds_per_cu / per_cu, p.lds_per_block) / reg_bytes(S));
+    if (b2 <= *b) return NDVM_OK;
+    DevProg *dp2 = nullptr;
+    if ((st = grad_program(tape, S, b2, build, &dp2)) != NDVM_OK) return st;
+    *dp = dp2;
+    *b = b2;
+    return NDVM_OK;
+}
+
 // Registers of a forward-only program: whatever one workgroup may hold.
 uint32_t fwd_budget(uint32_t S) {
     DeviceProps p;
@@ -472,8 +496,8 @@ ndvm_status ndvm_workspace_bytes(const ndvm_tape *tape, int64_t L, int with_grad
         uint64_t rows;
         DevProg *dp;
         if (with_grad) {
-            uint32_t b = reg_budget(p, waves_of(L, 1, S), S);
-            st = grad_program(const_cast<ndvm_tape *>(tape), S, b, true, &dp);
+            uint32_t b = 0;
+            st = single_grad_program(const_cast<ndvm_tape *>(tape), p, L, S, true, &dp, &b);
             if (st != NDVM_OK) return st;
             rows = ws_rows(*dp, b);
         } else {
@@ -571,9 +595,9 @@ static ndvm_status grad_impl(const ndvm_tape *tape, const double *params, int64_
     if ((st = device_props(&p)) != NDVM_OK) return st;
     int64_t Lp = lpad_of(L);
     const uint32_t S = choose_slots(p, L, 1);
-    uint32_t b = reg_budget(p, waves_of(L, 1, S), S);
+    uint32_t b = 0;
     DevProg *dp;
-    if ((st = grad_program(const_cast<ndvm_tape *>(tape), S, b, false, &dp)) != NDVM_OK) return st;
+    if ((st = single_grad_program(const_cast<ndvm_tape *>(tape), p, L, S, false, &dp, &b)) != NDVM_OK) return st;
     uint32_t r_lds = std::min(dp->meta.n_regs, b);
     size_t need = size_t(ws_rows(*dp, b) * uint64_t(Lp) * sizeof(double));
     if (static_ws) {
@@ -630,8 +654,7 @@ static ndvm_status points_layout(const ndvm_tape *tape, int64_t L, int64_t N, bo
     if (st != NDVM_OK) return st;
     const int64_t F = L * N;
     const uint32_t S = choose_slots(p, F, 1);
-    *b = reg_budget(p, waves_of(F, 1, S), S);
-    if ((st = grad_program(const_cast<ndvm_tape *>(tape), S, *b, build, dp)) != NDVM_OK) return st;
+    if ((st = single_grad_program(const_cast<ndvm_tape *>(tape), p, F, S, build, dp, b)) != NDVM_OK) return st;
     *replay_bytes = ws_rows(**dp, *b) * uint64_t(lpad_of(F)) * sizeof(double);
     *total = *replay_bytes + uint64_t(F) * (1 + tape->tape.n_params) * sizeof(double);
     return NDVM_OK;

@@ -9,6 +9,8 @@ prepared by the sizing call fails instead of scheduling.  Calls on a side
 stream without a caller workspace give bit-identical results to calls on the
 current stream.  A many-program launch that mixes a spilling program with
 small ones matches the oracle and each program's own single-program launch.
+A program whose registers do not fit the budget of an all-resident launch
+runs in rounds of waves rather than spilling.
 """
 import ctypes
 
@@ -237,3 +239,25 @@ def test_many_programs_mixing_a_spilling_program(nd, oracle_mod):
     torch.cuda.synchronize()
     ol, _, _ = oracle_mod.run(wide, params[1], [], grad=False)
     compare(fl.cpu().numpy(), None, ol, None)
+
+
+def test_register_hungry_program_runs_in_rounds_instead_of_spilling(nd, oracle_mod):
+    """A Kalman filter needs about 315 registers per lane.  At 32,768 lanes,
+    every wave resident would leave a budget of 160 and push the rest to HBM
+    rows; the launch instead keeps the program of 320 registers (the
+    workspace holds the same rows per lane as at 16,384 lanes, none for
+    spilled registers) and runs its waves in two rounds.  Results: bit for
+    bit those of a 16,384-lane launch on the same lanes, and the oracle on a
+    sample of lanes."""
+    w = configs.build("kalman_cv4", L=32768, T=12)
+    tape = nd.tape_upload(nd.tape_build(w.bytecode))
+    assert nd.workspace_bytes(tape, 32768) == 2 * nd.workspace_bytes(tape, 16384)
+    p = torch.tensor(w.params, device="cuda")
+    o = torch.tensor(w.obs, device="cuda")
+    lf, gf = nd.grad(tape, p, o)
+    lh, gh = nd.grad(tape, p[16384:].contiguous(), o)
+    torch.cuda.synchronize()
+    assert torch.equal(lf[16384:], lh) and torch.equal(gf[16384:], gh)
+    idx = np.r_[0:64, 16320:16448, 32704:32768]
+    lo, go, _ = oracle_mod.run(w.bytecode, w.params[idx], w.obs)
+    compare(lf.cpu().numpy()[idx], gf.cpu().numpy()[idx], lo, go)
