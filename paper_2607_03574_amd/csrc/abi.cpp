@@ -280,9 +280,15 @@ ndvm_status check_stream_and_launch(const LaunchArgs &A, const ProgStatic *table
     return NDVM_OK;
 }
 
-// Device tables of ProgStatic for ndvm_grad_many, cached per program set.
+// Device tables of ProgStatic for ndvm_grad_many, cached per program set, and
+// of per-XCD work items, cached per program set and lane blocks.
 std::mutex g_table_mu;
 std::map<std::vector<uint64_t>, void *> g_tables;
+struct ItemTable {
+    void *d = nullptr;   // null: the plain grid
+    uint32_t n_wg = 0;
+};
+std::map<std::vector<uint64_t>, ItemTable> g_items;
 
 // A many-program launch: per-program device programs for the launch's
 // register budget, their table of ProgStatic on the device (cached per
@@ -295,7 +301,52 @@ struct ManyLaunch {
     bool skips = false;     // some program has skippable branch arms
     uint64_t rows = 0;
     void *d_table = nullptr;
+    const uint64_t *d_items = nullptr;   // work item per workgroup (xcd_items), or null
+    uint32_t n_wg = 0;
 };
+
+// Work items of a many-program launch laid out per XCD.  Each of MI355X's
+// eight XCDs has its own L2, and workgroups are dispatched to them in turn
+// (workgroup w to XCD w mod 8), so a program whose waves run on every XCD is
+// fetched into every L2.  Whole programs are assigned to XCDs instead,
+// longest first to the XCD with the least work so far (the lanes of every
+// program are alike, so its instruction count measures its work), and
+// workgroup k + 8 i takes the i-th work item (program, lane block) of XCD k:
+// an XCD runs the lane blocks of one program one after another.  Used when
+// every XCD gets several programs and the largest XCD load is within 5% of
+// the mean; otherwise the launch keeps the plain grid.
+constexpr uint32_t kXcds = 8;
+bool xcd_items(const std::vector<uint32_t> &cost, uint64_t blocks, std::vector<uint64_t> *items) {
+    const uint32_t n = uint32_t(cost.size());
+    if (n < 4 * kXcds || blocks == 0 || blocks > 0xFFFFFFFFull) return false;
+    std::vector<uint32_t> order(n);
+    for (uint32_t q = 0; q < n; ++q) order[q] = q;
+    std::stable_sort(order.begin(), order.end(), [&](uint32_t x, uint32_t y) { return cost[x] > cost[y]; });
+    std::vector<uint64_t> load(kXcds, 0);
+    std::vector<std::vector<uint32_t>> progs(kXcds);
+    for (uint32_t q : order) {
+        const uint32_t k = uint32_t(std::min_element(load.begin(), load.end()) - load.begin());
+        progs[k].push_back(q);
+        load[k] += cost[q];
+    }
+    uint64_t total = 0, top = 0;
+    size_t len = 0;
+    for (uint32_t k = 0; k < kXcds; ++k) {
+        total += load[k];
+        top = std::max(top, load[k]);
+        len = std::max(len, progs[k].size());
+    }
+    if (top * 20 * kXcds > total * 21) return false;
+    const uint64_t n_wg = uint64_t(len) * blocks * kXcds;
+    if (n_wg > 0xFFFFFFFFull) return false;
+    items->assign(size_t(n_wg), ~uint64_t(0));
+    for (uint32_t k = 0; k < kXcds; ++k) {
+        uint64_t i = 0;
+        for (uint32_t q : progs[k])
+            for (uint64_t bx = 0; bx < blocks; ++bx) (*items)[size_t(k + kXcds * i++)] = uint64_t(q) << 32 | bx;
+    }
+    return true;
+}
 
 ndvm_status many_launch(const ndvm_tape *const *tapes, int n_prog, int64_t L, bool build, ManyLaunch *out) {
     DeviceProps p;
@@ -308,9 +359,11 @@ ndvm_status many_launch(const ndvm_tape *const *tapes, int n_prog, int64_t L, bo
     uint64_t row = 0;
     uint32_t r_launch = 0;
     int n_spill = 0;
+    std::vector<uint32_t> cost(static_cast<size_t>(n_prog));
     for (int q = 0; q < n_prog; ++q) {
         DevProg *dp;
         if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), S, b, build, &dp)) != NDVM_OK) return st;
+        cost[q] = dp->meta.n_instr;
         uint32_t r_lds = std::min(dp->meta.n_regs, b);
         r_launch = std::max(r_launch, r_lds);
         const bool spills = dp->meta.n_regs > r_lds;
@@ -328,6 +381,33 @@ ndvm_status many_launch(const ndvm_tape *const *tapes, int n_prog, int64_t L, bo
     out->variant = n_spill == 0 ? kLdsOnly : n_spill == n_prog ? kSpill : kPerProgram;
     if (n_prog == 0) return NDVM_OK;
     std::lock_guard<std::mutex> lk(g_table_mu);
+    // per-XCD work items (single launches only: at most kMaxProgPerLaunch programs)
+    const uint64_t blocks = uint64_t((L + 64 / S - 1) / (64 / S));
+    std::vector<uint64_t> ikey = key;
+    ikey.push_back(blocks);
+    auto ii = g_items.find(ikey);
+    if (ii == g_items.end() && build) {
+        ItemTable t;
+        std::vector<uint64_t> items;
+        if (n_prog <= kMaxProgPerLaunch && xcd_items(cost, blocks, &items)) {
+            if (hipMalloc(&t.d, items.size() * sizeof(uint64_t)) != hipSuccess) {
+                (void)hipGetLastError();
+                set_error("hipMalloc of the work-item table failed");
+                return NDVM_E_NOMEM;
+            }
+            if (hipMemcpy(t.d, items.data(), items.size() * sizeof(uint64_t), hipMemcpyHostToDevice) != hipSuccess) {
+                (void)hipFree(t.d);
+                set_error("copy of the work-item table failed");
+                return NDVM_E_DEVICE;
+            }
+            t.n_wg = uint32_t(items.size());
+        }
+        ii = g_items.emplace(ikey, t).first;
+    }
+    if (ii != g_items.end()) {   // a compute call for a lane count never sized keeps the plain grid
+        out->d_items = static_cast<const uint64_t *>(ii->second.d);
+        out->n_wg = ii->second.n_wg;
+    }
     auto it = g_tables.find(key);
     if (it != g_tables.end()) {
         out->d_table = it->second;
@@ -474,6 +554,16 @@ void ndvm_tape_free(ndvm_tape *t) {
             if (uses) {
                 (void)hipFree(it->second);
                 it = g_tables.erase(it);
+            } else {
+                ++it;
+            }
+        }
+        for (auto it = g_items.begin(); it != g_items.end();) {
+            bool uses = false;
+            for (size_t i = 0; i + 1 < it->first.size(); i += 2) uses = uses || it->first[i] == t->id;
+            if (uses) {
+                if (it->second.d) (void)hipFree(it->second.d);
+                it = g_items.erase(it);
             } else {
                 ++it;
             }
@@ -766,6 +856,10 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
             LaunchArgs A{obs, params + q0 * prog_stride_p, loss + int64_t(q0) * L,
                          grad ? grad + q0 * prog_stride_g : nullptr, static_cast<double *>(ws), ld_p, ld_g, L, Lp,
                          prog_stride_p, prog_stride_g};
+            if (ml.d_items) {   // one launch over every program, laid out per XCD
+                A.wg_items = ml.d_items;
+                A.n_wg = ml.n_wg;
+            }
             st = check_stream_and_launch(A, static_cast<const ProgStatic *>(d_table) + q0, none, uint32_t(nq),
                                          r_launch, variant, ml.skips, S, s);
             if (st != NDVM_OK) return st;

@@ -222,17 +222,30 @@ __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *
 
 }  // namespace
 
+// Program and lane block of this workgroup: the grid's (y, x), or the work
+// item the launch's table gives it (false: none).
+__device__ __forceinline__ bool work_item(const LaunchArgs &A, uint32_t &q, uint32_t &bx) {
+    if (!A.wg_items) {
+        q = blockIdx.y;
+        bx = blockIdx.x;
+        return true;
+    }
+    const uint64_t it = A.wg_items[blockIdx.x];
+    q = uint32_t(it >> 32);
+    bx = uint32_t(it);
+    return it != ~uint64_t(0);
+}
+
 template <int S, bool kSpill, bool kSkip>
 __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStatic *__restrict__ table,
-                                            const ProgStatic &single) {
+                                            const ProgStatic &single, uint32_t q, uint32_t bx) {
     extern __shared__ double lds_regs[];
     constexpr int LW = 64 / S;
-    const uint32_t q = blockIdx.y;
     const ProgStatic D = table ? table[q] : single;
     DevCtx<S, kSpill> c;
     const int t = threadIdx.x, l = t % LW;
     c.slot_ = uint32_t(t / LW);
-    c.lane = int64_t(blockIdx.x) * LW + l;
+    c.lane = int64_t(bx) * LW + l;
     c.active = c.lane < A.L;
     c.lc = c.active ? c.lane : A.L - 1;
     const AS_GLOBAL double *obs_row = (const AS_GLOBAL double *)A.obs;
@@ -261,14 +274,16 @@ __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStati
 template <int S, bool kSkip>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4)))
 ndvm_replay(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
-    replay_body<S, false, kSkip>(A, table, single);
+    uint32_t q, bx;
+    if (work_item(A, q, bx)) replay_body<S, false, kSkip>(A, table, single, q, bx);
 }
 
 // Registers beyond r_lds spill to lane-contiguous workspace rows.
 template <int S>
 __global__ void __launch_bounds__(64)
 ndvm_replay_spill(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
-    replay_body<S, true, true>(A, table, single);
+    uint32_t q, bx;
+    if (work_item(A, q, bx)) replay_body<S, true, true>(A, table, single, q, bx);
 }
 
 // Many programs in one launch, only some of which spill: each workgroup takes
@@ -277,10 +292,12 @@ ndvm_replay_spill(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic
 template <int S, bool kSkip>
 __global__ void __launch_bounds__(64)
 ndvm_replay_per_program(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
-    if (table[blockIdx.y].spills)
-        replay_body<S, true, true>(A, table, single);
+    uint32_t q, bx;
+    if (!work_item(A, q, bx)) return;
+    if (table[q].spills)
+        replay_body<S, true, true>(A, table, single, q, bx);
     else
-        replay_body<S, false, kSkip>(A, table, single);
+        replay_body<S, false, kSkip>(A, table, single, q, bx);
 }
 
 namespace {
@@ -302,7 +319,7 @@ hipError_t launch_s(const LaunchArgs &A, const ProgStatic *d_table, const ProgSt
             (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_smem);
     });
     constexpr int LW = 64 / S;
-    dim3 grid(uint32_t((A.L + LW - 1) / LW), n_prog), block(64);
+    dim3 grid = A.wg_items ? dim3(A.n_wg) : dim3(uint32_t((A.L + LW - 1) / LW), n_prog), block(64);
     size_t smem = size_t(r_lds) * LW * sizeof(double);
     if (variant == kPerProgram && d_table) {
         if (skips)

@@ -174,6 +174,12 @@ struct LaunchArgs {
     double *ws;
     int64_t ld_p, ld_g, L, Lpad, prog_stride_p, prog_stride_g;
     int64_t n_points = 0, obs_stride = 0;
+    // Many-program launches laid out per XCD: a one-dimensional grid of n_wg
+    // workgroups, workgroup w taking the work item wg_items[w] = program << 32
+    // | lane block (all ones: none).  Null: program blockIdx.y, lane block
+    // blockIdx.x.
+    const uint64_t *wg_items = nullptr;
+    uint32_t n_wg = 0;
 };
 
 }  // namespace ndvm
