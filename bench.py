@@ -194,7 +194,7 @@ def build_inputs(name, torch, device, policy="recompute", branch_skip=False):
     t0 = time.perf_counter()
     tapes_b = [nd.tape_build(bc) for bc in bcs]
     t1 = time.perf_counter()
-    tapes = [nd.tape_upload(t, policy=POLICIES[policy] | (nd.BRANCH_SKIP if branch_skip else 0)) for t in tapes_b]
+    tapes = nd.tape_upload_many(tapes_b, policy=POLICIES[policy] | (nd.BRANCH_SKIP if branch_skip else 0))
     t2 = time.perf_counter()
     if name == "random_programs":
         n_prog, L, P = p.shape

@@ -128,6 +128,20 @@ ndvm_status ndvm_tape_build(const uint8_t *bytecode, size_t bytecode_len,
 ndvm_status ndvm_tape_upload(const uint8_t *tape, size_t tape_len, int policy,
                              void *stream, ndvm_tape **out);
 
+/*
+ * ndvm_tape_upload for a population of n tapes (tape i: host bytes tapes[i],
+ * lens[i] of them), all with one `policy`: the tapes are validated and their
+ * forward programs scheduled on all host threads, then copied to GPU memory on
+ * `stream` in order.  On success out[i] receives tape i's handle (each
+ * released with ndvm_tape_free); on any error every out[i] is NULL, nothing is
+ * left allocated and the message names the first failing tape.  n = 0 is a
+ * no-op.  Library infrastructure for program populations (the replay of
+ * Section 3.4 applied to many candidate programs).
+ * Errors: as ndvm_tape_upload; NDVM_E_ARG for n < 0 or null arrays or tapes.
+ */
+ndvm_status ndvm_tape_upload_many(const uint8_t *const *tapes, const size_t *lens, int n, int policy,
+                                  void *stream, ndvm_tape **out);
+
 /* Sizes of an uploaded tape.  Library infrastructure (no passage of the
  * paper defines it): counts the caller may want for logging or sizing.
  * Errors: NDVM_E_ARG. */

@@ -25,7 +25,7 @@ BRANCH_SKIP = 0x100    # option OR'd into the policy: waves skip branch arms non
 NOALLOC_SCRATCH_BYTES = 64 << 20    # NDVM_NOALLOC_SCRATCH_BYTES
 
 # exported symbols of include/ndvm.h
-EXPORTS = ["ndvm_tape_build", "ndvm_tape_upload", "ndvm_tape_info_get", "ndvm_workspace_bytes",
+EXPORTS = ["ndvm_tape_build", "ndvm_tape_upload", "ndvm_tape_upload_many", "ndvm_tape_info_get", "ndvm_workspace_bytes",
            "ndvm_forward", "ndvm_grad", "ndvm_grad_many", "ndvm_workspace_bytes_many",
            "ndvm_tape_free", "ndvm_free", "ndvm_last_error", "ndvm_adam_step", "ndvm_grad_noalloc",
            "ndvm_grad_points", "ndvm_workspace_bytes_points", "ndvm_walk_prepare", "ndvm_walk_measure", "ndvm_walk_workspace_bytes",
@@ -54,6 +54,8 @@ def _sig(name, res, args):
 
 _tape_build = _sig("ndvm_tape_build", _int, [ctypes.c_char_p, _sz, ctypes.POINTER(_vp), ctypes.POINTER(_sz)])
 _tape_upload = _sig("ndvm_tape_upload", _int, [ctypes.c_char_p, _sz, _int, _vp, ctypes.POINTER(_vp)])
+_tape_upload_many = _sig("ndvm_tape_upload_many", _int, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_sz), _int,
+                                                         _int, _vp, ctypes.POINTER(_vp)])
 _tape_info = _sig("ndvm_tape_info_get", _int, [_vp, ctypes.POINTER(_Info)])
 _ws_bytes = _sig("ndvm_workspace_bytes", _int, [_vp, _i64, _int, ctypes.POINTER(_sz)])
 _ws_bytes_many = _sig("ndvm_workspace_bytes_many", _int, [ctypes.POINTER(_vp), _int, _i64, ctypes.POINTER(_sz)])
@@ -161,6 +163,16 @@ def tape_upload(tape_bytes: bytes, policy: int = POLICY_RECOMPUTE, stream=None) 
     _check(_tape_upload(tape_bytes, len(tape_bytes), policy, _stream_ptr(stream), ctypes.byref(h)),
            "ndvm_tape_upload")
     return Tape(h.value)
+
+
+def tape_upload_many(tapes: Sequence[bytes], policy: int = POLICY_RECOMPUTE, stream=None) -> list:
+    """tape_upload for a population of tapes (one library call)."""
+    n = len(tapes)
+    arr = (ctypes.c_char_p * n)(*tapes)
+    lens = (_sz * n)(*[len(t) for t in tapes])
+    hs = (_vp * n)()
+    _check(_tape_upload_many(arr, lens, n, policy, _stream_ptr(stream), hs), "ndvm_tape_upload_many")
+    return [Tape(h) for h in hs]
 
 
 def tape_info(tape: Tape) -> dict:

@@ -12,6 +12,7 @@
 #include <map>
 #include <memory>
 #include <mutex>
+#include <thread>
 #include <new>
 
 #include "common.h"
@@ -183,7 +184,14 @@ ndvm_status scheduled(F f, Schedule *out) {
 // budget b.  Scheduling and the program's upload happen only in the sizing
 // calls (build = true); a compute call finds the program or fails, so it
 // never schedules on the host or waits for a copy.
-ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, bool build, DevProg **out) {
+Schedule schedule_grad_of(const ndvm_tape *tape, uint32_t S, uint32_t b) {
+    return schedule_grad(tape->tape, b, S, tape->policy == NDVM_POLICY_SAVE, tape->arms ? kArmMinElems : 0);
+}
+
+// `pre`: the schedule, when the caller made it already (many-program sizing
+// schedules its programs in parallel).
+ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, bool build, DevProg **out,
+                         Schedule *pre = nullptr) {
     std::lock_guard<std::mutex> lk(tape->mu);
     const uint64_t key = (uint64_t(S) << 32) | b;
     auto it = tape->grad.find(key);
@@ -195,19 +203,71 @@ ndvm_status grad_program(ndvm_tape *tape, uint32_t S, uint32_t b, bool build, De
     if (it == tape->grad.end()) {
         const hipStream_t stream = nullptr;
         Schedule sch;
-        ndvm_status st = scheduled(
-            [&] {
-                return schedule_grad(tape->tape, b, S, tape->policy == NDVM_POLICY_SAVE,
-                                     tape->arms ? kArmMinElems : 0);
-            },
-            &sch);
-        if (st != NDVM_OK) return st;
+        if (pre) {
+            sch = std::move(*pre);
+        } else {
+            ndvm_status st = scheduled([&] { return schedule_grad_of(tape, S, b); }, &sch);
+            if (st != NDVM_OK) return st;
+        }
+        ndvm_status st;
         std::unique_ptr<DevProg> dp;
         st = upload_program(std::move(sch), tape->tape, stream, &dp);
         if (st != NDVM_OK) return st;
         it = tape->grad.emplace(key, std::move(dp)).first;
     }
     *out = it->second.get();
+    return NDVM_OK;
+}
+
+// Schedules of the programs among `tapes` that have no device program for
+// (S, b) yet, made on all host threads (each program's schedule is
+// independent of the others); the uploads stay with the caller.  On a
+// failure the first failing program's status and message are returned.
+ndvm_status schedule_many(const ndvm_tape *const *tapes, int n_prog, uint32_t S, uint32_t b,
+                          std::map<const ndvm_tape *, Schedule> *out) {
+    const uint64_t key = (uint64_t(S) << 32) | b;
+    std::vector<const ndvm_tape *> todo;
+    for (int q = 0; q < n_prog; ++q) {
+        ndvm_tape *t = const_cast<ndvm_tape *>(tapes[q]);
+        std::lock_guard<std::mutex> lk(t->mu);
+        if (!t->grad.count(key) && !out->count(t)) {
+            out->emplace(t, Schedule{});
+            todo.push_back(t);
+        }
+    }
+    if (todo.empty()) return NDVM_OK;
+    std::vector<Schedule> res(todo.size());
+    std::vector<ndvm_status> code(todo.size(), NDVM_OK);
+    std::vector<std::string> msg(todo.size());
+    std::atomic<size_t> next{0};
+    auto work = [&]() {
+        for (size_t i; (i = next.fetch_add(1)) < todo.size();) {
+            try {
+                res[i] = schedule_grad_of(todo[i], S, b);
+            } catch (const std::length_error &e) {
+                code[i] = NDVM_E_UNSUPPORTED;
+                msg[i] = std::string("program too large for the device format: ") + e.what();
+            } catch (const std::bad_alloc &) {
+                code[i] = NDVM_E_NOMEM;
+                msg[i] = "out of host memory";
+            } catch (const std::exception &e) {
+                code[i] = NDVM_E_INTERNAL;
+                msg[i] = std::string("internal error: ") + e.what();
+            }
+        }
+    };
+    const size_t n_threads = std::min<size_t>(todo.size(), std::max(1u, std::thread::hardware_concurrency()));
+    std::vector<std::thread> pool;
+    for (size_t k = 1; k < n_threads; ++k) pool.emplace_back(work);
+    work();
+    for (auto &th : pool) th.join();
+    for (size_t i = 0; i < todo.size(); ++i) {
+        if (code[i] != NDVM_OK) {
+            set_error(msg[i]);
+            return code[i];
+        }
+        (*out)[todo[i]] = std::move(res[i]);
+    }
     return NDVM_OK;
 }
 
@@ -243,13 +303,21 @@ uint32_t fwd_budget(uint32_t S) {
 }
 
 // Forward-only device program of `tape` with S slots.
-ndvm_status fwd_program(ndvm_tape *tape, uint32_t S, hipStream_t stream, DevProg **out) {
+Schedule schedule_forward_of(const ndvm_tape *tape, uint32_t S) {
+    return schedule_forward(tape->tape, S, fwd_budget(S), tape->arms ? kArmMinElems : 0);
+}
+
+// `pre`: the schedule, when the caller made it already.
+ndvm_status fwd_program(ndvm_tape *tape, uint32_t S, hipStream_t stream, DevProg **out, Schedule *pre = nullptr) {
     std::lock_guard<std::mutex> lk(tape->mu);
     auto it = tape->fwd.find(S);
     if (it == tape->fwd.end()) {
         Schedule sch;
-        ndvm_status st =
-            scheduled([&] { return schedule_forward(tape->tape, S, fwd_budget(S), tape->arms ? kArmMinElems : 0); }, &sch);
+        ndvm_status st = NDVM_OK;
+        if (pre)
+            sch = std::move(*pre);
+        else
+            st = scheduled([&] { return schedule_forward_of(tape, S); }, &sch);
         if (st != NDVM_OK) return st;
         std::unique_ptr<DevProg> dp;
         st = upload_program(std::move(sch), tape->tape, stream, &dp);
@@ -360,9 +428,13 @@ ndvm_status many_launch(const ndvm_tape *const *tapes, int n_prog, int64_t L, bo
     uint32_t r_launch = 0;
     int n_spill = 0;
     std::vector<uint32_t> cost(static_cast<size_t>(n_prog));
+    std::map<const ndvm_tape *, Schedule> pre;
+    if (build && (st = schedule_many(tapes, n_prog, S, b, &pre)) != NDVM_OK) return st;
     for (int q = 0; q < n_prog; ++q) {
         DevProg *dp;
-        if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), S, b, build, &dp)) != NDVM_OK) return st;
+        auto pi = pre.find(tapes[q]);
+        Schedule *ps = pi != pre.end() && pi->second.code.size() ? &pi->second : nullptr;
+        if ((st = grad_program(const_cast<ndvm_tape *>(tapes[q]), S, b, build, &dp, ps)) != NDVM_OK) return st;
         cost[q] = dp->meta.n_instr;
         uint32_t r_lds = std::min(dp->meta.n_regs, b);
         r_launch = std::max(r_launch, r_lds);
@@ -501,30 +573,111 @@ ndvm_status ndvm_tape_build(const uint8_t *bytecode, size_t len, uint8_t **tape,
     });
 }
 
+// Host part of an upload: parse and validate the tape into a new handle.
+static ndvm_status new_tape(const uint8_t *bytes, size_t len, int save, bool arms, std::unique_ptr<ndvm_tape> *out) {
+    auto h = std::make_unique<ndvm_tape>();
+    ndvm_status st = parse_tape(bytes, len, &h->tape);
+    if (st != NDVM_OK) return st;
+    h->tape_bytes = len;
+    h->policy = save;
+    h->arms = arms;
+    for (const TapeOp &o : h->tape.ops) h->n_selects += o.code == tp::SELECT;
+    *out = std::move(h);
+    return NDVM_OK;
+}
+
+static ndvm_status check_policy(int policy, const char *who) {
+    const int save = policy & ~NDVM_BRANCH_SKIP;
+    if (save != NDVM_POLICY_RECOMPUTE && save != NDVM_POLICY_SAVE) {
+        set_error(std::string(who) + ": unsupported save policy");
+        return NDVM_E_UNSUPPORTED;
+    }
+    return NDVM_OK;
+}
+
 ndvm_status ndvm_tape_upload(const uint8_t *bytes, size_t len, int policy, void *stream, ndvm_tape **out) {
     return guarded([&]() -> ndvm_status {
         if (!bytes || !out) {
             set_error("ndvm_tape_upload: null argument");
             return NDVM_E_ARG;
         }
-        const int save = policy & ~NDVM_BRANCH_SKIP;
-        if (save != NDVM_POLICY_RECOMPUTE && save != NDVM_POLICY_SAVE) {
-            set_error("ndvm_tape_upload: unsupported save policy");
-            return NDVM_E_UNSUPPORTED;
-        }
-        auto h = std::make_unique<ndvm_tape>();
-        ndvm_status st = parse_tape(bytes, len, &h->tape);
+        ndvm_status st = check_policy(policy, "ndvm_tape_upload");
         if (st != NDVM_OK) return st;
+        std::unique_ptr<ndvm_tape> h;
+        if ((st = new_tape(bytes, len, policy & ~NDVM_BRANCH_SKIP, (policy & NDVM_BRANCH_SKIP) != 0, &h)) != NDVM_OK)
+            return st;
         h->id = g_next_id++;
-        h->tape_bytes = len;
-        h->policy = save;
-        h->arms = (policy & NDVM_BRANCH_SKIP) != 0;
-        for (const TapeOp &o : h->tape.ops) h->n_selects += o.code == tp::SELECT;
         // schedule the forward program now: scheduling limits surface at upload
         DevProg *fp = nullptr;
         st = fwd_program(h.get(), 4, static_cast<hipStream_t>(stream), &fp);
         if (st != NDVM_OK) return st;
         *out = h.release();
+        return NDVM_OK;
+    });
+}
+
+ndvm_status ndvm_tape_upload_many(const uint8_t *const *tapes, const size_t *lens, int n, int policy, void *stream,
+                                  ndvm_tape **out) {
+    return guarded([&]() -> ndvm_status {
+        if (n < 0 || (n > 0 && (!tapes || !lens || !out))) {
+            set_error("ndvm_tape_upload_many: bad argument");
+            return NDVM_E_ARG;
+        }
+        for (int i = 0; i < n; ++i) {
+            out[i] = nullptr;
+            if (!tapes[i]) {
+                set_error("ndvm_tape_upload_many: null tape");
+                return NDVM_E_ARG;
+            }
+        }
+        ndvm_status st = check_policy(policy, "ndvm_tape_upload_many");
+        if (st != NDVM_OK || n == 0) return st;
+        const int save = policy & ~NDVM_BRANCH_SKIP;
+        const bool arms = (policy & NDVM_BRANCH_SKIP) != 0;
+        // parse and schedule the forward programs on all host threads
+        std::vector<std::unique_ptr<ndvm_tape>> hs(static_cast<size_t>(n));
+        std::vector<Schedule> fw(static_cast<size_t>(n));
+        std::vector<ndvm_status> code(static_cast<size_t>(n), NDVM_OK);
+        std::vector<std::string> msg(static_cast<size_t>(n));
+        std::atomic<int> next{0};
+        auto work = [&]() {
+            for (int i; (i = next.fetch_add(1)) < n;) {
+                try {
+                    if ((code[i] = new_tape(tapes[i], lens[i], save, arms, &hs[i])) != NDVM_OK) {
+                        msg[i] = get_error();
+                        continue;
+                    }
+                    fw[i] = schedule_forward_of(hs[i].get(), 4);
+                } catch (const std::length_error &e) {
+                    code[i] = NDVM_E_UNSUPPORTED;
+                    msg[i] = std::string("program too large for the device format: ") + e.what();
+                } catch (const std::bad_alloc &) {
+                    code[i] = NDVM_E_NOMEM;
+                    msg[i] = "out of host memory";
+                } catch (const std::exception &e) {
+                    code[i] = NDVM_E_INTERNAL;
+                    msg[i] = std::string("internal error: ") + e.what();
+                }
+            }
+        };
+        const int n_threads = std::min(n, int(std::max(1u, std::thread::hardware_concurrency())));
+        std::vector<std::thread> pool;
+        for (int k = 1; k < n_threads; ++k) pool.emplace_back(work);
+        work();
+        for (auto &th : pool) th.join();
+        for (int i = 0; i < n; ++i)
+            if (code[i] != NDVM_OK) {
+                set_error("ndvm_tape_upload_many: tape " + std::to_string(i) + ": " + msg[i]);
+                return code[i];
+            }
+        // upload in order; on a failure nothing is returned
+        for (int i = 0; i < n; ++i) {
+            hs[i]->id = g_next_id++;
+            DevProg *fp = nullptr;
+            if ((st = fwd_program(hs[i].get(), 4, static_cast<hipStream_t>(stream), &fp, &fw[i])) != NDVM_OK)
+                return st;
+        }
+        for (int i = 0; i < n; ++i) out[i] = hs[i].release();
         return NDVM_OK;
     });
 }

@@ -261,3 +261,25 @@ def test_register_hungry_program_runs_in_rounds_instead_of_spilling(nd, oracle_m
     idx = np.r_[0:64, 16320:16448, 32704:32768]
     lo, go, _ = oracle_mod.run(w.bytecode, w.params[idx], w.obs)
     compare(lf.cpu().numpy()[idx], gf.cpu().numpy()[idx], lo, go)
+
+
+def test_batch_upload_equals_single_uploads(nd):
+    """Tapes uploaded together (validated and scheduled on all host threads)
+    give the same device programs as tapes uploaded one by one: a
+    many-program gradient over either set is bit-identical, and so is each
+    tape's forward loss."""
+    w = configs.random_programs(n_prog=40, L=64, n=16, seed=12)
+    bs = [nd.tape_build(bc) for bc in w.programs]
+    one = [nd.tape_upload(b) for b in bs]
+    many = nd.tape_upload_many(bs)
+    assert len(many) == len(one)
+    p = torch.tensor(w.params, device="cuda")
+    o = torch.tensor(w.obs, device="cuda")
+    l1, g1 = nd.grad_many(one, p, o)
+    l2, g2 = nd.grad_many(many, p, o)
+    torch.cuda.synchronize()
+    assert torch.equal(l1, l2) and torch.equal(g1, g2)
+    for q in (0, 17, 39):
+        P = w.n_params_each[q]
+        pq = p[q, :, :P].contiguous()
+        assert torch.equal(nd.forward(one[q], pq, o), nd.forward(many[q], pq, o))

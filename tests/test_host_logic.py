@@ -126,6 +126,25 @@ def test_malformed_tape_rejected_before_gpu_work():
     assert e.value.status == nd.E_UNSUPPORTED
 
 
+def test_batch_upload_rejects_a_malformed_tape_before_gpu_work():
+    # the first failing tape is named; no handle is returned; the batch is
+    # validated on the host before anything is copied to the device
+    good = nd.tape_build(configs.exp_decay(L=1, n=4).bytecode)
+    bad = good[:-1]
+    with pytest.raises(nd.NdvmError) as e:
+        nd.tape_upload_many([good, good, bad, good, bad], stream=0)
+    assert e.value.status == nd.E_TAPE
+    assert "tape 2" in str(e.value)
+    assert nd.tape_upload_many([], stream=0) == []
+    lib = ctypes.CDLL(nd.LIB_PATH)
+    assert lib.ndvm_tape_upload_many(None, None, -1, 0, None, None) == nd.E_ARG
+    assert lib.ndvm_tape_upload_many(None, None, 1, 0, None, None) == nd.E_ARG
+    arr = (ctypes.c_char_p * 1)(good)
+    lens = (ctypes.c_size_t * 1)(len(good))
+    out = (ctypes.c_void_p * 1)()
+    assert lib.ndvm_tape_upload_many(arr, lens, 1, 77, None, out) == nd.E_UNSUPPORTED
+
+
 CASES = [("exp_decay", dict(L=9)), ("logistic_euler", dict(L=9, T=60)),
          ("lotka_volterra_rk4", dict(L=9, T=25)), ("kalman_cv4", dict(L=9, T=12))]
 
