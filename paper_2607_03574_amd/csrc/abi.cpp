@@ -303,8 +303,8 @@ uint32_t fwd_budget(uint32_t S) {
 }
 
 // Forward-only device program of `tape` with S slots.
-Schedule schedule_forward_of(const ndvm_tape *tape, uint32_t S) {
-    return schedule_forward(tape->tape, S, fwd_budget(S), tape->arms ? kArmMinElems : 0);
+Schedule schedule_forward_of(const ndvm_tape *tape, uint32_t S, uint32_t budget) {
+    return schedule_forward(tape->tape, S, budget, tape->arms ? kArmMinElems : 0);
 }
 
 // `pre`: the schedule, when the caller made it already.
@@ -317,7 +317,7 @@ ndvm_status fwd_program(ndvm_tape *tape, uint32_t S, hipStream_t stream, DevProg
         if (pre)
             sch = std::move(*pre);
         else
-            st = scheduled([&] { return schedule_forward_of(tape, S); }, &sch);
+            st = scheduled([&] { return schedule_forward_of(tape, S, fwd_budget(S)); }, &sch);
         if (st != NDVM_OK) return st;
         std::unique_ptr<DevProg> dp;
         st = upload_program(std::move(sch), tape->tape, stream, &dp);
@@ -634,7 +634,9 @@ ndvm_status ndvm_tape_upload_many(const uint8_t *const *tapes, const size_t *len
         if (st != NDVM_OK || n == 0) return st;
         const int save = policy & ~NDVM_BRANCH_SKIP;
         const bool arms = (policy & NDVM_BRANCH_SKIP) != 0;
-        // parse and schedule the forward programs on all host threads
+        // parse and schedule the forward programs on all host threads (the
+        // register budget comes from this thread's current device)
+        const uint32_t fb = fwd_budget(4);
         std::vector<std::unique_ptr<ndvm_tape>> hs(static_cast<size_t>(n));
         std::vector<Schedule> fw(static_cast<size_t>(n));
         std::vector<ndvm_status> code(static_cast<size_t>(n), NDVM_OK);
@@ -647,7 +649,7 @@ ndvm_status ndvm_tape_upload_many(const uint8_t *const *tapes, const size_t *len
                         msg[i] = get_error();
                         continue;
                     }
-                    fw[i] = schedule_forward_of(hs[i].get(), 4);
+                    fw[i] = schedule_forward_of(hs[i].get(), 4, fb);
                 } catch (const std::length_error &e) {
                     code[i] = NDVM_E_UNSUPPORTED;
                     msg[i] = std::string("program too large for the device format: ") + e.what();
