@@ -101,18 +101,29 @@ __device__ __forceinline__ uint32_t opaque(uint32_t v) {
 
 // LDS addresses of the four register fields of instruction P: each is the
 // broadcast byte offset plus this thread's lane address, one DPP-sourced add
-// per field (the s_nop covers the wait states a DPP read of a VGPR written
-// by a preceding VALU op needs).
+// per field.  A DPP read of a VGPR that a VALU op wrote needs two wait states
+// between them (the s_nop); the chunk word is written once per chunk, before
+// instruction 0, so only that instruction waits.  No VALU op of this kernel
+// writes EXEC.
 template <int P>
 __device__ __forceinline__ void field_addrs(uint32_t ch, uint32_t la, uint32_t &a, uint32_t &x, uint32_t &y,
                                             uint32_t &z) {
-    asm("s_nop 1\n\t"
-        "v_add_u32_dpp %0, %4, %5 row_newbcast:%6 row_mask:0xf bank_mask:0xf\n\t"
-        "v_add_u32_dpp %1, %4, %5 row_newbcast:%7 row_mask:0xf bank_mask:0xf\n\t"
-        "v_add_u32_dpp %2, %4, %5 row_newbcast:%8 row_mask:0xf bank_mask:0xf\n\t"
-        "v_add_u32_dpp %3, %4, %5 row_newbcast:%9 row_mask:0xf bank_mask:0xf"
-        : "=&v"(a), "=&v"(x), "=&v"(y), "=&v"(z)
-        : "v"(ch), "v"(la), "i"(4 * P), "i"(4 * P + 1), "i"(4 * P + 2), "i"(4 * P + 3));
+    if constexpr (P == 0) {
+        asm("s_nop 1\n\t"
+            "v_add_u32_dpp %0, %4, %5 row_newbcast:0 row_mask:0xf bank_mask:0xf\n\t"
+            "v_add_u32_dpp %1, %4, %5 row_newbcast:1 row_mask:0xf bank_mask:0xf\n\t"
+            "v_add_u32_dpp %2, %4, %5 row_newbcast:2 row_mask:0xf bank_mask:0xf\n\t"
+            "v_add_u32_dpp %3, %4, %5 row_newbcast:3 row_mask:0xf bank_mask:0xf"
+            : "=&v"(a), "=&v"(x), "=&v"(y), "=&v"(z)
+            : "v"(ch), "v"(la));
+    } else {
+        asm("v_add_u32_dpp %0, %4, %5 row_newbcast:%6 row_mask:0xf bank_mask:0xf\n\t"
+            "v_add_u32_dpp %1, %4, %5 row_newbcast:%7 row_mask:0xf bank_mask:0xf\n\t"
+            "v_add_u32_dpp %2, %4, %5 row_newbcast:%8 row_mask:0xf bank_mask:0xf\n\t"
+            "v_add_u32_dpp %3, %4, %5 row_newbcast:%9 row_mask:0xf bank_mask:0xf"
+            : "=&v"(a), "=&v"(x), "=&v"(y), "=&v"(z)
+            : "v"(ch), "v"(la), "i"(4 * P), "i"(4 * P + 1), "i"(4 * P + 2), "i"(4 * P + 3));
+    }
 }
 
 // Payload of instruction P of a chunk: register fields as LDS addresses,
@@ -149,70 +160,74 @@ __device__ __attribute__((noinline)) void cold_call(const C &c, uint32_t form, P
 }
 
 // Instruction P of the chunk held in `ch` (one dword per thread), header
-// lane hb + P of `hv`; returns 1 when it is END.
+// lane hb of `hv`.  END and the padding after it do nothing: the loop
+// below runs the chunks up to the one holding END and stops.
 template <int P, bool kSkip, class C>
-__device__ __forceinline__ uint32_t step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb) {
+__device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb) {
     if (kSkip && c.skip) {   // inside a skipped arm (never holds END)
         --c.skip;
-        return 0;
+        return;
     }
-    const uint32_t hdr = lane_word(hv, hb + P);
+    const uint32_t hdr = lane_word(hv, hb);
     const uint32_t form = hdr & slot::kFormMask;
     ChunkPayload<P> p;
     field_addrs<P>(ch, c.lane_addr, p.ha, p.hx, p.hy, p.hz);
     p.ch = ch;
     p.hdr = hdr;
     p.slot = c.slot_;
-    // multiply-add and the linear adjoint rule are tested one by one ahead
-    // of the dispatch tree; the empty asm hides that the later tests are on
-    // the same value, so the compiler cannot fold them into one balanced
-    // tree (which would put every form several compares deep)
-    if (form == slot::MAC) {
+    // multiply-add and the linear adjoint rule are tested one by one, each
+    // by its own header bit, ahead of the dispatch tree; the empty asm hides
+    // that the later tests are on the same value, so the compiler cannot
+    // fold them into one balanced tree (which would put every form several
+    // compares deep)
+    if (__builtin_expect((hdr & slot::kMacBit) != 0, 1)) {
         slotx::exec_mac(c, p);
-        return 0;
+        return;
     }
-    const uint32_t f1 = opaque(form);
-    if (f1 == slot::ACC) {
+    if (__builtin_expect((hdr & slot::kAccBit) != 0, 1)) {
         slotx::exec_acc(c, p);
-        return 0;
+        return;
     }
-    const uint32_t f2 = opaque(f1);
+    const uint32_t f2 = opaque(form);
     if (f2 < slot::HOT_END) {
         slotx::exec_hot(c, f2, p);
-        return 0;
+        return;
     }
-    if (f2 == slot::END) return 1;
+    if (f2 == slot::END) return;
     cold_call(c, f2,
               Payload{{row_word<4 * P>(ch), row_word<4 * P + 1>(ch), row_word<4 * P + 2>(ch), row_word<4 * P + 3>(ch)},
                       hdr, c.slot_, c.lane_addr});
-    return 0;
 }
 
-// Execute a slot program until END: the four instructions of each chunk in
-// straight-line code, chunk c + 2 requested when chunk c starts, headers
-// 64 at a time with the next group in flight (the program is padded for
-// these read-aheads; instructions after END are END too).
+// Execute a slot program through the chunk holding END: the four
+// instructions of each chunk in straight-line code, chunk c + 2 requested
+// when chunk c starts, the headers of 64 chunks at a time (four per thread)
+// with the next group in flight (the program is padded for these
+// read-aheads: the chunk holding END is followed by kFetchAhead chunks,
+// which is how the chunk count is known, and instructions after END are END
+// too).
 template <bool kSkip, int S, bool kSpill>
 __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *prog, uint32_t hdr_off) {
-    static_assert(slot::kChunk == 4 && slot::kFetchAhead == 2 && slot::kHeaderGroup == 64,
-                  "the fetch below reads four-instruction chunks two ahead and 64 headers a group");
+    static_assert(slot::kChunk == 4 && slot::kFetchAhead == 2 && slot::kHeaderGroup == 256,
+                  "the fetch below reads four-instruction chunks two ahead and the headers of 64 chunks a group");
+    using Hdr4 = uint32_t __attribute__((ext_vector_type(4)));
     const AS_GLOBAL uint32_t *pc = (const AS_GLOBAL uint32_t *)prog + threadIdx.x;
-    const AS_GLOBAL uint32_t *ph = (const AS_GLOBAL uint32_t *)prog + hdr_off + threadIdx.x;
+    const AS_GLOBAL Hdr4 *ph = (const AS_GLOBAL Hdr4 *)((const AS_GLOBAL uint32_t *)prog + hdr_off) + threadIdx.x;
     constexpr uint32_t W = slot::kChunkWords;
     uint32_t cur = pc[0], n1 = pc[W];
-    uint32_t hv = ph[0], hn = ph[64];
-    for (uint32_t chunk = 0;; ++chunk) {
+    Hdr4 hv = ph[0], hn = ph[64];
+    const uint32_t n_chunks = hdr_off / W - slot::kFetchAhead;
+    for (uint32_t chunk = 0; chunk < n_chunks; ++chunk) {
         pc += W;
         const uint32_t n2 = pc[W];
-        const uint32_t hb = (chunk & 15u) * 4;
-        uint32_t ended = step<0, kSkip>(c, cur, hv, hb);
-        ended |= step<1, kSkip>(c, cur, hv, hb);
-        ended |= step<2, kSkip>(c, cur, hv, hb);
-        ended |= step<3, kSkip>(c, cur, hv, hb);
-        if (ended) return;
+        const uint32_t hb = chunk & 63u;
+        step<0, kSkip>(c, cur, hv.x, hb);
+        step<1, kSkip>(c, cur, hv.y, hb);
+        step<2, kSkip>(c, cur, hv.z, hb);
+        step<3, kSkip>(c, cur, hv.w, hb);
         cur = n1;
         n1 = n2;
-        if ((chunk & 15u) == 15u) {
+        if (hb == 63u) {
             ph += 64;
             hv = hn;
             hn = ph[64];
@@ -280,7 +295,7 @@ ndvm_replay(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic singl
 
 // Registers beyond r_lds spill to lane-contiguous workspace rows.
 template <int S>
-__global__ void __launch_bounds__(64)
+__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4)))
 ndvm_replay_spill(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
     uint32_t q, bx;
     if (work_item(A, q, bx)) replay_body<S, true, true>(A, table, single, q, bx);
@@ -290,7 +305,7 @@ ndvm_replay_spill(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic
 // the variant its program needs, so one spilling program does not slow the
 // others down.
 template <int S, bool kSkip>
-__global__ void __launch_bounds__(64)
+__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4)))
 ndvm_replay_per_program(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
     uint32_t q, bx;
     if (!work_item(A, q, bx)) return;

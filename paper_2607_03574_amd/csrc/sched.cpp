@@ -2069,7 +2069,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
         const auto [first, cnt] = spans[i];
         const UOp &u0 = flat[first];
         const uint32_t f = u0.form;
-        uint32_t hdr = f | u0.imm << kImmShift;
+        uint32_t hdr = form_bits(f) | u0.imm << kImmShift;
         if (f == STLOSS || f == STGRAD) hdr = f | cnt << kImmShift;
         if (is_ckmove(f)) {   // the largest row count of the instruction's slots
             uint32_t mx = 1;

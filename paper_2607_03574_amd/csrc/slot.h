@@ -16,8 +16,9 @@
 //
 // Per instruction: a header word, the same for every slot:
 //   bits 0-5 form, bits 6-9 kFirst of slots 0-3 (first contribution to the
-//   target: store, do not add), bits 10-13 zero, bits 14-31 the form's
-//   immediate;
+//   target: store, do not add), bit 10 set when the form is MAC, bit 11 when
+//   it is ACC (the two most frequent forms, told apart by one bit test),
+//   bits 12-13 zero, bits 14-31 the form's immediate;
 // and per slot four words a, x, y, z: a register named in a field is held as
 // its byte offset in a lane's register file (register * 8 * 64/S), an index
 // (observation, parameter, constant, checkpoint row) as itself.
@@ -89,6 +90,11 @@ enum Unary : uint32_t { U_SIN = 0, U_COS };
 constexpr uint32_t kFormMask = 63u;
 constexpr uint32_t kSkipSideShift = 17, kSkipCountMask = (1u << kSkipSideShift) - 1;
 constexpr uint32_t kFirstShift = 6, kImmShift = 14;
+constexpr uint32_t kMacBit = 1u << 10, kAccBit = 1u << 11;
+// the form's own bits of a header (form number and its one-hot flag)
+inline uint32_t form_bits(uint32_t form) {
+    return form | (form == MAC ? kMacBit : 0u) | (form == ACC ? kAccBit : 0u);
+}
 constexpr uint32_t kMaxImm = (1u << 18) - 1;
 constexpr uint32_t kMaxBlock = 4;            // outputs of a block form (sink and trash rows reserved)
 
@@ -118,16 +124,17 @@ inline uint32_t dotb_imm(uint32_t K, uint32_t N, uint32_t sx, uint32_t sy, uint3
 // carries the micro-ops of slot r * S / 4, and thread 16r + j holds word j
 // of its row (instruction j / 4, word j % 4), so one coalesced dword load per
 // thread fetches the chunk and a row broadcast hands every thread of a slot
-// its words.  The headers follow the chunks, kHeaderGroup at a time (thread
-// t of a wave holds header t of a group).  The chunk holding END is followed
-// by two more chunks and the header group holding it by two more groups (the
-// fetch reads two ahead).  Slot counts 1, 2 and 4 (a slot's threads fill
-// whole rows).
+// its words.  The headers follow the chunks, kHeaderGroup at a time: thread
+// t of a wave holds the four headers of chunk t of a group (one 16-byte
+// load), so the four instructions of a chunk read their headers from one
+// lane.  The chunk holding END is followed by two more chunks and the header
+// group holding it by two more groups (the fetch reads two ahead).  Slot
+// counts 1, 2 and 4 (a slot's threads fill whole rows).
 constexpr uint32_t kChunk = 4;
 constexpr uint32_t kRows = 4;
 constexpr uint32_t kChunkWords = kRows * kChunk * 4;
 constexpr uint32_t kFetchAhead = 2;
-constexpr uint32_t kHeaderGroup = 64;
+constexpr uint32_t kHeaderGroup = 64 * kChunk;
 constexpr uint32_t kMaxSlots = 4;
 
 inline bool is_hot(uint32_t form) { return form >= MAC && form < HOT_END; }
