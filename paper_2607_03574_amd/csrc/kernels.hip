@@ -162,7 +162,7 @@ __device__ __attribute__((noinline)) void cold_call(const C &c, uint32_t form, P
 // Instruction P of the chunk held in `ch` (one dword per thread), header
 // lane hb of `hv`.  END and the padding after it do nothing: the loop
 // below runs the chunks up to the one holding END and stops.
-template <int P, bool kSkip, class C>
+template <int P, bool kSkip, bool kAccFirst, class C>
 __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb) {
     if (kSkip && c.skip) {   // inside a skipped arm (never holds END)
         --c.skip;
@@ -175,18 +175,36 @@ __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint3
     p.ch = ch;
     p.hdr = hdr;
     p.slot = c.slot_;
-    // multiply-add and the linear adjoint rule are tested one by one, each
-    // by its own header bit, ahead of the dispatch tree; the empty asm hides
-    // that the later tests are on the same value, so the compiler cannot
-    // fold them into one balanced tree (which would put every form several
-    // compares deep)
-    if (__builtin_expect((hdr & slot::kMacBit) != 0, 1)) {
-        slotx::exec_mac(c, p);
-        return;
-    }
-    if (__builtin_expect((hdr & slot::kAccBit) != 0, 1)) {
-        slotx::exec_acc(c, p);
-        return;
+    // the most frequent forms are tested one by one, each by its own header
+    // bit, ahead of the dispatch tree, in the launch's order: multiply-add
+    // then the linear adjoint rule, or the adjoint rule, multiply-add and
+    // multiply-subtract (programs whose reverse sweep dominates); the first
+    // runs straight into the next instruction.  The empty asm hides that the
+    // tree's tests are on the same value as the form, so the compiler cannot
+    // fold the tests into one balanced tree (which would put every form
+    // several compares deep).
+    if constexpr (kAccFirst) {
+        if (__builtin_expect((hdr & slot::kAccBit) != 0, 1)) {
+            slotx::exec_acc(c, p);
+            return;
+        }
+        if (__builtin_expect((hdr & slot::kMacBit) != 0, 1)) {
+            slotx::exec_mac(c, p);
+            return;
+        }
+        if (__builtin_expect((hdr & slot::kMsubBit) != 0, 1)) {
+            slotx::exec_msub(c, p);
+            return;
+        }
+    } else {
+        if (__builtin_expect((hdr & slot::kMacBit) != 0, 1)) {
+            slotx::exec_mac(c, p);
+            return;
+        }
+        if (__builtin_expect((hdr & slot::kAccBit) != 0, 1)) {
+            slotx::exec_acc(c, p);
+            return;
+        }
     }
     const uint32_t f2 = opaque(form);
     if (f2 < slot::HOT_END) {
@@ -206,7 +224,7 @@ __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint3
 // read-aheads: the chunk holding END is followed by kFetchAhead chunks,
 // which is how the chunk count is known, and instructions after END are END
 // too).
-template <bool kSkip, int S, bool kSpill>
+template <bool kSkip, bool kAccFirst, int S, bool kSpill>
 __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *prog, uint32_t hdr_off) {
     static_assert(slot::kChunk == 4 && slot::kFetchAhead == 2 && slot::kHeaderGroup == 256,
                   "the fetch below reads four-instruction chunks two ahead and the headers of 64 chunks a group");
@@ -221,10 +239,10 @@ __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *
         pc += W;
         const uint32_t n2 = pc[W];
         const uint32_t hb = chunk & 63u;
-        step<0, kSkip>(c, cur, hv.x, hb);
-        step<1, kSkip>(c, cur, hv.y, hb);
-        step<2, kSkip>(c, cur, hv.z, hb);
-        step<3, kSkip>(c, cur, hv.w, hb);
+        step<0, kSkip, kAccFirst>(c, cur, hv.x, hb);
+        step<1, kSkip, kAccFirst>(c, cur, hv.y, hb);
+        step<2, kSkip, kAccFirst>(c, cur, hv.z, hb);
+        step<3, kSkip, kAccFirst>(c, cur, hv.w, hb);
         cur = n1;
         n1 = n2;
         if (hb == 63u) {
@@ -251,7 +269,7 @@ __device__ __forceinline__ bool work_item(const LaunchArgs &A, uint32_t &q, uint
     return it != ~uint64_t(0);
 }
 
-template <int S, bool kSpill, bool kSkip>
+template <int S, bool kSpill, bool kSkip, bool kAccFirst>
 __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStatic *__restrict__ table,
                                             const ProgStatic &single, uint32_t q, uint32_t bx) {
     extern __shared__ double lds_regs[];
@@ -280,17 +298,18 @@ __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStati
     c.ld_p = A.ld_p;
     c.ld_g = A.ld_g;
     c.r_lds = D.r_lds;
-    run<kSkip>(c, D.prog, D.hdr_off);
+    run<kSkip, kAccFirst>(c, D.prog, D.hdr_off);
 }
 
 // All lane registers in LDS (the usual case: the scheduler fits the register
 // file to the launch's LDS budget).  kSkip: the program has skippable branch
-// arms (every instruction then tests the skip counter first).
-template <int S, bool kSkip>
+// arms (every instruction then tests the skip counter first).  kAccFirst:
+// the order of the form tests (see step).
+template <int S, bool kSkip, bool kAccFirst>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4)))
 ndvm_replay(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
     uint32_t q, bx;
-    if (work_item(A, q, bx)) replay_body<S, false, kSkip>(A, table, single, q, bx);
+    if (work_item(A, q, bx)) replay_body<S, false, kSkip, kAccFirst>(A, table, single, q, bx);
 }
 
 // Registers beyond r_lds spill to lane-contiguous workspace rows.
@@ -298,7 +317,7 @@ template <int S>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4)))
 ndvm_replay_spill(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
     uint32_t q, bx;
-    if (work_item(A, q, bx)) replay_body<S, true, true>(A, table, single, q, bx);
+    if (work_item(A, q, bx)) replay_body<S, true, true, false>(A, table, single, q, bx);
 }
 
 // Many programs in one launch, only some of which spill: each workgroup takes
@@ -310,24 +329,26 @@ ndvm_replay_per_program(LaunchArgs A, const ProgStatic *__restrict__ table, Prog
     uint32_t q, bx;
     if (!work_item(A, q, bx)) return;
     if (table[q].spills)
-        replay_body<S, true, true>(A, table, single, q, bx);
+        replay_body<S, true, true, false>(A, table, single, q, bx);
     else
-        replay_body<S, false, kSkip>(A, table, single, q, bx);
+        replay_body<S, false, kSkip, false>(A, table, single, q, bx);
 }
 
 namespace {
 
 template <int S>
 hipError_t launch_s(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                    uint32_t r_lds, int variant, bool skips, hipStream_t stream) {
+                    uint32_t r_lds, int variant, bool skips, bool acc_first, hipStream_t stream) {
     static std::once_flag once[64];
     int dev = 0;
     (void)hipGetDevice(&dev);
     std::call_once(once[dev & 63], [dev]() {
         int max_smem = 0;
         (void)hipDeviceGetAttribute(&max_smem, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-        for (const void *f : {reinterpret_cast<const void *>(&ndvm_replay<S, false>),
-                              reinterpret_cast<const void *>(&ndvm_replay<S, true>),
+        for (const void *f : {reinterpret_cast<const void *>(&ndvm_replay<S, false, false>),
+                              reinterpret_cast<const void *>(&ndvm_replay<S, true, false>),
+                              reinterpret_cast<const void *>(&ndvm_replay<S, false, true>),
+                              reinterpret_cast<const void *>(&ndvm_replay<S, true, true>),
                               reinterpret_cast<const void *>(&ndvm_replay_spill<S>),
                               reinterpret_cast<const void *>(&ndvm_replay_per_program<S, false>),
                               reinterpret_cast<const void *>(&ndvm_replay_per_program<S, true>)})
@@ -344,9 +365,14 @@ hipError_t launch_s(const LaunchArgs &A, const ProgStatic *d_table, const ProgSt
     } else if (variant == kSpill || variant == kPerProgram) {
         hipLaunchKernelGGL(ndvm_replay_spill<S>, grid, block, smem, stream, A, d_table, single);
     } else if (skips) {
-        hipLaunchKernelGGL((ndvm_replay<S, true>), grid, block, smem, stream, A, d_table, single);
+        if (acc_first)
+            hipLaunchKernelGGL((ndvm_replay<S, true, true>), grid, block, smem, stream, A, d_table, single);
+        else
+            hipLaunchKernelGGL((ndvm_replay<S, true, false>), grid, block, smem, stream, A, d_table, single);
+    } else if (acc_first) {
+        hipLaunchKernelGGL((ndvm_replay<S, false, true>), grid, block, smem, stream, A, d_table, single);
     } else {
-        hipLaunchKernelGGL((ndvm_replay<S, false>), grid, block, smem, stream, A, d_table, single);
+        hipLaunchKernelGGL((ndvm_replay<S, false, false>), grid, block, smem, stream, A, d_table, single);
     }
     return hipGetLastError();
 }
@@ -422,9 +448,10 @@ hipError_t scratch_address(void **out) {
 }
 
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, int variant, bool skips, uint32_t slots, hipStream_t stream) {
+                         uint32_t r_lds, int variant, bool skips, bool acc_first, uint32_t slots,
+                         hipStream_t stream) {
     switch (slots) {
-    case 4: return launch_s<4>(A, d_table, single, n_prog, r_lds, variant, skips, stream);
+    case 4: return launch_s<4>(A, d_table, single, n_prog, r_lds, variant, skips, acc_first, stream);
     default: return hipErrorInvalidValue;
     }
 }

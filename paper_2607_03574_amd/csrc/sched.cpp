@@ -2092,6 +2092,9 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
         }
         Sch.code[hdr_off + i] = hdr;
         Sch.n_slots_used += cnt;
+        Sch.n_mac += f == MAC;
+        Sch.n_acc += f == ACC;
+        Sch.n_msub += f == MSUB;
     }
     Sch.n_chunks = n_chunks;
     return Sch;

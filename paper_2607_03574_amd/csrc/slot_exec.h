@@ -187,8 +187,8 @@ NDVM_HD void dot_block(const C &c, const W &p) {
     dot_block_generic<ACC>(c, p, K, N, sx, sy, sc, neg);
 }
 
-// The two most frequent forms, also callable on their own (the kernel tests
-// for them ahead of the general dispatch).
+// The most frequent forms, also callable on their own (the kernel tests for
+// them ahead of the general dispatch).
 template <class C, class W>
 NDVM_HD void exec_mac(const C &c, const W &p) {
     const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
@@ -198,6 +198,11 @@ template <class C, class W>
 NDVM_HD void exec_acc(const C &c, const W &p) {
     const double x = c.ld(p.x()), y = c.ld(p.y()), base = c.ld(p.z());
     c.st(p.a(), x != 0.0 ? base + x * y : base);
+}
+template <class C, class W>
+NDVM_HD void exec_msub(const C &c, const W &p) {
+    const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+    c.st(p.a(), x * y - z);
 }
 
 // Hot micro-ops (forms below HOT_END): straight-line code, no per-lane
@@ -221,11 +226,7 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
     case DIV:
         c.st(p.a(), c.ld(p.x()) / c.ld(p.y()));
         return;
-    case MSUB: {
-        const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
-        c.st(p.a(), x * y - z);
-        return;
-    }
+    case MSUB: exec_msub(c, p); return;
     case RSUB: {
         const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
         c.st(p.a(), z - x * y);
