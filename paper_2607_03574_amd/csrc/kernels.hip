@@ -99,29 +99,34 @@ __device__ __forceinline__ uint32_t opaque(uint32_t v) {
     return v;
 }
 
-// LDS addresses of the four register fields of instruction P: each is the
-// broadcast byte offset plus this thread's lane address, one DPP-sourced add
-// per field.  A DPP read of a VGPR that a VALU op wrote needs two wait states
-// between them (the s_nop); the chunk word is written once per chunk, before
-// instruction 0, so only that instruction waits.  No VALU op of this kernel
-// writes EXEC.
-template <int P>
-__device__ __forceinline__ void field_addrs(uint32_t ch, uint32_t la, uint32_t &a, uint32_t &x, uint32_t &y,
-                                            uint32_t &z) {
-    if constexpr (P == 0) {
-        asm("s_nop 1\n\t"
-            "v_add_u32_dpp %0, %4, %5 row_newbcast:0 row_mask:0xf bank_mask:0xf\n\t"
-            "v_add_u32_dpp %1, %4, %5 row_newbcast:1 row_mask:0xf bank_mask:0xf\n\t"
-            "v_add_u32_dpp %2, %4, %5 row_newbcast:2 row_mask:0xf bank_mask:0xf\n\t"
-            "v_add_u32_dpp %3, %4, %5 row_newbcast:3 row_mask:0xf bank_mask:0xf"
-            : "=&v"(a), "=&v"(x), "=&v"(y), "=&v"(z)
-            : "v"(ch), "v"(la));
-    } else {
-        asm("v_add_u32_dpp %0, %4, %5 row_newbcast:%6 row_mask:0xf bank_mask:0xf\n\t"
+// LDS addresses of the four register fields of instruction P of the chunk
+// word `ch`: each is the broadcast byte offset plus this thread's lane
+// address, one DPP-sourced add per field.  A DPP read of a VGPR that a VALU
+// op wrote needs two wait states between them (the s_nop, kept where the
+// chunk word may just have been copied into place); no VALU op of this
+// kernel writes EXEC.  Volatile: the decode of the next instruction stays
+// where it is placed, in the shadow of the current instruction's loads.
+struct Fields {
+    uint32_t a, x, y, z;
+};
+template <int P, bool kNop>
+__device__ __forceinline__ void decode(uint32_t ch, uint32_t la, Fields &f) {
+    if constexpr (kNop) {
+        asm volatile(
+            "s_nop 1\n\t"
+            "v_add_u32_dpp %0, %4, %5 row_newbcast:%6 row_mask:0xf bank_mask:0xf\n\t"
             "v_add_u32_dpp %1, %4, %5 row_newbcast:%7 row_mask:0xf bank_mask:0xf\n\t"
             "v_add_u32_dpp %2, %4, %5 row_newbcast:%8 row_mask:0xf bank_mask:0xf\n\t"
             "v_add_u32_dpp %3, %4, %5 row_newbcast:%9 row_mask:0xf bank_mask:0xf"
-            : "=&v"(a), "=&v"(x), "=&v"(y), "=&v"(z)
+            : "=&v"(f.a), "=&v"(f.x), "=&v"(f.y), "=&v"(f.z)
+            : "v"(ch), "v"(la), "i"(4 * P), "i"(4 * P + 1), "i"(4 * P + 2), "i"(4 * P + 3));
+    } else {
+        asm volatile(
+            "v_add_u32_dpp %0, %4, %5 row_newbcast:%6 row_mask:0xf bank_mask:0xf\n\t"
+            "v_add_u32_dpp %1, %4, %5 row_newbcast:%7 row_mask:0xf bank_mask:0xf\n\t"
+            "v_add_u32_dpp %2, %4, %5 row_newbcast:%8 row_mask:0xf bank_mask:0xf\n\t"
+            "v_add_u32_dpp %3, %4, %5 row_newbcast:%9 row_mask:0xf bank_mask:0xf"
+            : "=&v"(f.a), "=&v"(f.x), "=&v"(f.y), "=&v"(f.z)
             : "v"(ch), "v"(la), "i"(4 * P), "i"(4 * P + 1), "i"(4 * P + 2), "i"(4 * P + 3));
     }
 }
@@ -159,22 +164,42 @@ __device__ __attribute__((noinline)) void cold_call(const C &c, uint32_t form, P
     slotx::exec_cold(c, form, p);
 }
 
+// The most frequent forms, written out here so that the decode of the next
+// instruction (`next`) is issued between their loads and their arithmetic,
+// while the loads are in flight.  Same arithmetic as the shared handlers.
+template <class C, class N>
+__device__ __forceinline__ void hot_mac(const C &c, const Fields &f, N &&next) {
+    const double x = c.ld(f.x), y = c.ld(f.y), z = c.ld(f.z);
+    next();
+    c.st(f.a, x * y + z);
+}
+template <class C, class N>
+__device__ __forceinline__ void hot_acc(const C &c, const Fields &f, N &&next) {
+    const double x = c.ld(f.x), y = c.ld(f.y), base = c.ld(f.z);
+    next();
+    c.st(f.a, x != 0.0 ? base + x * y : base);
+}
+template <class C, class N>
+__device__ __forceinline__ void hot_msub(const C &c, const Fields &f, N &&next) {
+    const double x = c.ld(f.x), y = c.ld(f.y), z = c.ld(f.z);
+    next();
+    c.st(f.a, x * y - z);
+}
+
 // Instruction P of the chunk held in `ch` (one dword per thread), header
-// lane hb of `hv`.  END and the padding after it do nothing: the loop
-// below runs the chunks up to the one holding END and stops.
-template <int P, bool kSkip, bool kAccFirst, class C>
-__device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb) {
+// lane hb of `hv`, register fields `f` (decoded by the previous
+// instruction); `next` decodes the following instruction.  END and the
+// padding after it do nothing: the loop below runs the chunks up to the one
+// holding END and stops.
+template <int P, bool kSkip, bool kAccFirst, class C, class N>
+__device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb, const Fields &f, N &&next) {
     if (kSkip && c.skip) {   // inside a skipped arm (never holds END)
         --c.skip;
+        next();
         return;
     }
     const uint32_t hdr = lane_word(hv, hb);
     const uint32_t form = hdr & slot::kFormMask;
-    ChunkPayload<P> p;
-    field_addrs<P>(ch, c.lane_addr, p.ha, p.hx, p.hy, p.hz);
-    p.ch = ch;
-    p.hdr = hdr;
-    p.slot = c.slot_;
     // the most frequent forms are tested one by one, each by its own header
     // bit, ahead of the dispatch tree, in the launch's order: multiply-add
     // then the linear adjoint rule, or the adjoint rule, multiply-add and
@@ -185,27 +210,36 @@ __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint3
     // several compares deep).
     if constexpr (kAccFirst) {
         if (__builtin_expect((hdr & slot::kAccBit) != 0, 1)) {
-            slotx::exec_acc(c, p);
+            hot_acc(c, f, next);
             return;
         }
         if (__builtin_expect((hdr & slot::kMacBit) != 0, 1)) {
-            slotx::exec_mac(c, p);
+            hot_mac(c, f, next);
             return;
         }
         if (__builtin_expect((hdr & slot::kMsubBit) != 0, 1)) {
-            slotx::exec_msub(c, p);
+            hot_msub(c, f, next);
             return;
         }
     } else {
         if (__builtin_expect((hdr & slot::kMacBit) != 0, 1)) {
-            slotx::exec_mac(c, p);
+            hot_mac(c, f, next);
             return;
         }
         if (__builtin_expect((hdr & slot::kAccBit) != 0, 1)) {
-            slotx::exec_acc(c, p);
+            hot_acc(c, f, next);
             return;
         }
     }
+    next();
+    ChunkPayload<P> p;
+    p.ha = f.a;
+    p.hx = f.x;
+    p.hy = f.y;
+    p.hz = f.z;
+    p.ch = ch;
+    p.hdr = hdr;
+    p.slot = c.slot_;
     const uint32_t f2 = opaque(form);
     if (f2 < slot::HOT_END) {
         slotx::exec_hot(c, f2, p);
@@ -235,14 +269,17 @@ __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *
     uint32_t cur = pc[0], n1 = pc[W];
     Hdr4 hv = ph[0], hn = ph[64];
     const uint32_t n_chunks = hdr_off / W - slot::kFetchAhead;
+    const uint32_t la = c.lane_addr;
+    Fields f0, f1, f2, f3;
+    decode<0, true>(cur, la, f0);
     for (uint32_t chunk = 0; chunk < n_chunks; ++chunk) {
         pc += W;
         const uint32_t n2 = pc[W];
         const uint32_t hb = chunk & 63u;
-        step<0, kSkip, kAccFirst>(c, cur, hv.x, hb);
-        step<1, kSkip, kAccFirst>(c, cur, hv.y, hb);
-        step<2, kSkip, kAccFirst>(c, cur, hv.z, hb);
-        step<3, kSkip, kAccFirst>(c, cur, hv.w, hb);
+        step<0, kSkip, kAccFirst>(c, cur, hv.x, hb, f0, [&] { decode<1, true>(cur, la, f1); });
+        step<1, kSkip, kAccFirst>(c, cur, hv.y, hb, f1, [&] { decode<2, false>(cur, la, f2); });
+        step<2, kSkip, kAccFirst>(c, cur, hv.z, hb, f2, [&] { decode<3, false>(cur, la, f3); });
+        step<3, kSkip, kAccFirst>(c, cur, hv.w, hb, f3, [&] { decode<0, true>(n1, la, f0); });
         cur = n1;
         n1 = n2;
         if (hb == 63u) {
