@@ -27,6 +27,7 @@ namespace {
 // register numbers (the host context's handles).
 struct P4 {
     uint32_t w[4], hdr, slot, reg_bytes;
+    uint32_t *n_loaded;   // calls of loaded() (a hot handler makes exactly one)
     uint32_t a() const { return w[0] / reg_bytes; }
     uint32_t x() const { return w[1] / reg_bytes; }
     uint32_t y() const { return w[2] / reg_bytes; }
@@ -34,6 +35,7 @@ struct P4 {
     uint32_t ix() const { return w[1]; }
     uint32_t imm() const { return hdr >> slot::kImmShift; }
     bool first() const { return (hdr >> (slot::kFirstShift + slot)) & 1u; }
+    void loaded() const { ++*n_loaded; }
 };
 
 struct HostCtx {
@@ -47,7 +49,8 @@ struct HostCtx {
     uint32_t n_ckpt;   // rows including the trash row
     int *fault;        // first problem seen: 1 register range, 2 unwritten read, 3 pool/param/obs index,
                        // 4 ckpt row, 6 read of a register another slot writes, 7 two slots write one register,
-                       // 8 form differs between slots, 9 output store or skip test inside a skipped arm
+                       // 8 form differs between slots, 9 output store or skip test inside a skipped arm,
+                       // 10 a hot handler marked its operand reads other than once
     uint32_t cur_slot = 0;
     bool cur_dummy = false;   // an unused slot (result to the sink): its reads are never checked
     std::vector<std::pair<uint32_t, double>> *pending;
@@ -249,14 +252,16 @@ int ndvm_emu_run(const uint8_t *tape, size_t len, int with_grad, uint32_t reg_bu
                 // slot sl's words sit in rows sl * 4 / S ..; take the first
                 const uint32_t r = sl * slot::kRows / slots;
                 const uint32_t *w = &S.code[size_t(i / K) * slot::kChunkWords + (size_t(r) * K + i % K) * 4];
-                const P4 p{{w[0], w[1], w[2], w[3]}, hdr, sl, reg_bytes};
+                uint32_t n_loaded = 0;
+                const P4 p{{w[0], w[1], w[2], w[3]}, hdr, sl, reg_bytes, &n_loaded};
                 c.cur_slot = sl;
                 c.cur_dummy = c.poison || (slot::writes_a(form) && p.a() == sink) ||
                               (form == slot::CKST && (p.ix() & slot::kCkRowMask) == S.n_ckpt_rows);
                 c.cur_accum = accumulates(form, p);
-                if (slot::is_hot(form))
+                if (slot::is_hot(form)) {
                     slotx::exec_hot(c, form, p);
-                else
+                    if (n_loaded != 1) c.flag(10);
+                } else
                     slotx::exec_cold(c, form, p);
             }
             c.commit();

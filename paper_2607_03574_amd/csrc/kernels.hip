@@ -132,10 +132,13 @@ __device__ __forceinline__ void decode(uint32_t ch, uint32_t la, Fields &f) {
 }
 
 // Payload of instruction P of a chunk: register fields as LDS addresses,
-// the header supplies the immediate and this slot's flags.
-template <int P>
+// the header supplies the immediate and this slot's flags; loaded() runs
+// the decode of the next instruction (the handlers call it once, between
+// their reads and their arithmetic).
+template <int P, class N>
 struct ChunkPayload {
     uint32_t ha, hx, hy, hz, ch, hdr, slot;
+    N *nx;
     __device__ __forceinline__ uint32_t a() const { return ha; }
     __device__ __forceinline__ uint32_t x() const { return hx; }
     __device__ __forceinline__ uint32_t y() const { return hy; }
@@ -143,6 +146,7 @@ struct ChunkPayload {
     __device__ __forceinline__ uint32_t ix() const { return row_word<4 * P + 1>(ch); }
     __device__ __forceinline__ uint32_t imm() const { return hdr >> slot::kImmShift; }
     __device__ __forceinline__ bool first() const { return (hdr >> (slot::kFirstShift + slot)) & 1u; }
+    __device__ __forceinline__ void loaded() const { (*nx)(); }
 };
 // Payload of a cold instruction, words read out
 struct Payload {
@@ -164,35 +168,13 @@ __device__ __attribute__((noinline)) void cold_call(const C &c, uint32_t form, P
     slotx::exec_cold(c, form, p);
 }
 
-// The most frequent forms, written out here so that the decode of the next
-// instruction (`next`) is issued between their loads and their arithmetic,
-// while the loads are in flight.  Same arithmetic as the shared handlers.
-template <class C, class N>
-__device__ __forceinline__ void hot_mac(const C &c, const Fields &f, N &&next) {
-    const double x = c.ld(f.x), y = c.ld(f.y), z = c.ld(f.z);
-    next();
-    c.st(f.a, x * y + z);
-}
-template <class C, class N>
-__device__ __forceinline__ void hot_acc(const C &c, const Fields &f, N &&next) {
-    const double x = c.ld(f.x), y = c.ld(f.y), base = c.ld(f.z);
-    next();
-    c.st(f.a, x != 0.0 ? base + x * y : base);
-}
-template <class C, class N>
-__device__ __forceinline__ void hot_msub(const C &c, const Fields &f, N &&next) {
-    const double x = c.ld(f.x), y = c.ld(f.y), z = c.ld(f.z);
-    next();
-    c.st(f.a, x * y - z);
-}
-
 // Instruction P of the chunk held in `ch` (one dword per thread), header
 // lane hb of `hv`, register fields `f` (decoded by the previous
 // instruction); `next` decodes the following instruction.  END and the
 // padding after it do nothing: the loop below runs the chunks up to the one
 // holding END and stops.
 template <int P, bool kSkip, bool kAccFirst, class C, class N>
-__device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb, const Fields &f, N &&next) {
+__device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb, const Fields &f, N &next) {
     if (kSkip && c.skip) {   // inside a skipped arm (never holds END)
         --c.skip;
         next();
@@ -200,6 +182,7 @@ __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint3
     }
     const uint32_t hdr = lane_word(hv, hb);
     const uint32_t form = hdr & slot::kFormMask;
+    const ChunkPayload<P, N> p{f.a, f.x, f.y, f.z, ch, hdr, c.slot_, &next};
     // the most frequent forms are tested one by one, each by its own header
     // bit, ahead of the dispatch tree, in the launch's order: multiply-add
     // then the linear adjoint rule, or the adjoint rule, multiply-add and
@@ -210,41 +193,33 @@ __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint3
     // several compares deep).
     if constexpr (kAccFirst) {
         if (__builtin_expect((hdr & slot::kAccBit) != 0, 1)) {
-            hot_acc(c, f, next);
+            slotx::exec_acc(c, p);
             return;
         }
         if (__builtin_expect((hdr & slot::kMacBit) != 0, 1)) {
-            hot_mac(c, f, next);
+            slotx::exec_mac(c, p);
             return;
         }
         if (__builtin_expect((hdr & slot::kMsubBit) != 0, 1)) {
-            hot_msub(c, f, next);
+            slotx::exec_msub(c, p);
             return;
         }
     } else {
         if (__builtin_expect((hdr & slot::kMacBit) != 0, 1)) {
-            hot_mac(c, f, next);
+            slotx::exec_mac(c, p);
             return;
         }
         if (__builtin_expect((hdr & slot::kAccBit) != 0, 1)) {
-            hot_acc(c, f, next);
+            slotx::exec_acc(c, p);
             return;
         }
     }
-    next();
-    ChunkPayload<P> p;
-    p.ha = f.a;
-    p.hx = f.x;
-    p.hy = f.y;
-    p.hz = f.z;
-    p.ch = ch;
-    p.hdr = hdr;
-    p.slot = c.slot_;
     const uint32_t f2 = opaque(form);
     if (f2 < slot::HOT_END) {
         slotx::exec_hot(c, f2, p);
         return;
     }
+    next();
     if (f2 == slot::END) return;
     cold_call(c, f2,
               Payload{{row_word<4 * P>(ch), row_word<4 * P + 1>(ch), row_word<4 * P + 2>(ch), row_word<4 * P + 3>(ch)},
@@ -276,10 +251,14 @@ __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *
         pc += W;
         const uint32_t n2 = pc[W];
         const uint32_t hb = chunk & 63u;
-        step<0, kSkip, kAccFirst>(c, cur, hv.x, hb, f0, [&] { decode<1, true>(cur, la, f1); });
-        step<1, kSkip, kAccFirst>(c, cur, hv.y, hb, f1, [&] { decode<2, false>(cur, la, f2); });
-        step<2, kSkip, kAccFirst>(c, cur, hv.z, hb, f2, [&] { decode<3, false>(cur, la, f3); });
-        step<3, kSkip, kAccFirst>(c, cur, hv.w, hb, f3, [&] { decode<0, true>(n1, la, f0); });
+        auto d1 = [&] { decode<1, true>(cur, la, f1); };
+        auto d2 = [&] { decode<2, false>(cur, la, f2); };
+        auto d3 = [&] { decode<3, false>(cur, la, f3); };
+        auto d0 = [&] { decode<0, true>(n1, la, f0); };   // instruction 0 of the next chunk
+        step<0, kSkip, kAccFirst>(c, cur, hv.x, hb, f0, d1);
+        step<1, kSkip, kAccFirst>(c, cur, hv.y, hb, f1, d2);
+        step<2, kSkip, kAccFirst>(c, cur, hv.z, hb, f2, d3);
+        step<3, kSkip, kAccFirst>(c, cur, hv.w, hb, f3, d0);
         cur = n1;
         n1 = n2;
         if (hb == 63u) {

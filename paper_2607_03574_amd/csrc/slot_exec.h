@@ -17,8 +17,11 @@
 //   void store_loss(double v, bool on) const;  void store_grad(uint32_t p, double v, bool on) const;
 //   uint32_t slot() const;
 // and W is the payload of this slot's micro-op: register handles a(), x(),
-// y(), z(), the raw field ix() (an index), the uniform immediate imm() and
-// this slot's first-contribution flag first().
+// y(), z(), the raw field ix() (an index), the uniform immediate imm(), this
+// slot's first-contribution flag first(), and loaded(), which every hot
+// handler calls exactly once, after issuing its operand reads and before
+// its arithmetic (the GPU decodes the next instruction there, while the
+// reads are in flight; the host emulator checks the count).
 //
 // Adjoint rules follow Appendix C, table tab:adjoints: contractions are fma
 // chains over the summation index in ascending order with a plain product as
@@ -87,6 +90,7 @@ NDVM_HD void any_nonzero(const C &c, const W &p) {
     double v[K];
 #pragma unroll
     for (uint32_t k = 0; k < K; ++k) v[k] = c.ld(c.adv(x, k));
+    p.loaded();
     bool nz = false;
 #pragma unroll
     for (uint32_t k = 0; k < K; ++k) nz = nz | (v[k] != 0.0);
@@ -121,6 +125,9 @@ NDVM_HD void dot_block_kn(const C &c, const W &p, uint32_t sx, uint32_t sy, uint
 #pragma unroll
         for (uint32_t j = 0; j < N; ++j) base[j] = base_of(c, c.adv(a, j), first);
     }
+    // the next instruction's decode after the products (with all operands
+    // live it would cost registers the wave does not have)
+    double out[N];
 #pragma unroll
     for (uint32_t j = 0; j < N; ++j) {
         double s = X[0] * Y[0][j];
@@ -130,14 +137,18 @@ NDVM_HD void dot_block_kn(const C &c, const W &p, uint32_t sx, uint32_t sy, uint
             if (neg) s = -s;
             s = g != 0.0 ? base[j] + s : base[j];
         }
-        c.st(c.adv(a, j), s);
+        out[j] = s;
     }
+    p.loaded();
+#pragma unroll
+    for (uint32_t j = 0; j < N; ++j) c.st(c.adv(a, j), out[j]);
 }
 
 // any K, N <= 7: the same arithmetic with uniform loop bounds
 template <bool ACC, class C, class W>
 NDVM_HD void dot_block_generic(const C &c, const W &p, uint32_t K, uint32_t N, uint32_t sx, uint32_t sy,
                                uint32_t sc, bool neg) {
+    p.loaded();
     const auto a = p.a(), x = p.x(), y = p.y();
     const double g = ACC ? c.ld(p.z()) : 1.0;
     const bool first = p.first();
@@ -192,16 +203,19 @@ NDVM_HD void dot_block(const C &c, const W &p) {
 template <class C, class W>
 NDVM_HD void exec_mac(const C &c, const W &p) {
     const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+    p.loaded();
     c.st(p.a(), x * y + z);
 }
 template <class C, class W>
 NDVM_HD void exec_acc(const C &c, const W &p) {
     const double x = c.ld(p.x()), y = c.ld(p.y()), base = c.ld(p.z());
+    p.loaded();
     c.st(p.a(), x != 0.0 ? base + x * y : base);
 }
 template <class C, class W>
 NDVM_HD void exec_msub(const C &c, const W &p) {
     const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+    p.loaded();
     c.st(p.a(), x * y - z);
 }
 
@@ -220,15 +234,20 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         const auto a = p.a();
         const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());
         const double base = base_of(c, a, p.first());
+        p.loaded();
         c.st(a, g != 0.0 ? base + x * y : base);
         return;
     }
-    case DIV:
-        c.st(p.a(), c.ld(p.x()) / c.ld(p.y()));
+    case DIV: {
+        const double x = c.ld(p.x()), y = c.ld(p.y());
+        p.loaded();
+        c.st(p.a(), x / y);
         return;
+    }
     case MSUB: exec_msub(c, p); return;
     case RSUB: {
         const double x = c.ld(p.x()), y = c.ld(p.y()), z = c.ld(p.z());
+        p.loaded();
         c.st(p.a(), z - x * y);
         return;
     }
@@ -236,6 +255,7 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         const auto a = p.a();
         const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());
         const double base = base_of(c, a, p.first());
+        p.loaded();
         c.st(a, g != 0.0 ? base + x / y : base);
         return;
     }
@@ -243,15 +263,18 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         const auto a = p.a();
         const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());
         const double base = base_of(c, a, p.first());
+        p.loaded();
         c.st(a, g != 0.0 ? base + -(x / y) : base);
         return;
     }
     case DOT: {
+        p.loaded();
         const uint32_t im = p.imm();
         c.st(p.a(), dot_chain(c, p.x(), p.y(), im & 31u, (im >> 6) & 63u, (im >> 12) & 63u));
         return;
     }
     case DOTACC: {
+        p.loaded();
         const uint32_t im = p.imm();
         const auto a = p.a();
         double s = dot_chain(c, p.x(), p.y(), im & 31u, (im >> 6) & 63u, (im >> 12) & 63u);
@@ -261,29 +284,38 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         c.st(a, g != 0.0 ? base + s : base);
         return;
     }
-    case CMPLT:
-        c.st(p.a(), c.ld(p.x()) < c.ld(p.y()) ? 1.0 : 0.0);
+    case CMPLT: {
+        const double x = c.ld(p.x()), y = c.ld(p.y());
+        p.loaded();
+        c.st(p.a(), x < y ? 1.0 : 0.0);
         return;
+    }
     case SELP: {   // the untaken arm's register may hold anything (its arm may have been skipped)
         const double q = c.ld(p.x()), y = c.ld_raw(p.y()), z = c.ld_raw(p.z());
+        p.loaded();
         c.check_written(q != 0.0 ? p.y() : p.z());
         c.st(p.a(), q != 0.0 ? y : z);
         return;
     }
-    case SKIP:   // wave-level branch skipping: every lane takes the other arm
-        c.skip_arm(c.ld(p.x()) != 0.0, p.imm());
+    case SKIP: {   // wave-level branch skipping: every lane takes the other arm
+        const double q = c.ld(p.x());
+        p.loaded();
+        c.skip_arm(q != 0.0, p.imm());
         return;
+    }
     case ACCSEL: {
         const auto a = p.a();
         const double x = c.ld(p.x()), q = c.ld(p.y()), g = c.ld(p.z());
         const bool want = (p.imm() & 1u) != 0;
         const double base = base_of(c, a, p.first());
+        p.loaded();
         c.st(a, ((g != 0.0) & ((q != 0.0) == want)) ? base + x : base);
         return;
     }
     case DET2: {
         const auto x = p.x();
         const double a0 = c.ld(x), a1 = c.ld(c.adv(x, 1)), a2 = c.ld(c.adv(x, 2)), a3 = c.ld(c.adv(x, 3));
+        p.loaded();
         const double t1 = a0 * a3;
         const double t2 = a1 * a2;
         c.st(p.a(), t1 - t2);
@@ -300,6 +332,7 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         default: break;
         }
         // other sizes: reads in groups of four; bitwise ors, so no lane skips a read
+        p.loaded();
         const auto x = p.x();
         bool nz = false;
         for (uint32_t k0 = 0; k0 < K; k0 += 4) {
@@ -314,6 +347,7 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
     }
     case GATEGT: {
         const double x = c.ld(p.x()), y = c.ld(p.y()), g = c.ld(p.z());
+        p.loaded();
         c.st(p.a(), ((g != 0.0) & (x > y)) ? 1.0 : 0.0);
         return;
     }
@@ -322,11 +356,13 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         const double x = c.ld(p.x()), v = c.ld(p.y()), g = c.ld(p.z());
         const double d = v > 0.0 ? x : (v < 0.0 ? -x : 0.0);
         const double base = base_of(c, a, p.first());
+        p.loaded();
         c.st(a, g != 0.0 ? base + d : base);
         return;
     }
     case SUMK: {
         // reads in groups of four, then the sum in index order
+        p.loaded();
         const uint32_t im = p.imm(), K = im & 63u, st = (im >> 6) & 63u;
         const auto x = p.x();
         double s = 0.0;
@@ -342,6 +378,7 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         return;
     }
     case ZERO:
+        p.loaded();
         c.st(p.a(), 0.0);
         return;
     case DOTB:
@@ -350,31 +387,55 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
     case DOTBACC:
         dot_block<true>(c, p);
         return;
-    case EXPF:
-        c.st(p.a(), exp(c.ld(p.x())));
+    case EXPF: {
+        const double x = c.ld(p.x());
+        p.loaded();
+        c.st(p.a(), exp(x));
         return;
-    case LOGCF:
-        c.st(p.a(), log(clampv(c.ld(p.x()))));
+    }
+    case LOGCF: {
+        const double x = c.ld(p.x());
+        p.loaded();
+        c.st(p.a(), log(clampv(x)));
         return;
-    case LOGF:
-        c.st(p.a(), log(c.ld(p.x())));
+    }
+    case LOGF: {
+        const double x = c.ld(p.x());
+        p.loaded();
+        c.st(p.a(), log(x));
         return;
-    case SQRTCF:
-        c.st(p.a(), sqrt(clampv(c.ld(p.x()))));
+    }
+    case SQRTCF: {
+        const double x = c.ld(p.x());
+        p.loaded();
+        c.st(p.a(), sqrt(clampv(x)));
         return;
-    case ABSF:
-        c.st(p.a(), fabs(c.ld(p.x())));
+    }
+    case ABSF: {
+        const double x = c.ld(p.x());
+        p.loaded();
+        c.st(p.a(), fabs(x));
         return;
+    }
 
-    case LDOBS:
-        c.st(p.a(), c.obsv(p.ix()));
+    case LDOBS: {
+        const double v = c.obsv(p.ix());
+        p.loaded();
+        c.st(p.a(), v);
         return;
-    case LDPARAM:
-        c.st(p.a(), c.param(p.ix()));
+    }
+    case LDPARAM: {
+        const double v = c.param(p.ix());
+        p.loaded();
+        c.st(p.a(), v);
         return;
-    case LDCONST:
-        c.st(p.a(), c.konst(p.ix()));
+    }
+    case LDCONST: {
+        const double v = c.konst(p.ix());
+        p.loaded();
+        c.st(p.a(), v);
         return;
+    }
     case CKST: {   // all loads issued before the first store
         const uint32_t m = p.imm(), f = p.ix(), row = f & kCkRowMask, n1 = f >> kCkRowBits;
         const auto a = p.a();
@@ -382,6 +443,7 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
 #pragma unroll
         for (uint32_t k = 0; k < kMaxCk; ++k)
             if (k < m) v[k] = c.ld(c.adv(a, k < n1 ? k : n1));
+        p.loaded();
 #pragma unroll
         for (uint32_t k = 0; k < kMaxCk; ++k)
             if (k < m) c.ckst(row + (k < n1 ? k : n1), v[k]);
@@ -396,6 +458,7 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
 #pragma unroll
         for (uint32_t k = 0; k < kMaxCk; ++k)
             if (k < m) v[k] = c.ckld(row + (k < n1 ? k : n1));
+        p.loaded();
 #pragma unroll
         for (uint32_t k = 0; k < kMaxCk; ++k)
             if (k < m) c.st(c.adv(a, k < n1 ? k : n1), v[k]);
@@ -406,6 +469,7 @@ NDVM_HD void exec_hot(const C &c, uint32_t form, const W &p) {
         return;
     }
     default:
+        p.loaded();
         return;
     }
 }
