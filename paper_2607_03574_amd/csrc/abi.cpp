@@ -21,7 +21,7 @@
 
 namespace ndvm {
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, int variant, bool skips, bool acc_first, uint32_t slots,
+                         uint32_t r_lds, int variant, bool skips, int order, uint32_t slots,
                          hipStream_t stream);
 bool slots_supported(uint32_t S);
 size_t scratch_bytes();
@@ -338,21 +338,25 @@ uint64_t ws_rows(const DevProg &dp, uint32_t b) {
     return uint64_t(dp.meta.n_ckpt_rows) + slot::kMaxBlock + (dp.meta.n_regs - r_lds);
 }
 
-// Order of the kernel's form tests for a launch whose programs hold these
-// instruction counts: the linear adjoint rule first (then multiply-add and
-// multiply-subtract) when it outnumbers multiply-add and multiply-subtracts
-// are frequent, as in a reverse sweep over ODE steps; multiply-add first
-// otherwise.  The first form tested runs without a taken branch, every
-// further test costs the forms behind it.
-bool acc_first_order(uint64_t n_mac, uint64_t n_acc, uint64_t n_msub, uint64_t n_instr) {
-    return n_acc > n_mac && n_msub * 16 >= n_instr;
+// Order of the kernel's form tests (slot::DispatchOrder) for a launch whose
+// programs hold these instruction counts: the linear adjoint rule first
+// (then multiply-add and multiply-subtract) when it outnumbers multiply-add
+// and multiply-subtracts are frequent, as in a reverse sweep over ODE steps;
+// multiply-add then the block dots when those are a quarter of the
+// instructions (small-matrix programs such as a Kalman filter); multiply-add
+// then the adjoint rule otherwise.  The first form tested runs without a
+// taken branch, every further test costs the forms behind it.
+int dispatch_order(uint64_t n_mac, uint64_t n_acc, uint64_t n_msub, uint64_t n_block, uint64_t n_instr) {
+    if (n_acc > n_mac && n_msub * 16 >= n_instr) return slot::kOrderAccMacMsub;
+    if (n_block * 4 >= n_instr && n_mac >= n_acc) return slot::kOrderMacBlock;
+    return slot::kOrderMacAcc;
 }
-bool acc_first_order(const Schedule &m) { return acc_first_order(m.n_mac, m.n_acc, m.n_msub, m.n_instr); }
+int dispatch_order(const Schedule &m) { return dispatch_order(m.n_mac, m.n_acc, m.n_msub, m.n_block, m.n_instr); }
 
 ndvm_status check_stream_and_launch(const LaunchArgs &A, const ProgStatic *table, const ProgStatic &single,
-                                    uint32_t n_prog, uint32_t r_lds, int variant, bool skips, bool acc_first,
+                                    uint32_t n_prog, uint32_t r_lds, int variant, bool skips, int order,
                                     uint32_t slots, hipStream_t stream) {
-    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, variant, skips, acc_first, slots, stream);
+    hipError_t e = launch_replay(A, table, single, n_prog, r_lds, variant, skips, order, slots, stream);
     if (e != hipSuccess) {
         set_error(std::string("kernel launch failed: ") + hipGetErrorString(e));
         return NDVM_E_DEVICE;
@@ -379,7 +383,7 @@ struct ManyLaunch {
     uint32_t S = 0, r_launch = 0;
     int variant = kLdsOnly;
     bool skips = false;     // some program has skippable branch arms
-    bool acc_first = false; // order of the kernel's form tests (acc_first_order over all programs)
+    int order = 0;          // order of the kernel's form tests (dispatch_order over all programs)
     uint64_t rows = 0;
     void *d_table = nullptr;
     const uint64_t *d_items = nullptr;   // work item per workgroup (xcd_items), or null
@@ -441,7 +445,7 @@ ndvm_status many_launch(const ndvm_tape *const *tapes, int n_prog, int64_t L, bo
     uint32_t r_launch = 0;
     int n_spill = 0;
     std::vector<uint32_t> cost(static_cast<size_t>(n_prog));
-    uint64_t n_mac = 0, n_acc = 0, n_msub = 0, n_instr = 0;
+    uint64_t n_mac = 0, n_acc = 0, n_msub = 0, n_block = 0, n_instr = 0;
     std::map<const ndvm_tape *, Schedule> pre;
     if (build && (st = schedule_many(tapes, n_prog, S, b, &pre)) != NDVM_OK) return st;
     for (int q = 0; q < n_prog; ++q) {
@@ -458,6 +462,7 @@ ndvm_status many_launch(const ndvm_tape *const *tapes, int n_prog, int64_t L, bo
         n_mac += dp->meta.n_mac;
         n_acc += dp->meta.n_acc;
         n_msub += dp->meta.n_msub;
+        n_block += dp->meta.n_block;
         n_instr += dp->meta.n_instr;
         table[q] = ProgStatic{dp->code, dp->consts, row, row + dp->meta.n_ckpt_rows + slot::kMaxBlock,
                               dp->meta.hdr_off, r_lds, spills};
@@ -466,7 +471,7 @@ ndvm_status many_launch(const ndvm_tape *const *tapes, int n_prog, int64_t L, bo
         key.push_back((uint64_t(S) << 32) | b);
     }
     out->S = S;
-    out->acc_first = acc_first_order(n_mac, n_acc, n_msub, n_instr);
+    out->order = dispatch_order(n_mac, n_acc, n_msub, n_block, n_instr);
     out->r_launch = r_launch;
     out->rows = row;
     out->variant = n_spill == 0 ? kLdsOnly : n_spill == n_prog ? kSpill : kPerProgram;
@@ -839,7 +844,7 @@ ndvm_status ndvm_forward(const ndvm_tape *tape, const double *params, int64_t L,
         const bool spills = dp.meta.n_regs > r_lds;
         ProgStatic D{dp.code, dp.consts, 0, uint64_t(dp.meta.n_ckpt_rows) + slot::kMaxBlock, dp.meta.hdr_off, r_lds, spills};
         return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, dp.meta.n_skips > 0,
-                                       acc_first_order(dp.meta), S, static_cast<hipStream_t>(stream));
+                                       dispatch_order(dp.meta), S, static_cast<hipStream_t>(stream));
     });
 }
 
@@ -888,7 +893,7 @@ static ndvm_status grad_impl(const ndvm_tape *tape, const double *params, int64_
     const bool spills = dp->meta.n_regs > r_lds;
     ProgStatic D{dp->code, dp->consts, 0, uint64_t(dp->meta.n_ckpt_rows) + slot::kMaxBlock, dp->meta.hdr_off, r_lds, spills};
     return check_stream_and_launch(A, nullptr, D, 1, r_lds, spills ? kSpill : kLdsOnly, dp->meta.n_skips > 0,
-                                   acc_first_order(dp->meta), S, static_cast<hipStream_t>(stream));
+                                   dispatch_order(dp->meta), S, static_cast<hipStream_t>(stream));
 }
 
 ndvm_status ndvm_grad(const ndvm_tape *tape, const double *params, int64_t L, int64_t ld_p, const double *obs,
@@ -977,7 +982,7 @@ ndvm_status ndvm_grad_points(const ndvm_tape *tape, const double *params, int64_
         DeviceProps pr;
         if ((st = device_props(&pr)) != NDVM_OK) return st;
         st = check_stream_and_launch(A, nullptr, D_, 1, r_lds, spills ? kSpill : kLdsOnly, dp->meta.n_skips > 0,
-                                     acc_first_order(dp->meta), choose_slots(pr, F, 1), s);
+                                     dispatch_order(dp->meta), choose_slots(pr, F, 1), s);
         if (st != NDVM_OK) return st;
         const hipError_t e = launch_fold_points(term, tgrad, L, n_points, P, scale, loss, grad, ld_g, s);
         if (e != hipSuccess) {
@@ -1035,7 +1040,7 @@ ndvm_status ndvm_grad_many(const ndvm_tape *const *tapes, int n_prog, const doub
                 A.n_wg = ml.n_wg;
             }
             st = check_stream_and_launch(A, static_cast<const ProgStatic *>(d_table) + q0, none, uint32_t(nq),
-                                         r_launch, variant, ml.skips, ml.acc_first, S, s);
+                                         r_launch, variant, ml.skips, ml.order, S, s);
             if (st != NDVM_OK) return st;
         }
         return NDVM_OK;

@@ -173,7 +173,7 @@ __device__ __attribute__((noinline)) void cold_call(const C &c, uint32_t form, P
 // instruction); `next` decodes the following instruction.  END and the
 // padding after it do nothing: the loop below runs the chunks up to the one
 // holding END and stops.
-template <int P, bool kSkip, bool kAccFirst, class C, class N>
+template <int P, bool kSkip, int kOrder, class C, class N>
 __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint32_t hb, const Fields &f, N &next) {
     if (kSkip && c.skip) {   // inside a skipped arm (never holds END)
         --c.skip;
@@ -184,14 +184,12 @@ __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint3
     const uint32_t form = hdr & slot::kFormMask;
     const ChunkPayload<P, N> p{f.a, f.x, f.y, f.z, ch, hdr, c.slot_, &next};
     // the most frequent forms are tested one by one, each by its own header
-    // bit, ahead of the dispatch tree, in the launch's order: multiply-add
-    // then the linear adjoint rule, or the adjoint rule, multiply-add and
-    // multiply-subtract (programs whose reverse sweep dominates); the first
-    // runs straight into the next instruction.  The empty asm hides that the
-    // tree's tests are on the same value as the form, so the compiler cannot
-    // fold the tests into one balanced tree (which would put every form
-    // several compares deep).
-    if constexpr (kAccFirst) {
+    // bit, ahead of the dispatch tree, in the launch's order (DispatchOrder);
+    // the first runs straight into the next instruction.  The empty asm
+    // hides that the tree's tests are on the same value as the form, so the
+    // compiler cannot fold the tests into one balanced tree (which would put
+    // every form several compares deep).
+    if constexpr (kOrder == slot::kOrderAccMacMsub) {
         if (__builtin_expect((hdr & slot::kAccBit) != 0, 1)) {
             slotx::exec_acc(c, p);
             return;
@@ -202,6 +200,18 @@ __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint3
         }
         if (__builtin_expect((hdr & slot::kMsubBit) != 0, 1)) {
             slotx::exec_msub(c, p);
+            return;
+        }
+    } else if constexpr (kOrder == slot::kOrderMacBlock) {
+        if (__builtin_expect((hdr & slot::kMacBit) != 0, 1)) {
+            slotx::exec_mac(c, p);
+            return;
+        }
+        if (__builtin_expect((hdr & slot::kBlockBit) != 0, 1)) {
+            if (form == slot::DOTB)
+                slotx::dot_block<false>(c, p);
+            else
+                slotx::dot_block<true>(c, p);
             return;
         }
     } else {
@@ -233,7 +243,7 @@ __device__ __forceinline__ void step(const C &c, uint32_t ch, uint32_t hv, uint3
 // read-aheads: the chunk holding END is followed by kFetchAhead chunks,
 // which is how the chunk count is known, and instructions after END are END
 // too).
-template <bool kSkip, bool kAccFirst, int S, bool kSpill>
+template <bool kSkip, int kOrder, int S, bool kSpill>
 __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *prog, uint32_t hdr_off) {
     static_assert(slot::kChunk == 4 && slot::kFetchAhead == 2 && slot::kHeaderGroup == 256,
                   "the fetch below reads four-instruction chunks two ahead and the headers of 64 chunks a group");
@@ -255,10 +265,10 @@ __device__ __forceinline__ void run(const DevCtx<S, kSpill> &c, const uint32_t *
         auto d2 = [&] { decode<2, false>(cur, la, f2); };
         auto d3 = [&] { decode<3, false>(cur, la, f3); };
         auto d0 = [&] { decode<0, true>(n1, la, f0); };   // instruction 0 of the next chunk
-        step<0, kSkip, kAccFirst>(c, cur, hv.x, hb, f0, d1);
-        step<1, kSkip, kAccFirst>(c, cur, hv.y, hb, f1, d2);
-        step<2, kSkip, kAccFirst>(c, cur, hv.z, hb, f2, d3);
-        step<3, kSkip, kAccFirst>(c, cur, hv.w, hb, f3, d0);
+        step<0, kSkip, kOrder>(c, cur, hv.x, hb, f0, d1);
+        step<1, kSkip, kOrder>(c, cur, hv.y, hb, f1, d2);
+        step<2, kSkip, kOrder>(c, cur, hv.z, hb, f2, d3);
+        step<3, kSkip, kOrder>(c, cur, hv.w, hb, f3, d0);
         cur = n1;
         n1 = n2;
         if (hb == 63u) {
@@ -285,7 +295,7 @@ __device__ __forceinline__ bool work_item(const LaunchArgs &A, uint32_t &q, uint
     return it != ~uint64_t(0);
 }
 
-template <int S, bool kSpill, bool kSkip, bool kAccFirst>
+template <int S, bool kSpill, bool kSkip, int kOrder>
 __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStatic *__restrict__ table,
                                             const ProgStatic &single, uint32_t q, uint32_t bx) {
     extern __shared__ double lds_regs[];
@@ -314,18 +324,18 @@ __device__ __forceinline__ void replay_body(const LaunchArgs &A, const ProgStati
     c.ld_p = A.ld_p;
     c.ld_g = A.ld_g;
     c.r_lds = D.r_lds;
-    run<kSkip, kAccFirst>(c, D.prog, D.hdr_off);
+    run<kSkip, kOrder>(c, D.prog, D.hdr_off);
 }
 
 // All lane registers in LDS (the usual case: the scheduler fits the register
 // file to the launch's LDS budget).  kSkip: the program has skippable branch
-// arms (every instruction then tests the skip counter first).  kAccFirst:
-// the order of the form tests (see step).
-template <int S, bool kSkip, bool kAccFirst>
+// arms (every instruction then tests the skip counter first).  kOrder: the
+// order of the form tests (DispatchOrder).
+template <int S, bool kSkip, int kOrder>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4)))
 ndvm_replay(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
     uint32_t q, bx;
-    if (work_item(A, q, bx)) replay_body<S, false, kSkip, kAccFirst>(A, table, single, q, bx);
+    if (work_item(A, q, bx)) replay_body<S, false, kSkip, kOrder>(A, table, single, q, bx);
 }
 
 // Registers beyond r_lds spill to lane-contiguous workspace rows.
@@ -333,7 +343,7 @@ template <int S>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4)))
 ndvm_replay_spill(LaunchArgs A, const ProgStatic *__restrict__ table, ProgStatic single) {
     uint32_t q, bx;
-    if (work_item(A, q, bx)) replay_body<S, true, true, false>(A, table, single, q, bx);
+    if (work_item(A, q, bx)) replay_body<S, true, true, slot::kOrderMacAcc>(A, table, single, q, bx);
 }
 
 // Many programs in one launch, only some of which spill: each workgroup takes
@@ -345,26 +355,42 @@ ndvm_replay_per_program(LaunchArgs A, const ProgStatic *__restrict__ table, Prog
     uint32_t q, bx;
     if (!work_item(A, q, bx)) return;
     if (table[q].spills)
-        replay_body<S, true, true, false>(A, table, single, q, bx);
+        replay_body<S, true, true, slot::kOrderMacAcc>(A, table, single, q, bx);
     else
-        replay_body<S, false, kSkip, false>(A, table, single, q, bx);
+        replay_body<S, false, kSkip, slot::kOrderMacAcc>(A, table, single, q, bx);
 }
 
 namespace {
 
+template <int S, bool kSkip>
+void launch_ordered(dim3 grid, dim3 block, size_t smem, hipStream_t stream, const LaunchArgs &A,
+                    const ProgStatic *d_table, const ProgStatic &single, int order) {
+    if (order == slot::kOrderAccMacMsub)
+        hipLaunchKernelGGL((ndvm_replay<S, kSkip, slot::kOrderAccMacMsub>), grid, block, smem, stream, A, d_table,
+                           single);
+    else if (order == slot::kOrderMacBlock)
+        hipLaunchKernelGGL((ndvm_replay<S, kSkip, slot::kOrderMacBlock>), grid, block, smem, stream, A, d_table,
+                           single);
+    else
+        hipLaunchKernelGGL((ndvm_replay<S, kSkip, slot::kOrderMacAcc>), grid, block, smem, stream, A, d_table,
+                           single);
+}
+
 template <int S>
 hipError_t launch_s(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                    uint32_t r_lds, int variant, bool skips, bool acc_first, hipStream_t stream) {
+                    uint32_t r_lds, int variant, bool skips, int order, hipStream_t stream) {
     static std::once_flag once[64];
     int dev = 0;
     (void)hipGetDevice(&dev);
     std::call_once(once[dev & 63], [dev]() {
         int max_smem = 0;
         (void)hipDeviceGetAttribute(&max_smem, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-        for (const void *f : {reinterpret_cast<const void *>(&ndvm_replay<S, false, false>),
-                              reinterpret_cast<const void *>(&ndvm_replay<S, true, false>),
-                              reinterpret_cast<const void *>(&ndvm_replay<S, false, true>),
-                              reinterpret_cast<const void *>(&ndvm_replay<S, true, true>),
+        for (const void *f : {reinterpret_cast<const void *>(&ndvm_replay<S, false, slot::kOrderMacAcc>),
+                              reinterpret_cast<const void *>(&ndvm_replay<S, true, slot::kOrderMacAcc>),
+                              reinterpret_cast<const void *>(&ndvm_replay<S, false, slot::kOrderAccMacMsub>),
+                              reinterpret_cast<const void *>(&ndvm_replay<S, true, slot::kOrderAccMacMsub>),
+                              reinterpret_cast<const void *>(&ndvm_replay<S, false, slot::kOrderMacBlock>),
+                              reinterpret_cast<const void *>(&ndvm_replay<S, true, slot::kOrderMacBlock>),
                               reinterpret_cast<const void *>(&ndvm_replay_spill<S>),
                               reinterpret_cast<const void *>(&ndvm_replay_per_program<S, false>),
                               reinterpret_cast<const void *>(&ndvm_replay_per_program<S, true>)})
@@ -381,14 +407,9 @@ hipError_t launch_s(const LaunchArgs &A, const ProgStatic *d_table, const ProgSt
     } else if (variant == kSpill || variant == kPerProgram) {
         hipLaunchKernelGGL(ndvm_replay_spill<S>, grid, block, smem, stream, A, d_table, single);
     } else if (skips) {
-        if (acc_first)
-            hipLaunchKernelGGL((ndvm_replay<S, true, true>), grid, block, smem, stream, A, d_table, single);
-        else
-            hipLaunchKernelGGL((ndvm_replay<S, true, false>), grid, block, smem, stream, A, d_table, single);
-    } else if (acc_first) {
-        hipLaunchKernelGGL((ndvm_replay<S, false, true>), grid, block, smem, stream, A, d_table, single);
+        launch_ordered<S, true>(grid, block, smem, stream, A, d_table, single, order);
     } else {
-        hipLaunchKernelGGL((ndvm_replay<S, false, false>), grid, block, smem, stream, A, d_table, single);
+        launch_ordered<S, false>(grid, block, smem, stream, A, d_table, single, order);
     }
     return hipGetLastError();
 }
@@ -464,10 +485,10 @@ hipError_t scratch_address(void **out) {
 }
 
 hipError_t launch_replay(const LaunchArgs &A, const ProgStatic *d_table, const ProgStatic &single, uint32_t n_prog,
-                         uint32_t r_lds, int variant, bool skips, bool acc_first, uint32_t slots,
+                         uint32_t r_lds, int variant, bool skips, int order, uint32_t slots,
                          hipStream_t stream) {
     switch (slots) {
-    case 4: return launch_s<4>(A, d_table, single, n_prog, r_lds, variant, skips, acc_first, stream);
+    case 4: return launch_s<4>(A, d_table, single, n_prog, r_lds, variant, skips, order, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -2095,6 +2095,7 @@ Schedule build(const Info &I, Builder &B, bool with_grad, uint32_t S, uint32_t r
         Sch.n_mac += f == MAC;
         Sch.n_acc += f == ACC;
         Sch.n_msub += f == MSUB;
+        Sch.n_block += f == DOTB || f == DOTBACC;
     }
     Sch.n_chunks = n_chunks;
     return Sch;

@@ -22,7 +22,7 @@ struct Schedule {
     uint64_t n_fwd_ops = 0, n_recompute_ops = 0, n_rev_ops = 0;
     uint64_t ckpt_elems_stored = 0, ckpt_elems_loaded = 0;
     uint32_t n_skips = 0;         // skippable branch arms (SKIP instructions)
-    uint64_t n_mac = 0, n_acc = 0, n_msub = 0;   // instructions of the three most frequent forms
+    uint64_t n_mac = 0, n_acc = 0, n_msub = 0, n_block = 0;   // instructions of the most frequent forms
 };
 
 // Smallest branch arm (in value elements) laid out behind a skip test: a

@@ -17,8 +17,9 @@
 // Per instruction: a header word, the same for every slot:
 //   bits 0-5 form, bits 6-9 kFirst of slots 0-3 (first contribution to the
 //   target: store, do not add), bit 10 set when the form is MAC, bit 11 when
-//   it is ACC, bit 12 when it is MSUB (the most frequent forms, each told
-//   apart by one bit test), bit 13 zero, bits 14-31 the form's immediate;
+//   it is ACC, bit 12 when it is MSUB, bit 13 when it is DOTB or DOTBACC (the
+//   most frequent forms, each told apart by one bit test), bits 14-31 the
+//   form's immediate;
 // and per slot four words a, x, y, z: a register named in a field is held as
 // its byte offset in a lane's register file (register * 8 * 64/S), an index
 // (observation, parameter, constant, checkpoint row) as itself.
@@ -90,10 +91,17 @@ enum Unary : uint32_t { U_SIN = 0, U_COS };
 constexpr uint32_t kFormMask = 63u;
 constexpr uint32_t kSkipSideShift = 17, kSkipCountMask = (1u << kSkipSideShift) - 1;
 constexpr uint32_t kFirstShift = 6, kImmShift = 14;
-constexpr uint32_t kMacBit = 1u << 10, kAccBit = 1u << 11, kMsubBit = 1u << 12;
+constexpr uint32_t kMacBit = 1u << 10, kAccBit = 1u << 11, kMsubBit = 1u << 12, kBlockBit = 1u << 13;
+// Order of the replay's bit tests ahead of its dispatch tree (chosen per
+// launch from the programs' instruction counts; the first form tested runs
+// without a taken branch): multiply-add then the linear adjoint rule; the
+// adjoint rule, multiply-add and multiply-subtract; multiply-add then the
+// block dots.
+enum DispatchOrder : int { kOrderMacAcc = 0, kOrderAccMacMsub = 1, kOrderMacBlock = 2 };
 // the form's own bits of a header (form number and its one-hot flag)
 inline uint32_t form_bits(uint32_t form) {
-    return form | (form == MAC ? kMacBit : 0u) | (form == ACC ? kAccBit : 0u) | (form == MSUB ? kMsubBit : 0u);
+    return form | (form == MAC ? kMacBit : 0u) | (form == ACC ? kAccBit : 0u) | (form == MSUB ? kMsubBit : 0u) |
+           (form == DOTB || form == DOTBACC ? kBlockBit : 0u);
 }
 constexpr uint32_t kMaxImm = (1u << 18) - 1;
 constexpr uint32_t kMaxBlock = 4;            // outputs of a block form (sink and trash rows reserved)
