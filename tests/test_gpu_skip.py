@@ -185,3 +185,45 @@ def test_skipping_under_the_adjoint_first_dispatch(nd, oracle_mod):
     np.testing.assert_array_equal(out["sorted"][1][inv], out["mixed"][1])
     r = judge(oracle_mod, bc, params, obs, out["mixed"][0], out["mixed"][1])
     record("skip_adjoint_first", **r)
+
+
+def test_skipping_under_the_block_dispatch(nd, oracle_mod):
+    """The Kalman filter with a branch on dt after its loop: a program whose
+    instructions are a quarter block dots runs the replay variant that tests
+    multiply-add and the block dots first and skips arms; lanes sorted by dt
+    (waves skip an arm) and interleaved give the same results bit for bit as
+    the upload without skipping, and pass the oracle's parity rules (the mix
+    holds at budgets 160 to 640 registers; 16,384 lanes give 320 on a 256-CU
+    GPU)."""
+    import emu
+    T, L = 40, 16384
+    bc = configs.kalman_program(T, branch_tail=True)
+    tape = nd.tape_build(bc)
+    for budget in (160, 320, 640):
+        headers, _ = emu.program(tape, True, budget, arms="option")
+        forms = headers & 63
+        n = int(np.argmax(forms == 63)) + 1
+        n_mac, n_acc = int(np.sum(forms[:n] == 1)), int(np.sum(forms[:n] == 2))
+        n_block = int(np.sum((forms[:n] == 18) | (forms[:n] == 19)))
+        assert 4 * n_block >= n and n_mac >= n_acc, (budget, n, n_mac, n_acc, n_block)
+        assert np.sum(forms[:n] == 32) > 0
+    w = configs.kalman(L=L, T=T)
+    params, obs = w.params, w.obs
+    order = np.argsort(params[:, 0], kind="stable")
+    o = torch.tensor(obs, device="cuda")
+    out = {}
+    for name, p_host, policy in (("sorted", params[order], nd.POLICY_RECOMPUTE | nd.BRANCH_SKIP),
+                                 ("sorted_plain", params[order], nd.POLICY_RECOMPUTE),
+                                 ("mixed", params, nd.POLICY_RECOMPUTE | nd.BRANCH_SKIP)):
+        t = nd.tape_upload(tape, policy)
+        loss, g = nd.grad(t, torch.tensor(np.ascontiguousarray(p_host), device="cuda"), o)
+        torch.cuda.synchronize()
+        out[name] = (loss.cpu().numpy(), g.cpu().numpy())
+    np.testing.assert_array_equal(out["sorted"][0], out["sorted_plain"][0])
+    np.testing.assert_array_equal(out["sorted"][1], out["sorted_plain"][1])
+    inv = np.empty_like(order)
+    inv[order] = np.arange(L)
+    np.testing.assert_array_equal(out["sorted"][0][inv], out["mixed"][0])
+    np.testing.assert_array_equal(out["sorted"][1][inv], out["mixed"][1])
+    r = judge(oracle_mod, bc, params, obs, out["mixed"][0], out["mixed"][1])
+    record("skip_block_dispatch", **r)

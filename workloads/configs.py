@@ -218,10 +218,12 @@ def lotka_volterra(L: int = 65536, T: int = 1000, seed: int = 3003):
 # --------------------------------------------------------------------------
 # config 4: 4-state constant-velocity Kalman filter, NLL
 # --------------------------------------------------------------------------
-def kalman_program(T: int) -> bytes:
+def kalman_program(T: int, branch_tail: bool = False) -> bytes:
     """params (dt, q1..q4, r1, r2, x0_1..x0_4, s); obs interleaved 2-D
     measurements.  Filter: predict, innovation, update in the standard
-    P+ = (I - K H) P- form."""
+    P+ = (I - K H) P- form.  branch_tail: the NLL is then reshaped by a
+    numeric branch on dt (one of two chains of six multiply-adds; a test
+    program with skippable arms)."""
     A = Asm(12, 2 * T)
     F, Ft, Q, H, Ht, R, X, P, I4, NLL = range(10)
     XM, PM, V, S, SI, KG = 10, 11, 12, 13, 14, 15
@@ -272,6 +274,14 @@ def kalman_program(T: int) -> bytes:
     A.add().push(2.0 * LN_2PI).add().push(0.5).mul()
     A.add().storel(NLL)
     A.endloop()
+    if branch_tail:
+        A.param(0).push(0.1).iflt()
+        for _ in range(6):
+            A.loadl(NLL).loadl(NLL).param(1).mul().push(1e-3).mul().add().storel(NLL)
+        A.else_()
+        for _ in range(6):
+            A.loadl(NLL).loadl(NLL).param(5).mul().push(2e-3).mul().add().storel(NLL)
+        A.endif()
     A.loadl(NLL).halt()
     return A.bytes()
 
