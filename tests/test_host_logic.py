@@ -327,7 +327,9 @@ NO_A = {28, 42, 43}                     # CKST STLOSS STGRAD (register a is read
 def test_device_program_encoding(name, kw):
     """The encoded program: known forms only, END once followed by END padding,
     register fields as byte offsets of whole 16-lane registers inside the
-    register file, slot flags only where a slot exists."""
+    register file, slot flags only where a slot exists, and the one-hot
+    dispatch bits (10: MAC, 11: ACC, 12: MSUB, 13: DOTB or DOTBACC) set
+    exactly on their forms (the kernel dispatches on these bits alone)."""
     w = configs.build(name, **kw)
     tape = nd.tape_build(w.bytecode)
     budget = 48
@@ -338,6 +340,11 @@ def test_device_program_encoding(name, kw):
     assert n == st["n_instr"]
     assert set(forms[n:len(words)].tolist()) <= {END}
     assert set(forms[:n].tolist()) <= HOT_FORMS | COLD_FORMS | {END}
+    bit = lambda b: ((headers[:n] >> b) & 1).astype(bool)
+    np.testing.assert_array_equal(bit(10), forms[:n] == 1)
+    np.testing.assert_array_equal(bit(11), forms[:n] == 2)
+    np.testing.assert_array_equal(bit(12), forms[:n] == 30)
+    np.testing.assert_array_equal(bit(13), (forms[:n] == 18) | (forms[:n] == 19))
     stride = 16 * 8
     for k in range(n - 1):
         f = int(forms[k])
